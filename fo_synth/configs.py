@@ -1,0 +1,139 @@
+"""Workload descriptions for the five server-side configurations.
+
+Each configuration is a split of a network between devices and the server:
+the devices send the activations of their last layer, and the server trains
+the remaining layers (the server-side network M_s of Sec. 3.1, trained in the
+activation branch of Algorithm 4).  The shapes below stand in for the paper's
+workloads (image classification on CIFAR-10 / Tiny ImageNet, sentiment
+analysis on SST-2 / IMDB, Sec. 5.1); no dataset is read.
+
+``param_layout`` fixes the order and shape of every server parameter inside
+the flat fp32 vector exchanged with the library (the "library layout").
+Convolution weights are stored as [Cout][kh][kw][Cin]; linear weights as
+[out][in]; the fused attention input projection as [3*d][d] with the query,
+key and value rows in that order.  Both the oracle and the HIP library derive
+this order independently from the architecture; tests compare the three.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Tuple
+
+
+@dataclass(frozen=True)
+class ConfigSpec:
+    cid: int
+    name: str
+    family: str              # "cnn" (C1), "vgg" (C2, C5), "resnet" (C3), "bert" (C4)
+    batch: int
+    in_shape: Tuple[int, ...]  # per-sample activation shape at the boundary (NCHW or [L, d])
+    n_classes: int
+    n_devices: int
+    dtype: str               # "f32" or "bf16" (activations and GEMM operands)
+    lr: float
+    momentum: float          # 0.0 = plain SGD
+    agg_n: int               # length of the flat device-side vector aggregated (0 = none)
+    agg_alpha: float
+    steps: int
+    extra: dict = field(default_factory=dict)
+
+
+CONFIGS = {
+    1: ConfigSpec(1, "tiny-cnn-fp32", "cnn", 16, (32, 16, 16), 10, 4, "f32",
+                  0.01, 0.0, 10_000, 0.5, 4),
+    2: ConfigSpec(2, "vgg16-split-bf16", "vgg", 64, (64, 16, 16), 10, 16, "bf16",
+                  0.01, 0.0, 0, 1.0, 100),
+    3: ConfigSpec(3, "resnet18-split-bf16", "resnet", 32, (64, 16, 16), 100, 32, "bf16",
+                  0.01, 0.9, 157_504, 1.0, 100, {"max_staleness": 8}),
+    4: ConfigSpec(4, "bert-base-split-bf16", "bert", 32, (128, 768), 2, 16, "bf16",
+                  0.01, 0.0, 0, 1.0, 100,
+                  {"layers": 10, "heads": 12, "ffn": 3072, "min_len": 32}),
+    5: ConfigSpec(5, "vgg16-split-128dev-bf16", "vgg", 64, (64, 16, 16), 10, 128, "bf16",
+                  0.01, 0.0, 38_720, 1.0, 1000,
+                  {"pool_bytes": 64 << 30, "bank": 256}),
+}
+
+
+def get_config(cid: int) -> ConfigSpec:
+    if cid not in CONFIGS:
+        raise ValueError(f"unknown config {cid}")
+    return CONFIGS[cid]
+
+
+# (name, shape, init kind, fan_in). kinds: "kaiming" = U(+-sqrt(6/fan_in)), "zeros", "ones"
+Entry = Tuple[str, Tuple[int, ...], str, int]
+
+VGG_SERVER_CONVS = [128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M", 512, 512, 512, "M"]
+
+
+def _conv(name: str, cout: int, cin: int, k: int, bias: bool) -> List[Entry]:
+    out = [(name + ".w", (cout, k, k, cin), "kaiming", cin * k * k)]
+    if bias:
+        out.append((name + ".b", (cout,), "zeros", 0))
+    return out
+
+
+def _linear(name: str, nout: int, nin: int) -> List[Entry]:
+    return [(name + ".w", (nout, nin), "kaiming", nin), (name + ".b", (nout,), "zeros", 0)]
+
+
+def _norm(name: str, c: int) -> List[Entry]:
+    return [(name + ".g", (c,), "ones", 0), (name + ".b", (c,), "zeros", 0)]
+
+
+def param_layout(cid: int) -> List[Entry]:
+    cfg = get_config(cid)
+    lay: List[Entry] = []
+    if cfg.family == "cnn":
+        lay += _conv("conv1", 64, 32, 3, True)
+        lay += _conv("conv2", 64, 64, 3, True)
+        lay += _linear("fc", 10, 64)
+    elif cfg.family == "vgg":
+        cin, i = cfg.in_shape[0], 0
+        for v in VGG_SERVER_CONVS:
+            if v == "M":
+                continue
+            lay += _conv(f"conv{i}", v, cin, 3, True)
+            cin, i = v, i + 1
+        lay += _linear("fc0", 512, 512)
+        lay += _linear("fc1", 512, 512)
+        lay += _linear("fc2", cfg.n_classes, 512)
+    elif cfg.family == "resnet":
+        cin = cfg.in_shape[0]
+        for li, c in ((2, 128), (3, 256), (4, 512)):
+            for bi in range(2):
+                p = f"layer{li}.{bi}"
+                lay += _conv(p + ".conv1", c, cin if bi == 0 else c, 3, False)
+                lay += _norm(p + ".bn1", c)
+                lay += _conv(p + ".conv2", c, c, 3, False)
+                lay += _norm(p + ".bn2", c)
+                if bi == 0:
+                    lay += _conv(p + ".ds", c, cin, 1, False)
+                    lay += _norm(p + ".dsbn", c)
+            cin = c
+        lay += _linear("fc", cfg.n_classes, 512)
+    elif cfg.family == "bert":
+        d, f = cfg.in_shape[1], cfg.extra["ffn"]
+        for li in range(cfg.extra["layers"]):
+            p = f"enc{li}"
+            lay += _linear(p + ".qkv", 3 * d, d)
+            lay += _linear(p + ".o", d, d)
+            lay += _norm(p + ".ln1", d)
+            lay += _linear(p + ".ffn1", f, d)
+            lay += _linear(p + ".ffn2", d, f)
+            lay += _norm(p + ".ln2", d)
+        lay += _linear("pool", d, d)
+        lay += _linear("cls", cfg.n_classes, d)
+    else:  # pragma: no cover
+        raise ValueError(cfg.family)
+    return lay
+
+
+def param_count(cid: int) -> int:
+    n = 0
+    for _, shape, _, _ in param_layout(cid):
+        k = 1
+        for s in shape:
+            k *= s
+        n += k
+    return n

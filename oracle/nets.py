@@ -1,0 +1,367 @@
+"""Server-side networks M_s of the five configurations and one training
+iteration of the activation branch of Algorithm 4 (forward of M_s, the loss
+f_s, the backward pass, then theta_s <- theta_s - gamma_s * grad).
+
+Test infrastructure (see package docstring).  The flat parameter order (the
+"library layout") is derived here from the architecture on its own; a test
+compares it with the workload description and with the library.  Convolution
+weights sit in the flat vector as [Cout][kh][kw][Cin] and are turned into the
+[Cout][Cin][kh][kw] form that ``layers.Conv2d`` expects when unpacked.
+
+The server never returns an activation gradient to the devices (the devices
+train on their local auxiliary loss instead, Sec. 3.1 and Alg. 1), so the
+first server layer's input gradient is not computed.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import layers as Lyr
+
+# architecture constants per configuration id (from the workload descriptions)
+VGG_PLAN = [128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M", 512, 512, 512, "M"]
+RESNET_STAGES = [(2, 128, 2), (3, 256, 2), (4, 512, 2)]  # (stage, channels, blocks)
+BERT = dict(d=768, heads=12, ffn=3072, layers=10, classes=2)
+FAMILY = {1: "cnn", 2: "vgg", 3: "resnet", 4: "bert", 5: "vgg"}
+IN_CH = {1: 32, 2: 64, 3: 64, 5: 64}
+CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10}
+
+
+def param_layout(cid: int):
+    """[(name, shape in the flat vector)] in flat order."""
+    fam = FAMILY[cid]
+    out = []
+
+    def conv(n, co, ci, k, bias=True):
+        out.append((n + ".w", (co, k, k, ci)))
+        if bias:
+            out.append((n + ".b", (co,)))
+
+    def lin(n, o, i):
+        out.append((n + ".w", (o, i)))
+        out.append((n + ".b", (o,)))
+
+    def norm(n, c):
+        out.append((n + ".g", (c,)))
+        out.append((n + ".b", (c,)))
+
+    if fam == "cnn":
+        conv("conv1", 64, 32, 3)
+        conv("conv2", 64, 64, 3)
+        lin("fc", 10, 64)
+    elif fam == "vgg":
+        ci, n = IN_CH[cid], 0
+        for v in VGG_PLAN:
+            if v != "M":
+                conv(f"conv{n}", v, ci, 3)
+                ci, n = v, n + 1
+        lin("fc0", 512, 512)
+        lin("fc1", 512, 512)
+        lin("fc2", CLASSES[cid], 512)
+    elif fam == "resnet":
+        ci = IN_CH[cid]
+        for st, c, nb in RESNET_STAGES:
+            for bi in range(nb):
+                p = f"layer{st}.{bi}"
+                conv(p + ".conv1", c, ci if bi == 0 else c, 3, bias=False)
+                norm(p + ".bn1", c)
+                conv(p + ".conv2", c, c, 3, bias=False)
+                norm(p + ".bn2", c)
+                if bi == 0:
+                    conv(p + ".ds", c, ci, 1, bias=False)
+                    norm(p + ".dsbn", c)
+            ci = c
+        lin("fc", CLASSES[cid], 512)
+    else:
+        d, f = BERT["d"], BERT["ffn"]
+        for li in range(BERT["layers"]):
+            p = f"enc{li}"
+            lin(p + ".qkv", 3 * d, d)
+            lin(p + ".o", d, d)
+            norm(p + ".ln1", d)
+            lin(p + ".ffn1", f, d)
+            lin(p + ".ffn2", d, f)
+            norm(p + ".ln2", d)
+        lin("pool", d, d)
+        lin("cls", BERT["classes"], d)
+    return out
+
+
+def unpack(cid, flat, dt):
+    P, off = {}, 0
+    for name, shape in param_layout(cid):
+        n = int(np.prod(shape))
+        a = np.asarray(flat[off:off + n], dtype=dt).reshape(shape)
+        if len(shape) == 4:  # [Co, kh, kw, Ci] -> [Co, Ci, kh, kw]
+            a = a.transpose(0, 3, 1, 2).copy()
+        P[name] = a
+        off += n
+    assert off == len(flat), (off, len(flat))
+    return P
+
+
+def pack(cid, G):
+    parts = []
+    for name, shape in param_layout(cid):
+        g = G[name]
+        if len(shape) == 4:
+            g = g.transpose(0, 2, 3, 1)
+        parts.append(np.asarray(g).reshape(-1))
+    return np.concatenate(parts)
+
+
+# ----------------------------------------------------------------------------- networks
+class _Net:
+    def grads(self):
+        return self.G
+
+
+class CNN(_Net):
+    """conv3x3 32->64 + ReLU, maxpool2, conv3x3 64->64 + ReLU, global average
+    pool, linear 64->10."""
+
+    def __init__(self, P):
+        self.c1 = Lyr.Conv2d(P["conv1.w"], P["conv1.b"])
+        self.r1, self.mp = Lyr.ReLU(), Lyr.MaxPool2()
+        self.c2 = Lyr.Conv2d(P["conv2.w"], P["conv2.b"])
+        self.r2, self.gap = Lyr.ReLU(), Lyr.GlobalAvgPool()
+        self.fc = Lyr.Linear(P["fc.w"], P["fc.b"])
+
+    def fwd(self, x, lengths=None):
+        h = self.mp.fwd(self.r1.fwd(self.c1.fwd(x)))
+        h = self.gap.fwd(self.r2.fwd(self.c2.fwd(h)))
+        return self.fc.fwd(h)
+
+    def bwd(self, dz):
+        dh = self.gap.bwd(self.fc.bwd(dz))
+        dh = self.mp.bwd(self.c2.bwd(self.r2.bwd(dh)))
+        self.c1.bwd(self.r1.bwd(dh), need_dx=False)
+        self.G = {"conv1.w": self.c1.dw, "conv1.b": self.c1.db, "conv2.w": self.c2.dw,
+                  "conv2.b": self.c2.db, "fc.w": self.fc.dw, "fc.b": self.fc.db}
+
+
+class VGG(_Net):
+    """VGG-16 after its second convolution and first pool: ten 3x3 convs
+    with ReLU and four 2x2 max pools, then 512-512-classes linear layers with
+    ReLU between them."""
+
+    def __init__(self, P, cid):
+        self.seq, n = [], 0
+        for v in VGG_PLAN:
+            if v == "M":
+                self.seq.append(("pool", Lyr.MaxPool2()))
+            else:
+                self.seq.append((f"conv{n}", Lyr.Conv2d(P[f"conv{n}.w"], P[f"conv{n}.b"])))
+                self.seq.append(("relu", Lyr.ReLU()))
+                n += 1
+        self.fcs = [Lyr.Linear(P[f"fc{i}.w"], P[f"fc{i}.b"]) for i in range(3)]
+        self.frelu = [Lyr.ReLU(), Lyr.ReLU()]
+
+    def fwd(self, x, lengths=None):
+        h = x
+        for _, l in self.seq:
+            h = l.fwd(h)
+        h = h.reshape(h.shape[0], -1)
+        for i in range(2):
+            h = self.frelu[i].fwd(self.fcs[i].fwd(h))
+        return self.fcs[2].fwd(h)
+
+    def bwd(self, dz):
+        G = {}
+        dh = self.fcs[2].bwd(dz)
+        for i in (1, 0):
+            dh = self.fcs[i].bwd(self.frelu[i].bwd(dh))
+        for i in range(3):
+            G[f"fc{i}.w"], G[f"fc{i}.b"] = self.fcs[i].dw, self.fcs[i].db
+        dh = dh.reshape(dh.shape[0], -1, 1, 1)  # the last pool leaves 1x1 maps
+        for idx in range(len(self.seq) - 1, -1, -1):
+            name, l = self.seq[idx]
+            if name.startswith("conv"):
+                dh = l.bwd(dh, need_dx=idx > 0)
+                G[name + ".w"], G[name + ".b"] = l.dw, l.db
+            else:
+                dh = l.bwd(dh)
+        self.G = G
+
+
+class BasicBlock:
+    """ReLU(BN(conv3x3(ReLU(BN(conv3x3_s(x))))) + shortcut(x)); shortcut is
+    BN(conv1x1_s(x)) when the shape changes, else x.  Convs carry no bias."""
+
+    def __init__(self, P, p, stride, down):
+        self.c1 = Lyr.Conv2d(P[p + ".conv1.w"], None, stride=stride, pad=1)
+        self.b1 = Lyr.BatchNorm2d(P[p + ".bn1.g"], P[p + ".bn1.b"])
+        self.r1 = Lyr.ReLU()
+        self.c2 = Lyr.Conv2d(P[p + ".conv2.w"], None, stride=1, pad=1)
+        self.b2 = Lyr.BatchNorm2d(P[p + ".bn2.g"], P[p + ".bn2.b"])
+        self.r2 = Lyr.ReLU()
+        self.down = down
+        if down:
+            self.cd = Lyr.Conv2d(P[p + ".ds.w"], None, stride=stride, pad=0)
+            self.bd = Lyr.BatchNorm2d(P[p + ".dsbn.g"], P[p + ".dsbn.b"])
+        self.p = p
+
+    def fwd(self, x):
+        h = self.r1.fwd(self.b1.fwd(self.c1.fwd(x)))
+        h = self.b2.fwd(self.c2.fwd(h))
+        sc = self.bd.fwd(self.cd.fwd(x)) if self.down else x
+        return self.r2.fwd(h + sc)
+
+    def bwd(self, dy, need_dx, G):
+        p = self.p
+        ds = self.r2.bwd(dy)
+        dh = self.b2.bwd(ds)
+        dh = self.c2.bwd(dh)
+        dh = self.b1.bwd(self.r1.bwd(dh))
+        dx = self.c1.bwd(dh, need_dx=need_dx)
+        G[p + ".conv1.w"], G[p + ".bn1.g"], G[p + ".bn1.b"] = self.c1.dw, self.b1.dg, self.b1.db
+        G[p + ".conv2.w"], G[p + ".bn2.g"], G[p + ".bn2.b"] = self.c2.dw, self.b2.dg, self.b2.db
+        if self.down:
+            dsc = self.cd.bwd(self.bd.bwd(ds), need_dx=need_dx)
+            G[p + ".ds.w"], G[p + ".dsbn.g"], G[p + ".dsbn.b"] = self.cd.dw, self.bd.dg, self.bd.db
+        else:
+            dsc = ds
+        return dx + dsc if need_dx else None
+
+
+class ResNet(_Net):
+    """ResNet-18 stages 2-4 (two BasicBlocks each, the first with stride 2
+    and a 1x1 projection shortcut), global average pool, linear 512->classes."""
+
+    def __init__(self, P, cid):
+        self.blocks = []
+        for st, c, nb in RESNET_STAGES:
+            for bi in range(nb):
+                self.blocks.append(BasicBlock(P, f"layer{st}.{bi}", 2 if bi == 0 else 1, bi == 0))
+        self.gap = Lyr.GlobalAvgPool()
+        self.fc = Lyr.Linear(P["fc.w"], P["fc.b"])
+
+    def fwd(self, x, lengths=None):
+        h = x
+        for b in self.blocks:
+            h = b.fwd(h)
+        return self.fc.fwd(self.gap.fwd(h))
+
+    def bwd(self, dz):
+        G = {}
+        dh = self.gap.bwd(self.fc.bwd(dz))
+        G["fc.w"], G["fc.b"] = self.fc.dw, self.fc.db
+        for i in range(len(self.blocks) - 1, -1, -1):
+            dh = self.blocks[i].bwd(dh, i > 0, G)
+        self.G = G
+
+
+class EncoderLayer:
+    """Post-LN transformer encoder layer: h = LN1(x + MHA(x));
+    y = LN2(h + W2 GELU(W1 h + b1) + b2)."""
+
+    def __init__(self, P, p, heads):
+        self.att = Lyr.MultiHeadAttention(P[p + ".qkv.w"], P[p + ".qkv.b"], P[p + ".o.w"], P[p + ".o.b"], heads)
+        self.ln1 = Lyr.LayerNorm(P[p + ".ln1.g"], P[p + ".ln1.b"])
+        self.f1 = Lyr.Linear(P[p + ".ffn1.w"], P[p + ".ffn1.b"])
+        self.act = Lyr.GELU()
+        self.f2 = Lyr.Linear(P[p + ".ffn2.w"], P[p + ".ffn2.b"])
+        self.ln2 = Lyr.LayerNorm(P[p + ".ln2.g"], P[p + ".ln2.b"])
+        self.p = p
+
+    def fwd(self, x, lengths):
+        h = self.ln1.fwd(x + self.att.fwd(x, lengths))
+        return self.ln2.fwd(h + self.f2.fwd(self.act.fwd(self.f1.fwd(h))))
+
+    def bwd(self, dy, need_dx, G):
+        p = self.p
+        du = self.ln2.bwd(dy)
+        dh = du + self.f1.bwd(self.act.bwd(self.f2.bwd(du)))
+        dv = self.ln1.bwd(dh)
+        dx = self.att.bwd(dv, need_dx)
+        G[p + ".ln2.g"], G[p + ".ln2.b"] = self.ln2.dg, self.ln2.db
+        G[p + ".ffn2.w"], G[p + ".ffn2.b"] = self.f2.dw, self.f2.db
+        G[p + ".ffn1.w"], G[p + ".ffn1.b"] = self.f1.dw, self.f1.db
+        G[p + ".ln1.g"], G[p + ".ln1.b"] = self.ln1.dg, self.ln1.db
+        G[p + ".o.w"], G[p + ".o.b"] = self.att.out.dw, self.att.out.db
+        G[p + ".qkv.w"], G[p + ".qkv.b"] = self.att.qkv.dw, self.att.qkv.db
+        return dv + dx if need_dx else None
+
+
+class Bert(_Net):
+    """Encoder layers, then the pooler tanh(W_p h_0 + b_p) on the first token
+    and a linear classifier."""
+
+    def __init__(self, P, nlayers=None):
+        n = BERT["layers"] if nlayers is None else nlayers
+        self.layers = [EncoderLayer(P, f"enc{i}", BERT["heads"]) for i in range(n)]
+        self.pool = Lyr.Linear(P["pool.w"], P["pool.b"])
+        self.tanh = Lyr.Tanh()
+        self.cls = Lyr.Linear(P["cls.w"], P["cls.b"])
+
+    def fwd(self, x, lengths):
+        h = x
+        for l in self.layers:
+            h = l.fwd(h, lengths)
+        self.hshape = h.shape
+        return self.cls.fwd(self.tanh.fwd(self.pool.fwd(h[:, 0, :])))
+
+    def bwd(self, dz):
+        G = {}
+        dp = self.pool.bwd(self.tanh.bwd(self.cls.bwd(dz)))
+        G["cls.w"], G["cls.b"] = self.cls.dw, self.cls.db
+        G["pool.w"], G["pool.b"] = self.pool.dw, self.pool.db
+        dh = np.zeros(self.hshape, dp.dtype)
+        dh[:, 0, :] = dp
+        for i in range(len(self.layers) - 1, -1, -1):
+            dh = self.layers[i].bwd(dh, i > 0, G)
+        self.G = G
+
+
+def build(cid, P):
+    fam = FAMILY[cid]
+    if fam == "cnn":
+        return CNN(P)
+    if fam == "vgg":
+        return VGG(P, cid)
+    if fam == "resnet":
+        return ResNet(P, cid)
+    return Bert(P)
+
+
+# ----------------------------------------------------------------------------- inputs
+def decode_acts(acts, dt):
+    """Activations as the devices sent them: fp32 arrays pass through;
+    uint16 arrays are bf16 bit patterns, widened exactly (bits << 16)."""
+    a = np.asarray(acts)
+    if a.dtype == np.uint16:
+        a = (a.astype(np.uint32) << np.uint32(16)).view(np.float32)
+    return a.astype(dt)
+
+
+# ----------------------------------------------------------------------------- training step
+def sgd_update(params, grads, lr, momentum=0.0, mom_buf=None):
+    """theta <- theta - lr * g (Alg. 4).  With momentum mu (config 3):
+    v <- mu v + g (v starts at 0, so the first v is g), theta <- theta - lr v."""
+    if momentum == 0.0:
+        return params - lr * grads, None
+    v = grads.copy() if mom_buf is None else momentum * mom_buf + grads
+    return params - lr * v, v
+
+
+def server_forward(cid, params_flat, acts, lengths=None, dt=np.float64):
+    P = unpack(cid, params_flat, dt)
+    net = build(cid, P)
+    return net.fwd(decode_acts(acts, dt), lengths)
+
+
+def server_step(cid, params_flat, acts, labels, lengths=None, lr=0.01, momentum=0.0,
+                mom_buf=None, dt=np.float64):
+    """One activation-branch iteration of Algorithm 4 on one batch.
+
+    Returns a dict with the loss, the logits, the flat gradient, the updated
+    flat parameters and (for momentum) the updated buffer, all in ``dt``."""
+    P = unpack(cid, params_flat, dt)
+    net = build(cid, P)
+    z = net.fwd(decode_acts(acts, dt), lengths)
+    loss, dz = Lyr.cross_entropy(z, np.asarray(labels))
+    net.bwd(dz)
+    g = pack(cid, net.grads()).astype(dt)
+    theta = np.asarray(params_flat, dtype=dt)
+    new, v = sgd_update(theta, g, lr, momentum, None if mom_buf is None else np.asarray(mom_buf, dt))
+    return {"loss": loss, "logits": z, "grads": g, "params": new, "momentum": v}

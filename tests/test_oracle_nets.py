@@ -1,0 +1,114 @@
+"""Pins for the oracle's whole server networks and training step (CPU only).
+
+* the flat parameter layout the oracle derives equals the workload description,
+* loss, logits and every gradient equal an independent fp64 autograd
+  implementation (PyTorch CPU),
+* central finite differences of the loss on sampled parameters,
+* closed forms: zero classifier gives loss ln C; lr = 0 leaves parameters
+  unchanged; momentum buffer recursion; padded tokens never matter."""
+import numpy as np
+import pytest
+
+import fo_synth as S
+import oracle
+from oracle import nets
+from tests import torch_ref
+
+SMALL_B = {1: 3, 2: 2, 3: 4, 4: 2, 5: 2}
+
+
+def _inputs(cid, B, sub=7):
+    acts = S.make_acts(cid, 1, batch=B, sub=sub)[0]
+    labels = S.make_labels(cid, 1, batch=B, sub=sub)[0]
+    lengths = S.make_lengths(cid, 1, batch=B, sub=sub)[0] if cid == 4 else None
+    return acts, labels, lengths
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_layout_matches_workload(cid):
+    a = [(n, tuple(s)) for n, s in nets.param_layout(cid)]
+    b = [(n, tuple(s)) for n, s, _, _ in S.param_layout(cid)]
+    assert a == b
+    assert sum(int(np.prod(s)) for _, s in a) == S.param_count(cid)
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4])
+def test_step_matches_independent_autograd(cid):
+    B = SMALL_B[cid]
+    theta = S.init_params(cid)
+    acts, labels, lengths = _inputs(cid, B)
+    r = oracle.server_step(cid, theta, acts, labels, lengths)
+    x = nets.decode_acts(acts, np.float64)
+    tl, tz, tg = torch_ref.step(cid, theta, x, labels, lengths)
+    assert abs(r["loss"] - tl) <= 1e-12 * abs(tl)
+    np.testing.assert_allclose(r["logits"], tz, rtol=0, atol=1e-11 * np.abs(tz).max())
+    # every gradient entry, normwise per tensor
+    off = 0
+    for name, shape, _, _ in S.param_layout(cid):
+        n = int(np.prod(shape))
+        g, t = r["grads"][off:off + n], tg[off:off + n]
+        scale = np.abs(t).max()
+        assert np.abs(g - t).max() <= 1e-9 * scale + 1e-300, name
+        off += n
+    np.testing.assert_allclose(r["params"], theta - 0.01 * r["grads"], rtol=1e-15, atol=1e-18)
+
+
+@pytest.mark.parametrize("cid,n_probe", [(1, 12), (3, 10)])
+def test_step_gradient_finite_differences(cid, n_probe):
+    B = 2
+    theta = S.init_params(cid).astype(np.float64)
+    acts, labels, lengths = _inputs(cid, B, sub=3)
+    r = oracle.server_step(cid, theta, acts, labels, lengths)
+    rng = np.random.default_rng(5)
+    idx = rng.choice(theta.size, size=n_probe, replace=False)
+    # also probe the last entries (classifier bias)
+    idx = np.concatenate([idx, [theta.size - 1]])
+    h = 1e-6
+    gmax = np.abs(r["grads"]).max()
+    for i in idx:
+        tp, tm = theta.copy(), theta.copy()
+        tp[i] += h
+        tm[i] -= h
+        lp = oracle.server_step(cid, tp, acts, labels, lengths)["loss"]
+        lm = oracle.server_step(cid, tm, acts, labels, lengths)["loss"]
+        num = (lp - lm) / (2 * h)
+        assert abs(num - r["grads"][i]) <= 1e-6 * gmax, (i, num, r["grads"][i])
+
+
+@pytest.mark.parametrize("cid,C", [(1, 10), (2, 10), (3, 100), (4, 2)])
+def test_zero_classifier_gives_ln_c(cid, C):
+    theta = S.init_params(cid).astype(np.float64)
+    lay = S.param_layout(cid)
+    nlast = sum(int(np.prod(s)) for _, s, _, _ in lay[-2:])
+    theta[-nlast:] = 0.0
+    acts, labels, lengths = _inputs(cid, SMALL_B[cid])
+    r = oracle.server_step(cid, theta, acts, labels, lengths)
+    assert r["loss"] == pytest.approx(np.log(C), abs=1e-15)
+    np.testing.assert_array_equal(r["logits"], 0.0)
+
+
+def test_lr_zero_and_momentum_recursion():
+    cid = 3
+    theta = S.init_params(cid).astype(np.float64)
+    acts, labels, _ = _inputs(cid, 2)
+    r0 = oracle.server_step(cid, theta, acts, labels, lr=0.0, momentum=0.9)
+    np.testing.assert_array_equal(r0["params"], theta)
+    r1 = oracle.server_step(cid, theta, acts, labels, lr=0.01, momentum=0.9)
+    np.testing.assert_array_equal(r1["momentum"], r1["grads"])        # v_1 = g_1
+    r2 = oracle.server_step(cid, r1["params"], acts, labels, lr=0.01, momentum=0.9, mom_buf=r1["momentum"])
+    np.testing.assert_allclose(r2["momentum"], 0.9 * r1["grads"] + r2["grads"], rtol=1e-15)
+    np.testing.assert_allclose(r2["params"], r1["params"] - 0.01 * r2["momentum"], rtol=1e-15)
+
+
+def test_padded_tokens_never_matter():
+    cid = 4
+    theta = S.init_params(cid)
+    acts, labels, lengths = _inputs(cid, 2)
+    lengths = np.array([40, 77], np.int32)
+    r = oracle.server_step(cid, theta, acts, labels, lengths)
+    x2 = nets.decode_acts(acts, np.float64).copy()
+    x2[0, 40:] = 123.0
+    x2[1, 77:] = -55.0
+    r2 = oracle.server_step(cid, theta, x2, labels, lengths)
+    np.testing.assert_allclose(r2["logits"], r["logits"], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(r2["grads"], r["grads"], rtol=1e-9, atol=1e-12 * np.abs(r["grads"]).max())
