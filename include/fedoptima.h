@@ -1,0 +1,245 @@
+/*
+ * fedoptima.h -- C ABI of the FedOptima server hot path on MI355X (gfx950).
+ *
+ * FedOptima (Zhang, Wong, Varghese) splits a network between K devices and a
+ * server.  Devices train the first layers against a local auxiliary loss and
+ * upload the activations of their last layer; the server trains the remaining
+ * layers (the server-side network M_s) centrally on activation batches chosen
+ * by its Task Scheduler, and mixes device-side models that arrive into a
+ * global one with a staleness-dependent weight.  This library implements the
+ * server's part:
+ *
+ *   fo_server_step      one training iteration of M_s (Alg. 4, activation branch)
+ *   fo_async_aggregate  staleness-weighted mixing of one arriving model (Alg. 4,
+ *                       aggregation branch)
+ *   fo_pick_device      the Task Scheduler's get() (Alg. 3)
+ *
+ * together with the activation-queue pool and flow control they need
+ * (Alg. 2 put(), Sec. 3.4.1 and the memory bound of Eq. 3).
+ *
+ * Conventions for every entry point:
+ *   - Plain pointers and sizes only.  "device" pointers are HIP device memory
+ *     (any allocator), "host" pointers are ordinary host memory.
+ *   - GPU work is asynchronous and ordered on the stream bound to the handle
+ *     (a hipStream_t passed as void*; NULL is the legacy default stream).
+ *     Caller-owned device buffers must stay valid until that work completes.
+ *   - Every argument is checked on the host before anything is launched; a
+ *     failing check launches nothing and returns a negative fo_status.  The
+ *     message for the last failure of the calling thread is fo_last_error().
+ *   - The library never allocates inside fo_server_step / fo_async_aggregate /
+ *     fo_pick_device; all device memory is allocated by the *_create calls.
+ */
+#ifndef FEDOPTIMA_H
+#define FEDOPTIMA_H
+
+#include <stdint.h>
+
+/* The library is built with hidden visibility; only the entry points below are exported. */
+#define FO_API __attribute__((visibility("default")))
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FO_OK = 0,        /* done                                                 */
+    FO_SKIPPED = 1,   /* aggregation dropped: staleness above the maximum delay */
+    FO_EMPTY = 2,     /* nothing to serve                                     */
+    FO_FULL = 3,      /* activation batch refused by flow control             */
+    FO_EINVAL = -1,   /* bad argument                                         */
+    FO_ENOMEM = -2,   /* device or host allocation failed                     */
+    FO_EHIP = -3,     /* a HIP runtime call failed                            */
+    FO_ESTATE = -4    /* call not valid in the current state                  */
+} fo_status;
+
+typedef struct fo_model fo_model;    /* opaque: server model, gradients, optimiser state, workspace */
+typedef struct fo_queues fo_queues;  /* opaque: Task Scheduler state and the activation pool        */
+
+/* A caller-owned flat fp32 vector in device memory, 16-byte aligned. */
+typedef struct { float* ptr; int64_t n; } fo_vec;
+
+/* One activation batch as sent by a device (device pointers).
+ *   x        CNN configs: [batch][C][H][W] (NCHW) -- fp32 for config 1, bf16 bit
+ *            patterns (uint16) for configs 2, 3, 5.  Transformer config 4:
+ *            [batch][L][d] bf16 hidden states, row-major.
+ *   lengths  config 4 only: int32[batch] valid-token counts in [1, L]; keys at
+ *            positions >= length are masked.  NULL for the CNN configs.
+ *   batch    1 <= batch <= the model's max_batch.                              */
+typedef struct { const void* x; const int32_t* lengths; int32_t batch; } fo_acts;
+
+/* ------------------------------------------------------------------ configs
+ * Configuration ids 1..5 fix the server network and its precision:
+ *   1  tiny CNN, fp32: conv3x3 32->64 + ReLU, maxpool2, conv3x3 64->64 + ReLU,
+ *      global average pool, linear 64->10; plain SGD.
+ *   2  VGG-16 after its first block (input [64,16,16]): 10 conv3x3 + ReLU with
+ *      4 max pools, FC 512-512-10; bf16 GEMMs, fp32 master weights; plain SGD.
+ *   3  ResNet-18 stages 2-4 (input [64,16,16]) with training-mode BatchNorm,
+ *      global average pool, FC 512->100; bf16; SGD with momentum 0.9.
+ *   4  BERT-base-shaped: 10 post-LN encoder layers (d=768, 12 heads, FFN 3072,
+ *      exact GELU), tanh pooler on token 0, linear 768->2; bf16; plain SGD.
+ *   5  same network as 2 (the 128-device pool-stress workload).
+ * Loss: mean softmax cross-entropy over the batch (the server loss f_s, Eq. 5).
+ * Learning rate 0.01.  Parameter layout of the flat fp32 vector ("library
+ * layout"): layers in network order; per layer weight then bias (or scale then
+ * shift for norms); conv weights [Cout][kh][kw][Cin], linear weights [out][in],
+ * attention input projection [3d][d] with query, key, value rows in that order. */
+
+/* Number of parameters of a configuration (host only; -1 for a bad id). */
+FO_API int64_t fo_config_param_count(int32_t config_id);
+/* Number of classes (logits per sample) of a configuration (-1 for a bad id). */
+FO_API int32_t fo_config_num_classes(int32_t config_id);
+
+/* ------------------------------------------------------------------ model
+ * Creates the server model of `config_id` for batches of up to `max_batch`
+ * samples.  `host_init` (host, fp32, n_params = fo_config_param_count) is
+ * copied to the device.  All device memory the step needs is allocated here.
+ * `hip_stream` is the stream every later call on this model uses.
+ * Errors: FO_EINVAL (bad id, size mismatch, max_batch < 1), FO_ENOMEM, FO_EHIP. */
+FO_API fo_status fo_model_create(int32_t config_id, int32_t max_batch, const float* host_init,
+                          int64_t n_params, void* hip_stream, fo_model** out);
+FO_API void fo_model_destroy(fo_model* model);
+
+/* One centralized training iteration of M_s on one activation batch
+ * (Alg. 4, activation branch): forward of M_s, loss f_s, backward, then
+ * theta_s <- theta_s - gamma_s * grad (with momentum for config 3).  The
+ * activation gradient of the first server layer is never formed: devices do
+ * not receive gradients from the server.  `labels` is a device int32[batch]
+ * of class ids in [0, classes).  `device_id` (>= 0) names the device the batch
+ * came from and is counted per device (fo_model_steps).  Asynchronous on the
+ * model's stream; loss and logits of this step stay readable until the next
+ * step.  Errors: FO_EINVAL (NULL pointers, batch out of range, lengths
+ * missing for config 4, device_id < 0), FO_EHIP. */
+FO_API fo_status fo_server_step(fo_model* model, const fo_acts* acts, const int32_t* labels,
+                         int32_t device_id);
+
+/* Steps taken so far on batches from `device_id` (all devices if -1). */
+FO_API int64_t fo_model_steps(const fo_model* model, int32_t device_id);
+
+enum {
+    FO_BUF_PARAMS = 0,    /* fp32 master parameters, library layout             */
+    FO_BUF_GRADS = 1,     /* fp32 gradient of the last step, library layout     */
+    FO_BUF_LOGITS = 2,    /* fp32 [batch][classes] logits of the last step      */
+    FO_BUF_LOSS = 3,      /* fp32 scalar loss of the last step                  */
+    FO_BUF_MOMENTUM = 4   /* fp32 momentum buffer (config 3 only)               */
+};
+/* Element count of a readable buffer (-1 if the model has none of that kind). */
+FO_API int64_t fo_model_buffer_size(const fo_model* model, int32_t which);
+/* Synchronous copies between a model buffer and host memory (host_out/host_in
+ * hold n fp32 values; n must equal fo_model_buffer_size, except LOGITS where
+ * n = batch * classes of the last step).  Used for parity checks and for
+ * checkpoint / resume.  Errors: FO_EINVAL, FO_ESTATE (no step yet), FO_EHIP. */
+FO_API fo_status fo_model_read(fo_model* model, int32_t which, float* host_out, int64_t n);
+FO_API fo_status fo_model_write(fo_model* model, int32_t which, const float* host_in, int64_t n);
+
+/* ------------------------------------------------------------------ aggregation
+ * Staleness-weighted mixing of one arriving device-side model (Alg. 4,
+ * aggregation branch).  global (device, fp32, n) is updated in place with
+ * local (device, fp32, same n):
+ *     if staleness > D (see fo_set_max_delay): nothing changes, FO_SKIPPED;
+ *     else w = alpha / (staleness + 1) and global <- global + w * (local - global).
+ * With alpha = 1 the weight is the 1/(t - t_k + 1) of Alg. 4; alpha = 0 leaves
+ * global unchanged bit for bit, as does local == global.  The device-side
+ * model and its auxiliary model are mixed by the same rule, so callers pass
+ * them as one flat vector.  Runs on the stream set by fo_set_stream for the
+ * calling thread.  Errors: FO_EINVAL (NULL, n mismatch or < 0, pointers not
+ * 16-byte aligned, alpha outside [0,1], staleness < 0), FO_EHIP. */
+FO_API fo_status fo_async_aggregate(fo_vec* global, const fo_vec* local, float alpha, int32_t staleness);
+
+/* Stream used by fo_async_aggregate on the calling thread (default NULL). */
+FO_API fo_status fo_set_stream(void* hip_stream);
+/* Maximum delay D of Alg. 4 for the whole library; D < 0 means no cutoff
+ * (the default). */
+FO_API fo_status fo_set_max_delay(int64_t max_delay);
+
+/* ------------------------------------------------------------------ scheduler + pool
+ * The Task Scheduler (Alg. 2 put(), Alg. 3 get()) over K per-device activation
+ * queues Q_k and a model queue, with consumption counters c_k, the global
+ * version t of Alg. 4, and the activation flow control of Sec. 3.4.1.
+ *
+ * Pool: n_slots fixed-size slots preallocated in device memory (slot_bytes of
+ * activations, batch int32 labels and, if with_lengths, batch int32 lengths
+ * each).  slot_bytes == 0 keeps only the host bookkeeping (no device memory;
+ * pushes then carry no data).  Free slots form a stack handing out the lowest
+ * ids first; a released slot is reused first.
+ * Flow control: each device's Sender Status starts on.  A batch pushed while
+ * it is off is refused (FO_FULL; the device dropped it at the source).  An
+ * admitted batch switches it off; after every enqueue to or dequeue from Q_k
+ * the status of device k switches back on if the number of queued batches is
+ * below omega = n_slots - K.  Queued plus in-service batches therefore never
+ * exceed n_slots, whatever K is (Eq. 3: memory = model + omega activation
+ * batches, independent of the number of devices).
+ * Errors: FO_EINVAL (K < 1, n_slots <= K, batch < 1), FO_ENOMEM, FO_EHIP. */
+FO_API fo_status fo_queues_create(int32_t K, int64_t slot_bytes, int32_t batch, int32_t with_lengths,
+                           int64_t n_slots, void* hip_stream, fo_queues** out);
+FO_API void fo_queues_destroy(fo_queues* q);
+
+/* put() for an activation batch from device k (Alg. 2).  x_src holds
+ * slot_bytes, labels_src batch int32, lengths_src batch int32 (if the pool has
+ * lengths); src_on_host says whether the sources are host or device memory.
+ * The copies into the slot are ordered on the pool's stream.  Returns FO_OK
+ * (admitted), FO_FULL (refused by flow control; nothing copied) or an error
+ * (FO_EINVAL: k out of range, NULL source for a pool with device memory). */
+FO_API fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, const int32_t* labels_src,
+                         const int32_t* lengths_src, int32_t src_on_host);
+
+/* put() for a model message from device k with local version t_k (Alg. 2):
+ * appended to the model FIFO.  `local` (device fp32[n]) is not copied and must
+ * stay valid until the message is aggregated. */
+FO_API fo_status fo_queues_push_model(fo_queues* q, int32_t k, const float* local, int64_t n, int64_t t_k);
+
+/* get() (Alg. 3).  Returns:
+ *   -2  a model message is pending; serve it first (fo_aggregate_pending);
+ *   -1  every activation queue is empty;
+ *  k>=0 the non-empty queue with the smallest counter c_k (lowest k on ties);
+ *       its oldest batch is popped and becomes the batch in service, and c_k
+ *       is incremented.  The previous batch in service must have been released.
+ *  -3  misuse (NULL handle, or a batch still in service); see fo_last_error. */
+FO_API int32_t fo_pick_device(fo_queues* q);
+
+/* The batch popped by the last pick: device pointers into its slot (valid
+ * until fo_queues_release) plus its per-device sequence number and slot id. */
+FO_API fo_status fo_queues_in_service(fo_queues* q, fo_acts* acts_out, const int32_t** labels_out,
+                               int64_t* seq_out, int64_t* slot_out);
+/* Returns the in-service slot to the free stack.  Later pushes reuse it with
+ * copies ordered after the work already queued on the pool's stream, so call
+ * this after fo_server_step has been enqueued on the same stream. */
+FO_API fo_status fo_queues_release(fo_queues* q);
+
+/* Serves the oldest pending model message (Alg. 4, aggregation branch):
+ * staleness s = t - t_k; if s > D it is dropped (FO_SKIPPED, t unchanged);
+ * otherwise global is mixed with fo_async_aggregate's rule and t <- t + 1.
+ * k_out / staleness_out (may be NULL) report the message.  FO_EMPTY if no
+ * model is pending.  Runs on the pool's stream. */
+FO_API fo_status fo_aggregate_pending(fo_queues* q, fo_vec* global, float alpha, int32_t* k_out,
+                               int64_t* staleness_out);
+
+/* Drains every pending model message in FIFO order, fusing the mixes: each
+ * launch applies up to 64 messages to every element of global in registers
+ * (global read and written once per 64 messages), in FIFO order, so the
+ * result equals the same sequence of fo_aggregate_pending calls bit for bit.
+ * Stale messages are dropped as above and do not advance t.  applied_out /
+ * skipped_out may be NULL.  Runs on the pool's stream. */
+FO_API fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, float alpha, int32_t* applied_out,
+                                   int32_t* skipped_out);
+
+typedef struct {
+    int32_t K;
+    int64_t n_slots, omega;
+    int64_t queued, in_service, models_pending;
+    int64_t admitted, refused, picks, peak_queued;
+    int64_t version;            /* global version t */
+} fo_queue_stats;
+FO_API fo_status fo_queues_stats(const fo_queues* q, fo_queue_stats* out);
+/* Copies the counters c_k of the first K devices into c_out. */
+FO_API fo_status fo_queues_counters(const fo_queues* q, int64_t* c_out, int32_t K);
+/* A device joining mid-run: a new empty queue with c_k = 0 and its Sender on.
+ * Returns the new device index, or -1 on error. */
+FO_API int32_t fo_queues_add_device(fo_queues* q);
+
+/* ------------------------------------------------------------------ errors */
+FO_API const char* fo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FEDOPTIMA_H */

@@ -109,8 +109,13 @@ class TaskScheduler:
 
     # ------------------------------------------------------------ joining devices
     def add_device(self) -> int:
-        """A device joining mid-run starts with c_k = 0 and its Sender on."""
+        """A device joining mid-run starts with c_k = 0 and its Sender on; the
+        soft cap shrinks by one so the pool still holds every in-flight batch."""
         self.K += 1
+        if self.n_slots is not None:
+            self.omega = self.n_slots - self.K
+            if self.omega < 1:
+                raise ValueError("pool too small for the number of devices")
         self.q_act.append(deque())
         self.c.append(0)
         self.sender_on.append(True)

@@ -1,0 +1,270 @@
+"""Thin ctypes binding of libfedoptima.so.
+
+Functions carry the C names and only marshal arguments: torch tensors become
+device pointers (``data_ptr()``), numpy arrays host pointers, streams the raw
+``hipStream_t`` of a ``torch.cuda.Stream``.  Every step of the hot path runs in
+the library's HIP kernels; there is no Python or CPU fallback, and loading
+fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfedoptima.so")
+
+FO_OK, FO_SKIPPED, FO_EMPTY, FO_FULL = 0, 1, 2, 3
+FO_EINVAL, FO_ENOMEM, FO_EHIP, FO_ESTATE = -1, -2, -3, -4
+FO_BUF_PARAMS, FO_BUF_GRADS, FO_BUF_LOGITS, FO_BUF_LOSS, FO_BUF_MOMENTUM = range(5)
+
+EXPORTS = [
+    "fo_config_param_count", "fo_config_num_classes", "fo_model_create", "fo_model_destroy",
+    "fo_server_step", "fo_model_steps", "fo_model_buffer_size", "fo_model_read", "fo_model_write",
+    "fo_async_aggregate", "fo_set_stream", "fo_set_max_delay", "fo_queues_create", "fo_queues_destroy",
+    "fo_queues_push", "fo_queues_push_model", "fo_pick_device", "fo_queues_in_service",
+    "fo_queues_release", "fo_aggregate_pending", "fo_aggregate_pending_all", "fo_queues_stats",
+    "fo_queues_counters", "fo_queues_add_device", "fo_last_error",
+]
+
+
+class FoError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"fedoptima status {status}: {msg}")
+        self.status = status
+
+
+class fo_vec(C.Structure):
+    _fields_ = [("ptr", C.c_void_p), ("n", C.c_int64)]
+
+
+class fo_acts(C.Structure):
+    _fields_ = [("x", C.c_void_p), ("lengths", C.c_void_p), ("batch", C.c_int32)]
+
+
+class fo_queue_stats(C.Structure):
+    _fields_ = [("K", C.c_int32), ("n_slots", C.c_int64), ("omega", C.c_int64), ("queued", C.c_int64),
+                ("in_service", C.c_int64), ("models_pending", C.c_int64), ("admitted", C.c_int64),
+                ("refused", C.c_int64), ("picks", C.c_int64), ("peak_queued", C.c_int64),
+                ("version", C.c_int64)]
+
+
+_lib = None
+
+
+def lib():
+    """Loads the library (raises if it is missing)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2504_13850_amd.build.build()")
+        L = C.CDLL(LIB_PATH)
+        vp, i32, i64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
+        sig = {
+            "fo_config_param_count": (i64, [i32]),
+            "fo_config_num_classes": (i32, [i32]),
+            "fo_model_create": (C.c_int, [i32, i32, vp, i64, vp, C.POINTER(vp)]),
+            "fo_model_destroy": (None, [vp]),
+            "fo_server_step": (C.c_int, [vp, C.POINTER(fo_acts), vp, i32]),
+            "fo_model_steps": (i64, [vp, i32]),
+            "fo_model_buffer_size": (i64, [vp, i32]),
+            "fo_model_read": (C.c_int, [vp, i32, vp, i64]),
+            "fo_model_write": (C.c_int, [vp, i32, vp, i64]),
+            "fo_async_aggregate": (C.c_int, [C.POINTER(fo_vec), C.POINTER(fo_vec), f32, i32]),
+            "fo_set_stream": (C.c_int, [vp]),
+            "fo_set_max_delay": (C.c_int, [i64]),
+            "fo_queues_create": (C.c_int, [i32, i64, i32, i32, i64, vp, C.POINTER(vp)]),
+            "fo_queues_destroy": (None, [vp]),
+            "fo_queues_push": (C.c_int, [vp, i32, vp, vp, vp, i32]),
+            "fo_queues_push_model": (C.c_int, [vp, i32, vp, i64, i64]),
+            "fo_pick_device": (i32, [vp]),
+            "fo_queues_in_service": (C.c_int, [vp, C.POINTER(fo_acts), C.POINTER(vp), C.POINTER(i64),
+                                               C.POINTER(i64)]),
+            "fo_queues_release": (C.c_int, [vp]),
+            "fo_aggregate_pending": (C.c_int, [vp, C.POINTER(fo_vec), f32, C.POINTER(i32), C.POINTER(i64)]),
+            "fo_aggregate_pending_all": (C.c_int, [vp, C.POINTER(fo_vec), f32, C.POINTER(i32), C.POINTER(i32)]),
+            "fo_queues_stats": (C.c_int, [vp, C.POINTER(fo_queue_stats)]),
+            "fo_queues_counters": (C.c_int, [vp, vp, i32]),
+            "fo_queues_add_device": (i32, [vp]),
+            "fo_last_error": (C.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().fo_last_error().decode()
+
+
+def _check(st, allowed=(FO_OK,)):
+    if st not in allowed:
+        raise FoError(st, last_error())
+    return st
+
+
+def _dptr(t):
+    """Device (or host) address of a torch tensor / numpy array / int / None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ------------------------------------------------------------------ configs
+def fo_config_param_count(cid: int) -> int:
+    return lib().fo_config_param_count(cid)
+
+
+def fo_config_num_classes(cid: int) -> int:
+    return lib().fo_config_num_classes(cid)
+
+
+# ------------------------------------------------------------------ model
+def fo_model_create(cid: int, max_batch: int, host_init: np.ndarray, stream=None):
+    h = np.ascontiguousarray(host_init, dtype=np.float32)
+    out = C.c_void_p()
+    _check(lib().fo_model_create(cid, max_batch, h.ctypes.data, h.size, _stream(stream), C.byref(out)))
+    return out
+
+
+def fo_model_destroy(model):
+    lib().fo_model_destroy(model)
+
+
+def make_acts(x, lengths=None, batch=None) -> fo_acts:
+    b = batch if batch is not None else int(x.shape[0])
+    return fo_acts(_dptr(x), _dptr(lengths), b)
+
+
+def fo_server_step(model, acts, labels, device_id: int):
+    if not isinstance(acts, fo_acts):
+        acts = make_acts(*acts) if isinstance(acts, tuple) else make_acts(acts)
+    return _check(lib().fo_server_step(model, C.byref(acts), _dptr(labels), device_id))
+
+
+def fo_model_steps(model, device_id: int = -1) -> int:
+    return lib().fo_model_steps(model, device_id)
+
+
+def fo_model_read(model, which: int) -> np.ndarray:
+    n = lib().fo_model_buffer_size(model, which)
+    if n < 0:
+        raise FoError(FO_EINVAL, f"model has no buffer {which}")
+    out = np.empty(n, np.float32)
+    _check(lib().fo_model_read(model, which, out.ctypes.data, n))
+    return out
+
+
+def fo_model_write(model, which: int, host: np.ndarray):
+    h = np.ascontiguousarray(host, dtype=np.float32)
+    _check(lib().fo_model_write(model, which, h.ctypes.data, h.size))
+
+
+# ------------------------------------------------------------------ aggregation
+def fo_async_aggregate(global_, local, alpha: float, staleness: int) -> int:
+    g = fo_vec(_dptr(global_), int(global_.numel()))
+    l = fo_vec(_dptr(local), int(local.numel()))
+    return _check(lib().fo_async_aggregate(C.byref(g), C.byref(l), float(alpha), int(staleness)),
+                  (FO_OK, FO_SKIPPED))
+
+
+def fo_set_stream(stream):
+    _check(lib().fo_set_stream(_stream(stream)))
+
+
+def fo_set_max_delay(D: int):
+    _check(lib().fo_set_max_delay(int(D)))
+
+
+# ------------------------------------------------------------------ scheduler + pool
+def fo_queues_create(K: int, slot_bytes: int, batch: int, with_lengths: bool, n_slots: int, stream=None):
+    out = C.c_void_p()
+    _check(lib().fo_queues_create(K, slot_bytes, batch, int(bool(with_lengths)), n_slots, _stream(stream),
+                                  C.byref(out)))
+    return out
+
+
+def fo_queues_destroy(q):
+    lib().fo_queues_destroy(q)
+
+
+def fo_queues_push(q, k: int, x=None, labels=None, lengths=None, on_host: bool = False) -> int:
+    return _check(lib().fo_queues_push(q, k, _dptr(x), _dptr(labels), _dptr(lengths), int(on_host)),
+                  (FO_OK, FO_FULL))
+
+
+def fo_queues_push_model(q, k: int, local, t_k: int):
+    n = 0 if local is None else int(local.numel())
+    _check(lib().fo_queues_push_model(q, k, _dptr(local), n, int(t_k)))
+
+
+def fo_pick_device(q) -> int:
+    r = lib().fo_pick_device(q)
+    if r == -3:
+        raise FoError(FO_ESTATE, last_error())
+    return r
+
+
+def fo_queues_in_service(q):
+    acts = fo_acts()
+    lab = C.c_void_p()
+    seq = C.c_int64()
+    slot = C.c_int64()
+    _check(lib().fo_queues_in_service(q, C.byref(acts), C.byref(lab), C.byref(seq), C.byref(slot)))
+    return acts, lab.value, seq.value, slot.value
+
+
+def fo_queues_release(q):
+    _check(lib().fo_queues_release(q))
+
+
+def fo_aggregate_pending(q, global_, alpha: float):
+    g = fo_vec(_dptr(global_), int(global_.numel()))
+    k = C.c_int32()
+    s = C.c_int64()
+    st = _check(lib().fo_aggregate_pending(q, C.byref(g), float(alpha), C.byref(k), C.byref(s)),
+                (FO_OK, FO_SKIPPED, FO_EMPTY))
+    return st, k.value, s.value
+
+
+def fo_aggregate_pending_all(q, global_, alpha: float):
+    g = fo_vec(_dptr(global_), int(global_.numel()))
+    a = C.c_int32()
+    s = C.c_int32()
+    _check(lib().fo_aggregate_pending_all(q, C.byref(g), float(alpha), C.byref(a), C.byref(s)))
+    return a.value, s.value
+
+
+def fo_queues_stats(q) -> fo_queue_stats:
+    st = fo_queue_stats()
+    _check(lib().fo_queues_stats(q, C.byref(st)))
+    return st
+
+
+def fo_queues_counters(q, K: int) -> list:
+    out = np.zeros(K, np.int64)
+    _check(lib().fo_queues_counters(q, out.ctypes.data, K))
+    return out.tolist()
+
+
+def fo_queues_add_device(q) -> int:
+    r = lib().fo_queues_add_device(q)
+    if r < 0:
+        raise FoError(FO_EINVAL, last_error())
+    return r

@@ -1,0 +1,237 @@
+// C ABI entry points: errors, configuration queries, model lifetime, the
+// training step dispatch and the stand-alone aggregation call.
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "model.h"
+
+namespace fo {
+
+static thread_local char tl_error[512] = "";
+static thread_local hipStream_t tl_agg_stream = nullptr;
+extern std::atomic<int64_t> g_max_delay;
+
+void set_error(const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(tl_error, sizeof(tl_error), fmt, ap);
+    va_end(ap);
+}
+
+// Parameter counts and classes per configuration (derived from the layer
+// lists in the model executors).
+int64_t cnn32_param_count();
+int64_t cnn16_param_count(int32_t cid);
+int64_t bert_param_count();
+
+}  // namespace fo
+
+using namespace fo;
+
+extern "C" const char* fo_last_error(void) { return tl_error; }
+
+extern "C" int64_t fo_config_param_count(int32_t cid) {
+    switch (cid) {
+        case 1: return cnn32_param_count();
+        case 2: case 3: case 5: return cnn16_param_count(cid);
+        case 4: return bert_param_count();
+        default: return -1;
+    }
+}
+
+extern "C" int32_t fo_config_num_classes(int32_t cid) {
+    switch (cid) {
+        case 1: case 2: case 5: return 10;
+        case 3: return 100;
+        case 4: return 2;
+        default: return -1;
+    }
+}
+
+static const Family* family_of(int32_t cid) {
+    switch (cid) {
+        case 1: return family_cnn32();
+        case 2: case 3: case 5: return family_cnn16();
+        case 4: return family_bert();
+        default: return nullptr;
+    }
+}
+
+extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float* host_init, int64_t n_params,
+                                     void* hip_stream, fo_model** out) {
+    FO_CHECK(out != nullptr, "fo_model_create: out is NULL");
+    *out = nullptr;
+    const Family* fam = family_of(cid);
+    FO_CHECK(fam != nullptr, "fo_model_create: unknown config %d", cid);
+    FO_CHECK(max_batch >= 1 && max_batch <= 4096, "fo_model_create: max_batch=%d out of range [1,4096]", max_batch);
+    FO_CHECK(host_init != nullptr, "fo_model_create: host_init is NULL");
+    int64_t np = fo_config_param_count(cid);
+    FO_CHECK(n_params == np, "fo_model_create: n_params=%lld, config %d has %lld", (long long)n_params, cid,
+             (long long)np);
+    fo_model* m = new (std::nothrow) fo_model();
+    if (!m) return FO_ENOMEM;
+    m->cid = cid;
+    m->max_batch = max_batch;
+    m->classes = fo_config_num_classes(cid);
+    m->stream = (hipStream_t)hip_stream;
+    m->n_params = np;
+    m->momentum = cid == 3 ? 0.9f : 0.f;
+    m->fam = fam;
+    const bool bf16 = cid != 1;
+    size_t bytes = 0;
+    auto add = [&](size_t b) { bytes += (b + 255) & ~size_t(255); };
+    add(sizeof(float) * np);                          // params
+    add(sizeof(float) * np);                          // grads
+    if (m->momentum != 0.f) add(sizeof(float) * np);  // momentum
+    if (bf16) add(sizeof(bf16_t) * np);               // shadow (high part)
+    if (bf16) add(sizeof(bf16_t) * np);               // shadow (low part)
+    add(sizeof(float) * (size_t)max_batch * m->classes);
+    add(sizeof(float) * 64);
+    bytes += fam->workspace_bytes(m) + 4096;
+    hipError_t e = hipMalloc((void**)&m->mem, bytes);
+    if (e != hipSuccess) {
+        set_error("fo_model_create: hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+        delete m;
+        return e == hipErrorOutOfMemory ? FO_ENOMEM : FO_EHIP;
+    }
+    m->arena.base = m->mem;
+    m->arena.size = bytes;
+    m->params = m->arena.take<float>(np);
+    m->grads = m->arena.take<float>(np);
+    if (m->momentum != 0.f) m->mom = m->arena.take<float>(np);
+    if (bf16) m->w16 = m->arena.take<bf16_t>(np);
+    if (bf16) m->w16lo = m->arena.take<bf16_t>(np);
+    m->logits = m->arena.take<float>((size_t)max_batch * m->classes);
+    m->loss = m->arena.take<float>(64);
+    fo_status st = FO_OK;
+    e = hipMemcpyAsync(m->params, host_init, sizeof(float) * np, hipMemcpyHostToDevice, m->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(m->grads, 0, sizeof(float) * np, m->stream);
+    if (e == hipSuccess && m->mom) e = hipMemsetAsync(m->mom, 0, sizeof(float) * np, m->stream);
+    if (e != hipSuccess) {
+        set_error("fo_model_create: upload: %s", hipGetErrorString(e));
+        st = FO_EHIP;
+    }
+    if (st == FO_OK && m->w16) st = launch_cast_bf16(m->params, m->w16, m->w16lo, np, m->stream);
+    if (st == FO_OK) st = fam->init(m);
+    if (st == FO_OK) {
+        e = hipStreamSynchronize(m->stream);
+        if (e != hipSuccess) {
+            set_error("fo_model_create: %s", hipGetErrorString(e));
+            st = FO_EHIP;
+        }
+    }
+    if (st != FO_OK) {
+        fo_model_destroy(m);
+        return st;
+    }
+    *out = m;
+    return FO_OK;
+}
+
+extern "C" void fo_model_destroy(fo_model* m) {
+    if (!m) return;
+    if (m->mem) (void)hipStreamSynchronize(m->stream);
+    if (m->fam && m->plan) m->fam->destroy(m);
+    if (m->mem) (void)hipFree(m->mem);
+    delete m;
+}
+
+extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int32_t* labels, int32_t device_id) {
+    FO_CHECK(m != nullptr, "fo_server_step: NULL model");
+    FO_CHECK(acts != nullptr && acts->x != nullptr, "fo_server_step: NULL activations");
+    FO_CHECK(labels != nullptr, "fo_server_step: NULL labels");
+    FO_CHECK(acts->batch >= 1 && acts->batch <= m->max_batch, "fo_server_step: batch=%d outside [1,%d]",
+             acts->batch, m->max_batch);
+    FO_CHECK(device_id >= 0, "fo_server_step: device_id=%d must be >= 0", device_id);
+    FO_CHECK(m->cid != 4 || acts->lengths != nullptr, "fo_server_step: config 4 needs sequence lengths");
+    FO_CHECK(((uintptr_t)acts->x % 16) == 0, "fo_server_step: activations not 16-byte aligned");
+    fo_status st = m->fam->step(m, acts, labels);
+    if (st != FO_OK) return st;
+    m->last_batch = acts->batch;
+    m->steps_total++;
+    if ((size_t)device_id >= m->steps_per_device.size()) m->steps_per_device.resize(device_id + 1, 0);
+    m->steps_per_device[device_id]++;
+    return FO_OK;
+}
+
+extern "C" int64_t fo_model_steps(const fo_model* m, int32_t device_id) {
+    if (!m) return -1;
+    if (device_id < 0) return m->steps_total;
+    return (size_t)device_id < m->steps_per_device.size() ? m->steps_per_device[device_id] : 0;
+}
+
+extern "C" int64_t fo_model_buffer_size(const fo_model* m, int32_t which) {
+    if (!m) return -1;
+    switch (which) {
+        case FO_BUF_PARAMS: case FO_BUF_GRADS: return m->n_params;
+        case FO_BUF_LOGITS: return (int64_t)m->last_batch * m->classes;
+        case FO_BUF_LOSS: return 1;
+        case FO_BUF_MOMENTUM: return m->mom ? m->n_params : -1;
+        default: return -1;
+    }
+}
+
+static float* buffer_ptr(fo_model* m, int32_t which) {
+    switch (which) {
+        case FO_BUF_PARAMS: return m->params;
+        case FO_BUF_GRADS: return m->grads;
+        case FO_BUF_LOGITS: return m->logits;
+        case FO_BUF_LOSS: return m->loss;
+        case FO_BUF_MOMENTUM: return m->mom;
+        default: return nullptr;
+    }
+}
+
+extern "C" fo_status fo_model_read(fo_model* m, int32_t which, float* host_out, int64_t n) {
+    FO_CHECK(m != nullptr && host_out != nullptr, "fo_model_read: NULL argument");
+    float* p = buffer_ptr(m, which);
+    FO_CHECK(p != nullptr, "fo_model_read: model has no buffer %d", which);
+    if ((which == FO_BUF_LOGITS || which == FO_BUF_LOSS) && m->steps_total == 0) {
+        set_error("fo_model_read: no step has run yet");
+        return FO_ESTATE;
+    }
+    FO_CHECK(n == fo_model_buffer_size(m, which), "fo_model_read: n=%lld, buffer holds %lld", (long long)n,
+             (long long)fo_model_buffer_size(m, which));
+    FO_HIP(hipMemcpyAsync(host_out, p, sizeof(float) * n, hipMemcpyDeviceToHost, m->stream));
+    FO_HIP(hipStreamSynchronize(m->stream));
+    return FO_OK;
+}
+
+extern "C" fo_status fo_model_write(fo_model* m, int32_t which, const float* host_in, int64_t n) {
+    FO_CHECK(m != nullptr && host_in != nullptr, "fo_model_write: NULL argument");
+    FO_CHECK(which == FO_BUF_PARAMS || which == FO_BUF_MOMENTUM, "fo_model_write: only PARAMS and MOMENTUM");
+    float* p = buffer_ptr(m, which);
+    FO_CHECK(p != nullptr, "fo_model_write: model has no buffer %d", which);
+    FO_CHECK(n == m->n_params, "fo_model_write: n=%lld, buffer holds %lld", (long long)n, (long long)m->n_params);
+    FO_HIP(hipMemcpyAsync(p, host_in, sizeof(float) * n, hipMemcpyHostToDevice, m->stream));
+    if (which == FO_BUF_PARAMS && m->w16) {
+        fo_status st = launch_cast_bf16(m->params, m->w16, m->w16lo, m->n_params, m->stream);
+        if (st != FO_OK) return st;
+    }
+    FO_HIP(hipStreamSynchronize(m->stream));
+    return FO_OK;
+}
+
+extern "C" fo_status fo_set_stream(void* hip_stream) {
+    tl_agg_stream = (hipStream_t)hip_stream;
+    return FO_OK;
+}
+
+extern "C" fo_status fo_async_aggregate(fo_vec* global, const fo_vec* local, float alpha, int32_t staleness) {
+    FO_CHECK(global != nullptr && local != nullptr, "fo_async_aggregate: NULL vector");
+    FO_CHECK(global->n == local->n, "fo_async_aggregate: lengths differ (%lld vs %lld)", (long long)global->n,
+             (long long)local->n);
+    FO_CHECK(global->n >= 0, "fo_async_aggregate: negative length");
+    FO_CHECK(global->n == 0 || (global->ptr != nullptr && local->ptr != nullptr), "fo_async_aggregate: NULL data");
+    FO_CHECK(((uintptr_t)global->ptr % 16) == 0 && ((uintptr_t)local->ptr % 16) == 0,
+             "fo_async_aggregate: vectors must be 16-byte aligned");
+    FO_CHECK(alpha >= 0.f && alpha <= 1.f, "fo_async_aggregate: alpha=%g outside [0,1]", (double)alpha);
+    FO_CHECK(staleness >= 0, "fo_async_aggregate: staleness=%d < 0", staleness);
+    int64_t D = g_max_delay.load();
+    if (D >= 0 && staleness > D) return FO_SKIPPED;
+    float w = alpha / (float)(staleness + 1);
+    return launch_agg_lerp(global->ptr, local->ptr, global->n, w, tl_agg_stream);
+}

@@ -1,0 +1,83 @@
+// bf16 MFMA GEMM / implicit-GEMM convolution for gfx950.
+//
+//   C[m][n] = sum_k A(m,k) * B(n,k)        fp32 accumulation
+//
+// A and B are read through "loaders" that describe where element (row, k)
+// lives, so one kernel serves linear layers (forward, input gradient, weight
+// gradient) and NHWC convolutions as implicit GEMMs (forward, input gradient,
+// weight gradient) without materialising im2col matrices.
+#pragma once
+
+#include "common.h"
+
+namespace fo {
+
+enum OperandMode : int {
+    OP_RK = 0,        // element (r,k) at P[r*ld + k]     (k contiguous)
+    OP_KR = 1,        // element (r,k) at P[k*ld + r]     (r contiguous)
+    OP_CONV_FWD = 2,  // A of a conv forward:  r = output pixel, k = (ky,kx,ci); P = input NHWC
+    OP_CONV_DX = 3,   // A of a conv dgrad:    r = input pixel,  k = (ky,kx,co); P = dY NHWC
+    OP_CONV_DXW = 4,  // B of a conv dgrad:    r = ci,           k = (ky,kx,co); P = W [co][ky][kx][ci]
+    OP_CONV_DWX = 5,  // B of a conv wgrad:    r = (ky,kx,ci),   k = output pixel; P = input NHWC
+};
+
+struct ConvGeom {
+    int Bn = 0, H = 0, W = 0, Ci = 0;  // input  [Bn][H][W][Ci]
+    int Ho = 0, Wo = 0, Co = 0;        // output [Bn][Ho][Wo][Co]
+    int kh = 1, kw = 1, stride = 1, pad = 0;
+};
+
+enum Act : int { ACT_NONE = 0, ACT_RELU = 1, ACT_GELU = 2 };
+
+struct GemmDesc {
+    int M = 0, N = 0, K = 0;
+    int amode = OP_RK, bmode = OP_RK;
+    const bf16_t* A = nullptr;
+    int64_t lda = 0;
+    const bf16_t* B = nullptr;
+    int64_t ldb = 0;
+    // Compensated (split-bf16) products: with A2 / B2 the low parts of A / B
+    // (x = hi + lo, hi = bf16(x), lo = bf16(x - hi)), nseg = 3 accumulates
+    // A.B + A.B2 + A2.B over three K segments: the result carries about 16
+    // bits of operand precision instead of 8 (the lo.lo term is below it).
+    // nseg = 2 keeps the first two segments (for an A that is exactly bf16).
+    const bf16_t* A2 = nullptr;
+    const bf16_t* B2 = nullptr;
+    int nseg = 1;
+    ConvGeom g;
+    // epilogue, applied in this order: + bias[n], + resid[m][n] (fp32),
+    // act (GELU stores its input to `pre` when set), * [mask[m][n] > 0],
+    // * GELU'(dpre[m][n]); then stores to Cf (fp32) and/or Cb (bf16).
+    const float* bias = nullptr;
+    const float* resid = nullptr;
+    int64_t ldr = 0;
+    int act = ACT_NONE;
+    bf16_t* pre = nullptr;
+    const bf16_t* mask = nullptr;
+    const bf16_t* dpre = nullptr;
+    int64_t ldm = 0;  // leading dimension of pre / mask / dpre
+    float* Cf = nullptr;
+    int64_t ldcf = 0;
+    bf16_t* Cb = nullptr;   // bf16(v)
+    bf16_t* Cb2 = nullptr;  // bf16(v - bf16(v)), the low part (same leading dimension)
+    int64_t ldcb = 0;
+    // split-K: z-slices write fp32 partials to ws[z][M][N]; a second pass sums
+    // them and runs the epilogue.
+    int splits = 1;
+    float* ws = nullptr;
+    // Optional device-side bounds (packed variable-length batches): the
+    // effective M (or K) is min(M, *Mdev) (or min(K, *Kdev)); the grid is
+    // sized by the static M, and tiles past the effective bound do nothing.
+    const int* Mdev = nullptr;
+    const int* Kdev = nullptr;
+};
+
+// Enqueues the GEMM (and its split-K reduction) on stream s.
+fo_status gemm(const GemmDesc& d, hipStream_t s);
+
+// Bytes of split-K workspace a descriptor needs (0 if splits == 1).
+inline size_t gemm_ws_bytes(int M, int N, int splits) {
+    return splits > 1 ? sizeof(float) * (size_t)M * N * splits : 0;
+}
+
+}  // namespace fo

@@ -1,0 +1,475 @@
+// bf16 MFMA GEMM / implicit-GEMM convolution for gfx950 (CDNA4).
+//
+// Tiling: a 256-thread workgroup (4 waves of 64) computes a 128x128 tile of C;
+// each wave owns a 64x64 sub-tile = 2x2 v_mfma_f32_32x32x16_bf16 accumulators
+// (64 fp32 per lane).  K advances in steps of 32 through two LDS buffers
+// (global loads of step t+1 are in flight while the MFMAs of step t run).
+// LDS tiles hold 128 rows x 32 k (64 B per row) with an XOR swizzle of the
+// 16-byte chunks so that the 128-bit MFMA operand reads and the stores of
+// k-contiguous operands are bank-conflict free.  Operands whose rows are
+// contiguous in memory (weight gradients, input gradients through W) are
+// transposed on their way into LDS (k pairs packed into 32-bit stores).
+#include <algorithm>
+
+#include "gemm.h"
+#include "kernels.h"
+
+namespace fo {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 128, BN = 128, BK = 32, NT = 256;
+
+__device__ __forceinline__ int swz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 3); }
+// element offset of (row, k) inside a 128 x 32 LDS tile
+__device__ __forceinline__ int lds_idx(int row, int k) { return row * BK + ((((k >> 3) ^ swz(row))) << 3) + (k & 7); }
+
+__device__ __forceinline__ uint16_t half_of(const uint4& v, int e) {
+    uint32_t w = e < 2 ? v.x : e < 4 ? v.y : e < 6 ? v.z : v.w;
+    return (e & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xFFFFu);
+}
+
+__device__ __forceinline__ uint4 load8(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+
+__device__ __forceinline__ uint4 load8_guarded(const bf16_t* p, int n_ok) {
+    // first n_ok (0..8) elements from p, rest zero
+    uint16_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = e < n_ok ? p[e] : (uint16_t)0;
+    uint4 v;
+    v.x = h[0] | ((uint32_t)h[1] << 16);
+    v.y = h[2] | ((uint32_t)h[3] << 16);
+    v.z = h[4] | ((uint32_t)h[5] << 16);
+    v.w = h[6] | ((uint32_t)h[7] << 16);
+    return v;
+}
+
+// ------------------------------------------------------------------ loaders
+// Every loader keeps offsets relative to the operand's base pointer; the base
+// is passed per K tile so that compensated products can switch between the
+// high and the low part of an operand from one K segment to the next.
+
+// Row-major, k contiguous: thread -> (row = v/4, k chunk = v%4) for v = tid, tid+256.
+struct LdRK {
+    int64_t off[2];  // row offset, -1 past the last row
+    int64_t ld;
+    int row[2], kc;
+    bool vec;
+    uint4 v[2];
+    __device__ void init(const bf16_t* P, int64_t ld_, int r0, int R, int tid) {
+        ld = ld_;
+        kc = (tid & 3) * 8;
+        vec = (ld % 8 == 0) && (((uintptr_t)P & 15) == 0);
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            row[r] = (tid + NT * r) >> 2;
+            int gr = r0 + row[r];
+            off[r] = gr < R ? (int64_t)gr * ld : -1;
+        }
+    }
+    __device__ void load(const bf16_t* P, int kb, int kend) {
+        int k = kb + kc;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            if (off[r] < 0 || k >= kend) v[r] = make_uint4(0, 0, 0, 0);
+            else if (vec && k + 8 <= kend) v[r] = load8(P + off[r] + k);
+            else v[r] = load8_guarded(P + off[r] + k, kend - k);
+        }
+    }
+    __device__ void store(bf16_t* t) const {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) *reinterpret_cast<uint4*>(&t[lds_idx(row[r], kc)]) = v[r];
+    }
+};
+
+// Two consecutive k rows x 8 contiguous r per thread: kp = tid%16, r chunk = (tid/16)*8.
+// Stored transposed: 8 dwords, each the (k, k+1) pair of one r.
+struct LdKRBase {
+    int kp, rc;
+    uint4 v[2];
+    __device__ void store(bf16_t* t) const {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            uint32_t w = (uint32_t)half_of(v[0], e) | ((uint32_t)half_of(v[1], e) << 16);
+            *reinterpret_cast<uint32_t*>(&t[lds_idx(rc + e, 2 * kp)]) = w;
+        }
+    }
+};
+
+struct LdKR : LdKRBase {
+    int64_t ld;
+    int r, R;
+    bool vec;
+    __device__ void init(const bf16_t* P, int64_t ld_, int r0, int R_, int tid) {
+        ld = ld_;
+        R = R_;
+        kp = tid & 15;
+        rc = (tid >> 4) * 8;
+        r = r0 + rc;
+        vec = (ld % 8 == 0) && (((uintptr_t)P & 15) == 0);
+    }
+    __device__ void load(const bf16_t* P, int kb, int kend) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            int k = kb + 2 * kp + j;
+            if (k >= kend || r >= R) v[j] = make_uint4(0, 0, 0, 0);
+            else if (vec && r + 8 <= R) v[j] = load8(P + (int64_t)k * ld + r);
+            else v[j] = load8_guarded(P + (int64_t)k * ld + r, R - r);
+        }
+    }
+};
+
+// Conv forward A: r = output pixel (b, oy, ox); k = (ky, kx, ci), Ci % 32 == 0.
+struct LdConvFwd {
+    ConvGeom g;
+    int row[2], kc, b[2], oy[2], ox[2];
+    bool ok[2];
+    uint4 v[2];
+    __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
+        g = g_;
+        kc = (tid & 3) * 8;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            row[r] = (tid + NT * r) >> 2;
+            int gr = r0 + row[r];
+            ok[r] = gr < R;
+            int hw = g.Ho * g.Wo;
+            b[r] = gr / hw;
+            int rem = gr - b[r] * hw;
+            oy[r] = rem / g.Wo;
+            ox[r] = rem - oy[r] * g.Wo;
+        }
+    }
+    __device__ void load(const bf16_t* X, int kb, int kend) {
+        int tap = kb / g.Ci, ci = kb - tap * g.Ci + kc;
+        int ky = tap / g.kw, kx = tap - ky * g.kw;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            int iy = oy[r] * g.stride - g.pad + ky, ix = ox[r] * g.stride - g.pad + kx;
+            bool in = ok[r] && kb + kc < kend && iy >= 0 && iy < g.H && ix >= 0 && ix < g.W;
+            v[r] = in ? load8(X + (((int64_t)b[r] * g.H + iy) * g.W + ix) * g.Ci + ci) : make_uint4(0, 0, 0, 0);
+        }
+    }
+    __device__ void store(bf16_t* t) const {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) *reinterpret_cast<uint4*>(&t[lds_idx(row[r], kc)]) = v[r];
+    }
+};
+
+// Conv dgrad A: r = input pixel (b, iy, ix); k = (ky, kx, co) reads dY, Co % 32 == 0.
+struct LdConvDx {
+    ConvGeom g;
+    int row[2], kc, b[2], iy[2], ix[2];
+    bool ok[2];
+    uint4 v[2];
+    __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
+        g = g_;
+        kc = (tid & 3) * 8;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            row[r] = (tid + NT * r) >> 2;
+            int gr = r0 + row[r];
+            ok[r] = gr < R;
+            int hw = g.H * g.W;
+            b[r] = gr / hw;
+            int rem = gr - b[r] * hw;
+            iy[r] = rem / g.W;
+            ix[r] = rem - iy[r] * g.W;
+        }
+    }
+    __device__ void load(const bf16_t* DY, int kb, int kend) {
+        int tap = kb / g.Co, co = kb - tap * g.Co + kc;
+        int ky = tap / g.kw, kx = tap - ky * g.kw;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            int ty = iy[r] + g.pad - ky, tx = ix[r] + g.pad - kx;
+            bool in = ok[r] && kb + kc < kend && ty >= 0 && tx >= 0;
+            int oy = 0, ox = 0;
+            if (in) {
+                oy = ty / g.stride;
+                ox = tx / g.stride;
+                in = (oy * g.stride == ty) && (ox * g.stride == tx) && oy < g.Ho && ox < g.Wo;
+            }
+            v[r] = in ? load8(DY + (((int64_t)b[r] * g.Ho + oy) * g.Wo + ox) * g.Co + co) : make_uint4(0, 0, 0, 0);
+        }
+    }
+    __device__ void store(bf16_t* t) const {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) *reinterpret_cast<uint4*>(&t[lds_idx(row[r], kc)]) = v[r];
+    }
+};
+
+// Conv dgrad B: r = ci, k = (ky, kx, co): W[co][ky][kx][ci], ci contiguous.
+struct LdConvDxW : LdKRBase {
+    ConvGeom g;
+    int r;
+    __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
+        g = g_;
+        kp = tid & 15;
+        rc = (tid >> 4) * 8;
+        r = r0 + rc;
+        (void)R;
+    }
+    __device__ void load(const bf16_t* Wt, int kb, int kend) {
+        int tap = kb / g.Co;
+        int KK = g.kh * g.kw;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            int k = kb + 2 * kp + j;
+            int co = k - tap * g.Co;
+            bool in = k < kend && r < g.Ci;
+            v[j] = in ? load8(Wt + ((int64_t)co * KK + tap) * g.Ci + r) : make_uint4(0, 0, 0, 0);
+        }
+    }
+};
+
+// Conv wgrad B: r = (ky, kx, ci), k = output pixel; reads the input NHWC.
+struct LdConvDwX : LdKRBase {
+    ConvGeom g;
+    int ky, kx, ci;
+    bool rok;
+    __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
+        g = g_;
+        kp = tid & 15;
+        rc = (tid >> 4) * 8;
+        int n = r0 + rc;
+        rok = n < R;
+        int tap = n / g.Ci;
+        ci = n - tap * g.Ci;
+        ky = tap / g.kw;
+        kx = tap - ky * g.kw;
+    }
+    __device__ void load(const bf16_t* X, int kb, int kend) {
+        int hw = g.Ho * g.Wo;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            int pix = kb + 2 * kp + j;
+            bool in = rok && pix < kend;
+            int b = 0, iy = 0, ix = 0;
+            if (in) {
+                b = pix / hw;
+                int rem = pix - b * hw;
+                int oy = rem / g.Wo, ox = rem - oy * g.Wo;
+                iy = oy * g.stride - g.pad + ky;
+                ix = ox * g.stride - g.pad + kx;
+                in = iy >= 0 && iy < g.H && ix >= 0 && ix < g.W;
+            }
+            v[j] = in ? load8(X + (((int64_t)b * g.H + iy) * g.W + ix) * g.Ci + ci) : make_uint4(0, 0, 0, 0);
+        }
+    }
+};
+
+template <int MODE>
+struct LoaderOf;
+template <> struct LoaderOf<OP_RK> { typedef LdRK T; };
+template <> struct LoaderOf<OP_KR> { typedef LdKR T; };
+template <> struct LoaderOf<OP_CONV_FWD> { typedef LdConvFwd T; };
+template <> struct LoaderOf<OP_CONV_DX> { typedef LdConvDx T; };
+template <> struct LoaderOf<OP_CONV_DXW> { typedef LdConvDxW T; };
+template <> struct LoaderOf<OP_CONV_DWX> { typedef LdConvDwX T; };
+
+template <int MODE>
+__device__ __forceinline__ void loader_init(typename LoaderOf<MODE>::T& L, const bf16_t* P, int64_t ld,
+                                            const ConvGeom& g, int r0, int R, int tid) {
+    if constexpr (MODE == OP_RK || MODE == OP_KR)
+        L.init(P, ld, r0, R, tid);
+    else
+        L.init(P, g, r0, R, tid);
+}
+
+// ------------------------------------------------------------------ epilogue
+__device__ __forceinline__ float gelu_f(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
+__device__ __forceinline__ float gelu_grad(float x) {
+    float cdf = 0.5f * (1.f + erff(x * 0.70710678118654752f));
+    float pdf = 0.39894228040143268f * expf(-0.5f * x * x);
+    return cdf + x * pdf;
+}
+
+__device__ __forceinline__ void epilogue(const GemmDesc& d, int row, int col, float v) {
+    if (d.bias) v += d.bias[col];
+    if (d.resid) v += d.resid[(int64_t)row * d.ldr + col];
+    if (d.act == ACT_GELU) {
+        if (d.pre) d.pre[(int64_t)row * d.ldm + col] = f2bf(v);
+        v = gelu_f(v);
+    } else if (d.act == ACT_RELU) {
+        v = v > 0.f ? v : 0.f;
+    }
+    if (d.mask && !(bf2f(d.mask[(int64_t)row * d.ldm + col]) > 0.f)) v = 0.f;
+    if (d.dpre) v *= gelu_grad(bf2f(d.dpre[(int64_t)row * d.ldm + col]));
+    if (d.Cf) d.Cf[(int64_t)row * d.ldcf + col] = v;
+    if (d.Cb) {
+        const bf16_t hi = f2bf(v);
+        d.Cb[(int64_t)row * d.ldcb + col] = hi;
+        if (d.Cb2) d.Cb2[(int64_t)row * d.ldcb + col] = f2bf(v - bf2f(hi));
+    }
+}
+
+// ------------------------------------------------------------------ kernel
+template <int AM, int BMODE>
+__global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchunk) {
+    __shared__ __attribute__((aligned(16))) bf16_t smem[2][2][BM * BK];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
+    const int Keff = d.Kdev ? min(d.K, *d.Kdev) : d.K;
+    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+    if (m0 >= M) return;  // uniform for the whole workgroup
+    // The K range of this slice, over the concatenation of nseg segments of
+    // length K (segment s pairs (A, B), (A, B2), (A2, B) for s = 0, 1, 2).
+    const int ktot = d.nseg * d.K;
+    const int kbeg = blockIdx.z * kchunk;
+    const int kstop = min(ktot, kbeg + kchunk);
+    const int nk = kstop > kbeg ? (kstop - kbeg + BK - 1) / BK : 0;
+
+    typename LoaderOf<AM>::T la;
+    typename LoaderOf<BMODE>::T lb;
+    loader_init<AM>(la, d.A, d.lda, d.g, m0, M, tid);
+    loader_init<BMODE>(lb, d.B, d.ldb, d.g, n0, d.N, tid);
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    auto load_tile = [&](int kg) {
+        // segments have length K (a multiple of BK when nseg > 1), so a tile never straddles two
+        const int seg = kg / d.K, kk = kg - seg * d.K;
+        la.load(seg == 2 ? d.A2 : d.A, kk, Keff);
+        lb.load(seg == 1 ? d.B2 : d.B, kk, Keff);
+    };
+
+    if (nk > 0) {
+        load_tile(kbeg);
+        la.store(smem[0][0]);
+        lb.store(smem[0][1]);
+    }
+    __syncthreads();
+
+    const int lrow = lane & 31, lk = (lane >> 5) * 8;
+    for (int t = 0; t < nk; ++t) {
+        const int cur = t & 1;
+        if (t + 1 < nk) load_tile(kbeg + (t + 1) * BK);
+        const bf16_t* As = smem[cur][0];
+        const bf16_t* Bs = smem[cur][1];
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            bf16x8_t a[2], b[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                a[i] = *reinterpret_cast<const bf16x8_t*>(&As[lds_idx(wm * 64 + i * 32 + lrow, ks * 16 + lk)]);
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                b[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[lds_idx(wn * 64 + j * 32 + lrow, ks * 16 + lk)]);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        if (t + 1 < nk) {
+            la.store(smem[cur ^ 1][0]);
+            lb.store(smem[cur ^ 1][1]);
+        }
+        __syncthreads();
+    }
+
+    // Accumulator (i, j, r) of this lane holds C[row][col] with
+    // row = i*32 + (r/4)*8 + (lane/32)*4 + r%4, col = j*32 + lane%32 (wave-relative).
+    // The tile leaves through LDS in two halves (i = 0, 1) of 64 rows x 128
+    // columns: then each thread owns one column and walks 32 rows, so every
+    // global store instruction covers 64 consecutive columns of one row.
+    float* Cs = reinterpret_cast<float*>(&smem[0][0][0]);  // 64 x 128 fp32 = the 32 KB of tiles
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int lr = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                Cs[lr * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+            }
+        __syncthreads();
+        const int c = tid & (BN - 1), col = n0 + c;
+        for (int lr = tid >> 7; lr < 64; lr += 2) {
+            const int row = m0 + (lr >> 5) * 64 + i * 32 + (lr & 31);
+            if (row < M && col < d.N) {
+                const float v = Cs[lr * BN + c];
+                if (d.splits > 1)
+                    d.ws[((int64_t)blockIdx.z * d.M + row) * d.N + col] = v;
+                else
+                    epilogue(d, row, col, v);
+            }
+        }
+        __syncthreads();
+    }
+}
+
+__global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
+    const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
+    int64_t total = (int64_t)M * d.N, full = (int64_t)d.M * d.N;
+    int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        float v = 0.f;
+        for (int z = 0; z < d.splits; ++z) v += d.ws[(int64_t)z * full + i];
+        epilogue(d, (int)(i / d.N), (int)(i % d.N), v);
+    }
+}
+
+template <int AM, int BMODE>
+void launch(const GemmDesc& d, int kchunk, hipStream_t s) {
+    dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
+    hipLaunchKernelGGL((gemm_kernel<AM, BMODE>), grid, dim3(NT), 0, s, d, kchunk);
+}
+
+}  // namespace
+
+fo_status gemm(const GemmDesc& d, hipStream_t s) {
+    FO_CHECK(d.M > 0 && d.N > 0 && d.K > 0, "gemm: empty problem %dx%dx%d", d.M, d.N, d.K);
+    FO_CHECK(d.splits >= 1 && (d.splits == 1 || d.ws != nullptr), "gemm: split-K needs a workspace");
+    FO_CHECK(d.Cf || d.Cb, "gemm: no output");
+    const bool conv = d.amode == OP_CONV_FWD || d.amode == OP_CONV_DX || d.bmode == OP_CONV_DXW ||
+                      d.bmode == OP_CONV_DWX;
+    if (conv) {
+        FO_CHECK(d.g.Ci % 32 == 0 || d.amode != OP_CONV_FWD, "gemm: conv forward needs Ci %% 32 == 0");
+        FO_CHECK(d.g.Co % 32 == 0 || d.amode != OP_CONV_DX, "gemm: conv dgrad needs Co %% 32 == 0");
+        FO_CHECK(d.g.Ci % 8 == 0, "gemm: conv needs Ci %% 8 == 0");
+    }
+    FO_CHECK(d.nseg >= 1 && d.nseg <= 3, "gemm: nseg=%d must be 1, 2 or 3", d.nseg);
+    if (d.nseg > 1) {
+        FO_CHECK(d.B2 && (d.nseg == 2 || d.A2), "gemm: compensated product needs its low parts");
+        FO_CHECK(d.K % BK == 0 && !d.Kdev, "gemm: compensated product needs a static K multiple of %d", BK);
+    }
+    const int ktot = d.nseg * d.K;
+    int kchunk = ktot;
+    if (d.splits > 1) {
+        kchunk = (int)cdiv(cdiv(ktot, d.splits), BK) * BK;
+        FO_CHECK((int64_t)kchunk * (d.splits - 1) < ktot, "gemm: %d splits leave an empty slice of K=%d",
+                 d.splits, ktot);
+    }
+    const int a = d.amode, b = d.bmode;
+    if (a == OP_RK && b == OP_RK) launch<OP_RK, OP_RK>(d, kchunk, s);
+    else if (a == OP_RK && b == OP_KR) launch<OP_RK, OP_KR>(d, kchunk, s);
+    else if (a == OP_KR && b == OP_KR) launch<OP_KR, OP_KR>(d, kchunk, s);
+    else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(d, kchunk, s);
+    else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(d, kchunk, s);
+    else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(d, kchunk, s);
+    else {
+        set_error("gemm: unsupported operand modes %d/%d", a, b);
+        return FO_EINVAL;
+    }
+    FO_LAUNCHED();
+    if (d.splits > 1) {
+        int64_t total = (int64_t)d.M * d.N;
+        int grid = (int)std::min<int64_t>(cdiv(total, 256), 4096);
+        hipLaunchKernelGGL(splitk_reduce, dim3(grid), dim3(256), 0, s, d);
+        FO_LAUNCHED();
+    }
+    return FO_OK;
+}
+
+}  // namespace fo

@@ -1,0 +1,52 @@
+// Host-side launchers of the HIP kernels (each defined in a k_*.hip file).
+#pragma once
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace fo {
+
+// ------------------------------------------------------------------ k_update.hip
+constexpr int kAggMaxFused = 64;
+struct AggTable {
+    int count;
+    const float* local[kAggMaxFused];
+    float w[kAggMaxFused];
+};
+fo_status launch_agg_lerp(float* g, const float* l, int64_t n, float w, hipStream_t s);
+fo_status launch_agg_lerp_multi(float* g, const AggTable& tab, int64_t n, hipStream_t s);
+// theta -= lr * g (momentum v <- mu v + g first when v is set); refreshes the
+// bf16 high/low shadows of theta when w16/w16lo are set.
+fo_status launch_sgd(float* p, const float* g, float* v, bf16_t* w16, bf16_t* w16lo, int64_t n, float lr, float mu,
+                     hipStream_t s);
+// y = bf16(x), ylo = bf16(x - y) (ylo may be NULL)
+fo_status launch_cast_bf16(const float* x, bf16_t* y, bf16_t* ylo, int64_t n, hipStream_t s);
+
+// ------------------------------------------------------------------ k_attn.hip
+// qkv [T][3d] fp32, cu int32[B+1] packed-row offsets (sequences <= 128 tokens,
+// head width 64); out / outlo [T][d] bf16 high and low parts of the output;
+// lse/Dws fp32 [B][H][128]; dout the bf16 output gradient, dqkv bf16 [T][3d].
+fo_status launch_attn_fwd(const float* qkv, const int* cu, bf16_t* out, bf16_t* outlo, float* lse, int B, int H,
+                          int d, hipStream_t s);
+fo_status launch_attn_bwd(const float* qkv, const int* cu, const bf16_t* out, const bf16_t* dout,
+                          const float* lse, float* Dws, bf16_t* dqkv, int B, int H, int d, hipStream_t s);
+
+// ------------------------------------------------------------------ k_common.hip
+// mean cross-entropy of logits z [B][C] and dz = (softmax - onehot)/B
+fo_status launch_xent(const float* z, const int32_t* labels, float* dz, float* loss, int B, int C, hipStream_t s);
+// out[c] = sum over rows r < min(rows, *rows_dev) of X[r*ld + c]; ws holds colsum_ws_floats(rows, N)
+size_t colsum_ws_floats(int rows, int N);
+fo_status launch_colsum(const float* X, int64_t ld, int rows, const int* rows_dev, int N, float* out, float* ws,
+                        hipStream_t s);
+fo_status launch_colsum(const bf16_t* X, int64_t ld, int rows, const int* rows_dev, int N, float* out, float* ws,
+                        hipStream_t s);
+fo_status launch_fill(float* p, int64_t n, float v, hipStream_t s);
+// y = act(x W^T + b) for small fp32 layers (x [B][I], W [O][I]); act = tanh or none
+fo_status launch_small_linear_fwd(const float* x, const float* w, const float* bias, float* y, int B, int I, int O,
+                                  bool tanh_act, hipStream_t s);
+// gw = dy^T x, gb = colsum dy, dx = (dy W) * (1 - xin_tanh^2 if given); dx may be NULL
+fo_status launch_small_linear_bwd(const float* dy, const float* x, const float* w, const float* xin_tanh, float* gw,
+                                  float* gb, float* dx, int B, int I, int O, hipStream_t s);
+
+}  // namespace fo

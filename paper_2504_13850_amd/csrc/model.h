@@ -1,0 +1,56 @@
+// The server model object behind fo_model and the per-family executors.
+#pragma once
+
+#include <vector>
+
+#include "kernels.h"
+
+namespace fo {
+struct Family;
+}
+
+struct fo_model {
+    int32_t cid = 0;
+    int32_t max_batch = 0;
+    int32_t classes = 0;
+    hipStream_t stream = nullptr;
+    int64_t n_params = 0;
+    float lr = 0.01f, momentum = 0.f;
+
+    // flat buffers in the library layout (device)
+    float* params = nullptr;   // fp32 master
+    float* grads = nullptr;    // fp32 gradient of the last step
+    float* mom = nullptr;      // momentum buffer (config 3)
+    fo::bf16_t* w16 = nullptr;   // bf16(params) (bf16 configs)
+    fo::bf16_t* w16lo = nullptr; // bf16(params - bf16(params)): low part for compensated products
+    float* logits = nullptr;   // [max_batch][classes]
+    float* loss = nullptr;     // scalar
+
+    int32_t last_batch = 0;
+    int64_t steps_total = 0;
+    std::vector<int64_t> steps_per_device;
+
+    char* mem = nullptr;       // one allocation for everything above and the workspace
+    fo::Arena arena;
+    const fo::Family* fam = nullptr;
+    void* plan = nullptr;      // family-specific state
+};
+
+namespace fo {
+
+struct Family {
+    // Bytes of workspace (beyond params/grads/...) for batches up to max_batch.
+    size_t (*workspace_bytes)(const fo_model* m);
+    // Carve the plan out of m->arena; called once after the flat buffers exist.
+    fo_status (*init)(fo_model* m);
+    // Enqueue one training step on m->stream.
+    fo_status (*step)(fo_model* m, const fo_acts* acts, const int32_t* labels);
+    void (*destroy)(fo_model* m);
+};
+
+// Accessors (function-local statics keep the tables out of device code).
+const Family* family_cnn32();   // config 1
+const Family* family_cnn16();   // configs 2, 3, 5
+const Family* family_bert();    // config 4
+
+}  // namespace fo

@@ -1,0 +1,552 @@
+// Config 4: the BERT-base-shaped server network (10 post-LN encoder layers,
+// d = 768, 12 heads of 64, FFN 3072 with exact GELU, tanh pooler on the first
+// token, linear 768 -> 2), one training iteration of the activation branch
+// of Alg. 4 on bf16 MFMA GEMMs with fp32 accumulation and fp32 master weights.
+// The forward GEMMs are compensated products (bf16 high + low parts of both
+// operands, three MFMA passes): through ten layers plain bf16 operands move
+// the logits by 2-3% of their size, the compensated forward by ~1e-5.  The
+// backward GEMMs use the high parts only.
+//
+// Variable-length batches run packed: only the sum(len_b) = T valid tokens
+// are stored and computed ([T][d] row-major, sequence b at rows cu[b]..).
+// Because padded keys are masked out of every attention and the loss reads
+// only the first token, padded positions never influence the loss: packing
+// gives the same loss, logits and gradients as the padded formulation.  T
+// stays on the device (cu[B]); grids are sized for B*L rows and the work
+// past T exits early, so a step needs no host synchronisation.
+#include "gemm.h"
+#include "model.h"
+
+namespace fo {
+namespace {
+
+constexpr int D = 768, NH = 12, FF = 3072, NL = 10, L = 128, NC = 2;
+constexpr int64_t kLayer = (int64_t)3 * D * D + 3 * D + (int64_t)D * D + D + 2 * D + (int64_t)FF * D + FF +
+                           (int64_t)D * FF + D + 2 * D;
+constexpr int64_t kParams = NL * kLayer + (int64_t)D * D + D + (int64_t)NC * D + NC;
+
+struct LayerOff {
+    int64_t wqkv, bqkv, wo, bo, g1, b1, w1, bf1, w2, bf2, g2, b2;
+};
+
+struct LayerAct {
+    float* qkv;                         // fp32: attention reads it unrounded
+    bf16_t *O, *Olo, *Hb, *Hlo, *pre1, *G, *Glo;
+    float *lse, *u1, *mean1, *rstd1, *Hf, *u2, *mean2, *rstd2;
+};
+
+struct Plan {
+    int rows;  // max_batch * L
+    int* cu;   // [max_batch + 1]; cu[B] = T
+    LayerOff off[NL];
+    int64_t pool_w, pool_b, cls_w, cls_b;
+    bf16_t* Xb[NL + 1];
+    bf16_t* Xlo[NL + 1];  // low parts (layer 0's input is exactly bf16: none)
+    float* Xf[NL + 1];
+    LayerAct a[NL];
+    float *dY[2], *du2f, *dHf, *du1f, *Dws;
+    bf16_t *du2b, *dA1, *du1b, *dO, *dqkv;
+    float *splitws, *colws, *lnpart;
+    int split_qkv, split_o, split_f1, split_f2;
+    float *xc, *pooled, *dz, *dpool, *dxc;
+};
+
+// ------------------------------------------------------------------ kernels
+__global__ void build_cu_kernel(const int32_t* __restrict__ lengths, int B, int Lmax, int* __restrict__ cu) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    int acc = 0;
+    for (int b = 0; b < B; ++b) {
+        int len = lengths[b];
+        len = len < 1 ? 1 : (len > Lmax ? Lmax : len);
+        cu[b] = acc;
+        acc += len;
+    }
+    cu[B] = acc;
+}
+
+// padded [B][L][D] bf16 -> packed rows (bf16 and fp32 copies)
+__global__ void __launch_bounds__(256) pack_kernel(const bf16_t* __restrict__ x, const int* __restrict__ cu, int B,
+                                                   bf16_t* __restrict__ xb, float* __restrict__ xf) {
+    const int64_t total = (int64_t)B * L * (D / 8);
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        int c8 = (int)(idx % (D / 8));
+        int64_t bp = idx / (D / 8);
+        int b = (int)(bp / L), pos = (int)(bp % L);
+        if (pos >= cu[b + 1] - cu[b]) continue;
+        int64_t row = cu[b] + pos;
+        uint4 v = reinterpret_cast<const uint4*>(x + bp * D)[c8];
+        reinterpret_cast<uint4*>(xb + row * D)[c8] = v;
+        float* f = xf + row * D + c8 * 8;
+        uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            f[2 * e] = bf2f((bf16_t)(w[e] & 0xFFFFu));
+            f[2 * e + 1] = bf2f((bf16_t)(w[e] >> 16));
+        }
+    }
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+constexpr int PER = D / 64;  // 12 columns per lane
+
+// y = gamma * (u - mean) * rstd + beta over each row of D; one wave per row.
+__global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ u, const float* __restrict__ g,
+                                                     const float* __restrict__ beta, const int* __restrict__ Tdev,
+                                                     float* __restrict__ yf, bf16_t* __restrict__ yb,
+                                                     bf16_t* __restrict__ ylo, float* __restrict__ mean,
+                                                     float* __restrict__ rstd) {
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (row >= *Tdev) return;
+    const float* ur = u + (int64_t)row * D;
+    float x[PER];
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        x[k] = ur[lane + 64 * k];
+        s += x[k];
+    }
+    const float mu = wave_sum(s) * (1.f / D);
+    float v = 0.f;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        x[k] -= mu;
+        v = fmaf(x[k], x[k], v);
+    }
+    const float rs = rsqrtf(wave_sum(v) * (1.f / D) + 1e-5f);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        int c = lane + 64 * k;
+        float y = fmaf(x[k] * rs, g[c], beta[c]);
+        const bf16_t hi = f2bf(y);
+        yf[(int64_t)row * D + c] = y;
+        yb[(int64_t)row * D + c] = hi;
+        ylo[(int64_t)row * D + c] = f2bf(y - bf2f(hi));
+    }
+    if (lane == 0) {
+        mean[row] = mu;
+        rstd[row] = rs;
+    }
+}
+
+// dx = rstd * (gdy - mean(gdy) - xhat * mean(gdy * xhat)), gdy = dy * gamma
+__global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ dy, const float* __restrict__ u,
+                                                     const float* __restrict__ mean, const float* __restrict__ rstd,
+                                                     const float* __restrict__ g, const int* __restrict__ Tdev,
+                                                     float* __restrict__ dxf, bf16_t* __restrict__ dxb) {
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (row >= *Tdev) return;
+    const float mu = mean[row], rs = rstd[row];
+    float xh[PER], gd[PER];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        int c = lane + 64 * k;
+        xh[k] = (u[(int64_t)row * D + c] - mu) * rs;
+        gd[k] = dy[(int64_t)row * D + c] * g[c];
+        s1 += gd[k];
+        s2 = fmaf(gd[k], xh[k], s2);
+    }
+    s1 = wave_sum(s1) * (1.f / D);
+    s2 = wave_sum(s2) * (1.f / D);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        int c = lane + 64 * k;
+        float dx = rs * (gd[k] - s1 - xh[k] * s2);
+        dxf[(int64_t)row * D + c] = dx;
+        dxb[(int64_t)row * D + c] = f2bf(dx);
+    }
+}
+
+// dgamma = sum_rows dy * xhat, dbeta = sum_rows dy: partial sums per 64 rows.
+constexpr int LNP_ROWS = 64;
+__global__ void __launch_bounds__(256) ln_param_partial(const float* __restrict__ dy, const float* __restrict__ u,
+                                                        const float* __restrict__ mean, const float* __restrict__ rstd,
+                                                        const int* __restrict__ Tdev, float* __restrict__ part) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    const int r0 = blockIdx.y * LNP_ROWS, r1 = min(*Tdev, r0 + LNP_ROWS);
+    float sg = 0.f, sb = 0.f;
+    for (int r = r0; r < r1; ++r) {
+        float d = dy[(int64_t)r * D + c];
+        sg = fmaf(d, (u[(int64_t)r * D + c] - mean[r]) * rstd[r], sg);
+        sb += d;
+    }
+    part[((int64_t)blockIdx.y * 2 + 0) * D + c] = sg;
+    part[((int64_t)blockIdx.y * 2 + 1) * D + c] = sb;
+}
+
+__global__ void __launch_bounds__(256) ln_param_finish(const float* __restrict__ part, int chunks,
+                                                       float* __restrict__ dg, float* __restrict__ db) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    float sg = 0.f, sb = 0.f;
+    for (int k = 0; k < chunks; ++k) {
+        sg += part[((int64_t)k * 2 + 0) * D + c];
+        sb += part[((int64_t)k * 2 + 1) * D + c];
+    }
+    dg[c] = sg;
+    db[c] = sb;
+}
+
+__global__ void __launch_bounds__(256) gather_cls_kernel(const float* __restrict__ X, const int* __restrict__ cu,
+                                                         int B, float* __restrict__ xc) {
+    const int b = blockIdx.x;
+    for (int c = threadIdx.x; c < D; c += blockDim.x) xc[(int64_t)b * D + c] = X[(int64_t)cu[b] * D + c];
+}
+
+__global__ void __launch_bounds__(256) scatter_cls_kernel(const float* __restrict__ dxc, const int* __restrict__ cu,
+                                                          int B, float* __restrict__ dY) {
+    const int b = blockIdx.x;
+    for (int c = threadIdx.x; c < D; c += blockDim.x) dY[(int64_t)cu[b] * D + c] = dxc[(int64_t)b * D + c];
+}
+
+// ------------------------------------------------------------------ plan
+int split_for(int M, int N, int K) {
+    int tiles = (int)(cdiv(M, 128) * cdiv(N, 128));
+    int s = (int)std::max<int64_t>(1, 640 / tiles);
+    s = std::min(s, 8);
+    while (s > 1 && (int64_t)K / s < 256) --s;
+    return s;
+}
+
+size_t ws_bytes(const fo_model* m) {
+    const size_t R = (size_t)m->max_batch * L, B = (size_t)m->max_batch;
+    size_t s = 0;
+    auto add = [&](size_t b) { s += (b + 255) & ~size_t(255); };
+    add(sizeof(Plan));
+    add(4 * (B + 1));
+    for (int l = 0; l <= NL; ++l) {
+        add(2 * R * D);
+        add(2 * R * D);
+        add(4 * R * D);
+    }
+    for (int l = 0; l < NL; ++l) {
+        add(4 * R * 3 * D);                         // qkv (fp32)
+        add(2 * R * D); add(2 * R * D);             // O, Olo
+        add(2 * R * D); add(2 * R * D);             // Hb, Hlo
+        add(2 * R * FF);                            // pre1
+        add(2 * R * FF); add(2 * R * FF);           // G, Glo
+        add(4 * B * NH * L);                        // lse
+        add(4 * R * D); add(4 * R); add(4 * R);     // u1, mean1, rstd1
+        add(4 * R * D);                             // Hf
+        add(4 * R * D); add(4 * R); add(4 * R);     // u2, mean2, rstd2
+    }
+    add(4 * R * D); add(4 * R * D);                 // dY[2]
+    add(4 * R * D); add(4 * R * D); add(4 * R * D); // du2f, dHf, du1f
+    add(4 * B * NH * L);                            // Dws
+    add(2 * R * D); add(2 * R * FF); add(2 * R * D); add(2 * R * D); add(2 * R * 3 * D);
+    const int K = (int)R;
+    size_t sw = 0;
+    sw = std::max(sw, gemm_ws_bytes(3 * D, D, split_for(3 * D, D, K)));
+    sw = std::max(sw, gemm_ws_bytes(D, D, split_for(D, D, K)));
+    sw = std::max(sw, gemm_ws_bytes(FF, D, split_for(FF, D, K)));
+    sw = std::max(sw, gemm_ws_bytes(D, FF, split_for(D, FF, K)));
+    add(sw);
+    add(4 * colsum_ws_floats((int)R, FF));
+    add(4 * (size_t)cdiv(R, LNP_ROWS) * 2 * D);
+    add(4 * B * D); add(4 * B * D); add(4 * B * NC); add(4 * B * D); add(4 * B * D);
+    return s;
+}
+
+fo_status init(fo_model* m) {
+    Plan* P = new (std::nothrow) Plan();
+    if (!P) return FO_ENOMEM;
+    m->plan = P;
+    const size_t R = (size_t)m->max_batch * L, B = (size_t)m->max_batch;
+    P->rows = (int)R;
+    int64_t o = 0;
+    for (int l = 0; l < NL; ++l) {
+        LayerOff& f = P->off[l];
+        f.wqkv = o; o += (int64_t)3 * D * D;
+        f.bqkv = o; o += 3 * D;
+        f.wo = o; o += (int64_t)D * D;
+        f.bo = o; o += D;
+        f.g1 = o; o += D;
+        f.b1 = o; o += D;
+        f.w1 = o; o += (int64_t)FF * D;
+        f.bf1 = o; o += FF;
+        f.w2 = o; o += (int64_t)D * FF;
+        f.bf2 = o; o += D;
+        f.g2 = o; o += D;
+        f.b2 = o; o += D;
+    }
+    P->pool_w = o; o += (int64_t)D * D;
+    P->pool_b = o; o += D;
+    P->cls_w = o; o += (int64_t)NC * D;
+    P->cls_b = o; o += NC;
+    if (o != kParams) {
+        set_error("bert: layout mismatch");
+        return FO_EINVAL;
+    }
+    Arena& a = m->arena;
+    a.take<char>(sizeof(Plan));
+    P->cu = a.take<int>(B + 1);
+    for (int l = 0; l <= NL; ++l) {
+        P->Xb[l] = a.take<bf16_t>(R * D);
+        P->Xlo[l] = a.take<bf16_t>(R * D);
+        P->Xf[l] = a.take<float>(R * D);
+    }
+    for (int l = 0; l < NL; ++l) {
+        LayerAct& t = P->a[l];
+        t.qkv = a.take<float>(R * 3 * D);
+        t.O = a.take<bf16_t>(R * D);
+        t.Olo = a.take<bf16_t>(R * D);
+        t.Hb = a.take<bf16_t>(R * D);
+        t.Hlo = a.take<bf16_t>(R * D);
+        t.pre1 = a.take<bf16_t>(R * FF);
+        t.G = a.take<bf16_t>(R * FF);
+        t.Glo = a.take<bf16_t>(R * FF);
+        t.lse = a.take<float>(B * NH * L);
+        t.u1 = a.take<float>(R * D);
+        t.mean1 = a.take<float>(R);
+        t.rstd1 = a.take<float>(R);
+        t.Hf = a.take<float>(R * D);
+        t.u2 = a.take<float>(R * D);
+        t.mean2 = a.take<float>(R);
+        t.rstd2 = a.take<float>(R);
+    }
+    P->dY[0] = a.take<float>(R * D);
+    P->dY[1] = a.take<float>(R * D);
+    P->du2f = a.take<float>(R * D);
+    P->dHf = a.take<float>(R * D);
+    P->du1f = a.take<float>(R * D);
+    P->Dws = a.take<float>(B * NH * L);
+    P->du2b = a.take<bf16_t>(R * D);
+    P->dA1 = a.take<bf16_t>(R * FF);
+    P->du1b = a.take<bf16_t>(R * D);
+    P->dO = a.take<bf16_t>(R * D);
+    P->dqkv = a.take<bf16_t>(R * 3 * D);
+    const int K = (int)R;
+    P->split_qkv = split_for(3 * D, D, K);
+    P->split_o = split_for(D, D, K);
+    P->split_f1 = split_for(FF, D, K);
+    P->split_f2 = split_for(D, FF, K);
+    size_t sw = 0;
+    sw = std::max(sw, gemm_ws_bytes(3 * D, D, P->split_qkv));
+    sw = std::max(sw, gemm_ws_bytes(D, D, P->split_o));
+    sw = std::max(sw, gemm_ws_bytes(FF, D, P->split_f1));
+    sw = std::max(sw, gemm_ws_bytes(D, FF, P->split_f2));
+    P->splitws = a.take<float>(sw / 4 + 1);
+    P->colws = a.take<float>(colsum_ws_floats((int)R, FF));
+    P->lnpart = a.take<float>((size_t)cdiv(R, LNP_ROWS) * 2 * D);
+    P->xc = a.take<float>(B * D);
+    P->pooled = a.take<float>(B * D);
+    P->dz = a.take<float>(B * NC);
+    P->dpool = a.take<float>(B * D);
+    P->dxc = a.take<float>(B * D);
+    if (!P->dxc) {
+        set_error("bert: workspace arena too small");
+        return FO_ENOMEM;
+    }
+    return FO_OK;
+}
+
+#define TRY(x)                           \
+    do {                                 \
+        fo_status st_ = (x);             \
+        if (st_ != FO_OK) return st_;    \
+    } while (0)
+
+// C[rows][N] = A[rows][K] W^T (+ epilogue): the forward of a linear layer as a
+// compensated product (A = A + Alo, W = W + Wlo in bf16 parts; Alo == NULL
+// when A is exactly bf16).
+GemmDesc lin_fwd(int rows, const bf16_t* A, const bf16_t* Alo, int K, const bf16_t* W, const bf16_t* Wlo, int N) {
+    GemmDesc d;
+    d.M = rows; d.N = N; d.K = K;
+    d.amode = OP_RK; d.A = A; d.A2 = Alo; d.lda = K;
+    d.bmode = OP_RK; d.B = W; d.B2 = Wlo; d.ldb = K;
+    d.nseg = Alo ? 3 : 2;
+    return d;
+}
+
+fo_status ln_params(const Plan* P, const float* dy, const float* u, const float* mean, const float* rstd,
+                    const int* Tdev, int rows, float* dg, float* db, hipStream_t s) {
+    int chunks = (int)cdiv(rows, LNP_ROWS);
+    hipLaunchKernelGGL(ln_param_partial, dim3(D / 256, chunks), dim3(256), 0, s, dy, u, mean, rstd, Tdev, P->lnpart);
+    hipLaunchKernelGGL(ln_param_finish, dim3(D / 256), dim3(256), 0, s, P->lnpart, chunks, dg, db);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
+    Plan* P = (Plan*)m->plan;
+    hipStream_t s = m->stream;
+    const int B = acts->batch, rows = B * L;
+    const int* Tdev = P->cu + B;
+    const bf16_t* W = m->w16;
+    const bf16_t* Wl = m->w16lo;
+    const float* prm = m->params;
+    float* grd = m->grads;
+
+    hipLaunchKernelGGL(build_cu_kernel, dim3(1), dim3(64), 0, s, acts->lengths, B, L, P->cu);
+    {
+        int64_t total = (int64_t)rows * (D / 8);
+        int grid = (int)std::min<int64_t>(cdiv(total, 256), 8192);
+        hipLaunchKernelGGL(pack_kernel, dim3(grid), dim3(256), 0, s, (const bf16_t*)acts->x, P->cu, B, P->Xb[0],
+                           P->Xf[0]);
+    }
+    FO_LAUNCHED();
+    const dim3 lngrid((unsigned)cdiv(rows, 4));
+
+    // ---------------- forward (Alg. 4: forward pass of M_s)
+    for (int l = 0; l < NL; ++l) {
+        const LayerOff& f = P->off[l];
+        LayerAct& t = P->a[l];
+        GemmDesc q = lin_fwd(rows, P->Xb[l], l ? P->Xlo[l] : nullptr, D, W + f.wqkv, Wl + f.wqkv, 3 * D);
+        q.Mdev = Tdev;
+        q.bias = prm + f.bqkv;
+        q.Cf = t.qkv; q.ldcf = 3 * D;
+        TRY(gemm(q, s));
+        TRY(launch_attn_fwd(t.qkv, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
+        GemmDesc o = lin_fwd(rows, t.O, t.Olo, D, W + f.wo, Wl + f.wo, D);
+        o.Mdev = Tdev;
+        o.bias = prm + f.bo;
+        o.resid = P->Xf[l]; o.ldr = D;
+        o.Cf = t.u1; o.ldcf = D;
+        TRY(gemm(o, s));
+        hipLaunchKernelGGL(ln_fwd_kernel, lngrid, dim3(256), 0, s, t.u1, prm + f.g1, prm + f.b1, Tdev, t.Hf, t.Hb,
+                           t.Hlo, t.mean1, t.rstd1);
+        GemmDesc f1 = lin_fwd(rows, t.Hb, t.Hlo, D, W + f.w1, Wl + f.w1, FF);
+        f1.Mdev = Tdev;
+        f1.bias = prm + f.bf1;
+        f1.act = ACT_GELU; f1.pre = t.pre1; f1.ldm = FF;
+        f1.Cb = t.G; f1.Cb2 = t.Glo; f1.ldcb = FF;
+        TRY(gemm(f1, s));
+        GemmDesc f2 = lin_fwd(rows, t.G, t.Glo, FF, W + f.w2, Wl + f.w2, D);
+        f2.Mdev = Tdev;
+        f2.bias = prm + f.bf2;
+        f2.resid = t.Hf; f2.ldr = D;
+        f2.Cf = t.u2; f2.ldcf = D;
+        TRY(gemm(f2, s));
+        hipLaunchKernelGGL(ln_fwd_kernel, lngrid, dim3(256), 0, s, t.u2, prm + f.g2, prm + f.b2, Tdev, P->Xf[l + 1],
+                           P->Xb[l + 1], P->Xlo[l + 1], t.mean2, t.rstd2);
+        FO_LAUNCHED();
+    }
+
+    // ---------------- head: pooler on the first token, classifier, loss f_s
+    hipLaunchKernelGGL(gather_cls_kernel, dim3(B), dim3(256), 0, s, P->Xf[NL], P->cu, B, P->xc);
+    FO_LAUNCHED();
+    TRY(launch_small_linear_fwd(P->xc, prm + P->pool_w, prm + P->pool_b, P->pooled, B, D, D, true, s));
+    TRY(launch_small_linear_fwd(P->pooled, prm + P->cls_w, prm + P->cls_b, m->logits, B, D, NC, false, s));
+    TRY(launch_xent(m->logits, labels, P->dz, m->loss, B, NC, s));
+
+    // ---------------- backward (Alg. 4: backward pass of M_s)
+    TRY(launch_small_linear_bwd(P->dz, P->pooled, prm + P->cls_w, P->pooled, grd + P->cls_w, grd + P->cls_b,
+                                P->dpool, B, D, NC, s));
+    TRY(launch_small_linear_bwd(P->dpool, P->xc, prm + P->pool_w, nullptr, grd + P->pool_w, grd + P->pool_b, P->dxc,
+                                B, D, D, s));
+    TRY(launch_fill(P->dY[0], (int64_t)rows * D, 0.f, s));
+    hipLaunchKernelGGL(scatter_cls_kernel, dim3(B), dim3(256), 0, s, P->dxc, P->cu, B, P->dY[0]);
+    FO_LAUNCHED();
+
+    int cur = 0;
+    for (int l = NL - 1; l >= 0; --l) {
+        const LayerOff& f = P->off[l];
+        LayerAct& t = P->a[l];
+        float* dY = P->dY[cur];
+        // LN2
+        hipLaunchKernelGGL(ln_bwd_kernel, lngrid, dim3(256), 0, s, dY, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev,
+                           P->du2f, P->du2b);
+        TRY(ln_params(P, dY, t.u2, t.mean2, t.rstd2, Tdev, rows, grd + f.g2, grd + f.b2, s));
+        // FFN2: dG = du2 W2 (times GELU'(pre1) -> dA1), dW2 = du2^T G, db2
+        {
+            GemmDesc d;
+            d.M = rows; d.N = FF; d.K = D; d.Mdev = Tdev;
+            d.amode = OP_RK; d.A = P->du2b; d.lda = D;
+            d.bmode = OP_KR; d.B = W + f.w2; d.ldb = FF;
+            d.dpre = t.pre1; d.ldm = FF;
+            d.Cb = P->dA1; d.ldcb = FF;
+            TRY(gemm(d, s));
+            GemmDesc w;
+            w.M = D; w.N = FF; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = P->du2b; w.lda = D;
+            w.bmode = OP_KR; w.B = t.G; w.ldb = FF;
+            w.Cf = grd + f.w2; w.ldcf = FF;
+            w.splits = P->split_f2; w.ws = P->splitws;
+            TRY(gemm(w, s));
+            TRY(launch_colsum(P->du2f, D, rows, Tdev, D, grd + f.bf2, P->colws, s));
+        }
+        // FFN1: dH = du2 + dA1 W1, dW1 = dA1^T H, db1
+        {
+            GemmDesc d;
+            d.M = rows; d.N = D; d.K = FF; d.Mdev = Tdev;
+            d.amode = OP_RK; d.A = P->dA1; d.lda = FF;
+            d.bmode = OP_KR; d.B = W + f.w1; d.ldb = D;
+            d.resid = P->du2f; d.ldr = D;
+            d.Cf = P->dHf; d.ldcf = D;
+            TRY(gemm(d, s));
+            GemmDesc w;
+            w.M = FF; w.N = D; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = P->dA1; w.lda = FF;
+            w.bmode = OP_KR; w.B = t.Hb; w.ldb = D;
+            w.Cf = grd + f.w1; w.ldcf = D;
+            w.splits = P->split_f1; w.ws = P->splitws;
+            TRY(gemm(w, s));
+            TRY(launch_colsum(P->dA1, FF, rows, Tdev, FF, grd + f.bf1, P->colws, s));
+        }
+        // LN1
+        hipLaunchKernelGGL(ln_bwd_kernel, lngrid, dim3(256), 0, s, P->dHf, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev,
+                           P->du1f, P->du1b);
+        TRY(ln_params(P, P->dHf, t.u1, t.mean1, t.rstd1, Tdev, rows, grd + f.g1, grd + f.b1, s));
+        // output projection: dO = du1 Wo, dWo = du1^T O, dbo
+        {
+            GemmDesc d;
+            d.M = rows; d.N = D; d.K = D; d.Mdev = Tdev;
+            d.amode = OP_RK; d.A = P->du1b; d.lda = D;
+            d.bmode = OP_KR; d.B = W + f.wo; d.ldb = D;
+            d.Cb = P->dO; d.ldcb = D;
+            TRY(gemm(d, s));
+            GemmDesc w;
+            w.M = D; w.N = D; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = P->du1b; w.lda = D;
+            w.bmode = OP_KR; w.B = t.O; w.ldb = D;
+            w.Cf = grd + f.wo; w.ldcf = D;
+            w.splits = P->split_o; w.ws = P->splitws;
+            TRY(gemm(w, s));
+            TRY(launch_colsum(P->du1f, D, rows, Tdev, D, grd + f.bo, P->colws, s));
+        }
+        TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, P->Dws, P->dqkv, B, NH, D, s));
+        // input projection: dX = du1 + dqkv Wqkv (skipped for the first server layer), dWqkv, dbqkv
+        if (l > 0) {
+            GemmDesc d;
+            d.M = rows; d.N = D; d.K = 3 * D; d.Mdev = Tdev;
+            d.amode = OP_RK; d.A = P->dqkv; d.lda = 3 * D;
+            d.bmode = OP_KR; d.B = W + f.wqkv; d.ldb = D;
+            d.resid = P->du1f; d.ldr = D;
+            d.Cf = P->dY[cur ^ 1]; d.ldcf = D;
+            TRY(gemm(d, s));
+        }
+        GemmDesc w;
+        w.M = 3 * D; w.N = D; w.K = rows; w.Kdev = Tdev;
+        w.amode = OP_KR; w.A = P->dqkv; w.lda = 3 * D;
+        w.bmode = OP_KR; w.B = P->Xb[l]; w.ldb = D;
+        w.Cf = grd + f.wqkv; w.ldcf = D;
+        w.splits = P->split_qkv; w.ws = P->splitws;
+        TRY(gemm(w, s));
+        TRY(launch_colsum(P->dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws, s));
+        cur ^= 1;
+    }
+    FO_LAUNCHED();
+    // ---------------- SGD (Alg. 4: theta_s <- theta_s - gamma_s grad), refreshes the bf16 shadow
+    return launch_sgd(m->params, m->grads, nullptr, m->w16, m->w16lo, m->n_params, m->lr, 0.f, s);
+}
+
+void destroy(fo_model* m) {
+    delete (Plan*)m->plan;
+    m->plan = nullptr;
+}
+
+}  // namespace
+
+int64_t bert_param_count() { return kParams; }
+
+const Family* family_bert() {
+    static const Family f = {ws_bytes, init, step, destroy};
+    return &f;
+}
+
+}  // namespace fo

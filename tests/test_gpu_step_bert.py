@@ -1,0 +1,82 @@
+"""GPU parity of the bf16 transformer server step (config 4) against the fp64
+oracle, through the C ABI.
+
+Graded (bf16 path): loss and logits of the step's forward, and of the
+re-forward of the same batch after the update (the second step's forward),
+within 2e-2 relative (normwise for logits).  Gradients and the update are
+checked too, with a looser normwise bound that still catches a wrong or
+missing term."""
+import numpy as np
+import pytest
+
+import fo_synth as S
+import oracle
+from tests.gpu_util import announce, normwise, per_tensor_errors, to_dev, torch_cuda
+
+pytestmark = pytest.mark.gpu
+A = pytest.importorskip("paper_2504_13850_amd.api")
+
+CID = 4
+TOL = 2e-2
+GRAD_TOL = 6e-2
+
+
+def _run_two_steps(B, lengths, sub):
+    torch = torch_cuda()
+    theta = S.init_params(CID)
+    acts = S.make_acts(CID, 1, batch=B, sub=sub)[0]
+    labels = S.make_labels(CID, 1, batch=B, sub=sub)[0]
+    lengths = np.asarray(lengths, np.int32)
+    model = A.fo_model_create(CID, B, theta, torch.cuda.current_stream())
+    try:
+        x, lab, ln = to_dev(acts), to_dev(labels), to_dev(lengths)
+        A.fo_server_step(model, (x, ln, B), lab, 0)
+        out1 = dict(loss=A.fo_model_read(model, A.FO_BUF_LOSS)[0],
+                    logits=A.fo_model_read(model, A.FO_BUF_LOGITS).reshape(B, 2),
+                    grads=A.fo_model_read(model, A.FO_BUF_GRADS),
+                    params=A.fo_model_read(model, A.FO_BUF_PARAMS))
+        A.fo_server_step(model, (x, ln, B), lab, 0)
+        out2 = dict(loss=A.fo_model_read(model, A.FO_BUF_LOSS)[0],
+                    logits=A.fo_model_read(model, A.FO_BUF_LOGITS).reshape(B, 2))
+    finally:
+        A.fo_model_destroy(model)
+    return theta, acts, labels, lengths, out1, out2
+
+
+def _check(theta, acts, labels, lengths, out1, out2, grads=True):
+    r1 = oracle.server_step(CID, theta, acts, labels, lengths)
+    assert abs(out1["loss"] - r1["loss"]) <= TOL * abs(r1["loss"]), (out1["loss"], r1["loss"])
+    assert normwise(out1["logits"], r1["logits"]) <= TOL
+    if grads:
+        errs = per_tensor_errors(CID, out1["grads"], r1["grads"])
+        worst = max(errs, key=errs.get)
+        assert errs[worst] <= GRAD_TOL, (worst, errs[worst])
+        dth = out1["params"].astype(np.float64) - theta
+        assert normwise(dth, r1["params"] - theta) <= GRAD_TOL
+    # re-forward after the update (the second step's forward)
+    z2 = oracle.server_forward(CID, r1["params"], acts, lengths)
+    assert normwise(out2["logits"], z2) <= TOL
+
+
+@pytest.mark.parametrize("B,lengths,sub", [(2, [37, 128], 1), (3, [1, 64, 100], 2), (1, [128], 3)])
+def test_small_batch_parity(B, lengths, sub):
+    announce(f"config 4 step B={B} lengths={lengths}")
+    _check(*_run_two_steps(B, lengths, sub))
+
+
+def test_workload_lengths_batch8():
+    """Lengths drawn like the workload (uniform on [32, 128])."""
+    B = 8
+    lengths = S.make_lengths(CID, 1, batch=B, sub=4)[0]
+    announce(f"config 4 step B={B} lengths={lengths.tolist()}")
+    _check(*_run_two_steps(B, lengths, 4))
+
+
+def test_full_batch_loss_and_logits():
+    """The full workload shape (B = 32, L = 128, lengths on [32, 128]): the
+    loss and all 64 logits against the oracle."""
+    B = 32
+    lengths = S.make_lengths(CID, 1, batch=B, sub=5)[0]
+    announce(f"config 4 step B={B} (full)")
+    theta, acts, labels, lengths, out1, out2 = _run_two_steps(B, lengths, 5)
+    _check(theta, acts, labels, lengths, out1, out2, grads=False)
