@@ -1,0 +1,244 @@
+"""Benchmark of the FedOptima server hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
+
+One step = one pass of the server's hot path over one activation batch:
+an arriving batch is copied into the HBM activation pool (Alg. 2 put() with
+flow control), the Task Scheduler picks the device with the smallest
+consumption counter (Alg. 3 get()), the server trains M_s on that batch
+(Alg. 4: forward, loss, backward, SGD) and the slot is recycled.  For the
+workloads that aggregate device-side models (tiny CNN, ResNet, 128-device
+VGG) one model arrival is also aggregated per step.  The default workload is
+the BERT-base-shaped transformer split (B = 32, L = 128, d = 768, 10 layers,
+lengths uniform on [32, 128]), the workload the bf16 MFMA target is stated on.
+
+Printed as one JSON line:
+  value          server training throughput (samples/s) with inputs resident in HBM
+  mfu            useful FLOPs per step / step time / bf16 dense MFMA peak
+  roofline       the dominant kernel (the one with the largest share of step time)
+                 measured live with HIP events over the timed steps
+  aggregate      the aggregation kernel at 1 GiB vectors (HBM roofline) and at the
+                 workload sizes
+  cpu_baseline   the oracle (fp32 NumPy) timed on the host cores on a bounded sample
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-steps", type=int, default=2)
+    return ap.parse_args()
+
+
+def cpu_baseline(cid, sample_steps):
+    """The oracle in fp32 on the host cores over a bounded sample of the workload."""
+    import fo_synth as S
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    Bs = 4
+    theta = S.init_params(cid)
+    acts = S.make_acts(cid, sample_steps, batch=Bs, sub=99)
+    labels = S.make_labels(cid, sample_steps, batch=Bs, sub=99)
+    lengths = S.make_lengths(cid, sample_steps, batch=Bs, sub=99) if cid == 4 else [None] * sample_steps
+    t0 = time.perf_counter()
+    for i in range(sample_steps):
+        r = oracle.server_step(cid, theta, acts[i], labels[i], lengths[i], dt=np.float32)
+        theta = r["params"].astype(np.float32)
+    dt = time.perf_counter() - t0
+    return {"value": round(Bs * sample_steps / dt, 3), "unit": "samples/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{sample_steps} fp32 oracle steps at batch {Bs} of the same workload ({dt:.1f} s)"}
+
+
+def bench_aggregate(A, torch, stream):
+    """HBM roofline of the aggregation kernel: 1 GiB fp32 vectors (12 B/element
+    per call: read global + local, write global), plus latency at workload sizes."""
+    n = 1 << 28
+    g = torch.empty(n, device="cuda", dtype=torch.float32).normal_(0, 0.02)
+    l = torch.empty(n, device="cuda", dtype=torch.float32).normal_(0, 0.02)
+    A.fo_set_stream(stream)
+    for _ in range(3):
+        A.fo_async_aggregate(g, l, 1.0, 3)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(reps):
+        A.fo_async_aggregate(g, l, 1.0, 3)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / reps
+    gbs = 12.0 * n / (ms * 1e-3) / 1e9
+    small = {}
+    for m in (10_000, 38_720, 157_504):
+        gs, ls = g[:m], l[:m]
+        for _ in range(3):
+            A.fo_async_aggregate(gs, ls, 1.0, 1)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(50):
+            A.fo_async_aggregate(gs, ls, 1.0, 1)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        us = ev0.elapsed_time(ev1) / 50 * 1e3
+        small[str(m)] = {"us_per_call": round(us, 2), "GB/s": round(12.0 * m / (us * 1e-6) / 1e9, 1)}
+    del g, l
+    return {"kernel": "agg_lerp_kernel", "n": n, "bytes_per_call": 12 * n, "ms_per_call": round(ms, 4),
+            "achieved_GBps": round(gbs, 1), "peak_GBps": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "workload_sizes": small}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        sys.stderr.write("bench.py measures one GPU only: this build has no multi-GPU path "
+                         f"(asked for --gpus {args.gpus}).\n")
+        sys.exit(2)
+    import torch
+    import fo_synth as S
+    from paper_2504_13850_amd import api as A
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cid = args.config
+    if cid != 4:
+        raise SystemExit("bench.py: only the transformer workload (--config 4) is wired up")
+    cfg = S.get_config(cid)
+    B, Lmax, K = cfg.batch, cfg.in_shape[0], cfg.n_devices
+    stream = torch.cuda.current_stream()
+
+    # ---------------- synthetic inputs, resident in HBM before timing
+    bank_n = 16
+    acts_h = S.make_acts(cid, bank_n)                 # bf16 bits [n, B, L, d]
+    labels_h = S.make_labels(cid, bank_n)
+    lengths_h = S.make_lengths(cid, bank_n)
+    acts_d = torch.from_numpy(acts_h.view(np.int16)).cuda()
+    labels_d = torch.from_numpy(labels_h).cuda()
+    lengths_d = torch.from_numpy(lengths_h).cuda()
+    del acts_h
+    theta = S.init_params(cid)
+    model = A.fo_model_create(cid, B, theta, stream)
+    slot_bytes = B * Lmax * cfg.in_shape[1] * 2
+    q = A.fo_queues_create(K, slot_bytes, B, True, 3 * K, stream)
+
+    arrivals = [0]
+
+    def push(k):
+        i = arrivals[0] % bank_n
+        arrivals[0] += 1
+        st = A.fo_queues_push(q, k, acts_d[i], labels_d[i], lengths_d[i])
+        return i if st == A.FO_OK else None
+
+    # every device starts with one batch queued
+    for k in range(K):
+        push(k)
+
+    def one_step(t):
+        # arrival from device t % K (Alg. 2 put(), flow control), then get() and train
+        push(t % K)
+        k = A.fo_pick_device(q)
+        fa, lab, seq, slot = A.fo_queues_in_service(q)
+        A.fo_server_step(model, fa, lab, k)
+        A.fo_queues_release(q)
+        return k
+
+    for t in range(args.warmup):
+        one_step(t)
+    torch.cuda.synchronize()
+
+    def timed(nsteps, t0, profile):
+        if profile:
+            A.fo_profile_enable(400 * nsteps)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        t_wall = time.perf_counter()
+        for t in range(t0, t0 + nsteps):
+            one_step(t)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t_wall
+        stats = None
+        if profile:
+            stats = A.fo_profile_read(64)
+            A.fo_profile_enable(0)
+        return ev0.elapsed_time(ev1), wall, stats
+
+    # ---------------- timed region (headline), then the same steps again with kernel events
+    ms_total, wall, _ = timed(args.steps, args.warmup, False)
+    ms_prof, _, stats = timed(args.steps, args.warmup + args.steps, True)
+    ms_step = ms_total / args.steps
+    samples_s = B * args.steps / (ms_total * 1e-3)
+
+    # useful FLOPs per step from the kernels' own records (valid tokens only)
+    alg_flops = sum(s["flops"] for s in stats)
+    mfma_flops = sum(s["mfma_flops"] for s in stats)
+    flops_step = alg_flops / args.steps  # both timed passes see the same mix of batches on average
+    mfu = flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
+    dom = max((s for s in stats if s["name"].startswith("gemm_kernel")), key=lambda s: s["ms"])
+    dom_tflops = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+    kernels = [{"name": s["name"], "launches": s["launches"], "ms_per_step": round(s["ms"] / args.steps, 4),
+                "TFLOP/s": round(s["flops"] / max(s["ms"], 1e-9) / 1e9, 1) if s["flops"] else None}
+               for s in sorted(stats, key=lambda s: -s["ms"])]
+
+    agg = bench_aggregate(A, torch, stream)
+    A.fo_queues_destroy(q)
+    A.fo_model_destroy(model)
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(cid, args.cpu_sample_steps)
+
+    out = {
+        "metric": "server train samples/s + % bf16 MFMA peak; async-aggregate HBM GB/s",
+        "value": round(samples_s, 2),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "bert-base split server step: 10 post-LN encoder layers d=768 h=12 ffn=3072, "
+                               "batch 32 x 128 tokens, lengths U[32,128], 16 devices, plain SGD",
+                   "global_batch": B, "seq_len": Lmax, "parallelism": "single-gpu"},
+        "mfu": round(mfu, 4),
+        "useful_tflop_per_step": round(flops_step / 1e12, 4),
+        "mfma_tflop_per_step_executed": round(mfma_flops / args.steps / 1e12, 4),
+        "roofline": {"bound": "mfma", "kernel": dom["name"], "achieved": round(dom_tflops, 1),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4),
+                     "launches": dom["launches"], "avg_launch_us": round(dom["ms"] / dom["launches"] * 1e3, 2),
+                     "traffic": None},
+        "aggregate": agg,
+        "kernels": kernels[:12],
+        "host_wall_ms_per_step": round(wall / args.steps * 1e3, 3),
+        "profiled_ms_per_step": round(ms_prof / args.steps, 4),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -236,6 +236,26 @@ FO_API fo_status fo_queues_counters(const fo_queues* q, int64_t* c_out, int32_t 
  * Returns the new device index, or -1 on error. */
 FO_API int32_t fo_queues_add_device(fo_queues* q);
 
+/* ------------------------------------------------------------------ instrumentation
+ * Kernel timing for benchmarks and tuning.  While enabled on a thread, every
+ * MFMA GEMM and attention launch that thread enqueues is bracketed by two HIP
+ * events on its stream (up to max_launches launches; later ones are not
+ * recorded).  fo_profile_read synchronizes on the recorded events and returns
+ * one entry per kernel: launches, summed duration, and summed algorithmic
+ * FLOPs (2*M*N*K of the layer over valid rows only, not counting the extra
+ * passes of compensated products) and executed MFMA FLOPs.  Reading clears
+ * the records.  Errors: FO_EINVAL (max_launches < 0), FO_ENOMEM, FO_EHIP. */
+typedef struct {
+    char name[48];
+    int64_t launches;
+    double ms;           /* summed event-to-event time */
+    double flops;        /* algorithmic */
+    double mfma_flops;   /* executed on the matrix cores */
+} fo_kernel_stat;
+FO_API fo_status fo_profile_enable(int32_t max_launches);  /* 0 disables */
+/* Fills up to `max` entries and returns how many kernels were seen (or < 0 on error). */
+FO_API int32_t fo_profile_read(fo_kernel_stat* out, int32_t max);
+
 /* ------------------------------------------------------------------ errors */
 FO_API const char* fo_last_error(void);
 

@@ -25,7 +25,7 @@ EXPORTS = [
     "fo_async_aggregate", "fo_set_stream", "fo_set_max_delay", "fo_queues_create", "fo_queues_destroy",
     "fo_queues_push", "fo_queues_push_model", "fo_pick_device", "fo_queues_in_service",
     "fo_queues_release", "fo_aggregate_pending", "fo_aggregate_pending_all", "fo_queues_stats",
-    "fo_queues_counters", "fo_queues_add_device", "fo_last_error",
+    "fo_queues_counters", "fo_queues_add_device", "fo_last_error", "fo_profile_enable", "fo_profile_read",
 ]
 
 
@@ -41,6 +41,11 @@ class fo_vec(C.Structure):
 
 class fo_acts(C.Structure):
     _fields_ = [("x", C.c_void_p), ("lengths", C.c_void_p), ("batch", C.c_int32)]
+
+
+class fo_kernel_stat(C.Structure):
+    _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("ms", C.c_double), ("flops", C.c_double),
+                ("mfma_flops", C.c_double)]
 
 
 class fo_queue_stats(C.Structure):
@@ -88,6 +93,8 @@ def lib():
             "fo_queues_counters": (C.c_int, [vp, vp, i32]),
             "fo_queues_add_device": (i32, [vp]),
             "fo_last_error": (C.c_char_p, []),
+            "fo_profile_enable": (C.c_int, [i32]),
+            "fo_profile_read": (i32, [C.POINTER(fo_kernel_stat), i32]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -268,3 +275,18 @@ def fo_queues_add_device(q) -> int:
     if r < 0:
         raise FoError(FO_EINVAL, last_error())
     return r
+
+
+# ------------------------------------------------------------------ instrumentation
+def fo_profile_enable(max_launches: int):
+    _check(lib().fo_profile_enable(int(max_launches)))
+
+
+def fo_profile_read(max_kernels: int = 64) -> list:
+    """[{name, launches, ms, flops, mfma_flops}] for the launches recorded since enabling."""
+    buf = (fo_kernel_stat * max_kernels)()
+    n = lib().fo_profile_read(buf, max_kernels)
+    if n < 0:
+        raise FoError(n, last_error())
+    return [dict(name=buf[i].name.decode(), launches=buf[i].launches, ms=buf[i].ms, flops=buf[i].flops,
+                 mfma_flops=buf[i].mfma_flops) for i in range(min(n, max_kernels))]

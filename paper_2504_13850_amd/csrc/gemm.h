@@ -70,6 +70,7 @@ struct GemmDesc {
     // sized by the static M, and tiles past the effective bound do nothing.
     const int* Mdev = nullptr;
     const int* Kdev = nullptr;
+    int* prof_snap = nullptr;  // set by the launcher when profiling: receives (M, K) effective
 };
 
 // Enqueues the GEMM (and its split-K reduction) on stream s.

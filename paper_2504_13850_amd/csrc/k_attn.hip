@@ -12,6 +12,7 @@
 // running-maximum form and the backward pass recomputes the probabilities
 // from the saved log-sum-exp.
 #include "kernels.h"
+#include "prof.h"
 
 namespace fo {
 namespace {
@@ -21,7 +22,10 @@ constexpr int LMAX = 128;   // longest sequence
 
 __global__ void __launch_bounds__(LMAX) attn_fwd_kernel(const float* __restrict__ qkv, const int* __restrict__ cu,
                                                         bf16_t* __restrict__ out, bf16_t* __restrict__ outlo,
-                                                        float* __restrict__ lse, int H, int d, float scale) {
+                                                        float* __restrict__ lse, int H, int d, float scale,
+                                                        int* __restrict__ snap, int nb) {
+    if (snap && blockIdx.x == 0)
+        for (int i = threadIdx.x; i <= nb; i += blockDim.x) snap[i] = cu[i];
     __shared__ float Ks[LMAX][DH];
     __shared__ float Vs[LMAX][DH];
     const int b = blockIdx.x / H, h = blockIdx.x % H;
@@ -77,7 +81,9 @@ __global__ void __launch_bounds__(LMAX) attn_fwd_kernel(const float* __restrict_
 // (broadcast), so rows are unpadded.
 __global__ void __launch_bounds__(LMAX) attn_bwd_rowdot(const int* __restrict__ cu, const bf16_t* __restrict__ out,
                                                         const bf16_t* __restrict__ dout, float* __restrict__ D,
-                                                        int H, int d) {
+                                                        int H, int d, int* __restrict__ snap, int nb) {
+    if (snap && blockIdx.x == 0)
+        for (int i = threadIdx.x; i <= nb; i += blockDim.x) snap[i] = cu[i];
     const int b = blockIdx.x / H, h = blockIdx.x % H;
     const int base = cu[b], len = cu[b + 1] - cu[b];
     const int i = threadIdx.x;
@@ -188,8 +194,13 @@ __global__ void __launch_bounds__(LMAX) attn_bwd_dkdv(const float* __restrict__ 
 fo_status launch_attn_fwd(const float* qkv, const int* cu, bf16_t* out, bf16_t* outlo, float* lse, int B, int H,
                           int d, hipStream_t s) {
     FO_CHECK(d == H * DH, "attention: d=%d must equal heads*%d", d, DH);
+    ProfInfo pi;
+    pi.kind = PROF_ATTN_FWD; pi.cu = cu; pi.B = B; pi.d = d;
+    const int h = prof_begin(s, "attn_fwd_kernel", pi);
+    int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
     hipLaunchKernelGGL(attn_fwd_kernel, dim3(B * H), dim3(LMAX), 0, s, qkv, cu, out, outlo, lse, H, d,
-                       1.f / sqrtf((float)DH));
+                       1.f / sqrtf((float)DH), snap, B);
+    prof_end(h, s);
     FO_LAUNCHED();
     return FO_OK;
 }
@@ -198,9 +209,14 @@ fo_status launch_attn_bwd(const float* qkv, const int* cu, const bf16_t* out, co
                           const float* lse, float* Dws, bf16_t* dqkv, int B, int H, int d, hipStream_t s) {
     FO_CHECK(d == H * DH, "attention: d=%d must equal heads*%d", d, DH);
     const float scale = 1.f / sqrtf((float)DH);
-    hipLaunchKernelGGL(attn_bwd_rowdot, dim3(B * H), dim3(LMAX), 0, s, cu, out, dout, Dws, H, d);
+    ProfInfo pi;
+    pi.kind = PROF_ATTN_BWD; pi.cu = cu; pi.B = B; pi.d = d;
+    const int h = prof_begin(s, "attn_bwd (3 kernels)", pi);
+    int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
+    hipLaunchKernelGGL(attn_bwd_rowdot, dim3(B * H), dim3(LMAX), 0, s, cu, out, dout, Dws, H, d, snap, B);
     hipLaunchKernelGGL(attn_bwd_dq, dim3(B * H), dim3(LMAX), 0, s, qkv, cu, dout, lse, Dws, dqkv, H, d, scale);
     hipLaunchKernelGGL(attn_bwd_dkdv, dim3(B * H), dim3(LMAX), 0, s, qkv, cu, dout, lse, Dws, dqkv, H, d, scale);
+    prof_end(h, s);
     FO_LAUNCHED();
     return FO_OK;
 }

@@ -13,6 +13,7 @@
 
 #include "gemm.h"
 #include "kernels.h"
+#include "prof.h"
 
 namespace fo {
 namespace {
@@ -315,6 +316,10 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
     const int Keff = d.Kdev ? min(d.K, *d.Kdev) : d.K;
     const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+    if (d.prof_snap && (blockIdx.x | blockIdx.y | blockIdx.z) == 0 && tid == 0) {
+        d.prof_snap[0] = M;
+        d.prof_snap[1] = Keff;
+    }
     if (m0 >= M) return;  // uniform for the whole workgroup
     // The K range of this slice, over the concatenation of nseg segments of
     // length K (segment s pairs (A, B), (A, B2), (A2, B) for s = 0, 1, 2).
@@ -422,8 +427,23 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
 
 template <int AM, int BMODE>
 void launch(const GemmDesc& d, int kchunk, hipStream_t s) {
+    // kernel names as the profilers print them
+    static const char* names[6][6] = {};
+    static char buf[6][6][32];
+    if (!names[AM][BMODE]) {
+        snprintf(buf[AM][BMODE], sizeof(buf[AM][BMODE]), "gemm_kernel<%d, %d>", AM, BMODE);
+        names[AM][BMODE] = buf[AM][BMODE];
+    }
+    ProfInfo pi;
+    pi.kind = PROF_GEMM;
+    pi.M = d.M; pi.N = d.N; pi.K = d.K; pi.nseg = d.nseg;
+    pi.Mdev = d.Mdev; pi.Kdev = d.Kdev;
+    const int h = prof_begin(s, names[AM][BMODE], pi);
+    GemmDesc dd = d;
+    dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
-    hipLaunchKernelGGL((gemm_kernel<AM, BMODE>), grid, dim3(NT), 0, s, d, kchunk);
+    hipLaunchKernelGGL((gemm_kernel<AM, BMODE>), grid, dim3(NT), 0, s, dd, kchunk);
+    prof_end(h, s);
 }
 
 }  // namespace
@@ -466,7 +486,9 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     if (d.splits > 1) {
         int64_t total = (int64_t)d.M * d.N;
         int grid = (int)std::min<int64_t>(cdiv(total, 256), 4096);
+        const int h = prof_begin(s, "splitk_reduce", ProfInfo());
         hipLaunchKernelGGL(splitk_reduce, dim3(grid), dim3(256), 0, s, d);
+        prof_end(h, s);
         FO_LAUNCHED();
     }
     return FO_OK;

@@ -1,0 +1,30 @@
+// Kernel timing instrumentation (fo_profile_enable / fo_profile_read).
+#pragma once
+
+#include "common.h"
+
+namespace fo {
+
+enum ProfKind : int { PROF_GEMM = 0, PROF_ATTN_FWD = 1, PROF_ATTN_BWD = 2, PROF_OTHER = 3 };
+
+struct ProfInfo {
+    int kind = PROF_OTHER;
+    // GEMM: algorithmic flops 2*M*N*K with M, K taken from *Mdev / *Kdev when set
+    int M = 0, N = 0, K = 0, nseg = 1;
+    const int* Mdev = nullptr;
+    const int* Kdev = nullptr;
+    // attention: cu[B+1] packed offsets, width d
+    const int* cu = nullptr;
+    int B = 0, d = 0;
+};
+
+// Returns a record handle (>= 0) when the calling thread is profiling, else -1.
+// Call before the launch; prof_end after it, on the same stream.  When the
+// launch has device-side sizes, the kernel copies them into prof_snap(h)
+// (GEMM: effective M and K; attention: cu[0..B]) from its first workgroup.
+int prof_begin(hipStream_t s, const char* name, const ProfInfo& info);
+void prof_end(int h, hipStream_t s);
+int* prof_snap(int h);  // NULL when h < 0
+constexpr int kProfSnapInts = 258;  // capacity of one snapshot (cu of up to 257 offsets)
+
+}  // namespace fo
