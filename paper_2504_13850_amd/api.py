@@ -26,7 +26,9 @@ EXPORTS = [
     "fo_queues_push", "fo_queues_push_model", "fo_pick_device", "fo_queues_in_service",
     "fo_queues_release", "fo_aggregate_pending", "fo_aggregate_pending_all", "fo_queues_stats",
     "fo_queues_counters", "fo_queues_add_device", "fo_last_error", "fo_profile_enable", "fo_profile_read",
+    "fo_gemm_bf16", "fo_conv2d_bf16",
 ]
+FO_LAYOUT_ROW_K, FO_LAYOUT_K_ROW = 0, 1
 
 
 class FoError(RuntimeError):
@@ -95,6 +97,9 @@ def lib():
             "fo_last_error": (C.c_char_p, []),
             "fo_profile_enable": (C.c_int, [i32]),
             "fo_profile_read": (i32, [C.POINTER(fo_kernel_stat), i32]),
+            "fo_gemm_bf16": (C.c_int, [i32, i32, i32, i32, vp, vp, i64, i32, vp, vp, i64, vp, i64, i32, vp, vp]),
+            "fo_conv2d_bf16": (C.c_int, [i32, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32,
+                                         vp, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -290,3 +295,16 @@ def fo_profile_read(max_kernels: int = 64) -> list:
         raise FoError(n, last_error())
     return [dict(name=buf[i].name.decode(), launches=buf[i].launches, ms=buf[i].ms, flops=buf[i].flops,
                  mfma_flops=buf[i].mfma_flops) for i in range(min(n, max_kernels))]
+
+
+# ------------------------------------------------------------------ kernel-level entry points
+def fo_gemm_bf16(M, N, K, a_layout, A, A_lo, lda, b_layout, B, B_lo, ldb, C, ldc, splits=1, workspace=None,
+                 stream=None):
+    _check(lib().fo_gemm_bf16(M, N, K, a_layout, _dptr(A), _dptr(A_lo), lda, b_layout, _dptr(B), _dptr(B_lo), ldb,
+                              _dptr(C), ldc, splits, _dptr(workspace), _stream(stream)))
+
+
+def fo_conv2d_bf16(pass_, Bn, H, W, Ci, Co, k, stride, pad, inp, inp_lo, in2, w, w_lo, out, splits=1,
+                   workspace=None, stream=None):
+    _check(lib().fo_conv2d_bf16(pass_, Bn, H, W, Ci, Co, k, stride, pad, _dptr(inp), _dptr(inp_lo), _dptr(in2),
+                                _dptr(w), _dptr(w_lo), _dptr(out), splits, _dptr(workspace), _stream(stream)))

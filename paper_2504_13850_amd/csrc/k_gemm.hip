@@ -467,14 +467,14 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     const int ktot = d.nseg * d.K;
     int kchunk = ktot;
     if (d.splits > 1) {
+        // slices past the end of K have no work and write zero partials
         kchunk = (int)cdiv(cdiv(ktot, d.splits), BK) * BK;
-        FO_CHECK((int64_t)kchunk * (d.splits - 1) < ktot, "gemm: %d splits leave an empty slice of K=%d",
-                 d.splits, ktot);
     }
     const int a = d.amode, b = d.bmode;
     if (a == OP_RK && b == OP_RK) launch<OP_RK, OP_RK>(d, kchunk, s);
     else if (a == OP_RK && b == OP_KR) launch<OP_RK, OP_KR>(d, kchunk, s);
     else if (a == OP_KR && b == OP_KR) launch<OP_KR, OP_KR>(d, kchunk, s);
+    else if (a == OP_KR && b == OP_RK) launch<OP_KR, OP_RK>(d, kchunk, s);
     else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(d, kchunk, s);
     else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(d, kchunk, s);
     else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(d, kchunk, s);

@@ -18,8 +18,12 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _declared():
-    txt = open(os.path.join(ROOT, "include", "fedoptima.h")).read()
-    return sorted(set(re.findall(r"^FO_API [^;]*?\b(fo_\w+)\(", txt, flags=re.M)))
+    names = set()
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if h.endswith(".h"):
+            txt = open(os.path.join(ROOT, "include", h)).read()
+            names |= set(re.findall(r"^FO_API [^;]*?\b(fo_\w+)\(", txt, flags=re.M))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_symbol():
