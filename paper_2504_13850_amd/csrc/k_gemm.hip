@@ -2,9 +2,10 @@
 //
 // Tiling: a 256-thread workgroup (4 waves of 64) computes a 128x128 tile of C;
 // each wave owns a 64x64 sub-tile = 2x2 v_mfma_f32_32x32x16_bf16 accumulators
-// (64 fp32 per lane).  K advances in steps of 32 through two LDS buffers
-// (global loads of step t+1 are in flight while the MFMAs of step t run).
-// LDS tiles hold 128 rows x 32 k (64 B per row) with an XOR swizzle of the
+// (64 fp32 per lane).  K advances in tiles of 64 through two LDS buffers; the
+// global loads of tile t+2 are issued before the MFMAs of tile t, into one of
+// two register sets, so each load has two compute phases to arrive.  LDS
+// tiles hold 128 rows x 64 k (128 B per row) with an XOR swizzle of the
 // 16-byte chunks so that the 128-bit MFMA operand reads and the stores of
 // k-contiguous operands are bank-conflict free.  Operands whose rows are
 // contiguous in memory (weight gradients, input gradients through W) are
@@ -21,11 +22,15 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128, BN = 128, BK = 32, NT = 256;
+constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
+constexpr int NV = BM * BK / 8 / NT;  // 16-byte vectors per thread per operand per K tile (4)
 
-__device__ __forceinline__ int swz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 3); }
-// element offset of (row, k) inside a 128 x 32 LDS tile
-__device__ __forceinline__ int lds_idx(int row, int k) { return row * BK + ((((k >> 3) ^ swz(row))) << 3) + (k & 7); }
+// LDS tiles are 128 rows x 64 k with rows padded to 72 elements (144 B = 36
+// banks): 8 consecutive rows start 4 banks apart, so the 128-bit operand reads
+// (8 rows, one 16-byte chunk each) and the row-contiguous stores are bank
+// conflict free, and every read of a lane is its own base plus a constant.
+constexpr int LDR = BK + 8;
+__device__ __forceinline__ int lds_idx(int row, int k) { return row * LDR + k; }
 
 __device__ __forceinline__ uint16_t half_of(const uint4& v, int e) {
     uint32_t w = e < 2 ? v.x : e < 4 ? v.y : e < 6 ? v.z : v.w;
@@ -48,216 +53,235 @@ __device__ __forceinline__ uint4 load8_guarded(const bf16_t* p, int n_ok) {
 }
 
 // ------------------------------------------------------------------ loaders
-// Every loader keeps offsets relative to the operand's base pointer; the base
-// is passed per K tile so that compensated products can switch between the
-// high and the low part of an operand from one K segment to the next.
+// A loader keeps the address state of its thread; load() fills NV registers
+// for the K tile starting at kb (operand base P passed per tile, so that
+// compensated products can switch between high and low parts), store() puts
+// them into an LDS tile.
 
-// Row-major, k contiguous: thread -> (row = v/4, k chunk = v%4) for v = tid, tid+256.
+// Row-major, k contiguous: rows (tid/8) + 32 v, k chunk (tid % 8) * 8.
 struct LdRK {
-    int64_t off[2];  // row offset, -1 past the last row
-    int64_t ld;
-    int row[2], kc;
+    int64_t off[NV];  // row offsets, -1 past the last row
+    int kc;
     bool vec;
-    uint4 v[2];
-    __device__ void init(const bf16_t* P, int64_t ld_, int r0, int R, int tid) {
-        ld = ld_;
-        kc = (tid & 3) * 8;
+    __device__ void init(const bf16_t* P, int64_t ld, int r0, int R, int tid) {
+        kc = (tid & 7) * 8;
         vec = (ld % 8 == 0) && (((uintptr_t)P & 15) == 0);
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            row[r] = (tid + NT * r) >> 2;
-            int gr = r0 + row[r];
-            off[r] = gr < R ? (int64_t)gr * ld : -1;
+        for (int v = 0; v < NV; ++v) {
+            const int gr = r0 + (tid >> 3) + 32 * v;
+            off[v] = gr < R ? (int64_t)gr * ld : -1;
         }
     }
-    __device__ void load(const bf16_t* P, int kb, int kend) {
-        int k = kb + kc;
+    __device__ void load(const bf16_t* P, int kb, int kend, uint4* r) const {
+        const int k = kb + kc;
+        if (vec && kb + BK <= kend && off[NV - 1] >= 0) {  // interior tile: no checks
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            if (off[r] < 0 || k >= kend) v[r] = make_uint4(0, 0, 0, 0);
-            else if (vec && k + 8 <= kend) v[r] = load8(P + off[r] + k);
-            else v[r] = load8_guarded(P + off[r] + k, kend - k);
+            for (int v = 0; v < NV; ++v) r[v] = load8(P + off[v] + k);
+            return;
+        }
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            if (off[v] < 0 || k >= kend) r[v] = make_uint4(0, 0, 0, 0);
+            else if (vec && k + 8 <= kend) r[v] = load8(P + off[v] + k);
+            else r[v] = load8_guarded(P + off[v] + k, kend - k);
         }
     }
-    __device__ void store(bf16_t* t) const {
+    __device__ void store(bf16_t* t, const uint4* r, int tid) const {
 #pragma unroll
-        for (int r = 0; r < 2; ++r) *reinterpret_cast<uint4*>(&t[lds_idx(row[r], kc)]) = v[r];
+        for (int v = 0; v < NV; ++v) *reinterpret_cast<uint4*>(&t[lds_idx((tid >> 3) + 32 * v, kc)]) = r[v];
     }
 };
 
-// Two consecutive k rows x 8 contiguous r per thread: kp = tid%16, r chunk = (tid/16)*8.
-// Stored transposed: 8 dwords, each the (k, k+1) pair of one r.
+// Rows contiguous: per thread the k pair (2 kp, 2 kp + 1), kp = tid % 32, and
+// two chunks of 8 rows, rc_q = (tid / 32) * 8 + 64 q.  Register v = 2 q + j holds
+// k row 2 kp + j; the store transposes into (k, k+1) dword pairs.
 struct LdKRBase {
     int kp, rc;
-    uint4 v[2];
-    __device__ void store(bf16_t* t) const {
+    __device__ void store(bf16_t* t, const uint4* r, int) const {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            uint32_t w = (uint32_t)half_of(v[0], e) | ((uint32_t)half_of(v[1], e) << 16);
-            *reinterpret_cast<uint32_t*>(&t[lds_idx(rc + e, 2 * kp)]) = w;
-        }
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                uint32_t w = (uint32_t)half_of(r[2 * q], e) | ((uint32_t)half_of(r[2 * q + 1], e) << 16);
+                *reinterpret_cast<uint32_t*>(&t[lds_idx(rc + 64 * q + e, 2 * kp)]) = w;
+            }
     }
 };
 
 struct LdKR : LdKRBase {
     int64_t ld;
-    int r, R;
+    int r0c, R;
     bool vec;
     __device__ void init(const bf16_t* P, int64_t ld_, int r0, int R_, int tid) {
         ld = ld_;
         R = R_;
-        kp = tid & 15;
-        rc = (tid >> 4) * 8;
-        r = r0 + rc;
+        kp = tid & 31;
+        rc = (tid >> 5) * 8;
+        r0c = r0 + rc;
         vec = (ld % 8 == 0) && (((uintptr_t)P & 15) == 0);
     }
-    __device__ void load(const bf16_t* P, int kb, int kend) {
+    __device__ void load(const bf16_t* P, int kb, int kend, uint4* r) const {
+        if (vec && kb + BK <= kend && r0c + 64 + 8 <= R) {  // interior tile: no checks
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            int k = kb + 2 * kp + j;
-            if (k >= kend || r >= R) v[j] = make_uint4(0, 0, 0, 0);
-            else if (vec && r + 8 <= R) v[j] = load8(P + (int64_t)k * ld + r);
-            else v[j] = load8_guarded(P + (int64_t)k * ld + r, R - r);
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) r[2 * q + j] = load8(P + (int64_t)(kb + 2 * kp + j) * ld + r0c + 64 * q);
+            return;
         }
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int k = kb + 2 * kp + j, rr = r0c + 64 * q;
+                uint4& o = r[2 * q + j];
+                if (k >= kend || rr >= R) o = make_uint4(0, 0, 0, 0);
+                else if (vec && rr + 8 <= R) o = load8(P + (int64_t)k * ld + rr);
+                else o = load8_guarded(P + (int64_t)k * ld + rr, R - rr);
+            }
     }
 };
 
-// Conv forward A: r = output pixel (b, oy, ox); k = (ky, kx, ci), Ci % 32 == 0.
+// Conv forward A: rows = output pixels (b, oy, ox); k = (ky, kx, ci), Ci % 64 == 0
+// so that a K tile lies within one filter tap.
 struct LdConvFwd {
     ConvGeom g;
-    int row[2], kc, b[2], oy[2], ox[2];
-    bool ok[2];
-    uint4 v[2];
+    int kc, b[NV], oy[NV], ox[NV];
+    bool ok[NV];
     __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
         g = g_;
-        kc = (tid & 3) * 8;
+        kc = (tid & 7) * 8;
+        const int hw = g.Ho * g.Wo;
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            row[r] = (tid + NT * r) >> 2;
-            int gr = r0 + row[r];
-            ok[r] = gr < R;
-            int hw = g.Ho * g.Wo;
-            b[r] = gr / hw;
-            int rem = gr - b[r] * hw;
-            oy[r] = rem / g.Wo;
-            ox[r] = rem - oy[r] * g.Wo;
+        for (int v = 0; v < NV; ++v) {
+            const int gr = r0 + (tid >> 3) + 32 * v;
+            ok[v] = gr < R;
+            b[v] = gr / hw;
+            const int rem = gr - b[v] * hw;
+            oy[v] = rem / g.Wo;
+            ox[v] = rem - oy[v] * g.Wo;
         }
     }
-    __device__ void load(const bf16_t* X, int kb, int kend) {
-        int tap = kb / g.Ci, ci = kb - tap * g.Ci + kc;
-        int ky = tap / g.kw, kx = tap - ky * g.kw;
+    __device__ void load(const bf16_t* X, int kb, int kend, uint4* r) const {
+        const int tap = kb / g.Ci, ci = kb - tap * g.Ci + kc;
+        const int ky = tap / g.kw, kx = tap - ky * g.kw;
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            int iy = oy[r] * g.stride - g.pad + ky, ix = ox[r] * g.stride - g.pad + kx;
-            bool in = ok[r] && kb + kc < kend && iy >= 0 && iy < g.H && ix >= 0 && ix < g.W;
-            v[r] = in ? load8(X + (((int64_t)b[r] * g.H + iy) * g.W + ix) * g.Ci + ci) : make_uint4(0, 0, 0, 0);
+        for (int v = 0; v < NV; ++v) {
+            const int iy = oy[v] * g.stride - g.pad + ky, ix = ox[v] * g.stride - g.pad + kx;
+            const bool in = ok[v] && kb + kc < kend && iy >= 0 && iy < g.H && ix >= 0 && ix < g.W;
+            r[v] = in ? load8(X + (((int64_t)b[v] * g.H + iy) * g.W + ix) * g.Ci + ci) : make_uint4(0, 0, 0, 0);
         }
     }
-    __device__ void store(bf16_t* t) const {
+    __device__ void store(bf16_t* t, const uint4* r, int tid) const {
 #pragma unroll
-        for (int r = 0; r < 2; ++r) *reinterpret_cast<uint4*>(&t[lds_idx(row[r], kc)]) = v[r];
+        for (int v = 0; v < NV; ++v) *reinterpret_cast<uint4*>(&t[lds_idx((tid >> 3) + 32 * v, kc)]) = r[v];
     }
 };
 
-// Conv dgrad A: r = input pixel (b, iy, ix); k = (ky, kx, co) reads dY, Co % 32 == 0.
+// Conv input-gradient A: rows = input pixels (b, iy, ix); k = (ky, kx, co) over dY, Co % 64 == 0.
 struct LdConvDx {
     ConvGeom g;
-    int row[2], kc, b[2], iy[2], ix[2];
-    bool ok[2];
-    uint4 v[2];
+    int kc, b[NV], iy[NV], ix[NV];
+    bool ok[NV];
     __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
         g = g_;
-        kc = (tid & 3) * 8;
+        kc = (tid & 7) * 8;
+        const int hw = g.H * g.W;
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            row[r] = (tid + NT * r) >> 2;
-            int gr = r0 + row[r];
-            ok[r] = gr < R;
-            int hw = g.H * g.W;
-            b[r] = gr / hw;
-            int rem = gr - b[r] * hw;
-            iy[r] = rem / g.W;
-            ix[r] = rem - iy[r] * g.W;
+        for (int v = 0; v < NV; ++v) {
+            const int gr = r0 + (tid >> 3) + 32 * v;
+            ok[v] = gr < R;
+            b[v] = gr / hw;
+            const int rem = gr - b[v] * hw;
+            iy[v] = rem / g.W;
+            ix[v] = rem - iy[v] * g.W;
         }
     }
-    __device__ void load(const bf16_t* DY, int kb, int kend) {
-        int tap = kb / g.Co, co = kb - tap * g.Co + kc;
-        int ky = tap / g.kw, kx = tap - ky * g.kw;
+    __device__ void load(const bf16_t* DY, int kb, int kend, uint4* r) const {
+        const int tap = kb / g.Co, co = kb - tap * g.Co + kc;
+        const int ky = tap / g.kw, kx = tap - ky * g.kw;
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            int ty = iy[r] + g.pad - ky, tx = ix[r] + g.pad - kx;
-            bool in = ok[r] && kb + kc < kend && ty >= 0 && tx >= 0;
+        for (int v = 0; v < NV; ++v) {
+            const int ty = iy[v] + g.pad - ky, tx = ix[v] + g.pad - kx;
+            bool in = ok[v] && kb + kc < kend && ty >= 0 && tx >= 0;
             int oy = 0, ox = 0;
             if (in) {
                 oy = ty / g.stride;
                 ox = tx / g.stride;
                 in = (oy * g.stride == ty) && (ox * g.stride == tx) && oy < g.Ho && ox < g.Wo;
             }
-            v[r] = in ? load8(DY + (((int64_t)b[r] * g.Ho + oy) * g.Wo + ox) * g.Co + co) : make_uint4(0, 0, 0, 0);
+            r[v] = in ? load8(DY + (((int64_t)b[v] * g.Ho + oy) * g.Wo + ox) * g.Co + co) : make_uint4(0, 0, 0, 0);
         }
     }
-    __device__ void store(bf16_t* t) const {
+    __device__ void store(bf16_t* t, const uint4* r, int tid) const {
 #pragma unroll
-        for (int r = 0; r < 2; ++r) *reinterpret_cast<uint4*>(&t[lds_idx(row[r], kc)]) = v[r];
+        for (int v = 0; v < NV; ++v) *reinterpret_cast<uint4*>(&t[lds_idx((tid >> 3) + 32 * v, kc)]) = r[v];
     }
 };
 
-// Conv dgrad B: r = ci, k = (ky, kx, co): W[co][ky][kx][ci], ci contiguous.
+// Conv input-gradient B: rows = ci, k = (ky, kx, co): W[co][ky][kx][ci], ci contiguous.
 struct LdConvDxW : LdKRBase {
     ConvGeom g;
     int r;
     __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
         g = g_;
-        kp = tid & 15;
-        rc = (tid >> 4) * 8;
+        kp = tid & 31;
+        rc = (tid >> 5) * 8;
         r = r0 + rc;
         (void)R;
     }
-    __device__ void load(const bf16_t* Wt, int kb, int kend) {
-        int tap = kb / g.Co;
-        int KK = g.kh * g.kw;
+    __device__ void load(const bf16_t* Wt, int kb, int kend, uint4* o) const {
+        const int tap = kb / g.Co;
+        const int KK = g.kh * g.kw;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            int k = kb + 2 * kp + j;
-            int co = k - tap * g.Co;
-            bool in = k < kend && r < g.Ci;
-            v[j] = in ? load8(Wt + ((int64_t)co * KK + tap) * g.Ci + r) : make_uint4(0, 0, 0, 0);
-        }
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int k = kb + 2 * kp + j, co = k - tap * g.Co, rr = r + 64 * q;
+                const bool in = k < kend && rr < g.Ci;
+                o[2 * q + j] = in ? load8(Wt + ((int64_t)co * KK + tap) * g.Ci + rr) : make_uint4(0, 0, 0, 0);
+            }
     }
 };
 
-// Conv wgrad B: r = (ky, kx, ci), k = output pixel; reads the input NHWC.
+// Conv weight-gradient B: rows = (ky, kx, ci), k = output pixel; reads the input NHWC.
 struct LdConvDwX : LdKRBase {
     ConvGeom g;
-    int ky, kx, ci;
-    bool rok;
+    int ky[2], kx[2], ci[2];
+    bool rok[2];
     __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
         g = g_;
-        kp = tid & 15;
-        rc = (tid >> 4) * 8;
-        int n = r0 + rc;
-        rok = n < R;
-        int tap = n / g.Ci;
-        ci = n - tap * g.Ci;
-        ky = tap / g.kw;
-        kx = tap - ky * g.kw;
+        kp = tid & 31;
+        rc = (tid >> 5) * 8;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int n = r0 + rc + 64 * q;
+            rok[q] = n < R;
+            const int tap = n / g.Ci;
+            ci[q] = n - tap * g.Ci;
+            ky[q] = tap / g.kw;
+            kx[q] = tap - ky[q] * g.kw;
+        }
     }
-    __device__ void load(const bf16_t* X, int kb, int kend) {
-        int hw = g.Ho * g.Wo;
+    __device__ void load(const bf16_t* X, int kb, int kend, uint4* o) const {
+        const int hw = g.Ho * g.Wo;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            int pix = kb + 2 * kp + j;
-            bool in = rok && pix < kend;
-            int b = 0, iy = 0, ix = 0;
-            if (in) {
+            const int pix = kb + 2 * kp + j;
+            int b = 0, oy = 0, ox = 0;
+            const bool pin = pix < kend;
+            if (pin) {
                 b = pix / hw;
-                int rem = pix - b * hw;
-                int oy = rem / g.Wo, ox = rem - oy * g.Wo;
-                iy = oy * g.stride - g.pad + ky;
-                ix = ox * g.stride - g.pad + kx;
-                in = iy >= 0 && iy < g.H && ix >= 0 && ix < g.W;
+                const int rem = pix - b * hw;
+                oy = rem / g.Wo;
+                ox = rem - oy * g.Wo;
             }
-            v[j] = in ? load8(X + (((int64_t)b * g.H + iy) * g.W + ix) * g.Ci + ci) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int iy = oy * g.stride - g.pad + ky[q], ix = ox * g.stride - g.pad + kx[q];
+                const bool in = pin && rok[q] && iy >= 0 && iy < g.H && ix >= 0 && ix < g.W;
+                o[2 * q + j] = in ? load8(X + (((int64_t)b * g.H + iy) * g.W + ix) * g.Ci + ci[q])
+                                  : make_uint4(0, 0, 0, 0);
+            }
         }
     }
 };
@@ -310,7 +334,8 @@ __device__ __forceinline__ void epilogue(const GemmDesc& d, int row, int col, fl
 // ------------------------------------------------------------------ kernel
 template <int AM, int BMODE>
 __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchunk) {
-    __shared__ __attribute__((aligned(16))) bf16_t smem[2][2][BM * BK];
+    // two K tiles (A and B each 128 x 72 bf16) = 72 KB; reused for the C tile
+    __shared__ __attribute__((aligned(16))) bf16_t smem[2][2][BM * LDR];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
@@ -321,9 +346,11 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
         d.prof_snap[1] = Keff;
     }
     if (m0 >= M) return;  // uniform for the whole workgroup
-    // The K range of this slice, over the concatenation of nseg segments of
-    // length K (segment s pairs (A, B), (A, B2), (A2, B) for s = 0, 1, 2).
-    const int ktot = d.nseg * d.K;
+    // The K range of this slice, over the concatenation of nseg segments
+    // (segment s pairs (A, B), (A, B2), (A2, B) for s = 0, 1, 2), each padded
+    // to a whole number of K tiles (the loaders zero-fill past K).
+    const int kseg = d.nseg > 1 ? (d.K + BK - 1) / BK * BK : d.K;
+    const int ktot = d.nseg * kseg;
     const int kbeg = blockIdx.z * kchunk;
     const int kstop = min(ktot, kbeg + kchunk);
     const int nk = kstop > kbeg ? (kstop - kbeg + BK - 1) / BK : 0;
@@ -341,76 +368,95 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    auto load_tile = [&](int kg) {
-        // segments have length K (a multiple of BK when nseg > 1), so a tile never straddles two
-        const int seg = kg / d.K, kk = kg - seg * d.K;
-        la.load(seg == 2 ? d.A2 : d.A, kk, Keff);
-        lb.load(seg == 1 ? d.B2 : d.B, kk, Keff);
+    // tile t's loads land in register set t % 2; they are issued two compute
+    // phases before the registers are stored to LDS
+    uint4 ra0[NV], rb0[NV], ra1[NV], rb1[NV];
+    // the (segment, offset) of the next tile to load, advanced without division;
+    // segments are whole tiles long, so a tile never straddles two
+    int ld_seg = kseg > 0 ? kbeg / kseg : 0, ld_kk = kbeg - ld_seg * kseg;
+    auto load_tile = [&](uint4* ra, uint4* rb) {
+        la.load(ld_seg == 2 ? d.A2 : d.A, ld_kk, Keff, ra);
+        lb.load(ld_seg == 1 ? d.B2 : d.B, ld_kk, Keff, rb);
+        ld_kk += BK;
+        if (ld_kk >= kseg) {
+            ld_kk -= kseg;
+            ++ld_seg;
+        }
     };
-
-    if (nk > 0) {
-        load_tile(kbeg);
-        la.store(smem[0][0]);
-        lb.store(smem[0][1]);
-    }
-    __syncthreads();
-
     const int lrow = lane & 31, lk = (lane >> 5) * 8;
-    for (int t = 0; t < nk; ++t) {
-        const int cur = t & 1;
-        if (t + 1 < nk) load_tile(kbeg + (t + 1) * BK);
-        const bf16_t* As = smem[cur][0];
-        const bf16_t* Bs = smem[cur][1];
+    const int aoff = lds_idx(wm * 64 + lrow, lk), boff = lds_idx(wn * 64 + lrow, lk);
+    auto compute = [&](const bf16_t* As, const bf16_t* Bs) {
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             bf16x8_t a[2], b[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i)
-                a[i] = *reinterpret_cast<const bf16x8_t*>(&As[lds_idx(wm * 64 + i * 32 + lrow, ks * 16 + lk)]);
+                a[i] = *reinterpret_cast<const bf16x8_t*>(&As[aoff + i * 32 * LDR + ks * 16]);
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                b[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[lds_idx(wn * 64 + j * 32 + lrow, ks * 16 + lk)]);
+                b[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[boff + j * 32 * LDR + ks * 16]);
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
+    };
+
+    if (nk > 0) load_tile(ra0, rb0);
+    if (nk > 1) load_tile(ra1, rb1);
+    if (nk > 0) {
+        la.store(smem[0][0], ra0, tid);
+        lb.store(smem[0][1], rb0, tid);
+    }
+    __syncthreads();
+    for (int t = 0; t < nk; t += 2) {
+        // even step: compute tile t from buffer 0, stage tile t+1 (set 1) into buffer 1
+        if (t + 2 < nk) load_tile(ra0, rb0);
+        compute(smem[0][0], smem[0][1]);
         if (t + 1 < nk) {
-            la.store(smem[cur ^ 1][0]);
-            lb.store(smem[cur ^ 1][1]);
+            la.store(smem[1][0], ra1, tid);
+            lb.store(smem[1][1], rb1, tid);
+        }
+        __syncthreads();
+        if (t + 1 >= nk) break;
+        // odd step: compute tile t+1 from buffer 1, stage tile t+2 (set 0) into buffer 0
+        if (t + 3 < nk) load_tile(ra1, rb1);
+        compute(smem[1][0], smem[1][1]);
+        if (t + 2 < nk) {
+            la.store(smem[0][0], ra0, tid);
+            lb.store(smem[0][1], rb0, tid);
         }
         __syncthreads();
     }
 
     // Accumulator (i, j, r) of this lane holds C[row][col] with
     // row = i*32 + (r/4)*8 + (lane/32)*4 + r%4, col = j*32 + lane%32 (wave-relative).
-    // The tile leaves through LDS in two halves (i = 0, 1) of 64 rows x 128
-    // columns: then each thread owns one column and walks 32 rows, so every
-    // global store instruction covers 64 consecutive columns of one row.
-    float* Cs = reinterpret_cast<float*>(&smem[0][0][0]);  // 64 x 128 fp32 = the 32 KB of tiles
+    // The 128 x 128 tile leaves through LDS: each thread then owns one column and
+    // walks 64 rows, so every global store instruction covers 64 consecutive
+    // columns of one row.
+    float* Cs = reinterpret_cast<float*>(&smem[0][0][0]);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int lr = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                const int lr = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
                 Cs[lr * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
             }
-        __syncthreads();
-        const int c = tid & (BN - 1), col = n0 + c;
-        for (int lr = tid >> 7; lr < 64; lr += 2) {
-            const int row = m0 + (lr >> 5) * 64 + i * 32 + (lr & 31);
-            if (row < M && col < d.N) {
-                const float v = Cs[lr * BN + c];
-                if (d.splits > 1)
-                    d.ws[((int64_t)blockIdx.z * d.M + row) * d.N + col] = v;
-                else
-                    epilogue(d, row, col, v);
-            }
+    __syncthreads();
+    const int c = tid & (BN - 1), col = n0 + c;
+    if (col < d.N) {
+        for (int lr = tid >> 7; lr < BM; lr += 2) {
+            const int row = m0 + lr;
+            if (row >= M) break;
+            const float v = Cs[lr * BN + c];
+            if (d.splits > 1)
+                d.ws[((int64_t)blockIdx.z * d.M + row) * d.N + col] = v;
+            else
+                epilogue(d, row, col, v);
         }
-        __syncthreads();
     }
 }
 
@@ -455,16 +501,16 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     const bool conv = d.amode == OP_CONV_FWD || d.amode == OP_CONV_DX || d.bmode == OP_CONV_DXW ||
                       d.bmode == OP_CONV_DWX;
     if (conv) {
-        FO_CHECK(d.g.Ci % 32 == 0 || d.amode != OP_CONV_FWD, "gemm: conv forward needs Ci %% 32 == 0");
-        FO_CHECK(d.g.Co % 32 == 0 || d.amode != OP_CONV_DX, "gemm: conv dgrad needs Co %% 32 == 0");
+        FO_CHECK(d.g.Ci % BK == 0 || d.amode != OP_CONV_FWD, "gemm: conv forward needs Ci %% %d == 0", BK);
+        FO_CHECK(d.g.Co % BK == 0 || d.amode != OP_CONV_DX, "gemm: conv dgrad needs Co %% %d == 0", BK);
         FO_CHECK(d.g.Ci % 8 == 0, "gemm: conv needs Ci %% 8 == 0");
     }
     FO_CHECK(d.nseg >= 1 && d.nseg <= 3, "gemm: nseg=%d must be 1, 2 or 3", d.nseg);
     if (d.nseg > 1) {
         FO_CHECK(d.B2 && (d.nseg == 2 || d.A2), "gemm: compensated product needs its low parts");
-        FO_CHECK(d.K % BK == 0 && !d.Kdev, "gemm: compensated product needs a static K multiple of %d", BK);
+        FO_CHECK(!d.Kdev, "gemm: compensated product needs a static K");
     }
-    const int ktot = d.nseg * d.K;
+    const int ktot = d.nseg * (d.nseg > 1 ? (int)cdiv(d.K, BK) * BK : d.K);
     int kchunk = ktot;
     if (d.splits > 1) {
         // slices past the end of K have no work and write zero partials

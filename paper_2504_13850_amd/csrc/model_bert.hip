@@ -213,6 +213,17 @@ int split_for(int M, int N, int K) {
     return s;
 }
 
+// K slices for a forward / input-gradient product over the packed rows: enough
+// workgroups for the 256 CUs (two resident per CU), fused epilogue in the
+// reduction pass.  K here is the product's full reduction length (with the
+// compensated segments).
+int split_rows(int rows, int N, int K) {
+    int tiles = (int)(cdiv(rows, 128) * cdiv(N, 128));
+    int s = std::max(1, std::min(4, 512 / std::max(tiles, 1)));
+    while (s > 1 && K / s < 512) --s;
+    return s;
+}
+
 size_t ws_bytes(const fo_model* m) {
     const size_t R = (size_t)m->max_batch * L, B = (size_t)m->max_batch;
     size_t s = 0;
@@ -245,6 +256,7 @@ size_t ws_bytes(const fo_model* m) {
     sw = std::max(sw, gemm_ws_bytes(D, D, split_for(D, D, K)));
     sw = std::max(sw, gemm_ws_bytes(FF, D, split_for(FF, D, K)));
     sw = std::max(sw, gemm_ws_bytes(D, FF, split_for(D, FF, K)));
+    sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
     add(sw);
     add(4 * colsum_ws_floats((int)R, FF));
     add(4 * (size_t)cdiv(R, LNP_ROWS) * 2 * D);
@@ -330,6 +342,7 @@ fo_status init(fo_model* m) {
     sw = std::max(sw, gemm_ws_bytes(D, D, P->split_o));
     sw = std::max(sw, gemm_ws_bytes(FF, D, P->split_f1));
     sw = std::max(sw, gemm_ws_bytes(D, FF, P->split_f2));
+    sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
     P->splitws = a.take<float>(sw / 4 + 1);
     P->colws = a.take<float>(colsum_ws_floats((int)R, FF));
     P->lnpart = a.take<float>((size_t)cdiv(R, LNP_ROWS) * 2 * D);
@@ -404,6 +417,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         TRY(launch_attn_fwd(t.qkv, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
         GemmDesc o = lin_fwd(rows, t.O, t.Olo, D, W + f.wo, Wl + f.wo, D);
         o.Mdev = Tdev;
+        o.splits = split_rows(rows, D, 3 * D); o.ws = P->splitws;
         o.bias = prm + f.bo;
         o.resid = P->Xf[l]; o.ldr = D;
         o.Cf = t.u1; o.ldcf = D;
@@ -418,6 +432,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         TRY(gemm(f1, s));
         GemmDesc f2 = lin_fwd(rows, t.G, t.Glo, FF, W + f.w2, Wl + f.w2, D);
         f2.Mdev = Tdev;
+        f2.splits = split_rows(rows, D, 3 * FF); f2.ws = P->splitws;
         f2.bias = prm + f.bf2;
         f2.resid = t.Hf; f2.ldr = D;
         f2.Cf = t.u2; f2.ldcf = D;
@@ -478,6 +493,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.bmode = OP_KR; d.B = W + f.w1; d.ldb = D;
             d.resid = P->du2f; d.ldr = D;
             d.Cf = P->dHf; d.ldcf = D;
+            d.splits = split_rows(rows, D, FF); d.ws = P->splitws;
             TRY(gemm(d, s));
             GemmDesc w;
             w.M = FF; w.N = D; w.K = rows; w.Kdev = Tdev;
@@ -499,6 +515,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.amode = OP_RK; d.A = P->du1b; d.lda = D;
             d.bmode = OP_KR; d.B = W + f.wo; d.ldb = D;
             d.Cb = P->dO; d.ldcb = D;
+            d.splits = split_rows(rows, D, D); d.ws = P->splitws;
             TRY(gemm(d, s));
             GemmDesc w;
             w.M = D; w.N = D; w.K = rows; w.Kdev = Tdev;
@@ -518,6 +535,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.bmode = OP_KR; d.B = W + f.wqkv; d.ldb = D;
             d.resid = P->du1f; d.ldr = D;
             d.Cf = P->dY[cur ^ 1]; d.ldcf = D;
+            d.splits = split_rows(rows, D, 3 * D); d.ws = P->splitws;
             TRY(gemm(d, s));
         }
         GemmDesc w;
