@@ -61,6 +61,10 @@ struct GemmDesc {
     bf16_t* Cb = nullptr;   // bf16(v)
     bf16_t* Cb2 = nullptr;  // bf16(v - bf16(v)), the low part (same leading dimension)
     int64_t ldcb = 0;
+    // Column sums of the stored value: colpart[m / 128][n] = sum of v over the
+    // valid rows of that 128-row tile (no split-K); launch_colsum_finish with
+    // rows_per_part 128 completes them.
+    float* colpart = nullptr;
     // split-K: z-slices write fp32 partials to ws[z][M][N]; a second pass sums
     // them and runs the epilogue.
     int splits = 1;

@@ -33,9 +33,12 @@ __global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, 
     if (threadIdx.x == 0) loss[0] = part[0] / (float)B;
 }
 
-// Column sums of a [rows][N] matrix in two passes: blocks of (256 columns x
-// 64 rows) write partial sums, then one thread per column adds them.
-constexpr int CS_ROWS = 64;
+// Column sums of a [rows][N] matrix in two passes.  colsum_partial: a block
+// covers 64 columns (one per lane) and CS_ROWS rows, its four waves take
+// interleaved rows with eight loads in flight per lane, and the block writes
+// one partial row.  colsum_finish adds the partial rows that cover valid rows,
+// in chunk order (the result does not depend on scheduling).
+constexpr int CS_ROWS = 128;
 
 template <typename T>
 __device__ __forceinline__ float ld_as_f(const T* p);
@@ -46,23 +49,59 @@ template <typename T>
 __global__ void __launch_bounds__(256) colsum_partial(const T* __restrict__ X, int64_t ld, int rows,
                                                       const int* __restrict__ rows_dev, int N,
                                                       float* __restrict__ part) {
+    __shared__ float red[4][64];
     const int R = rows_dev ? min(rows, *rows_dev) : rows;
-    const int col = blockIdx.x * 256 + threadIdx.x;
     const int r0 = blockIdx.y * CS_ROWS;
-    if (col >= N) return;
-    float s = 0.f;
+    if (r0 >= R) return;  // uniform: this chunk holds no valid row
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = blockIdx.x * 64 + lane;
     const int r1 = min(R, r0 + CS_ROWS);
-    for (int r = r0; r < r1; ++r) s += ld_as_f<T>(X + (int64_t)r * ld + col);
-    part[(int64_t)blockIdx.y * N + col] = s;
+    float s = 0.f;
+    if (col < N) {
+        int r = r0 + wave;
+        for (; r + 28 < r1; r += 32) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = ld_as_f<T>(X + (int64_t)(r + 4 * u) * ld + col);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; r < r1; r += 4) s += ld_as_f<T>(X + (int64_t)r * ld + col);
+    }
+    red[wave][lane] = s;
+    __syncthreads();
+    if (wave == 0 && col < N)
+        part[(int64_t)blockIdx.y * N + col] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
 }
 
-__global__ void __launch_bounds__(256) colsum_finish(const float* __restrict__ part, int chunks, int N,
-                                                     float* __restrict__ out) {
-    const int col = blockIdx.x * 256 + threadIdx.x;
-    if (col >= N) return;
+// part[p][N] for p < ceil(min(rows, *rows_dev) / rows_per_part); column col
+// goes to out.p[col / out.seg][col % out.seg].
+__global__ void __launch_bounds__(256) colsum_finish(const float* __restrict__ part, int rows,
+                                                     const int* __restrict__ rows_dev, int rows_per_part, int N,
+                                                     ColOut out) {
+    __shared__ float red[4][64];
+    const int R = rows_dev ? min(rows, *rows_dev) : rows;
+    const int nparts = (R + rows_per_part - 1) / rows_per_part;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = blockIdx.x * 64 + lane;
     float s = 0.f;
-    for (int c = 0; c < chunks; ++c) s += part[(int64_t)c * N + col];
-    out[col] = s;
+    if (col < N) {
+        int p = wave;
+        for (; p + 28 < nparts; p += 32) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(p + 4 * u) * N + col];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; p < nparts; p += 4) s += part[(int64_t)p * N + col];
+    }
+    red[wave][lane] = s;
+    __syncthreads();
+    if (wave == 0 && col < N) {
+        const int j = col / out.seg;
+        out.p[j][col - j * out.seg] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+    }
 }
 
 __global__ void __launch_bounds__(256) fill_kernel(float* __restrict__ p, int64_t n, float v) {
@@ -70,24 +109,50 @@ __global__ void __launch_bounds__(256) fill_kernel(float* __restrict__ p, int64_
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
 }
 
-// y[b][o] = act(bias[o] + sum_i x[b][i] w[o][i]); one wave per output o, lanes
-// stride over i (coalesced rows of w), every b handled by the same wave.
+// y[b][o] = act(bias[o] + sum_i x[b][i] w[o][i]) for I <= 64 * SL_PER.  One
+// block per output o holds row o of w in registers (lanes over i); its four
+// waves take the batch rows two at a time.
+constexpr int SL_PER = 12;
+
+__device__ __forceinline__ float wave_sum64(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
 template <int ACT>
 __global__ void __launch_bounds__(256) small_linear_fwd_kernel(const float* __restrict__ x, const float* __restrict__ w,
                                                                const float* __restrict__ bias, float* __restrict__ y,
                                                                int B, int I, int O) {
-    const int lane = threadIdx.x & 63;
-    const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (o >= O) return;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int o = blockIdx.x;
     const float* wr = w + (int64_t)o * I;
-    for (int b = 0; b < B; ++b) {
-        const float* xr = x + (int64_t)b * I;
-        float s = 0.f;
-        for (int i = lane; i < I; i += 64) s = fmaf(xr[i], wr[i], s);
-        for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    float wv[SL_PER];
+#pragma unroll
+    for (int k = 0; k < SL_PER; ++k) {
+        const int i = lane + 64 * k;
+        wv[k] = i < I ? wr[i] : 0.f;
+    }
+    const float bo = bias[o];
+    for (int b = wave; b < B; b += 8) {
+        const bool two = b + 4 < B;
+        const float* x0 = x + (int64_t)b * I;
+        const float* x1 = x + (int64_t)(two ? b + 4 : b) * I;
+        float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+        for (int k = 0; k < SL_PER; ++k) {
+            const int i = lane + 64 * k;
+            if (i < I) {
+                s0 = fmaf(x0[i], wv[k], s0);
+                s1 = fmaf(x1[i], wv[k], s1);
+            }
+        }
+        s0 = wave_sum64(s0);
+        s1 = wave_sum64(s1);
         if (lane == 0) {
-            float v = s + bias[o];
-            y[(int64_t)b * O + o] = ACT == 1 ? tanhf(v) : v;
+            const float v0 = s0 + bo, v1 = s1 + bo;
+            y[(int64_t)b * O + o] = ACT == 1 ? tanhf(v0) : v0;
+            if (two) y[(int64_t)(b + 4) * O + o] = ACT == 1 ? tanhf(v1) : v1;
         }
     }
 }
@@ -110,19 +175,64 @@ __global__ void __launch_bounds__(256) small_linear_wgrad_kernel(const float* __
     }
 }
 
-// dx[b][i] = (sum_o dy[b][o] w[o][i]) * (ACT == tanh ? 1 - y[b][i]^2 : 1)   (y = the input's own activation)
-template <int ACT>
-__global__ void __launch_bounds__(256) small_linear_dgrad_kernel(const float* __restrict__ dy,
-                                                                 const float* __restrict__ w,
+// Input gradient of a small linear layer, dx[b][i] = sum_o dy[b][o] w[o][i],
+// as partial sums over chunks of SD_K outputs: block (i-tile, o-chunk, b-group)
+// stages w[o-chunk][i-tile] and dy[b-group][o-chunk] in LDS and writes
+// part[o-chunk][b][i]; small_linear_dgrad_finish adds the chunks in order and
+// applies the derivative of the input's tanh when given.
+constexpr int SD_K = 64, SD_I = 64, SD_B = 32;
+
+__global__ void __launch_bounds__(256) small_linear_dgrad_partial(const float* __restrict__ dy,
+                                                                  const float* __restrict__ w, float* __restrict__ part,
+                                                                  int B, int I, int O) {
+    __shared__ float ws[SD_K][SD_I];
+    __shared__ float ds[SD_B][SD_K + 1];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int i0 = blockIdx.x * SD_I, o0 = blockIdx.y * SD_K, b0 = blockIdx.z * SD_B;
+    for (int e = tid; e < SD_K * SD_I; e += 256) {
+        const int ok = e / SD_I, ii = e % SD_I;
+        ws[ok][ii] = (o0 + ok < O && i0 + ii < I) ? w[(int64_t)(o0 + ok) * I + i0 + ii] : 0.f;
+    }
+    for (int e = tid; e < SD_B * SD_K; e += 256) {
+        const int bb = e / SD_K, ok = e % SD_K;
+        ds[bb][ok] = (b0 + bb < B && o0 + ok < O) ? dy[(int64_t)(b0 + bb) * O + o0 + ok] : 0.f;
+    }
+    __syncthreads();
+    // lane: column i0 + lane; wave: batch rows b0 + wave + 4 j
+    float acc[SD_B / 4];
+#pragma unroll
+    for (int j = 0; j < SD_B / 4; ++j) acc[j] = 0.f;
+#pragma unroll 8
+    for (int k = 0; k < SD_K; ++k) {
+        const float wk = ws[k][lane];
+#pragma unroll
+        for (int j = 0; j < SD_B / 4; ++j) acc[j] = fmaf(ds[wave + 4 * j][k], wk, acc[j]);
+    }
+    const int i = i0 + lane;
+    if (i < I) {
+#pragma unroll
+        for (int j = 0; j < SD_B / 4; ++j) {
+            const int b = b0 + wave + 4 * j;
+            if (b < B) part[((int64_t)blockIdx.y * B + b) * I + i] = acc[j];
+        }
+    }
+}
+
+__global__ void __launch_bounds__(256) small_linear_dgrad_finish(const float* __restrict__ part, int chunks,
                                                                  const float* __restrict__ yin,
-                                                                 float* __restrict__ dx, int B, int I, int O) {
-    int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (int64_t)B * I) return;
-    int b = (int)(idx / I), i = (int)(idx % I);
+                                                                 float* __restrict__ dx, int64_t n) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= n) return;
     float s = 0.f;
-    for (int o = 0; o < O; ++o) s = fmaf(dy[(int64_t)b * O + o], w[(int64_t)o * I + i], s);
-    if (ACT == 1) {
-        float t = yin[idx];
+    int c = 0;
+    for (; c + 3 < chunks; c += 4) {
+        const float v0 = part[(int64_t)c * n + idx], v1 = part[(int64_t)(c + 1) * n + idx];
+        const float v2 = part[(int64_t)(c + 2) * n + idx], v3 = part[(int64_t)(c + 3) * n + idx];
+        s += (v0 + v1) + (v2 + v3);
+    }
+    for (; c < chunks; ++c) s += part[(int64_t)c * n + idx];
+    if (yin) {
+        const float t = yin[idx];
         s *= 1.f - t * t;
     }
     dx[idx] = s;
@@ -138,15 +248,26 @@ fo_status launch_xent(const float* z, const int32_t* labels, float* dz, float* l
 
 size_t colsum_ws_floats(int rows, int N) { return (size_t)cdiv(rows, CS_ROWS) * N; }
 
+fo_status launch_colsum_finish(const float* part, int rows, const int* rows_dev, int rows_per_part, int N,
+                               const ColOut& out, hipStream_t s) {
+    FO_CHECK(out.seg > 0 && cdiv(N, out.seg) <= 3, "colsum: %d columns in segments of %d", N, out.seg);
+    hipLaunchKernelGGL(colsum_finish, dim3(cdiv(N, 64)), dim3(256), 0, s, part, rows, rows_dev, rows_per_part, N,
+                       out);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
 template <typename T>
 static fo_status colsum_impl(const T* X, int64_t ld, int rows, const int* rows_dev, int N, float* out, float* ws,
                              hipStream_t s) {
-    int chunks = (int)cdiv(rows, CS_ROWS);
-    hipLaunchKernelGGL((colsum_partial<T>), dim3(cdiv(N, 256), chunks), dim3(256), 0, s, X, ld, rows, rows_dev, N,
-                       ws);
-    hipLaunchKernelGGL(colsum_finish, dim3(cdiv(N, 256)), dim3(256), 0, s, ws, chunks, N, out);
+    if (rows <= 0 || N <= 0) return FO_OK;
+    hipLaunchKernelGGL((colsum_partial<T>), dim3(cdiv(N, 64), cdiv(rows, CS_ROWS)), dim3(256), 0, s, X, ld, rows,
+                       rows_dev, N, ws);
     FO_LAUNCHED();
-    return FO_OK;
+    ColOut o;
+    o.p[0] = out;
+    o.seg = N;
+    return launch_colsum_finish(ws, rows, rows_dev, CS_ROWS, N, o, s);
 }
 
 fo_status launch_colsum(const float* X, int64_t ld, int rows, const int* rows_dev, int N, float* out, float* ws,
@@ -168,26 +289,29 @@ fo_status launch_fill(float* p, int64_t n, float v, hipStream_t s) {
 
 fo_status launch_small_linear_fwd(const float* x, const float* w, const float* bias, float* y, int B, int I, int O,
                                   bool tanh_act, hipStream_t s) {
-    dim3 grid((unsigned)cdiv(O, 4));
+    FO_CHECK(I <= 64 * SL_PER, "small linear: %d inputs (at most %d)", I, 64 * SL_PER);
+    if (B <= 0 || O <= 0) return FO_OK;
     if (tanh_act)
-        hipLaunchKernelGGL((small_linear_fwd_kernel<1>), grid, dim3(256), 0, s, x, w, bias, y, B, I, O);
+        hipLaunchKernelGGL((small_linear_fwd_kernel<1>), dim3(O), dim3(256), 0, s, x, w, bias, y, B, I, O);
     else
-        hipLaunchKernelGGL((small_linear_fwd_kernel<0>), grid, dim3(256), 0, s, x, w, bias, y, B, I, O);
+        hipLaunchKernelGGL((small_linear_fwd_kernel<0>), dim3(O), dim3(256), 0, s, x, w, bias, y, B, I, O);
     FO_LAUNCHED();
     return FO_OK;
 }
 
+size_t small_linear_ws_floats(int B, int I, int O) { return (size_t)cdiv(O, SD_K) * B * I; }
+
 fo_status launch_small_linear_bwd(const float* dy, const float* x, const float* w, const float* xin_tanh, float* gw,
-                                  float* gb, float* dx, int B, int I, int O, hipStream_t s) {
+                                  float* gb, float* dx, int B, int I, int O, float* ws, hipStream_t s) {
     int64_t nw = std::max<int64_t>((int64_t)O * I, O);
     hipLaunchKernelGGL(small_linear_wgrad_kernel, dim3(cdiv(nw, 256)), dim3(256), 0, s, dy, x, gw, gb, B, I, O);
     if (dx) {
-        if (xin_tanh)
-            hipLaunchKernelGGL((small_linear_dgrad_kernel<1>), dim3(cdiv((int64_t)B * I, 256)), dim3(256), 0, s, dy,
-                               w, xin_tanh, dx, B, I, O);
-        else
-            hipLaunchKernelGGL((small_linear_dgrad_kernel<0>), dim3(cdiv((int64_t)B * I, 256)), dim3(256), 0, s, dy,
-                               w, xin_tanh, dx, B, I, O);
+        const int chunks = (int)cdiv(O, SD_K);
+        hipLaunchKernelGGL(small_linear_dgrad_partial, dim3(cdiv(I, SD_I), chunks, cdiv(B, SD_B)), dim3(256), 0, s,
+                           dy, w, ws, B, I, O);
+        const int64_t n = (int64_t)B * I;
+        hipLaunchKernelGGL(small_linear_dgrad_finish, dim3(cdiv(n, 256)), dim3(256), 0, s, ws, chunks, xin_tanh, dx,
+                           n);
     }
     FO_LAUNCHED();
     return FO_OK;

@@ -312,7 +312,7 @@ __device__ __forceinline__ float gelu_grad(float x) {
     return cdf + x * pdf;
 }
 
-__device__ __forceinline__ void epilogue(const GemmDesc& d, int row, int col, float v) {
+__device__ __forceinline__ float epilogue(const GemmDesc& d, int row, int col, float v) {
     if (d.bias) v += d.bias[col];
     if (d.resid) v += d.resid[(int64_t)row * d.ldr + col];
     if (d.act == ACT_GELU) {
@@ -329,6 +329,7 @@ __device__ __forceinline__ void epilogue(const GemmDesc& d, int row, int col, fl
         d.Cb[(int64_t)row * d.ldcb + col] = hi;
         if (d.Cb2) d.Cb2[(int64_t)row * d.ldcb + col] = f2bf(v - bf2f(hi));
     }
+    return v;
 }
 
 // ------------------------------------------------------------------ kernel
@@ -447,6 +448,7 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
             }
     __syncthreads();
     const int c = tid & (BN - 1), col = n0 + c;
+    float csum = 0.f;
     if (col < d.N) {
         for (int lr = tid >> 7; lr < BM; lr += 2) {
             const int row = m0 + lr;
@@ -455,19 +457,49 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
             if (d.splits > 1)
                 d.ws[((int64_t)blockIdx.z * d.M + row) * d.N + col] = v;
             else
-                epilogue(d, row, col, v);
+                csum += epilogue(d, row, col, v);
         }
+    }
+    if (d.colpart) {  // uniform; the two row halves of a column meet in LDS
+        __syncthreads();
+        if (tid >= BN) Cs[c] = csum;
+        __syncthreads();
+        if (tid < BN && col < d.N) d.colpart[(int64_t)blockIdx.y * d.N + col] = csum + Cs[c];
     }
 }
 
+// Sums the split-K partials and runs the epilogue; four columns per thread
+// when N % 4 == 0, with the slices loaded four at a time.
 __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
     const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
-    int64_t total = (int64_t)M * d.N, full = (int64_t)d.M * d.N;
-    int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-        float v = 0.f;
-        for (int z = 0; z < d.splits; ++z) v += d.ws[(int64_t)z * full + i];
-        epilogue(d, (int)(i / d.N), (int)(i % d.N), v);
+    const int64_t full = (int64_t)d.M * d.N;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int S = d.splits;
+    if ((d.N & 3) == 0) {
+        const int64_t total4 = (int64_t)M * d.N / 4;
+        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total4; i += stride) {
+            const float* p = d.ws + 4 * i;
+            f32x4 v = *reinterpret_cast<const f32x4*>(p);
+            int z = 1;
+            for (; z + 3 < S; z += 4) {
+                const f32x4 a = *reinterpret_cast<const f32x4*>(p + z * full);
+                const f32x4 b = *reinterpret_cast<const f32x4*>(p + (z + 1) * full);
+                const f32x4 e = *reinterpret_cast<const f32x4*>(p + (z + 2) * full);
+                const f32x4 f = *reinterpret_cast<const f32x4*>(p + (z + 3) * full);
+                v += (a + b) + (e + f);
+            }
+            for (; z < S; ++z) v += *reinterpret_cast<const f32x4*>(p + z * full);
+            const int row = (int)(4 * i / d.N), col = (int)(4 * i % d.N);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) epilogue(d, row, col + e, v[e]);
+        }
+    } else {
+        const int64_t total = (int64_t)M * d.N;
+        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+            float v = 0.f;
+            for (int z = 0; z < S; ++z) v += d.ws[(int64_t)z * full + i];
+            epilogue(d, (int)(i / d.N), (int)(i % d.N), v);
+        }
     }
 }
 
@@ -498,6 +530,7 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     FO_CHECK(d.M > 0 && d.N > 0 && d.K > 0, "gemm: empty problem %dx%dx%d", d.M, d.N, d.K);
     FO_CHECK(d.splits >= 1 && (d.splits == 1 || d.ws != nullptr), "gemm: split-K needs a workspace");
     FO_CHECK(d.Cf || d.Cb, "gemm: no output");
+    FO_CHECK(!d.colpart || d.splits == 1, "gemm: column sums need splits == 1");
     const bool conv = d.amode == OP_CONV_FWD || d.amode == OP_CONV_DX || d.bmode == OP_CONV_DXW ||
                       d.bmode == OP_CONV_DWX;
     if (conv) {
@@ -531,6 +564,7 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     FO_LAUNCHED();
     if (d.splits > 1) {
         int64_t total = (int64_t)d.M * d.N;
+        if (d.N % 4 == 0) total /= 4;
         int grid = (int)std::min<int64_t>(cdiv(total, 256), 4096);
         const int h = prof_begin(s, "splitk_reduce", ProfInfo());
         hipLaunchKernelGGL(splitk_reduce, dim3(grid), dim3(256), 0, s, d);

@@ -41,12 +41,22 @@ fo_status launch_colsum(const float* X, int64_t ld, int rows, const int* rows_de
                         hipStream_t s);
 fo_status launch_colsum(const bf16_t* X, int64_t ld, int rows, const int* rows_dev, int N, float* out, float* ws,
                         hipStream_t s);
+// Destination of a column-sum finish: column c goes to p[c / seg][c % seg] (up to three outputs).
+struct ColOut {
+    float* p[3] = {nullptr, nullptr, nullptr};
+    int seg = 0;
+};
+// Adds partial rows part[p][N] over p < ceil(min(rows, *rows_dev) / rows_per_part), in order.
+fo_status launch_colsum_finish(const float* part, int rows, const int* rows_dev, int rows_per_part, int N,
+                               const ColOut& out, hipStream_t s);
 fo_status launch_fill(float* p, int64_t n, float v, hipStream_t s);
-// y = act(x W^T + b) for small fp32 layers (x [B][I], W [O][I]); act = tanh or none
+// y = x w^T + bias (tanh when tanh_act) for x [B][I], w [O][I], I <= 768
 fo_status launch_small_linear_fwd(const float* x, const float* w, const float* bias, float* y, int B, int I, int O,
                                   bool tanh_act, hipStream_t s);
-// gw = dy^T x, gb = colsum dy, dx = (dy W) * (1 - xin_tanh^2 if given); dx may be NULL
+// gw = dy^T x, gb = colsum dy, dx = (dy W) * (1 - xin_tanh^2 if given); dx may be NULL.
+// ws holds small_linear_ws_floats(B, I, O) floats when dx is set.
+size_t small_linear_ws_floats(int B, int I, int O);
 fo_status launch_small_linear_bwd(const float* dy, const float* x, const float* w, const float* xin_tanh, float* gw,
-                                  float* gb, float* dx, int B, int I, int O, hipStream_t s);
+                                  float* gb, float* dx, int B, int I, int O, float* ws, hipStream_t s);
 
 }  // namespace fo

@@ -46,7 +46,7 @@ struct Plan {
     LayerAct a[NL];
     float *dY[2], *du2f, *dHf, *du1f, *Dws;
     bf16_t *du2b, *dA1, *du1b, *dO, *dqkv;
-    float *splitws, *colws, *lnpart;
+    float *splitws, *colws, *lnpart, *slws;
     int split_qkv, split_o, split_f1, split_f2;
     float *xc, *pooled, *dz, *dpool, *dxc;
 };
@@ -134,62 +134,68 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ u
     }
 }
 
-// dx = rstd * (gdy - mean(gdy) - xhat * mean(gdy * xhat)), gdy = dy * gamma
+// dx = rstd * (gdy - mean(gdy) - xhat * mean(gdy * xhat)), gdy = dy * gamma.
+// A block takes LNB_ROWS consecutive rows (a quarter per wave) and also
+// writes column partial sums of the norm's parameter gradients and of dx:
+// part[block][0][c] = sum dy * xhat (dgamma), part[block][1][c] = sum dy
+// (dbeta), part[block][2][c] = sum dx (the bias gradient of the sublayer
+// whose sum with the residual this norm normalises).
+constexpr int LNB_ROWS = 16;
+
 __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ dy, const float* __restrict__ u,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
                                                      const float* __restrict__ g, const int* __restrict__ Tdev,
-                                                     float* __restrict__ dxf, bf16_t* __restrict__ dxb) {
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-    if (row >= *Tdev) return;
-    const float mu = mean[row], rs = rstd[row];
-    float xh[PER], gd[PER];
-    float s1 = 0.f, s2 = 0.f;
+                                                     float* __restrict__ dxf, bf16_t* __restrict__ dxb,
+                                                     float* __restrict__ part) {
+    __shared__ float red[4][D];
+    const int T = *Tdev;
+    const int r0 = blockIdx.x * LNB_ROWS;
+    if (r0 >= T) return;  // uniform
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    float gam[PER], pg[PER], pb[PER], px[PER];
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
-        int c = lane + 64 * k;
-        xh[k] = (u[(int64_t)row * D + c] - mu) * rs;
-        gd[k] = dy[(int64_t)row * D + c] * g[c];
-        s1 += gd[k];
-        s2 = fmaf(gd[k], xh[k], s2);
+        gam[k] = g[lane + 64 * k];
+        pg[k] = pb[k] = px[k] = 0.f;
     }
-    s1 = wave_sum(s1) * (1.f / D);
-    s2 = wave_sum(s2) * (1.f / D);
+    for (int i = 0; i < LNB_ROWS / 4; ++i) {
+        const int row = r0 + wave * (LNB_ROWS / 4) + i;
+        if (row >= T) break;
+        const float mu = mean[row], rs = rstd[row];
+        float xh[PER], gd[PER];
+        float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        int c = lane + 64 * k;
-        float dx = rs * (gd[k] - s1 - xh[k] * s2);
-        dxf[(int64_t)row * D + c] = dx;
-        dxb[(int64_t)row * D + c] = f2bf(dx);
+        for (int k = 0; k < PER; ++k) {
+            const int c = lane + 64 * k;
+            const float d = dy[(int64_t)row * D + c];
+            xh[k] = (u[(int64_t)row * D + c] - mu) * rs;
+            gd[k] = d * gam[k];
+            pg[k] = fmaf(d, xh[k], pg[k]);
+            pb[k] += d;
+            s1 += gd[k];
+            s2 = fmaf(gd[k], xh[k], s2);
+        }
+        s1 = wave_sum(s1) * (1.f / D);
+        s2 = wave_sum(s2) * (1.f / D);
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int c = lane + 64 * k;
+            const float dx = rs * (gd[k] - s1 - xh[k] * s2);
+            px[k] += dx;
+            dxf[(int64_t)row * D + c] = dx;
+            dxb[(int64_t)row * D + c] = f2bf(dx);
+        }
     }
-}
-
-// dgamma = sum_rows dy * xhat, dbeta = sum_rows dy: partial sums per 64 rows.
-constexpr int LNP_ROWS = 64;
-__global__ void __launch_bounds__(256) ln_param_partial(const float* __restrict__ dy, const float* __restrict__ u,
-                                                        const float* __restrict__ mean, const float* __restrict__ rstd,
-                                                        const int* __restrict__ Tdev, float* __restrict__ part) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    const int r0 = blockIdx.y * LNP_ROWS, r1 = min(*Tdev, r0 + LNP_ROWS);
-    float sg = 0.f, sb = 0.f;
-    for (int r = r0; r < r1; ++r) {
-        float d = dy[(int64_t)r * D + c];
-        sg = fmaf(d, (u[(int64_t)r * D + c] - mean[r]) * rstd[r], sg);
-        sb += d;
+    float* out = part + (int64_t)blockIdx.x * 3 * D;
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+#pragma unroll
+        for (int k = 0; k < PER; ++k) red[wave][lane + 64 * k] = q == 0 ? pg[k] : (q == 1 ? pb[k] : px[k]);
+        __syncthreads();
+        for (int c = threadIdx.x; c < D; c += 256)
+            out[q * D + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+        __syncthreads();
     }
-    part[((int64_t)blockIdx.y * 2 + 0) * D + c] = sg;
-    part[((int64_t)blockIdx.y * 2 + 1) * D + c] = sb;
-}
-
-__global__ void __launch_bounds__(256) ln_param_finish(const float* __restrict__ part, int chunks,
-                                                       float* __restrict__ dg, float* __restrict__ db) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    float sg = 0.f, sb = 0.f;
-    for (int k = 0; k < chunks; ++k) {
-        sg += part[((int64_t)k * 2 + 0) * D + c];
-        sb += part[((int64_t)k * 2 + 1) * D + c];
-    }
-    dg[c] = sg;
-    db[c] = sb;
 }
 
 __global__ void __launch_bounds__(256) gather_cls_kernel(const float* __restrict__ X, const int* __restrict__ cu,
@@ -259,7 +265,8 @@ size_t ws_bytes(const fo_model* m) {
     sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
     add(sw);
     add(4 * colsum_ws_floats((int)R, FF));
-    add(4 * (size_t)cdiv(R, LNP_ROWS) * 2 * D);
+    add(4 * (size_t)cdiv(R, LNB_ROWS) * 3 * D);
+    add(4 * small_linear_ws_floats((int)B, D, D));
     add(4 * B * D); add(4 * B * D); add(4 * B * NC); add(4 * B * D); add(4 * B * D);
     return s;
 }
@@ -345,7 +352,8 @@ fo_status init(fo_model* m) {
     sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
     P->splitws = a.take<float>(sw / 4 + 1);
     P->colws = a.take<float>(colsum_ws_floats((int)R, FF));
-    P->lnpart = a.take<float>((size_t)cdiv(R, LNP_ROWS) * 2 * D);
+    P->lnpart = a.take<float>((size_t)cdiv(R, LNB_ROWS) * 3 * D);
+    P->slws = a.take<float>(small_linear_ws_floats((int)B, D, D));
     P->xc = a.take<float>(B * D);
     P->pooled = a.take<float>(B * D);
     P->dz = a.take<float>(B * NC);
@@ -376,13 +384,20 @@ GemmDesc lin_fwd(int rows, const bf16_t* A, const bf16_t* Alo, int K, const bf16
     return d;
 }
 
-fo_status ln_params(const Plan* P, const float* dy, const float* u, const float* mean, const float* rstd,
-                    const int* Tdev, int rows, float* dg, float* db, hipStream_t s) {
-    int chunks = (int)cdiv(rows, LNP_ROWS);
-    hipLaunchKernelGGL(ln_param_partial, dim3(D / 256, chunks), dim3(256), 0, s, dy, u, mean, rstd, Tdev, P->lnpart);
-    hipLaunchKernelGGL(ln_param_finish, dim3(D / 256), dim3(256), 0, s, P->lnpart, chunks, dg, db);
+// Backward of a norm: dx (fp32 and bf16) plus dgamma, dbeta and the column
+// sum of dx (into dbias_below).
+fo_status ln_bwd(const Plan* P, const float* dy, const float* u, const float* mean, const float* rstd,
+                 const float* gamma, const int* Tdev, int rows, float* dxf, bf16_t* dxb, float* dg, float* db,
+                 float* dbias_below, hipStream_t s) {
+    hipLaunchKernelGGL(ln_bwd_kernel, dim3(cdiv(rows, LNB_ROWS)), dim3(256), 0, s, dy, u, mean, rstd, gamma, Tdev,
+                       dxf, dxb, P->lnpart);
     FO_LAUNCHED();
-    return FO_OK;
+    ColOut o;
+    o.p[0] = dg;
+    o.p[1] = db;
+    o.p[2] = dbias_below;
+    o.seg = D;
+    return launch_colsum_finish(P->lnpart, rows, Tdev, LNB_ROWS, 3 * D, o, s);
 }
 
 fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
@@ -451,9 +466,9 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
 
     // ---------------- backward (Alg. 4: backward pass of M_s)
     TRY(launch_small_linear_bwd(P->dz, P->pooled, prm + P->cls_w, P->pooled, grd + P->cls_w, grd + P->cls_b,
-                                P->dpool, B, D, NC, s));
+                                P->dpool, B, D, NC, P->slws, s));
     TRY(launch_small_linear_bwd(P->dpool, P->xc, prm + P->pool_w, nullptr, grd + P->pool_w, grd + P->pool_b, P->dxc,
-                                B, D, D, s));
+                                B, D, D, P->slws, s));
     TRY(launch_fill(P->dY[0], (int64_t)rows * D, 0.f, s));
     hipLaunchKernelGGL(scatter_cls_kernel, dim3(B), dim3(256), 0, s, P->dxc, P->cu, B, P->dY[0]);
     FO_LAUNCHED();
@@ -464,9 +479,8 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         LayerAct& t = P->a[l];
         float* dY = P->dY[cur];
         // LN2
-        hipLaunchKernelGGL(ln_bwd_kernel, lngrid, dim3(256), 0, s, dY, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev,
-                           P->du2f, P->du2b);
-        TRY(ln_params(P, dY, t.u2, t.mean2, t.rstd2, Tdev, rows, grd + f.g2, grd + f.b2, s));
+        TRY(ln_bwd(P, dY, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, P->du2b, grd + f.g2, grd + f.b2,
+                   grd + f.bf2, s));
         // FFN2: dG = du2 W2 (times GELU'(pre1) -> dA1), dW2 = du2^T G, db2
         {
             GemmDesc d;
@@ -475,7 +489,12 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.bmode = OP_KR; d.B = W + f.w2; d.ldb = FF;
             d.dpre = t.pre1; d.ldm = FF;
             d.Cb = P->dA1; d.ldcb = FF;
+            d.colpart = P->colws;
             TRY(gemm(d, s));
+            ColOut cb;
+            cb.p[0] = grd + f.bf1;
+            cb.seg = FF;
+            TRY(launch_colsum_finish(P->colws, rows, Tdev, 128, FF, cb, s));
             GemmDesc w;
             w.M = D; w.N = FF; w.K = rows; w.Kdev = Tdev;
             w.amode = OP_KR; w.A = P->du2b; w.lda = D;
@@ -483,7 +502,6 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             w.Cf = grd + f.w2; w.ldcf = FF;
             w.splits = P->split_f2; w.ws = P->splitws;
             TRY(gemm(w, s));
-            TRY(launch_colsum(P->du2f, D, rows, Tdev, D, grd + f.bf2, P->colws, s));
         }
         // FFN1: dH = du2 + dA1 W1, dW1 = dA1^T H, db1
         {
@@ -502,12 +520,10 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             w.Cf = grd + f.w1; w.ldcf = D;
             w.splits = P->split_f1; w.ws = P->splitws;
             TRY(gemm(w, s));
-            TRY(launch_colsum(P->dA1, FF, rows, Tdev, FF, grd + f.bf1, P->colws, s));
         }
         // LN1
-        hipLaunchKernelGGL(ln_bwd_kernel, lngrid, dim3(256), 0, s, P->dHf, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev,
-                           P->du1f, P->du1b);
-        TRY(ln_params(P, P->dHf, t.u1, t.mean1, t.rstd1, Tdev, rows, grd + f.g1, grd + f.b1, s));
+        TRY(ln_bwd(P, P->dHf, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, P->du1b, grd + f.g1,
+                   grd + f.b1, grd + f.bo, s));
         // output projection: dO = du1 Wo, dWo = du1^T O, dbo
         {
             GemmDesc d;
@@ -524,7 +540,6 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             w.Cf = grd + f.wo; w.ldcf = D;
             w.splits = P->split_o; w.ws = P->splitws;
             TRY(gemm(w, s));
-            TRY(launch_colsum(P->du1f, D, rows, Tdev, D, grd + f.bo, P->colws, s));
         }
         TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, P->Dws, P->dqkv, B, NH, D, s));
         // input projection: dX = du1 + dqkv Wqkv (skipped for the first server layer), dWqkv, dbqkv
