@@ -65,283 +65,364 @@ __device__ __forceinline__ float half_sum(float v) {
     return v;
 }
 
-constexpr int PADJ = LMAX + 8;  // LDS row stride (bf16) of the key dimension
+constexpr int PADJ = LMAX + 8;  // LDS row stride (bf16) of arrays indexed [.][key or query]
+constexpr int PADK = DH + 8;    // LDS row stride (bf16) of row-major [token][head column] arrays
 
-// Forward on the matrix cores.  Workgroup = (sequence, head), wave w owns
-// query rows 32w..32w+31.  S = Q K^T and O = P V are compensated products
-// (bf16 high/low parts of both operands, three MFMAs each) so that the
-// attention keeps about 16 bits of operand precision.  The v_mfma 32x32x16
-// operand layouts: lane l supplies row (l mod 32) and k = 8*(l div 32) + 0..7
-// of A, column (l mod 32) and the same k of B; the accumulator holds
-// C[8*(r div 4) + 4*(l div 32) + (r mod 4)][l mod 32] in register r.
-__global__ void __launch_bounds__(256) attn_fwd_mfma(const float* __restrict__ qkv, const int* __restrict__ cu,
-                                                     bf16_t* __restrict__ out, bf16_t* __restrict__ outlo,
-                                                     float* __restrict__ lse, int H, int d, float scale,
-                                                     int* __restrict__ snap, int nb) {
-    __shared__ __attribute__((aligned(16))) bf16_t Vt[2][DH][PADJ];      // V^T (high, low), zero past len
-    __shared__ __attribute__((aligned(16))) bf16_t Ps[4][2][32][PADJ];   // per-wave P (high, low)
+// Transposed orientation.  Both passes compute S^T = K Q^T: a wave owns 32
+// queries, which sit on the accumulator columns, so every lane holds one
+// query and 16 keys per 32x32 tile (key j = 32 jt + 8 (r div 4) + 4 (l div
+// 32) + r mod 4 in register r).  Row statistics over keys then reduce within
+// the lane plus one exchange between the half-waves, and a tile of P^T (or
+// dS^T) already is the B operand of a product that sums over keys, provided
+// the A operand takes its k index through the same permutation: for k block
+// kb of tile jt, lane half h supplies keys 32 jt + 16 kb + {4h..4h+3} and
+// 32 jt + 16 kb + 8 + {4h..4h+3} (registers 8 kb .. 8 kb + 7).
+
+// Eight bf16 of an LDS row at key offsets {j, .., j+3, j+8, .., j+11}.
+__device__ __forceinline__ bf16x8_t ld_perm(const bf16_t* row, int j) {
+    const uint2 a = *reinterpret_cast<const uint2*>(row + j);
+    const uint2 c = *reinterpret_cast<const uint2*>(row + j + 8);
+    const u32x4_t v = {a.x, a.y, c.x, c.y};
+    return __builtin_bit_cast(bf16x8_t, v);
+}
+
+__device__ __forceinline__ uint2 pack4(bf16_t a, bf16_t b, bf16_t c, bf16_t e) {
+    return make_uint2((uint32_t)a | ((uint32_t)b << 16), (uint32_t)c | ((uint32_t)e << 16));
+}
+
+// Forward.  Workgroup = (sequence, head), wave w owns queries 32w..32w+31.
+// S^T = K Q^T and O^T = V^T P^T are compensated products (bf16 high/low parts
+// of both operands, three MFMAs each), so the attention keeps about 16 bits
+// of operand precision.  K (row-major) and V^T are staged in LDS once, with
+// every global load of the workgroup issued before the first LDS store.
+__global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const float* __restrict__ qkv, const int* __restrict__ cu,
+                                                        bf16_t* __restrict__ out, bf16_t* __restrict__ outlo,
+                                                        float* __restrict__ lse, int H, int d, float scale,
+                                                        int* __restrict__ snap, int nb) {
+    __shared__ __attribute__((aligned(16))) bf16_t Ks[2][LMAX][PADK];  // K (high, low), zero past len
+    __shared__ __attribute__((aligned(16))) bf16_t Vt[2][DH][PADJ];    // V^T (high, low), zero past len
     if (snap && blockIdx.x == 0)
         for (int i = threadIdx.x; i <= nb; i += blockDim.x) snap[i] = cu[i];
     const int b = blockIdx.x / H, h = blockIdx.x % H;
     const int base = cu[b], len = cu[b + 1] - cu[b];
     const int ld = 3 * d;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    for (int idx = tid; idx < LMAX * DH; idx += blockDim.x) {
-        const int j = idx / DH, c = idx % DH;
-        const float v = j < len ? qkv[(int64_t)(base + j) * ld + 2 * d + h * DH + c] : 0.f;
-        const bf16_t hi = f2bf(v);
-        Vt[0][c][j] = hi;
-        Vt[1][c][j] = f2bf(v - bf2f(hi));
-    }
-    __syncthreads();
-    const int i0 = 32 * w;
-    const bool active = i0 < len;
-    const int nj = (len + 31) >> 5;
     const int lr = lane & 31, lh = lane >> 5;
-    f32x16 S[4];
-    float rmax[16], rsum[16];
-    if (active) {
-        bf16x8_t qh[4], ql[4];
-        const int qi = i0 + lr;
+    const int i0 = 32 * w, qi = i0 + lr;
+    const bool active = i0 < len;
+    float qv[4][8];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            float v[8];
-            load8f(qkv + (int64_t)(base + qi) * ld + h * DH + 16 * kk + 8 * lh, qi < len, scale, v);
-            split8(v, qh[kk], ql[kk]);
-        }
+    for (int kk = 0; kk < 4; ++kk)
+        load8f(qkv + (int64_t)(base + qi) * ld + h * DH + 16 * kk + 8 * lh, qi < len, scale, qv[kk]);
+    {
+        // thread: head columns c4..c4+3 of tokens j = tid/16 + 16u
+        const int c4 = (tid & 15) * 4;
+        float4 kv[8], vv[8];
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) S[jt][r] = 0.f;
-            if (jt < nj) {
-                const int kj = 32 * jt + lr;
-#pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    float v[8];
-                    bf16x8_t kh, kl;
-                    load8f(qkv + (int64_t)(base + kj) * ld + d + h * DH + 16 * kk + 8 * lh, kj < len, 1.f, v);
-                    split8(v, kh, kl);
-                    S[jt] = mfma3(qh[kk], ql[kk], kh, kl, S[jt]);
-                }
+        for (int u = 0; u < 8; ++u) {
+            const int j = (tid >> 4) + 16 * u;
+            const float* row = qkv + (int64_t)(base + j) * ld + d + h * DH + c4;
+            kv[u] = vv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (j < len) {
+                kv[u] = *reinterpret_cast<const float4*>(row);
+                vv[u] = *reinterpret_cast<const float4*>(row + d);
             }
         }
-        // masked softmax over keys, rows spread as in the accumulator layout
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = (tid >> 4) + 16 * u;
+            const float ke[4] = {kv[u].x, kv[u].y, kv[u].z, kv[u].w};
+            const float ve[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
+            bf16_t kh[4], kl[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                kh[q] = f2bf(ke[q]);
+                kl[q] = f2bf(ke[q] - bf2f(kh[q]));
+                const bf16_t vh = f2bf(ve[q]);
+                Vt[0][c4 + q][j] = vh;
+                Vt[1][c4 + q][j] = f2bf(ve[q] - bf2f(vh));
+            }
+            *reinterpret_cast<uint2*>(&Ks[0][j][c4]) = pack4(kh[0], kh[1], kh[2], kh[3]);
+            *reinterpret_cast<uint2*>(&Ks[1][j][c4]) = pack4(kl[0], kl[1], kl[2], kl[3]);
+        }
+    }
+    __syncthreads();
+    if (!active) return;  // no barrier follows
+    const int nj = (len + 31) >> 5;
+    bf16x8_t qh[4], ql[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) split8(qv[kk], qh[kk], ql[kk]);
+    f32x16 S[4];
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) S[jt][r] = 0.f;
+        if (jt < nj) {
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const bf16x8_t kh = *reinterpret_cast<const bf16x8_t*>(&Ks[0][32 * jt + lr][16 * kk + 8 * lh]);
+                const bf16x8_t kl = *reinterpret_cast<const bf16x8_t*>(&Ks[1][32 * jt + lr][16 * kk + 8 * lh]);
+                S[jt] = mfma3(kh, kl, qh[kk], ql[kk], S[jt]);
+            }
+        }
+    }
+    // softmax over the keys of this lane's query
+    float m = -INFINITY;
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            float m = -INFINITY;
-#pragma unroll
-            for (int jt = 0; jt < 4; ++jt)
-                if (jt < nj && 32 * jt + lr < len) m = fmaxf(m, S[jt][r]);
-            m = half_max(m);
-            float sum = 0.f;
-#pragma unroll
-            for (int jt = 0; jt < 4; ++jt) {
-                const float p = (jt < nj && 32 * jt + lr < len) ? expf(S[jt][r] - m) : 0.f;
-                S[jt][r] = p;
-                sum += p;
-            }
-            sum = half_sum(sum);
-            rmax[r] = m;
-            rsum[r] = sum;
-            const float inv = 1.f / sum;
-            const int il = 8 * (r >> 2) + 4 * lh + (r & 3);
-#pragma unroll
-            for (int jt = 0; jt < 4; ++jt) {
-                if (jt < nj) {
-                    const float p = S[jt][r] * inv;
-                    const bf16_t ph = f2bf(p);
-                    Ps[w][0][il][32 * jt + lr] = ph;
-                    Ps[w][1][il][32 * jt + lr] = f2bf(p - bf2f(ph));
-                }
-            }
+            const int j = 32 * jt + 8 * (r >> 2) + 4 * lh + (r & 3);
+            if (jt < nj && j < len) m = fmaxf(m, S[jt][r]);
         }
-    }
-    __syncthreads();
-    if (!active) return;
+    m = fmaxf(m, __shfl_xor(m, 32));
+    float sum = 0.f;
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int j = 32 * jt + 8 * (r >> 2) + 4 * lh + (r & 3);
+            const float p = (jt < nj && j < len) ? expf(S[jt][r] - m) : 0.f;
+            S[jt][r] = p;
+            sum += p;
+        }
+    sum += __shfl_xor(sum, 32);
+    const float inv = 1.f / sum;
+    // O^T = V^T P^T
     f32x16 O[2];
 #pragma unroll
     for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) O[dt][r] = 0.f;
-    for (int jk = 0; jk < 2 * nj; ++jk) {
-        const int jc = 16 * jk + 8 * lh;
-        const bf16x8_t ph = *reinterpret_cast<const bf16x8_t*>(&Ps[w][0][lr][jc]);
-        const bf16x8_t pl = *reinterpret_cast<const bf16x8_t*>(&Ps[w][1][lr][jc]);
 #pragma unroll
-        for (int dt = 0; dt < 2; ++dt) {
-            const bf16x8_t vh = *reinterpret_cast<const bf16x8_t*>(&Vt[0][32 * dt + lr][jc]);
-            const bf16x8_t vl = *reinterpret_cast<const bf16x8_t*>(&Vt[1][32 * dt + lr][jc]);
-            O[dt] = mfma3(ph, pl, vh, vl, O[dt]);
-        }
-    }
+    for (int jt = 0; jt < 4; ++jt) {
+        if (jt >= nj) break;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int i = i0 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        if (i < len) {
+        for (int kb = 0; kb < 2; ++kb) {
+            float pv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pv[e] = S[jt][8 * kb + e] * inv;
+            bf16x8_t ph, pl;
+            split8(pv, ph, pl);
+            const int jb = 32 * jt + 16 * kb + 4 * lh;
 #pragma unroll
             for (int dt = 0; dt < 2; ++dt) {
-                const float v = O[dt][r];
-                const bf16_t hi = f2bf(v);
-                const int64_t o = (int64_t)(base + i) * d + h * DH + 32 * dt + lr;
-                out[o] = hi;
-                outlo[o] = f2bf(v - bf2f(hi));
+                const bf16x8_t vh = ld_perm(&Vt[0][32 * dt + lr][0], jb);
+                const bf16x8_t vl = ld_perm(&Vt[1][32 * dt + lr][0], jb);
+                O[dt] = mfma3(vh, vl, ph, pl, O[dt]);
             }
-            if (lr == 0) lse[((int64_t)b * H + h) * LMAX + i] = rmax[r] + logf(rsum[r]);
         }
+    }
+    if (qi < len) {
+        // O^T accumulator: head column c = 32 dt + 8 q + 4 lh + (r mod 4), query qi
+        const int64_t o = (int64_t)(base + qi) * d + h * DH;
+#pragma unroll
+        for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                bf16_t hi[4], lo[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float v = O[dt][4 * q + e];
+                    hi[e] = f2bf(v);
+                    lo[e] = f2bf(v - bf2f(hi[e]));
+                }
+                const int c = 32 * dt + 8 * q + 4 * lh;
+                *reinterpret_cast<uint2*>(out + o + c) = pack4(hi[0], hi[1], hi[2], hi[3]);
+                *reinterpret_cast<uint2*>(outlo + o + c) = pack4(lo[0], lo[1], lo[2], lo[3]);
+            }
+        if (lh == 0) lse[((int64_t)b * H + h) * LMAX + qi] = m + logf(sum);
     }
 }
 
-// Backward.  With P = softmax(S), S = scale * Q K^T:
-//   D_i = sum_c dO_ic O_ic;  dS_ij = P_ij (dO_i . V_j - D_i)
-//   dQ_i = scale * sum_j dS_ij K_j;  dK_j = scale * sum_i dS_ij Q_i;  dV_j = sum_i P_ij dO_i
-// D comes from its own small kernel (thread per query row); the probabilities
-// are recomputed from the forward's log-sum-exp.
-__global__ void __launch_bounds__(LMAX) attn_bwd_rowdot(const int* __restrict__ cu, const bf16_t* __restrict__ out,
-                                                        const bf16_t* __restrict__ dout, float* __restrict__ D,
-                                                        int H, int d, int* __restrict__ snap, int nb) {
+// Backward (plain bf16 products: the backward feeds gradients only).  With
+// P = softmax(S), S = scale Q K^T and D_i = sum_c dO_ic O_ic:
+//   dS_ij = P_ij (dO_i . V_j - D_i)
+//   dQ_i = scale sum_j dS_ij K_j;  dK_j = scale sum_i dS_ij Q_i;  dV_j = sum_i P_ij dO_i
+// Phase 1, wave w on queries 32w..: S^T = K (scale Q)^T and dP^T = V dO^T from
+// row-major K, V in LDS; P^T = exp(S^T - lse) from the forward's log-sum-exp,
+// dS^T; both go to LDS for phase 2, and dQ^T = K^T dS^T takes dS^T straight from
+// the registers.  Phase 2, wave w on keys 32w..: dK = dS^T (scale Q) and
+// dV = P^T dO.
+__global__ void __launch_bounds__(256) attn_bwd_mfma(const float* __restrict__ qkv, const int* __restrict__ cu,
+                                                     const bf16_t* __restrict__ out, const bf16_t* __restrict__ dout,
+                                                     const float* __restrict__ lse, bf16_t* __restrict__ dqkv, int H,
+                                                     int d, float scale, int* __restrict__ snap, int nb) {
+    __shared__ __attribute__((aligned(16))) bf16_t Kr[LMAX][PADK];   // K
+    __shared__ __attribute__((aligned(16))) bf16_t Vr[LMAX][PADK];   // V
+    __shared__ __attribute__((aligned(16))) bf16_t Kt[DH][PADJ];     // K^T
+    __shared__ __attribute__((aligned(16))) bf16_t Qt[DH][PADJ];     // (scale Q)^T
+    __shared__ __attribute__((aligned(16))) bf16_t Gt[DH][PADJ];     // dO^T
+    __shared__ __attribute__((aligned(16))) bf16_t Pt[LMAX][PADJ];   // P^T
+    __shared__ __attribute__((aligned(16))) bf16_t Dst[LMAX][PADJ];  // dS^T
     if (snap && blockIdx.x == 0)
         for (int i = threadIdx.x; i <= nb; i += blockDim.x) snap[i] = cu[i];
-    const int b = blockIdx.x / H, h = blockIdx.x % H;
-    const int base = cu[b], len = cu[b + 1] - cu[b];
-    const int i = threadIdx.x;
-    if (i >= len) return;
-    const bf16_t* orow = out + (int64_t)(base + i) * d + h * DH;
-    const bf16_t* drow = dout + (int64_t)(base + i) * d + h * DH;
-    float acc = 0.f;
-    for (int c = 0; c < DH; ++c) acc = fmaf(bf2f(drow[c]), bf2f(orow[c]), acc);
-    D[((int64_t)b * H + h) * LMAX + i] = acc;
-}
-
-// Backward on the matrix cores (plain bf16 products: the backward feeds
-// gradients only).  Workgroup = (sequence, head); wave w owns query rows and
-// key rows 32w..32w+31.  Phase 1: each wave recomputes P = exp(S - lse) for
-// its query rows, dP = dO V^T, and dS = P (dP - D), and leaves P^T, dS^T and dS
-// in LDS.  Phase 2: dQ = scale dS K for its query rows, dK = dS^T (scale Q) and
-// dV = P^T dO for its key rows, from LDS-staged K^T, (scale Q)^T and dO^T.
-__global__ void __launch_bounds__(256) attn_bwd_mfma(const float* __restrict__ qkv, const int* __restrict__ cu,
-                                                     const bf16_t* __restrict__ dout, const float* __restrict__ lse,
-                                                     const float* __restrict__ Dv, bf16_t* __restrict__ dqkv, int H,
-                                                     int d, float scale) {
-    __shared__ __attribute__((aligned(16))) bf16_t Kt[DH][PADJ];
-    __shared__ __attribute__((aligned(16))) bf16_t Qt[DH][PADJ];
-    __shared__ __attribute__((aligned(16))) bf16_t Gt[DH][PADJ];
-    __shared__ __attribute__((aligned(16))) bf16_t Pt[LMAX][PADJ];
-    __shared__ __attribute__((aligned(16))) bf16_t Dst[LMAX][PADJ];
-    __shared__ __attribute__((aligned(16))) bf16_t Dsr[LMAX][PADJ];
     const int b = blockIdx.x / H, h = blockIdx.x % H;
     const int base = cu[b], len = cu[b + 1] - cu[b];
     const int ld = 3 * d;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int lr = lane & 31, lh = lane >> 5;
-    for (int idx = tid; idx < LMAX * DH; idx += blockDim.x) {
-        const int j = idx / DH, c = idx % DH;
-        const bool ok = j < len;
-        const float* row = qkv + (int64_t)(base + j) * ld + h * DH + c;
-        Qt[c][j] = f2bf(ok ? row[0] * scale : 0.f);
-        Kt[c][j] = f2bf(ok ? row[d] : 0.f);
-        Gt[c][j] = ok ? dout[(int64_t)(base + j) * d + h * DH + c] : (bf16_t)0;
-    }
-    const int i0 = 32 * w;
+    const int i0 = 32 * w, qi = i0 + lr;
     const bool active = i0 < len;
     const int nj = (len + 31) >> 5;
     const int64_t rb = ((int64_t)b * H + h) * LMAX;
+    // this lane's query: scale Q, dO and O at head columns 16 kk + 8 lh + 0..7
+    float qv[4][8];
+    u32x4_t gv[4], ov[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        const int c = h * DH + 16 * kk + 8 * lh;
+        load8f(qkv + (int64_t)(base + qi) * ld + c, qi < len, scale, qv[kk]);
+        gv[kk] = ov[kk] = u32x4_t{0u, 0u, 0u, 0u};
+        if (qi < len) {
+            gv[kk] = *reinterpret_cast<const u32x4_t*>(dout + (int64_t)(base + qi) * d + c);
+            ov[kk] = *reinterpret_cast<const u32x4_t*>(out + (int64_t)(base + qi) * d + c);
+        }
+    }
+    const float lq = qi < len ? lse[rb + qi] : 0.f;
+    {
+        const int c4 = (tid & 15) * 4;
+        float4 qs[8], ks[8], vs[8];
+        uint2 gs[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = (tid >> 4) + 16 * u;
+            const bool ok = j < len;
+            const float* row = qkv + (int64_t)(base + j) * ld + h * DH + c4;
+            qs[u] = ks[u] = vs[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            gs[u] = make_uint2(0, 0);
+            if (ok) {
+                qs[u] = *reinterpret_cast<const float4*>(row);
+                ks[u] = *reinterpret_cast<const float4*>(row + d);
+                vs[u] = *reinterpret_cast<const float4*>(row + 2 * d);
+                gs[u] = *reinterpret_cast<const uint2*>(dout + (int64_t)(base + j) * d + h * DH + c4);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = (tid >> 4) + 16 * u;
+            const float qe[4] = {qs[u].x, qs[u].y, qs[u].z, qs[u].w};
+            const float ke[4] = {ks[u].x, ks[u].y, ks[u].z, ks[u].w};
+            const float ve[4] = {vs[u].x, vs[u].y, vs[u].z, vs[u].w};
+            bf16_t kb[4], vb[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                kb[q] = f2bf(ke[q]);
+                vb[q] = f2bf(ve[q]);
+                Kt[c4 + q][j] = kb[q];
+                Qt[c4 + q][j] = f2bf(qe[q] * scale);
+            }
+            Gt[c4 + 0][j] = (bf16_t)(gs[u].x & 0xFFFFu);
+            Gt[c4 + 1][j] = (bf16_t)(gs[u].x >> 16);
+            Gt[c4 + 2][j] = (bf16_t)(gs[u].y & 0xFFFFu);
+            Gt[c4 + 3][j] = (bf16_t)(gs[u].y >> 16);
+            *reinterpret_cast<uint2*>(&Kr[j][c4]) = pack4(kb[0], kb[1], kb[2], kb[3]);
+            *reinterpret_cast<uint2*>(&Vr[j][c4]) = pack4(vb[0], vb[1], vb[2], vb[3]);
+        }
+    }
+    __syncthreads();
+    f32x16 dq[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dq[t][r] = 0.f;
     if (active) {
         bf16x8_t qa[4], ga[4];
-        const int qi = i0 + lr;
+        float dsum = 0.f;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-            float v[8];
             bf16x8_t lo;
-            load8f(qkv + (int64_t)(base + qi) * ld + h * DH + 16 * kk + 8 * lh, qi < len, scale, v);
-            split8(v, qa[kk], lo);
-            u32x4_t gv = {0u, 0u, 0u, 0u};
-            if (qi < len)
-                gv = *reinterpret_cast<const u32x4_t*>(dout + (int64_t)(base + qi) * d + h * DH + 16 * kk + 8 * lh);
-            ga[kk] = __builtin_bit_cast(bf16x8_t, gv);
-        }
-        float Lr[16], Dr[16];
+            split8(qv[kk], qa[kk], lo);
+            ga[kk] = __builtin_bit_cast(bf16x8_t, gv[kk]);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int i = i0 + 8 * (r >> 2) + 4 * lh + (r & 3);
-            Lr[r] = i < len ? lse[rb + i] : 0.f;
-            Dr[r] = i < len ? Dv[rb + i] : 0.f;
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t g2 = gv[kk][e], o2 = ov[kk][e];
+                dsum = fmaf(bf2f((bf16_t)(g2 & 0xFFFFu)), bf2f((bf16_t)(o2 & 0xFFFFu)), dsum);
+                dsum = fmaf(bf2f((bf16_t)(g2 >> 16)), bf2f((bf16_t)(o2 >> 16)), dsum);
+            }
         }
+        const float Dq = dsum + __shfl_xor(dsum, 32);
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
-            if (jt >= nj) continue;
+            if (jt >= nj) break;
             f32x16 S, G;
 #pragma unroll
             for (int r = 0; r < 16; ++r) S[r] = G[r] = 0.f;
-            const int kj = 32 * jt + lr;
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
-                float v[8];
-                bf16x8_t kb, vb, lo;
-                const float* krow = qkv + (int64_t)(base + kj) * ld + h * DH + 16 * kk + 8 * lh;
-                load8f(krow + d, kj < len, 1.f, v);
-                split8(v, kb, lo);
-                load8f(krow + 2 * d, kj < len, 1.f, v);
-                split8(v, vb, lo);
-                S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[kk], kb, S, 0, 0, 0);
-                G = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga[kk], vb, G, 0, 0, 0);
+                const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(&Kr[32 * jt + lr][16 * kk + 8 * lh]);
+                const bf16x8_t vb = *reinterpret_cast<const bf16x8_t*>(&Vr[32 * jt + lr][16 * kk + 8 * lh]);
+                S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qa[kk], S, 0, 0, 0);
+                G = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vb, ga[kk], G, 0, 0, 0);
             }
+            float dsv[16];
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                uint32_t pw[2], sw[2];
+            for (int r = 0; r < 16; ++r) {
+                const int j = 32 * jt + 8 * (r >> 2) + 4 * lh + (r & 3);
+                const bool ok = qi < len && j < len;
+                const float p = ok ? expf(S[r] - lq) : 0.f;
+                const float ds = ok ? p * (G[r] - Dq) : 0.f;
+                dsv[r] = ds;
+                Pt[j][qi] = f2bf(p);
+                Dst[j][qi] = f2bf(ds);
+            }
+            // dQ^T += K^T dS^T over this tile's keys
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int r = 4 * rr + q;
-                    const int i = i0 + 8 * rr + 4 * lh + q;
-                    const bool ok = i < len && kj < len;
-                    const float p = ok ? expf(S[r] - Lr[r]) : 0.f;
-                    const float ds = ok ? p * (G[r] - Dr[r]) : 0.f;
-                    const bf16_t pb = f2bf(p), sb = f2bf(ds);
-                    Dsr[i][kj] = sb;
-                    if (q & 1) {
-                        pw[q >> 1] |= (uint32_t)pb << 16;
-                        sw[q >> 1] |= (uint32_t)sb << 16;
-                    } else {
-                        pw[q >> 1] = pb;
-                        sw[q >> 1] = sb;
-                    }
-                }
-                const int ib = i0 + 8 * rr + 4 * lh;
-                *reinterpret_cast<uint2*>(&Pt[kj][ib]) = make_uint2(pw[0], pw[1]);
-                *reinterpret_cast<uint2*>(&Dst[kj][ib]) = make_uint2(sw[0], sw[1]);
+            for (int kb = 0; kb < 2; ++kb) {
+                u32x4_t sv;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    sv[e] = (uint32_t)f2bf(dsv[8 * kb + 2 * e]) | ((uint32_t)f2bf(dsv[8 * kb + 2 * e + 1]) << 16);
+                const bf16x8_t bs = __builtin_bit_cast(bf16x8_t, sv);
+                const int jb = 32 * jt + 16 * kb + 4 * lh;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+                    dq[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_perm(&Kt[32 * t + lr][0], jb), bs, dq[t], 0,
+                                                                    0, 0);
             }
         }
     }
     __syncthreads();
-    if (!active) return;
-    f32x16 dq[2], dk[2], dv[2];
+    if (!active) return;  // no barrier follows
+    if (qi < len) {
+        // dQ^T accumulator: head column c = 32 t + 8 q + 4 lh + (r mod 4), query qi
+        bf16_t* row = dqkv + (int64_t)(base + qi) * ld + h * DH;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                bf16_t o[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = f2bf(dq[t][4 * q + e] * scale);
+                *reinterpret_cast<uint2*>(row + 32 * t + 8 * q + 4 * lh) = pack4(o[0], o[1], o[2], o[3]);
+            }
+    }
+    f32x16 dk[2], dv[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dq[t][r] = dk[t][r] = dv[t][r] = 0.f;
+        for (int r = 0; r < 16; ++r) dk[t][r] = dv[t][r] = 0.f;
+    const int j0 = 32 * w;
     for (int k16 = 0; k16 < 2 * nj; ++k16) {
         const int kc = 16 * k16 + 8 * lh;
-        const bf16x8_t a_ds = *reinterpret_cast<const bf16x8_t*>(&Dsr[i0 + lr][kc]);  // dS rows (query block)
-        const bf16x8_t a_dst = *reinterpret_cast<const bf16x8_t*>(&Dst[i0 + lr][kc]); // dS^T rows (key block)
-        const bf16x8_t a_pt = *reinterpret_cast<const bf16x8_t*>(&Pt[i0 + lr][kc]);   // P^T rows (key block)
+        const bf16x8_t a_ds = *reinterpret_cast<const bf16x8_t*>(&Dst[j0 + lr][kc]);
+        const bf16x8_t a_p = *reinterpret_cast<const bf16x8_t*>(&Pt[j0 + lr][kc]);
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            const bf16x8_t bk = *reinterpret_cast<const bf16x8_t*>(&Kt[32 * t + lr][kc]);
             const bf16x8_t bq = *reinterpret_cast<const bf16x8_t*>(&Qt[32 * t + lr][kc]);
             const bf16x8_t bg = *reinterpret_cast<const bf16x8_t*>(&Gt[32 * t + lr][kc]);
-            dq[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_ds, bk, dq[t], 0, 0, 0);
-            dk[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_dst, bq, dk[t], 0, 0, 0);
-            dv[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_pt, bg, dv[t], 0, 0, 0);
+            dk[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_ds, bq, dk[t], 0, 0, 0);
+            dv[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_p, bg, dv[t], 0, 0, 0);
         }
     }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-        const int i = i0 + 8 * (r >> 2) + 4 * lh + (r & 3);  // query row for dq, key row for dk / dv
-        if (i >= len) continue;
-        bf16_t* row = dqkv + (int64_t)(base + i) * ld + h * DH;
+        const int j = j0 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        if (j >= len) continue;
+        bf16_t* row = dqkv + (int64_t)(base + j) * ld + h * DH;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             const int c = 32 * t + lr;
-            row[c] = f2bf(dq[t][r] * scale);
             row[d + c] = f2bf(dk[t][r]);
             row[2 * d + c] = f2bf(dv[t][r]);
         }
@@ -365,15 +446,15 @@ fo_status launch_attn_fwd(const float* qkv, const int* cu, bf16_t* out, bf16_t* 
 }
 
 fo_status launch_attn_bwd(const float* qkv, const int* cu, const bf16_t* out, const bf16_t* dout,
-                          const float* lse, float* Dws, bf16_t* dqkv, int B, int H, int d, hipStream_t s) {
+                          const float* lse, bf16_t* dqkv, int B, int H, int d, hipStream_t s) {
     FO_CHECK(d == H * DH, "attention: d=%d must equal heads*%d", d, DH);
     const float scale = 1.f / sqrtf((float)DH);
     ProfInfo pi;
     pi.kind = PROF_ATTN_BWD; pi.cu = cu; pi.B = B; pi.d = d;
-    const int h = prof_begin(s, "attn_bwd (rowdot + mfma)", pi);
+    const int h = prof_begin(s, "attn_bwd_mfma", pi);
     int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
-    hipLaunchKernelGGL(attn_bwd_rowdot, dim3(B * H), dim3(LMAX), 0, s, cu, out, dout, Dws, H, d, snap, B);
-    hipLaunchKernelGGL(attn_bwd_mfma, dim3(B * H), dim3(256), 0, s, qkv, cu, dout, lse, Dws, dqkv, H, d, scale);
+    hipLaunchKernelGGL(attn_bwd_mfma, dim3(B * H), dim3(256), 0, s, qkv, cu, out, dout, lse, dqkv, H, d, scale, snap,
+                       B);
     prof_end(h, s);
     FO_LAUNCHED();
     return FO_OK;

@@ -39,6 +39,10 @@ __device__ __forceinline__ uint16_t half_of(const uint4& v, int e) {
 
 __device__ __forceinline__ uint4 load8(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
 
+// Sixteen zero bytes in device memory (never written): the source of the
+// chunks of an aligned tile that lie outside the operand.
+__device__ __attribute__((aligned(16))) bf16_t kZero8[8];
+
 __device__ __forceinline__ uint4 load8_guarded(const bf16_t* p, int n_ok) {
     // first n_ok (0..8) elements from p, rest zero
     uint16_t h[8];
@@ -62,10 +66,12 @@ __device__ __forceinline__ uint4 load8_guarded(const bf16_t* p, int n_ok) {
 struct LdRK {
     int64_t off[NV];  // row offsets, -1 past the last row
     int kc;
-    bool vec;
+    bool vec;   // 16-byte aligned rows
+    bool full;  // all 128 rows of the tile exist (uniform over the workgroup)
     __device__ void init(const bf16_t* P, int64_t ld, int r0, int R, int tid) {
         kc = (tid & 7) * 8;
         vec = (ld % 8 == 0) && (((uintptr_t)P & 15) == 0);
+        full = r0 + BM <= R;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
             const int gr = r0 + (tid >> 3) + 32 * v;
@@ -74,7 +80,7 @@ struct LdRK {
     }
     __device__ void load(const bf16_t* P, int kb, int kend, uint4* r) const {
         const int k = kb + kc;
-        if (vec && kb + BK <= kend && off[NV - 1] >= 0) {  // interior tile: no checks
+        if (vec && full && kb + BK <= kend) {  // interior tile: no checks (a uniform branch)
 #pragma unroll
             for (int v = 0; v < NV; ++v) r[v] = load8(P + off[v] + k);
             return;
@@ -85,6 +91,17 @@ struct LdRK {
             else if (vec && k + 8 <= kend) r[v] = load8(P + off[v] + k);
             else r[v] = load8_guarded(P + off[v] + k, kend - k);
         }
+    }
+    // Aligned operands (16-byte rows, K and kend multiples of 8): every 8-element
+    // chunk is wholly inside or wholly outside, so one predicated 16-byte load
+    // per chunk covers the edges as well.
+    // Every load is issued (an outside chunk reads kZero8), so the number of
+    // loads in flight is static and the wait before the LDS store covers only
+    // the older register set.
+    __device__ void load_al(const bf16_t* P, int kb, int kend, uint4* r) const {
+        const int k = kb + kc;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) r[v] = load8(off[v] >= 0 && k < kend ? P + off[v] + k : kZero8);
     }
     __device__ void store(bf16_t* t, const uint4* r, int tid) const {
 #pragma unroll
@@ -111,7 +128,7 @@ struct LdKRBase {
 struct LdKR : LdKRBase {
     int64_t ld;
     int r0c, R;
-    bool vec;
+    bool vec, full;
     __device__ void init(const bf16_t* P, int64_t ld_, int r0, int R_, int tid) {
         ld = ld_;
         R = R_;
@@ -119,9 +136,10 @@ struct LdKR : LdKRBase {
         rc = (tid >> 5) * 8;
         r0c = r0 + rc;
         vec = (ld % 8 == 0) && (((uintptr_t)P & 15) == 0);
+        full = r0 + BM <= R;
     }
     __device__ void load(const bf16_t* P, int kb, int kend, uint4* r) const {
-        if (vec && kb + BK <= kend && r0c + 64 + 8 <= R) {  // interior tile: no checks
+        if (vec && full && kb + BK <= kend) {  // interior tile: no checks (a uniform branch)
 #pragma unroll
             for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -137,6 +155,17 @@ struct LdKR : LdKRBase {
                 if (k >= kend || rr >= R) o = make_uint4(0, 0, 0, 0);
                 else if (vec && rr + 8 <= R) o = load8(P + (int64_t)k * ld + rr);
                 else o = load8_guarded(P + (int64_t)k * ld + rr, R - rr);
+            }
+    }
+    // Aligned operands (16-byte rows, R a multiple of 8): predicated 16-byte
+    // loads, always issued as in LdRK::load_al.
+    __device__ void load_al(const bf16_t* P, int kb, int kend, uint4* r) const {
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int k = kb + 2 * kp + j, rr = r0c + 64 * q;
+                r[2 * q + j] = load8(k < kend && rr < R ? P + (int64_t)k * ld + rr : kZero8);
             }
     }
 };
@@ -305,24 +334,59 @@ __device__ __forceinline__ void loader_init(typename LoaderOf<MODE>::T& L, const
 }
 
 // ------------------------------------------------------------------ epilogue
-__device__ __forceinline__ float gelu_f(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
+// Standard normal CDF without a library erf: Phi(-|x|) = erfc(z) / 2 with
+// z = |x| / sqrt(2), and erfc(z) = t exp(-z^2 + P(t)), t = 1 / (1 + z / 2), P
+// the degree-9 Chebyshev fit of Numerical Recipes' erfcc (fractional error
+// below 1.2e-7 for every z >= 0).  In fp32 the GELU built on it is within
+// 4e-7 absolute and 2e-5 relative of the exact one over the whole real line.
+__device__ __forceinline__ float norm_cdf(float x) {
+    const float z = fabsf(x) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.5f, z, 1.f));
+    float p = 0.17087277f;
+    p = fmaf(p, t, -0.82215223f);
+    p = fmaf(p, t, 1.48851587f);
+    p = fmaf(p, t, -1.13520398f);
+    p = fmaf(p, t, 0.27886807f);
+    p = fmaf(p, t, -0.18628806f);
+    p = fmaf(p, t, 0.09678418f);
+    p = fmaf(p, t, 0.37409196f);
+    p = fmaf(p, t, 1.00002368f);
+    p = fmaf(p, t, -1.26551223f);
+    const float q = 0.5f * t * __expf(fmaf(-z, z, p));  // Phi(-|x|)
+    return x >= 0.f ? 1.f - q : q;
+}
+__device__ __forceinline__ float gelu_f(float x) { return x * norm_cdf(x); }
+// d/dx [x Phi(x)] = Phi(x) + x phi(x)
 __device__ __forceinline__ float gelu_grad(float x) {
-    float cdf = 0.5f * (1.f + erff(x * 0.70710678118654752f));
-    float pdf = 0.39894228040143268f * expf(-0.5f * x * x);
-    return cdf + x * pdf;
+    return fmaf(x, 0.39894228040143268f * __expf(-0.5f * x * x), norm_cdf(x));
 }
 
-__device__ __forceinline__ float epilogue(const GemmDesc& d, int row, int col, float v) {
-    if (d.bias) v += d.bias[col];
-    if (d.resid) v += d.resid[(int64_t)row * d.ldr + col];
+// The epilogue in two halves: epi_load fetches the per-element operands
+// (residual, ReLU mask, GELU input), epi_store applies activation, mask and
+// GELU' and stores, so that a thread can issue the loads of several rows
+// before it needs any of them.
+struct EpiIn {
+    float resid = 0.f, mask = 1.f, dpre = 0.f;
+};
+
+__device__ __forceinline__ EpiIn epi_load(const GemmDesc& d, int row, int col) {
+    EpiIn e;
+    if (d.resid) e.resid = d.resid[(int64_t)row * d.ldr + col];
+    if (d.mask) e.mask = bf2f(d.mask[(int64_t)row * d.ldm + col]);
+    if (d.dpre) e.dpre = bf2f(d.dpre[(int64_t)row * d.ldm + col]);
+    return e;
+}
+
+// v already holds bias and residual
+__device__ __forceinline__ float epi_store(const GemmDesc& d, int row, int col, float v, const EpiIn& e) {
     if (d.act == ACT_GELU) {
         if (d.pre) d.pre[(int64_t)row * d.ldm + col] = f2bf(v);
         v = gelu_f(v);
     } else if (d.act == ACT_RELU) {
         v = v > 0.f ? v : 0.f;
     }
-    if (d.mask && !(bf2f(d.mask[(int64_t)row * d.ldm + col]) > 0.f)) v = 0.f;
-    if (d.dpre) v *= gelu_grad(bf2f(d.dpre[(int64_t)row * d.ldm + col]));
+    if (d.mask && !(e.mask > 0.f)) v = 0.f;
+    if (d.dpre) v *= gelu_grad(e.dpre);
     if (d.Cf) d.Cf[(int64_t)row * d.ldcf + col] = v;
     if (d.Cb) {
         const bf16_t hi = f2bf(v);
@@ -332,8 +396,14 @@ __device__ __forceinline__ float epilogue(const GemmDesc& d, int row, int col, f
     return v;
 }
 
+__device__ __forceinline__ float epilogue(const GemmDesc& d, int row, int col, float v) {
+    const EpiIn e = epi_load(d, row, col);
+    if (d.bias) v += d.bias[col];
+    return epi_store(d, row, col, v + e.resid, e);
+}
+
 // ------------------------------------------------------------------ kernel
-template <int AM, int BMODE>
+template <int AM, int BMODE, bool AL>
 __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchunk) {
     // two K tiles (A and B each 128 x 72 bf16) = 72 KB; reused for the C tile
     __shared__ __attribute__((aligned(16))) bf16_t smem[2][2][BM * LDR];
@@ -350,10 +420,13 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     // The K range of this slice, over the concatenation of nseg segments
     // (segment s pairs (A, B), (A, B2), (A2, B) for s = 0, 1, 2), each padded
     // to a whole number of K tiles (the loaders zero-fill past K).
-    const int kseg = d.nseg > 1 ? (d.K + BK - 1) / BK * BK : d.K;
+    // With a device-side K (plain products only) the slices split the
+    // effective K, so that none of them runs over zero-filled tiles.
+    const int kseg = d.nseg > 1 ? (d.K + BK - 1) / BK * BK : Keff;
     const int ktot = d.nseg * kseg;
-    const int kbeg = blockIdx.z * kchunk;
-    const int kstop = min(ktot, kbeg + kchunk);
+    const int kc = (d.Kdev && d.splits > 1) ? ((ktot + d.splits - 1) / d.splits + BK - 1) / BK * BK : kchunk;
+    const int kbeg = blockIdx.z * kc;
+    const int kstop = min(ktot, kbeg + kc);
     const int nk = kstop > kbeg ? (kstop - kbeg + BK - 1) / BK : 0;
 
     typename LoaderOf<AM>::T la;
@@ -375,9 +448,19 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     // the (segment, offset) of the next tile to load, advanced without division;
     // segments are whole tiles long, so a tile never straddles two
     int ld_seg = kseg > 0 ? kbeg / kseg : 0, ld_kk = kbeg - ld_seg * kseg;
+    int ld_t = 0;  // index (within this slice) of the next tile to load
     auto load_tile = [&](uint4* ra, uint4* rb) {
-        la.load(ld_seg == 2 ? d.A2 : d.A, ld_kk, Keff, ra);
-        lb.load(ld_seg == 1 ? d.B2 : d.B, ld_kk, Keff, rb);
+        if constexpr (AL) {
+            // a prefetch past the slice's last tile reads zeros only: its
+            // (segment, offset) may name a low part that does not exist
+            const int ke = ld_t < nk ? Keff : 0;
+            la.load_al(ld_seg == 2 ? d.A2 : d.A, ld_kk, ke, ra);
+            lb.load_al(ld_seg == 1 ? d.B2 : d.B, ld_kk, ke, rb);
+        } else {
+            la.load(ld_seg == 2 ? d.A2 : d.A, ld_kk, Keff, ra);
+            lb.load(ld_seg == 1 ? d.B2 : d.B, ld_kk, Keff, rb);
+        }
+        ++ld_t;
         ld_kk += BK;
         if (ld_kk >= kseg) {
             ld_kk -= kseg;
@@ -404,30 +487,37 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
         }
     };
 
-    if (nk > 0) load_tile(ra0, rb0);
-    if (nk > 1) load_tile(ra1, rb1);
+    // The aligned variant issues every prefetch, also past the last tile (those
+    // read zeros or operand memory and are never stored): with a static number
+    // of loads in flight, each wait covers exactly the register set it needs.
+    if (AL || nk > 0) load_tile(ra0, rb0);
+    if (AL || nk > 1) load_tile(ra1, rb1);
     if (nk > 0) {
         la.store(smem[0][0], ra0, tid);
         lb.store(smem[0][1], rb0, tid);
     }
     __syncthreads();
-    for (int t = 0; t < nk; t += 2) {
-        // even step: compute tile t from buffer 0, stage tile t+1 (set 1) into buffer 1
-        if (t + 2 < nk) load_tile(ra0, rb0);
+    // two K tiles per trip and no exit inside the body (an exit between the
+    // halves makes the compiler keep the accumulators in two register sets)
+    int t = 0;
+    for (; t + 1 < nk; t += 2) {
+        // even half: compute tile t from buffer 0, stage tile t+1 (set 1) into buffer 1
+        if (AL || t + 2 < nk) load_tile(ra0, rb0);
         compute(smem[0][0], smem[0][1]);
-        if (t + 1 < nk) {
-            la.store(smem[1][0], ra1, tid);
-            lb.store(smem[1][1], rb1, tid);
-        }
+        la.store(smem[1][0], ra1, tid);
+        lb.store(smem[1][1], rb1, tid);
         __syncthreads();
-        if (t + 1 >= nk) break;
-        // odd step: compute tile t+1 from buffer 1, stage tile t+2 (set 0) into buffer 0
-        if (t + 3 < nk) load_tile(ra1, rb1);
+        // odd half: compute tile t+1 from buffer 1, stage tile t+2 (set 0) into buffer 0
+        if (AL || t + 3 < nk) load_tile(ra1, rb1);
         compute(smem[1][0], smem[1][1]);
         if (t + 2 < nk) {
             la.store(smem[0][0], ra0, tid);
             lb.store(smem[0][1], rb0, tid);
         }
+        __syncthreads();
+    }
+    if (t < nk) {  // odd tile count: the last tile is in buffer 0
+        compute(smem[0][0], smem[0][1]);
         __syncthreads();
     }
 
@@ -450,14 +540,28 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     const int c = tid & (BN - 1), col = n0 + c;
     float csum = 0.f;
     if (col < d.N) {
-        for (int lr = tid >> 7; lr < BM; lr += 2) {
-            const int row = m0 + lr;
-            if (row >= M) break;
-            const float v = Cs[lr * BN + c];
-            if (d.splits > 1)
-                d.ws[((int64_t)blockIdx.z * d.M + row) * d.N + col] = v;
-            else
-                csum += epilogue(d, row, col, v);
+        if (d.splits > 1) {
+            for (int lr = tid >> 7; lr < BM; lr += 2) {
+                const int row = m0 + lr;
+                if (row >= M) break;
+                d.ws[((int64_t)blockIdx.z * d.M + row) * d.N + col] = Cs[lr * BN + c];
+            }
+        } else {
+            const float bcol = d.bias ? d.bias[col] : 0.f;
+            // eight rows per batch: their operand loads are in flight together
+            for (int lr0 = tid >> 7; lr0 < BM && m0 + lr0 < M; lr0 += 16) {
+                EpiIn e[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int row = m0 + lr0 + 2 * u;
+                    if (row < M) e[u] = epi_load(d, row, col);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int lr = lr0 + 2 * u, row = m0 + lr;
+                    if (row < M) csum += epi_store(d, row, col, Cs[lr * BN + c] + bcol + e[u].resid, e[u]);
+                }
+            }
         }
     }
     if (d.colpart) {  // uniform; the two row halves of a column meet in LDS
@@ -503,7 +607,7 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
     }
 }
 
-template <int AM, int BMODE>
+template <int AM, int BMODE, bool AL = false>
 void launch(const GemmDesc& d, int kchunk, hipStream_t s) {
     // kernel names as the profilers print them
     static const char* names[6][6] = {};
@@ -520,7 +624,7 @@ void launch(const GemmDesc& d, int kchunk, hipStream_t s) {
     GemmDesc dd = d;
     dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
-    hipLaunchKernelGGL((gemm_kernel<AM, BMODE>), grid, dim3(NT), 0, s, dd, kchunk);
+    hipLaunchKernelGGL((gemm_kernel<AM, BMODE, AL>), grid, dim3(NT), 0, s, dd, kchunk);
     prof_end(h, s);
 }
 
@@ -550,10 +654,19 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
         kchunk = (int)cdiv(cdiv(ktot, d.splits), BK) * BK;
     }
     const int a = d.amode, b = d.bmode;
-    if (a == OP_RK && b == OP_RK) launch<OP_RK, OP_RK>(d, kchunk, s);
-    else if (a == OP_RK && b == OP_KR) launch<OP_RK, OP_KR>(d, kchunk, s);
-    else if (a == OP_KR && b == OP_KR) launch<OP_KR, OP_KR>(d, kchunk, s);
-    else if (a == OP_KR && b == OP_RK) launch<OP_KR, OP_RK>(d, kchunk, s);
+    // aligned variant: every contiguous dimension a multiple of 8 and 16-byte rows
+    auto al16 = [](const void* p) { return p == nullptr || ((uintptr_t)p & 15) == 0; };
+    auto op_aligned = [&](int mode, const bf16_t* P, const bf16_t* P2, int64_t ld, int rows) {
+        if (ld % 8 != 0 || !al16(P) || !al16(P2)) return false;
+        return mode == OP_RK ? (d.K % 8 == 0 && !d.Kdev) : (rows % 8 == 0);
+    };
+    // (a k-major A with a device-side row bound may end inside an 8-row chunk)
+    const bool al = (a == OP_RK || a == OP_KR) && (b == OP_RK || b == OP_KR) && !(a == OP_KR && d.Mdev) &&
+                    op_aligned(a, d.A, d.A2, d.lda, d.M) && op_aligned(b, d.B, d.B2, d.ldb, d.N);
+    if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(d, kchunk, s) : launch<OP_RK, OP_RK>(d, kchunk, s);
+    else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KR, true>(d, kchunk, s) : launch<OP_RK, OP_KR>(d, kchunk, s);
+    else if (a == OP_KR && b == OP_KR) al ? launch<OP_KR, OP_KR, true>(d, kchunk, s) : launch<OP_KR, OP_KR>(d, kchunk, s);
+    else if (a == OP_KR && b == OP_RK) al ? launch<OP_KR, OP_RK, true>(d, kchunk, s) : launch<OP_KR, OP_RK>(d, kchunk, s);
     else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(d, kchunk, s);
     else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(d, kchunk, s);
     else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(d, kchunk, s);

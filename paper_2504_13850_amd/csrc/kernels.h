@@ -30,7 +30,7 @@ fo_status launch_cast_bf16(const float* x, bf16_t* y, bf16_t* ylo, int64_t n, hi
 fo_status launch_attn_fwd(const float* qkv, const int* cu, bf16_t* out, bf16_t* outlo, float* lse, int B, int H,
                           int d, hipStream_t s);
 fo_status launch_attn_bwd(const float* qkv, const int* cu, const bf16_t* out, const bf16_t* dout,
-                          const float* lse, float* Dws, bf16_t* dqkv, int B, int H, int d, hipStream_t s);
+                          const float* lse, bf16_t* dqkv, int B, int H, int d, hipStream_t s);
 
 // ------------------------------------------------------------------ k_common.hip
 // mean cross-entropy of logits z [B][C] and dz = (softmax - onehot)/B

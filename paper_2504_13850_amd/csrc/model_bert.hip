@@ -44,7 +44,7 @@ struct Plan {
     bf16_t* Xlo[NL + 1];  // low parts (layer 0's input is exactly bf16: none)
     float* Xf[NL + 1];
     LayerAct a[NL];
-    float *dY[2], *du2f, *dHf, *du1f, *Dws;
+    float *dY[2], *du2f, *dHf, *du1f;
     bf16_t *du2b, *dA1, *du1b, *dO, *dqkv;
     float *splitws, *colws, *lnpart, *slws;
     int split_qkv, split_o, split_f1, split_f2;
@@ -254,7 +254,6 @@ size_t ws_bytes(const fo_model* m) {
     }
     add(4 * R * D); add(4 * R * D);                 // dY[2]
     add(4 * R * D); add(4 * R * D); add(4 * R * D); // du2f, dHf, du1f
-    add(4 * B * NH * L);                            // Dws
     add(2 * R * D); add(2 * R * FF); add(2 * R * D); add(2 * R * D); add(2 * R * 3 * D);
     const int K = (int)R;
     size_t sw = 0;
@@ -333,7 +332,6 @@ fo_status init(fo_model* m) {
     P->du2f = a.take<float>(R * D);
     P->dHf = a.take<float>(R * D);
     P->du1f = a.take<float>(R * D);
-    P->Dws = a.take<float>(B * NH * L);
     P->du2b = a.take<bf16_t>(R * D);
     P->dA1 = a.take<bf16_t>(R * FF);
     P->du1b = a.take<bf16_t>(R * D);
@@ -541,7 +539,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             w.splits = P->split_o; w.ws = P->splitws;
             TRY(gemm(w, s));
         }
-        TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, P->Dws, P->dqkv, B, NH, D, s));
+        TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, P->dqkv, B, NH, D, s));
         // input projection: dX = du1 + dqkv Wqkv (skipped for the first server layer), dWqkv, dbqkv
         if (l > 0) {
             GemmDesc d;
