@@ -7,46 +7,90 @@
 
 namespace fo {
 
+// Streaming shape shared by the kernels below: a block pass covers SCHUNK
+// 16-byte vectors (SU per thread, 256 apart, so each load instruction of a
+// wave reads 1 KiB contiguous); every load of a pass is issued before the
+// first use, and full passes carry no per-lane bounds test.
+constexpr int SU = 4;
+constexpr int64_t SCHUNK = 256 * SU;
+
+__device__ __forceinline__ f32x4 lerp4(f32x4 a, f32x4 b, float w) {
+    a.x = __builtin_fmaf(w, b.x - a.x, a.x);
+    a.y = __builtin_fmaf(w, b.y - a.y, a.y);
+    a.z = __builtin_fmaf(w, b.z - a.z, a.z);
+    a.w = __builtin_fmaf(w, b.w - a.w, a.w);
+    return a;
+}
+
 // ------------------------------------------------------------------ aggregation
 // g <- g + w (l - g), one FMA per element after the difference, so w = 0 and
 // l == g leave g bit for bit.
 __global__ void __launch_bounds__(256) agg_lerp_kernel(float* __restrict__ g, const float* __restrict__ l,
                                                        int64_t n4, int64_t n, float w) {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    int64_t stride = (int64_t)gridDim.x * blockDim.x;
     f32x4* g4 = reinterpret_cast<f32x4*>(g);
     const f32x4* l4 = reinterpret_cast<const f32x4*>(l);
-    for (; i < n4; i += stride) {
-        f32x4 a = g4[i];
-        f32x4 b = __builtin_nontemporal_load(&l4[i]);
-        a.x = __builtin_fmaf(w, b.x - a.x, a.x);
-        a.y = __builtin_fmaf(w, b.y - a.y, a.y);
-        a.z = __builtin_fmaf(w, b.z - a.z, a.z);
-        a.w = __builtin_fmaf(w, b.w - a.w, a.w);
-        g4[i] = a;
+    const int tid = threadIdx.x;
+    const int64_t step = (int64_t)gridDim.x * SCHUNK;
+    int64_t base = (int64_t)blockIdx.x * SCHUNK;
+    for (; base + SCHUNK <= n4; base += step) {
+        f32x4 a[SU], b[SU];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            a[u] = __builtin_nontemporal_load(&g4[base + 256 * u + tid]);
+            b[u] = __builtin_nontemporal_load(&l4[base + 256 * u + tid]);
+        }
+#pragma unroll
+        for (int u = 0; u < SU; ++u) __builtin_nontemporal_store(lerp4(a[u], b[u], w), &g4[base + 256 * u + tid]);
+    }
+    if (base < n4) {  // the partial last pass
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int64_t i = base + 256 * u + tid;
+            if (i < n4) g4[i] = lerp4(g4[i], l4[i], w);
+        }
     }
     // tail (n not a multiple of 4): handled by the first threads
     int64_t t = n4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t < n) g[t] = __builtin_fmaf(w, l[t] - g[t], g[t]);
 }
 
-// Several arrivals applied in order to each element while it sits in a register.
+// Several arrivals applied in order to each element while it sits in a
+// register; the next arrival's vectors load while the current one is applied.
+constexpr int MU = 2;
+
 __global__ void __launch_bounds__(256) agg_lerp_multi_kernel(float* __restrict__ g, AggTable tab, int64_t n4,
                                                              int64_t n) {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    int64_t stride = (int64_t)gridDim.x * blockDim.x;
     f32x4* g4 = reinterpret_cast<f32x4*>(g);
-    for (; i < n4; i += stride) {
-        f32x4 a = g4[i];
-        for (int m = 0; m < tab.count; ++m) {
-            const f32x4 b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(tab.local[m]) + i);
-            const float w = tab.w[m];
-            a.x = __builtin_fmaf(w, b.x - a.x, a.x);
-            a.y = __builtin_fmaf(w, b.y - a.y, a.y);
-            a.z = __builtin_fmaf(w, b.z - a.z, a.z);
-            a.w = __builtin_fmaf(w, b.w - a.w, a.w);
+    const int tid = threadIdx.x;
+    const int64_t chunk = 256 * MU;
+    for (int64_t base = (int64_t)blockIdx.x * chunk; base < n4; base += (int64_t)gridDim.x * chunk) {
+        int64_t idx[MU];
+        bool ok[MU];
+        f32x4 a[MU], b[MU];
+#pragma unroll
+        for (int u = 0; u < MU; ++u) {
+            idx[u] = base + 256 * u + tid;
+            ok[u] = idx[u] < n4;
+            if (!ok[u]) idx[u] = 0;  // in range; the result is not stored
+            a[u] = g4[idx[u]];
+            b[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(tab.local[0]) + idx[u]);
         }
-        g4[i] = a;
+        for (int m = 0; m < tab.count; ++m) {
+            f32x4 c[MU];
+            const int mn = m + 1 < tab.count ? m + 1 : m;
+#pragma unroll
+            for (int u = 0; u < MU; ++u)
+                c[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(tab.local[mn]) + idx[u]);
+            const float w = tab.w[m];
+#pragma unroll
+            for (int u = 0; u < MU; ++u) {
+                a[u] = lerp4(a[u], b[u], w);
+                b[u] = c[u];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < MU; ++u)
+            if (ok[u]) g4[idx[u]] = a[u];
     }
     int64_t t = n4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t < n) {
@@ -56,12 +100,13 @@ __global__ void __launch_bounds__(256) agg_lerp_multi_kernel(float* __restrict__
     }
 }
 
-static int stream_grid(int64_t n4) {
-    // 256 CUs x 8 blocks of 256 threads saturate HBM; small vectors use fewer.
-    int64_t blocks = cdiv(n4 > 0 ? n4 : 1, 256);
+static int stream_grid(int64_t n4, int64_t chunk) {
+    // 256 CUs x 8 blocks of 256 threads keep HBM busy; small vectors use fewer.
+    int64_t blocks = cdiv(n4 > 0 ? n4 : 1, chunk);
     if (blocks > 2048) blocks = 2048;
     return (int)blocks;
 }
+static int stream_grid(int64_t n4) { return stream_grid(n4, SCHUNK); }
 
 fo_status launch_agg_lerp(float* g, const float* l, int64_t n, float w, hipStream_t s) {
     if (n == 0) return FO_OK;
@@ -77,7 +122,7 @@ fo_status launch_agg_lerp(float* g, const float* l, int64_t n, float w, hipStrea
 fo_status launch_agg_lerp_multi(float* g, const AggTable& tab, int64_t n, hipStream_t s) {
     if (n == 0 || tab.count == 0) return FO_OK;
     int64_t n4 = n / 4;
-    int grid = stream_grid(n4);
+    int grid = stream_grid(n4, 256 * MU);
     hipLaunchKernelGGL(agg_lerp_multi_kernel, dim3(grid), dim3(256), 0, s, g, tab, n4, n);
     FO_LAUNCHED();
     return FO_OK;
@@ -87,39 +132,66 @@ fo_status launch_agg_lerp_multi(float* g, const AggTable& tab, int64_t n, hipStr
 // theta <- theta - lr * g; optional momentum v <- mu v + g, theta <- theta - lr v;
 // optional bf16 shadow of theta for the MFMA GEMM operands.
 template <bool MOM, bool SHADOW>
+__device__ __forceinline__ void sgd_store(float* p, float* v, bf16_t* w16, bf16_t* w16lo, int64_t i, f32x4 a,
+                                          f32x4 d, f32x4 m, float lr, float mu) {
+    if (MOM) {
+        m.x = __builtin_fmaf(mu, m.x, d.x);
+        m.y = __builtin_fmaf(mu, m.y, d.y);
+        m.z = __builtin_fmaf(mu, m.z, d.z);
+        m.w = __builtin_fmaf(mu, m.w, d.w);
+        __builtin_nontemporal_store(m, reinterpret_cast<f32x4*>(v) + i);
+        d = m;
+    }
+    a.x = __builtin_fmaf(-lr, d.x, a.x);
+    a.y = __builtin_fmaf(-lr, d.y, a.y);
+    a.z = __builtin_fmaf(-lr, d.z, a.z);
+    a.w = __builtin_fmaf(-lr, d.w, a.w);
+    __builtin_nontemporal_store(a, reinterpret_cast<f32x4*>(p) + i);
+    if (SHADOW) {
+        const bf16_t hx = f2bf(a.x), hy = f2bf(a.y), hz = f2bf(a.z), hw = f2bf(a.w);
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        u32x2 h, lo;
+        h.x = (uint32_t)hx | ((uint32_t)hy << 16);
+        h.y = (uint32_t)hz | ((uint32_t)hw << 16);
+        lo.x = (uint32_t)f2bf(a.x - bf2f(hx)) | ((uint32_t)f2bf(a.y - bf2f(hy)) << 16);
+        lo.y = (uint32_t)f2bf(a.z - bf2f(hz)) | ((uint32_t)f2bf(a.w - bf2f(hw)) << 16);
+        __builtin_nontemporal_store(h, reinterpret_cast<u32x2*>(w16) + i);
+        __builtin_nontemporal_store(lo, reinterpret_cast<u32x2*>(w16lo) + i);
+    }
+}
+
+// ------------------------------------------------------------------ SGD
+// theta <- theta - lr * g; optional momentum v <- mu v + g, theta <- theta - lr v;
+// optional bf16 shadow (high and low parts) of theta for the MFMA GEMM operands.
+template <bool MOM, bool SHADOW>
 __global__ void __launch_bounds__(256) sgd_kernel(float* __restrict__ p, const float* __restrict__ g,
                                                   float* __restrict__ v, bf16_t* __restrict__ w16,
                                                   bf16_t* __restrict__ w16lo, int64_t n4, int64_t n, float lr,
                                                   float mu) {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (; i < n4; i += stride) {
-        float4 a = reinterpret_cast<float4*>(p)[i];
-        float4 d = reinterpret_cast<const float4*>(g)[i];
-        if (MOM) {
-            float4 m = reinterpret_cast<float4*>(v)[i];
-            m.x = __builtin_fmaf(mu, m.x, d.x);
-            m.y = __builtin_fmaf(mu, m.y, d.y);
-            m.z = __builtin_fmaf(mu, m.z, d.z);
-            m.w = __builtin_fmaf(mu, m.w, d.w);
-            reinterpret_cast<float4*>(v)[i] = m;
-            d = m;
+    const f32x4* p4 = reinterpret_cast<const f32x4*>(p);
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(g);
+    const f32x4* v4 = reinterpret_cast<const f32x4*>(v);
+    const int tid = threadIdx.x;
+    const int64_t step = (int64_t)gridDim.x * SCHUNK;
+    int64_t base = (int64_t)blockIdx.x * SCHUNK;
+    for (; base + SCHUNK <= n4; base += step) {
+        f32x4 a[SU], d[SU], m[SU];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int64_t i = base + 256 * u + tid;
+            a[u] = __builtin_nontemporal_load(p4 + i);
+            d[u] = __builtin_nontemporal_load(g4 + i);
+            if (MOM) m[u] = __builtin_nontemporal_load(v4 + i);
         }
-        a.x = __builtin_fmaf(-lr, d.x, a.x);
-        a.y = __builtin_fmaf(-lr, d.y, a.y);
-        a.z = __builtin_fmaf(-lr, d.z, a.z);
-        a.w = __builtin_fmaf(-lr, d.w, a.w);
-        reinterpret_cast<float4*>(p)[i] = a;
-        if (SHADOW) {
-            const bf16_t hx = f2bf(a.x), hy = f2bf(a.y), hz = f2bf(a.z), hw = f2bf(a.w);
-            uint2 h;
-            h.x = (uint32_t)hx | ((uint32_t)hy << 16);
-            h.y = (uint32_t)hz | ((uint32_t)hw << 16);
-            reinterpret_cast<uint2*>(w16)[i] = h;
-            uint2 lo;
-            lo.x = (uint32_t)f2bf(a.x - bf2f(hx)) | ((uint32_t)f2bf(a.y - bf2f(hy)) << 16);
-            lo.y = (uint32_t)f2bf(a.z - bf2f(hz)) | ((uint32_t)f2bf(a.w - bf2f(hw)) << 16);
-            reinterpret_cast<uint2*>(w16lo)[i] = lo;
+#pragma unroll
+        for (int u = 0; u < SU; ++u)
+            sgd_store<MOM, SHADOW>(p, v, w16, w16lo, base + 256 * u + tid, a[u], d[u], m[u], lr, mu);
+    }
+    if (base < n4) {  // the partial last pass
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int64_t i = base + 256 * u + tid;
+            if (i < n4) sgd_store<MOM, SHADOW>(p, v, w16, w16lo, i, p4[i], g4[i], MOM ? v4[i] : f32x4{}, lr, mu);
         }
     }
     int64_t t = n4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
