@@ -46,6 +46,11 @@ def parse():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=2)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a 1 GiB device-to-device copy (the HBM counter calibration kernel)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench with "
+                         "--calib-copy into the HBM traffic summary (JSON on stdout)")
     return ap.parse_args()
 
 
@@ -70,6 +75,95 @@ def cpu_baseline(cid, sample_steps):
     dt = time.perf_counter() - t0
     return {"value": round(Bs * sample_steps / dt, 3), "unit": "samples/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{sample_steps} fp32 oracle steps at batch {Bs} of the same workload ({dt:.1f} s)"}
+
+
+# ---------------------------------------------------------------- HBM traffic
+# The kernels whose HBM bytes are taken from rocprofv3 counters: (name prefix in
+# the profiler's kernel names, the sources that define them).
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_bert_step.txt")
+TRAFFIC_KERNELS = {
+    "gemm_kernel<0, 0>": ("gemm_kernel<0, 0,", ["paper_2504_13850_amd/csrc/k_gemm.hip",
+                                                 "paper_2504_13850_amd/csrc/gemm.h"]),
+    "agg_lerp_kernel": ("agg_lerp_kernel(", ["paper_2504_13850_amd/csrc/k_update.hip"]),
+}
+CALIB_BYTES = 1 << 30
+
+
+def source_hash(files):
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def summarize_pmc(fetch_csv, write_csv):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the traffic kernels, scaled
+    by what the same counters read for the 1 GiB calibration copy."""
+    import csv
+    import statistics
+
+    def read(path, counter):
+        rows = {}
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                key = r["Dispatch_Id"]
+                rows[key] = (r["Kernel_Name"], rows.get(key, (None, 0.0))[1] + float(r["Counter_Value"]))
+        return list(rows.values())
+
+    out = {"counters_kib_per_dispatch": {}, "calibration": {}}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = read(path, counter)
+        copies = [v for n, v in rows if "copyBuffer" in n and v * 1024 > CALIB_BYTES / 2]
+        if not copies:
+            raise SystemExit(f"no calibration copy found in {path}")
+        factor = (CALIB_BYTES / 1024) / statistics.mean(copies)
+        out["calibration"][counter] = {"copy_bytes": CALIB_BYTES, "dispatches": len(copies),
+                                       "mean_kib": round(statistics.mean(copies), 1), "factor": round(factor, 5)}
+        for name, (prefix, _) in TRAFFIC_KERNELS.items():
+            vals = [v for n, v in rows if prefix in n]
+            if name == "agg_lerp_kernel":  # the 1 GiB sweep calls only
+                vals = [v for v in vals if v * 1024 > (1 << 29)]
+            if vals:
+                out["counters_kib_per_dispatch"].setdefault(name, {})[counter] = {
+                    "dispatches": len(vals), "mean_kib": round(statistics.mean(vals), 1)}
+    kern = {}
+    for name, (prefix, files) in TRAFFIC_KERNELS.items():
+        c = out["counters_kib_per_dispatch"].get(name, {})
+        if "FETCH_SIZE" not in c or "WRITE_SIZE" not in c:
+            continue
+        rd = c["FETCH_SIZE"]["mean_kib"] * 1024 * out["calibration"]["FETCH_SIZE"]["factor"]
+        wr = c["WRITE_SIZE"]["mean_kib"] * 1024 * out["calibration"]["WRITE_SIZE"]["factor"]
+        kern[name] = {"read_bytes_per_launch": round(rd), "write_bytes_per_launch": round(wr),
+                      "bytes_per_launch": round(rd + wr), "source_sha256": source_hash(files)}
+    out["kernels"] = kern
+    return out
+
+
+def traffic_for(name):
+    """HBM bytes per launch from the committed counter summary, or None when it
+    is missing or the kernel's source changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            summary = json.load(fh)
+        k = summary["kernels"][name]
+        if k["source_sha256"] != source_hash(TRAFFIC_KERNELS[name][1]):
+            return None
+        return k["bytes_per_launch"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def calib_copy(torch):
+    src = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def bench_aggregate(A, torch, stream):
@@ -112,6 +206,9 @@ def bench_aggregate(A, torch, stream):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        print(json.dumps(summarize_pmc(*args.summarize_pmc), indent=1))
+        return
     if args.gpus != 1:
         sys.stderr.write("bench.py measures one GPU only: this build has no multi-GPU path "
                          f"(asked for --gpus {args.gpus}).\n")
@@ -203,6 +300,11 @@ def main():
                for s in sorted(stats, key=lambda s: -s["ms"])]
 
     agg = bench_aggregate(A, torch, stream)
+    t_agg = traffic_for("agg_lerp_kernel")
+    agg["traffic"] = t_agg
+    agg["traffic_frac_of_algorithmic"] = round(t_agg / agg["bytes_per_call"], 4) if t_agg else None
+    if args.calib_copy:
+        calib_copy(torch)
     A.fo_queues_destroy(q)
     A.fo_model_destroy(model)
 
@@ -230,7 +332,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": dom["name"], "achieved": round(dom_tflops, 1),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4),
                      "launches": dom["launches"], "avg_launch_us": round(dom["ms"] / dom["launches"] * 1e3, 2),
-                     "traffic": None},
+                     "traffic": traffic_for(dom["name"])},
         "aggregate": agg,
         "kernels": kernels[:12],
         "host_wall_ms_per_step": round(wall / args.steps * 1e3, 3),

@@ -9,6 +9,8 @@
 //
 // Both passes run on the matrix cores (v_mfma_f32_32x32x16_bf16) with the
 // whole (sequence, head) resident in LDS: sequences are at most 128 tokens.
+#include <hip/hip_ext.h>
+
 #include "kernels.h"
 #include "prof.h"
 
@@ -436,11 +438,12 @@ fo_status launch_attn_fwd(const float* qkv, const int* cu, bf16_t* out, bf16_t* 
     FO_CHECK(d == H * DH, "attention: d=%d must equal heads*%d", d, DH);
     ProfInfo pi;
     pi.kind = PROF_ATTN_FWD; pi.cu = cu; pi.B = B; pi.d = d;
-    const int h = prof_begin(s, "attn_fwd_mfma", pi);
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext("attn_fwd_mfma", pi, &ea, &eb);
     int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
-    hipLaunchKernelGGL(attn_fwd_mfma, dim3(B * H), dim3(256), 0, s, qkv, cu, out, outlo, lse, H, d,
-                       1.f / sqrtf((float)DH), snap, B);
-    prof_end(h, s);
+    hipExtLaunchKernelGGL(attn_fwd_mfma, dim3(B * H), dim3(256), 0, s, ea, eb, 0, qkv, cu, out, outlo, lse, H, d,
+                          1.f / sqrtf((float)DH), snap, B);
+    prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;
 }
@@ -451,11 +454,12 @@ fo_status launch_attn_bwd(const float* qkv, const int* cu, const bf16_t* out, co
     const float scale = 1.f / sqrtf((float)DH);
     ProfInfo pi;
     pi.kind = PROF_ATTN_BWD; pi.cu = cu; pi.B = B; pi.d = d;
-    const int h = prof_begin(s, "attn_bwd_mfma", pi);
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext("attn_bwd_mfma", pi, &ea, &eb);
     int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
-    hipLaunchKernelGGL(attn_bwd_mfma, dim3(B * H), dim3(256), 0, s, qkv, cu, out, dout, lse, dqkv, H, d, scale, snap,
-                       B);
-    prof_end(h, s);
+    hipExtLaunchKernelGGL(attn_bwd_mfma, dim3(B * H), dim3(256), 0, s, ea, eb, 0, qkv, cu, out, dout, lse, dqkv, H, d,
+                          scale, snap, B);
+    prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;
 }

@@ -12,6 +12,8 @@
 // transposed on their way into LDS (k pairs packed into 32-bit stores).
 #include <algorithm>
 
+#include <hip/hip_ext.h>
+
 #include "gemm.h"
 #include "kernels.h"
 #include "prof.h"
@@ -411,12 +413,28 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     const int wm = wave >> 1, wn = wave & 1;
     const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
     const int Keff = d.Kdev ? min(d.K, *d.Kdev) : d.K;
-    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
     if (d.prof_snap && (blockIdx.x | blockIdx.y | blockIdx.z) == 0 && tid == 0) {
         d.prof_snap[0] = M;
         d.prof_snap[1] = Keff;
     }
-    if (m0 >= M) return;  // uniform for the whole workgroup
+    // XCD-aware tile order.  Workgroups are handed to the eight XCDs round
+    // robin by linear id, and each XCD has its own L2: the first W ids (the
+    // tiles below the effective M; the rest exit) are renumbered so that XCD x
+    // owns a contiguous range, walked in groups of GM tile rows (M fastest),
+    // which keeps the A row blocks and B column blocks it reads few and shared.
+    constexpr int GM = 8;
+    const int nN = gridDim.x, nMe = (M + BM - 1) / BM;
+    const int W = nMe * nN * (int)gridDim.z;
+    const int w = blockIdx.x + nN * (blockIdx.y + gridDim.y * blockIdx.z);
+    if (w >= W) return;  // uniform for the whole workgroup
+    const int xq = W >> 3, xr = W & 7, xc = w & 7;
+    const int nid = xc * xq + min(xc, xr) + (w >> 3);
+    const int T1 = nMe * nN;
+    const int zt = nid / T1, tt = nid - zt * T1;
+    const int g = tt / (GM * nN), tg = tt - g * GM * nN;
+    const int gr = min(GM, nMe - g * GM);
+    const int mt = g * GM + tg % gr, nt = tg / gr;
+    const int m0 = mt * BM, n0 = nt * BN;
     // The K range of this slice, over the concatenation of nseg segments
     // (segment s pairs (A, B), (A, B2), (A2, B) for s = 0, 1, 2), each padded
     // to a whole number of K tiles (the loaders zero-fill past K).
@@ -425,7 +443,7 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     const int kseg = d.nseg > 1 ? (d.K + BK - 1) / BK * BK : Keff;
     const int ktot = d.nseg * kseg;
     const int kc = (d.Kdev && d.splits > 1) ? ((ktot + d.splits - 1) / d.splits + BK - 1) / BK * BK : kchunk;
-    const int kbeg = blockIdx.z * kc;
+    const int kbeg = zt * kc;
     const int kstop = min(ktot, kbeg + kc);
     const int nk = kstop > kbeg ? (kstop - kbeg + BK - 1) / BK : 0;
 
@@ -544,7 +562,7 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
             for (int lr = tid >> 7; lr < BM; lr += 2) {
                 const int row = m0 + lr;
                 if (row >= M) break;
-                d.ws[((int64_t)blockIdx.z * d.M + row) * d.N + col] = Cs[lr * BN + c];
+                d.ws[((int64_t)zt * d.M + row) * d.N + col] = Cs[lr * BN + c];
             }
         } else {
             const float bcol = d.bias ? d.bias[col] : 0.f;
@@ -568,7 +586,7 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
         __syncthreads();
         if (tid >= BN) Cs[c] = csum;
         __syncthreads();
-        if (tid < BN && col < d.N) d.colpart[(int64_t)blockIdx.y * d.N + col] = csum + Cs[c];
+        if (tid < BN && col < d.N) d.colpart[(int64_t)mt * d.N + col] = csum + Cs[c];
     }
 }
 
@@ -620,12 +638,13 @@ void launch(const GemmDesc& d, int kchunk, hipStream_t s) {
     pi.kind = PROF_GEMM;
     pi.M = d.M; pi.N = d.N; pi.K = d.K; pi.nseg = d.nseg;
     pi.Mdev = d.Mdev; pi.Kdev = d.Kdev;
-    const int h = prof_begin(s, names[AM][BMODE], pi);
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext(names[AM][BMODE], pi, &ea, &eb);
     GemmDesc dd = d;
     dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
-    hipLaunchKernelGGL((gemm_kernel<AM, BMODE, AL>), grid, dim3(NT), 0, s, dd, kchunk);
-    prof_end(h, s);
+    hipExtLaunchKernelGGL((gemm_kernel<AM, BMODE, AL>), grid, dim3(NT), 0, s, ea, eb, 0, dd, kchunk);
+    prof_end_ext(h);
 }
 
 }  // namespace
@@ -679,9 +698,10 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
         int64_t total = (int64_t)d.M * d.N;
         if (d.N % 4 == 0) total /= 4;
         int grid = (int)std::min<int64_t>(cdiv(total, 256), 4096);
-        const int h = prof_begin(s, "splitk_reduce", ProfInfo());
-        hipLaunchKernelGGL(splitk_reduce, dim3(grid), dim3(256), 0, s, d);
-        prof_end(h, s);
+        hipEvent_t ea, eb;
+        const int h = prof_begin_ext("splitk_reduce", ProfInfo(), &ea, &eb);
+        hipExtLaunchKernelGGL(splitk_reduce, dim3(grid), dim3(256), 0, s, ea, eb, 0, d);
+        prof_end_ext(h);
         FO_LAUNCHED();
     }
     return FO_OK;

@@ -57,6 +57,26 @@ int prof_begin(hipStream_t s, const char* name, const ProfInfo& info) {
     return h;
 }
 
+int prof_begin_ext(const char* name, const ProfInfo& info, hipEvent_t* a, hipEvent_t* b) {
+    *a = *b = nullptr;
+    Profiler* p = tl_prof;
+    if (!p || (int)p->recs.size() >= p->cap) return -1;
+    const int h = (int)p->recs.size();
+    Rec r;
+    r.name = name;
+    r.info = info;
+    r.a = *a = p->events[2 * h];
+    r.b = *b = p->events[2 * h + 1];
+    p->recs.push_back(r);
+    return h;
+}
+
+void prof_end_ext(int h) {
+    Profiler* p = tl_prof;
+    if (!p || h < 0 || h >= (int)p->recs.size()) return;
+    p->recs[h].closed = true;
+}
+
 int* prof_snap(int h) {
     Profiler* p = tl_prof;
     if (!p || h < 0 || h >= (int)p->recs.size()) return nullptr;

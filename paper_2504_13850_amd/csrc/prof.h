@@ -24,6 +24,11 @@ struct ProfInfo {
 // (GEMM: effective M and K; attention: cu[0..B]) from its first workgroup.
 int prof_begin(hipStream_t s, const char* name, const ProfInfo& info);
 void prof_end(int h, hipStream_t s);
+// The same record for a launch through hipExtLaunchKernelGGL, which stamps the
+// returned start / stop events at the kernel's own dispatch begin and end (no
+// event packets around it): *a = *b = nullptr when the thread is not profiling.
+int prof_begin_ext(const char* name, const ProfInfo& info, hipEvent_t* a, hipEvent_t* b);
+void prof_end_ext(int h);
 int* prof_snap(int h);  // NULL when h < 0
 constexpr int kProfSnapInts = 258;  // capacity of one snapshot (cu of up to 257 offsets)
 
