@@ -38,8 +38,8 @@ FO_API fo_status fo_gemm_bf16(int32_t M, int32_t N, int32_t K, int32_t a_layout,
  *   pass 1 (input gradient):   out[Bn][H][W][Ci]  = conv^T(dy, w)         dy = in [Bn][Ho][Wo][Co]
  *   pass 2 (weight gradient):  out[Co][k][k][Ci]  = sum over pixels dy (x) x   (in = dy, in2 = x)
  * Ho = (H + 2 pad - k) / stride + 1 (same for W).  For pass 0, in_lo / w_lo give
- * compensated products as in fo_gemm_bf16.  Requires Ci % 32 == 0 (pass 0),
- * Co % 32 == 0 (pass 1) and Ci % 8 == 0.  splits / workspace as above (workspace
+ * compensated products as in fo_gemm_bf16.  Requires Ci % 64 == 0 (pass 0),
+ * Co % 64 == 0 (pass 1) and Ci % 8 == 0.  splits / workspace as above (workspace
  * floats: splits * rows * cols of the pass's output matrix). */
 FO_API fo_status fo_conv2d_bf16(int32_t pass, int32_t Bn, int32_t H, int32_t W, int32_t Ci, int32_t Co, int32_t k,
                                 int32_t stride, int32_t pad, const uint16_t* in, const uint16_t* in_lo,
