@@ -127,50 +127,57 @@ struct LdKRBase {
     }
 };
 
-struct LdKR : LdKRBase {
+// Rows contiguous (k-major memory [k][R]): thread = (k quad kq = tid % 16, row
+// chunk tid / 16); register j holds k row 4 kq + j at rows rr0 .. rr0 + 7, and the
+// store packs the four k values of each row into one 8-byte LDS write (a
+// wave's writes of one row offset cover 64 banks without conflict).
+struct LdKR {
     int64_t ld;
-    int r0c, R;
+    int kq, mrow, rr0, R;
     bool vec, full;
     __device__ void init(const bf16_t* P, int64_t ld_, int r0, int R_, int tid) {
         ld = ld_;
         R = R_;
-        kp = tid & 31;
-        rc = (tid >> 5) * 8;
-        r0c = r0 + rc;
+        kq = tid & 15;
+        mrow = (tid >> 4) * 8;
+        rr0 = r0 + mrow;
         vec = (ld % 8 == 0) && (((uintptr_t)P & 15) == 0);
         full = r0 + BM <= R;
     }
     __device__ void load(const bf16_t* P, int kb, int kend, uint4* r) const {
         if (vec && full && kb + BK <= kend) {  // interior tile: no checks (a uniform branch)
 #pragma unroll
-            for (int q = 0; q < 2; ++q)
-#pragma unroll
-                for (int j = 0; j < 2; ++j) r[2 * q + j] = load8(P + (int64_t)(kb + 2 * kp + j) * ld + r0c + 64 * q);
+            for (int j = 0; j < 4; ++j) r[j] = load8(P + (int64_t)(kb + 4 * kq + j) * ld + rr0);
             return;
         }
 #pragma unroll
-        for (int q = 0; q < 2; ++q)
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int k = kb + 2 * kp + j, rr = r0c + 64 * q;
-                uint4& o = r[2 * q + j];
-                if (k >= kend || rr >= R) o = make_uint4(0, 0, 0, 0);
-                else if (vec && rr + 8 <= R) o = load8(P + (int64_t)k * ld + rr);
-                else o = load8_guarded(P + (int64_t)k * ld + rr, R - rr);
-            }
+        for (int j = 0; j < 4; ++j) {
+            const int k = kb + 4 * kq + j;
+            if (k >= kend || rr0 >= R) r[j] = make_uint4(0, 0, 0, 0);
+            else if (vec && rr0 + 8 <= R) r[j] = load8(P + (int64_t)k * ld + rr0);
+            else r[j] = load8_guarded(P + (int64_t)k * ld + rr0, R - rr0);
+        }
     }
     // Aligned operands (16-byte rows, R a multiple of 8): predicated 16-byte
     // loads, always issued as in LdRK::load_al.
     __device__ void load_al(const bf16_t* P, int kb, int kend, uint4* r) const {
 #pragma unroll
-        for (int q = 0; q < 2; ++q)
+        for (int j = 0; j < 4; ++j) {
+            const int k = kb + 4 * kq + j;
+            r[j] = load8(k < kend && rr0 < R ? P + (int64_t)k * ld + rr0 : kZero8);
+        }
+    }
+    __device__ void store(bf16_t* t, const uint4* r, int) const {
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int k = kb + 2 * kp + j, rr = r0c + 64 * q;
-                r[2 * q + j] = load8(k < kend && rr < R ? P + (int64_t)k * ld + rr : kZero8);
-            }
+        for (int e = 0; e < 8; ++e) {
+            uint2 w;
+            w.x = (uint32_t)half_of(r[0], e) | ((uint32_t)half_of(r[1], e) << 16);
+            w.y = (uint32_t)half_of(r[2], e) | ((uint32_t)half_of(r[3], e) << 16);
+            *reinterpret_cast<uint2*>(&t[lds_idx(mrow + e, 4 * kq)]) = w;
+        }
     }
 };
+
 
 // Conv forward A: rows = output pixels (b, oy, ox); k = (ky, kx, ci), Ci % 64 == 0
 // so that a K tile lies within one filter tap.
@@ -405,8 +412,27 @@ __device__ __forceinline__ float epilogue(const GemmDesc& d, int row, int col, f
 }
 
 // ------------------------------------------------------------------ kernel
+// The K range over the concatenation of nseg segments (segment s pairs (A, B),
+// (A, B2), (A2, B) for s = 0, 1, 2), each padded to a whole number of K tiles
+// when nseg > 1 (the loaders zero-fill past K).
+__device__ __forceinline__ int gemm_kseg(const GemmDesc& d, int Keff) {
+    return d.nseg > 1 ? (d.K + BK - 1) / BK * BK : Keff;
+}
+
+// Split-K slices in use.  With a device-side row bound the launch's slice count
+// is a maximum: the kernel and the reduction both take as many slices as keep
+// two workgroups per CU busy over the active tiles, each at least four K tiles
+// long.  With static sizes every launched slice is used.
+__device__ __forceinline__ int active_splits(const GemmDesc& d, int M_eff, int ktot) {
+    if (d.splits <= 1 || !d.Mdev) return d.splits;
+    const int tiles = ((M_eff + BM - 1) / BM) * ((d.N + BN - 1) / BN);
+    int s = min(d.splits, max(1, 512 / max(tiles, 1)));
+    while (s > 1 && ktot < 4 * BK * s) --s;
+    return s;
+}
+
 template <int AM, int BMODE, bool AL>
-__global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchunk) {
+__global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
     // two K tiles (A and B each 128 x 72 bf16) = 72 KB; reused for the C tile
     __shared__ __attribute__((aligned(16))) bf16_t smem[2][2][BM * LDR];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -423,8 +449,11 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     // owns a contiguous range, walked in groups of GM tile rows (M fastest),
     // which keeps the A row blocks and B column blocks it reads few and shared.
     constexpr int GM = 8;
+    const int kseg = gemm_kseg(d, Keff);
+    const int ktot = d.nseg * kseg;
+    const int S = active_splits(d, M, ktot);
     const int nN = gridDim.x, nMe = (M + BM - 1) / BM;
-    const int W = nMe * nN * (int)gridDim.z;
+    const int W = nMe * nN * S;
     const int w = blockIdx.x + nN * (blockIdx.y + gridDim.y * blockIdx.z);
     if (w >= W) return;  // uniform for the whole workgroup
     const int xq = W >> 3, xr = W & 7, xc = w & 7;
@@ -435,14 +464,8 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     const int gr = min(GM, nMe - g * GM);
     const int mt = g * GM + tg % gr, nt = tg / gr;
     const int m0 = mt * BM, n0 = nt * BN;
-    // The K range of this slice, over the concatenation of nseg segments
-    // (segment s pairs (A, B), (A, B2), (A2, B) for s = 0, 1, 2), each padded
-    // to a whole number of K tiles (the loaders zero-fill past K).
-    // With a device-side K (plain products only) the slices split the
-    // effective K, so that none of them runs over zero-filled tiles.
-    const int kseg = d.nseg > 1 ? (d.K + BK - 1) / BK * BK : Keff;
-    const int ktot = d.nseg * kseg;
-    const int kc = (d.Kdev && d.splits > 1) ? ((ktot + d.splits - 1) / d.splits + BK - 1) / BK * BK : kchunk;
+    // this slice's K range (slices are whole K tiles long)
+    const int kc = ((ktot + S - 1) / S + BK - 1) / BK * BK;
     const int kbeg = zt * kc;
     const int kstop = min(ktot, kbeg + kc);
     const int nk = kstop > kbeg ? (kstop - kbeg + BK - 1) / BK : 0;
@@ -558,7 +581,7 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d, int kchun
     const int c = tid & (BN - 1), col = n0 + c;
     float csum = 0.f;
     if (col < d.N) {
-        if (d.splits > 1) {
+        if (S > 1) {
             for (int lr = tid >> 7; lr < BM; lr += 2) {
                 const int row = m0 + lr;
                 if (row >= M) break;
@@ -596,7 +619,9 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
     const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
     const int64_t full = (int64_t)d.M * d.N;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    const int S = d.splits;
+    const int Keff = d.Kdev ? min(d.K, *d.Kdev) : d.K;
+    const int S = active_splits(d, M, d.nseg * gemm_kseg(d, Keff));
+    if (S <= 1) return;  // the GEMM ran the epilogue itself
     if ((d.N & 3) == 0) {
         const int64_t total4 = (int64_t)M * d.N / 4;
         for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total4; i += stride) {
@@ -626,7 +651,7 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
 }
 
 template <int AM, int BMODE, bool AL = false>
-void launch(const GemmDesc& d, int kchunk, hipStream_t s) {
+void launch(const GemmDesc& d, hipStream_t s) {
     // kernel names as the profilers print them
     static const char* names[6][6] = {};
     static char buf[6][6][32];
@@ -643,7 +668,7 @@ void launch(const GemmDesc& d, int kchunk, hipStream_t s) {
     GemmDesc dd = d;
     dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
-    hipExtLaunchKernelGGL((gemm_kernel<AM, BMODE, AL>), grid, dim3(NT), 0, s, ea, eb, 0, dd, kchunk);
+    hipExtLaunchKernelGGL((gemm_kernel<AM, BMODE, AL>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
     prof_end_ext(h);
 }
 
@@ -666,12 +691,6 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
         FO_CHECK(d.B2 && (d.nseg == 2 || d.A2), "gemm: compensated product needs its low parts");
         FO_CHECK(!d.Kdev, "gemm: compensated product needs a static K");
     }
-    const int ktot = d.nseg * (d.nseg > 1 ? (int)cdiv(d.K, BK) * BK : d.K);
-    int kchunk = ktot;
-    if (d.splits > 1) {
-        // slices past the end of K have no work and write zero partials
-        kchunk = (int)cdiv(cdiv(ktot, d.splits), BK) * BK;
-    }
     const int a = d.amode, b = d.bmode;
     // aligned variant: every contiguous dimension a multiple of 8 and 16-byte rows
     auto al16 = [](const void* p) { return p == nullptr || ((uintptr_t)p & 15) == 0; };
@@ -682,13 +701,13 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     // (a k-major A with a device-side row bound may end inside an 8-row chunk)
     const bool al = (a == OP_RK || a == OP_KR) && (b == OP_RK || b == OP_KR) && !(a == OP_KR && d.Mdev) &&
                     op_aligned(a, d.A, d.A2, d.lda, d.M) && op_aligned(b, d.B, d.B2, d.ldb, d.N);
-    if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(d, kchunk, s) : launch<OP_RK, OP_RK>(d, kchunk, s);
-    else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KR, true>(d, kchunk, s) : launch<OP_RK, OP_KR>(d, kchunk, s);
-    else if (a == OP_KR && b == OP_KR) al ? launch<OP_KR, OP_KR, true>(d, kchunk, s) : launch<OP_KR, OP_KR>(d, kchunk, s);
-    else if (a == OP_KR && b == OP_RK) al ? launch<OP_KR, OP_RK, true>(d, kchunk, s) : launch<OP_KR, OP_RK>(d, kchunk, s);
-    else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(d, kchunk, s);
-    else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(d, kchunk, s);
-    else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(d, kchunk, s);
+    if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(d, s) : launch<OP_RK, OP_RK>(d, s);
+    else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KR, true>(d, s) : launch<OP_RK, OP_KR>(d, s);
+    else if (a == OP_KR && b == OP_KR) al ? launch<OP_KR, OP_KR, true>(d, s) : launch<OP_KR, OP_KR>(d, s);
+    else if (a == OP_KR && b == OP_RK) al ? launch<OP_KR, OP_RK, true>(d, s) : launch<OP_KR, OP_RK>(d, s);
+    else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(d, s);
+    else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(d, s);
+    else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(d, s);
     else {
         set_error("gemm: unsupported operand modes %d/%d", a, b);
         return FO_EINVAL;

@@ -211,22 +211,23 @@ __global__ void __launch_bounds__(256) scatter_cls_kernel(const float* __restric
 }
 
 // ------------------------------------------------------------------ plan
+// K slices of a weight-gradient product (static M x N, K = the packed rows):
+// as many as fit one round of two workgroups per CU (a second, mostly empty
+// round would double the time), each at least 256 long.
 int split_for(int M, int N, int K) {
     int tiles = (int)(cdiv(M, 128) * cdiv(N, 128));
-    int s = (int)std::max<int64_t>(1, 640 / tiles);
-    s = std::min(s, 8);
+    int s = std::max(1, std::min(8, 512 / std::max(tiles, 1)));
     while (s > 1 && (int64_t)K / s < 256) --s;
     return s;
 }
 
-// K slices for a forward / input-gradient product over the packed rows: enough
-// workgroups for the 256 CUs (two resident per CU), fused epilogue in the
-// reduction pass.  K here is the product's full reduction length (with the
-// compensated segments).
-int split_rows(int rows, int N, int K) {
-    int tiles = (int)(cdiv(rows, 128) * cdiv(N, 128));
-    int s = std::max(1, std::min(4, 512 / std::max(tiles, 1)));
-    while (s > 1 && K / s < 512) --s;
+// Maximum K slices of a forward / input-gradient product over the packed rows;
+// the kernel takes as many of them as the device-side row count needs to fill
+// the CUs (fused epilogue in the reduction pass).  K is the product's full
+// reduction length, with the compensated segments.
+int split_rows(int K) {
+    int s = 4;
+    while (s > 1 && K / s < 256) --s;
     return s;
 }
 
@@ -430,7 +431,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         TRY(launch_attn_fwd(t.qkv, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
         GemmDesc o = lin_fwd(rows, t.O, t.Olo, D, W + f.wo, Wl + f.wo, D);
         o.Mdev = Tdev;
-        o.splits = split_rows(rows, D, 3 * D); o.ws = P->splitws;
+        o.splits = split_rows(3 * D); o.ws = P->splitws;
         o.bias = prm + f.bo;
         o.resid = P->Xf[l]; o.ldr = D;
         o.Cf = t.u1; o.ldcf = D;
@@ -445,7 +446,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         TRY(gemm(f1, s));
         GemmDesc f2 = lin_fwd(rows, t.G, t.Glo, FF, W + f.w2, Wl + f.w2, D);
         f2.Mdev = Tdev;
-        f2.splits = split_rows(rows, D, 3 * FF); f2.ws = P->splitws;
+        f2.splits = split_rows(3 * FF); f2.ws = P->splitws;
         f2.bias = prm + f.bf2;
         f2.resid = t.Hf; f2.ldr = D;
         f2.Cf = t.u2; f2.ldcf = D;
@@ -509,7 +510,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.bmode = OP_KR; d.B = W + f.w1; d.ldb = D;
             d.resid = P->du2f; d.ldr = D;
             d.Cf = P->dHf; d.ldcf = D;
-            d.splits = split_rows(rows, D, FF); d.ws = P->splitws;
+            d.splits = split_rows(FF); d.ws = P->splitws;
             TRY(gemm(d, s));
             GemmDesc w;
             w.M = FF; w.N = D; w.K = rows; w.Kdev = Tdev;
@@ -529,7 +530,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.amode = OP_RK; d.A = P->du1b; d.lda = D;
             d.bmode = OP_KR; d.B = W + f.wo; d.ldb = D;
             d.Cb = P->dO; d.ldcb = D;
-            d.splits = split_rows(rows, D, D); d.ws = P->splitws;
+            d.splits = split_rows(D); d.ws = P->splitws;
             TRY(gemm(d, s));
             GemmDesc w;
             w.M = D; w.N = D; w.K = rows; w.Kdev = Tdev;
@@ -548,7 +549,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.bmode = OP_KR; d.B = W + f.wqkv; d.ldb = D;
             d.resid = P->du1f; d.ldr = D;
             d.Cf = P->dY[cur ^ 1]; d.ldcf = D;
-            d.splits = split_rows(rows, D, 3 * D); d.ws = P->splitws;
+            d.splits = split_rows(3 * D); d.ws = P->splitws;
             TRY(gemm(d, s));
         }
         GemmDesc w;

@@ -93,10 +93,11 @@ struct Plan {
     size_t act_max;           // elements of the largest activation
 };
 
+// K slices of a conv weight gradient (K = output pixels of the batch): as many
+// as fit one round of two workgroups per CU, each at least 256 long.
 int split_for(int M, int N, int K) {
     int tiles = (int)(cdiv(M, 128) * cdiv(N, 128));
-    int s = (int)std::max<int64_t>(1, 640 / tiles);
-    s = std::min(s, 8);
+    int s = std::max(1, std::min(8, 512 / std::max(tiles, 1)));
     while (s > 1 && (int64_t)K / s < 256) --s;
     return s;
 }
