@@ -41,8 +41,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (transformer 30, 128-device VGG 1000)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (transformer 5, 128-device VGG 10)")
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=2)
@@ -204,6 +204,158 @@ def bench_aggregate(A, torch, stream):
             "workload_sizes": small}
 
 
+VGG_STEP_GFLOP = 102.9  # useful FLOPs of one VGG-16 split server step at B = 64 (fwd + dgrad + wgrad)
+
+
+def fused_aggregation(A, torch, n, m):
+    """One fused drain of m model messages into an n-element global: µs and GB/s
+    against its (m + 2) * 4 * n algorithmic bytes."""
+    g = torch.zeros(n, device="cuda", dtype=torch.float32)
+    locs = [torch.full((n,), float(i + 1), device="cuda", dtype=torch.float32) for i in range(m)]
+    q = A.fo_queues_create(m, 0, 1, False, 2 * m)
+    try:
+        def queue_models():
+            for k in range(m):
+                A.fo_queues_push_model(q, k, locs[k], 0)
+            if A.fo_pick_device(q) != -2:
+                raise RuntimeError("fused aggregation: no model pending")
+        queue_models()
+        A.fo_aggregate_pending_all(q, g, 1.0)
+        torch.cuda.synchronize()
+        reps = 10
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ms = 0.0
+        for _ in range(reps):
+            queue_models()  # host bookkeeping only, outside the timed span
+            torch.cuda.synchronize()
+            ev0.record()
+            applied, _ = A.fo_aggregate_pending_all(q, g, 1.0)
+            ev1.record()
+            torch.cuda.synchronize()
+            ms += ev0.elapsed_time(ev1)
+            assert applied == m
+        us = ms / reps * 1e3
+        nbytes = (m + 2) * 4 * n
+        return {"n": n, "arrivals": m, "us_per_drain": round(us, 2), "bytes": nbytes,
+                "GB/s": round(nbytes / (us * 1e-6) / 1e9, 1), "frac_of_hbm": round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    finally:
+        A.fo_queues_destroy(q)
+
+
+def bench_vgg128(args, A, torch, S):
+    """The 128-device VGG-16 split workload: lognormal device rates, Poisson
+    arrivals per server step, each arrival an activation batch (flow-controlled
+    put into a 64 GiB HBM pool, copied from a bank of 256 distinct batches) and a
+    model message (staleness-weighted aggregation of the 38,720-parameter
+    device-side part, fused per drain); then one pick and one server step."""
+    cid = 5
+    cfg = S.get_config(cid)
+    K, B = cfg.n_devices, cfg.batch
+    stream = torch.cuda.current_stream()
+    steps, warm = args.steps, args.warmup
+    rates = S.make_arrival_rates(cid)
+    counts = S.make_arrival_counts(cid, rates, warm + steps)
+    bank_n = cfg.extra["bank"]
+    acts_d = torch.from_numpy(S.make_acts(cid, bank_n).view(np.int16)).cuda()
+    labels_d = torch.from_numpy(S.make_labels(cid, bank_n)).cuda()
+    model = A.fo_model_create(cid, B, S.init_params(cid), stream)
+    slot_bytes = int(acts_d[0].numel()) * 2
+    n_slots = cfg.extra["pool_bytes"] // slot_bytes
+    q = A.fo_queues_create(K, slot_bytes, B, False, n_slots, stream)
+    A.fo_set_max_delay(-1)
+    n = cfg.agg_n
+    glob = torch.from_numpy(S.make_global_vector(cid)).cuda()
+    locs = torch.from_numpy(S.make_local_vectors(cid, K)).cuda()
+    dev_version = [0] * K
+    seq = [0]
+    tallies = {"arrivals": 0, "applied": 0, "skipped": 0, "drains": 0, "idle_steps": 0}
+
+    def one_step(t):
+        senders = []
+        row = counts[t]
+        for k in np.nonzero(row)[0].tolist():
+            for _ in range(int(row[k])):
+                i = seq[0] % bank_n
+                seq[0] += 1
+                A.fo_queues_push(q, k, acts_d[i], labels_d[i])
+                A.fo_queues_push_model(q, k, locs[k], dev_version[k])
+                senders.append(k)
+        tallies["arrivals"] += len(senders)
+        k = A.fo_pick_device(q)
+        if k == -2:  # Alg. 3: models first
+            applied, skipped = A.fo_aggregate_pending_all(q, glob, 1.0)
+            tallies["applied"] += applied
+            tallies["skipped"] += skipped
+            tallies["drains"] += 1
+            v = A.fo_queues_stats(q).version
+            for kk in senders:  # each sender receives the aggregated global (Alg. 4)
+                dev_version[kk] = v
+            k = A.fo_pick_device(q)
+        if k < 0:
+            tallies["idle_steps"] += 1
+            return
+        fa, lab, _, _ = A.fo_queues_in_service(q)
+        A.fo_server_step(model, fa, lab, k)
+        A.fo_queues_release(q)
+
+    try:
+        for t in range(warm):
+            one_step(t)
+        torch.cuda.synchronize()
+        st0 = A.fo_queues_stats(q)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        wall0 = time.perf_counter()
+        for t in range(warm, warm + steps):
+            one_step(t)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        ms = ev0.elapsed_time(ev1)
+        st = A.fo_queues_stats(q)
+        trained = st.picks - st0.picks
+        # the server step alone on a resident batch, for the step-only rate and MFU
+        k = A.fo_pick_device(q)
+        assert k >= 0
+        fa, lab, _, _ = A.fo_queues_in_service(q)
+        for _ in range(3):
+            A.fo_server_step(model, fa, lab, k)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(20):
+            A.fo_server_step(model, fa, lab, k)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        A.fo_queues_release(q)
+        step_ms = e0.elapsed_time(e1) / 20
+    finally:
+        A.fo_queues_destroy(q)
+        A.fo_model_destroy(model)
+    fused = [fused_aggregation(A, torch, n, 64), fused_aggregation(A, torch, 1 << 24, 16)]
+    value = B * trained / (ms * 1e-3)
+    out = {
+        "metric": "server train samples/s (128-device loop: arrivals, flow control, fused aggregation, pick, step)",
+        "value": round(value, 2), "unit": "samples/s", "n_gpus": 1, "steps": steps, "warmup": warm,
+        "ms_per_step": round(ms / steps, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "vgg16 split server step, batch 64 of [64,16,16] bf16 activations, 128 devices, "
+                               "arrivals Poisson(lambda_k), lambda_k ~ LogNormal(0,1), 64 GiB activation pool, "
+                               "aggregation of the 38,720-parameter device part per arrival (alpha 1, no delay cap)",
+                   "global_batch": B, "parallelism": "single-gpu"},
+        "loop": {"trained_batches": trained, "idle_steps": tallies["idle_steps"],
+                 "arrivals": tallies["arrivals"], "admitted": st.admitted - st0.admitted,
+                 "refused": st.refused - st0.refused, "refused_total": st.refused,
+                 "pool_slots": n_slots, "omega": st.omega, "pool_peak_occupancy": st.peak_queued,
+                 "models_applied": tallies["applied"], "models_skipped": tallies["skipped"],
+                 "fused_drains": tallies["drains"], "host_wall_ms_per_step": round(wall / steps * 1e3, 3)},
+        "step_only": {"ms": round(step_ms, 4), "samples_per_s": round(B / (step_ms * 1e-3), 1),
+                      "mfu": round(VGG_STEP_GFLOP * 1e9 / (step_ms * 1e-3) / (PEAK_BF16_TFLOPS * 1e12), 4)},
+        "fused_aggregation": fused,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -219,8 +371,16 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cid = args.config
+    if cid == 5:
+        args.steps = 1000 if args.steps is None else args.steps
+        args.warmup = 10 if args.warmup is None else args.warmup
+        bench_vgg128(args, A, torch, S)
+        return
     if cid != 4:
-        raise SystemExit("bench.py: only the transformer workload (--config 4) is wired up")
+        raise SystemExit("bench.py: workloads are --config 4 (transformer, default) and --config 5 "
+                         "(128-device VGG with Poisson arrivals)")
+    args.steps = 30 if args.steps is None else args.steps
+    args.warmup = 5 if args.warmup is None else args.warmup
     cfg = S.get_config(cid)
     B, Lmax, K = cfg.batch, cfg.in_shape[0], cfg.n_devices
     stream = torch.cuda.current_stream()

@@ -66,6 +66,10 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2504_13850_amd.build.build()")
+        # One HIP runtime per process: torch ships its own copy of the runtime
+        # under the same soname, so loading torch first binds the library to it
+        # and torch's streams and device pointers are valid in the library.
+        import torch  # noqa: F401
         L = C.CDLL(LIB_PATH)
         vp, i32, i64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
         sig = {

@@ -40,7 +40,7 @@ extern "C" fo_status fo_conv2d_bf16(int32_t pass, int32_t Bn, int32_t H, int32_t
              "fo_conv2d_bf16: bad geometry");
     FO_CHECK(H + 2 * pad >= k && W + 2 * pad >= k, "fo_conv2d_bf16: kernel larger than the padded input");
     FO_CHECK(in && out && (pass == 2 ? in2 != nullptr : w != nullptr), "fo_conv2d_bf16: NULL operand");
-    FO_CHECK(Ci % 8 == 0 && (pass != 0 || Ci % 32 == 0) && (pass != 1 || Co % 32 == 0),
+    FO_CHECK(Ci % 8 == 0 && (pass != 0 || Ci % 64 == 0) && (pass != 1 || Co % 64 == 0),
              "fo_conv2d_bf16: channel counts not supported (Ci=%d, Co=%d)", Ci, Co);
     FO_CHECK(!in_lo || w_lo, "fo_conv2d_bf16: in_lo needs w_lo");
     FO_CHECK(splits >= 1 && (splits == 1 || workspace), "fo_conv2d_bf16: split-K needs a workspace");

@@ -49,7 +49,8 @@ struct Conv {
     int cin, cout, k, stride, pad, H, W, Ho, Wo;
     int64_t w, b;               // parameter offsets (b < 0: no bias)
     int64_t g, be;              // batch-norm scale / shift offsets (< 0: none)
-    int splits;
+    int splits;                 // K slices of the weight gradient
+    int fsplits, dsplits;       // K slices of the forward and of the input gradient
     // activations
     bf16_t *yh, *yl;            // VGG: post-ReLU output (hi, lo)
     float *z, *mean, *rstd;     // ResNet: pre-norm output and its batch statistics
@@ -93,8 +94,10 @@ struct Plan {
     size_t act_max;           // elements of the largest activation
 };
 
-// K slices of a conv weight gradient (K = output pixels of the batch): as many
-// as fit one round of two workgroups per CU, each at least 256 long.
+// K slices of a conv product: as many as fit one round of two workgroups per
+// CU over its output tiles, each at least 256 long.  The deep layers have few
+// output tiles (2x2 maps: M = 4 B) and long K (9 Cin up to 4608), so without
+// slices most CUs would sit idle.
 int split_for(int M, int N, int K) {
     int tiles = (int)(cdiv(M, 128) * cdiv(N, 128));
     int s = std::max(1, std::min(8, 512 / std::max(tiles, 1)));
@@ -118,6 +121,8 @@ void build(Plan& P, int cid, int B) {
         if (bias) { c.b = o; o += cout; }
         if (bn) { c.g = o; o += cout; c.be = o; o += cout; }
         c.splits = split_for(cout, k * k * cin, B * c.Ho * c.Wo);
+        c.fsplits = split_for(B * c.Ho * c.Wo, cout, 3 * (int)cdiv(k * k * cin, 64) * 64);
+        c.dsplits = split_for(B * H * H, cin, k * k * cout);
         P.convs.push_back(c);
         return (int)P.convs.size() - 1;
     };
@@ -197,6 +202,8 @@ size_t ws_bytes(const fo_model* m) {
         if (P.resnet) { add(4 * n); add(4 * c.cout); add(4 * c.cout); }
         else { add(2 * n); add(2 * n); }
         sw = std::max(sw, gemm_ws_bytes(c.cout, c.k * c.k * c.cin, c.splits));
+        sw = std::max(sw, gemm_ws_bytes(B * c.Ho * c.Wo, c.cout, c.fsplits));
+        sw = std::max(sw, gemm_ws_bytes(B * c.H * c.W, c.cin, c.dsplits));
         red = std::max(red, bn_ws_floats(B * c.Ho * c.Wo, c.cout));
         red = std::max(red, colsum_ws_floats(B * c.Ho * c.Wo, c.cout));
     }
@@ -246,6 +253,8 @@ fo_status init(fo_model* m) {
             c.yl = a.take<bf16_t>(n);
         }
         sw = std::max(sw, gemm_ws_bytes(c.cout, c.k * c.k * c.cin, c.splits));
+        sw = std::max(sw, gemm_ws_bytes(B * c.Ho * c.Wo, c.cout, c.fsplits));
+        sw = std::max(sw, gemm_ws_bytes(B * c.H * c.W, c.cin, c.dsplits));
         red = std::max(red, bn_ws_floats(B * c.Ho * c.Wo, c.cout));
         red = std::max(red, colsum_ws_floats(B * c.Ho * c.Wo, c.cout));
     }
@@ -305,6 +314,7 @@ GemmDesc conv_fwd_desc(const fo_model* m, const Conv& c, int B, const bf16_t* xh
     d.bmode = OP_RK; d.B = m->w16 + c.w; d.B2 = m->w16lo + c.w; d.ldb = d.K;
     d.nseg = xl ? 3 : 2;
     d.g = geom(c, B);
+    d.splits = c.fsplits; d.ws = static_cast<const Plan*>(m->plan)->splitws;
     return d;
 }
 
@@ -332,6 +342,7 @@ fo_status conv_dgrad(fo_model* m, const Conv& c, int B, const bf16_t* dzb, const
     d.resid = resid; d.ldr = c.cin;
     d.Cf = outf; d.ldcf = c.cin;
     d.Cb = outb; d.ldcb = c.cin;
+    d.splits = c.dsplits; d.ws = static_cast<const Plan*>(m->plan)->splitws;
     return gemm(d, m->stream);
 }
 

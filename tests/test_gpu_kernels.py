@@ -105,12 +105,14 @@ def test_conv_passes(case):
     announce(f"conv {case}")
     (x, w, dy), (y_ref, dx_ref, dw_ref), Ho = _conv_case(case, sum(case))
     xd, wd, dyd = _dev16(x), _dev16(w), _dev16(dy)
-    y = torch.zeros((Bn, Ho, Ho, Co), dtype=torch.float32, device="cuda")
-    A.fo_conv2d_bf16(0, Bn, H, H, Ci, Co, k, st, pad, xd, None, None, wd, None, y)
-    assert normwise(y.cpu().numpy(), y_ref) <= 1e-5
-    dx = torch.zeros((Bn, H, H, Ci), dtype=torch.float32, device="cuda")
-    A.fo_conv2d_bf16(1, Bn, H, H, Ci, Co, k, st, pad, dyd, None, None, wd, None, dx)
-    assert normwise(dx.cpu().numpy(), dx_ref) <= 1e-5
+    for splits in (1, 4):  # split-K forward and input gradient: fp32 partials, epilogue in the reduction
+        ws = torch.empty(splits * Bn * H * H * max(Ci, Co), dtype=torch.float32, device="cuda")
+        y = torch.zeros((Bn, Ho, Ho, Co), dtype=torch.float32, device="cuda")
+        A.fo_conv2d_bf16(0, Bn, H, H, Ci, Co, k, st, pad, xd, None, None, wd, None, y, splits, ws)
+        assert normwise(y.cpu().numpy(), y_ref) <= 1e-5, splits
+        dx = torch.zeros((Bn, H, H, Ci), dtype=torch.float32, device="cuda")
+        A.fo_conv2d_bf16(1, Bn, H, H, Ci, Co, k, st, pad, dyd, None, None, wd, None, dx, splits, ws)
+        assert normwise(dx.cpu().numpy(), dx_ref) <= 1e-5, splits
     for splits in (1, 4):
         dw = torch.zeros((Co, k, k, Ci), dtype=torch.float32, device="cuda")
         rows, cols = Co, k * k * Ci
