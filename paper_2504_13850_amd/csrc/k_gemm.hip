@@ -431,6 +431,92 @@ __device__ __forceinline__ int active_splits(const GemmDesc& d, int M_eff, int k
     return s;
 }
 
+// The output tile and K slice of a workgroup.
+struct TileJob {
+    int m0, n0, mt, zt, S;
+};
+
+// XCD-aware tile order.  Workgroups are handed to the eight XCDs round robin
+// by linear id, and each XCD has its own L2: the first W ids (the tiles below
+// the effective M, times the slices in use; the rest exit) are renumbered so
+// that XCD x owns a contiguous range, walked in groups of GM tile rows (M
+// fastest), which keeps the A row blocks and B column blocks it reads few and
+// shared.  Returns false when the workgroup has no tile.
+__device__ __forceinline__ bool map_tile(const GemmDesc& d, int M, int ktot_split, TileJob& job) {
+    constexpr int GM = 8;
+    const int S = active_splits(d, M, ktot_split);
+    const int nN = gridDim.x, nMe = (M + BM - 1) / BM;
+    const int W = nMe * nN * S;
+    const int w = blockIdx.x + nN * (blockIdx.y + gridDim.y * blockIdx.z);
+    if (w >= W) return false;
+    const int xq = W >> 3, xr = W & 7, xc = w & 7;
+    const int nid = xc * xq + min(xc, xr) + (w >> 3);
+    const int T1 = nMe * nN;
+    const int zt = nid / T1, tt = nid - zt * T1;
+    const int g = tt / (GM * nN), tg = tt - g * GM * nN;
+    const int gr = min(GM, nMe - g * GM);
+    job.mt = g * GM + tg % gr;
+    job.m0 = job.mt * BM;
+    job.n0 = (tg / gr) * BN;
+    job.zt = zt;
+    job.S = S;
+    return true;
+}
+
+// The 128 x 128 accumulator tile leaves through LDS (Cs, 64 KB): accumulator
+// (i, j, r) of a lane holds C[row][col] with row = i*32 + (r/4)*8 +
+// (lane/32)*4 + r%4, col = j*32 + lane%32 (wave-relative).  Each thread then
+// owns one column and walks 64 rows, so every global store instruction covers
+// 64 consecutive columns of one row.  Split slices store fp32 partials; a
+// whole product runs the epilogue (and the optional column sums).
+__device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc)[2][2], float* Cs, const TileJob& job,
+                                           int M, int tid) {
+    const int lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int lr = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                Cs[lr * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+            }
+    __syncthreads();
+    const int m0 = job.m0, c = tid & (BN - 1), col = job.n0 + c;
+    float csum = 0.f;
+    if (col < d.N) {
+        if (job.S > 1) {
+            for (int lr = tid >> 7; lr < BM; lr += 2) {
+                const int row = m0 + lr;
+                if (row >= M) break;
+                d.ws[((int64_t)job.zt * d.M + row) * d.N + col] = Cs[lr * BN + c];
+            }
+        } else {
+            const float bcol = d.bias ? d.bias[col] : 0.f;
+            // eight rows per batch: their operand loads are in flight together
+            for (int lr0 = tid >> 7; lr0 < BM && m0 + lr0 < M; lr0 += 16) {
+                EpiIn e[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int row = m0 + lr0 + 2 * u;
+                    if (row < M) e[u] = epi_load(d, row, col);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int lr = lr0 + 2 * u, row = m0 + lr;
+                    if (row < M) csum += epi_store(d, row, col, Cs[lr * BN + c] + bcol + e[u].resid, e[u]);
+                }
+            }
+        }
+    }
+    if (d.colpart) {  // uniform; the two row halves of a column meet in LDS
+        __syncthreads();
+        if (tid >= BN) Cs[c] = csum;
+        __syncthreads();
+        if (tid < BN && col < d.N) d.colpart[(int64_t)job.mt * d.N + col] = csum + Cs[c];
+    }
+}
+
 template <int AM, int BMODE, bool AL>
 __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
     // two K tiles (A and B each 128 x 72 bf16) = 72 KB; reused for the C tile
@@ -443,27 +529,11 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
         d.prof_snap[0] = M;
         d.prof_snap[1] = Keff;
     }
-    // XCD-aware tile order.  Workgroups are handed to the eight XCDs round
-    // robin by linear id, and each XCD has its own L2: the first W ids (the
-    // tiles below the effective M; the rest exit) are renumbered so that XCD x
-    // owns a contiguous range, walked in groups of GM tile rows (M fastest),
-    // which keeps the A row blocks and B column blocks it reads few and shared.
-    constexpr int GM = 8;
+    TileJob job;
+    if (!map_tile(d, M, d.nseg * gemm_kseg(d, Keff), job)) return;  // uniform for the whole workgroup
     const int kseg = gemm_kseg(d, Keff);
     const int ktot = d.nseg * kseg;
-    const int S = active_splits(d, M, ktot);
-    const int nN = gridDim.x, nMe = (M + BM - 1) / BM;
-    const int W = nMe * nN * S;
-    const int w = blockIdx.x + nN * (blockIdx.y + gridDim.y * blockIdx.z);
-    if (w >= W) return;  // uniform for the whole workgroup
-    const int xq = W >> 3, xr = W & 7, xc = w & 7;
-    const int nid = xc * xq + min(xc, xr) + (w >> 3);
-    const int T1 = nMe * nN;
-    const int zt = nid / T1, tt = nid - zt * T1;
-    const int g = tt / (GM * nN), tg = tt - g * GM * nN;
-    const int gr = min(GM, nMe - g * GM);
-    const int mt = g * GM + tg % gr, nt = tg / gr;
-    const int m0 = mt * BM, n0 = nt * BN;
+    const int S = job.S, zt = job.zt, m0 = job.m0, n0 = job.n0;
     // this slice's K range (slices are whole K tiles long)
     const int kc = ((ktot + S - 1) / S + BK - 1) / BK * BK;
     const int kbeg = zt * kc;
@@ -562,55 +632,144 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
         __syncthreads();
     }
 
-    // Accumulator (i, j, r) of this lane holds C[row][col] with
-    // row = i*32 + (r/4)*8 + (lane/32)*4 + r%4, col = j*32 + lane%32 (wave-relative).
-    // The 128 x 128 tile leaves through LDS: each thread then owns one column and
-    // walks 64 rows, so every global store instruction covers 64 consecutive
-    // columns of one row.
-    float* Cs = reinterpret_cast<float*>(&smem[0][0][0]);
+    store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
+}
+
+// ------------------------------------------------------------------ single-pass compensated product
+// C = A.B + A.B_lo + A_lo.B (NSEG = 3) or A.B + A.B_lo (NSEG = 2) for aligned
+// row-major operands (K contiguous, K, lda, ldb multiples of 8): every K tile
+// stages the high and low parts of both operands once and issues the two or
+// three MFMAs of each fragment pair back to back, instead of running the K loop
+// once per segment.  Per MFMA that is two thirds of the LDS reads, two thirds
+// of the LDS writes and a third of the barriers of the segmented form.  K tiles
+// of 32 with rows padded to 40 elements (80 B: eight consecutive rows start 20
+// banks apart, so both the 16-byte stores and the operand reads are conflict
+// free) keep two stages of four tiles at 80 KB, two workgroups per CU.
+constexpr int CBK = 32, CLD = CBK + 8;
+
+struct LdRKc {  // one 128 x 32 tile: rows (tid / 4) + 64 v, k chunk (tid % 4) * 8
+    int64_t off[2];
+    int kc;
+    __device__ void init(int64_t ld, int r0, int R, int tid) {
+        kc = (tid & 3) * 8;
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+            const int gr = r0 + (tid >> 2) + 64 * v;
+            off[v] = gr < R ? (int64_t)gr * ld : -1;
+        }
+    }
+    __device__ void load(const bf16_t* P, int kb, int kend, uint4* r) const {
+        const int k = kb + kc;
+#pragma unroll
+        for (int v = 0; v < 2; ++v) r[v] = load8(off[v] >= 0 && k < kend ? P + off[v] + k : kZero8);
+    }
+    __device__ void store(bf16_t* t, const uint4* r, int tid) const {
+#pragma unroll
+        for (int v = 0; v < 2; ++v) *reinterpret_cast<uint4*>(&t[((tid >> 2) + 64 * v) * CLD + kc]) = r[v];
+    }
+};
+
+template <int NSEG>
+__global__ void __launch_bounds__(NT, 2) gemm_comp_kernel(const GemmDesc d) {
+    // two stages of four 128 x 40 tiles (A, A_lo, B, B_lo) = 80 KB; reused for the C tile
+    __shared__ __attribute__((aligned(16))) bf16_t smem[2][4][BM * CLD];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
+    const int K = d.K;
+    if (d.prof_snap && (blockIdx.x | blockIdx.y | blockIdx.z) == 0 && tid == 0) {
+        d.prof_snap[0] = M;
+        d.prof_snap[1] = K;
+    }
+    TileJob job;
+    // the slice count follows the segmented form's rule (the reduction pass uses it too)
+    if (!map_tile(d, M, d.nseg * gemm_kseg(d, K), job)) return;  // uniform for the whole workgroup
+    const int S = job.S;
+    const int kpad = (K + CBK - 1) / CBK * CBK;
+    const int kc = ((kpad + S - 1) / S + CBK - 1) / CBK * CBK;
+    const int kbeg = job.zt * kc;
+    const int kstop = min(kpad, kbeg + kc);
+    const int nk = kstop > kbeg ? (kstop - kbeg) / CBK : 0;
+
+    LdRKc la, lb;
+    la.init(d.lda, job.m0, M, tid);
+    lb.init(d.ldb, job.n0, d.N, tid);
+
+    f32x16 acc[2][2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int lr = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                Cs[lr * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
-            }
-    __syncthreads();
-    const int c = tid & (BN - 1), col = n0 + c;
-    float csum = 0.f;
-    if (col < d.N) {
-        if (S > 1) {
-            for (int lr = tid >> 7; lr < BM; lr += 2) {
-                const int row = m0 + lr;
-                if (row >= M) break;
-                d.ws[((int64_t)zt * d.M + row) * d.N + col] = Cs[lr * BN + c];
-            }
-        } else {
-            const float bcol = d.bias ? d.bias[col] : 0.f;
-            // eight rows per batch: their operand loads are in flight together
-            for (int lr0 = tid >> 7; lr0 < BM && m0 + lr0 < M; lr0 += 16) {
-                EpiIn e[8];
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // register set per stage: [A, A_lo, B, B_lo][2]; every load is issued (tiles
+    // past the slice read zeros), so each wait covers only the set it needs
+    uint4 r0[4][2], r1[4][2];
+    int ld_t = 0;
+    auto load_tile = [&](uint4 (&r)[4][2]) {
+        const int kb = kbeg + ld_t * CBK;
+        const int ke = ld_t < nk ? K : 0;
+        la.load(d.A, kb, ke, r[0]);
+        if (NSEG == 3) la.load(d.A2, kb, ke, r[1]);
+        lb.load(d.B, kb, ke, r[2]);
+        lb.load(d.B2, kb, ke, r[3]);
+        ++ld_t;
+    };
+    auto store_stage = [&](bf16_t (*st)[BM * CLD], const uint4 (&r)[4][2]) {
+        la.store(st[0], r[0], tid);
+        if (NSEG == 3) la.store(st[1], r[1], tid);
+        lb.store(st[2], r[2], tid);
+        lb.store(st[3], r[3], tid);
+    };
+    const int lrow = lane & 31, lk = (lane >> 5) * 8;
+    const int aoff = (wm * 64 + lrow) * CLD + lk, boff = (wn * 64 + lrow) * CLD + lk;
+    auto compute = [&](bf16_t (*st)[BM * CLD]) {
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int row = m0 + lr0 + 2 * u;
-                    if (row < M) e[u] = epi_load(d, row, col);
-                }
+        for (int ks = 0; ks < CBK / 16; ++ks) {
+            bf16x8_t a[2], al[2], b[2], bl[2];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int lr = lr0 + 2 * u, row = m0 + lr;
-                    if (row < M) csum += epi_store(d, row, col, Cs[lr * BN + c] + bcol + e[u].resid, e[u]);
-                }
+            for (int i = 0; i < 2; ++i) {
+                a[i] = *reinterpret_cast<const bf16x8_t*>(&st[0][aoff + i * 32 * CLD + ks * 16]);
+                if (NSEG == 3) al[i] = *reinterpret_cast<const bf16x8_t*>(&st[1][aoff + i * 32 * CLD + ks * 16]);
             }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                b[j] = *reinterpret_cast<const bf16x8_t*>(&st[2][boff + j * 32 * CLD + ks * 16]);
+                bl[j] = *reinterpret_cast<const bf16x8_t*>(&st[3][boff + j * 32 * CLD + ks * 16]);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bl[j], acc[i][j], 0, 0, 0);
+                    if (NSEG == 3)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], b[j], acc[i][j], 0, 0, 0);
+                }
         }
-    }
-    if (d.colpart) {  // uniform; the two row halves of a column meet in LDS
+    };
+
+    load_tile(r0);
+    load_tile(r1);
+    if (nk > 0) store_stage(smem[0], r0);
+    __syncthreads();
+    int t = 0;
+    for (; t + 1 < nk; t += 2) {  // two K tiles per trip, no exit inside the body
+        load_tile(r0);
+        compute(smem[0]);
+        store_stage(smem[1], r1);
         __syncthreads();
-        if (tid >= BN) Cs[c] = csum;
+        load_tile(r1);
+        compute(smem[1]);
+        if (t + 2 < nk) store_stage(smem[0], r0);
         __syncthreads();
-        if (tid < BN && col < d.N) d.colpart[(int64_t)mt * d.N + col] = csum + Cs[c];
     }
+    if (t < nk) {  // odd tile count: the last tile is in stage 0
+        compute(smem[0]);
+        __syncthreads();
+    }
+    store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
 }
 
 // Sums the split-K partials and runs the epilogue; four columns per thread
@@ -648,6 +807,21 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
             epilogue(d, (int)(i / d.N), (int)(i % d.N), v);
         }
     }
+}
+
+template <int NSEG>
+void launch_comp(const GemmDesc& d, hipStream_t s) {
+    ProfInfo pi;
+    pi.kind = PROF_GEMM;
+    pi.M = d.M; pi.N = d.N; pi.K = d.K; pi.nseg = d.nseg;
+    pi.Mdev = d.Mdev; pi.Kdev = d.Kdev;
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext(NSEG == 3 ? "gemm_comp_kernel<3>" : "gemm_comp_kernel<2>", pi, &ea, &eb);
+    GemmDesc dd = d;
+    dd.prof_snap = prof_snap(h);
+    dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
+    hipExtLaunchKernelGGL((gemm_comp_kernel<NSEG>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
+    prof_end_ext(h);
 }
 
 template <int AM, int BMODE, bool AL = false>
@@ -701,7 +875,9 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     // (a k-major A with a device-side row bound may end inside an 8-row chunk)
     const bool al = (a == OP_RK || a == OP_KR) && (b == OP_RK || b == OP_KR) && !(a == OP_KR && d.Mdev) &&
                     op_aligned(a, d.A, d.A2, d.lda, d.M) && op_aligned(b, d.B, d.B2, d.ldb, d.N);
-    if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(d, s) : launch<OP_RK, OP_RK>(d, s);
+    if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
+        d.nseg == 3 ? launch_comp<3>(d, s) : launch_comp<2>(d, s);
+    else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(d, s) : launch<OP_RK, OP_RK>(d, s);
     else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KR, true>(d, s) : launch<OP_RK, OP_KR>(d, s);
     else if (a == OP_KR && b == OP_KR) al ? launch<OP_KR, OP_KR, true>(d, s) : launch<OP_KR, OP_KR>(d, s);
     else if (a == OP_KR && b == OP_RK) al ? launch<OP_KR, OP_RK, true>(d, s) : launch<OP_KR, OP_RK>(d, s);

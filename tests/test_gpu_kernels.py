@@ -79,6 +79,26 @@ def test_gemm_compensated(M, N, K, with_alo):
     assert normwise(C.cpu().numpy(), av @ bv.T) <= 2e-5
 
 
+@pytest.mark.parametrize("M,N,K,splits,with_alo", [(300, 200, 1000, 3, True), (129, 640, 2048, 4, True),
+                                                    (256, 130, 512, 2, False)])
+def test_gemm_compensated_split_k(M, N, K, splits, with_alo):
+    """The single-pass compensated product with K slices (fp32 partials, reduction pass)."""
+    torch = torch_cuda()
+    announce(f"gemm compensated split-K {M}x{N}x{K} s={splits}")
+    rng = np.random.default_rng(M + K)
+    if with_alo:
+        ah, al, av = _split(rng, (M, K))
+    else:
+        ah, av = _bf16(rng, (M, K))
+        al = None
+    bh, bl, bv = _split(rng, (N, K))
+    C = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+    ws = torch.empty(splits * M * N, dtype=torch.float32, device="cuda")
+    A.fo_gemm_bf16(M, N, K, 0, _dev16(ah), None if al is None else _dev16(al), K, 0, _dev16(bh), _dev16(bl), K, C, N,
+                   splits, ws)
+    assert normwise(C.cpu().numpy(), av @ bv.T) <= 2e-5
+
+
 CONVS = [  # (Bn, H, Ci, Co, k, stride, pad)
     (2, 16, 64, 128, 3, 1, 1), (3, 8, 128, 256, 3, 1, 1), (2, 4, 256, 512, 3, 1, 1), (2, 2, 512, 512, 3, 1, 1),
     (32, 2, 512, 512, 3, 1, 1), (2, 16, 64, 128, 3, 2, 1), (4, 4, 256, 512, 3, 2, 1), (2, 16, 64, 128, 1, 2, 0),
