@@ -75,6 +75,7 @@ struct GemmDesc {
     const int* Mdev = nullptr;
     const int* Kdev = nullptr;
     int* prof_snap = nullptr;  // set by the launcher when profiling: receives (M, K) effective
+    int vec_epi = 0;           // set by the launcher: the epilogue may move four columns per access
 };
 
 // Enqueues the GEMM (and its split-K reduction) on stream s.

@@ -411,6 +411,74 @@ __device__ __forceinline__ float epilogue(const GemmDesc& d, int row, int col, f
     return epi_store(d, row, col, v + e.resid, e);
 }
 
+// The same epilogue on four consecutive columns (col % 4 == 0) with 16-byte
+// (fp32) and 8-byte (bf16) accesses, one address computation per operand; used
+// when the launcher found every operand aligned for it (vec_epi).
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ f32x4 bf4_to_f(u32x2 w) {
+    f32x4 f;
+    f.x = bf2f((bf16_t)(w.x & 0xFFFFu));
+    f.y = bf2f((bf16_t)(w.x >> 16));
+    f.z = bf2f((bf16_t)(w.y & 0xFFFFu));
+    f.w = bf2f((bf16_t)(w.y >> 16));
+    return f;
+}
+__device__ __forceinline__ u32x2 f_to_bf4(f32x4 v, f32x4* lo) {
+    const bf16_t h0 = f2bf(v.x), h1 = f2bf(v.y), h2 = f2bf(v.z), h3 = f2bf(v.w);
+    if (lo) {
+        lo->x = v.x - bf2f(h0);
+        lo->y = v.y - bf2f(h1);
+        lo->z = v.z - bf2f(h2);
+        lo->w = v.w - bf2f(h3);
+    }
+    u32x2 w;
+    w.x = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    w.y = (uint32_t)h2 | ((uint32_t)h3 << 16);
+    return w;
+}
+
+struct EpiIn4 {
+    f32x4 resid = {0.f, 0.f, 0.f, 0.f}, mask = {1.f, 1.f, 1.f, 1.f}, dpre = {0.f, 0.f, 0.f, 0.f};
+};
+
+__device__ __forceinline__ EpiIn4 epi_load4(const GemmDesc& d, int row, int col) {
+    EpiIn4 e;
+    if (d.resid) e.resid = *reinterpret_cast<const f32x4*>(d.resid + (int64_t)row * d.ldr + col);
+    if (d.mask) e.mask = bf4_to_f(*reinterpret_cast<const u32x2*>(d.mask + (int64_t)row * d.ldm + col));
+    if (d.dpre) e.dpre = bf4_to_f(*reinterpret_cast<const u32x2*>(d.dpre + (int64_t)row * d.ldm + col));
+    return e;
+}
+
+// v already holds bias and residual
+__device__ __forceinline__ f32x4 epi_store4(const GemmDesc& d, int row, int col, f32x4 v, const EpiIn4& e) {
+    if (d.act == ACT_GELU) {
+        if (d.pre) *reinterpret_cast<u32x2*>(d.pre + (int64_t)row * d.ldm + col) = f_to_bf4(v, nullptr);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = gelu_f(v[q]);
+    } else if (d.act == ACT_RELU) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = v[q] > 0.f ? v[q] : 0.f;
+    }
+    if (d.mask) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (!(e.mask[q] > 0.f)) v[q] = 0.f;
+    }
+    if (d.dpre) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] *= gelu_grad(e.dpre[q]);
+    }
+    if (d.Cf) *reinterpret_cast<f32x4*>(d.Cf + (int64_t)row * d.ldcf + col) = v;
+    if (d.Cb) {
+        f32x4 lo;
+        const int64_t o = (int64_t)row * d.ldcb + col;
+        *reinterpret_cast<u32x2*>(d.Cb + o) = f_to_bf4(v, d.Cb2 ? &lo : nullptr);
+        if (d.Cb2) *reinterpret_cast<u32x2*>(d.Cb2 + o) = f_to_bf4(lo, nullptr);
+    }
+    return v;
+}
+
 // ------------------------------------------------------------------ kernel
 // The K range over the concatenation of nseg segments (segment s pairs (A, B),
 // (A, B2), (A2, B) for s = 0, 1, 2), each padded to a whole number of K tiles
@@ -482,6 +550,53 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
                 Cs[lr * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
             }
     __syncthreads();
+    if (d.vec_epi) {
+        // four columns per thread (a wave covers two rows of 128): rows
+        // tid / 32 + 8 u, columns n0 + 4 (tid % 32) .. + 3
+        const int m0 = job.m0, c4 = (tid & 31) * 4, col = job.n0 + c4, rr = tid >> 5;
+        f32x4 csum = {0.f, 0.f, 0.f, 0.f};
+        if (col < d.N) {
+            if (job.S > 1) {
+                for (int lr = rr; lr < BM && m0 + lr < M; lr += 8)
+                    *reinterpret_cast<f32x4*>(d.ws + ((int64_t)job.zt * d.M + m0 + lr) * d.N + col) =
+                        *reinterpret_cast<const f32x4*>(&Cs[lr * BN + c4]);
+            } else {
+                f32x4 bias = {0.f, 0.f, 0.f, 0.f};
+                if (d.bias) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) bias[q] = d.bias[col + q];
+                }
+                for (int lr0 = rr; lr0 < BM && m0 + lr0 < M; lr0 += 64) {
+                    EpiIn4 e[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int row = m0 + lr0 + 8 * u;
+                        if (row < M) e[u] = epi_load4(d, row, col);
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int lr = lr0 + 8 * u, row = m0 + lr;
+                        if (row < M)
+                            csum += epi_store4(d, row, col,
+                                               *reinterpret_cast<const f32x4*>(&Cs[lr * BN + c4]) + bias + e[u].resid,
+                                               e[u]);
+                    }
+                }
+            }
+        }
+        if (d.colpart) {  // uniform; the eight row groups of a column meet in LDS
+            __syncthreads();
+            *reinterpret_cast<f32x4*>(&Cs[rr * BN + c4]) = csum;
+            __syncthreads();
+            if (tid < BN && job.n0 + tid < d.N) {
+                float t = 0.f;
+#pragma unroll
+                for (int g = 0; g < 8; ++g) t += Cs[g * BN + tid];
+                d.colpart[(int64_t)job.mt * d.N + job.n0 + tid] = t;
+            }
+        }
+        return;
+    }
     const int m0 = job.m0, c = tid & (BN - 1), col = job.n0 + c;
     float csum = 0.f;
     if (col < d.N) {
@@ -796,8 +911,18 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
             }
             for (; z < S; ++z) v += *reinterpret_cast<const f32x4*>(p + z * full);
             const int row = (int)(4 * i / d.N), col = (int)(4 * i % d.N);
+            if (d.vec_epi) {
+                f32x4 bias = {0.f, 0.f, 0.f, 0.f};
+                if (d.bias) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) epilogue(d, row, col + e, v[e]);
+                    for (int q = 0; q < 4; ++q) bias[q] = d.bias[col + q];
+                }
+                const EpiIn4 e = epi_load4(d, row, col);
+                epi_store4(d, row, col, v + bias + e.resid, e);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) epilogue(d, row, col + e, v[e]);
+            }
         }
     } else {
         const int64_t total = (int64_t)M * d.N;
@@ -865,6 +990,19 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
         FO_CHECK(d.B2 && (d.nseg == 2 || d.A2), "gemm: compensated product needs its low parts");
         FO_CHECK(!d.Kdev, "gemm: compensated product needs a static K");
     }
+    // four-column epilogue: N and every leading dimension multiples of 4, fp32
+    // operands 16-byte and bf16 operands 8-byte aligned
+    GemmDesc dv = d;
+    {
+        auto al = [](const void* p, uintptr_t m) { return p == nullptr || ((uintptr_t)p & (m - 1)) == 0; };
+        bool v = d.N % 4 == 0 && al(d.ws, 16) && al(d.Cf, 16) && al(d.resid, 16) && al(d.Cb, 8) && al(d.Cb2, 8) &&
+                 al(d.pre, 8) && al(d.mask, 8) && al(d.dpre, 8) && al(d.colpart, 4);
+        if (d.Cf) v = v && d.ldcf % 4 == 0;
+        if (d.resid) v = v && d.ldr % 4 == 0;
+        if (d.Cb) v = v && d.ldcb % 4 == 0;
+        if (d.pre || d.mask || d.dpre) v = v && d.ldm % 4 == 0;
+        dv.vec_epi = v ? 1 : 0;
+    }
     const int a = d.amode, b = d.bmode;
     // aligned variant: every contiguous dimension a multiple of 8 and 16-byte rows
     auto al16 = [](const void* p) { return p == nullptr || ((uintptr_t)p & 15) == 0; };
@@ -876,14 +1014,14 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     const bool al = (a == OP_RK || a == OP_KR) && (b == OP_RK || b == OP_KR) && !(a == OP_KR && d.Mdev) &&
                     op_aligned(a, d.A, d.A2, d.lda, d.M) && op_aligned(b, d.B, d.B2, d.ldb, d.N);
     if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
-        d.nseg == 3 ? launch_comp<3>(d, s) : launch_comp<2>(d, s);
-    else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(d, s) : launch<OP_RK, OP_RK>(d, s);
-    else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KR, true>(d, s) : launch<OP_RK, OP_KR>(d, s);
-    else if (a == OP_KR && b == OP_KR) al ? launch<OP_KR, OP_KR, true>(d, s) : launch<OP_KR, OP_KR>(d, s);
-    else if (a == OP_KR && b == OP_RK) al ? launch<OP_KR, OP_RK, true>(d, s) : launch<OP_KR, OP_RK>(d, s);
-    else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(d, s);
-    else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(d, s);
-    else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(d, s);
+        d.nseg == 3 ? launch_comp<3>(dv, s) : launch_comp<2>(dv, s);
+    else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(dv, s) : launch<OP_RK, OP_RK>(dv, s);
+    else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KR, true>(dv, s) : launch<OP_RK, OP_KR>(dv, s);
+    else if (a == OP_KR && b == OP_KR) al ? launch<OP_KR, OP_KR, true>(dv, s) : launch<OP_KR, OP_KR>(dv, s);
+    else if (a == OP_KR && b == OP_RK) al ? launch<OP_KR, OP_RK, true>(dv, s) : launch<OP_KR, OP_RK>(dv, s);
+    else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(dv, s);
+    else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(dv, s);
+    else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(dv, s);
     else {
         set_error("gemm: unsupported operand modes %d/%d", a, b);
         return FO_EINVAL;
@@ -895,7 +1033,7 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
         int grid = (int)std::min<int64_t>(cdiv(total, 256), 4096);
         hipEvent_t ea, eb;
         const int h = prof_begin_ext("splitk_reduce", ProfInfo(), &ea, &eb);
-        hipExtLaunchKernelGGL(splitk_reduce, dim3(grid), dim3(256), 0, s, ea, eb, 0, d);
+        hipExtLaunchKernelGGL(splitk_reduce, dim3(grid), dim3(256), 0, s, ea, eb, 0, dv);
         prof_end_ext(h);
         FO_LAUNCHED();
     }
