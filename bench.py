@@ -82,8 +82,8 @@ def cpu_baseline(cid, sample_steps):
 # the profiler's kernel names, the sources that define them).
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_bert_step.txt")
 TRAFFIC_KERNELS = {
-    "gemm_comp_kernel<3>": ("gemm_comp_kernel<3>", ["paper_2504_13850_amd/csrc/k_gemm.hip",
-                                                    "paper_2504_13850_amd/csrc/gemm.h"]),
+    "gemm_comp_dma_kernel<3>": ("gemm_comp_dma_kernel<3>", ["paper_2504_13850_amd/csrc/k_gemm.hip",
+                                                            "paper_2504_13850_amd/csrc/gemm.h"]),
     "gemm_kernel<0, 0>": ("gemm_kernel<0, 0,", ["paper_2504_13850_amd/csrc/k_gemm.hip",
                                                  "paper_2504_13850_amd/csrc/gemm.h"]),
     "agg_lerp_kernel": ("agg_lerp_kernel(", ["paper_2504_13850_amd/csrc/k_update.hip"]),

@@ -755,39 +755,46 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
 // row-major operands (K contiguous, K, lda, ldb multiples of 8): every K tile
 // stages the high and low parts of both operands once and issues the two or
 // three MFMAs of each fragment pair back to back, instead of running the K loop
-// once per segment.  Per MFMA that is two thirds of the LDS reads, two thirds
-// of the LDS writes and a third of the barriers of the segmented form.  K tiles
-// of 32 with rows padded to 40 elements (80 B: eight consecutive rows start 20
-// banks apart, so both the 16-byte stores and the operand reads are conflict
-// free) keep two stages of four tiles at 80 KB, two workgroups per CU.
-constexpr int CBK = 32, CLD = CBK + 8;
+// once per segment.  Per MFMA that is two thirds of the LDS reads and a third
+// of the barriers of the segmented form.
+constexpr int CBK = 32;
 
-struct LdRKc {  // one 128 x 32 tile: rows (tid / 4) + 64 v, k chunk (tid % 4) * 8
+// The operand tiles go straight from global memory into LDS
+// (global_load_lds_dwordx4: lane L of a wave writes 16 bytes at the
+// instruction's LDS base + 16 L), so there are no LDS store instructions and no
+// staging registers.  A 128 x 32 tile is 128 rows of 64 bytes, the 16-byte chunk c of
+// row r at position c ^ ((r / 4) mod 4): one instruction fills 16 rows, and
+// the operand reads of any eight consecutive rows hit distinct banks.  Two
+// stages in separate arrays (the halves of the unrolled loop name them
+// statically); the copy of tile t+1 is issued before the MFMAs of tile t.
+#define FO_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+
+struct DmaRKc {  // one 128 x 32 tile; this wave's instructions are q = wave and wave + 4
     int64_t off[2];
-    int kc;
-    __device__ void init(int64_t ld, int r0, int R, int tid) {
-        kc = (tid & 3) * 8;
+    int koff;
+    __device__ void init(int64_t ld, int r0, int R, int lane, int wave) {
+        koff = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
 #pragma unroll
         for (int v = 0; v < 2; ++v) {
-            const int gr = r0 + (tid >> 2) + 64 * v;
+            const int gr = r0 + 16 * (wave + 4 * v) + (lane >> 2);
             off[v] = gr < R ? (int64_t)gr * ld : -1;
         }
     }
-    __device__ void load(const bf16_t* P, int kb, int kend, uint4* r) const {
-        const int k = kb + kc;
+    __device__ void copy(const bf16_t* P, int kb, int kend, bf16_t* tile, int wave) const {
+        const int k = kb + koff;
 #pragma unroll
-        for (int v = 0; v < 2; ++v) r[v] = load8(off[v] >= 0 && k < kend ? P + off[v] + k : kZero8);
-    }
-    __device__ void store(bf16_t* t, const uint4* r, int tid) const {
-#pragma unroll
-        for (int v = 0; v < 2; ++v) *reinterpret_cast<uint4*>(&t[((tid >> 2) + 64 * v) * CLD + kc]) = r[v];
+        for (int v = 0; v < 2; ++v)
+            __builtin_amdgcn_global_load_lds(off[v] >= 0 && k < kend ? P + off[v] + k : kZero8,
+                                             FO_LDS(tile + (wave + 4 * v) * 512), 16, 0, 0);
     }
 };
 
 template <int NSEG>
-__global__ void __launch_bounds__(NT, 2) gemm_comp_kernel(const GemmDesc d) {
-    // two stages of four 128 x 40 tiles (A, A_lo, B, B_lo) = 80 KB; reused for the C tile
-    __shared__ __attribute__((aligned(16))) bf16_t smem[2][4][BM * CLD];
+__global__ void __launch_bounds__(NT, 2) gemm_comp_dma_kernel(const GemmDesc d) {
+    // two stages of four unpadded 128 x 32 tiles (A, A_lo, B, B_lo) = 64 KB; reused for the C tile
+    __shared__ __attribute__((aligned(1024))) bf16_t smem[2][4][BM * CBK];
+    bf16_t (*st0)[BM * CBK] = smem[0];
+    bf16_t (*st1)[BM * CBK] = smem[1];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
@@ -797,7 +804,6 @@ __global__ void __launch_bounds__(NT, 2) gemm_comp_kernel(const GemmDesc d) {
         d.prof_snap[1] = K;
     }
     TileJob job;
-    // the slice count follows the segmented form's rule (the reduction pass uses it too)
     if (!map_tile(d, M, d.nseg * gemm_kseg(d, K), job)) return;  // uniform for the whole workgroup
     const int S = job.S;
     const int kpad = (K + CBK - 1) / CBK * CBK;
@@ -806,9 +812,9 @@ __global__ void __launch_bounds__(NT, 2) gemm_comp_kernel(const GemmDesc d) {
     const int kstop = min(kpad, kbeg + kc);
     const int nk = kstop > kbeg ? (kstop - kbeg) / CBK : 0;
 
-    LdRKc la, lb;
-    la.init(d.lda, job.m0, M, tid);
-    lb.init(d.ldb, job.n0, d.N, tid);
+    DmaRKc la, lb;
+    la.init(d.lda, job.m0, M, lane, wave);
+    lb.init(d.ldb, job.n0, d.N, lane, wave);
 
     f32x16 acc[2][2];
 #pragma unroll
@@ -818,40 +824,33 @@ __global__ void __launch_bounds__(NT, 2) gemm_comp_kernel(const GemmDesc d) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    // register set per stage: [A, A_lo, B, B_lo][2]; every load is issued (tiles
-    // past the slice read zeros), so each wait covers only the set it needs
-    uint4 r0[4][2], r1[4][2];
-    int ld_t = 0;
-    auto load_tile = [&](uint4 (&r)[4][2]) {
-        const int kb = kbeg + ld_t * CBK;
-        const int ke = ld_t < nk ? K : 0;
-        la.load(d.A, kb, ke, r[0]);
-        if (NSEG == 3) la.load(d.A2, kb, ke, r[1]);
-        lb.load(d.B, kb, ke, r[2]);
-        lb.load(d.B2, kb, ke, r[3]);
-        ++ld_t;
+    auto copy_tile = [&](bf16_t (*st)[BM * CBK], int t) {
+        const int kb = kbeg + t * CBK;
+        la.copy(d.A, kb, K, st[0], wave);
+        if (NSEG == 3) la.copy(d.A2, kb, K, st[1], wave);
+        lb.copy(d.B, kb, K, st[2], wave);
+        lb.copy(d.B2, kb, K, st[3], wave);
     };
-    auto store_stage = [&](bf16_t (*st)[BM * CLD], const uint4 (&r)[4][2]) {
-        la.store(st[0], r[0], tid);
-        if (NSEG == 3) la.store(st[1], r[1], tid);
-        lb.store(st[2], r[2], tid);
-        lb.store(st[3], r[3], tid);
+    const int lrow = lane & 31, lc = lane >> 5;
+    auto frag = [&](const bf16_t* t, int row, int ks) {
+        const int C = 2 * ks + lc;
+        return *reinterpret_cast<const bf16x8_t*>(&t[row * CBK + 8 * (C ^ ((row >> 2) & 3))]);
     };
-    const int lrow = lane & 31, lk = (lane >> 5) * 8;
-    const int aoff = (wm * 64 + lrow) * CLD + lk, boff = (wn * 64 + lrow) * CLD + lk;
-    auto compute = [&](bf16_t (*st)[BM * CLD]) {
+    auto compute = [&](bf16_t (*st)[BM * CBK]) {
 #pragma unroll
         for (int ks = 0; ks < CBK / 16; ++ks) {
             bf16x8_t a[2], al[2], b[2], bl[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
-                a[i] = *reinterpret_cast<const bf16x8_t*>(&st[0][aoff + i * 32 * CLD + ks * 16]);
-                if (NSEG == 3) al[i] = *reinterpret_cast<const bf16x8_t*>(&st[1][aoff + i * 32 * CLD + ks * 16]);
+                const int row = wm * 64 + i * 32 + lrow;
+                a[i] = frag(st[0], row, ks);
+                if (NSEG == 3) al[i] = frag(st[1], row, ks);
             }
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                b[j] = *reinterpret_cast<const bf16x8_t*>(&st[2][boff + j * 32 * CLD + ks * 16]);
-                bl[j] = *reinterpret_cast<const bf16x8_t*>(&st[3][boff + j * 32 * CLD + ks * 16]);
+                const int row = wn * 64 + j * 32 + lrow;
+                b[j] = frag(st[2], row, ks);
+                bl[j] = frag(st[3], row, ks);
             }
 #pragma unroll
             for (int i = 0; i < 2; ++i)
@@ -865,23 +864,22 @@ __global__ void __launch_bounds__(NT, 2) gemm_comp_kernel(const GemmDesc d) {
         }
     };
 
-    load_tile(r0);
-    load_tile(r1);
-    if (nk > 0) store_stage(smem[0], r0);
-    __syncthreads();
+    if (nk > 0) copy_tile(st0, 0);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed
+    __syncthreads();                // and every other wave's
     int t = 0;
-    for (; t + 1 < nk; t += 2) {  // two K tiles per trip, no exit inside the body
-        load_tile(r0);
-        compute(smem[0]);
-        store_stage(smem[1], r1);
+    for (; t + 1 < nk; t += 2) {
+        copy_tile(st1, t + 1);
+        compute(st0);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-        load_tile(r1);
-        compute(smem[1]);
-        if (t + 2 < nk) store_stage(smem[0], r0);
+        if (t + 2 < nk) copy_tile(st0, t + 2);
+        compute(st1);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
-    if (t < nk) {  // odd tile count: the last tile is in stage 0
-        compute(smem[0]);
+    if (t < nk) {
+        compute(st0);
         __syncthreads();
     }
     store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
@@ -941,11 +939,11 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
     pi.M = d.M; pi.N = d.N; pi.K = d.K; pi.nseg = d.nseg;
     pi.Mdev = d.Mdev; pi.Kdev = d.Kdev;
     hipEvent_t ea, eb;
-    const int h = prof_begin_ext(NSEG == 3 ? "gemm_comp_kernel<3>" : "gemm_comp_kernel<2>", pi, &ea, &eb);
+    const int h = prof_begin_ext(NSEG == 3 ? "gemm_comp_dma_kernel<3>" : "gemm_comp_dma_kernel<2>", pi, &ea, &eb);
     GemmDesc dd = d;
     dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
-    hipExtLaunchKernelGGL((gemm_comp_kernel<NSEG>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
+    hipExtLaunchKernelGGL((gemm_comp_dma_kernel<NSEG>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
     prof_end_ext(h);
 }
 
