@@ -26,8 +26,12 @@
  *   - Every argument is checked on the host before anything is launched; a
  *     failing check launches nothing and returns a negative fo_status.  The
  *     message for the last failure of the calling thread is fo_last_error().
- *   - The library never allocates inside fo_server_step / fo_async_aggregate /
- *     fo_pick_device; all device memory is allocated by the *_create calls.
+ *   - The library never allocates device memory inside fo_server_step /
+ *     fo_async_aggregate / fo_pick_device; all device memory is allocated by
+ *     the *_create calls.  In graph mode (fo_set_graph_mode) the first
+ *     fo_server_step of a model at a new batch size creates a private capture
+ *     stream and instantiates a HIP graph (host-side objects, freed by
+ *     fo_model_destroy).
  */
 #ifndef FEDOPTIMA_H
 #define FEDOPTIMA_H
@@ -111,6 +115,18 @@ FO_API void fo_model_destroy(fo_model* model);
  * missing for config 4, device_id < 0), FO_EHIP. */
 FO_API fo_status fo_server_step(fo_model* model, const fo_acts* acts, const int32_t* labels,
                          int32_t device_id);
+
+/* Process-wide switch for how fo_server_step issues its kernels (default 1).
+ * Every step of a model at one batch size is the same sequence of launches
+ * over the same buffers, so with enable != 0 the step copies the batch (and
+ * labels, lengths) into staging buffers owned by the model, captures the
+ * launch sequence once per batch size into a HIP graph on a private stream,
+ * and replays that graph on the model's stream afterwards.  Results are
+ * bit-identical to enable == 0, which launches every kernel directly.  While
+ * the calling thread profiles (fo_profile_enable) steps always launch
+ * directly.  Steps already captured stay cached until fo_model_destroy.
+ * Returns FO_OK. */
+FO_API fo_status fo_set_graph_mode(int32_t enable);
 
 /* Steps taken so far on batches from `device_id` (all devices if -1). */
 FO_API int64_t fo_model_steps(const fo_model* model, int32_t device_id);

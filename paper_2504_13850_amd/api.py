@@ -26,7 +26,7 @@ EXPORTS = [
     "fo_queues_push", "fo_queues_push_model", "fo_pick_device", "fo_queues_in_service",
     "fo_queues_release", "fo_aggregate_pending", "fo_aggregate_pending_all", "fo_queues_stats",
     "fo_queues_counters", "fo_queues_add_device", "fo_last_error", "fo_profile_enable", "fo_profile_read",
-    "fo_gemm_bf16", "fo_conv2d_bf16",
+    "fo_set_graph_mode", "fo_gemm_bf16", "fo_conv2d_bf16",
 ]
 FO_LAYOUT_ROW_K, FO_LAYOUT_K_ROW = 0, 1
 
@@ -100,6 +100,7 @@ def lib():
             "fo_queues_add_device": (i32, [vp]),
             "fo_last_error": (C.c_char_p, []),
             "fo_profile_enable": (C.c_int, [i32]),
+            "fo_set_graph_mode": (C.c_int, [i32]),
             "fo_profile_read": (i32, [C.POINTER(fo_kernel_stat), i32]),
             "fo_gemm_bf16": (C.c_int, [i32, i32, i32, i32, vp, vp, i64, i32, vp, vp, i64, vp, i64, i32, vp, vp]),
             "fo_conv2d_bf16": (C.c_int, [i32, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32,
@@ -172,6 +173,10 @@ def fo_server_step(model, acts, labels, device_id: int):
     if not isinstance(acts, fo_acts):
         acts = make_acts(*acts) if isinstance(acts, tuple) else make_acts(acts)
     return _check(lib().fo_server_step(model, C.byref(acts), _dptr(labels), device_id))
+
+
+def fo_set_graph_mode(enable: bool):
+    _check(lib().fo_set_graph_mode(1 if enable else 0))
 
 
 def fo_model_steps(model, device_id: int = -1) -> int:

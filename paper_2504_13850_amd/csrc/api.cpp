@@ -7,6 +7,7 @@
 #include <new>
 
 #include "model.h"
+#include "prof.h"
 
 namespace fo {
 
@@ -90,6 +91,9 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
     if (bf16) add(sizeof(bf16_t) * np);               // shadow (low part)
     add(sizeof(float) * (size_t)max_batch * m->classes);
     add(sizeof(float) * 64);
+    add((size_t)fam->sample_bytes * max_batch);       // staged batch (graph replay)
+    add(sizeof(int32_t) * max_batch);                 // staged labels
+    add(sizeof(int32_t) * max_batch);                 // staged lengths
     bytes += fam->workspace_bytes(m) + 4096;
     hipError_t e = hipMalloc((void**)&m->mem, bytes);
     if (e != hipSuccess) {
@@ -106,6 +110,9 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
     if (bf16) m->w16lo = m->arena.take<bf16_t>(np);
     m->logits = m->arena.take<float>((size_t)max_batch * m->classes);
     m->loss = m->arena.take<float>(64);
+    m->stage_x = m->arena.take<char>((size_t)fam->sample_bytes * max_batch);
+    m->stage_labels = m->arena.take<int32_t>(max_batch);
+    m->stage_lengths = m->arena.take<int32_t>(max_batch);
     fo_status st = FO_OK;
     e = hipMemcpyAsync(m->params, host_init, sizeof(float) * np, hipMemcpyHostToDevice, m->stream);
     if (e == hipSuccess) e = hipMemsetAsync(m->grads, 0, sizeof(float) * np, m->stream);
@@ -134,9 +141,85 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
 extern "C" void fo_model_destroy(fo_model* m) {
     if (!m) return;
     if (m->mem) (void)hipStreamSynchronize(m->stream);
+    for (auto& kv : m->graphs) (void)hipGraphExecDestroy(kv.second);
+    m->graphs.clear();
+    if (m->capture_stream) (void)hipStreamDestroy(m->capture_stream);
     if (m->fam && m->plan) m->fam->destroy(m);
     if (m->mem) (void)hipFree(m->mem);
     delete m;
+}
+
+// ------------------------------------------------------------------ graph replay of the step
+// A step is a fixed sequence of launches for a given batch size (sizes that
+// depend on the batch's contents, such as the packed token count, stay on the
+// device), so it is captured once per batch size into a HIP graph and replayed:
+// one launch instead of one per kernel.  The batch, labels and lengths are first
+// copied into model-owned buffers, so the graph never names the caller's
+// pointers.  Capture runs on a private stream (the null stream cannot be
+// captured) with the model's stream swapped for it; replays go to the model's
+// stream.
+static int g_graph_mode = 1;
+
+static fo_status step_graph(fo_model* m, const fo_acts* acts, const int32_t* labels) {
+    const int B = acts->batch;
+    hipError_t e = hipMemcpyAsync(m->stage_x, acts->x, (size_t)m->fam->sample_bytes * B, hipMemcpyDeviceToDevice,
+                                  m->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(m->stage_labels, labels, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, m->stream);
+    if (e == hipSuccess && acts->lengths)
+        e = hipMemcpyAsync(m->stage_lengths, acts->lengths, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, m->stream);
+    if (e != hipSuccess) {
+        set_error("fo_server_step: staging copy: %s", hipGetErrorString(e));
+        return FO_EHIP;
+    }
+    auto it = m->graphs.find(B);
+    if (it == m->graphs.end()) {
+        if (!m->capture_stream && hipStreamCreateWithFlags(&m->capture_stream, hipStreamNonBlocking) != hipSuccess) {
+            m->capture_stream = nullptr;
+            set_error("fo_server_step: hipStreamCreateWithFlags failed");
+            return FO_EHIP;
+        }
+        fo_acts staged;
+        staged.x = m->stage_x;
+        staged.lengths = acts->lengths ? m->stage_lengths : nullptr;
+        staged.batch = B;
+        hipStream_t user = m->stream;
+        e = hipStreamBeginCapture(m->capture_stream, hipStreamCaptureModeThreadLocal);
+        if (e != hipSuccess) {
+            set_error("fo_server_step: hipStreamBeginCapture: %s", hipGetErrorString(e));
+            return FO_EHIP;
+        }
+        m->stream = m->capture_stream;
+        const fo_status st = m->fam->step(m, &staged, m->stage_labels);
+        m->stream = user;
+        hipGraph_t g = nullptr;
+        e = hipStreamEndCapture(m->capture_stream, &g);
+        if (st != FO_OK || e != hipSuccess) {
+            if (g) (void)hipGraphDestroy(g);
+            if (st != FO_OK) return st;
+            set_error("fo_server_step: hipStreamEndCapture: %s", hipGetErrorString(e));
+            return FO_EHIP;
+        }
+        hipGraphExec_t ex = nullptr;
+        e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(g);
+        if (e != hipSuccess) {
+            set_error("fo_server_step: hipGraphInstantiate: %s", hipGetErrorString(e));
+            return FO_EHIP;
+        }
+        it = m->graphs.emplace(B, ex).first;
+    }
+    e = hipGraphLaunch(it->second, m->stream);
+    if (e != hipSuccess) {
+        set_error("fo_server_step: hipGraphLaunch: %s", hipGetErrorString(e));
+        return FO_EHIP;
+    }
+    return FO_OK;
+}
+
+extern "C" fo_status fo_set_graph_mode(int32_t enable) {
+    g_graph_mode = enable != 0;
+    return FO_OK;
 }
 
 extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int32_t* labels, int32_t device_id) {
@@ -148,7 +231,8 @@ extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int3
     FO_CHECK(device_id >= 0, "fo_server_step: device_id=%d must be >= 0", device_id);
     FO_CHECK(m->cid != 4 || acts->lengths != nullptr, "fo_server_step: config 4 needs sequence lengths");
     FO_CHECK(((uintptr_t)acts->x % 16) == 0, "fo_server_step: activations not 16-byte aligned");
-    fo_status st = m->fam->step(m, acts, labels);
+    // Kernel profiling records every launch with its own events: run eagerly then.
+    fo_status st = (g_graph_mode && !prof_active()) ? step_graph(m, acts, labels) : m->fam->step(m, acts, labels);
     if (st != FO_OK) return st;
     m->last_batch = acts->batch;
     m->steps_total++;

@@ -1,6 +1,7 @@
 // The server model object behind fo_model and the per-family executors.
 #pragma once
 
+#include <map>
 #include <vector>
 
 #include "kernels.h"
@@ -30,6 +31,14 @@ struct fo_model {
     int64_t steps_total = 0;
     std::vector<int64_t> steps_per_device;
 
+    // Graph replay of the step: the batch is first copied into these model-owned
+    // buffers, so the captured launches never name the caller's pointers.
+    void* stage_x = nullptr;             // max_batch * sample bytes
+    int32_t* stage_labels = nullptr;     // [max_batch]
+    int32_t* stage_lengths = nullptr;    // [max_batch]
+    hipStream_t capture_stream = nullptr;  // private (capture cannot run on the null stream)
+    std::map<int32_t, hipGraphExec_t> graphs;  // one per batch size
+
     char* mem = nullptr;       // one allocation for everything above and the workspace
     fo::Arena arena;
     const fo::Family* fam = nullptr;
@@ -39,6 +48,8 @@ struct fo_model {
 namespace fo {
 
 struct Family {
+    // Bytes of one input sample at the boundary (activations of one batch row).
+    int64_t sample_bytes;
     // Bytes of workspace (beyond params/grads/...) for batches up to max_batch.
     size_t (*workspace_bytes)(const fo_model* m);
     // Carve the plan out of m->arena; called once after the flat buffers exist.

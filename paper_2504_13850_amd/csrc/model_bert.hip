@@ -577,7 +577,7 @@ void destroy(fo_model* m) {
 int64_t bert_param_count() { return kParams; }
 
 const Family* family_bert() {
-    static const Family f = {ws_bytes, init, step, destroy};
+    static const Family f = {(int64_t)L * D * 2, ws_bytes, init, step, destroy};
     return &f;
 }
 

@@ -556,7 +556,7 @@ void destroy(fo_model* m) {
 int64_t cnn16_param_count(int32_t cid) { return count_params(cid); }
 
 const Family* family_cnn16() {
-    static const Family f = {ws_bytes, init, step, destroy};
+    static const Family f = {(int64_t)kIn * kHW * kHW * 2, ws_bytes, init, step, destroy};
     return &f;
 }
 

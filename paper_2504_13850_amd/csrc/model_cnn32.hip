@@ -296,7 +296,7 @@ void destroy(fo_model* m) {
 int64_t cnn32_param_count() { return kParams; }
 
 const Family* family_cnn32() {
-    static const Family f = {ws_bytes, init, step, destroy};
+    static const Family f = {(int64_t)C0 * H0 * W0 * 4, ws_bytes, init, step, destroy};
     return &f;
 }
 

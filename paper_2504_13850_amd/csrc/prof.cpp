@@ -77,6 +77,8 @@ void prof_end_ext(int h) {
     p->recs[h].closed = true;
 }
 
+bool prof_active() { return tl_prof != nullptr; }
+
 int* prof_snap(int h) {
     Profiler* p = tl_prof;
     if (!p || h < 0 || h >= (int)p->recs.size()) return nullptr;

@@ -30,6 +30,7 @@ void prof_end(int h, hipStream_t s);
 int prof_begin_ext(const char* name, const ProfInfo& info, hipEvent_t* a, hipEvent_t* b);
 void prof_end_ext(int h);
 int* prof_snap(int h);  // NULL when h < 0
+bool prof_active();     // the calling thread is recording launches
 constexpr int kProfSnapInts = 258;  // capacity of one snapshot (cu of up to 257 offsets)
 
 }  // namespace fo
