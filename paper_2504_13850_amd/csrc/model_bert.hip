@@ -45,10 +45,17 @@ struct Plan {
     float* Xf[NL + 1];
     LayerAct a[NL];
     float *dY[2], *du2f, *dHf, *du1f;
-    bf16_t *du2b, *dA1, *du1b, *dO, *dqkv;
-    float *splitws, *colws, *lnpart, *slws;
+    // operands of the weight gradients, one set per layer parity: the gradients
+    // of layer l run on the side stream while the main stream goes on to l - 1
+    bf16_t *du2b[2], *dA1[2], *du1b[2], *dqkv[2];
+    bf16_t* dO;
+    float *splitws, *splitws2, *colws, *lnpart, *slws;
     int split_qkv, split_o, split_f1, split_f2;
     float *xc, *pooled, *dz, *dpool, *dxc;
+    hipStream_t side = nullptr;      // weight gradients of the backward
+    hipEvent_t ev_fork = nullptr;    // main -> side: an operand is ready
+    hipEvent_t ev_done[2] = {};      // side -> main: a parity's operands are free again
+    hipEvent_t ev_join = nullptr;    // side -> main: every weight gradient is written
 };
 
 // ------------------------------------------------------------------ kernels
@@ -255,7 +262,10 @@ size_t ws_bytes(const fo_model* m) {
     }
     add(4 * R * D); add(4 * R * D);                 // dY[2]
     add(4 * R * D); add(4 * R * D); add(4 * R * D); // du2f, dHf, du1f
-    add(2 * R * D); add(2 * R * FF); add(2 * R * D); add(2 * R * D); add(2 * R * 3 * D);
+    for (int p = 0; p < 2; ++p) {
+        add(2 * R * D); add(2 * R * FF); add(2 * R * D); add(2 * R * 3 * D);  // du2b, dA1, du1b, dqkv
+    }
+    add(2 * R * D);                                 // dO
     const int K = (int)R;
     size_t sw = 0;
     sw = std::max(sw, gemm_ws_bytes(3 * D, D, split_for(3 * D, D, K)));
@@ -264,6 +274,7 @@ size_t ws_bytes(const fo_model* m) {
     sw = std::max(sw, gemm_ws_bytes(D, FF, split_for(D, FF, K)));
     sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
     add(sw);
+    add(sw);  // the side stream's split-K partials
     add(4 * colsum_ws_floats((int)R, FF));
     add(4 * (size_t)cdiv(R, LNB_ROWS) * 3 * D);
     add(4 * small_linear_ws_floats((int)B, D, D));
@@ -333,11 +344,13 @@ fo_status init(fo_model* m) {
     P->du2f = a.take<float>(R * D);
     P->dHf = a.take<float>(R * D);
     P->du1f = a.take<float>(R * D);
-    P->du2b = a.take<bf16_t>(R * D);
-    P->dA1 = a.take<bf16_t>(R * FF);
-    P->du1b = a.take<bf16_t>(R * D);
+    for (int p = 0; p < 2; ++p) {
+        P->du2b[p] = a.take<bf16_t>(R * D);
+        P->dA1[p] = a.take<bf16_t>(R * FF);
+        P->du1b[p] = a.take<bf16_t>(R * D);
+        P->dqkv[p] = a.take<bf16_t>(R * 3 * D);
+    }
     P->dO = a.take<bf16_t>(R * D);
-    P->dqkv = a.take<bf16_t>(R * 3 * D);
     const int K = (int)R;
     P->split_qkv = split_for(3 * D, D, K);
     P->split_o = split_for(D, D, K);
@@ -350,6 +363,7 @@ fo_status init(fo_model* m) {
     sw = std::max(sw, gemm_ws_bytes(D, FF, P->split_f2));
     sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
     P->splitws = a.take<float>(sw / 4 + 1);
+    P->splitws2 = a.take<float>(sw / 4 + 1);
     P->colws = a.take<float>(colsum_ws_floats((int)R, FF));
     P->lnpart = a.take<float>((size_t)cdiv(R, LNB_ROWS) * 3 * D);
     P->slws = a.take<float>(small_linear_ws_floats((int)B, D, D));
@@ -362,6 +376,17 @@ fo_status init(fo_model* m) {
         set_error("bert: workspace arena too small");
         return FO_ENOMEM;
     }
+    // default priority, no implicit ordering with the null stream
+    FO_HIP(hipStreamCreateWithFlags(&P->side, hipStreamNonBlocking));
+    for (hipEvent_t* e : {&P->ev_fork, &P->ev_done[0], &P->ev_done[1], &P->ev_join})
+        FO_HIP(hipEventCreateWithFlags(e, hipEventDisableTiming));
+    return FO_OK;
+}
+
+// Orders `to` after everything enqueued so far on `from`.
+fo_status order_after(hipStream_t to, hipStream_t from, hipEvent_t e) {
+    FO_HIP(hipEventRecord(e, from));
+    FO_HIP(hipStreamWaitEvent(to, e, 0));
     return FO_OK;
 }
 
@@ -472,103 +497,126 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     hipLaunchKernelGGL(scatter_cls_kernel, dim3(B), dim3(256), 0, s, P->dxc, P->cu, B, P->dY[0]);
     FO_LAUNCHED();
 
+    // Weight gradients go to the side stream as soon as their operands exist;
+    // the main stream carries the input-gradient chain.  Layer l's operands sit
+    // in the parity l % 2 buffers, which layer l - 2 reuses only after the side
+    // stream has finished with them.
+    hipStream_t s2 = P->side;
     int cur = 0;
     for (int l = NL - 1; l >= 0; --l) {
         const LayerOff& f = P->off[l];
         LayerAct& t = P->a[l];
         float* dY = P->dY[cur];
+        const int pb = l & 1;
+        bf16_t *du2b = P->du2b[pb], *dA1 = P->dA1[pb], *du1b = P->du1b[pb], *dqkv = P->dqkv[pb];
+        if (l + 2 < NL) FO_HIP(hipStreamWaitEvent(s, P->ev_done[pb], 0));
         // LN2
-        TRY(ln_bwd(P, dY, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, P->du2b, grd + f.g2, grd + f.b2,
+        TRY(ln_bwd(P, dY, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, du2b, grd + f.g2, grd + f.b2,
                    grd + f.bf2, s));
+        TRY(order_after(s2, s, P->ev_fork));
         // FFN2: dG = du2 W2 (times GELU'(pre1) -> dA1), dW2 = du2^T G, db2
         {
+            GemmDesc w;
+            w.M = D; w.N = FF; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = du2b; w.lda = D;
+            w.bmode = OP_KR; w.B = t.G; w.ldb = FF;
+            w.Cf = grd + f.w2; w.ldcf = FF;
+            w.splits = P->split_f2; w.ws = P->splitws2;
+            TRY(gemm(w, s2));
             GemmDesc d;
             d.M = rows; d.N = FF; d.K = D; d.Mdev = Tdev;
-            d.amode = OP_RK; d.A = P->du2b; d.lda = D;
+            d.amode = OP_RK; d.A = du2b; d.lda = D;
             d.bmode = OP_KR; d.B = W + f.w2; d.ldb = FF;
             d.dpre = t.pre1; d.ldm = FF;
-            d.Cb = P->dA1; d.ldcb = FF;
+            d.Cb = dA1; d.ldcb = FF;
             d.colpart = P->colws;
             TRY(gemm(d, s));
             ColOut cb;
             cb.p[0] = grd + f.bf1;
             cb.seg = FF;
             TRY(launch_colsum_finish(P->colws, rows, Tdev, 128, FF, cb, s));
-            GemmDesc w;
-            w.M = D; w.N = FF; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = P->du2b; w.lda = D;
-            w.bmode = OP_KR; w.B = t.G; w.ldb = FF;
-            w.Cf = grd + f.w2; w.ldcf = FF;
-            w.splits = P->split_f2; w.ws = P->splitws;
-            TRY(gemm(w, s));
+            TRY(order_after(s2, s, P->ev_fork));
         }
         // FFN1: dH = du2 + dA1 W1, dW1 = dA1^T H, db1
         {
+            GemmDesc w;
+            w.M = FF; w.N = D; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = dA1; w.lda = FF;
+            w.bmode = OP_KR; w.B = t.Hb; w.ldb = D;
+            w.Cf = grd + f.w1; w.ldcf = D;
+            w.splits = P->split_f1; w.ws = P->splitws2;
+            TRY(gemm(w, s2));
             GemmDesc d;
             d.M = rows; d.N = D; d.K = FF; d.Mdev = Tdev;
-            d.amode = OP_RK; d.A = P->dA1; d.lda = FF;
+            d.amode = OP_RK; d.A = dA1; d.lda = FF;
             d.bmode = OP_KR; d.B = W + f.w1; d.ldb = D;
             d.resid = P->du2f; d.ldr = D;
             d.Cf = P->dHf; d.ldcf = D;
             d.splits = split_rows(FF); d.ws = P->splitws;
             TRY(gemm(d, s));
-            GemmDesc w;
-            w.M = FF; w.N = D; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = P->dA1; w.lda = FF;
-            w.bmode = OP_KR; w.B = t.Hb; w.ldb = D;
-            w.Cf = grd + f.w1; w.ldcf = D;
-            w.splits = P->split_f1; w.ws = P->splitws;
-            TRY(gemm(w, s));
         }
         // LN1
-        TRY(ln_bwd(P, P->dHf, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, P->du1b, grd + f.g1,
+        TRY(ln_bwd(P, P->dHf, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, du1b, grd + f.g1,
                    grd + f.b1, grd + f.bo, s));
+        TRY(order_after(s2, s, P->ev_fork));
         // output projection: dO = du1 Wo, dWo = du1^T O, dbo
         {
+            GemmDesc w;
+            w.M = D; w.N = D; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = du1b; w.lda = D;
+            w.bmode = OP_KR; w.B = t.O; w.ldb = D;
+            w.Cf = grd + f.wo; w.ldcf = D;
+            w.splits = P->split_o; w.ws = P->splitws2;
+            TRY(gemm(w, s2));
             GemmDesc d;
             d.M = rows; d.N = D; d.K = D; d.Mdev = Tdev;
-            d.amode = OP_RK; d.A = P->du1b; d.lda = D;
+            d.amode = OP_RK; d.A = du1b; d.lda = D;
             d.bmode = OP_KR; d.B = W + f.wo; d.ldb = D;
             d.Cb = P->dO; d.ldcb = D;
             d.splits = split_rows(D); d.ws = P->splitws;
             TRY(gemm(d, s));
-            GemmDesc w;
-            w.M = D; w.N = D; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = P->du1b; w.lda = D;
-            w.bmode = OP_KR; w.B = t.O; w.ldb = D;
-            w.Cf = grd + f.wo; w.ldcf = D;
-            w.splits = P->split_o; w.ws = P->splitws;
-            TRY(gemm(w, s));
         }
-        TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, P->dqkv, B, NH, D, s));
-        // input projection: dX = du1 + dqkv Wqkv (skipped for the first server layer), dWqkv, dbqkv
+        TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, dqkv, B, NH, D, s));
+        TRY(order_after(s2, s, P->ev_fork));
+        // input projection: dWqkv on the side stream; dX = du1 + dqkv Wqkv (skipped
+        // for the first server layer) and dbqkv on the main stream
+        {
+            GemmDesc w;
+            w.M = 3 * D; w.N = D; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = dqkv; w.lda = 3 * D;
+            w.bmode = OP_KR; w.B = P->Xb[l]; w.ldb = D;
+            w.Cf = grd + f.wqkv; w.ldcf = D;
+            w.splits = P->split_qkv; w.ws = P->splitws2;
+            TRY(gemm(w, s2));
+            FO_HIP(hipEventRecord(P->ev_done[pb], s2));
+        }
         if (l > 0) {
             GemmDesc d;
             d.M = rows; d.N = D; d.K = 3 * D; d.Mdev = Tdev;
-            d.amode = OP_RK; d.A = P->dqkv; d.lda = 3 * D;
+            d.amode = OP_RK; d.A = dqkv; d.lda = 3 * D;
             d.bmode = OP_KR; d.B = W + f.wqkv; d.ldb = D;
             d.resid = P->du1f; d.ldr = D;
             d.Cf = P->dY[cur ^ 1]; d.ldcf = D;
             d.splits = split_rows(3 * D); d.ws = P->splitws;
             TRY(gemm(d, s));
         }
-        GemmDesc w;
-        w.M = 3 * D; w.N = D; w.K = rows; w.Kdev = Tdev;
-        w.amode = OP_KR; w.A = P->dqkv; w.lda = 3 * D;
-        w.bmode = OP_KR; w.B = P->Xb[l]; w.ldb = D;
-        w.Cf = grd + f.wqkv; w.ldcf = D;
-        w.splits = P->split_qkv; w.ws = P->splitws;
-        TRY(gemm(w, s));
-        TRY(launch_colsum(P->dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws, s));
+        TRY(launch_colsum(dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws, s));
         cur ^= 1;
     }
     FO_LAUNCHED();
+    TRY(order_after(s, s2, P->ev_join));
     // ---------------- SGD (Alg. 4: theta_s <- theta_s - gamma_s grad), refreshes the bf16 shadow
     return launch_sgd(m->params, m->grads, nullptr, m->w16, m->w16lo, m->n_params, m->lr, 0.f, s);
 }
 
 void destroy(fo_model* m) {
-    delete (Plan*)m->plan;
+    Plan* P = (Plan*)m->plan;
+    if (P) {
+        for (hipEvent_t e : {P->ev_fork, P->ev_done[0], P->ev_done[1], P->ev_join})
+            if (e) (void)hipEventDestroy(e);
+        if (P->side) (void)hipStreamDestroy(P->side);
+    }
+    delete P;
     m->plan = nullptr;
 }
 
