@@ -179,6 +179,69 @@ struct LdKR {
 };
 
 
+// Rows contiguous, aligned (16-byte rows, R a multiple of 8), staged without a
+// transpose: the LDS tile is [64 k][128 rows] and the MFMA operand fragments
+// come out of it through the LDS transpose read (ds_read_b64_tr_b16).  Thread
+// = (row chunk c = tid % 16, k row kr = tid / 16): register j holds k row
+// kr + 16 j, rows r0 + 8 c .. + 7, so every 16 lanes load and store one whole
+// k row (256 B).  Row segments of 32 elements (64 B) are XOR-swizzled by
+// k mod 4: the four k rows that half a wave's transpose read touches then fall
+// in distinct 64-byte bank groups.
+__device__ __forceinline__ int kr_idx(int k, int r) { return k * BM + (r ^ ((k & 3) << 5)); }
+
+struct LdKRt {
+    int64_t base;  // element offset of (k row kr, row r0 + 8 c)
+    int64_t ld;
+    int kr, rc;
+    bool rowok, full;
+    __device__ void init(const bf16_t* P, int64_t ld_, int r0, int R, int tid) {
+        ld = ld_;
+        kr = tid >> 4;
+        rc = (tid & 15) * 8;
+        rowok = r0 + rc < R;
+        full = r0 + BM <= R;
+        base = (int64_t)kr * ld + r0 + rc;
+    }
+    // every load is issued (an outside chunk reads kZero8), as in LdRK::load_al
+    __device__ void load_al(const bf16_t* P, int kb, int kend, uint4* r) const {
+        const bf16_t* p = P + base + (int64_t)kb * ld;
+        if (full && kb + BK <= kend) {  // interior tile (uniform)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) r[j] = load8(p + 16 * j * ld);
+            return;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) r[j] = load8(rowok && kb + kr + 16 * j < kend ? p + 16 * j * ld : kZero8);
+    }
+    __device__ void store(bf16_t* t, const uint4* r, int) const {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4*>(&t[kr_idx(kr + 16 * j, rc)]) = r[j];
+    }
+};
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+// One 32 x 16 MFMA operand fragment (lane l: row l % 32, k = 8 (l / 32) .. + 7)
+// from a [k][row] tile: two transpose reads of four k each.  Within a group of
+// 16 lanes the read hands lane i element i % 4 of the 8 bytes addressed by lane
+// 4 j + i / 4, for j = 0..3; so lane (g = l / 16, s = l % 16) addresses k row
+// 8 (g / 2) + s / 4 (+ 4 for the second read), rows 16 (g % 2) + 4 (s % 4)
+// .. + 3 of the fragment.  off.x / off.y are those addresses for k block 0
+// (the swizzle depends on k mod 4 only, so block kb adds 16 kb rows).
+__device__ __forceinline__ bf16x8_t frag_tr(const bf16_t* T, int2 off, int kadd) {
+    const s16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + off.x + kadd));
+    const s16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + off.y + kadd));
+    const s16x8_t v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8_t, v);
+}
+__device__ __forceinline__ int2 frag_tr_off(int lane, int row0) {
+    const int g = lane >> 4, s = lane & 15;
+    const int k = 8 * (g >> 1) + (s >> 2), r = row0 + 16 * (g & 1) + 4 * (s & 3);
+    return make_int2(kr_idx(k, r), kr_idx(k + 4, r));
+}
+
 // Conv forward A: rows = output pixels (b, oy, ox); k = (ky, kx, ci), Ci % 64 == 0
 // so that a K tile lies within one filter tap.
 struct LdConvFwd {
@@ -332,11 +395,13 @@ template <> struct LoaderOf<OP_CONV_FWD> { typedef LdConvFwd T; };
 template <> struct LoaderOf<OP_CONV_DX> { typedef LdConvDx T; };
 template <> struct LoaderOf<OP_CONV_DXW> { typedef LdConvDxW T; };
 template <> struct LoaderOf<OP_CONV_DWX> { typedef LdConvDwX T; };
+constexpr int OP_KRT = 6;  // OP_KR staged untransposed, read through the LDS transpose
+template <> struct LoaderOf<OP_KRT> { typedef LdKRt T; };
 
 template <int MODE>
 __device__ __forceinline__ void loader_init(typename LoaderOf<MODE>::T& L, const bf16_t* P, int64_t ld,
                                             const ConvGeom& g, int r0, int R, int tid) {
-    if constexpr (MODE == OP_RK || MODE == OP_KR)
+    if constexpr (MODE == OP_RK || MODE == OP_KR || MODE == OP_KRT)
         L.init(P, ld, r0, R, tid);
     else
         L.init(P, g, r0, R, tid);
@@ -695,16 +760,20 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
     };
     const int lrow = lane & 31, lk = (lane >> 5) * 8;
     const int aoff = lds_idx(wm * 64 + lrow, lk), boff = lds_idx(wn * 64 + lrow, lk);
+    const int2 atr0 = frag_tr_off(lane, wm * 64), atr1 = frag_tr_off(lane, wm * 64 + 32);
+    const int2 btr0 = frag_tr_off(lane, wn * 64), btr1 = frag_tr_off(lane, wn * 64 + 32);
     auto compute = [&](const bf16_t* As, const bf16_t* Bs) {
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             bf16x8_t a[2], b[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i)
-                a[i] = *reinterpret_cast<const bf16x8_t*>(&As[aoff + i * 32 * LDR + ks * 16]);
+                a[i] = AM == OP_KRT ? frag_tr(As, i ? atr1 : atr0, ks * 16 * BM)
+                                    : *reinterpret_cast<const bf16x8_t*>(&As[aoff + i * 32 * LDR + ks * 16]);
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                b[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[boff + j * 32 * LDR + ks * 16]);
+                b[j] = BMODE == OP_KRT ? frag_tr(Bs, j ? btr1 : btr0, ks * 16 * BM)
+                                       : *reinterpret_cast<const bf16x8_t*>(&Bs[boff + j * 32 * LDR + ks * 16]);
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -950,8 +1019,8 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
 template <int AM, int BMODE, bool AL = false>
 void launch(const GemmDesc& d, hipStream_t s) {
     // kernel names as the profilers print them
-    static const char* names[6][6] = {};
-    static char buf[6][6][32];
+    static const char* names[7][7] = {};
+    static char buf[7][7][32];
     if (!names[AM][BMODE]) {
         snprintf(buf[AM][BMODE], sizeof(buf[AM][BMODE]), "gemm_kernel<%d, %d>", AM, BMODE);
         names[AM][BMODE] = buf[AM][BMODE];
@@ -1014,9 +1083,9 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
         d.nseg == 3 ? launch_comp<3>(dv, s) : launch_comp<2>(dv, s);
     else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(dv, s) : launch<OP_RK, OP_RK>(dv, s);
-    else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KR, true>(dv, s) : launch<OP_RK, OP_KR>(dv, s);
-    else if (a == OP_KR && b == OP_KR) al ? launch<OP_KR, OP_KR, true>(dv, s) : launch<OP_KR, OP_KR>(dv, s);
-    else if (a == OP_KR && b == OP_RK) al ? launch<OP_KR, OP_RK, true>(dv, s) : launch<OP_KR, OP_RK>(dv, s);
+    else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KRT, true>(dv, s) : launch<OP_RK, OP_KR>(dv, s);
+    else if (a == OP_KR && b == OP_KR) al ? launch<OP_KRT, OP_KRT, true>(dv, s) : launch<OP_KR, OP_KR>(dv, s);
+    else if (a == OP_KR && b == OP_RK) al ? launch<OP_KRT, OP_RK, true>(dv, s) : launch<OP_KR, OP_RK>(dv, s);
     else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(dv, s);
     else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(dv, s);
     else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(dv, s);
