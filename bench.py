@@ -1,6 +1,6 @@
 """Benchmark of the FedOptima server hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..5, default 4]
 
 One step = one pass of the server's hot path over one activation batch:
 an arriving batch is copied into the HBM activation pool (Alg. 2 put() with
@@ -43,9 +43,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (transformer 30, 128-device VGG 1000)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (transformer 5, 128-device VGG 10)")
-    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--config", type=int, default=4, help="1-3: the parity workloads' step loops; 4: "
+                    "transformer (default); 5: 128-device VGG with Poisson arrivals")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-steps", type=int, default=2)
+    ap.add_argument("--cpu-sample-steps", type=int, default=8)
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a 1 GiB device-to-device copy (the HBM counter calibration kernel)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -207,6 +208,24 @@ def bench_aggregate(A, torch, stream):
 
 
 VGG_STEP_GFLOP = 102.9  # useful FLOPs of one VGG-16 split server step at B = 64 (fwd + dgrad + wgrad)
+PEAK_F32_TFLOPS = 157.3  # MI355X fp32 vector
+
+# The step-loop workloads: K devices with one batch queued each, one arrival and
+# one step per iteration (plus one model aggregation where the workload has a
+# device-side model).  gflop: useful FLOPs of a step where no kernel records them.
+WORKLOADS = {
+    1: {"workload": "tiny CNN split server step (fp32): conv3x3 32->64, maxpool, conv3x3 64->64, GAP, "
+                    "linear 64->10, batch 16 of [32,16,16], 4 devices, aggregation of 10,000 params per step "
+                    "(alpha 0.5, staleness = device id)", "peak": PEAK_F32_TFLOPS, "gflop": 0.5285},
+    2: {"workload": "vgg16 split server step, batch 64 of [64,16,16] bf16 activations, 16 devices",
+        "peak": PEAK_BF16_TFLOPS, "gflop": VGG_STEP_GFLOP},
+    3: {"workload": "resnet18 split server step (layer2-4, BatchNorm train mode, momentum 0.9), batch 32 of "
+                    "[64,16,16] bf16 activations, 32 devices, aggregation of 157,504 params per step "
+                    "(alpha 1, staleness U{0..8})", "peak": PEAK_BF16_TFLOPS, "gflop": 19.0},
+    4: {"workload": "bert-base split server step: 10 post-LN encoder layers d=768 h=12 ffn=3072, "
+                    "batch 32 x 128 tokens, lengths U[32,128], 16 devices, plain SGD",
+        "peak": PEAK_BF16_TFLOPS, "gflop": 1099.0},
+}
 
 
 def fused_aggregation(A, torch, n, m):
@@ -378,35 +397,41 @@ def main():
         args.warmup = 10 if args.warmup is None else args.warmup
         bench_vgg128(args, A, torch, S)
         return
-    if cid != 4:
-        raise SystemExit("bench.py: workloads are --config 4 (transformer, default) and --config 5 "
-                         "(128-device VGG with Poisson arrivals)")
+    if cid not in WORKLOADS:
+        raise SystemExit("bench.py: --config 1..5 (4, the transformer, is the default)")
     args.steps = 30 if args.steps is None else args.steps
     args.warmup = 5 if args.warmup is None else args.warmup
     cfg = S.get_config(cid)
-    B, Lmax, K = cfg.batch, cfg.in_shape[0], cfg.n_devices
+    B, K = cfg.batch, cfg.n_devices
+    bert = cfg.family == "bert"
     stream = torch.cuda.current_stream()
 
     # ---------------- synthetic inputs, resident in HBM before timing
     bank_n = 16
-    acts_h = S.make_acts(cid, bank_n)                 # bf16 bits [n, B, L, d]
+    acts_h = S.make_acts(cid, bank_n)                 # fp32, or bf16 bits, [n, B, ...]
     labels_h = S.make_labels(cid, bank_n)
-    lengths_h = S.make_lengths(cid, bank_n)
-    acts_d = torch.from_numpy(acts_h.view(np.int16)).cuda()
+    acts_d = torch.from_numpy(acts_h if cfg.dtype == "f32" else acts_h.view(np.int16)).cuda()
     labels_d = torch.from_numpy(labels_h).cuda()
-    lengths_d = torch.from_numpy(lengths_h).cuda()
+    lengths_d = torch.from_numpy(S.make_lengths(cid, bank_n)).cuda() if bert else None
     del acts_h
     theta = S.init_params(cid)
     model = A.fo_model_create(cid, B, theta, stream)
-    slot_bytes = B * Lmax * cfg.in_shape[1] * 2
-    q = A.fo_queues_create(K, slot_bytes, B, True, 3 * K, stream)
+    slot_bytes = int(acts_d[0].numel() * acts_d.element_size())
+    q = A.fo_queues_create(K, slot_bytes, B, bert, 3 * K, stream)
+    # device-side models aggregated once per step (Alg. 4, model branch), where the workload has them
+    agg_glob = agg_locs = agg_stale = None
+    if cfg.agg_n:
+        agg_glob = torch.from_numpy(S.make_global_vector(cid)).cuda()
+        agg_locs = torch.from_numpy(S.make_local_vectors(cid, K)).cuda()
+        agg_stale = S.make_staleness(cid, args.warmup + 2 * args.steps, 8) if cid == 3 else None
+        A.fo_set_stream(stream)
 
     arrivals = [0]
 
     def push(k):
         i = arrivals[0] % bank_n
         arrivals[0] += 1
-        st = A.fo_queues_push(q, k, acts_d[i], labels_d[i], lengths_d[i])
+        st = A.fo_queues_push(q, k, acts_d[i], labels_d[i], lengths_d[i] if bert else None)
         return i if st == A.FO_OK else None
 
     # every device starts with one batch queued
@@ -420,6 +445,9 @@ def main():
         fa, lab, seq, slot = A.fo_queues_in_service(q)
         A.fo_server_step(model, fa, lab, k)
         A.fo_queues_release(q)
+        if agg_glob is not None:  # one model arrival: device k's local model, staleness as in the workload
+            s = k if cid == 1 else int(agg_stale[t])
+            A.fo_async_aggregate(agg_glob, agg_locs[k], cfg.agg_alpha, s)
         return k
 
     for t in range(args.warmup):
@@ -450,13 +478,25 @@ def main():
     ms_step = ms_total / args.steps
     samples_s = B * args.steps / (ms_total * 1e-3)
 
-    # useful FLOPs per step from the kernels' own records (valid tokens only)
+    wl = WORKLOADS[cid]
+    peak = wl["peak"]
+    # useful FLOPs per step from the kernels' own records (valid tokens only), or
+    # the workload's fixed count where its kernels carry no records (fp32 CNN)
     alg_flops = sum(s["flops"] for s in stats)
     mfma_flops = sum(s["mfma_flops"] for s in stats)
-    flops_step = alg_flops / args.steps  # both timed passes see the same mix of batches on average
-    mfu = flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
-    dom = max((s for s in stats if s["name"].startswith("gemm")), key=lambda s: s["ms"])
-    dom_tflops = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+    flops_step = alg_flops / args.steps if alg_flops else wl["gflop"] * 1e9
+    mfu = flops_step / (ms_step * 1e-3) / (peak * 1e12)
+    gemms = [s for s in stats if s["name"].startswith("gemm")]
+    if gemms:
+        dom = max(gemms, key=lambda s: s["ms"])
+        dom_tflops = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "kernel": dom["name"], "achieved": round(dom_tflops, 1), "peak": peak,
+                    "unit": "TFLOP/s", "frac": round(dom_tflops / peak, 4), "launches": dom["launches"],
+                    "avg_launch_us": round(dom["ms"] / dom["launches"] * 1e3, 2), "traffic": traffic_for(dom["name"])}
+    else:  # the fp32 direct-convolution CNN: the whole step against the fp32 vector peak
+        roofline = {"bound": "alu", "kernel": "whole step (fp32 direct convolutions, not instrumented)",
+                    "achieved": round(flops_step / (ms_step * 1e-3) / 1e12, 3), "peak": peak, "unit": "TFLOP/s",
+                    "frac": round(mfu, 5), "traffic": None}
     kernels = [{"name": s["name"], "launches": s["launches"], "ms_per_step": round(s["ms"] / args.steps, 4),
                 "TFLOP/s": round(s["flops"] / max(s["ms"], 1e-9) / 1e9, 1) if s["flops"] else None}
                for s in sorted(stats, key=lambda s: -s["ms"])]
@@ -472,6 +512,9 @@ def main():
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(cid, args.cpu_sample_steps)
 
+    config = {"workload": wl["workload"], "global_batch": B, "parallelism": "single-gpu"}
+    if bert:
+        config["seq_len"] = cfg.in_shape[0]
     out = {
         "metric": "server train samples/s + % bf16 MFMA peak; async-aggregate HBM GB/s",
         "value": round(samples_s, 2),
@@ -483,18 +526,14 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "f32" if cfg.dtype == "f32" else "bf16",
         "data": "synthetic",
-        "config": {"workload": "bert-base split server step: 10 post-LN encoder layers d=768 h=12 ffn=3072, "
-                               "batch 32 x 128 tokens, lengths U[32,128], 16 devices, plain SGD",
-                   "global_batch": B, "seq_len": Lmax, "parallelism": "single-gpu"},
-        "mfu": round(mfu, 4),
-        "useful_tflop_per_step": round(flops_step / 1e12, 4),
+        "config": config,
+        "mfu": round(mfu, 5),
+        "mfu_peak_tflops": peak,
+        "useful_tflop_per_step": round(flops_step / 1e12, 6),
         "mfma_tflop_per_step_executed": round(mfma_flops / args.steps / 1e12, 4),
-        "roofline": {"bound": "mfma", "kernel": dom["name"], "achieved": round(dom_tflops, 1),
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4),
-                     "launches": dom["launches"], "avg_launch_us": round(dom["ms"] / dom["launches"] * 1e3, 2),
-                     "traffic": traffic_for(dom["name"])},
+        "roofline": roofline,
         "aggregate": agg,
         "kernels": kernels[:12],
         "host_wall_ms_per_step": round(wall / args.steps * 1e3, 3),
