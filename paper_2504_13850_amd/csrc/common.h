@@ -54,13 +54,27 @@ __host__ __device__ inline float bf2f(bf16_t h) {
     return v.f;
 }
 
-// fp32 -> bf16, round to nearest even (inputs are finite).
+// fp32 -> bf16, round to nearest even (inputs are finite).  Device code uses
+// the gfx950 conversion instruction (v_cvt_pk_bf16_f32, the same rounding);
+// host code rounds the bit pattern.
 __host__ __device__ inline bf16_t f2bf(float f) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_bit_cast(bf16_t, (__bf16)f);
+#else
     union { uint32_t u; float f; } v;
     v.f = f;
     uint32_t u = v.u;
     u += 0x7FFFu + ((u >> 16) & 1u);
     return (bf16_t)(u >> 16);
+#endif
+}
+
+// Two fp32 -> one packed bf16 pair (a in the low half), round to nearest even.
+__device__ inline uint32_t f2bf2(float a, float b) {
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const f32x2_t v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }

@@ -29,10 +29,8 @@ __device__ __forceinline__ void split8(const float* v, bf16x8_t& hi, bf16x8_t& l
     u32x4_t h, l;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        const bf16_t h0 = f2bf(v[2 * e]), h1 = f2bf(v[2 * e + 1]);
-        const bf16_t l0 = f2bf(v[2 * e] - bf2f(h0)), l1 = f2bf(v[2 * e + 1] - bf2f(h1));
-        h[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        l[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        h[e] = f2bf2(v[2 * e], v[2 * e + 1]);
+        l[e] = f2bf2(v[2 * e] - bf2f((bf16_t)(h[e] & 0xFFFFu)), v[2 * e + 1] - bf2f((bf16_t)(h[e] >> 16)));
     }
     hi = __builtin_bit_cast(bf16x8_t, h);
     lo = __builtin_bit_cast(bf16x8_t, l);

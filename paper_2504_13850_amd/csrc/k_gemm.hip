@@ -490,16 +490,15 @@ __device__ __forceinline__ f32x4 bf4_to_f(u32x2 w) {
     return f;
 }
 __device__ __forceinline__ u32x2 f_to_bf4(f32x4 v, f32x4* lo) {
-    const bf16_t h0 = f2bf(v.x), h1 = f2bf(v.y), h2 = f2bf(v.z), h3 = f2bf(v.w);
-    if (lo) {
-        lo->x = v.x - bf2f(h0);
-        lo->y = v.y - bf2f(h1);
-        lo->z = v.z - bf2f(h2);
-        lo->w = v.w - bf2f(h3);
-    }
     u32x2 w;
-    w.x = (uint32_t)h0 | ((uint32_t)h1 << 16);
-    w.y = (uint32_t)h2 | ((uint32_t)h3 << 16);
+    w.x = f2bf2(v.x, v.y);
+    w.y = f2bf2(v.z, v.w);
+    if (lo) {
+        lo->x = v.x - bf2f((bf16_t)(w.x & 0xFFFFu));
+        lo->y = v.y - bf2f((bf16_t)(w.x >> 16));
+        lo->z = v.z - bf2f((bf16_t)(w.y & 0xFFFFu));
+        lo->w = v.w - bf2f((bf16_t)(w.y >> 16));
+    }
     return w;
 }
 
