@@ -46,16 +46,17 @@ struct GemmDesc {
     int nseg = 1;
     ConvGeom g;
     // epilogue, applied in this order: + bias[n], + resid[m][n] (fp32),
-    // act (GELU stores its input to `pre` when set), * [mask[m][n] > 0],
-    // * GELU'(dpre[m][n]); then stores to Cf (fp32) and/or Cb (bf16).
+    // act (GELU also stores its derivative at the input, GELU'(x), to `dact_out`
+    // when set), * [mask[m][n] > 0], * dact[m][n] (a stored activation
+    // derivative); then stores to Cf (fp32) and/or Cb (bf16).
     const float* bias = nullptr;
     const float* resid = nullptr;
     int64_t ldr = 0;
     int act = ACT_NONE;
-    bf16_t* pre = nullptr;
+    bf16_t* dact_out = nullptr;
     const bf16_t* mask = nullptr;
-    const bf16_t* dpre = nullptr;
-    int64_t ldm = 0;  // leading dimension of pre / mask / dpre
+    const bf16_t* dact = nullptr;
+    int64_t ldm = 0;  // leading dimension of dact_out / mask / dact
     float* Cf = nullptr;
     int64_t ldcf = 0;
     bf16_t* Cb = nullptr;   // bf16(v)

@@ -440,27 +440,27 @@ __device__ __forceinline__ float gelu_grad(float x) {
 // GELU' and stores, so that a thread can issue the loads of several rows
 // before it needs any of them.
 struct EpiIn {
-    float resid = 0.f, mask = 1.f, dpre = 0.f;
+    float resid = 0.f, mask = 1.f, dact = 1.f;
 };
 
 __device__ __forceinline__ EpiIn epi_load(const GemmDesc& d, int row, int col) {
     EpiIn e;
     if (d.resid) e.resid = d.resid[(int64_t)row * d.ldr + col];
     if (d.mask) e.mask = bf2f(d.mask[(int64_t)row * d.ldm + col]);
-    if (d.dpre) e.dpre = bf2f(d.dpre[(int64_t)row * d.ldm + col]);
+    if (d.dact) e.dact = bf2f(d.dact[(int64_t)row * d.ldm + col]);
     return e;
 }
 
 // v already holds bias and residual
 __device__ __forceinline__ float epi_store(const GemmDesc& d, int row, int col, float v, const EpiIn& e) {
     if (d.act == ACT_GELU) {
-        if (d.pre) d.pre[(int64_t)row * d.ldm + col] = f2bf(v);
+        if (d.dact_out) d.dact_out[(int64_t)row * d.ldm + col] = f2bf(gelu_grad(v));
         v = gelu_f(v);
     } else if (d.act == ACT_RELU) {
         v = v > 0.f ? v : 0.f;
     }
     if (d.mask && !(e.mask > 0.f)) v = 0.f;
-    if (d.dpre) v *= gelu_grad(e.dpre);
+    if (d.dact) v *= e.dact;
     if (d.Cf) d.Cf[(int64_t)row * d.ldcf + col] = v;
     if (d.Cb) {
         const bf16_t hi = f2bf(v);
@@ -503,21 +503,26 @@ __device__ __forceinline__ u32x2 f_to_bf4(f32x4 v, f32x4* lo) {
 }
 
 struct EpiIn4 {
-    f32x4 resid = {0.f, 0.f, 0.f, 0.f}, mask = {1.f, 1.f, 1.f, 1.f}, dpre = {0.f, 0.f, 0.f, 0.f};
+    f32x4 resid = {0.f, 0.f, 0.f, 0.f}, mask = {1.f, 1.f, 1.f, 1.f}, dact = {1.f, 1.f, 1.f, 1.f};
 };
 
 __device__ __forceinline__ EpiIn4 epi_load4(const GemmDesc& d, int row, int col) {
     EpiIn4 e;
     if (d.resid) e.resid = *reinterpret_cast<const f32x4*>(d.resid + (int64_t)row * d.ldr + col);
     if (d.mask) e.mask = bf4_to_f(*reinterpret_cast<const u32x2*>(d.mask + (int64_t)row * d.ldm + col));
-    if (d.dpre) e.dpre = bf4_to_f(*reinterpret_cast<const u32x2*>(d.dpre + (int64_t)row * d.ldm + col));
+    if (d.dact) e.dact = bf4_to_f(*reinterpret_cast<const u32x2*>(d.dact + (int64_t)row * d.ldm + col));
     return e;
 }
 
 // v already holds bias and residual
 __device__ __forceinline__ f32x4 epi_store4(const GemmDesc& d, int row, int col, f32x4 v, const EpiIn4& e) {
     if (d.act == ACT_GELU) {
-        if (d.pre) *reinterpret_cast<u32x2*>(d.pre + (int64_t)row * d.ldm + col) = f_to_bf4(v, nullptr);
+        if (d.dact_out) {
+            f32x4 g;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) g[q] = gelu_grad(v[q]);
+            *reinterpret_cast<u32x2*>(d.dact_out + (int64_t)row * d.ldm + col) = f_to_bf4(g, nullptr);
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[q] = gelu_f(v[q]);
     } else if (d.act == ACT_RELU) {
@@ -529,10 +534,7 @@ __device__ __forceinline__ f32x4 epi_store4(const GemmDesc& d, int row, int col,
         for (int q = 0; q < 4; ++q)
             if (!(e.mask[q] > 0.f)) v[q] = 0.f;
     }
-    if (d.dpre) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] *= gelu_grad(e.dpre[q]);
-    }
+    if (d.dact) v *= e.dact;
     if (d.Cf) *reinterpret_cast<f32x4*>(d.Cf + (int64_t)row * d.ldcf + col) = v;
     if (d.Cb) {
         f32x4 lo;
@@ -857,12 +859,19 @@ struct DmaRKc {  // one 128 x 32 tile; this wave's instructions are q = wave and
     }
 };
 
-template <int NSEG>
-__global__ void __launch_bounds__(NT, 2) gemm_comp_dma_kernel(const GemmDesc d) {
-    // two stages of four unpadded 128 x 32 tiles (A, A_lo, B, B_lo) = 64 KB; reused for the C tile
-    __shared__ __attribute__((aligned(1024))) bf16_t smem[2][4][BM * CBK];
-    bf16_t (*st0)[BM * CBK] = smem[0];
-    bf16_t (*st1)[BM * CBK] = smem[1];
+// s_waitcnt immediate that waits for at most n vector memory operations in
+// flight and does not wait on LDS / scalar memory or exports.
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// NST stages in a ring: the copy of tile t + NST - 1 is issued before the MFMAs
+// of tile t.  Every copy is issued, also past the slice's last tile (those read
+// kZero8 into a stage that is not read again), so the number of copies in
+// flight is static and each wait names exactly the tile it needs.
+template <int NSEG, int NST>
+__global__ void __launch_bounds__(NT, NST == 2 ? 2 : 1) gemm_comp_dma_kernel(const GemmDesc d) {
+    // NST stages of four unpadded 128 x 32 tiles (A, A_lo, B, B_lo) = 32 KB each;
+    // reused for the C tile (64 KB)
+    __shared__ __attribute__((aligned(1024))) bf16_t smem[NST][4][BM * CBK];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
@@ -892,12 +901,13 @@ __global__ void __launch_bounds__(NT, 2) gemm_comp_dma_kernel(const GemmDesc d) 
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+    constexpr int CPT = NSEG == 3 ? 8 : 6;  // copy instructions per tile and thread
     auto copy_tile = [&](bf16_t (*st)[BM * CBK], int t) {
-        const int kb = kbeg + t * CBK;
-        la.copy(d.A, kb, K, st[0], wave);
-        if (NSEG == 3) la.copy(d.A2, kb, K, st[1], wave);
-        lb.copy(d.B, kb, K, st[2], wave);
-        lb.copy(d.B2, kb, K, st[3], wave);
+        const int kb = kbeg + t * CBK, ke = t < nk ? K : 0;
+        la.copy(d.A, kb, ke, st[0], wave);
+        if (NSEG == 3) la.copy(d.A2, kb, ke, st[1], wave);
+        lb.copy(d.B, kb, ke, st[2], wave);
+        lb.copy(d.B2, kb, ke, st[3], wave);
     };
     const int lrow = lane & 31, lc = lane >> 5;
     auto frag = [&](const bf16_t* t, int row, int ks) {
@@ -931,25 +941,27 @@ __global__ void __launch_bounds__(NT, 2) gemm_comp_dma_kernel(const GemmDesc d) 
                 }
         }
     };
+    // one step: issue the copy NST - 1 tiles ahead, compute tile t, wait until
+    // tile t + 1 has landed in every wave
+    auto step = [&](int t, int u) {
+        copy_tile(smem[(u + NST - 1) % NST], t + NST - 1);
+        compute(smem[u]);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));
+        __syncthreads();
+    };
 
-    if (nk > 0) copy_tile(st0, 0);
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed
-    __syncthreads();                // and every other wave's
+#pragma unroll
+    for (int u = 0; u < NST - 1; ++u) copy_tile(smem[u], u);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));  // tile 0 has landed
+    __syncthreads();
     int t = 0;
-    for (; t + 1 < nk; t += 2) {
-        copy_tile(st1, t + 1);
-        compute(st0);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (t + 2 < nk) copy_tile(st0, t + 2);
-        compute(st1);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+    for (; t + NST <= nk; t += NST) {  // whole rounds: static stage indices
+#pragma unroll
+        for (int u = 0; u < NST; ++u) step(t + u, u);
     }
-    if (t < nk) {
-        compute(st0);
-        __syncthreads();
-    }
+    for (int u = 0; t < nk; ++t, ++u) step(t, u);  // the rest of a round (stage index u < NST)
+    __builtin_amdgcn_s_waitcnt(0);  // copies past the last tile
+    __syncthreads();
     store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
 }
 
@@ -1000,7 +1012,7 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
     }
 }
 
-template <int NSEG>
+template <int NSEG, int NST = 2>
 void launch_comp(const GemmDesc& d, hipStream_t s) {
     ProfInfo pi;
     pi.kind = PROF_GEMM;
@@ -1011,7 +1023,7 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
     GemmDesc dd = d;
     dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
-    hipExtLaunchKernelGGL((gemm_comp_dma_kernel<NSEG>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
+    hipExtLaunchKernelGGL((gemm_comp_dma_kernel<NSEG, NST>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
     prof_end_ext(h);
 }
 
@@ -1062,11 +1074,11 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     {
         auto al = [](const void* p, uintptr_t m) { return p == nullptr || ((uintptr_t)p & (m - 1)) == 0; };
         bool v = d.N % 4 == 0 && al(d.ws, 16) && al(d.Cf, 16) && al(d.resid, 16) && al(d.Cb, 8) && al(d.Cb2, 8) &&
-                 al(d.pre, 8) && al(d.mask, 8) && al(d.dpre, 8) && al(d.colpart, 4);
+                 al(d.dact_out, 8) && al(d.mask, 8) && al(d.dact, 8) && al(d.colpart, 4);
         if (d.Cf) v = v && d.ldcf % 4 == 0;
         if (d.resid) v = v && d.ldr % 4 == 0;
         if (d.Cb) v = v && d.ldcb % 4 == 0;
-        if (d.pre || d.mask || d.dpre) v = v && d.ldm % 4 == 0;
+        if (d.dact_out || d.mask || d.dact) v = v && d.ldm % 4 == 0;
         dv.vec_epi = v ? 1 : 0;
     }
     const int a = d.amode, b = d.bmode;
@@ -1079,6 +1091,7 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     // (a k-major A with a device-side row bound may end inside an 8-row chunk)
     const bool al = (a == OP_RK || a == OP_KR) && (b == OP_RK || b == OP_KR) && !(a == OP_KR && d.Mdev) &&
                     op_aligned(a, d.A, d.A2, d.lda, d.M) && op_aligned(b, d.B, d.B2, d.ldb, d.N);
+    // (two stages and two workgroups per CU beat deeper rings at one per CU)
     if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
         d.nseg == 3 ? launch_comp<3>(dv, s) : launch_comp<2>(dv, s);
     else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(dv, s) : launch<OP_RK, OP_RK>(dv, s);

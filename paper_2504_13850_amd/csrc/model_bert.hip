@@ -31,7 +31,7 @@ struct LayerOff {
 
 struct LayerAct {
     float* qkv;                         // fp32: attention reads it unrounded
-    bf16_t *O, *Olo, *Hb, *Hlo, *pre1, *G, *Glo;
+    bf16_t *O, *Olo, *Hb, *Hlo, *dgelu1, *G, *Glo;  // dgelu1 = GELU'(FFN1 pre-activation)
     float *lse, *u1, *mean1, *rstd1, *Hf, *u2, *mean2, *rstd2;
 };
 
@@ -253,7 +253,7 @@ size_t ws_bytes(const fo_model* m) {
         add(4 * R * 3 * D);                         // qkv (fp32)
         add(2 * R * D); add(2 * R * D);             // O, Olo
         add(2 * R * D); add(2 * R * D);             // Hb, Hlo
-        add(2 * R * FF);                            // pre1
+        add(2 * R * FF);                            // dgelu1
         add(2 * R * FF); add(2 * R * FF);           // G, Glo
         add(4 * B * NH * L);                        // lse
         add(4 * R * D); add(4 * R); add(4 * R);     // u1, mean1, rstd1
@@ -327,7 +327,7 @@ fo_status init(fo_model* m) {
         t.Olo = a.take<bf16_t>(R * D);
         t.Hb = a.take<bf16_t>(R * D);
         t.Hlo = a.take<bf16_t>(R * D);
-        t.pre1 = a.take<bf16_t>(R * FF);
+        t.dgelu1 = a.take<bf16_t>(R * FF);
         t.G = a.take<bf16_t>(R * FF);
         t.Glo = a.take<bf16_t>(R * FF);
         t.lse = a.take<float>(B * NH * L);
@@ -466,7 +466,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         GemmDesc f1 = lin_fwd(rows, t.Hb, t.Hlo, D, W + f.w1, Wl + f.w1, FF);
         f1.Mdev = Tdev;
         f1.bias = prm + f.bf1;
-        f1.act = ACT_GELU; f1.pre = t.pre1; f1.ldm = FF;
+        f1.act = ACT_GELU; f1.dact_out = t.dgelu1; f1.ldm = FF;
         f1.Cb = t.G; f1.Cb2 = t.Glo; f1.ldcb = FF;
         TRY(gemm(f1, s));
         GemmDesc f2 = lin_fwd(rows, t.G, t.Glo, FF, W + f.w2, Wl + f.w2, D);
@@ -514,7 +514,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         TRY(ln_bwd(P, dY, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, du2b, grd + f.g2, grd + f.b2,
                    grd + f.bf2, s));
         TRY(order_after(s2, s, P->ev_fork));
-        // FFN2: dG = du2 W2 (times GELU'(pre1) -> dA1), dW2 = du2^T G, db2
+        // FFN2: dG = du2 W2 (times GELU' of the FFN1 pre-activation -> dA1), dW2 = du2^T G, db2
         {
             GemmDesc w;
             w.M = D; w.N = FF; w.K = rows; w.Kdev = Tdev;
@@ -527,7 +527,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.M = rows; d.N = FF; d.K = D; d.Mdev = Tdev;
             d.amode = OP_RK; d.A = du2b; d.lda = D;
             d.bmode = OP_KR; d.B = W + f.w2; d.ldb = FF;
-            d.dpre = t.pre1; d.ldm = FF;
+            d.dact = t.dgelu1; d.ldm = FF;
             d.Cb = dA1; d.ldcb = FF;
             d.colpart = P->colws;
             TRY(gemm(d, s));
