@@ -430,9 +430,11 @@ __device__ __forceinline__ float norm_cdf(float x) {
     return x >= 0.f ? 1.f - q : q;
 }
 __device__ __forceinline__ float gelu_f(float x) { return x * norm_cdf(x); }
-// d/dx [x Phi(x)] = Phi(x) + x phi(x)
-__device__ __forceinline__ float gelu_grad(float x) {
-    return fmaf(x, 0.39894228040143268f * __expf(-0.5f * x * x), norm_cdf(x));
+// GELU(x) = x Phi(x) and its derivative Phi(x) + x phi(x), sharing Phi(x)
+__device__ __forceinline__ float gelu_and_grad(float x, float* grad) {
+    const float p = norm_cdf(x);
+    *grad = fmaf(x, 0.39894228040143268f * __expf(-0.5f * x * x), p);
+    return x * p;
 }
 
 // The epilogue in two halves: epi_load fetches the per-element operands
@@ -454,8 +456,13 @@ __device__ __forceinline__ EpiIn epi_load(const GemmDesc& d, int row, int col) {
 // v already holds bias and residual
 __device__ __forceinline__ float epi_store(const GemmDesc& d, int row, int col, float v, const EpiIn& e) {
     if (d.act == ACT_GELU) {
-        if (d.dact_out) d.dact_out[(int64_t)row * d.ldm + col] = f2bf(gelu_grad(v));
-        v = gelu_f(v);
+        if (d.dact_out) {
+            float g;
+            v = gelu_and_grad(v, &g);
+            d.dact_out[(int64_t)row * d.ldm + col] = f2bf(g);
+        } else {
+            v = gelu_f(v);
+        }
     } else if (d.act == ACT_RELU) {
         v = v > 0.f ? v : 0.f;
     }
@@ -520,11 +527,16 @@ __device__ __forceinline__ f32x4 epi_store4(const GemmDesc& d, int row, int col,
         if (d.dact_out) {
             f32x4 g;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) g[q] = gelu_grad(v[q]);
+            for (int q = 0; q < 4; ++q) {
+                float gq;
+                v[q] = gelu_and_grad(v[q], &gq);
+                g[q] = gq;
+            }
             *reinterpret_cast<u32x2*>(d.dact_out + (int64_t)row * d.ldm + col) = f_to_bf4(g, nullptr);
-        }
+        } else {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = gelu_f(v[q]);
+            for (int q = 0; q < 4; ++q) v[q] = gelu_f(v[q]);
+        }
     } else if (d.act == ACT_RELU) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[q] = v[q] > 0.f ? v[q] : 0.f;
