@@ -24,12 +24,14 @@ fo_status launch_sgd(float* p, const float* g, float* v, bf16_t* w16, bf16_t* w1
 fo_status launch_cast_bf16(const float* x, bf16_t* y, bf16_t* ylo, int64_t n, hipStream_t s);
 
 // ------------------------------------------------------------------ k_attn.hip
-// qkv [T][3d] fp32, cu int32[B+1] packed-row offsets (sequences <= 128 tokens,
-// head width 64); out / outlo [T][d] bf16 high and low parts of the output;
-// lse/Dws fp32 [B][H][128]; dout the bf16 output gradient, dqkv bf16 [T][3d].
-fo_status launch_attn_fwd(const float* qkv, const int* cu, bf16_t* out, bf16_t* outlo, float* lse, int B, int H,
-                          int d, hipStream_t s);
-fo_status launch_attn_bwd(const float* qkv, const int* cu, const bf16_t* out, const bf16_t* dout,
+// qkv / qkvlo [T][3d] bf16 high and low parts of the projection, cu int32[B+1]
+// packed-row offsets (sequences <= 128 tokens, head width 64); out / outlo [T][d]
+// bf16 high and low parts of the output; lse fp32 [B][H][128] (natural log);
+// dout the bf16 output gradient, dqkv bf16 [T][3d].  The backward reads the
+// high parts only.
+fo_status launch_attn_fwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu, bf16_t* out, bf16_t* outlo,
+                          float* lse, int B, int H, int d, hipStream_t s);
+fo_status launch_attn_bwd(const bf16_t* qkv, const int* cu, const bf16_t* out, const bf16_t* dout,
                           const float* lse, bf16_t* dqkv, int B, int H, int d, hipStream_t s);
 
 // ------------------------------------------------------------------ k_common.hip

@@ -30,7 +30,7 @@ struct LayerOff {
 };
 
 struct LayerAct {
-    float* qkv;                         // fp32: attention reads it unrounded
+    bf16_t *qkv, *qkvlo;                // projection output, bf16 high and low parts
     bf16_t *O, *Olo, *Hb, *Hlo, *dgelu1, *G, *Glo;  // dgelu1 = GELU'(FFN1 pre-activation)
     float *lse, *u1, *mean1, *rstd1, *Hf, *u2, *mean2, *rstd2;
 };
@@ -250,7 +250,7 @@ size_t ws_bytes(const fo_model* m) {
         add(4 * R * D);
     }
     for (int l = 0; l < NL; ++l) {
-        add(4 * R * 3 * D);                         // qkv (fp32)
+        add(2 * R * 3 * D); add(2 * R * 3 * D);     // qkv, qkvlo
         add(2 * R * D); add(2 * R * D);             // O, Olo
         add(2 * R * D); add(2 * R * D);             // Hb, Hlo
         add(2 * R * FF);                            // dgelu1
@@ -322,7 +322,8 @@ fo_status init(fo_model* m) {
     }
     for (int l = 0; l < NL; ++l) {
         LayerAct& t = P->a[l];
-        t.qkv = a.take<float>(R * 3 * D);
+        t.qkv = a.take<bf16_t>(R * 3 * D);
+        t.qkvlo = a.take<bf16_t>(R * 3 * D);
         t.O = a.take<bf16_t>(R * D);
         t.Olo = a.take<bf16_t>(R * D);
         t.Hb = a.take<bf16_t>(R * D);
@@ -451,9 +452,9 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         GemmDesc q = lin_fwd(rows, P->Xb[l], l ? P->Xlo[l] : nullptr, D, W + f.wqkv, Wl + f.wqkv, 3 * D);
         q.Mdev = Tdev;
         q.bias = prm + f.bqkv;
-        q.Cf = t.qkv; q.ldcf = 3 * D;
+        q.Cb = t.qkv; q.Cb2 = t.qkvlo; q.ldcb = 3 * D;
         TRY(gemm(q, s));
-        TRY(launch_attn_fwd(t.qkv, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
+        TRY(launch_attn_fwd(t.qkv, t.qkvlo, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
         GemmDesc o = lin_fwd(rows, t.O, t.Olo, D, W + f.wo, Wl + f.wo, D);
         o.Mdev = Tdev;
         o.splits = split_rows(3 * D); o.ws = P->splitws;
