@@ -134,25 +134,37 @@ __global__ void __launch_bounds__(256) small_linear_fwd_kernel(const float* __re
         wv[k] = i < I ? wr[i] : 0.f;
     }
     const float bo = bias[o];
-    for (int b = wave; b < B; b += 8) {
-        const bool two = b + 4 < B;
-        const float* x0 = x + (int64_t)b * I;
-        const float* x1 = x + (int64_t)(two ? b + 4 : b) * I;
-        float s0 = 0.f, s1 = 0.f;
+    // wave w takes batch rows w, w + 4, ...; eight rows at a time with all
+    // their loads issued before the first product
+    constexpr int RB = 8;
+    for (int b0 = wave; b0 < B; b0 += 4 * RB) {
+        float s[RB];
 #pragma unroll
-        for (int k = 0; k < SL_PER; ++k) {
-            const int i = lane + 64 * k;
-            if (i < I) {
-                s0 = fmaf(x0[i], wv[k], s0);
-                s1 = fmaf(x1[i], wv[k], s1);
+        for (int u = 0; u < RB; ++u) {
+            const int b = min(b0 + 4 * u, B - 1);  // rows past B repeat row B - 1 and are not stored
+            const float* xr = x + (int64_t)b * I;
+            float xv[SL_PER];
+#pragma unroll
+            for (int k = 0; k < SL_PER; ++k) {
+                const int i = lane + 64 * k;
+                xv[k] = i < I ? xr[i] : 0.f;
             }
+            float a = 0.f;
+#pragma unroll
+            for (int k = 0; k < SL_PER; ++k) a = fmaf(xv[k], wv[k], a);
+            s[u] = a;
         }
-        s0 = wave_sum64(s0);
-        s1 = wave_sum64(s1);
+#pragma unroll
+        for (int u = 0; u < RB; ++u) s[u] = wave_sum64(s[u]);
         if (lane == 0) {
-            const float v0 = s0 + bo, v1 = s1 + bo;
-            y[(int64_t)b * O + o] = ACT == 1 ? tanhf(v0) : v0;
-            if (two) y[(int64_t)(b + 4) * O + o] = ACT == 1 ? tanhf(v1) : v1;
+#pragma unroll
+            for (int u = 0; u < RB; ++u) {
+                const int b = b0 + 4 * u;
+                if (b < B) {
+                    const float v = s[u] + bo;
+                    y[(int64_t)b * O + o] = ACT == 1 ? tanhf(v) : v;
+                }
+            }
         }
     }
 }
@@ -164,8 +176,20 @@ __global__ void __launch_bounds__(256) small_linear_wgrad_kernel(const float* __
     int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx < (int64_t)O * I) {
         int o = (int)(idx / I), i = (int)(idx % I);
+        // batch rows eight at a time, their loads issued together; one running sum
         float s = 0.f;
-        for (int b = 0; b < B; ++b) s = fmaf(dy[(int64_t)b * O + o], x[(int64_t)b * I + i], s);
+        int b = 0;
+        for (; b + 8 <= B; b += 8) {
+            float dv[8], xv[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                dv[u] = dy[(int64_t)(b + u) * O + o];
+                xv[u] = x[(int64_t)(b + u) * I + i];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s = fmaf(dv[u], xv[u], s);
+        }
+        for (; b < B; ++b) s = fmaf(dy[(int64_t)b * O + o], x[(int64_t)b * I + i], s);
         gw[idx] = s;
     }
     if (idx < O) {

@@ -100,9 +100,23 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
-constexpr int PER = D / 64;  // 12 columns per lane
 
 // y = gamma * (u - mean) * rstd + beta over each row of D; one wave per row.
+// LayerNorm over rows of D = 768: one wave per row, each lane four adjacent
+// columns 4 lane + 256 k (k = 0..2) with 16-byte loads and stores.
+constexpr int PER4 = D / 256;
+__device__ __forceinline__ f32x4 ld4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+__device__ __forceinline__ void st4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+__device__ __forceinline__ void st4bf(bf16_t* p, f32x4 v) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
+}
+__device__ __forceinline__ f32x4 bf4lo(f32x4 v) {  // v - bf16(v), elementwise
+    f32x4 r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r[q] = v[q] - bf2f(f2bf(v[q]));
+    return r;
+}
+
 __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ u, const float* __restrict__ g,
                                                      const float* __restrict__ beta, const int* __restrict__ Tdev,
                                                      float* __restrict__ yf, bf16_t* __restrict__ yb,
@@ -111,93 +125,113 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ u
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
     if (row >= *Tdev) return;
     const float* ur = u + (int64_t)row * D;
-    float x[PER];
+    f32x4 x[PER4];
     float s = 0.f;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        x[k] = ur[lane + 64 * k];
-        s += x[k];
+    for (int k = 0; k < PER4; ++k) {
+        x[k] = ld4(ur + 4 * lane + 256 * k);
+        s += (x[k][0] + x[k][1]) + (x[k][2] + x[k][3]);
     }
     const float mu = wave_sum(s) * (1.f / D);
     float v = 0.f;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
+    for (int k = 0; k < PER4; ++k) {
         x[k] -= mu;
-        v = fmaf(x[k], x[k], v);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v = fmaf(x[k][q], x[k][q], v);
     }
     const float rs = rsqrtf(wave_sum(v) * (1.f / D) + 1e-5f);
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        int c = lane + 64 * k;
-        float y = fmaf(x[k] * rs, g[c], beta[c]);
-        const bf16_t hi = f2bf(y);
-        yf[(int64_t)row * D + c] = y;
-        yb[(int64_t)row * D + c] = hi;
-        ylo[(int64_t)row * D + c] = f2bf(y - bf2f(hi));
+    for (int k = 0; k < PER4; ++k) {
+        const int c = 4 * lane + 256 * k;
+        const f32x4 gg = ld4(g + c), bb = ld4(beta + c);
+        f32x4 y;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) y[q] = fmaf(x[k][q] * rs, gg[q], bb[q]);
+        st4(yf + (int64_t)row * D + c, y);
+        st4bf(yb + (int64_t)row * D + c, y);
+        st4bf(ylo + (int64_t)row * D + c, bf4lo(y));
     }
     if (lane == 0) {
         mean[row] = mu;
         rstd[row] = rs;
     }
 }
-
 // dx = rstd * (gdy - mean(gdy) - xhat * mean(gdy * xhat)), gdy = dy * gamma.
-// A block takes LNB_ROWS consecutive rows (a quarter per wave) and also
-// writes column partial sums of the norm's parameter gradients and of dx:
-// part[block][0][c] = sum dy * xhat (dgamma), part[block][1][c] = sum dy
-// (dbeta), part[block][2][c] = sum dx (the bias gradient of the sublayer
-// whose sum with the residual this norm normalises).
+// A block takes LNB_ROWS consecutive rows (a quarter per wave, all of a wave's
+// rows loaded first) and also writes column partial sums of the norm's
+// parameter gradients and of dx: part[block][0][c] = sum dy * xhat (dgamma),
+// part[block][1][c] = sum dy (dbeta), part[block][2][c] = sum dx (the bias
+// gradient of the sublayer whose sum with the residual this norm normalises).
 constexpr int LNB_ROWS = 16;
-
 __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ dy, const float* __restrict__ u,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
                                                      const float* __restrict__ g, const int* __restrict__ Tdev,
                                                      float* __restrict__ dxf, bf16_t* __restrict__ dxb,
                                                      float* __restrict__ part) {
+    constexpr int RW = LNB_ROWS / 4;  // rows per wave
     __shared__ float red[4][D];
     const int T = *Tdev;
     const int r0 = blockIdx.x * LNB_ROWS;
     if (r0 >= T) return;  // uniform
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    float gam[PER], pg[PER], pb[PER], px[PER];
+    f32x4 gam[PER4], pg[PER4], pb[PER4], px[PER4];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        gam[k] = g[lane + 64 * k];
-        pg[k] = pb[k] = px[k] = 0.f;
+    for (int k = 0; k < PER4; ++k) {
+        gam[k] = ld4(g + 4 * lane + 256 * k);
+        pg[k] = pb[k] = px[k] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    for (int i = 0; i < LNB_ROWS / 4; ++i) {
-        const int row = r0 + wave * (LNB_ROWS / 4) + i;
+    f32x4 dv[RW][PER4], uv[RW][PER4];
+    float mu[RW], rs[RW];
+#pragma unroll
+    for (int i = 0; i < RW; ++i) {
+        const int row = min(r0 + wave * RW + i, T - 1);  // rows past T load row T - 1 and are skipped
+        mu[i] = mean[row];
+        rs[i] = rstd[row];
+#pragma unroll
+        for (int k = 0; k < PER4; ++k) {
+            dv[i][k] = ld4(dy + (int64_t)row * D + 4 * lane + 256 * k);
+            uv[i][k] = ld4(u + (int64_t)row * D + 4 * lane + 256 * k);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < RW; ++i) {
+        const int row = r0 + wave * RW + i;
         if (row >= T) break;
-        const float mu = mean[row], rs = rstd[row];
-        float xh[PER], gd[PER];
+        f32x4 xh[PER4], gd[PER4];
         float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int c = lane + 64 * k;
-            const float d = dy[(int64_t)row * D + c];
-            xh[k] = (u[(int64_t)row * D + c] - mu) * rs;
-            gd[k] = d * gam[k];
-            pg[k] = fmaf(d, xh[k], pg[k]);
-            pb[k] += d;
-            s1 += gd[k];
-            s2 = fmaf(gd[k], xh[k], s2);
+        for (int k = 0; k < PER4; ++k) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float d = dv[i][k][q];
+                xh[k][q] = (uv[i][k][q] - mu[i]) * rs[i];
+                gd[k][q] = d * gam[k][q];
+                pg[k][q] = fmaf(d, xh[k][q], pg[k][q]);
+                pb[k][q] += d;
+                s1 += gd[k][q];
+                s2 = fmaf(gd[k][q], xh[k][q], s2);
+            }
         }
         s1 = wave_sum(s1) * (1.f / D);
         s2 = wave_sum(s2) * (1.f / D);
 #pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int c = lane + 64 * k;
-            const float dx = rs * (gd[k] - s1 - xh[k] * s2);
+        for (int k = 0; k < PER4; ++k) {
+            const int c = 4 * lane + 256 * k;
+            f32x4 dx;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) dx[q] = rs[i] * (gd[k][q] - s1 - xh[k][q] * s2);
             px[k] += dx;
-            dxf[(int64_t)row * D + c] = dx;
-            dxb[(int64_t)row * D + c] = f2bf(dx);
+            st4(dxf + (int64_t)row * D + c, dx);
+            st4bf(dxb + (int64_t)row * D + c, dx);
         }
     }
     float* out = part + (int64_t)blockIdx.x * 3 * D;
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
 #pragma unroll
-        for (int k = 0; k < PER; ++k) red[wave][lane + 64 * k] = q == 0 ? pg[k] : (q == 1 ? pb[k] : px[k]);
+        for (int k = 0; k < PER4; ++k)
+            *reinterpret_cast<f32x4*>(&red[wave][4 * lane + 256 * k]) = q == 0 ? pg[k] : (q == 1 ? pb[k] : px[k]);
         __syncthreads();
         for (int c = threadIdx.x; c < D; c += 256)
             out[q * D + c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
