@@ -77,6 +77,35 @@ struct GemmDesc {
     const int* Kdev = nullptr;
     int* prof_snap = nullptr;  // set by the launcher when profiling: receives (M, K) effective
     int vec_epi = 0;           // set by the launcher: the epilogue may move four columns per access
+    // With split-K: leave the partials in ws and skip the reduction pass; the
+    // consumer sums them (see SplitRows).  A launch that runs unsplit (one
+    // active slice) still applies its epilogue and writes Cf.
+    bool defer_reduce = false;
+};
+
+// Split-K slices a launch with a device-side row bound M_eff uses: as many as
+// keep two workgroups per CU busy over the active 128 x 128 tiles, each slice
+// at least four 64-long K tiles (ktot: the reduction length including the
+// compensated segments).  With a static row count every launched slice is used.
+__device__ __forceinline__ int gemm_active_splits(int splits, int M_eff, int N, int ktot) {
+    if (splits <= 1) return splits;
+    const int tiles = ((M_eff + 127) / 128) * ((N + 127) / 128);
+    int s = min(splits, max(1, 512 / max(tiles, 1)));
+    while (s > 1 && ktot < 4 * 64 * s) --s;
+    return s;
+}
+
+// A product's rows as a consumer reads them when the producing GEMM deferred
+// its split-K reduction: row r = x[r] if the launch ran unsplit, else
+// (sum of ws[z][r] over the active slices, in the reduction pass's order)
+// + bias + resid[r].  N columns, leading dimension N everywhere.
+struct SplitRows {
+    const float* x = nullptr;
+    const float* ws = nullptr;    // [splits][M][N] (NULL: x only)
+    const float* bias = nullptr;  // [N] or NULL
+    const float* resid = nullptr; // [M][N] or NULL
+    int M = 0, N = 0, splits = 1, ktot = 0;
+    __device__ int active(int M_eff) const { return ws ? gemm_active_splits(splits, M_eff, N, ktot) : 1; }
 };
 
 // Enqueues the GEMM (and its split-K reduction) on stream s.

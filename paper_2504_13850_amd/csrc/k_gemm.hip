@@ -570,11 +570,7 @@ __device__ __forceinline__ int gemm_kseg(const GemmDesc& d, int Keff) {
 // two workgroups per CU busy over the active tiles, each at least four K tiles
 // long.  With static sizes every launched slice is used.
 __device__ __forceinline__ int active_splits(const GemmDesc& d, int M_eff, int ktot) {
-    if (d.splits <= 1 || !d.Mdev) return d.splits;
-    const int tiles = ((M_eff + BM - 1) / BM) * ((d.N + BN - 1) / BN);
-    int s = min(d.splits, max(1, 512 / max(tiles, 1)));
-    while (s > 1 && ktot < 4 * BK * s) --s;
-    return s;
+    return d.Mdev ? gemm_active_splits(d.splits, M_eff, d.N, ktot) : d.splits;
 }
 
 // The output tile and K slice of a workgroup.
@@ -1118,7 +1114,7 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
         return FO_EINVAL;
     }
     FO_LAUNCHED();
-    if (d.splits > 1) {
+    if (d.splits > 1 && !d.defer_reduce) {
         int64_t total = (int64_t)d.M * d.N;
         if (d.N % 4 == 0) total /= 4;
         int grid = (int)std::min<int64_t>(cdiv(total, 256), 4096);

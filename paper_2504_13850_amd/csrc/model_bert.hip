@@ -117,19 +117,83 @@ __device__ __forceinline__ f32x4 bf4lo(f32x4 v) {  // v - bf16(v), elementwise
     return r;
 }
 
-__global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ u, const float* __restrict__ g,
-                                                     const float* __restrict__ beta, const int* __restrict__ Tdev,
-                                                     float* __restrict__ yf, bf16_t* __restrict__ yb,
-                                                     bf16_t* __restrict__ ylo, float* __restrict__ mean,
-                                                     float* __restrict__ rstd) {
+// The lane's PER4 column groups (4 lane + 256 k .. + 3) of row `row` of a product
+// whose split-K reduction was deferred to this consumer, summed over its S
+// active slices (the reduction pass's order) plus bias and residual; S = 1: the
+// product's own output.  S is a template parameter so that every load of the
+// row is in flight before the first add.
+template <int S>
+__device__ __forceinline__ void split_row(const SplitRows& src, int row, int lane, f32x4 (&x)[PER4]) {
+    if constexpr (S == 1) {
+#pragma unroll
+        for (int k = 0; k < PER4; ++k) x[k] = ld4(src.x + (int64_t)row * D + 4 * lane + 256 * k);
+    } else {
+        const int64_t full = (int64_t)src.M * D;
+        f32x4 p[PER4][S], bb[PER4], rr[PER4];
+        const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < PER4; ++k) {
+            const int c = 4 * lane + 256 * k;
+#pragma unroll
+            for (int z = 0; z < S; ++z) p[k][z] = ld4(src.ws + z * full + (int64_t)row * D + c);
+            bb[k] = src.bias ? ld4(src.bias + c) : zero;
+            rr[k] = src.resid ? ld4(src.resid + (int64_t)row * D + c) : zero;
+        }
+#pragma unroll
+        for (int k = 0; k < PER4; ++k) {
+            f32x4 v = p[k][0];
+            int z = 1;
+#pragma unroll
+            for (; z + 3 < S; z += 4) v += (p[k][z] + p[k][z + 1]) + (p[k][z + 2] + p[k][z + 3]);
+#pragma unroll
+            for (; z < S; ++z) v += p[k][z];
+            x[k] = (v + bb[k]) + rr[k];
+        }
+    }
+}
+__device__ __forceinline__ void load_split_row(const SplitRows& src, int S, int row, int lane, f32x4 (&x)[PER4]) {
+    switch (S) {
+        case 2: split_row<2>(src, row, lane, x); break;
+        case 3: split_row<3>(src, row, lane, x); break;
+        case 4: split_row<4>(src, row, lane, x); break;
+        case 1: split_row<1>(src, row, lane, x); break;
+        default: {  // not used here (the products feeding a LayerNorm split at most 4 ways)
+            const int64_t full = (int64_t)src.M * D;
+            const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < PER4; ++k) {
+                const int c = 4 * lane + 256 * k;
+                const float* p = src.ws + (int64_t)row * D + c;
+                f32x4 v = ld4(p);
+                int z = 1;
+                for (; z + 3 < S; z += 4)
+                    v += (ld4(p + z * full) + ld4(p + (z + 1) * full)) + (ld4(p + (z + 2) * full) + ld4(p + (z + 3) * full));
+                for (; z < S; ++z) v += ld4(p + z * full);
+                x[k] = (v + (src.bias ? ld4(src.bias + c) : zero)) +
+                       (src.resid ? ld4(src.resid + (int64_t)row * D + c) : zero);
+            }
+        }
+    }
+}
+
+// The input row u comes from `src` (a product whose split-K reduction is
+// summed here when deferred; the sum is then also stored to u_store, the
+// copy the backward reads).
+__global__ void __launch_bounds__(256) ln_fwd_kernel(const SplitRows src, float* __restrict__ u_store,
+                                                     const float* __restrict__ g, const float* __restrict__ beta,
+                                                     const int* __restrict__ Tdev, float* __restrict__ yf,
+                                                     bf16_t* __restrict__ yb, bf16_t* __restrict__ ylo,
+                                                     float* __restrict__ mean, float* __restrict__ rstd) {
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-    if (row >= *Tdev) return;
-    const float* ur = u + (int64_t)row * D;
+    const int T = *Tdev;
+    if (row >= T) return;
+    const int S = src.active(T);
     f32x4 x[PER4];
+    load_split_row(src, S, row, lane, x);
     float s = 0.f;
 #pragma unroll
     for (int k = 0; k < PER4; ++k) {
-        x[k] = ld4(ur + 4 * lane + 256 * k);
+        if (S > 1) st4(u_store + (int64_t)row * D + 4 * lane + 256 * k, x[k]);
         s += (x[k][0] + x[k][1]) + (x[k][2] + x[k][3]);
     }
     const float mu = wave_sum(s) * (1.f / D);
@@ -164,7 +228,7 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ u
 // part[block][1][c] = sum dy (dbeta), part[block][2][c] = sum dx (the bias
 // gradient of the sublayer whose sum with the residual this norm normalises).
 constexpr int LNB_ROWS = 16;
-__global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ dy, const float* __restrict__ u,
+__global__ void __launch_bounds__(256) ln_bwd_kernel(const SplitRows dy, const float* __restrict__ u,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
                                                      const float* __restrict__ g, const int* __restrict__ Tdev,
                                                      float* __restrict__ dxf, bf16_t* __restrict__ dxb,
@@ -175,6 +239,7 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ d
     const int r0 = blockIdx.x * LNB_ROWS;
     if (r0 >= T) return;  // uniform
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int S = dy.active(T);
     f32x4 gam[PER4], pg[PER4], pb[PER4], px[PER4];
 #pragma unroll
     for (int k = 0; k < PER4; ++k) {
@@ -188,11 +253,9 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* __restrict__ d
         const int row = min(r0 + wave * RW + i, T - 1);  // rows past T load row T - 1 and are skipped
         mu[i] = mean[row];
         rs[i] = rstd[row];
+        load_split_row(dy, S, row, lane, dv[i]);
 #pragma unroll
-        for (int k = 0; k < PER4; ++k) {
-            dv[i][k] = ld4(dy + (int64_t)row * D + 4 * lane + 256 * k);
-            uv[i][k] = ld4(u + (int64_t)row * D + 4 * lane + 256 * k);
-        }
+        for (int k = 0; k < PER4; ++k) uv[i][k] = ld4(u + (int64_t)row * D + 4 * lane + 256 * k);
     }
 #pragma unroll
     for (int i = 0; i < RW; ++i) {
@@ -445,7 +508,29 @@ GemmDesc lin_fwd(int rows, const bf16_t* A, const bf16_t* Alo, int K, const bf16
 
 // Backward of a norm: dx (fp32 and bf16) plus dgamma, dbeta and the column
 // sum of dx (into dbias_below).
-fo_status ln_bwd(const Plan* P, const float* dy, const float* u, const float* mean, const float* rstd,
+// The rows of a GEMM's output as its consumer reads them when the GEMM leaves
+// its split-K reduction to that consumer (Cf, ldcf = ldr = N).
+SplitRows deferred_rows(const GemmDesc& g) {
+    SplitRows r;
+    r.x = g.Cf;
+    r.ws = g.splits > 1 ? g.ws : nullptr;
+    r.bias = g.bias;
+    r.resid = g.resid;
+    r.M = g.M;
+    r.N = g.N;
+    r.splits = g.splits;
+    r.ktot = g.nseg * (g.nseg > 1 ? (int)cdiv(g.K, 64) * 64 : g.K);
+    return r;
+}
+SplitRows plain_rows(const float* x, int M) {
+    SplitRows r;
+    r.x = x;
+    r.M = M;
+    r.N = D;
+    return r;
+}
+
+fo_status ln_bwd(const Plan* P, const SplitRows& dy, const float* u, const float* mean, const float* rstd,
                  const float* gamma, const int* Tdev, int rows, float* dxf, bf16_t* dxb, float* dg, float* db,
                  float* dbias_below, hipStream_t s) {
     hipLaunchKernelGGL(ln_bwd_kernel, dim3(cdiv(rows, LNB_ROWS)), dim3(256), 0, s, dy, u, mean, rstd, gamma, Tdev,
@@ -495,9 +580,10 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         o.bias = prm + f.bo;
         o.resid = P->Xf[l]; o.ldr = D;
         o.Cf = t.u1; o.ldcf = D;
+        o.defer_reduce = true;  // summed by the LayerNorm below
         TRY(gemm(o, s));
-        hipLaunchKernelGGL(ln_fwd_kernel, lngrid, dim3(256), 0, s, t.u1, prm + f.g1, prm + f.b1, Tdev, t.Hf, t.Hb,
-                           t.Hlo, t.mean1, t.rstd1);
+        hipLaunchKernelGGL(ln_fwd_kernel, lngrid, dim3(256), 0, s, deferred_rows(o), t.u1, prm + f.g1, prm + f.b1,
+                           Tdev, t.Hf, t.Hb, t.Hlo, t.mean1, t.rstd1);
         GemmDesc f1 = lin_fwd(rows, t.Hb, t.Hlo, D, W + f.w1, Wl + f.w1, FF);
         f1.Mdev = Tdev;
         f1.bias = prm + f.bf1;
@@ -510,9 +596,10 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         f2.bias = prm + f.bf2;
         f2.resid = t.Hf; f2.ldr = D;
         f2.Cf = t.u2; f2.ldcf = D;
+        f2.defer_reduce = true;
         TRY(gemm(f2, s));
-        hipLaunchKernelGGL(ln_fwd_kernel, lngrid, dim3(256), 0, s, t.u2, prm + f.g2, prm + f.b2, Tdev, P->Xf[l + 1],
-                           P->Xb[l + 1], P->Xlo[l + 1], t.mean2, t.rstd2);
+        hipLaunchKernelGGL(ln_fwd_kernel, lngrid, dim3(256), 0, s, deferred_rows(f2), t.u2, prm + f.g2, prm + f.b2,
+                           Tdev, P->Xf[l + 1], P->Xb[l + 1], P->Xlo[l + 1], t.mean2, t.rstd2);
         FO_LAUNCHED();
     }
 
@@ -538,15 +625,15 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     // stream has finished with them.
     hipStream_t s2 = P->side;
     int cur = 0;
+    SplitRows dy_rows = plain_rows(P->dY[0], rows);  // the LN2 backward's input: dY, or the deferred dX of the layer above
     for (int l = NL - 1; l >= 0; --l) {
         const LayerOff& f = P->off[l];
         LayerAct& t = P->a[l];
-        float* dY = P->dY[cur];
         const int pb = l & 1;
         bf16_t *du2b = P->du2b[pb], *dA1 = P->dA1[pb], *du1b = P->du1b[pb], *dqkv = P->dqkv[pb];
         if (l + 2 < NL) FO_HIP(hipStreamWaitEvent(s, P->ev_done[pb], 0));
         // LN2
-        TRY(ln_bwd(P, dY, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, du2b, grd + f.g2, grd + f.b2,
+        TRY(ln_bwd(P, dy_rows, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, du2b, grd + f.g2, grd + f.b2,
                    grd + f.bf2, s));
         TRY(order_after(s2, s, P->ev_fork));
         // FFN2: dG = du2 W2 (times GELU' of the FFN1 pre-activation -> dA1), dW2 = du2^T G, db2
@@ -572,6 +659,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             TRY(launch_colsum_finish(P->colws, rows, Tdev, 128, FF, cb, s));
             TRY(order_after(s2, s, P->ev_fork));
         }
+        SplitRows dh_rows;
         // FFN1: dH = du2 + dA1 W1, dW1 = dA1^T H, db1
         {
             GemmDesc w;
@@ -588,10 +676,12 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.resid = P->du2f; d.ldr = D;
             d.Cf = P->dHf; d.ldcf = D;
             d.splits = split_rows(FF); d.ws = P->splitws;
+            d.defer_reduce = true;  // summed by the LN1 backward
             TRY(gemm(d, s));
+            dh_rows = deferred_rows(d);
         }
         // LN1
-        TRY(ln_bwd(P, P->dHf, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, du1b, grd + f.g1,
+        TRY(ln_bwd(P, dh_rows, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, du1b, grd + f.g1,
                    grd + f.b1, grd + f.bo, s));
         TRY(order_after(s2, s, P->ev_fork));
         // output projection: dO = du1 Wo, dWo = du1^T O, dbo
@@ -633,7 +723,9 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.resid = P->du1f; d.ldr = D;
             d.Cf = P->dY[cur ^ 1]; d.ldcf = D;
             d.splits = split_rows(3 * D); d.ws = P->splitws;
+            d.defer_reduce = true;  // summed by the next layer's LN2 backward
             TRY(gemm(d, s));
+            dy_rows = deferred_rows(d);
         }
         TRY(launch_colsum(dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws, s));
         cur ^= 1;
