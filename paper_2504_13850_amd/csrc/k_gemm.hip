@@ -11,6 +11,7 @@
 // contiguous in memory (weight gradients, input gradients through W) are
 // transposed on their way into LDS (k pairs packed into 32-bit stores).
 #include <algorithm>
+#include <type_traits>
 
 #include <hip/hip_ext.h>
 
@@ -850,6 +851,9 @@ constexpr int CBK = 32;
 struct DmaRKc {  // one 128 x 32 tile; this wave's instructions are q = wave and wave + 4
     int64_t off[2];
     int koff;
+    __device__ void init(const GemmDesc& d, bool is_a, int r0, int R, int lane, int wave) {
+        init(is_a ? d.lda : d.ldb, r0, R, lane, wave);
+    }
     __device__ void init(int64_t ld, int r0, int R, int lane, int wave) {
         koff = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
 #pragma unroll
@@ -867,6 +871,43 @@ struct DmaRKc {  // one 128 x 32 tile; this wave's instructions are q = wave and
     }
 };
 
+// The A operand of a convolution forward (implicit GEMM: rows = output pixels
+// (b, oy, ox), k = (ky, kx, ci) over the NHWC input, Ci % 64 == 0 so that a
+// 32-wide K tile lies in one filter tap), in the same 128 x 32 LDS tile layout
+// as DmaRKc: each lane copies the 16 bytes of channels it owns from the input
+// pixel its row reads at the tile's tap, or the zero block in the padding.
+struct DmaConvA {
+    ConvGeom g;
+    int b[2], iy0[2], ix0[2];
+    bool ok[2];
+    int koff;
+    __device__ void init(const GemmDesc& d, bool, int r0, int R, int lane, int wave) {
+        g = d.g;
+        koff = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
+        const int hw = g.Ho * g.Wo;
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+            const int gr = r0 + 16 * (wave + 4 * v) + (lane >> 2);
+            ok[v] = gr < R;
+            b[v] = gr / hw;
+            const int rem = gr - b[v] * hw, oy = rem / g.Wo, ox = rem - oy * g.Wo;
+            iy0[v] = oy * g.stride - g.pad;
+            ix0[v] = ox * g.stride - g.pad;
+        }
+    }
+    __device__ void copy(const bf16_t* X, int kb, int kend, bf16_t* tile, int wave) const {
+        const int tap = kb / g.Ci, ci = kb - tap * g.Ci + koff;
+        const int ky = tap / g.kw, kx = tap - ky * g.kw;
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+            const int iy = iy0[v] + ky, ix = ix0[v] + kx;
+            const bool in = ok[v] && kb < kend && iy >= 0 && iy < g.H && ix >= 0 && ix < g.W;
+            __builtin_amdgcn_global_load_lds(in ? X + (((int64_t)b[v] * g.H + iy) * g.W + ix) * g.Ci + ci : kZero8,
+                                             FO_LDS(tile + (wave + 4 * v) * 512), 16, 0, 0);
+        }
+    }
+};
+
 // s_waitcnt immediate that waits for at most n vector memory operations in
 // flight and does not wait on LDS / scalar memory or exports.
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
@@ -875,7 +916,7 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) |
 // of tile t.  Every copy is issued, also past the slice's last tile (those read
 // kZero8 into a stage that is not read again), so the number of copies in
 // flight is static and each wait names exactly the tile it needs.
-template <int NSEG, int NST>
+template <int NSEG, int NST, class LA>
 __global__ void __launch_bounds__(NT, NST == 2 ? 2 : 1) gemm_comp_dma_kernel(const GemmDesc d) {
     // NST stages of four unpadded 128 x 32 tiles (A, A_lo, B, B_lo) = 32 KB each;
     // reused for the C tile (64 KB)
@@ -897,9 +938,10 @@ __global__ void __launch_bounds__(NT, NST == 2 ? 2 : 1) gemm_comp_dma_kernel(con
     const int kstop = min(kpad, kbeg + kc);
     const int nk = kstop > kbeg ? (kstop - kbeg) / CBK : 0;
 
-    DmaRKc la, lb;
-    la.init(d.lda, job.m0, M, lane, wave);
-    lb.init(d.ldb, job.n0, d.N, lane, wave);
+    LA la;
+    DmaRKc lb;
+    la.init(d, true, job.m0, M, lane, wave);
+    lb.init(d, false, job.n0, d.N, lane, wave);
 
     f32x16 acc[2][2];
 #pragma unroll
@@ -1020,18 +1062,21 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
     }
 }
 
-template <int NSEG, int NST = 2>
+template <int NSEG, class LA = DmaRKc, int NST = 2>
 void launch_comp(const GemmDesc& d, hipStream_t s) {
     ProfInfo pi;
     pi.kind = PROF_GEMM;
     pi.M = d.M; pi.N = d.N; pi.K = d.K; pi.nseg = d.nseg;
     pi.Mdev = d.Mdev; pi.Kdev = d.Kdev;
     hipEvent_t ea, eb;
-    const int h = prof_begin_ext(NSEG == 3 ? "gemm_comp_dma_kernel<3>" : "gemm_comp_dma_kernel<2>", pi, &ea, &eb);
+    constexpr bool conv = std::is_same<LA, DmaConvA>::value;
+    const char* name = conv ? (NSEG == 3 ? "gemm_comp_dma_kernel<3, conv>" : "gemm_comp_dma_kernel<2, conv>")
+                            : (NSEG == 3 ? "gemm_comp_dma_kernel<3>" : "gemm_comp_dma_kernel<2>");
+    const int h = prof_begin_ext(name, pi, &ea, &eb);
     GemmDesc dd = d;
     dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
-    hipExtLaunchKernelGGL((gemm_comp_dma_kernel<NSEG, NST>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
+    hipExtLaunchKernelGGL((gemm_comp_dma_kernel<NSEG, NST, LA>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
     prof_end_ext(h);
 }
 
@@ -1099,6 +1144,10 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     // (a k-major A with a device-side row bound may end inside an 8-row chunk)
     const bool al = (a == OP_RK || a == OP_KR) && (b == OP_RK || b == OP_KR) && !(a == OP_KR && d.Mdev) &&
                     op_aligned(a, d.A, d.A2, d.lda, d.M) && op_aligned(b, d.B, d.B2, d.ldb, d.N);
+    // compensated convolution forward, single pass with copies straight into LDS:
+    // 16-byte aligned input and weights, Ci % 64 == 0, static sizes
+    const bool conv_comp = a == OP_CONV_FWD && b == OP_RK && d.nseg > 1 && !d.Kdev && d.g.Ci % 64 == 0 &&
+                           al16(d.A) && al16(d.A2) && op_aligned(OP_RK, d.B, d.B2, d.ldb, d.N);
     // (two stages and two workgroups per CU beat deeper rings at one per CU)
     if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
         d.nseg == 3 ? launch_comp<3>(dv, s) : launch_comp<2>(dv, s);
@@ -1106,6 +1155,8 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KRT, true>(dv, s) : launch<OP_RK, OP_KR>(dv, s);
     else if (a == OP_KR && b == OP_KR) al ? launch<OP_KRT, OP_KRT, true>(dv, s) : launch<OP_KR, OP_KR>(dv, s);
     else if (a == OP_KR && b == OP_RK) al ? launch<OP_KRT, OP_RK, true>(dv, s) : launch<OP_KR, OP_RK>(dv, s);
+    else if (a == OP_CONV_FWD && b == OP_RK && conv_comp)
+        d.nseg == 3 ? launch_comp<3, DmaConvA>(dv, s) : launch_comp<2, DmaConvA>(dv, s);
     else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(dv, s);
     else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(dv, s);
     else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(dv, s);
