@@ -298,6 +298,8 @@ struct LdConvDx {
             ix[v] = rem - iy[v] * g.W;
         }
     }
+    // (every load is issued, zero-filled outside: usable by the aligned kernel)
+    __device__ void load_al(const bf16_t* P, int kb, int kend, uint4* r) const { load(P, kb, kend, r); }
     __device__ void load(const bf16_t* DY, int kb, int kend, uint4* r) const {
         const int tap = kb / g.Co, co = kb - tap * g.Co + kc;
         const int ky = tap / g.kw, kx = tap - ky * g.kw;
@@ -345,6 +347,34 @@ struct LdConvDxW : LdKRBase {
     }
 };
 
+// The same operand staged untransposed for the LDS transpose read (as LdKRt):
+// tile [64 k = co][128 rows = ci] of one filter tap (Co % 64 == 0, Ci % 8 == 0),
+// sixteen lanes per k row.
+struct LdConvDxWt {
+    ConvGeom g;
+    int kr, rl, rc;  // k row, row within the tile, operand row (ci)
+    bool rowok;
+    int64_t ldk;     // elements between consecutive co
+    __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
+        g = g_;
+        kr = tid >> 4;
+        rl = (tid & 15) * 8;
+        rc = r0 + rl;
+        rowok = rc < R;
+        ldk = (int64_t)g.kh * g.kw * g.Ci;
+    }
+    __device__ void load_al(const bf16_t* Wt, int kb, int kend, uint4* o) const {
+        const int tap = kb / g.Co, co0 = kb - tap * g.Co;
+        const bf16_t* p = Wt + (int64_t)(co0 + kr) * ldk + (int64_t)tap * g.Ci + rc;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = load8(rowok && kb + kr + 16 * j < kend ? p + 16 * j * ldk : kZero8);
+    }
+    __device__ void store(bf16_t* t, const uint4* r, int) const {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4*>(&t[kr_idx(kr + 16 * j, rl)]) = r[j];
+    }
+};
+
 // Conv weight-gradient B: rows = (ky, kx, ci), k = output pixel; reads the input NHWC.
 struct LdConvDwX : LdKRBase {
     ConvGeom g;
@@ -364,6 +394,8 @@ struct LdConvDwX : LdKRBase {
             kx[q] = tap - ky[q] * g.kw;
         }
     }
+    // (every load is issued, zero-filled outside: usable by the aligned kernel)
+    __device__ void load_al(const bf16_t* P, int kb, int kend, uint4* r) const { load(P, kb, kend, r); }
     __device__ void load(const bf16_t* X, int kb, int kend, uint4* o) const {
         const int hw = g.Ho * g.Wo;
 #pragma unroll
@@ -398,6 +430,8 @@ template <> struct LoaderOf<OP_CONV_DXW> { typedef LdConvDxW T; };
 template <> struct LoaderOf<OP_CONV_DWX> { typedef LdConvDwX T; };
 constexpr int OP_KRT = 6;  // OP_KR staged untransposed, read through the LDS transpose
 template <> struct LoaderOf<OP_KRT> { typedef LdKRt T; };
+constexpr int OP_CONV_DXWT = 7;  // OP_CONV_DXW staged untransposed, read through the LDS transpose
+template <> struct LoaderOf<OP_CONV_DXWT> { typedef LdConvDxWt T; };
 
 template <int MODE>
 __device__ __forceinline__ void loader_init(typename LoaderOf<MODE>::T& L, const bf16_t* P, int64_t ld,
@@ -778,11 +812,11 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
             bf16x8_t a[2], b[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i)
-                a[i] = AM == OP_KRT ? frag_tr(As, i ? atr1 : atr0, ks * 16 * BM)
+                a[i] = (AM == OP_KRT || AM == OP_CONV_DXWT) ? frag_tr(As, i ? atr1 : atr0, ks * 16 * BM)
                                     : *reinterpret_cast<const bf16x8_t*>(&As[aoff + i * 32 * LDR + ks * 16]);
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                b[j] = BMODE == OP_KRT ? frag_tr(Bs, j ? btr1 : btr0, ks * 16 * BM)
+                b[j] = (BMODE == OP_KRT || BMODE == OP_CONV_DXWT) ? frag_tr(Bs, j ? btr1 : btr0, ks * 16 * BM)
                                        : *reinterpret_cast<const bf16x8_t*>(&Bs[boff + j * 32 * LDR + ks * 16]);
 #pragma unroll
             for (int i = 0; i < 2; ++i)
@@ -1083,8 +1117,8 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
 template <int AM, int BMODE, bool AL = false>
 void launch(const GemmDesc& d, hipStream_t s) {
     // kernel names as the profilers print them
-    static const char* names[7][7] = {};
-    static char buf[7][7][32];
+    static const char* names[8][8] = {};
+    static char buf[8][8][32];
     if (!names[AM][BMODE]) {
         snprintf(buf[AM][BMODE], sizeof(buf[AM][BMODE]), "gemm_kernel<%d, %d>", AM, BMODE);
         names[AM][BMODE] = buf[AM][BMODE];
@@ -1144,6 +1178,8 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     // (a k-major A with a device-side row bound may end inside an 8-row chunk)
     const bool al = (a == OP_RK || a == OP_KR) && (b == OP_RK || b == OP_KR) && !(a == OP_KR && d.Mdev) &&
                     op_aligned(a, d.A, d.A2, d.lda, d.M) && op_aligned(b, d.B, d.B2, d.ldb, d.N);
+    // a 16-byte aligned operand whose contiguous rows come in whole chunks of 8
+    auto conv_al = [&](const bf16_t* P, int rows) { return al16(P) && rows % 8 == 0; };
     // compensated convolution forward, single pass with copies straight into LDS:
     // 16-byte aligned input and weights, Ci % 64 == 0, static sizes
     const bool conv_comp = a == OP_CONV_FWD && b == OP_RK && d.nseg > 1 && !d.Kdev && d.g.Ci % 64 == 0 &&
@@ -1158,7 +1194,11 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     else if (a == OP_CONV_FWD && b == OP_RK && conv_comp)
         d.nseg == 3 ? launch_comp<3, DmaConvA>(dv, s) : launch_comp<2, DmaConvA>(dv, s);
     else if (a == OP_CONV_FWD && b == OP_RK) launch<OP_CONV_FWD, OP_RK>(dv, s);
+    else if (a == OP_CONV_DX && b == OP_CONV_DXW && conv_al(d.B, d.g.Ci))
+        launch<OP_CONV_DX, OP_CONV_DXWT, true>(dv, s);
     else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(dv, s);
+    else if (a == OP_KR && b == OP_CONV_DWX && conv_al(d.A, d.M) && d.lda % 8 == 0 && !d.Mdev && !d.Kdev)
+        launch<OP_KRT, OP_CONV_DWX, true>(dv, s);
     else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(dv, s);
     else {
         set_error("gemm: unsupported operand modes %d/%d", a, b);
