@@ -420,6 +420,46 @@ struct LdConvDwX : LdKRBase {
     }
 };
 
+// The same operand staged untransposed for the LDS transpose read: tile
+// [64 k = output pixels][128 rows = (ky, kx, ci)].  Thread = one pixel (tid / 4)
+// and four 8-row chunks 8 (tid % 4 + 4 j), so a thread decomposes one pixel
+// per K tile; four lanes read 64 contiguous bytes of one input pixel.
+struct LdConvDwXt {
+    ConvGeom g;
+    int kr, c0;
+    int ky[4], kx[4], ci[4];
+    bool rok[4];
+    __device__ void init(const bf16_t*, const ConvGeom& g_, int r0, int R, int tid) {
+        g = g_;
+        kr = tid >> 2;
+        c0 = (tid & 3) * 8;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int n = r0 + c0 + 32 * j;
+            rok[j] = n < R;
+            const int tap = n / g.Ci;
+            ci[j] = n - tap * g.Ci;
+            ky[j] = tap / g.kw;
+            kx[j] = tap - ky[j] * g.kw;
+        }
+    }
+    __device__ void load_al(const bf16_t* X, int kb, int kend, uint4* o) const {
+        const int pix = kb + kr, hw = g.Ho * g.Wo;
+        const bool pin = pix < kend;
+        const int b = pix / hw, rem = pix - b * hw, oy = rem / g.Wo, ox = rem - oy * g.Wo;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int iy = oy * g.stride - g.pad + ky[j], ix = ox * g.stride - g.pad + kx[j];
+            const bool in = pin && rok[j] && iy >= 0 && iy < g.H && ix >= 0 && ix < g.W;
+            o[j] = load8(in ? X + (((int64_t)b * g.H + iy) * g.W + ix) * g.Ci + ci[j] : kZero8);
+        }
+    }
+    __device__ void store(bf16_t* t, const uint4* r, int) const {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4*>(&t[kr_idx(kr, c0 + 32 * j)]) = r[j];
+    }
+};
+
 template <int MODE>
 struct LoaderOf;
 template <> struct LoaderOf<OP_RK> { typedef LdRK T; };
@@ -432,6 +472,8 @@ constexpr int OP_KRT = 6;  // OP_KR staged untransposed, read through the LDS tr
 template <> struct LoaderOf<OP_KRT> { typedef LdKRt T; };
 constexpr int OP_CONV_DXWT = 7;  // OP_CONV_DXW staged untransposed, read through the LDS transpose
 template <> struct LoaderOf<OP_CONV_DXWT> { typedef LdConvDxWt T; };
+constexpr int OP_CONV_DWXT = 8;  // OP_CONV_DWX staged untransposed, read through the LDS transpose
+template <> struct LoaderOf<OP_CONV_DWXT> { typedef LdConvDwXt T; };
 
 template <int MODE>
 __device__ __forceinline__ void loader_init(typename LoaderOf<MODE>::T& L, const bf16_t* P, int64_t ld,
@@ -812,11 +854,11 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
             bf16x8_t a[2], b[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i)
-                a[i] = (AM == OP_KRT || AM == OP_CONV_DXWT) ? frag_tr(As, i ? atr1 : atr0, ks * 16 * BM)
+                a[i] = (AM == OP_KRT || AM == OP_CONV_DXWT || AM == OP_CONV_DWXT) ? frag_tr(As, i ? atr1 : atr0, ks * 16 * BM)
                                     : *reinterpret_cast<const bf16x8_t*>(&As[aoff + i * 32 * LDR + ks * 16]);
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                b[j] = (BMODE == OP_KRT || BMODE == OP_CONV_DXWT) ? frag_tr(Bs, j ? btr1 : btr0, ks * 16 * BM)
+                b[j] = (BMODE == OP_KRT || BMODE == OP_CONV_DXWT || BMODE == OP_CONV_DWXT) ? frag_tr(Bs, j ? btr1 : btr0, ks * 16 * BM)
                                        : *reinterpret_cast<const bf16x8_t*>(&Bs[boff + j * 32 * LDR + ks * 16]);
 #pragma unroll
             for (int i = 0; i < 2; ++i)
@@ -1117,8 +1159,8 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
 template <int AM, int BMODE, bool AL = false>
 void launch(const GemmDesc& d, hipStream_t s) {
     // kernel names as the profilers print them
-    static const char* names[8][8] = {};
-    static char buf[8][8][32];
+    static const char* names[9][9] = {};
+    static char buf[9][9][32];
     if (!names[AM][BMODE]) {
         snprintf(buf[AM][BMODE], sizeof(buf[AM][BMODE]), "gemm_kernel<%d, %d>", AM, BMODE);
         names[AM][BMODE] = buf[AM][BMODE];
@@ -1198,7 +1240,7 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
         launch<OP_CONV_DX, OP_CONV_DXWT, true>(dv, s);
     else if (a == OP_CONV_DX && b == OP_CONV_DXW) launch<OP_CONV_DX, OP_CONV_DXW>(dv, s);
     else if (a == OP_KR && b == OP_CONV_DWX && conv_al(d.A, d.M) && d.lda % 8 == 0 && !d.Mdev && !d.Kdev)
-        launch<OP_KRT, OP_CONV_DWX, true>(dv, s);
+        launch<OP_KRT, OP_CONV_DWXT, true>(dv, s);
     else if (a == OP_KR && b == OP_CONV_DWX) launch<OP_KR, OP_CONV_DWX>(dv, s);
     else {
         set_error("gemm: unsupported operand modes %d/%d", a, b);
