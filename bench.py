@@ -82,11 +82,13 @@ def cpu_baseline(cid, sample_steps):
 # The kernels whose HBM bytes are taken from rocprofv3 counters: (name prefix in
 # the profiler's kernel names, the sources that define them).
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_bert_step.txt")
+GEMM_SOURCES = ["paper_2504_13850_amd/csrc/k_gemm.hip", "paper_2504_13850_amd/csrc/gemm.h",
+                "paper_2504_13850_amd/csrc/common.h"]
 TRAFFIC_KERNELS = {
-    "gemm_comp_dma_kernel<3>": ("gemm_comp_dma_kernel<3>", ["paper_2504_13850_amd/csrc/k_gemm.hip",
-                                                            "paper_2504_13850_amd/csrc/gemm.h"]),
-    "gemm_kernel<0, 0>": ("gemm_kernel<0, 0,", ["paper_2504_13850_amd/csrc/k_gemm.hip",
-                                                 "paper_2504_13850_amd/csrc/gemm.h"]),
+    # compensated forward products, input gradients, weight gradients of the transformer step
+    "gemm_comp_dma_kernel<3>": ("gemm_comp_dma_kernel<3, 2, fo::(anonymous namespace)::DmaRKc>", GEMM_SOURCES),
+    "gemm_kernel<0, 6>": ("gemm_kernel<0, 6, true>", GEMM_SOURCES),
+    "gemm_kernel<6, 6>": ("gemm_kernel<6, 6, true>", GEMM_SOURCES),
     "agg_lerp_kernel": ("agg_lerp_kernel(", ["paper_2504_13850_amd/csrc/k_update.hip"]),
 }
 CALIB_BYTES = 1 << 30
