@@ -62,6 +62,14 @@ struct GemmDesc {
     bf16_t* Cb = nullptr;   // bf16(v)
     bf16_t* Cb2 = nullptr;  // bf16(v - bf16(v)), the low part (same leading dimension)
     int64_t ldcb = 0;
+    // Fused SGD (Alg. 4's update) on a weight gradient stored in the weight's
+    // own layout (Cf, leading dimension ldcf): after the store, theta[m][n]
+    // becomes fma(-sgd_lr, v, theta[m][n]) and its bf16 high and low parts go to
+    // sgd_hi / sgd_lo (same indexing).  Needs Cf.
+    float* sgd_theta = nullptr;
+    bf16_t* sgd_hi = nullptr;
+    bf16_t* sgd_lo = nullptr;
+    float sgd_lr = 0.f;
     // Column sums of the stored value: colpart[m / 128][n] = sum of v over the
     // valid rows of that 128-row tile (no split-K); launch_colsum_finish with
     // rows_per_part 128 completes them.
@@ -77,6 +85,7 @@ struct GemmDesc {
     const int* Kdev = nullptr;
     int* prof_snap = nullptr;  // set by the launcher when profiling: receives (M, K) effective
     int vec_epi = 0;           // set by the launcher: the epilogue may move four columns per access
+    int variant = 0;           // kernel variant override (0: the launcher's choice)
     // With split-K: leave the partials in ws and skip the reduction pass; the
     // consumer sums them (see SplitRows).  A launch that runs unsplit (one
     // active slice) still applies its epilogue and writes Cf.

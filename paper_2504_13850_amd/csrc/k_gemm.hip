@@ -546,6 +546,14 @@ __device__ __forceinline__ float epi_store(const GemmDesc& d, int row, int col, 
     if (d.mask && !(e.mask > 0.f)) v = 0.f;
     if (d.dact) v *= e.dact;
     if (d.Cf) d.Cf[(int64_t)row * d.ldcf + col] = v;
+    if (d.sgd_theta) {
+        const int64_t o = (int64_t)row * d.ldcf + col;
+        const float th = __builtin_fmaf(-d.sgd_lr, v, d.sgd_theta[o]);
+        d.sgd_theta[o] = th;
+        const bf16_t h = f2bf(th);
+        d.sgd_hi[o] = h;
+        d.sgd_lo[o] = f2bf(th - bf2f(h));
+    }
     if (d.Cb) {
         const bf16_t hi = f2bf(v);
         d.Cb[(int64_t)row * d.ldcb + col] = hi;
@@ -625,6 +633,15 @@ __device__ __forceinline__ f32x4 epi_store4(const GemmDesc& d, int row, int col,
     }
     if (d.dact) v *= e.dact;
     if (d.Cf) *reinterpret_cast<f32x4*>(d.Cf + (int64_t)row * d.ldcf + col) = v;
+    if (d.sgd_theta) {
+        const int64_t o = (int64_t)row * d.ldcf + col;
+        f32x4 th = *reinterpret_cast<const f32x4*>(d.sgd_theta + o), lo;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) th[q] = __builtin_fmaf(-d.sgd_lr, v[q], th[q]);
+        *reinterpret_cast<f32x4*>(d.sgd_theta + o) = th;
+        *reinterpret_cast<u32x2*>(d.sgd_hi + o) = f_to_bf4(th, &lo);
+        *reinterpret_cast<u32x2*>(d.sgd_lo + o) = f_to_bf4(lo, nullptr);
+    }
     if (d.Cb) {
         f32x4 lo;
         const int64_t o = (int64_t)row * d.ldcb + col;
@@ -661,10 +678,11 @@ struct TileJob {
 // that XCD x owns a contiguous range, walked in groups of GM tile rows (M
 // fastest), which keeps the A row blocks and B column blocks it reads few and
 // shared.  Returns false when the workgroup has no tile.
+template <int BMt = BM>
 __device__ __forceinline__ bool map_tile(const GemmDesc& d, int M, int ktot_split, TileJob& job) {
     constexpr int GM = 8;
     const int S = active_splits(d, M, ktot_split);
-    const int nN = gridDim.x, nMe = (M + BM - 1) / BM;
+    const int nN = gridDim.x, nMe = (M + BMt - 1) / BMt;
     const int W = nMe * nN * S;
     const int w = blockIdx.x + nN * (blockIdx.y + gridDim.y * blockIdx.z);
     if (w >= W) return false;
@@ -675,7 +693,7 @@ __device__ __forceinline__ bool map_tile(const GemmDesc& d, int M, int ktot_spli
     const int g = tt / (GM * nN), tg = tt - g * GM * nN;
     const int gr = min(GM, nMe - g * GM);
     job.mt = g * GM + tg % gr;
-    job.m0 = job.mt * BM;
+    job.m0 = job.mt * BMt;
     job.n0 = (tg / gr) * BN;
     job.zt = zt;
     job.S = S;
@@ -688,8 +706,12 @@ __device__ __forceinline__ bool map_tile(const GemmDesc& d, int M, int ktot_spli
 // owns one column and walks 64 rows, so every global store instruction covers
 // 64 consecutive columns of one row.  Split slices store fp32 partials; a
 // whole product runs the epilogue (and the optional column sums).
+// BMt rows by NTt threads (4 waves of 64 x 64 per 128 rows); RP = NTt / 32 rows per
+// pass of the four-column path, HP = NTt / 128 row groups of the one-column path.
+template <int BMt = BM, int NTt = NT>
 __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc)[2][2], float* Cs, const TileJob& job,
                                            int M, int tid) {
+    constexpr int RP = NTt / 32, HP = NTt / 128;
     const int lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -708,7 +730,7 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
         f32x4 csum = {0.f, 0.f, 0.f, 0.f};
         if (col < d.N) {
             if (job.S > 1) {
-                for (int lr = rr; lr < BM && m0 + lr < M; lr += 8)
+                for (int lr = rr; lr < BMt && m0 + lr < M; lr += RP)
                     *reinterpret_cast<f32x4*>(d.ws + ((int64_t)job.zt * d.M + m0 + lr) * d.N + col) =
                         *reinterpret_cast<const f32x4*>(&Cs[lr * BN + c4]);
             } else {
@@ -717,16 +739,16 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
 #pragma unroll
                     for (int q = 0; q < 4; ++q) bias[q] = d.bias[col + q];
                 }
-                for (int lr0 = rr; lr0 < BM && m0 + lr0 < M; lr0 += 64) {
+                for (int lr0 = rr; lr0 < BMt && m0 + lr0 < M; lr0 += 8 * RP) {
                     EpiIn4 e[8];
 #pragma unroll
                     for (int u = 0; u < 8; ++u) {
-                        const int row = m0 + lr0 + 8 * u;
+                        const int row = m0 + lr0 + RP * u;
                         if (row < M) e[u] = epi_load4(d, row, col);
                     }
 #pragma unroll
                     for (int u = 0; u < 8; ++u) {
-                        const int lr = lr0 + 8 * u, row = m0 + lr;
+                        const int lr = lr0 + RP * u, row = m0 + lr;
                         if (row < M)
                             csum += epi_store4(d, row, col,
                                                *reinterpret_cast<const f32x4*>(&Cs[lr * BN + c4]) + bias + e[u].resid,
@@ -742,7 +764,7 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
             if (tid < BN && job.n0 + tid < d.N) {
                 float t = 0.f;
 #pragma unroll
-                for (int g = 0; g < 8; ++g) t += Cs[g * BN + tid];
+                for (int g = 0; g < RP; ++g) t += Cs[g * BN + tid];
                 d.colpart[(int64_t)job.mt * d.N + job.n0 + tid] = t;
             }
         }
@@ -752,7 +774,7 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
     float csum = 0.f;
     if (col < d.N) {
         if (job.S > 1) {
-            for (int lr = tid >> 7; lr < BM; lr += 2) {
+            for (int lr = tid >> 7; lr < BMt; lr += HP) {
                 const int row = m0 + lr;
                 if (row >= M) break;
                 d.ws[((int64_t)job.zt * d.M + row) * d.N + col] = Cs[lr * BN + c];
@@ -760,26 +782,31 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
         } else {
             const float bcol = d.bias ? d.bias[col] : 0.f;
             // eight rows per batch: their operand loads are in flight together
-            for (int lr0 = tid >> 7; lr0 < BM && m0 + lr0 < M; lr0 += 16) {
+            for (int lr0 = tid >> 7; lr0 < BMt && m0 + lr0 < M; lr0 += 8 * HP) {
                 EpiIn e[8];
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
-                    const int row = m0 + lr0 + 2 * u;
+                    const int row = m0 + lr0 + HP * u;
                     if (row < M) e[u] = epi_load(d, row, col);
                 }
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
-                    const int lr = lr0 + 2 * u, row = m0 + lr;
+                    const int lr = lr0 + HP * u, row = m0 + lr;
                     if (row < M) csum += epi_store(d, row, col, Cs[lr * BN + c] + bcol + e[u].resid, e[u]);
                 }
             }
         }
     }
-    if (d.colpart) {  // uniform; the two row halves of a column meet in LDS
+    if (d.colpart) {  // uniform; the HP row groups of a column meet in LDS
         __syncthreads();
-        if (tid >= BN) Cs[c] = csum;
+        if (tid >= BN) Cs[(tid >> 7) * BN + c] = csum;
         __syncthreads();
-        if (tid < BN && col < d.N) d.colpart[(int64_t)job.mt * d.N + col] = csum + Cs[c];
+        if (tid < BN && col < d.N) {
+            float t = csum;
+#pragma unroll
+            for (int g = 1; g < HP; ++g) t += Cs[g * BN + c];
+            d.colpart[(int64_t)job.mt * d.N + col] = t;
+        }
     }
 }
 
@@ -1091,6 +1118,136 @@ __global__ void __launch_bounds__(NT, NST == 2 ? 2 : 1) gemm_comp_dma_kernel(con
     store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
 }
 
+// The same single-pass product on 64*WM x 128 tiles: 2*WM waves of 64 x 64
+// (WM along M, two along N), NST stages of the A, A_lo, B and B_lo row tiles
+// (64 bytes per row, layout as DmaRKc) and one workgroup per CU.  With WM = 4
+// and three stages (144 KB of LDS) each copy is issued two K tiles before it is
+// read, twice the distance of the two-stage 128 x 128 form, and every K tile
+// moves 48 KB for twice the MFMA work of a 32 KB tile of that form.
+template <int NQ, int NW>
+struct DmaRows {  // one operand tile; this wave's instructions are q = wave + NW v (16 rows each)
+    int64_t off[NQ];
+    int koff;
+    __device__ void init(int64_t ld, int r0, int R, int lane, int wave) {
+        koff = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
+#pragma unroll
+        for (int v = 0; v < NQ; ++v) {
+            const int gr = r0 + 16 * (wave + NW * v) + (lane >> 2);
+            off[v] = gr < R ? (int64_t)gr * ld : -1;
+        }
+    }
+    __device__ void copy(const bf16_t* P, int kb, int kend, bf16_t* tile, int wave) const {
+        const int k = kb + koff;
+#pragma unroll
+        for (int v = 0; v < NQ; ++v)
+            __builtin_amdgcn_global_load_lds(off[v] >= 0 && k < kend ? P + off[v] + k : kZero8,
+                                             FO_LDS(tile + (wave + NW * v) * 512), 16, 0, 0);
+    }
+};
+
+template <int NSEG, int WM, int NST>
+__global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDesc d) {
+    constexpr int NW = 2 * WM, NTt = 64 * NW, BMt = 64 * WM;
+    constexpr int QA = BMt / 16 / NW, QB = BN / 16 / NW;
+    static_assert(QA >= 1 && QB >= 1, "tile rows per wave");
+    // stage rows: A [0, BMt), A_lo [BMt, 2 BMt), B [2 BMt, 2 BMt + BN), B_lo after
+    constexpr int SR = 2 * BMt + 2 * BN;
+    // the stages, reused for the C tile (BMt x BN fp32)
+    constexpr int SMEM = NST * SR * CBK > 2 * BMt * BN ? NST * SR * CBK : 2 * BMt * BN;
+    __shared__ __attribute__((aligned(1024))) bf16_t smem_flat[SMEM];
+    bf16_t(*smem)[SR * CBK] = reinterpret_cast<bf16_t(*)[SR * CBK]>(smem_flat);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
+    const int K = d.K;
+    if (d.prof_snap && (blockIdx.x | blockIdx.y | blockIdx.z) == 0 && tid == 0) {
+        d.prof_snap[0] = M;
+        d.prof_snap[1] = K;
+    }
+    TileJob job;
+    if (!map_tile<BMt>(d, M, d.nseg * gemm_kseg(d, K), job)) return;  // uniform for the whole workgroup
+    const int S = job.S;
+    const int kpad = (K + CBK - 1) / CBK * CBK;
+    const int kc = ((kpad + S - 1) / S + CBK - 1) / CBK * CBK;
+    const int kbeg = job.zt * kc;
+    const int kstop = min(kpad, kbeg + kc);
+    const int nk = kstop > kbeg ? (kstop - kbeg) / CBK : 0;
+
+    DmaRows<QA, NW> la;
+    DmaRows<QB, NW> lb;
+    la.init(d.lda, job.m0, M, lane, wave);
+    lb.init(d.ldb, job.n0, d.N, lane, wave);
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    constexpr int CPT = (NSEG == 3 ? 2 : 1) * QA + 2 * QB;  // copy instructions per tile and thread
+    auto copy_tile = [&](bf16_t* st, int t) {
+        const int kb = kbeg + t * CBK, ke = t < nk ? K : 0;
+        la.copy(d.A, kb, ke, st, wave);
+        if (NSEG == 3) la.copy(d.A2, kb, ke, st + BMt * CBK, wave);
+        lb.copy(d.B, kb, ke, st + 2 * BMt * CBK, wave);
+        lb.copy(d.B2, kb, ke, st + (2 * BMt + BN) * CBK, wave);
+    };
+    const int lrow = lane & 31, lc = lane >> 5;
+    auto frag = [&](const bf16_t* t, int row, int ks) {
+        const int C = 2 * ks + lc;
+        return *reinterpret_cast<const bf16x8_t*>(&t[row * CBK + 8 * (C ^ ((row >> 2) & 3))]);
+    };
+    auto compute = [&](const bf16_t* st) {
+#pragma unroll
+        for (int ks = 0; ks < CBK / 16; ++ks) {
+            bf16x8_t a[2], al[2], b[2], bl[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int row = wm * 64 + i * 32 + lrow;
+                a[i] = frag(st, row, ks);
+                if (NSEG == 3) al[i] = frag(st, BMt + row, ks);
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int row = wn * 64 + j * 32 + lrow;
+                b[j] = frag(st, 2 * BMt + row, ks);
+                bl[j] = frag(st, 2 * BMt + BN + row, ks);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bl[j], acc[i][j], 0, 0, 0);
+                    if (NSEG == 3)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], b[j], acc[i][j], 0, 0, 0);
+                }
+        }
+    };
+    auto step = [&](int t, int u) {
+        copy_tile(smem[(u + NST - 1) % NST], t + NST - 1);
+        compute(smem[u]);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));
+        __syncthreads();
+    };
+
+#pragma unroll
+    for (int u = 0; u < NST - 1; ++u) copy_tile(smem[u], u);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));  // tile 0 has landed
+    __syncthreads();
+    int t = 0;
+    for (; t + NST <= nk; t += NST) {
+#pragma unroll
+        for (int u = 0; u < NST; ++u) step(t + u, u);
+    }
+    for (int u = 0; t < nk; ++t, ++u) step(t, u);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    store_tile<BMt, NTt>(d, acc, reinterpret_cast<float*>(smem_flat), job, M, tid);
+}
+
 // Sums the split-K partials and runs the epilogue; four columns per thread
 // when N % 4 == 0, with the slices loaded four at a time.
 __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
@@ -1156,6 +1313,29 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
     prof_end_ext(h);
 }
 
+// (explicit instantiations: clang emits a host launch stub for each)
+template __global__ void gemm_dma_wide_kernel<3, 4, 3>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<2, 4, 3>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<3, 4, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<2, 4, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<3, 2, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<2, 2, 2>(const GemmDesc);
+
+template <int NSEG, int WM, int NST>
+void launch_wide(const GemmDesc& d, hipStream_t s) {
+    ProfInfo pi;
+    pi.kind = PROF_GEMM;
+    pi.M = d.M; pi.N = d.N; pi.K = d.K; pi.nseg = d.nseg;
+    pi.Mdev = d.Mdev; pi.Kdev = d.Kdev;
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext(NSEG == 3 ? "gemm_dma_wide_kernel<3>" : "gemm_dma_wide_kernel<2>", pi, &ea, &eb);
+    GemmDesc dd = d;
+    dd.prof_snap = prof_snap(h);
+    dim3 grid((d.N + BN - 1) / BN, (d.M + 64 * WM - 1) / (64 * WM), d.splits);
+    hipExtLaunchKernelGGL((gemm_dma_wide_kernel<NSEG, WM, NST>), grid, dim3(128 * WM), 0, s, ea, eb, 0, dd);
+    prof_end_ext(h);
+}
+
 template <int AM, int BMODE, bool AL = false>
 void launch(const GemmDesc& d, hipStream_t s) {
     // kernel names as the profilers print them
@@ -1185,6 +1365,8 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     FO_CHECK(d.splits >= 1 && (d.splits == 1 || d.ws != nullptr), "gemm: split-K needs a workspace");
     FO_CHECK(d.Cf || d.Cb, "gemm: no output");
     FO_CHECK(!d.colpart || d.splits == 1, "gemm: column sums need splits == 1");
+    FO_CHECK(!d.sgd_theta || (d.Cf && d.sgd_hi && d.sgd_lo && !d.defer_reduce),
+             "gemm: the fused SGD needs Cf, both bf16 parts and a reduction in this call");
     const bool conv = d.amode == OP_CONV_FWD || d.amode == OP_CONV_DX || d.bmode == OP_CONV_DXW ||
                       d.bmode == OP_CONV_DWX;
     if (conv) {
@@ -1203,7 +1385,8 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     {
         auto al = [](const void* p, uintptr_t m) { return p == nullptr || ((uintptr_t)p & (m - 1)) == 0; };
         bool v = d.N % 4 == 0 && al(d.ws, 16) && al(d.Cf, 16) && al(d.resid, 16) && al(d.Cb, 8) && al(d.Cb2, 8) &&
-                 al(d.dact_out, 8) && al(d.mask, 8) && al(d.dact, 8) && al(d.colpart, 4);
+                 al(d.dact_out, 8) && al(d.mask, 8) && al(d.dact, 8) && al(d.colpart, 4) && al(d.sgd_theta, 16) &&
+                 al(d.sgd_hi, 8) && al(d.sgd_lo, 8);
         if (d.Cf) v = v && d.ldcf % 4 == 0;
         if (d.resid) v = v && d.ldr % 4 == 0;
         if (d.Cb) v = v && d.ldcb % 4 == 0;
@@ -1227,7 +1410,13 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     const bool conv_comp = a == OP_CONV_FWD && b == OP_RK && d.nseg > 1 && !d.Kdev && d.g.Ci % 64 == 0 &&
                            al16(d.A) && al16(d.A2) && op_aligned(OP_RK, d.B, d.B2, d.ldb, d.N);
     // (two stages and two workgroups per CU beat deeper rings at one per CU)
-    if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
+    if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev && d.variant == 1 && !d.colpart)
+        d.nseg == 3 ? launch_wide<3, 4, 3>(dv, s) : launch_wide<2, 4, 3>(dv, s);
+    else if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev && d.variant == 2 && !d.colpart)
+        d.nseg == 3 ? launch_wide<3, 4, 2>(dv, s) : launch_wide<2, 4, 2>(dv, s);
+    else if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev && d.variant == 3)
+        d.nseg == 3 ? launch_wide<3, 2, 2>(dv, s) : launch_wide<2, 2, 2>(dv, s);
+    else if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
         d.nseg == 3 ? launch_comp<3>(dv, s) : launch_comp<2>(dv, s);
     else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(dv, s) : launch<OP_RK, OP_RK>(dv, s);
     else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KRT, true>(dv, s) : launch<OP_RK, OP_KR>(dv, s);

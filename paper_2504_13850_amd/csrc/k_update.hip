@@ -230,6 +230,35 @@ fo_status launch_sgd(float* p, const float* g, float* v, bf16_t* w16, bf16_t* w1
     return FO_OK;
 }
 
+// The same plain update (no momentum) restricted to a list of parameter ranges:
+// block b updates elements [chunks[2b], chunks[2b] + chunks[2b + 1]) with the
+// arithmetic of sgd_kernel; used for the parameters whose update is not fused
+// into their weight-gradient product.
+__global__ void __launch_bounds__(256) sgd_chunks_kernel(float* __restrict__ p, const float* __restrict__ g,
+                                                         bf16_t* __restrict__ w16, bf16_t* __restrict__ w16lo,
+                                                         const int64_t* __restrict__ chunks, float lr) {
+    const int64_t off = chunks[2 * blockIdx.x], len = chunks[2 * blockIdx.x + 1];
+    for (int64_t i = threadIdx.x; i < len; i += blockDim.x) {
+        const int64_t t = off + i;
+        const float a = __builtin_fmaf(-lr, g[t], p[t]);
+        p[t] = a;
+        if (w16) {
+            const bf16_t h = f2bf(a);
+            w16[t] = h;
+            w16lo[t] = f2bf(a - bf2f(h));
+        }
+    }
+}
+
+fo_status launch_sgd_chunks(float* p, const float* g, bf16_t* w16, bf16_t* w16lo, const int64_t* chunks,
+                            int nchunks, float lr, hipStream_t s) {
+    if (nchunks == 0) return FO_OK;
+    FO_CHECK(!w16 == !w16lo, "sgd: the bf16 shadow needs both parts");
+    hipLaunchKernelGGL(sgd_chunks_kernel, dim3(nchunks), dim3(256), 0, s, p, g, w16, w16lo, chunks, lr);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
 // fp32 -> (bf16 high part, bf16 low part) of the master weights.
 __global__ void cast_bf16_kernel(const float* __restrict__ x, bf16_t* __restrict__ y, bf16_t* __restrict__ ylo,
                                  int64_t n) {

@@ -20,6 +20,10 @@ fo_status launch_agg_lerp_multi(float* g, const AggTable& tab, int64_t n, hipStr
 // bf16 high/low shadows of theta when w16/w16lo are set.
 fo_status launch_sgd(float* p, const float* g, float* v, bf16_t* w16, bf16_t* w16lo, int64_t n, float lr, float mu,
                      hipStream_t s);
+// The same update on the ranges [chunks[2i], chunks[2i] + chunks[2i + 1]) (device
+// array, one block per range).
+fo_status launch_sgd_chunks(float* p, const float* g, bf16_t* w16, bf16_t* w16lo, const int64_t* chunks,
+                            int nchunks, float lr, hipStream_t s);
 // y = bf16(x), ylo = bf16(x - y) (ylo may be NULL)
 fo_status launch_cast_bf16(const float* x, bf16_t* y, bf16_t* ylo, int64_t n, hipStream_t s);
 

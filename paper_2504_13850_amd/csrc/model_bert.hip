@@ -52,6 +52,10 @@ struct Plan {
     float *splitws, *splitws2, *colws, *lnpart, *slws;
     int split_qkv, split_o, split_f1, split_f2;
     float *xc, *pooled, *dz, *dpool, *dxc;
+    // parameter ranges whose SGD update is not fused into a weight-gradient
+    // product (biases, norm parameters, pooler, classifier): device [n][2]
+    int64_t* sgd_chunks = nullptr;
+    int n_sgd_chunks = 0;
     hipStream_t side = nullptr;      // weight gradients of the backward
     hipEvent_t ev_fork = nullptr;    // main -> side: an operand is ready
     hipEvent_t ev_done[2] = {};      // side -> main: a parity's operands are free again
@@ -335,6 +339,31 @@ int split_rows(int K) {
     return s;
 }
 
+// The ranges of the flat parameter vector that the final SGD pass updates:
+// everything except the four weight matrices of each layer, whose update runs
+// in the epilogue of their weight-gradient products.  Ranges are cut into
+// chunks of at most 4096 (one block each).
+constexpr int kSgdChunk = 4096;
+constexpr int kMaxSgdChunks = 512;
+std::vector<int64_t> sgd_ranges(const LayerOff* off, int64_t pool_w) {
+    std::vector<int64_t> r;
+    auto add = [&](int64_t a, int64_t b) {
+        for (int64_t o = a; o < b; o += kSgdChunk) {
+            r.push_back(o);
+            r.push_back(std::min<int64_t>(kSgdChunk, b - o));
+        }
+    };
+    for (int l = 0; l < NL; ++l) {
+        const LayerOff& f = off[l];
+        add(f.bqkv, f.wo);  // bqkv
+        add(f.bo, f.w1);    // bo, ln1 gamma, beta
+        add(f.bf1, f.w2);   // bf1
+        add(f.bf2, l + 1 < NL ? off[l + 1].wqkv : pool_w);  // bf2, ln2 gamma, beta
+    }
+    add(pool_w, kParams);  // pooler and classifier
+    return r;
+}
+
 size_t ws_bytes(const fo_model* m) {
     const size_t R = (size_t)m->max_batch * L, B = (size_t)m->max_batch;
     size_t s = 0;
@@ -376,6 +405,7 @@ size_t ws_bytes(const fo_model* m) {
     add(4 * (size_t)cdiv(R, LNB_ROWS) * 3 * D);
     add(4 * small_linear_ws_floats((int)B, D, D));
     add(4 * B * D); add(4 * B * D); add(4 * B * NC); add(4 * B * D); add(4 * B * D);
+    add(16 * kMaxSgdChunks);
     return s;
 }
 
@@ -470,6 +500,17 @@ fo_status init(fo_model* m) {
     P->dz = a.take<float>(B * NC);
     P->dpool = a.take<float>(B * D);
     P->dxc = a.take<float>(B * D);
+    P->sgd_chunks = a.take<int64_t>(2 * kMaxSgdChunks);
+    if (!P->sgd_chunks) {
+        set_error("bert: workspace arena too small");
+        return FO_ENOMEM;
+    }
+    {
+        const std::vector<int64_t> r = sgd_ranges(P->off, P->pool_w);
+        P->n_sgd_chunks = (int)(r.size() / 2);
+        FO_CHECK(P->n_sgd_chunks <= kMaxSgdChunks, "bert: %d SGD ranges", P->n_sgd_chunks);
+        FO_HIP(hipMemcpy(P->sgd_chunks, r.data(), r.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+    }
     if (!P->dxc) {
         set_error("bert: workspace arena too small");
         return FO_ENOMEM;
@@ -619,11 +660,25 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     hipLaunchKernelGGL(scatter_cls_kernel, dim3(B), dim3(256), 0, s, P->dxc, P->cu, B, P->dY[0]);
     FO_LAUNCHED();
 
-    // Weight gradients go to the side stream as soon as their operands exist;
-    // the main stream carries the input-gradient chain.  Layer l's operands sit
+    // Weight gradients go to the side stream, each as soon as the input-gradient
+    // product that reads the same weight has been issued on the main stream:
+    // the weight-gradient product also applies the SGD update to its weight
+    // (fused epilogue), so it must not overwrite the weight before that read.
+    // The main stream carries the input-gradient chain.  Layer l's operands sit
     // in the parity l % 2 buffers, which layer l - 2 reuses only after the side
     // stream has finished with them.
     hipStream_t s2 = P->side;
+    const float lr = m->lr;
+    float* prmw = m->params;
+    bf16_t* w16 = m->w16;
+    bf16_t* w16lo = m->w16lo;
+    auto wgrad_sgd = [&](GemmDesc& w, int64_t off) {  // dW -> grads, theta -= lr dW, bf16 parts
+        w.Cf = grd + off;
+        w.sgd_theta = prmw + off;
+        w.sgd_hi = w16 + off;
+        w.sgd_lo = w16lo + off;
+        w.sgd_lr = lr;
+    };
     int cur = 0;
     SplitRows dy_rows = plain_rows(P->dY[0], rows);  // the LN2 backward's input: dY, or the deferred dX of the layer above
     for (int l = NL - 1; l >= 0; --l) {
@@ -635,16 +690,8 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         // LN2
         TRY(ln_bwd(P, dy_rows, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, du2b, grd + f.g2, grd + f.b2,
                    grd + f.bf2, s));
-        TRY(order_after(s2, s, P->ev_fork));
-        // FFN2: dG = du2 W2 (times GELU' of the FFN1 pre-activation -> dA1), dW2 = du2^T G, db2
+        // FFN2: dG = du2 W2 (times GELU' of the FFN1 pre-activation -> dA1), db2; then dW2 = du2^T G
         {
-            GemmDesc w;
-            w.M = D; w.N = FF; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = du2b; w.lda = D;
-            w.bmode = OP_KR; w.B = t.G; w.ldb = FF;
-            w.Cf = grd + f.w2; w.ldcf = FF;
-            w.splits = P->split_f2; w.ws = P->splitws2;
-            TRY(gemm(w, s2));
             GemmDesc d;
             d.M = rows; d.N = FF; d.K = D; d.Mdev = Tdev;
             d.amode = OP_RK; d.A = du2b; d.lda = D;
@@ -653,22 +700,22 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.Cb = dA1; d.ldcb = FF;
             d.colpart = P->colws;
             TRY(gemm(d, s));
+            TRY(order_after(s2, s, P->ev_fork));
+            GemmDesc w;
+            w.M = D; w.N = FF; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = du2b; w.lda = D;
+            w.bmode = OP_KR; w.B = t.G; w.ldb = FF;
+            wgrad_sgd(w, f.w2); w.ldcf = FF;
+            w.splits = P->split_f2; w.ws = P->splitws2;
+            TRY(gemm(w, s2));
             ColOut cb;
             cb.p[0] = grd + f.bf1;
             cb.seg = FF;
             TRY(launch_colsum_finish(P->colws, rows, Tdev, 128, FF, cb, s));
-            TRY(order_after(s2, s, P->ev_fork));
         }
         SplitRows dh_rows;
-        // FFN1: dH = du2 + dA1 W1, dW1 = dA1^T H, db1
+        // FFN1: dH = du2 + dA1 W1; then dW1 = dA1^T H
         {
-            GemmDesc w;
-            w.M = FF; w.N = D; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = dA1; w.lda = FF;
-            w.bmode = OP_KR; w.B = t.Hb; w.ldb = D;
-            w.Cf = grd + f.w1; w.ldcf = D;
-            w.splits = P->split_f1; w.ws = P->splitws2;
-            TRY(gemm(w, s2));
             GemmDesc d;
             d.M = rows; d.N = D; d.K = FF; d.Mdev = Tdev;
             d.amode = OP_RK; d.A = dA1; d.lda = FF;
@@ -679,20 +726,20 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.defer_reduce = true;  // summed by the LN1 backward
             TRY(gemm(d, s));
             dh_rows = deferred_rows(d);
+            TRY(order_after(s2, s, P->ev_fork));
+            GemmDesc w;
+            w.M = FF; w.N = D; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = dA1; w.lda = FF;
+            w.bmode = OP_KR; w.B = t.Hb; w.ldb = D;
+            wgrad_sgd(w, f.w1); w.ldcf = D;
+            w.splits = P->split_f1; w.ws = P->splitws2;
+            TRY(gemm(w, s2));
         }
         // LN1
         TRY(ln_bwd(P, dh_rows, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, du1b, grd + f.g1,
                    grd + f.b1, grd + f.bo, s));
-        TRY(order_after(s2, s, P->ev_fork));
-        // output projection: dO = du1 Wo, dWo = du1^T O, dbo
+        // output projection: dO = du1 Wo; then dWo = du1^T O
         {
-            GemmDesc w;
-            w.M = D; w.N = D; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = du1b; w.lda = D;
-            w.bmode = OP_KR; w.B = t.O; w.ldb = D;
-            w.Cf = grd + f.wo; w.ldcf = D;
-            w.splits = P->split_o; w.ws = P->splitws2;
-            TRY(gemm(w, s2));
             GemmDesc d;
             d.M = rows; d.N = D; d.K = D; d.Mdev = Tdev;
             d.amode = OP_RK; d.A = du1b; d.lda = D;
@@ -700,21 +747,18 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.Cb = P->dO; d.ldcb = D;
             d.splits = split_rows(D); d.ws = P->splitws;
             TRY(gemm(d, s));
+            TRY(order_after(s2, s, P->ev_fork));
+            GemmDesc w;
+            w.M = D; w.N = D; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = du1b; w.lda = D;
+            w.bmode = OP_KR; w.B = t.O; w.ldb = D;
+            wgrad_sgd(w, f.wo); w.ldcf = D;
+            w.splits = P->split_o; w.ws = P->splitws2;
+            TRY(gemm(w, s2));
         }
         TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, dqkv, B, NH, D, s));
-        TRY(order_after(s2, s, P->ev_fork));
-        // input projection: dWqkv on the side stream; dX = du1 + dqkv Wqkv (skipped
-        // for the first server layer) and dbqkv on the main stream
-        {
-            GemmDesc w;
-            w.M = 3 * D; w.N = D; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = dqkv; w.lda = 3 * D;
-            w.bmode = OP_KR; w.B = P->Xb[l]; w.ldb = D;
-            w.Cf = grd + f.wqkv; w.ldcf = D;
-            w.splits = P->split_qkv; w.ws = P->splitws2;
-            TRY(gemm(w, s2));
-            FO_HIP(hipEventRecord(P->ev_done[pb], s2));
-        }
+        // input projection: dX = du1 + dqkv Wqkv (skipped for the first server
+        // layer) and dbqkv on the main stream; then dWqkv on the side stream
         if (l > 0) {
             GemmDesc d;
             d.M = rows; d.N = D; d.K = 3 * D; d.Mdev = Tdev;
@@ -727,13 +771,25 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             TRY(gemm(d, s));
             dy_rows = deferred_rows(d);
         }
+        TRY(order_after(s2, s, P->ev_fork));
+        {
+            GemmDesc w;
+            w.M = 3 * D; w.N = D; w.K = rows; w.Kdev = Tdev;
+            w.amode = OP_KR; w.A = dqkv; w.lda = 3 * D;
+            w.bmode = OP_KR; w.B = P->Xb[l]; w.ldb = D;
+            wgrad_sgd(w, f.wqkv); w.ldcf = D;
+            w.splits = P->split_qkv; w.ws = P->splitws2;
+            TRY(gemm(w, s2));
+            FO_HIP(hipEventRecord(P->ev_done[pb], s2));
+        }
         TRY(launch_colsum(dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws, s));
         cur ^= 1;
     }
     FO_LAUNCHED();
     TRY(order_after(s, s2, P->ev_join));
-    // ---------------- SGD (Alg. 4: theta_s <- theta_s - gamma_s grad), refreshes the bf16 shadow
-    return launch_sgd(m->params, m->grads, nullptr, m->w16, m->w16lo, m->n_params, m->lr, 0.f, s);
+    // ---------------- SGD (Alg. 4: theta_s <- theta_s - gamma_s grad) of the
+    // parameters not updated by their weight-gradient product; refreshes the bf16 shadow
+    return launch_sgd_chunks(m->params, m->grads, m->w16, m->w16lo, P->sgd_chunks, P->n_sgd_chunks, m->lr, s);
 }
 
 void destroy(fo_model* m) {
