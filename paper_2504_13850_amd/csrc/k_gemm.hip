@@ -678,7 +678,7 @@ struct TileJob {
 // that XCD x owns a contiguous range, walked in groups of GM tile rows (M
 // fastest), which keeps the A row blocks and B column blocks it reads few and
 // shared.  Returns false when the workgroup has no tile.
-template <int BMt = BM>
+template <int BMt = BM, int BNt = BN>
 __device__ __forceinline__ bool map_tile(const GemmDesc& d, int M, int ktot_split, TileJob& job) {
     constexpr int GM = 8;
     const int S = active_splits(d, M, ktot_split);
@@ -694,7 +694,7 @@ __device__ __forceinline__ bool map_tile(const GemmDesc& d, int M, int ktot_spli
     const int gr = min(GM, nMe - g * GM);
     job.mt = g * GM + tg % gr;
     job.m0 = job.mt * BMt;
-    job.n0 = (tg / gr) * BN;
+    job.n0 = (tg / gr) * BNt;
     job.zt = zt;
     job.S = S;
     return true;
@@ -708,31 +708,33 @@ __device__ __forceinline__ bool map_tile(const GemmDesc& d, int M, int ktot_spli
 // whole product runs the epilogue (and the optional column sums).
 // BMt rows by NTt threads (4 waves of 64 x 64 per 128 rows); RP = NTt / 32 rows per
 // pass of the four-column path, HP = NTt / 128 row groups of the one-column path.
-template <int BMt = BM, int NTt = NT>
-__device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc)[2][2], float* Cs, const TileJob& job,
-                                           int M, int tid) {
-    constexpr int RP = NTt / 32, HP = NTt / 128;
+template <int BMt = BM, int NTt = NT, int BNt = BN, int WNF = 2>
+__device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc)[2][WNF], float* Cs,
+                                           const TileJob& job, int M, int tid) {
+    // TPR threads per row in the four-column path, RP rows per pass; HP row
+    // groups in the one-column path
+    constexpr int TPR = BNt / 4, RP = NTt / TPR, HP = NTt / BNt;
+    static_assert(BNt == 32 * 2 * WNF && HP >= 1, "tile shape");
     const int lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < WNF; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int lr = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                Cs[lr * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+                Cs[lr * BNt + wn * 32 * WNF + j * 32 + (lane & 31)] = acc[i][j][r];
             }
     __syncthreads();
     if (d.vec_epi) {
-        // four columns per thread (a wave covers two rows of 128): rows
-        // tid / 32 + 8 u, columns n0 + 4 (tid % 32) .. + 3
-        const int m0 = job.m0, c4 = (tid & 31) * 4, col = job.n0 + c4, rr = tid >> 5;
+        // four columns per thread: rows tid / TPR + RP u, columns n0 + 4 (tid % TPR) .. + 3
+        const int m0 = job.m0, c4 = (tid % TPR) * 4, col = job.n0 + c4, rr = tid / TPR;
         f32x4 csum = {0.f, 0.f, 0.f, 0.f};
         if (col < d.N) {
             if (job.S > 1) {
                 for (int lr = rr; lr < BMt && m0 + lr < M; lr += RP)
                     *reinterpret_cast<f32x4*>(d.ws + ((int64_t)job.zt * d.M + m0 + lr) * d.N + col) =
-                        *reinterpret_cast<const f32x4*>(&Cs[lr * BN + c4]);
+                        *reinterpret_cast<const f32x4*>(&Cs[lr * BNt + c4]);
             } else {
                 f32x4 bias = {0.f, 0.f, 0.f, 0.f};
                 if (d.bias) {
@@ -751,38 +753,38 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
                         const int lr = lr0 + RP * u, row = m0 + lr;
                         if (row < M)
                             csum += epi_store4(d, row, col,
-                                               *reinterpret_cast<const f32x4*>(&Cs[lr * BN + c4]) + bias + e[u].resid,
+                                               *reinterpret_cast<const f32x4*>(&Cs[lr * BNt + c4]) + bias + e[u].resid,
                                                e[u]);
                     }
                 }
             }
         }
-        if (d.colpart) {  // uniform; the eight row groups of a column meet in LDS
+        if (d.colpart) {  // uniform; the RP row groups of a column meet in LDS
             __syncthreads();
-            *reinterpret_cast<f32x4*>(&Cs[rr * BN + c4]) = csum;
+            *reinterpret_cast<f32x4*>(&Cs[rr * BNt + c4]) = csum;
             __syncthreads();
-            if (tid < BN && job.n0 + tid < d.N) {
+            if (tid < BNt && job.n0 + tid < d.N) {
                 float t = 0.f;
 #pragma unroll
-                for (int g = 0; g < RP; ++g) t += Cs[g * BN + tid];
+                for (int g = 0; g < RP; ++g) t += Cs[g * BNt + tid];
                 d.colpart[(int64_t)job.mt * d.N + job.n0 + tid] = t;
             }
         }
         return;
     }
-    const int m0 = job.m0, c = tid & (BN - 1), col = job.n0 + c;
+    const int m0 = job.m0, c = tid % BNt, col = job.n0 + c;
     float csum = 0.f;
     if (col < d.N) {
         if (job.S > 1) {
-            for (int lr = tid >> 7; lr < BMt; lr += HP) {
+            for (int lr = tid / BNt; lr < BMt; lr += HP) {
                 const int row = m0 + lr;
                 if (row >= M) break;
-                d.ws[((int64_t)job.zt * d.M + row) * d.N + col] = Cs[lr * BN + c];
+                d.ws[((int64_t)job.zt * d.M + row) * d.N + col] = Cs[lr * BNt + c];
             }
         } else {
             const float bcol = d.bias ? d.bias[col] : 0.f;
             // eight rows per batch: their operand loads are in flight together
-            for (int lr0 = tid >> 7; lr0 < BMt && m0 + lr0 < M; lr0 += 8 * HP) {
+            for (int lr0 = tid / BNt; lr0 < BMt && m0 + lr0 < M; lr0 += 8 * HP) {
                 EpiIn e[8];
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
@@ -792,19 +794,19 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
                     const int lr = lr0 + HP * u, row = m0 + lr;
-                    if (row < M) csum += epi_store(d, row, col, Cs[lr * BN + c] + bcol + e[u].resid, e[u]);
+                    if (row < M) csum += epi_store(d, row, col, Cs[lr * BNt + c] + bcol + e[u].resid, e[u]);
                 }
             }
         }
     }
     if (d.colpart) {  // uniform; the HP row groups of a column meet in LDS
         __syncthreads();
-        if (tid >= BN) Cs[(tid >> 7) * BN + c] = csum;
+        if (tid >= BNt) Cs[(tid / BNt) * BNt + c] = csum;
         __syncthreads();
-        if (tid < BN && col < d.N) {
+        if (tid < BNt && col < d.N) {
             float t = csum;
 #pragma unroll
-            for (int g = 1; g < HP; ++g) t += Cs[g * BN + c];
+            for (int g = 1; g < HP; ++g) t += Cs[g * BNt + c];
             d.colpart[(int64_t)job.mt * d.N + col] = t;
         }
     }
@@ -1145,15 +1147,15 @@ struct DmaRows {  // one operand tile; this wave's instructions are q = wave + N
     }
 };
 
-template <int NSEG, int WM, int NST>
+template <int NSEG, int WM, int WNF, int NST>
 __global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDesc d) {
-    constexpr int NW = 2 * WM, NTt = 64 * NW, BMt = 64 * WM;
-    constexpr int QA = BMt / 16 / NW, QB = BN / 16 / NW;
+    constexpr int NW = 2 * WM, NTt = 64 * NW, BMt = 64 * WM, BNt = 64 * WNF;
+    constexpr int QA = BMt / 16 / NW, QB = BNt / 16 / NW;
     static_assert(QA >= 1 && QB >= 1, "tile rows per wave");
-    // stage rows: A [0, BMt), A_lo [BMt, 2 BMt), B [2 BMt, 2 BMt + BN), B_lo after
-    constexpr int SR = 2 * BMt + 2 * BN;
+    // stage rows: A [0, BMt), A_lo [BMt, 2 BMt), B [2 BMt, 2 BMt + BNt), B_lo after
+    constexpr int SR = 2 * BMt + 2 * BNt;
     // the stages, reused for the C tile (BMt x BN fp32)
-    constexpr int SMEM = NST * SR * CBK > 2 * BMt * BN ? NST * SR * CBK : 2 * BMt * BN;
+    constexpr int SMEM = NST * SR * CBK > 2 * BMt * BNt ? NST * SR * CBK : 2 * BMt * BNt;
     __shared__ __attribute__((aligned(1024))) bf16_t smem_flat[SMEM];
     bf16_t(*smem)[SR * CBK] = reinterpret_cast<bf16_t(*)[SR * CBK]>(smem_flat);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1165,7 +1167,7 @@ __global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDe
         d.prof_snap[1] = K;
     }
     TileJob job;
-    if (!map_tile<BMt>(d, M, d.nseg * gemm_kseg(d, K), job)) return;  // uniform for the whole workgroup
+    if (!map_tile<BMt, BNt>(d, M, d.nseg * gemm_kseg(d, K), job)) return;  // uniform for the whole workgroup
     const int S = job.S;
     const int kpad = (K + CBK - 1) / CBK * CBK;
     const int kc = ((kpad + S - 1) / S + CBK - 1) / CBK * CBK;
@@ -1178,11 +1180,11 @@ __global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDe
     la.init(d.lda, job.m0, M, lane, wave);
     lb.init(d.ldb, job.n0, d.N, lane, wave);
 
-    f32x16 acc[2][2];
+    f32x16 acc[2][WNF];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < WNF; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
@@ -1192,7 +1194,7 @@ __global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDe
         la.copy(d.A, kb, ke, st, wave);
         if (NSEG == 3) la.copy(d.A2, kb, ke, st + BMt * CBK, wave);
         lb.copy(d.B, kb, ke, st + 2 * BMt * CBK, wave);
-        lb.copy(d.B2, kb, ke, st + (2 * BMt + BN) * CBK, wave);
+        lb.copy(d.B2, kb, ke, st + (2 * BMt + BNt) * CBK, wave);
     };
     const int lrow = lane & 31, lc = lane >> 5;
     auto frag = [&](const bf16_t* t, int row, int ks) {
@@ -1202,7 +1204,7 @@ __global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDe
     auto compute = [&](const bf16_t* st) {
 #pragma unroll
         for (int ks = 0; ks < CBK / 16; ++ks) {
-            bf16x8_t a[2], al[2], b[2], bl[2];
+            bf16x8_t a[2], al[2], b[WNF], bl[WNF];
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
                 const int row = wm * 64 + i * 32 + lrow;
@@ -1210,15 +1212,15 @@ __global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDe
                 if (NSEG == 3) al[i] = frag(st, BMt + row, ks);
             }
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int row = wn * 64 + j * 32 + lrow;
+            for (int j = 0; j < WNF; ++j) {
+                const int row = wn * 32 * WNF + j * 32 + lrow;
                 b[j] = frag(st, 2 * BMt + row, ks);
-                bl[j] = frag(st, 2 * BMt + BN + row, ks);
+                bl[j] = frag(st, 2 * BMt + BNt + row, ks);
             }
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
+                for (int j = 0; j < WNF; ++j) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bl[j], acc[i][j], 0, 0, 0);
                     if (NSEG == 3)
@@ -1245,7 +1247,7 @@ __global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDe
     for (int u = 0; t < nk; ++t, ++u) step(t, u);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    store_tile<BMt, NTt>(d, acc, reinterpret_cast<float*>(smem_flat), job, M, tid);
+    store_tile<BMt, NTt, BNt, WNF>(d, acc, reinterpret_cast<float*>(smem_flat), job, M, tid);
 }
 
 // Sums the split-K partials and runs the epilogue; four columns per thread
@@ -1314,14 +1316,18 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
 }
 
 // (explicit instantiations: clang emits a host launch stub for each)
-template __global__ void gemm_dma_wide_kernel<3, 4, 3>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<2, 4, 3>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<3, 4, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<2, 4, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<3, 2, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<2, 2, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<3, 4, 2, 3>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<3, 4, 2, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<3, 2, 2, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<3, 2, 4, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<3, 2, 4, 3>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<2, 4, 2, 3>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<2, 4, 2, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<2, 2, 2, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<2, 2, 4, 2>(const GemmDesc);
+template __global__ void gemm_dma_wide_kernel<2, 2, 4, 3>(const GemmDesc);
 
-template <int NSEG, int WM, int NST>
+template <int NSEG, int WM, int WNF, int NST>
 void launch_wide(const GemmDesc& d, hipStream_t s) {
     ProfInfo pi;
     pi.kind = PROF_GEMM;
@@ -1331,8 +1337,8 @@ void launch_wide(const GemmDesc& d, hipStream_t s) {
     const int h = prof_begin_ext(NSEG == 3 ? "gemm_dma_wide_kernel<3>" : "gemm_dma_wide_kernel<2>", pi, &ea, &eb);
     GemmDesc dd = d;
     dd.prof_snap = prof_snap(h);
-    dim3 grid((d.N + BN - 1) / BN, (d.M + 64 * WM - 1) / (64 * WM), d.splits);
-    hipExtLaunchKernelGGL((gemm_dma_wide_kernel<NSEG, WM, NST>), grid, dim3(128 * WM), 0, s, ea, eb, 0, dd);
+    dim3 grid((d.N + 64 * WNF - 1) / (64 * WNF), (d.M + 64 * WM - 1) / (64 * WM), d.splits);
+    hipExtLaunchKernelGGL((gemm_dma_wide_kernel<NSEG, WM, WNF, NST>), grid, dim3(128 * WM), 0, s, ea, eb, 0, dd);
     prof_end_ext(h);
 }
 
@@ -1410,12 +1416,17 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     const bool conv_comp = a == OP_CONV_FWD && b == OP_RK && d.nseg > 1 && !d.Kdev && d.g.Ci % 64 == 0 &&
                            al16(d.A) && al16(d.A2) && op_aligned(OP_RK, d.B, d.B2, d.ldb, d.N);
     // (two stages and two workgroups per CU beat deeper rings at one per CU)
-    if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev && d.variant == 1 && !d.colpart)
-        d.nseg == 3 ? launch_wide<3, 4, 3>(dv, s) : launch_wide<2, 4, 3>(dv, s);
-    else if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev && d.variant == 2 && !d.colpart)
-        d.nseg == 3 ? launch_wide<3, 4, 2>(dv, s) : launch_wide<2, 4, 2>(dv, s);
-    else if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev && d.variant == 3)
-        d.nseg == 3 ? launch_wide<3, 2, 2>(dv, s) : launch_wide<2, 2, 2>(dv, s);
+    const bool comp_rk = a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev;
+    if (comp_rk && d.variant == 1 && !d.colpart)
+        d.nseg == 3 ? launch_wide<3, 4, 2, 3>(dv, s) : launch_wide<2, 4, 2, 3>(dv, s);
+    else if (comp_rk && d.variant == 2 && !d.colpart)
+        d.nseg == 3 ? launch_wide<3, 4, 2, 2>(dv, s) : launch_wide<2, 4, 2, 2>(dv, s);
+    else if (comp_rk && d.variant == 3)
+        d.nseg == 3 ? launch_wide<3, 2, 2, 2>(dv, s) : launch_wide<2, 2, 2, 2>(dv, s);
+    else if (comp_rk && d.variant == 4 && !d.colpart)
+        d.nseg == 3 ? launch_wide<3, 2, 4, 2>(dv, s) : launch_wide<2, 2, 4, 2>(dv, s);
+    else if (comp_rk && d.variant == 5 && !d.colpart)
+        d.nseg == 3 ? launch_wide<3, 2, 4, 3>(dv, s) : launch_wide<2, 2, 4, 3>(dv, s);
     else if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
         d.nseg == 3 ? launch_comp<3>(dv, s) : launch_comp<2>(dv, s);
     else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(dv, s) : launch<OP_RK, OP_RK>(dv, s);

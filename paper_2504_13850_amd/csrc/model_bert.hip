@@ -49,7 +49,11 @@ struct Plan {
     // of layer l run on the side stream while the main stream goes on to l - 1
     bf16_t *du2b[2], *dA1[2], *du1b[2], *dqkv[2];
     bf16_t* dO;
-    float *splitws, *splitws2, *colws, *lnpart, *slws;
+    float *splitws, *splitws2, *slws;
+    // column-sum partials per layer parity, finished on the side stream: the FFN1
+    // bias gradient (colwsF), the two norms' dgamma / dbeta / bias gradient
+    // (lnpart[parity][0] LN2, [1] LN1); colws2: the side stream's own (bqkv)
+    float *colwsF[2], *lnpart[2][2], *colws2;
     int split_qkv, split_o, split_f1, split_f2;
     float *xc, *pooled, *dz, *dpool, *dxc;
     // parameter ranges whose SGD update is not fused into a weight-gradient
@@ -401,8 +405,9 @@ size_t ws_bytes(const fo_model* m) {
     sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
     add(sw);
     add(sw);  // the side stream's split-K partials
-    add(4 * colsum_ws_floats((int)R, FF));
-    add(4 * (size_t)cdiv(R, LNB_ROWS) * 3 * D);
+    for (int q = 0; q < 2; ++q) add(4 * colsum_ws_floats((int)R, FF));
+    add(4 * colsum_ws_floats((int)R, 3 * D));
+    for (int q = 0; q < 4; ++q) add(4 * (size_t)cdiv(R, LNB_ROWS) * 3 * D);
     add(4 * small_linear_ws_floats((int)B, D, D));
     add(4 * B * D); add(4 * B * D); add(4 * B * NC); add(4 * B * D); add(4 * B * D);
     add(16 * kMaxSgdChunks);
@@ -492,8 +497,9 @@ fo_status init(fo_model* m) {
     sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
     P->splitws = a.take<float>(sw / 4 + 1);
     P->splitws2 = a.take<float>(sw / 4 + 1);
-    P->colws = a.take<float>(colsum_ws_floats((int)R, FF));
-    P->lnpart = a.take<float>((size_t)cdiv(R, LNB_ROWS) * 3 * D);
+    for (int q = 0; q < 2; ++q) P->colwsF[q] = a.take<float>(colsum_ws_floats((int)R, FF));
+    P->colws2 = a.take<float>(colsum_ws_floats((int)R, 3 * D));
+    for (int q = 0; q < 4; ++q) P->lnpart[q / 2][q % 2] = a.take<float>((size_t)cdiv(R, LNB_ROWS) * 3 * D);
     P->slws = a.take<float>(small_linear_ws_floats((int)B, D, D));
     P->xc = a.take<float>(B * D);
     P->pooled = a.take<float>(B * D);
@@ -571,18 +577,22 @@ SplitRows plain_rows(const float* x, int M) {
     return r;
 }
 
-fo_status ln_bwd(const Plan* P, const SplitRows& dy, const float* u, const float* mean, const float* rstd,
-                 const float* gamma, const int* Tdev, int rows, float* dxf, bf16_t* dxb, float* dg, float* db,
-                 float* dbias_below, hipStream_t s) {
+fo_status ln_bwd(const SplitRows& dy, const float* u, const float* mean, const float* rstd, const float* gamma,
+                 const int* Tdev, int rows, float* dxf, bf16_t* dxb, float* part, hipStream_t s) {
     hipLaunchKernelGGL(ln_bwd_kernel, dim3(cdiv(rows, LNB_ROWS)), dim3(256), 0, s, dy, u, mean, rstd, gamma, Tdev,
-                       dxf, dxb, P->lnpart);
+                       dxf, dxb, part);
     FO_LAUNCHED();
+    return FO_OK;
+}
+// dgamma, dbeta and the bias gradient of the sublayer below from ln_bwd's partials
+fo_status ln_bwd_finish(const float* part, const int* Tdev, int rows, float* dg, float* db, float* dbias_below,
+                        hipStream_t s) {
     ColOut o;
     o.p[0] = dg;
     o.p[1] = db;
     o.p[2] = dbias_below;
     o.seg = D;
-    return launch_colsum_finish(P->lnpart, rows, Tdev, LNB_ROWS, 3 * D, o, s);
+    return launch_colsum_finish(part, rows, Tdev, LNB_ROWS, 3 * D, o, s);
 }
 
 fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
@@ -660,24 +670,32 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     hipLaunchKernelGGL(scatter_cls_kernel, dim3(B), dim3(256), 0, s, P->dxc, P->cu, B, P->dY[0]);
     FO_LAUNCHED();
 
-    // Weight gradients go to the side stream, each as soon as the input-gradient
-    // product that reads the same weight has been issued on the main stream:
-    // the weight-gradient product also applies the SGD update to its weight
-    // (fused epilogue), so it must not overwrite the weight before that read.
-    // The main stream carries the input-gradient chain.  Layer l's operands sit
-    // in the parity l % 2 buffers, which layer l - 2 reuses only after the side
-    // stream has finished with them.
+    // Weight gradients: the four products of layer l go to the side stream
+    // together, after the main stream has issued layer l's input-gradient chain
+    // (each weight-gradient product also applies the SGD update to its weight in
+    // its epilogue, so it must follow the input-gradient product that reads that
+    // weight).  They run while the main stream carries on with layer l - 1.  One
+    // fork and one wait per layer: every cross-stream edge of a captured graph
+    // costs several microseconds of idle GPU.  Layer l's operands sit in the
+    // parity l % 2 buffers, which layer l - 2 reuses only after the side stream
+    // has finished with them.
     hipStream_t s2 = P->side;
     const float lr = m->lr;
     float* prmw = m->params;
     bf16_t* w16 = m->w16;
     bf16_t* w16lo = m->w16lo;
-    auto wgrad_sgd = [&](GemmDesc& w, int64_t off) {  // dW -> grads, theta -= lr dW, bf16 parts
-        w.Cf = grd + off;
+    auto wgrad = [&](int M_, int N_, const bf16_t* A_, const bf16_t* B_, int64_t off, int splits) {
+        GemmDesc w;  // dW = A^T B over the packed rows -> grads; theta -= lr dW; bf16 parts
+        w.M = M_; w.N = N_; w.K = rows; w.Kdev = Tdev;
+        w.amode = OP_KR; w.A = A_; w.lda = M_;
+        w.bmode = OP_KR; w.B = B_; w.ldb = N_;
+        w.Cf = grd + off; w.ldcf = N_;
         w.sgd_theta = prmw + off;
         w.sgd_hi = w16 + off;
         w.sgd_lo = w16lo + off;
         w.sgd_lr = lr;
+        w.splits = splits; w.ws = P->splitws2;
+        return gemm(w, s2);
     };
     int cur = 0;
     SplitRows dy_rows = plain_rows(P->dY[0], rows);  // the LN2 backward's input: dY, or the deferred dX of the layer above
@@ -688,9 +706,8 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         bf16_t *du2b = P->du2b[pb], *dA1 = P->dA1[pb], *du1b = P->du1b[pb], *dqkv = P->dqkv[pb];
         if (l + 2 < NL) FO_HIP(hipStreamWaitEvent(s, P->ev_done[pb], 0));
         // LN2
-        TRY(ln_bwd(P, dy_rows, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, du2b, grd + f.g2, grd + f.b2,
-                   grd + f.bf2, s));
-        // FFN2: dG = du2 W2 (times GELU' of the FFN1 pre-activation -> dA1), db2; then dW2 = du2^T G
+        TRY(ln_bwd(dy_rows, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, du2b, P->lnpart[pb][0], s));
+        // FFN2: dG = du2 W2, times GELU' of the FFN1 pre-activation -> dA1; db1
         {
             GemmDesc d;
             d.M = rows; d.N = FF; d.K = D; d.Mdev = Tdev;
@@ -698,23 +715,11 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.bmode = OP_KR; d.B = W + f.w2; d.ldb = FF;
             d.dact = t.dgelu1; d.ldm = FF;
             d.Cb = dA1; d.ldcb = FF;
-            d.colpart = P->colws;
+            d.colpart = P->colwsF[pb];
             TRY(gemm(d, s));
-            TRY(order_after(s2, s, P->ev_fork));
-            GemmDesc w;
-            w.M = D; w.N = FF; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = du2b; w.lda = D;
-            w.bmode = OP_KR; w.B = t.G; w.ldb = FF;
-            wgrad_sgd(w, f.w2); w.ldcf = FF;
-            w.splits = P->split_f2; w.ws = P->splitws2;
-            TRY(gemm(w, s2));
-            ColOut cb;
-            cb.p[0] = grd + f.bf1;
-            cb.seg = FF;
-            TRY(launch_colsum_finish(P->colws, rows, Tdev, 128, FF, cb, s));
         }
         SplitRows dh_rows;
-        // FFN1: dH = du2 + dA1 W1; then dW1 = dA1^T H
+        // FFN1: dH = du2 + dA1 W1
         {
             GemmDesc d;
             d.M = rows; d.N = D; d.K = FF; d.Mdev = Tdev;
@@ -726,19 +731,10 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.defer_reduce = true;  // summed by the LN1 backward
             TRY(gemm(d, s));
             dh_rows = deferred_rows(d);
-            TRY(order_after(s2, s, P->ev_fork));
-            GemmDesc w;
-            w.M = FF; w.N = D; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = dA1; w.lda = FF;
-            w.bmode = OP_KR; w.B = t.Hb; w.ldb = D;
-            wgrad_sgd(w, f.w1); w.ldcf = D;
-            w.splits = P->split_f1; w.ws = P->splitws2;
-            TRY(gemm(w, s2));
         }
         // LN1
-        TRY(ln_bwd(P, dh_rows, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, du1b, grd + f.g1,
-                   grd + f.b1, grd + f.bo, s));
-        // output projection: dO = du1 Wo; then dWo = du1^T O
+        TRY(ln_bwd(dh_rows, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, du1b, P->lnpart[pb][1], s));
+        // output projection: dO = du1 Wo
         {
             GemmDesc d;
             d.M = rows; d.N = D; d.K = D; d.Mdev = Tdev;
@@ -747,18 +743,9 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.Cb = P->dO; d.ldcb = D;
             d.splits = split_rows(D); d.ws = P->splitws;
             TRY(gemm(d, s));
-            TRY(order_after(s2, s, P->ev_fork));
-            GemmDesc w;
-            w.M = D; w.N = D; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = du1b; w.lda = D;
-            w.bmode = OP_KR; w.B = t.O; w.ldb = D;
-            wgrad_sgd(w, f.wo); w.ldcf = D;
-            w.splits = P->split_o; w.ws = P->splitws2;
-            TRY(gemm(w, s2));
         }
         TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, dqkv, B, NH, D, s));
-        // input projection: dX = du1 + dqkv Wqkv (skipped for the first server
-        // layer) and dbqkv on the main stream; then dWqkv on the side stream
+        // input projection: dX = du1 + dqkv Wqkv (skipped for the first server layer), dbqkv
         if (l > 0) {
             GemmDesc d;
             d.M = rows; d.N = D; d.K = 3 * D; d.Mdev = Tdev;
@@ -771,18 +758,24 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             TRY(gemm(d, s));
             dy_rows = deferred_rows(d);
         }
+        // the layer's parameter gradients off the input-gradient chain: bias and
+        // norm gradients from their partials, then the weight gradients with
+        // their SGD updates
         TRY(order_after(s2, s, P->ev_fork));
+        TRY(ln_bwd_finish(P->lnpart[pb][0], Tdev, rows, grd + f.g2, grd + f.b2, grd + f.bf2, s2));
         {
-            GemmDesc w;
-            w.M = 3 * D; w.N = D; w.K = rows; w.Kdev = Tdev;
-            w.amode = OP_KR; w.A = dqkv; w.lda = 3 * D;
-            w.bmode = OP_KR; w.B = P->Xb[l]; w.ldb = D;
-            wgrad_sgd(w, f.wqkv); w.ldcf = D;
-            w.splits = P->split_qkv; w.ws = P->splitws2;
-            TRY(gemm(w, s2));
-            FO_HIP(hipEventRecord(P->ev_done[pb], s2));
+            ColOut cb;
+            cb.p[0] = grd + f.bf1;
+            cb.seg = FF;
+            TRY(launch_colsum_finish(P->colwsF[pb], rows, Tdev, 128, FF, cb, s2));
         }
-        TRY(launch_colsum(dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws, s));
+        TRY(ln_bwd_finish(P->lnpart[pb][1], Tdev, rows, grd + f.g1, grd + f.b1, grd + f.bo, s2));
+        TRY(launch_colsum(dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws2, s2));
+        TRY(wgrad(D, FF, du2b, t.G, f.w2, P->split_f2));              // dW2 = du2^T G
+        TRY(wgrad(FF, D, dA1, t.Hb, f.w1, P->split_f1));              // dW1 = dA1^T H
+        TRY(wgrad(D, D, du1b, t.O, f.wo, P->split_o));                // dWo = du1^T O
+        TRY(wgrad(3 * D, D, dqkv, P->Xb[l], f.wqkv, P->split_qkv));  // dWqkv = dqkv^T X
+        FO_HIP(hipEventRecord(P->ev_done[pb], s2));
         cur ^= 1;
     }
     FO_LAUNCHED();
