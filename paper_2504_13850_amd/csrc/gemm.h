@@ -85,7 +85,6 @@ struct GemmDesc {
     const int* Kdev = nullptr;
     int* prof_snap = nullptr;  // set by the launcher when profiling: receives (M, K) effective
     int vec_epi = 0;           // set by the launcher: the epilogue may move four columns per access
-    int variant = 0;           // kernel variant override (0: the launcher's choice)
     // With split-K: leave the partials in ws and skip the reduction pass; the
     // consumer sums them (see SplitRows).  A launch that runs unsplit (one
     // active slice) still applies its epilogue and writes Cf.

@@ -1016,6 +1016,22 @@ struct DmaConvA {
 // s_waitcnt immediate that waits for at most n vector memory operations in
 // flight and does not wait on LDS / scalar memory or exports.
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+// The same, and no LDS operation in flight (lgkmcnt(0)): the wait that closes a
+// ring step, after which no wave may still be reading the stage the next copy
+// overwrites.
+constexpr int vmcnt_lds0_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
+
+// Workgroup barrier without the release / acquire fences of __syncthreads:
+// with copies into LDS in flight the compiler turns those fences into a wait
+// for every outstanding copy (vmcnt(0)) before the barrier, which collapses a
+// ring of stages to a single one.  The callers wait explicitly for the copies
+// the next step reads; the wavefront-scope fences only keep the compiler from
+// moving memory operations across the barrier.
+__device__ __forceinline__ void ring_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 // NST stages in a ring: the copy of tile t + NST - 1 is issued before the MFMAs
 // of tile t.  Every copy is issued, also past the slice's last tile (those read
@@ -1101,14 +1117,14 @@ __global__ void __launch_bounds__(NT, NST == 2 ? 2 : 1) gemm_comp_dma_kernel(con
     auto step = [&](int t, int u) {
         copy_tile(smem[(u + NST - 1) % NST], t + NST - 1);
         compute(smem[u]);
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));
-        __syncthreads();
+        __builtin_amdgcn_s_waitcnt(vmcnt_lds0_imm(CPT * (NST - 2)));
+        ring_barrier();
     };
 
 #pragma unroll
     for (int u = 0; u < NST - 1; ++u) copy_tile(smem[u], u);
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));  // tile 0 has landed
-    __syncthreads();
+    ring_barrier();
     int t = 0;
     for (; t + NST <= nk; t += NST) {  // whole rounds: static stage indices
 #pragma unroll
@@ -1118,136 +1134,6 @@ __global__ void __launch_bounds__(NT, NST == 2 ? 2 : 1) gemm_comp_dma_kernel(con
     __builtin_amdgcn_s_waitcnt(0);  // copies past the last tile
     __syncthreads();
     store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
-}
-
-// The same single-pass product on 64*WM x 128 tiles: 2*WM waves of 64 x 64
-// (WM along M, two along N), NST stages of the A, A_lo, B and B_lo row tiles
-// (64 bytes per row, layout as DmaRKc) and one workgroup per CU.  With WM = 4
-// and three stages (144 KB of LDS) each copy is issued two K tiles before it is
-// read, twice the distance of the two-stage 128 x 128 form, and every K tile
-// moves 48 KB for twice the MFMA work of a 32 KB tile of that form.
-template <int NQ, int NW>
-struct DmaRows {  // one operand tile; this wave's instructions are q = wave + NW v (16 rows each)
-    int64_t off[NQ];
-    int koff;
-    __device__ void init(int64_t ld, int r0, int R, int lane, int wave) {
-        koff = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
-#pragma unroll
-        for (int v = 0; v < NQ; ++v) {
-            const int gr = r0 + 16 * (wave + NW * v) + (lane >> 2);
-            off[v] = gr < R ? (int64_t)gr * ld : -1;
-        }
-    }
-    __device__ void copy(const bf16_t* P, int kb, int kend, bf16_t* tile, int wave) const {
-        const int k = kb + koff;
-#pragma unroll
-        for (int v = 0; v < NQ; ++v)
-            __builtin_amdgcn_global_load_lds(off[v] >= 0 && k < kend ? P + off[v] + k : kZero8,
-                                             FO_LDS(tile + (wave + NW * v) * 512), 16, 0, 0);
-    }
-};
-
-template <int NSEG, int WM, int WNF, int NST>
-__global__ void __launch_bounds__(128 * WM, 1) gemm_dma_wide_kernel(const GemmDesc d) {
-    constexpr int NW = 2 * WM, NTt = 64 * NW, BMt = 64 * WM, BNt = 64 * WNF;
-    constexpr int QA = BMt / 16 / NW, QB = BNt / 16 / NW;
-    static_assert(QA >= 1 && QB >= 1, "tile rows per wave");
-    // stage rows: A [0, BMt), A_lo [BMt, 2 BMt), B [2 BMt, 2 BMt + BNt), B_lo after
-    constexpr int SR = 2 * BMt + 2 * BNt;
-    // the stages, reused for the C tile (BMt x BN fp32)
-    constexpr int SMEM = NST * SR * CBK > 2 * BMt * BNt ? NST * SR * CBK : 2 * BMt * BNt;
-    __shared__ __attribute__((aligned(1024))) bf16_t smem_flat[SMEM];
-    bf16_t(*smem)[SR * CBK] = reinterpret_cast<bf16_t(*)[SR * CBK]>(smem_flat);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
-    const int K = d.K;
-    if (d.prof_snap && (blockIdx.x | blockIdx.y | blockIdx.z) == 0 && tid == 0) {
-        d.prof_snap[0] = M;
-        d.prof_snap[1] = K;
-    }
-    TileJob job;
-    if (!map_tile<BMt, BNt>(d, M, d.nseg * gemm_kseg(d, K), job)) return;  // uniform for the whole workgroup
-    const int S = job.S;
-    const int kpad = (K + CBK - 1) / CBK * CBK;
-    const int kc = ((kpad + S - 1) / S + CBK - 1) / CBK * CBK;
-    const int kbeg = job.zt * kc;
-    const int kstop = min(kpad, kbeg + kc);
-    const int nk = kstop > kbeg ? (kstop - kbeg) / CBK : 0;
-
-    DmaRows<QA, NW> la;
-    DmaRows<QB, NW> lb;
-    la.init(d.lda, job.m0, M, lane, wave);
-    lb.init(d.ldb, job.n0, d.N, lane, wave);
-
-    f32x16 acc[2][WNF];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < WNF; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    constexpr int CPT = (NSEG == 3 ? 2 : 1) * QA + 2 * QB;  // copy instructions per tile and thread
-    auto copy_tile = [&](bf16_t* st, int t) {
-        const int kb = kbeg + t * CBK, ke = t < nk ? K : 0;
-        la.copy(d.A, kb, ke, st, wave);
-        if (NSEG == 3) la.copy(d.A2, kb, ke, st + BMt * CBK, wave);
-        lb.copy(d.B, kb, ke, st + 2 * BMt * CBK, wave);
-        lb.copy(d.B2, kb, ke, st + (2 * BMt + BNt) * CBK, wave);
-    };
-    const int lrow = lane & 31, lc = lane >> 5;
-    auto frag = [&](const bf16_t* t, int row, int ks) {
-        const int C = 2 * ks + lc;
-        return *reinterpret_cast<const bf16x8_t*>(&t[row * CBK + 8 * (C ^ ((row >> 2) & 3))]);
-    };
-    auto compute = [&](const bf16_t* st) {
-#pragma unroll
-        for (int ks = 0; ks < CBK / 16; ++ks) {
-            bf16x8_t a[2], al[2], b[WNF], bl[WNF];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int row = wm * 64 + i * 32 + lrow;
-                a[i] = frag(st, row, ks);
-                if (NSEG == 3) al[i] = frag(st, BMt + row, ks);
-            }
-#pragma unroll
-            for (int j = 0; j < WNF; ++j) {
-                const int row = wn * 32 * WNF + j * 32 + lrow;
-                b[j] = frag(st, 2 * BMt + row, ks);
-                bl[j] = frag(st, 2 * BMt + BNt + row, ks);
-            }
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < WNF; ++j) {
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bl[j], acc[i][j], 0, 0, 0);
-                    if (NSEG == 3)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], b[j], acc[i][j], 0, 0, 0);
-                }
-        }
-    };
-    auto step = [&](int t, int u) {
-        copy_tile(smem[(u + NST - 1) % NST], t + NST - 1);
-        compute(smem[u]);
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));
-        __syncthreads();
-    };
-
-#pragma unroll
-    for (int u = 0; u < NST - 1; ++u) copy_tile(smem[u], u);
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));  // tile 0 has landed
-    __syncthreads();
-    int t = 0;
-    for (; t + NST <= nk; t += NST) {
-#pragma unroll
-        for (int u = 0; u < NST; ++u) step(t + u, u);
-    }
-    for (int u = 0; t < nk; ++t, ++u) step(t, u);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    store_tile<BMt, NTt, BNt, WNF>(d, acc, reinterpret_cast<float*>(smem_flat), job, M, tid);
 }
 
 // Sums the split-K partials and runs the epilogue; four columns per thread
@@ -1312,33 +1198,6 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
     dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
     hipExtLaunchKernelGGL((gemm_comp_dma_kernel<NSEG, NST, LA>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
-    prof_end_ext(h);
-}
-
-// (explicit instantiations: clang emits a host launch stub for each)
-template __global__ void gemm_dma_wide_kernel<3, 4, 2, 3>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<3, 4, 2, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<3, 2, 2, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<3, 2, 4, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<3, 2, 4, 3>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<2, 4, 2, 3>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<2, 4, 2, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<2, 2, 2, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<2, 2, 4, 2>(const GemmDesc);
-template __global__ void gemm_dma_wide_kernel<2, 2, 4, 3>(const GemmDesc);
-
-template <int NSEG, int WM, int WNF, int NST>
-void launch_wide(const GemmDesc& d, hipStream_t s) {
-    ProfInfo pi;
-    pi.kind = PROF_GEMM;
-    pi.M = d.M; pi.N = d.N; pi.K = d.K; pi.nseg = d.nseg;
-    pi.Mdev = d.Mdev; pi.Kdev = d.Kdev;
-    hipEvent_t ea, eb;
-    const int h = prof_begin_ext(NSEG == 3 ? "gemm_dma_wide_kernel<3>" : "gemm_dma_wide_kernel<2>", pi, &ea, &eb);
-    GemmDesc dd = d;
-    dd.prof_snap = prof_snap(h);
-    dim3 grid((d.N + 64 * WNF - 1) / (64 * WNF), (d.M + 64 * WM - 1) / (64 * WM), d.splits);
-    hipExtLaunchKernelGGL((gemm_dma_wide_kernel<NSEG, WM, WNF, NST>), grid, dim3(128 * WM), 0, s, ea, eb, 0, dd);
     prof_end_ext(h);
 }
 
@@ -1415,19 +1274,9 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     // 16-byte aligned input and weights, Ci % 64 == 0, static sizes
     const bool conv_comp = a == OP_CONV_FWD && b == OP_RK && d.nseg > 1 && !d.Kdev && d.g.Ci % 64 == 0 &&
                            al16(d.A) && al16(d.A2) && op_aligned(OP_RK, d.B, d.B2, d.ldb, d.N);
-    // (two stages and two workgroups per CU beat deeper rings at one per CU)
-    const bool comp_rk = a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev;
-    if (comp_rk && d.variant == 1 && !d.colpart)
-        d.nseg == 3 ? launch_wide<3, 4, 2, 3>(dv, s) : launch_wide<2, 4, 2, 3>(dv, s);
-    else if (comp_rk && d.variant == 2 && !d.colpart)
-        d.nseg == 3 ? launch_wide<3, 4, 2, 2>(dv, s) : launch_wide<2, 4, 2, 2>(dv, s);
-    else if (comp_rk && d.variant == 3)
-        d.nseg == 3 ? launch_wide<3, 2, 2, 2>(dv, s) : launch_wide<2, 2, 2, 2>(dv, s);
-    else if (comp_rk && d.variant == 4 && !d.colpart)
-        d.nseg == 3 ? launch_wide<3, 2, 4, 2>(dv, s) : launch_wide<2, 2, 4, 2>(dv, s);
-    else if (comp_rk && d.variant == 5 && !d.colpart)
-        d.nseg == 3 ? launch_wide<3, 2, 4, 3>(dv, s) : launch_wide<2, 2, 4, 3>(dv, s);
-    else if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
+    // (two stages and two workgroups per CU beat deeper rings at one per CU, and
+    // 256 x 128 tiles with a three-stage ring at one per CU on these products)
+    if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
         d.nseg == 3 ? launch_comp<3>(dv, s) : launch_comp<2>(dv, s);
     else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(dv, s) : launch<OP_RK, OP_RK>(dv, s);
     else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KRT, true>(dv, s) : launch<OP_RK, OP_KR>(dv, s);

@@ -627,7 +627,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         TRY(launch_attn_fwd(t.qkv, t.qkvlo, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
         GemmDesc o = lin_fwd(rows, t.O, t.Olo, D, W + f.wo, Wl + f.wo, D);
         o.Mdev = Tdev;
-        o.splits = split_rows(3 * D); o.ws = P->splitws;
+        o.splits = 2; o.ws = P->splitws;  // (two slices time like four and halve the LayerNorm's reads)
         o.bias = prm + f.bo;
         o.resid = P->Xf[l]; o.ldr = D;
         o.Cf = t.u1; o.ldcf = D;
@@ -740,8 +740,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.M = rows; d.N = D; d.K = D; d.Mdev = Tdev;
             d.amode = OP_RK; d.A = du1b; d.lda = D;
             d.bmode = OP_KR; d.B = W + f.wo; d.ldb = D;
-            d.Cb = P->dO; d.ldcb = D;
-            d.splits = split_rows(D); d.ws = P->splitws;
+            d.Cb = P->dO; d.ldcb = D;  // (unsplit: faster than split-K plus its reduction here)
             TRY(gemm(d, s));
         }
         TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, dqkv, B, NH, D, s));
