@@ -325,10 +325,11 @@ __global__ void __launch_bounds__(256) scatter_cls_kernel(const float* __restric
 // ------------------------------------------------------------------ plan
 // K slices of a weight-gradient product (static M x N, K = the packed rows):
 // as many as fit one round of two workgroups per CU (a second, mostly empty
-// round would double the time), each at least 256 long.
+// round would double the time), at most four (the reduction's reads grow with
+// the count), each at least 256 long.
 int split_for(int M, int N, int K) {
     int tiles = (int)(cdiv(M, 128) * cdiv(N, 128));
-    int s = std::max(1, std::min(8, 512 / std::max(tiles, 1)));
+    int s = std::max(1, std::min(4, 512 / std::max(tiles, 1)));
     while (s > 1 && (int64_t)K / s < 256) --s;
     return s;
 }
@@ -727,7 +728,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.bmode = OP_KR; d.B = W + f.w1; d.ldb = D;
             d.resid = P->du2f; d.ldr = D;
             d.Cf = P->dHf; d.ldcf = D;
-            d.splits = split_rows(FF); d.ws = P->splitws;
+            d.splits = 2; d.ws = P->splitws;  // (two slices: half the partials for the LayerNorm to read)
             d.defer_reduce = true;  // summed by the LN1 backward
             TRY(gemm(d, s));
             dh_rows = deferred_rows(d);
@@ -752,7 +753,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             d.bmode = OP_KR; d.B = W + f.wqkv; d.ldb = D;
             d.resid = P->du1f; d.ldr = D;
             d.Cf = P->dY[cur ^ 1]; d.ldcf = D;
-            d.splits = split_rows(3 * D); d.ws = P->splitws;
+            d.splits = 2; d.ws = P->splitws;  // (as for FFN1)
             d.defer_reduce = true;  // summed by the next layer's LN2 backward
             TRY(gemm(d, s));
             dy_rows = deferred_rows(d);
