@@ -385,6 +385,134 @@ __global__ void __launch_bounds__(256) attn_bwd_mfma(const bf16_t* __restrict__ 
     }
 }
 
+// Attention of the first token only (the CLS query of each sequence), for
+// the last encoder layer, whose output is read at token 0 alone.  One
+// workgroup per (sequence, head), thread j on key j, in fp32 from the bf16
+// (high, low) parts of q, k and v.  Forward: out row b (compact, [B][d],
+// high and low parts) and lse[b H + h] = log sum_j exp(s_j), s_j = scale q.k_j.
+__device__ __forceinline__ float ldhl(const bf16_t* hi, const bf16_t* lo, int64_t o) {
+    return bf2f(hi[o]) + bf2f(lo[o]);
+}
+__device__ __forceinline__ float block_reduce2(float v, float* red, bool is_max) {
+    // two waves of 64
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const float u = __shfl_xor(v, off);
+        v = is_max ? fmaxf(v, u) : v + u;
+    }
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    const float r = is_max ? fmaxf(red[0], red[1]) : red[0] + red[1];
+    __syncthreads();
+    return r;
+}
+
+__global__ void __launch_bounds__(128) attn_cls_fwd(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ qkvlo,
+                                                     const int* __restrict__ cu, bf16_t* __restrict__ out,
+                                                     bf16_t* __restrict__ outlo, float* __restrict__ lse, int H, int d,
+                                                     float scale) {
+    __shared__ float qs[DH], p[LMAX], part[2][DH], red[2];
+    const int b = blockIdx.x / H, h = blockIdx.x % H;
+    const int base = cu[b], len = cu[b + 1] - cu[b];
+    const int64_t ld = 3 * d;
+    const int t = threadIdx.x;
+    if (t < DH) qs[t] = ldhl(qkv, qkvlo, (int64_t)base * ld + h * DH + t);
+    __syncthreads();
+    float sc = -INFINITY;
+    if (t < len) {
+        const int64_t o = (int64_t)(base + t) * ld + d + h * DH;
+        float acc = 0.f;
+#pragma unroll 8
+        for (int c = 0; c < DH; ++c) acc = fmaf(qs[c], ldhl(qkv, qkvlo, o + c), acc);
+        sc = acc * scale;
+    }
+    const float m = block_reduce2(sc, red, true);
+    const float e = t < len ? expf(sc - m) : 0.f;
+    const float sum = block_reduce2(e, red, false);
+    p[t] = e / sum;
+    if (t == 0) lse[(int64_t)b * H + h] = m + logf(sum);
+    __syncthreads();
+    // o_c = sum_j p_j v_jc: thread (half, c) sums the keys of its half
+    const int c = t & (DH - 1), half = t >> 6;
+    float acc = 0.f;
+    for (int j = half; j < len; j += 2) acc = fmaf(p[j], ldhl(qkv, qkvlo, (int64_t)(base + j) * ld + 2 * d + h * DH + c), acc);
+    part[half][c] = acc;
+    __syncthreads();
+    if (t < DH) {
+        const float v = part[0][t] + part[1][t];
+        const bf16_t hi = f2bf(v);
+        const int64_t o = (int64_t)b * d + h * DH + t;
+        out[o] = hi;
+        outlo[o] = f2bf(v - bf2f(hi));
+    }
+}
+
+// Backward of attn_cls_fwd, given dO of the first token (compact rows, bf16)
+// and the forward's O (compact, high and low parts) and lse:
+//   p_j = exp(s_j - lse), D = dO . O, ds_j = p_j (dO . v_j - D)
+//   dq = scale sum_j ds_j k_j (row 0 of the sequence), dk_j = scale ds_j q,
+//   dv_j = p_j dO; the query part of every other row is zero.  Writes every
+// row of the sequence in dqkv (bf16, [T][3d]).
+__global__ void __launch_bounds__(128) attn_cls_bwd(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ qkvlo,
+                                                     const int* __restrict__ cu, const bf16_t* __restrict__ out,
+                                                     const bf16_t* __restrict__ outlo, const bf16_t* __restrict__ dout,
+                                                     const float* __restrict__ lse, bf16_t* __restrict__ dqkv, int H,
+                                                     int d, float scale) {
+    __shared__ float qs[DH], dos[DH], p[LMAX], ds[LMAX], part[2][DH], red[2];
+    const int b = blockIdx.x / H, h = blockIdx.x % H;
+    const int base = cu[b], len = cu[b + 1] - cu[b];
+    const int64_t ld = 3 * d;
+    const int t = threadIdx.x;
+    float dprod = 0.f;
+    if (t < DH) {
+        qs[t] = ldhl(qkv, qkvlo, (int64_t)base * ld + h * DH + t);
+        const int64_t o = (int64_t)b * d + h * DH + t;
+        dos[t] = bf2f(dout[o]);
+        dprod = dos[t] * ldhl(out, outlo, o);
+    }
+    const float Dv = block_reduce2(dprod, red, false);  // (also orders the stores of qs, dos)
+    const float L = lse[(int64_t)b * H + h];
+    float pj = 0.f, dsj = 0.f;
+    if (t < len) {
+        const int64_t o = (int64_t)(base + t) * ld + h * DH;
+        float sacc = 0.f, dpacc = 0.f;
+#pragma unroll 8
+        for (int c = 0; c < DH; ++c) {
+            sacc = fmaf(qs[c], ldhl(qkv, qkvlo, o + d + c), sacc);
+            dpacc = fmaf(dos[c], ldhl(qkv, qkvlo, o + 2 * d + c), dpacc);
+        }
+        pj = expf(sacc * scale - L);
+        dsj = pj * (dpacc - Dv);
+    }
+    p[t] = pj;
+    ds[t] = dsj;
+    __syncthreads();
+    // dq (row 0): thread (half, c) sums its half of the keys
+    const int c = t & (DH - 1), half = t >> 6;
+    float acc = 0.f;
+    for (int j = half; j < len; j += 2) acc = fmaf(ds[j], ldhl(qkv, qkvlo, (int64_t)(base + j) * ld + d + h * DH + c), acc);
+    part[half][c] = acc;
+    // rows: eight threads per row, 8 columns each, for the q (zero past row 0), k and v parts
+    for (int idx = t; idx < len * 8; idx += blockDim.x) {
+        const int j = idx >> 3, c8 = (idx & 7) * 8;
+        bf16_t* row = dqkv + (int64_t)(base + j) * ld + h * DH + c8;
+        uint4 kz, vz;
+        uint32_t kw[4], vw[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            kw[e] = f2bf2(scale * ds[j] * qs[c8 + 2 * e], scale * ds[j] * qs[c8 + 2 * e + 1]);
+            vw[e] = f2bf2(p[j] * dos[c8 + 2 * e], p[j] * dos[c8 + 2 * e + 1]);
+        }
+        kz = make_uint4(kw[0], kw[1], kw[2], kw[3]);
+        vz = make_uint4(vw[0], vw[1], vw[2], vw[3]);
+        if (j > 0) *reinterpret_cast<uint4*>(row) = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(row + d) = kz;
+        *reinterpret_cast<uint4*>(row + 2 * d) = vz;
+    }
+    __syncthreads();
+    if (t < DH) dqkv[(int64_t)base * ld + h * DH + t] = f2bf(scale * (part[0][t] + part[1][t]));
+}
+
 }  // namespace
 
 fo_status launch_attn_fwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu, bf16_t* out, bf16_t* outlo,
@@ -413,6 +541,31 @@ fo_status launch_attn_bwd(const bf16_t* qkv, const int* cu, const bf16_t* out, c
     int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
     hipExtLaunchKernelGGL(attn_bwd_mfma, dim3(B * H), dim3(256), 0, s, ea, eb, 0, qkv, cu, out, dout, lse, dqkv, H, d,
                           scale, snap, B);
+    prof_end_ext(h);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+fo_status launch_attn_cls_fwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu, bf16_t* out, bf16_t* outlo,
+                              float* lse, int B, int H, int d, hipStream_t s) {
+    FO_CHECK(d == H * DH, "attention: d=%d must equal heads*%d", d, DH);
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext("attn_cls_fwd", ProfInfo(), &ea, &eb);
+    hipExtLaunchKernelGGL(attn_cls_fwd, dim3(B * H), dim3(128), 0, s, ea, eb, 0, qkv, qkvlo, cu, out, outlo, lse, H, d,
+                          1.f / sqrtf((float)DH));
+    prof_end_ext(h);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+fo_status launch_attn_cls_bwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu, const bf16_t* out,
+                              const bf16_t* outlo, const bf16_t* dout, const float* lse, bf16_t* dqkv, int B, int H,
+                              int d, hipStream_t s) {
+    FO_CHECK(d == H * DH, "attention: d=%d must equal heads*%d", d, DH);
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext("attn_cls_bwd", ProfInfo(), &ea, &eb);
+    hipExtLaunchKernelGGL(attn_cls_bwd, dim3(B * H), dim3(128), 0, s, ea, eb, 0, qkv, qkvlo, cu, out, outlo, dout, lse,
+                          dqkv, H, d, 1.f / sqrtf((float)DH));
     prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;

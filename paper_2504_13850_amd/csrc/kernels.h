@@ -37,6 +37,15 @@ fo_status launch_attn_fwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu,
                           float* lse, int B, int H, int d, hipStream_t s);
 fo_status launch_attn_bwd(const bf16_t* qkv, const int* cu, const bf16_t* out, const bf16_t* dout,
                           const float* lse, bf16_t* dqkv, int B, int H, int d, hipStream_t s);
+// The same attention for the first token of each sequence only (the last
+// encoder layer, read at token 0 alone): out / outlo and lse are compact
+// ([B][d], [B][H]); the backward writes every row of dqkv (the query part of
+// rows past the first is zero).
+fo_status launch_attn_cls_fwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu, bf16_t* out, bf16_t* outlo,
+                              float* lse, int B, int H, int d, hipStream_t s);
+fo_status launch_attn_cls_bwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu, const bf16_t* out,
+                              const bf16_t* outlo, const bf16_t* dout, const float* lse, bf16_t* dqkv, int B, int H,
+                              int d, hipStream_t s);
 
 // ------------------------------------------------------------------ k_common.hip
 // mean cross-entropy of logits z [B][C] and dz = (softmax - onehot)/B

@@ -37,7 +37,7 @@ struct LayerAct {
 
 struct Plan {
     int rows;  // max_batch * L
-    int* cu;   // [max_batch + 1]; cu[B] = T
+    int* cu;   // [max_batch + 2]; cu[B] = T, cu[B + 1] = B
     LayerOff off[NL];
     int64_t pool_w, pool_b, cls_w, cls_b;
     bf16_t* Xb[NL + 1];
@@ -55,7 +55,8 @@ struct Plan {
     // (lnpart[parity][0] LN2, [1] LN1); colws2: the side stream's own (bqkv)
     float *colwsF[2], *lnpart[2][2], *colws2;
     int split_qkv, split_o, split_f1, split_f2;
-    float *xc, *pooled, *dz, *dpool, *dxc;
+    float *pooled, *dz, *dpool, *dxc;
+    float* xres;  // the last layer's residual input at the first tokens, [B][D]
     // parameter ranges whose SGD update is not fused into a weight-gradient
     // product (biases, norm parameters, pooler, classifier): device [n][2]
     int64_t* sgd_chunks = nullptr;
@@ -77,6 +78,7 @@ __global__ void build_cu_kernel(const int32_t* __restrict__ lengths, int B, int 
         acc += len;
     }
     cu[B] = acc;
+    cu[B + 1] = B;  // the row count of the last layer's first-token rows
 }
 
 // padded [B][L][D] bf16 -> packed rows (bf16 and fp32 copies)
@@ -374,7 +376,7 @@ size_t ws_bytes(const fo_model* m) {
     size_t s = 0;
     auto add = [&](size_t b) { s += (b + 255) & ~size_t(255); };
     add(sizeof(Plan));
-    add(4 * (B + 1));
+    add(4 * (B + 2));
     for (int l = 0; l <= NL; ++l) {
         add(2 * R * D);
         add(2 * R * D);
@@ -410,7 +412,7 @@ size_t ws_bytes(const fo_model* m) {
     add(4 * colsum_ws_floats((int)R, 3 * D));
     for (int q = 0; q < 4; ++q) add(4 * (size_t)cdiv(R, LNB_ROWS) * 3 * D);
     add(4 * small_linear_ws_floats((int)B, D, D));
-    add(4 * B * D); add(4 * B * D); add(4 * B * NC); add(4 * B * D); add(4 * B * D);
+    add(4 * B * D); add(4 * B * NC); add(4 * B * D); add(4 * B * D); add(4 * B * D);
     add(16 * kMaxSgdChunks);
     return s;
 }
@@ -447,7 +449,7 @@ fo_status init(fo_model* m) {
     }
     Arena& a = m->arena;
     a.take<char>(sizeof(Plan));
-    P->cu = a.take<int>(B + 1);
+    P->cu = a.take<int>(B + 2);
     for (int l = 0; l <= NL; ++l) {
         P->Xb[l] = a.take<bf16_t>(R * D);
         P->Xlo[l] = a.take<bf16_t>(R * D);
@@ -502,11 +504,11 @@ fo_status init(fo_model* m) {
     P->colws2 = a.take<float>(colsum_ws_floats((int)R, 3 * D));
     for (int q = 0; q < 4; ++q) P->lnpart[q / 2][q % 2] = a.take<float>((size_t)cdiv(R, LNB_ROWS) * 3 * D);
     P->slws = a.take<float>(small_linear_ws_floats((int)B, D, D));
-    P->xc = a.take<float>(B * D);
     P->pooled = a.take<float>(B * D);
     P->dz = a.take<float>(B * NC);
     P->dpool = a.take<float>(B * D);
     P->dxc = a.take<float>(B * D);
+    P->xres = a.take<float>(B * D);
     P->sgd_chunks = a.take<int64_t>(2 * kMaxSgdChunks);
     if (!P->sgd_chunks) {
         set_error("bert: workspace arena too small");
@@ -614,62 +616,77 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
                            P->Xf[0]);
     }
     FO_LAUNCHED();
-    const dim3 lngrid((unsigned)cdiv(rows, 4));
 
     // ---------------- forward (Alg. 4: forward pass of M_s)
+    // The loss reads the last layer's output at the first token of each
+    // sequence only, so that layer runs its key / value projection over every
+    // token and everything after it (first-token attention, output projection,
+    // norms, FFN) over the B first-token rows, compactly ([B][D], row b =
+    // sequence b).  The result is exact: no other row of the last layer reaches
+    // the loss.
+    const int* Bdev = P->cu + B + 1;  // device copy of B
     for (int l = 0; l < NL; ++l) {
         const LayerOff& f = P->off[l];
         LayerAct& t = P->a[l];
+        const bool cls = l == NL - 1;
         GemmDesc q = lin_fwd(rows, P->Xb[l], l ? P->Xlo[l] : nullptr, D, W + f.wqkv, Wl + f.wqkv, 3 * D);
         q.Mdev = Tdev;
         q.bias = prm + f.bqkv;
         q.Cb = t.qkv; q.Cb2 = t.qkvlo; q.ldcb = 3 * D;
         TRY(gemm(q, s));
-        TRY(launch_attn_fwd(t.qkv, t.qkvlo, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
-        GemmDesc o = lin_fwd(rows, t.O, t.Olo, D, W + f.wo, Wl + f.wo, D);
-        o.Mdev = Tdev;
-        o.splits = 2; o.ws = P->splitws;  // (two slices time like four and halve the LayerNorm's reads)
+        // rows of the rest of the layer: every token, or the B first tokens
+        const int M = cls ? B : rows;
+        const int* Mdev = cls ? Bdev : Tdev;
+        const dim3 lng((unsigned)cdiv(M, 4));
+        if (cls) {
+            TRY(launch_attn_cls_fwd(t.qkv, t.qkvlo, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
+            hipLaunchKernelGGL(gather_cls_kernel, dim3(B), dim3(256), 0, s, P->Xf[l], P->cu, B, P->xres);
+            FO_LAUNCHED();
+        } else {
+            TRY(launch_attn_fwd(t.qkv, t.qkvlo, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
+        }
+        GemmDesc o = lin_fwd(M, t.O, t.Olo, D, W + f.wo, Wl + f.wo, D);
+        o.Mdev = Mdev;
+        o.splits = cls ? 8 : 2; o.ws = P->splitws;  // (two slices time like four and halve the LayerNorm's reads)
         o.bias = prm + f.bo;
-        o.resid = P->Xf[l]; o.ldr = D;
+        o.resid = cls ? P->xres : P->Xf[l]; o.ldr = D;
         o.Cf = t.u1; o.ldcf = D;
         o.defer_reduce = true;  // summed by the LayerNorm below
         TRY(gemm(o, s));
-        hipLaunchKernelGGL(ln_fwd_kernel, lngrid, dim3(256), 0, s, deferred_rows(o), t.u1, prm + f.g1, prm + f.b1,
-                           Tdev, t.Hf, t.Hb, t.Hlo, t.mean1, t.rstd1);
-        GemmDesc f1 = lin_fwd(rows, t.Hb, t.Hlo, D, W + f.w1, Wl + f.w1, FF);
-        f1.Mdev = Tdev;
+        hipLaunchKernelGGL(ln_fwd_kernel, lng, dim3(256), 0, s, deferred_rows(o), t.u1, prm + f.g1, prm + f.b1, Mdev,
+                           t.Hf, t.Hb, t.Hlo, t.mean1, t.rstd1);
+        GemmDesc f1 = lin_fwd(M, t.Hb, t.Hlo, D, W + f.w1, Wl + f.w1, FF);
+        f1.Mdev = Mdev;
+        if (cls) { f1.splits = 4; f1.ws = P->splitws; }  // (B rows: K slices for parallelism)
         f1.bias = prm + f.bf1;
         f1.act = ACT_GELU; f1.dact_out = t.dgelu1; f1.ldm = FF;
         f1.Cb = t.G; f1.Cb2 = t.Glo; f1.ldcb = FF;
         TRY(gemm(f1, s));
-        GemmDesc f2 = lin_fwd(rows, t.G, t.Glo, FF, W + f.w2, Wl + f.w2, D);
-        f2.Mdev = Tdev;
-        f2.splits = split_rows(3 * FF); f2.ws = P->splitws;
+        GemmDesc f2 = lin_fwd(M, t.G, t.Glo, FF, W + f.w2, Wl + f.w2, D);
+        f2.Mdev = Mdev;
+        f2.splits = cls ? 8 : split_rows(3 * FF); f2.ws = P->splitws;
         f2.bias = prm + f.bf2;
         f2.resid = t.Hf; f2.ldr = D;
         f2.Cf = t.u2; f2.ldcf = D;
         f2.defer_reduce = true;
         TRY(gemm(f2, s));
-        hipLaunchKernelGGL(ln_fwd_kernel, lngrid, dim3(256), 0, s, deferred_rows(f2), t.u2, prm + f.g2, prm + f.b2,
-                           Tdev, P->Xf[l + 1], P->Xb[l + 1], P->Xlo[l + 1], t.mean2, t.rstd2);
+        hipLaunchKernelGGL(ln_fwd_kernel, lng, dim3(256), 0, s, deferred_rows(f2), t.u2, prm + f.g2, prm + f.b2, Mdev,
+                           P->Xf[l + 1], P->Xb[l + 1], P->Xlo[l + 1], t.mean2, t.rstd2);
         FO_LAUNCHED();
     }
 
-    // ---------------- head: pooler on the first token, classifier, loss f_s
-    hipLaunchKernelGGL(gather_cls_kernel, dim3(B), dim3(256), 0, s, P->Xf[NL], P->cu, B, P->xc);
-    FO_LAUNCHED();
-    TRY(launch_small_linear_fwd(P->xc, prm + P->pool_w, prm + P->pool_b, P->pooled, B, D, D, true, s));
+    // ---------------- head: pooler on the first token (row b of the last
+    // layer's compact output), classifier, loss f_s
+    const float* xcls = P->Xf[NL];
+    TRY(launch_small_linear_fwd(xcls, prm + P->pool_w, prm + P->pool_b, P->pooled, B, D, D, true, s));
     TRY(launch_small_linear_fwd(P->pooled, prm + P->cls_w, prm + P->cls_b, m->logits, B, D, NC, false, s));
     TRY(launch_xent(m->logits, labels, P->dz, m->loss, B, NC, s));
 
     // ---------------- backward (Alg. 4: backward pass of M_s)
     TRY(launch_small_linear_bwd(P->dz, P->pooled, prm + P->cls_w, P->pooled, grd + P->cls_w, grd + P->cls_b,
                                 P->dpool, B, D, NC, P->slws, s));
-    TRY(launch_small_linear_bwd(P->dpool, P->xc, prm + P->pool_w, nullptr, grd + P->pool_w, grd + P->pool_b, P->dxc,
+    TRY(launch_small_linear_bwd(P->dpool, xcls, prm + P->pool_w, nullptr, grd + P->pool_w, grd + P->pool_b, P->dxc,
                                 B, D, D, P->slws, s));
-    TRY(launch_fill(P->dY[0], (int64_t)rows * D, 0.f, s));
-    hipLaunchKernelGGL(scatter_cls_kernel, dim3(B), dim3(256), 0, s, P->dxc, P->cu, B, P->dY[0]);
-    FO_LAUNCHED();
 
     // Weight gradients: the four products of layer l go to the side stream
     // together, after the main stream has issued layer l's input-gradient chain
@@ -685,9 +702,10 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     float* prmw = m->params;
     bf16_t* w16 = m->w16;
     bf16_t* w16lo = m->w16lo;
-    auto wgrad = [&](int M_, int N_, const bf16_t* A_, const bf16_t* B_, int64_t off, int splits) {
-        GemmDesc w;  // dW = A^T B over the packed rows -> grads; theta -= lr dW; bf16 parts
-        w.M = M_; w.N = N_; w.K = rows; w.Kdev = Tdev;
+    auto wgrad = [&](int M_, int N_, const bf16_t* A_, const bf16_t* B_, int64_t off, int K_, const int* Kdev_,
+                     int splits) {
+        GemmDesc w;  // dW = A^T B over K_ rows -> grads; theta -= lr dW; bf16 parts
+        w.M = M_; w.N = N_; w.K = K_; w.Kdev = Kdev_;
         w.amode = OP_KR; w.A = A_; w.lda = M_;
         w.bmode = OP_KR; w.B = B_; w.ldb = N_;
         w.Cf = grd + off; w.ldcf = N_;
@@ -699,19 +717,25 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         return gemm(w, s2);
     };
     int cur = 0;
-    SplitRows dy_rows = plain_rows(P->dY[0], rows);  // the LN2 backward's input: dY, or the deferred dX of the layer above
+    SplitRows dy_rows;  // the LN2 backward's input: the deferred dX of the layer above
     for (int l = NL - 1; l >= 0; --l) {
         const LayerOff& f = P->off[l];
         LayerAct& t = P->a[l];
         const int pb = l & 1;
         bf16_t *du2b = P->du2b[pb], *dA1 = P->dA1[pb], *du1b = P->du1b[pb], *dqkv = P->dqkv[pb];
         if (l + 2 < NL) FO_HIP(hipStreamWaitEvent(s, P->ev_done[pb], 0));
+        // the last layer runs on its B first-token rows (compact) down to the
+        // attention, whose backward reaches every key and value row
+        const bool cls = l == NL - 1;
+        const int M = cls ? B : rows;
+        const int* Mdev = cls ? Bdev : Tdev;
+        if (cls) dy_rows = plain_rows(P->dxc, B);
         // LN2
-        TRY(ln_bwd(dy_rows, t.u2, t.mean2, t.rstd2, prm + f.g2, Tdev, rows, P->du2f, du2b, P->lnpart[pb][0], s));
+        TRY(ln_bwd(dy_rows, t.u2, t.mean2, t.rstd2, prm + f.g2, Mdev, M, P->du2f, du2b, P->lnpart[pb][0], s));
         // FFN2: dG = du2 W2, times GELU' of the FFN1 pre-activation -> dA1; db1
         {
             GemmDesc d;
-            d.M = rows; d.N = FF; d.K = D; d.Mdev = Tdev;
+            d.M = M; d.N = FF; d.K = D; d.Mdev = Mdev;
             d.amode = OP_RK; d.A = du2b; d.lda = D;
             d.bmode = OP_KR; d.B = W + f.w2; d.ldb = FF;
             d.dact = t.dgelu1; d.ldm = FF;
@@ -723,35 +747,46 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         // FFN1: dH = du2 + dA1 W1
         {
             GemmDesc d;
-            d.M = rows; d.N = D; d.K = FF; d.Mdev = Tdev;
+            d.M = M; d.N = D; d.K = FF; d.Mdev = Mdev;
             d.amode = OP_RK; d.A = dA1; d.lda = FF;
             d.bmode = OP_KR; d.B = W + f.w1; d.ldb = D;
             d.resid = P->du2f; d.ldr = D;
             d.Cf = P->dHf; d.ldcf = D;
-            d.splits = 2; d.ws = P->splitws;  // (two slices: half the partials for the LayerNorm to read)
+            d.splits = cls ? 8 : 2; d.ws = P->splitws;  // (two slices: half the partials for the LayerNorm to read)
             d.defer_reduce = true;  // summed by the LN1 backward
             TRY(gemm(d, s));
             dh_rows = deferred_rows(d);
         }
         // LN1
-        TRY(ln_bwd(dh_rows, t.u1, t.mean1, t.rstd1, prm + f.g1, Tdev, rows, P->du1f, du1b, P->lnpart[pb][1], s));
+        TRY(ln_bwd(dh_rows, t.u1, t.mean1, t.rstd1, prm + f.g1, Mdev, M, P->du1f, du1b, P->lnpart[pb][1], s));
         // output projection: dO = du1 Wo
         {
             GemmDesc d;
-            d.M = rows; d.N = D; d.K = D; d.Mdev = Tdev;
+            d.M = M; d.N = D; d.K = D; d.Mdev = Mdev;
             d.amode = OP_RK; d.A = du1b; d.lda = D;
             d.bmode = OP_KR; d.B = W + f.wo; d.ldb = D;
             d.Cb = P->dO; d.ldcb = D;  // (unsplit: faster than split-K plus its reduction here)
+            if (cls) { d.splits = 4; d.ws = P->splitws; }  // (B rows: K slices for parallelism)
             TRY(gemm(d, s));
         }
-        TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, dqkv, B, NH, D, s));
+        const float* du1_full = P->du1f;  // du1 over every row, the residual of dX
+        if (cls) {
+            TRY(launch_attn_cls_bwd(t.qkv, t.qkvlo, P->cu, t.O, t.Olo, P->dO, t.lse, dqkv, B, NH, D, s));
+            // du1 is nonzero at the first tokens only
+            TRY(launch_fill(P->dHf, (int64_t)rows * D, 0.f, s));
+            hipLaunchKernelGGL(scatter_cls_kernel, dim3(B), dim3(256), 0, s, P->du1f, P->cu, B, P->dHf);
+            FO_LAUNCHED();
+            du1_full = P->dHf;
+        } else {
+            TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, dqkv, B, NH, D, s));
+        }
         // input projection: dX = du1 + dqkv Wqkv (skipped for the first server layer), dbqkv
         if (l > 0) {
             GemmDesc d;
             d.M = rows; d.N = D; d.K = 3 * D; d.Mdev = Tdev;
             d.amode = OP_RK; d.A = dqkv; d.lda = 3 * D;
             d.bmode = OP_KR; d.B = W + f.wqkv; d.ldb = D;
-            d.resid = P->du1f; d.ldr = D;
+            d.resid = du1_full; d.ldr = D;
             d.Cf = P->dY[cur ^ 1]; d.ldcf = D;
             d.splits = 2; d.ws = P->splitws;  // (as for FFN1)
             d.defer_reduce = true;  // summed by the next layer's LN2 backward
@@ -762,19 +797,25 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         // norm gradients from their partials, then the weight gradients with
         // their SGD updates
         TRY(order_after(s2, s, P->ev_fork));
-        TRY(ln_bwd_finish(P->lnpart[pb][0], Tdev, rows, grd + f.g2, grd + f.b2, grd + f.bf2, s2));
+        TRY(ln_bwd_finish(P->lnpart[pb][0], Mdev, M, grd + f.g2, grd + f.b2, grd + f.bf2, s2));
         {
             ColOut cb;
             cb.p[0] = grd + f.bf1;
             cb.seg = FF;
-            TRY(launch_colsum_finish(P->colwsF[pb], rows, Tdev, 128, FF, cb, s2));
+            TRY(launch_colsum_finish(P->colwsF[pb], M, Mdev, 128, FF, cb, s2));
         }
-        TRY(ln_bwd_finish(P->lnpart[pb][1], Tdev, rows, grd + f.g1, grd + f.b1, grd + f.bo, s2));
+        TRY(ln_bwd_finish(P->lnpart[pb][1], Mdev, M, grd + f.g1, grd + f.b1, grd + f.bo, s2));
         TRY(launch_colsum(dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws2, s2));
-        TRY(wgrad(D, FF, du2b, t.G, f.w2, P->split_f2));              // dW2 = du2^T G
-        TRY(wgrad(FF, D, dA1, t.Hb, f.w1, P->split_f1));              // dW1 = dA1^T H
-        TRY(wgrad(D, D, du1b, t.O, f.wo, P->split_o));                // dWo = du1^T O
-        TRY(wgrad(3 * D, D, dqkv, P->Xb[l], f.wqkv, P->split_qkv));  // dWqkv = dqkv^T X
+        if (cls) {  // over the B first-token rows (static count)
+            TRY(wgrad(D, FF, du2b, t.G, f.w2, B, nullptr, 1));
+            TRY(wgrad(FF, D, dA1, t.Hb, f.w1, B, nullptr, 1));
+            TRY(wgrad(D, D, du1b, t.O, f.wo, B, nullptr, 1));
+        } else {
+            TRY(wgrad(D, FF, du2b, t.G, f.w2, rows, Tdev, P->split_f2));  // dW2 = du2^T G
+            TRY(wgrad(FF, D, dA1, t.Hb, f.w1, rows, Tdev, P->split_f1));  // dW1 = dA1^T H
+            TRY(wgrad(D, D, du1b, t.O, f.wo, rows, Tdev, P->split_o));    // dWo = du1^T O
+        }
+        TRY(wgrad(3 * D, D, dqkv, P->Xb[l], f.wqkv, rows, Tdev, P->split_qkv));  // dWqkv = dqkv^T X
         FO_HIP(hipEventRecord(P->ev_done[pb], s2));
         cur ^= 1;
     }
