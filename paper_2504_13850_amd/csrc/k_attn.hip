@@ -407,39 +407,70 @@ __device__ __forceinline__ float block_reduce2(float v, float* red, bool is_max)
     return r;
 }
 
+// Eight consecutive values from the (high, low) parts at element offset o (16-byte aligned).
+__device__ __forceinline__ void ld8hl(const bf16_t* hi, const bf16_t* lo, int64_t o, float* v) {
+    const uint4 h = *reinterpret_cast<const uint4*>(hi + o), l = *reinterpret_cast<const uint4*>(lo + o);
+    const uint32_t hw[4] = {h.x, h.y, h.z, h.w}, lw[4] = {l.x, l.y, l.z, l.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        v[2 * e] = bf2f((bf16_t)(hw[e] & 0xFFFFu)) + bf2f((bf16_t)(lw[e] & 0xFFFFu));
+        v[2 * e + 1] = bf2f((bf16_t)(hw[e] >> 16)) + bf2f((bf16_t)(lw[e] >> 16));
+    }
+}
+// q . row over the head's 64 columns (row offset o), q in LDS
+__device__ __forceinline__ float dot64(const float* q, const bf16_t* hi, const bf16_t* lo, int64_t o) {
+    float acc = 0.f, v[8];
+#pragma unroll
+    for (int c8 = 0; c8 < DH; c8 += 8) {
+        ld8hl(hi, lo, o + c8, v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = fmaf(q[c8 + e], v[e], acc);
+    }
+    return acc;
+}
+// sum_j w_j row_j[c] for the 64 columns of a head: thread t takes the eight
+// columns 8 (t % 8) .. and the keys j = t / 8 (mod 16); the sixteen partial sums
+// of a column meet in LDS (part, 16 x 64) and thread c < 64 returns column c.
+__device__ __forceinline__ float wsum64(const float* w, int len, const bf16_t* hi, const bf16_t* lo, int64_t o0,
+                                        int64_t ld, float (*part)[DH]) {
+    const int t = threadIdx.x, c8 = (t & 7) * 8, g = t >> 3;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, v[8];
+    for (int j = g; j < len; j += 16) {
+        ld8hl(hi, lo, o0 + (int64_t)j * ld + c8, v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(w[j], v[e], acc[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[g][c8 + e] = acc[e];
+    __syncthreads();
+    float r = 0.f;
+    if (t < DH) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) r += part[k][t];
+    }
+    return r;
+}
+
 __global__ void __launch_bounds__(128) attn_cls_fwd(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ qkvlo,
                                                      const int* __restrict__ cu, bf16_t* __restrict__ out,
                                                      bf16_t* __restrict__ outlo, float* __restrict__ lse, int H, int d,
                                                      float scale) {
-    __shared__ float qs[DH], p[LMAX], part[2][DH], red[2];
+    __shared__ float qs[DH], p[LMAX], part[16][DH], red[2];
     const int b = blockIdx.x / H, h = blockIdx.x % H;
     const int base = cu[b], len = cu[b + 1] - cu[b];
     const int64_t ld = 3 * d;
     const int t = threadIdx.x;
     if (t < DH) qs[t] = ldhl(qkv, qkvlo, (int64_t)base * ld + h * DH + t);
     __syncthreads();
-    float sc = -INFINITY;
-    if (t < len) {
-        const int64_t o = (int64_t)(base + t) * ld + d + h * DH;
-        float acc = 0.f;
-#pragma unroll 8
-        for (int c = 0; c < DH; ++c) acc = fmaf(qs[c], ldhl(qkv, qkvlo, o + c), acc);
-        sc = acc * scale;
-    }
+    const float sc = t < len ? scale * dot64(qs, qkv, qkvlo, (int64_t)(base + t) * ld + d + h * DH) : -INFINITY;
     const float m = block_reduce2(sc, red, true);
     const float e = t < len ? expf(sc - m) : 0.f;
     const float sum = block_reduce2(e, red, false);
     p[t] = e / sum;
     if (t == 0) lse[(int64_t)b * H + h] = m + logf(sum);
     __syncthreads();
-    // o_c = sum_j p_j v_jc: thread (half, c) sums the keys of its half
-    const int c = t & (DH - 1), half = t >> 6;
-    float acc = 0.f;
-    for (int j = half; j < len; j += 2) acc = fmaf(p[j], ldhl(qkv, qkvlo, (int64_t)(base + j) * ld + 2 * d + h * DH + c), acc);
-    part[half][c] = acc;
-    __syncthreads();
+    const float v = wsum64(p, len, qkv, qkvlo, (int64_t)base * ld + 2 * d + h * DH, ld, part);
     if (t < DH) {
-        const float v = part[0][t] + part[1][t];
         const bf16_t hi = f2bf(v);
         const int64_t o = (int64_t)b * d + h * DH + t;
         out[o] = hi;
@@ -458,7 +489,7 @@ __global__ void __launch_bounds__(128) attn_cls_bwd(const bf16_t* __restrict__ q
                                                      const bf16_t* __restrict__ outlo, const bf16_t* __restrict__ dout,
                                                      const float* __restrict__ lse, bf16_t* __restrict__ dqkv, int H,
                                                      int d, float scale) {
-    __shared__ float qs[DH], dos[DH], p[LMAX], ds[LMAX], part[2][DH], red[2];
+    __shared__ float qs[DH], dos[DH], p[LMAX], ds[LMAX], part[16][DH], red[2];
     const int b = blockIdx.x / H, h = blockIdx.x % H;
     const int base = cu[b], len = cu[b + 1] - cu[b];
     const int64_t ld = 3 * d;
@@ -475,42 +506,29 @@ __global__ void __launch_bounds__(128) attn_cls_bwd(const bf16_t* __restrict__ q
     float pj = 0.f, dsj = 0.f;
     if (t < len) {
         const int64_t o = (int64_t)(base + t) * ld + h * DH;
-        float sacc = 0.f, dpacc = 0.f;
-#pragma unroll 8
-        for (int c = 0; c < DH; ++c) {
-            sacc = fmaf(qs[c], ldhl(qkv, qkvlo, o + d + c), sacc);
-            dpacc = fmaf(dos[c], ldhl(qkv, qkvlo, o + 2 * d + c), dpacc);
-        }
-        pj = expf(sacc * scale - L);
-        dsj = pj * (dpacc - Dv);
+        pj = expf(scale * dot64(qs, qkv, qkvlo, o + d) - L);
+        dsj = pj * (dot64(dos, qkv, qkvlo, o + 2 * d) - Dv);
     }
     p[t] = pj;
     ds[t] = dsj;
     __syncthreads();
-    // dq (row 0): thread (half, c) sums its half of the keys
-    const int c = t & (DH - 1), half = t >> 6;
-    float acc = 0.f;
-    for (int j = half; j < len; j += 2) acc = fmaf(ds[j], ldhl(qkv, qkvlo, (int64_t)(base + j) * ld + d + h * DH + c), acc);
-    part[half][c] = acc;
     // rows: eight threads per row, 8 columns each, for the q (zero past row 0), k and v parts
     for (int idx = t; idx < len * 8; idx += blockDim.x) {
         const int j = idx >> 3, c8 = (idx & 7) * 8;
         bf16_t* row = dqkv + (int64_t)(base + j) * ld + h * DH + c8;
-        uint4 kz, vz;
         uint32_t kw[4], vw[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             kw[e] = f2bf2(scale * ds[j] * qs[c8 + 2 * e], scale * ds[j] * qs[c8 + 2 * e + 1]);
             vw[e] = f2bf2(p[j] * dos[c8 + 2 * e], p[j] * dos[c8 + 2 * e + 1]);
         }
-        kz = make_uint4(kw[0], kw[1], kw[2], kw[3]);
-        vz = make_uint4(vw[0], vw[1], vw[2], vw[3]);
         if (j > 0) *reinterpret_cast<uint4*>(row) = make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4*>(row + d) = kz;
-        *reinterpret_cast<uint4*>(row + 2 * d) = vz;
+        *reinterpret_cast<uint4*>(row + d) = make_uint4(kw[0], kw[1], kw[2], kw[3]);
+        *reinterpret_cast<uint4*>(row + 2 * d) = make_uint4(vw[0], vw[1], vw[2], vw[3]);
     }
-    __syncthreads();
-    if (t < DH) dqkv[(int64_t)base * ld + h * DH + t] = f2bf(scale * (part[0][t] + part[1][t]));
+    // dq (row 0)
+    const float dq = wsum64(ds, len, qkv, qkvlo, (int64_t)base * ld + d + h * DH, ld, part);
+    if (t < DH) dqkv[(int64_t)base * ld + h * DH + t] = f2bf(scale * dq);
 }
 
 }  // namespace
