@@ -326,12 +326,12 @@ __global__ void __launch_bounds__(256) scatter_cls_kernel(const float* __restric
 
 // ------------------------------------------------------------------ plan
 // K slices of a weight-gradient product (static M x N, K = the packed rows):
-// as many as fit one round of two workgroups per CU (a second, mostly empty
-// round would double the time), at most four (the reduction's reads grow with
-// the count), each at least 256 long.
+// about 300 workgroups in all (these products share the GPU with the
+// input-gradient chain; fewer slices also leave less for the reduction to
+// read), at most four, each at least 256 long.
 int split_for(int M, int N, int K) {
     int tiles = (int)(cdiv(M, 128) * cdiv(N, 128));
-    int s = std::max(1, std::min(4, 512 / std::max(tiles, 1)));
+    int s = std::max(1, std::min(4, 300 / std::max(tiles, 1)));
     while (s > 1 && (int64_t)K / s < 256) --s;
     return s;
 }
