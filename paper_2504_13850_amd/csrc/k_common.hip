@@ -104,6 +104,40 @@ __global__ void __launch_bounds__(256) colsum_finish(const float* __restrict__ p
     }
 }
 
+// colsum_finish over several jobs: blocks are dealt to the jobs in order, each
+// job taking ceil(N / 64) of them; the arithmetic per column is colsum_finish's.
+__global__ void __launch_bounds__(256) colsum_finish_multi(const ColJobs jobs) {
+    __shared__ float red[4][64];
+    int bid = blockIdx.x, ji = 0;
+    while (ji < jobs.n - 1 && bid >= (jobs.j[ji].N + 63) / 64) {
+        bid -= (jobs.j[ji].N + 63) / 64;
+        ++ji;
+    }
+    const ColJob& J = jobs.j[ji];
+    const int R = J.rows_dev ? min(J.rows, *J.rows_dev) : J.rows;
+    const int nparts = (R + J.rows_per_part - 1) / J.rows_per_part;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = bid * 64 + lane;
+    float s = 0.f;
+    if (col < J.N) {
+        int p = wave;
+        for (; p + 28 < nparts; p += 32) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = J.part[(int64_t)(p + 4 * u) * J.N + col];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; p < nparts; p += 4) s += J.part[(int64_t)p * J.N + col];
+    }
+    red[wave][lane] = s;
+    __syncthreads();
+    if (wave == 0 && col < J.N) {
+        const int j = col / J.out.seg;
+        J.out.p[j][col - j * J.out.seg] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+    }
+}
+
 __global__ void __launch_bounds__(256) fill_kernel(float* __restrict__ p, int64_t n, float v) {
     int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
@@ -277,6 +311,31 @@ fo_status launch_colsum_finish(const float* part, int rows, const int* rows_dev,
     FO_CHECK(out.seg > 0 && cdiv(N, out.seg) <= 3, "colsum: %d columns in segments of %d", N, out.seg);
     hipLaunchKernelGGL(colsum_finish, dim3(cdiv(N, 64)), dim3(256), 0, s, part, rows, rows_dev, rows_per_part, N,
                        out);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+fo_status launch_colsum_finish_multi(const ColJobs& jobs, hipStream_t s) {
+    FO_CHECK(jobs.n >= 1 && jobs.n <= 4, "colsum: %d jobs", jobs.n);
+    int blocks = 0;
+    for (int i = 0; i < jobs.n; ++i) {
+        const ColJob& J = jobs.j[i];
+        FO_CHECK(J.part && J.N > 0 && J.rows_per_part > 0 && J.out.seg > 0 && cdiv(J.N, J.out.seg) <= 3,
+                 "colsum: bad job %d", i);
+        blocks += (int)cdiv(J.N, 64);
+    }
+    hipLaunchKernelGGL(colsum_finish_multi, dim3(blocks), dim3(256), 0, s, jobs);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+int colsum_rows_per_part() { return CS_ROWS; }
+
+fo_status launch_colsum_partial(const bf16_t* X, int64_t ld, int rows, const int* rows_dev, int N, float* ws,
+                                hipStream_t s) {
+    if (rows <= 0 || N <= 0) return FO_OK;
+    hipLaunchKernelGGL((colsum_partial<bf16_t>), dim3(cdiv(N, 64), cdiv(rows, CS_ROWS)), dim3(256), 0, s, X, ld,
+                       rows, rows_dev, N, ws);
     FO_LAUNCHED();
     return FO_OK;
 }

@@ -64,6 +64,25 @@ struct ColOut {
 // Adds partial rows part[p][N] over p < ceil(min(rows, *rows_dev) / rows_per_part), in order.
 fo_status launch_colsum_finish(const float* part, int rows, const int* rows_dev, int rows_per_part, int N,
                                const ColOut& out, hipStream_t s);
+// Several finishing passes in one launch: job i adds the partial rows of part_i
+// (as launch_colsum_finish) into out_i; at most four jobs.
+struct ColJob {
+    const float* part = nullptr;
+    int rows = 0, rows_per_part = 1, N = 0;
+    const int* rows_dev = nullptr;
+    ColOut out;
+};
+struct ColJobs {
+    ColJob j[4];
+    int n = 0;
+};
+fo_status launch_colsum_finish_multi(const ColJobs& jobs, hipStream_t s);
+// The first pass of launch_colsum alone: ws receives the partial rows (CS_ROWS
+// rows each) that launch_colsum_finish (rows_per_part = colsum_rows_per_part())
+// completes.
+fo_status launch_colsum_partial(const bf16_t* X, int64_t ld, int rows, const int* rows_dev, int N, float* ws,
+                                hipStream_t s);
+int colsum_rows_per_part();
 fo_status launch_fill(float* p, int64_t n, float v, hipStream_t s);
 // y = x w^T + bias (tanh when tanh_act) for x [B][I], w [O][I], I <= 768
 fo_status launch_small_linear_fwd(const float* x, const float* w, const float* bias, float* y, int B, int I, int O,

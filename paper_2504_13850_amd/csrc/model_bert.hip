@@ -587,17 +587,6 @@ fo_status ln_bwd(const SplitRows& dy, const float* u, const float* mean, const f
     FO_LAUNCHED();
     return FO_OK;
 }
-// dgamma, dbeta and the bias gradient of the sublayer below from ln_bwd's partials
-fo_status ln_bwd_finish(const float* part, const int* Tdev, int rows, float* dg, float* db, float* dbias_below,
-                        hipStream_t s) {
-    ColOut o;
-    o.p[0] = dg;
-    o.p[1] = db;
-    o.p[2] = dbias_below;
-    o.seg = D;
-    return launch_colsum_finish(part, rows, Tdev, LNB_ROWS, 3 * D, o, s);
-}
-
 fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     Plan* P = (Plan*)m->plan;
     hipStream_t s = m->stream;
@@ -797,15 +786,27 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         // norm gradients from their partials, then the weight gradients with
         // their SGD updates
         TRY(order_after(s2, s, P->ev_fork));
-        TRY(ln_bwd_finish(P->lnpart[pb][0], Mdev, M, grd + f.g2, grd + f.b2, grd + f.bf2, s2));
+        TRY(launch_colsum_partial(dqkv, 3 * D, rows, Tdev, 3 * D, P->colws2, s2));
         {
-            ColOut cb;
-            cb.p[0] = grd + f.bf1;
-            cb.seg = FF;
-            TRY(launch_colsum_finish(P->colwsF[pb], M, Mdev, 128, FF, cb, s2));
+            // one launch finishes LN2's dgamma / dbeta / dbias of FFN2, the FFN1 bias,
+            // LN1's dgamma / dbeta / dbias of the output projection and the QKV bias
+            ColJobs cj;
+            cj.n = 4;
+            auto ln_job = [&](ColJob& J, const float* part, float* dg, float* db, float* dbias) {
+                J.part = part; J.rows = M; J.rows_dev = Mdev; J.rows_per_part = LNB_ROWS; J.N = 3 * D;
+                J.out.p[0] = dg; J.out.p[1] = db; J.out.p[2] = dbias; J.out.seg = D;
+            };
+            ln_job(cj.j[0], P->lnpart[pb][0], grd + f.g2, grd + f.b2, grd + f.bf2);
+            ln_job(cj.j[1], P->lnpart[pb][1], grd + f.g1, grd + f.b1, grd + f.bo);
+            ColJob& jf = cj.j[2];
+            jf.part = P->colwsF[pb]; jf.rows = M; jf.rows_dev = Mdev; jf.rows_per_part = 128; jf.N = FF;
+            jf.out.p[0] = grd + f.bf1; jf.out.seg = FF;
+            ColJob& jq = cj.j[3];
+            jq.part = P->colws2; jq.rows = rows; jq.rows_dev = Tdev; jq.rows_per_part = colsum_rows_per_part();
+            jq.N = 3 * D;
+            jq.out.p[0] = grd + f.bqkv; jq.out.seg = 3 * D;
+            TRY(launch_colsum_finish_multi(cj, s2));
         }
-        TRY(ln_bwd_finish(P->lnpart[pb][1], Mdev, M, grd + f.g1, grd + f.b1, grd + f.bo, s2));
-        TRY(launch_colsum(dqkv, 3 * D, rows, Tdev, 3 * D, grd + f.bqkv, P->colws2, s2));
         if (cls) {  // over the B first-token rows (static count)
             TRY(wgrad(D, FF, du2b, t.G, f.w2, B, nullptr, 1));
             TRY(wgrad(FF, D, dA1, t.Hb, f.w1, B, nullptr, 1));
