@@ -136,11 +136,12 @@ __device__ __forceinline__ bf16x8_t ld8(const bf16_t* p, bool ok) {
 __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ qkvlo,
                                                         const int* __restrict__ cu, bf16_t* __restrict__ out,
                                                         bf16_t* __restrict__ outlo, float* __restrict__ lse, int H,
-                                                        int d, float scale, int* __restrict__ snap, int nb) {
+                                                        int d, float scale, int* __restrict__ snap, int nb,
+                                                        const int* __restrict__ order) {
     __shared__ __attribute__((aligned(16))) bf16_t Kh[LMAX * DH], Kl[LMAX * DH], Vh[LMAX * DH], Vl[LMAX * DH];
     if (snap && blockIdx.x == 0)
         for (int i = threadIdx.x; i <= nb; i += blockDim.x) snap[i] = cu[i];
-    const int b = blockIdx.x / H, h = blockIdx.x % H;
+    const int b = order ? order[blockIdx.x / H] : blockIdx.x / H, h = blockIdx.x % H;
     const int base = cu[b], len = cu[b + 1] - cu[b];
     const int64_t ld = 3 * d;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -250,12 +251,13 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const bf16_t* __restrict
 __global__ void __launch_bounds__(256) attn_bwd_mfma(const bf16_t* __restrict__ qkv, const int* __restrict__ cu,
                                                      const bf16_t* __restrict__ out, const bf16_t* __restrict__ dout,
                                                      const float* __restrict__ lse, bf16_t* __restrict__ dqkv, int H,
-                                                     int d, float scale, int* __restrict__ snap, int nb) {
+                                                     int d, float scale, int* __restrict__ snap, int nb,
+                                                     const int* __restrict__ order) {
     __shared__ __attribute__((aligned(16))) bf16_t Kr[LMAX * DH], Vr[LMAX * DH], Qr[LMAX * DH], Gr[LMAX * DH];
     __shared__ __attribute__((aligned(16))) bf16_t Pq[LMAX * LMAX], Dq[LMAX * LMAX];  // [query][key]
     if (snap && blockIdx.x == 0)
         for (int i = threadIdx.x; i <= nb; i += blockDim.x) snap[i] = cu[i];
-    const int b = blockIdx.x / H, h = blockIdx.x % H;
+    const int b = order ? order[blockIdx.x / H] : blockIdx.x / H, h = blockIdx.x % H;
     const int base = cu[b], len = cu[b + 1] - cu[b];
     const int64_t ld = 3 * d;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -534,7 +536,7 @@ __global__ void __launch_bounds__(128) attn_cls_bwd(const bf16_t* __restrict__ q
 }  // namespace
 
 fo_status launch_attn_fwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu, bf16_t* out, bf16_t* outlo,
-                          float* lse, int B, int H, int d, hipStream_t s) {
+                          float* lse, int B, int H, int d, hipStream_t s, const int* order) {
     FO_CHECK(d == H * DH, "attention: d=%d must equal heads*%d", d, DH);
     ProfInfo pi;
     pi.kind = PROF_ATTN_FWD; pi.cu = cu; pi.B = B; pi.d = d;
@@ -542,14 +544,14 @@ fo_status launch_attn_fwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu,
     const int h = prof_begin_ext("attn_fwd_mfma", pi, &ea, &eb);
     int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
     hipExtLaunchKernelGGL(attn_fwd_mfma, dim3(B * H), dim3(256), 0, s, ea, eb, 0, qkv, qkvlo, cu, out, outlo, lse, H,
-                          d, 1.f / sqrtf((float)DH), snap, B);
+                          d, 1.f / sqrtf((float)DH), snap, B, order);
     prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;
 }
 
 fo_status launch_attn_bwd(const bf16_t* qkv, const int* cu, const bf16_t* out, const bf16_t* dout,
-                          const float* lse, bf16_t* dqkv, int B, int H, int d, hipStream_t s) {
+                          const float* lse, bf16_t* dqkv, int B, int H, int d, hipStream_t s, const int* order) {
     FO_CHECK(d == H * DH, "attention: d=%d must equal heads*%d", d, DH);
     const float scale = 1.f / sqrtf((float)DH);
     ProfInfo pi;
@@ -558,7 +560,7 @@ fo_status launch_attn_bwd(const bf16_t* qkv, const int* cu, const bf16_t* out, c
     const int h = prof_begin_ext("attn_bwd_mfma", pi, &ea, &eb);
     int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
     hipExtLaunchKernelGGL(attn_bwd_mfma, dim3(B * H), dim3(256), 0, s, ea, eb, 0, qkv, cu, out, dout, lse, dqkv, H, d,
-                          scale, snap, B);
+                          scale, snap, B, order);
     prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;

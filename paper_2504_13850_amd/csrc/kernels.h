@@ -33,10 +33,13 @@ fo_status launch_cast_bf16(const float* x, bf16_t* y, bf16_t* ylo, int64_t n, hi
 // bf16 high and low parts of the output; lse fp32 [B][H][128] (natural log);
 // dout the bf16 output gradient, dqkv bf16 [T][3d].  The backward reads the
 // high parts only.
+// order (device, optional): the sequences in the order their workgroups are
+// launched, e.g. longest first so that short ones fill in behind long ones.
 fo_status launch_attn_fwd(const bf16_t* qkv, const bf16_t* qkvlo, const int* cu, bf16_t* out, bf16_t* outlo,
-                          float* lse, int B, int H, int d, hipStream_t s);
+                          float* lse, int B, int H, int d, hipStream_t s, const int* order = nullptr);
 fo_status launch_attn_bwd(const bf16_t* qkv, const int* cu, const bf16_t* out, const bf16_t* dout,
-                          const float* lse, bf16_t* dqkv, int B, int H, int d, hipStream_t s);
+                          const float* lse, bf16_t* dqkv, int B, int H, int d, hipStream_t s,
+                          const int* order = nullptr);
 // The same attention for the first token of each sequence only (the last
 // encoder layer, read at token 0 alone): out / outlo and lse are compact
 // ([B][d], [B][H]); the backward writes every row of dqkv (the query part of

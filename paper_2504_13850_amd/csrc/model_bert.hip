@@ -37,7 +37,7 @@ struct LayerAct {
 
 struct Plan {
     int rows;  // max_batch * L
-    int* cu;   // [max_batch + 2]; cu[B] = T, cu[B + 1] = B
+    int* cu;   // [2 max_batch + 2]; cu[B] = T, cu[B + 1] = B, then the sequences by decreasing length
     LayerOff off[NL];
     int64_t pool_w, pool_b, cls_w, cls_b;
     bf16_t* Xb[NL + 1];
@@ -79,6 +79,18 @@ __global__ void build_cu_kernel(const int32_t* __restrict__ lengths, int B, int 
     }
     cu[B] = acc;
     cu[B + 1] = B;  // the row count of the last layer's first-token rows
+    // cu[B + 2 ..]: the sequences by decreasing length (ties by index), the
+    // launch order of the attention workgroups
+    int* order = cu + B + 2;
+    for (int b = 0; b < B; ++b) {
+        const int lb = cu[b + 1] - cu[b];
+        int j = b;
+        while (j > 0 && cu[order[j - 1] + 1] - cu[order[j - 1]] < lb) {
+            order[j] = order[j - 1];
+            --j;
+        }
+        order[j] = b;
+    }
 }
 
 // padded [B][L][D] bf16 -> packed rows (bf16 and fp32 copies)
@@ -376,7 +388,7 @@ size_t ws_bytes(const fo_model* m) {
     size_t s = 0;
     auto add = [&](size_t b) { s += (b + 255) & ~size_t(255); };
     add(sizeof(Plan));
-    add(4 * (B + 2));
+    add(4 * (2 * B + 2));
     for (int l = 0; l <= NL; ++l) {
         add(2 * R * D);
         add(2 * R * D);
@@ -449,7 +461,7 @@ fo_status init(fo_model* m) {
     }
     Arena& a = m->arena;
     a.take<char>(sizeof(Plan));
-    P->cu = a.take<int>(B + 2);
+    P->cu = a.take<int>(2 * B + 2);
     for (int l = 0; l <= NL; ++l) {
         P->Xb[l] = a.take<bf16_t>(R * D);
         P->Xlo[l] = a.take<bf16_t>(R * D);
@@ -632,7 +644,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             hipLaunchKernelGGL(gather_cls_kernel, dim3(B), dim3(256), 0, s, P->Xf[l], P->cu, B, P->xres);
             FO_LAUNCHED();
         } else {
-            TRY(launch_attn_fwd(t.qkv, t.qkvlo, P->cu, t.O, t.Olo, t.lse, B, NH, D, s));
+            TRY(launch_attn_fwd(t.qkv, t.qkvlo, P->cu, t.O, t.Olo, t.lse, B, NH, D, s, P->cu + B + 2));
         }
         GemmDesc o = lin_fwd(M, t.O, t.Olo, D, W + f.wo, Wl + f.wo, D);
         o.Mdev = Mdev;
@@ -767,7 +779,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             FO_LAUNCHED();
             du1_full = P->dHf;
         } else {
-            TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, dqkv, B, NH, D, s));
+            TRY(launch_attn_bwd(t.qkv, P->cu, t.O, P->dO, t.lse, dqkv, B, NH, D, s, P->cu + B + 2));
         }
         // input projection: dX = du1 + dqkv Wqkv (skipped for the first server layer), dbqkv
         if (l > 0) {
