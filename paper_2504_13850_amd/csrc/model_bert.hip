@@ -68,28 +68,33 @@ struct Plan {
 };
 
 // ------------------------------------------------------------------ kernels
-__global__ void build_cu_kernel(const int32_t* __restrict__ lengths, int B, int Lmax, int* __restrict__ cu) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    int acc = 0;
-    for (int b = 0; b < B; ++b) {
-        int len = lengths[b];
-        len = len < 1 ? 1 : (len > Lmax ? Lmax : len);
-        cu[b] = acc;
-        acc += len;
+// Packed offsets cu[0..B] (cu[B] = T), cu[B + 1] = B, and from cu + B + 2 the
+// sequences by decreasing length (ties by index): the launch order of the
+// attention workgroups.  The clamped lengths go to LDS (dynamic, B ints); a
+// thread per sequence computes its rank, one thread the prefix sum.
+__global__ void __launch_bounds__(256) build_cu_kernel(const int32_t* __restrict__ lengths, int B, int Lmax,
+                                                       int* __restrict__ cu) {
+    extern __shared__ int lens[];
+    for (int b = threadIdx.x; b < B; b += blockDim.x) {
+        const int len = lengths[b];
+        lens[b] = len < 1 ? 1 : (len > Lmax ? Lmax : len);
     }
-    cu[B] = acc;
-    cu[B + 1] = B;  // the row count of the last layer's first-token rows
-    // cu[B + 2 ..]: the sequences by decreasing length (ties by index), the
-    // launch order of the attention workgroups
-    int* order = cu + B + 2;
-    for (int b = 0; b < B; ++b) {
-        const int lb = cu[b + 1] - cu[b];
-        int j = b;
-        while (j > 0 && cu[order[j - 1] + 1] - cu[order[j - 1]] < lb) {
-            order[j] = order[j - 1];
-            --j;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int acc = 0;
+        for (int b = 0; b < B; ++b) {
+            cu[b] = acc;
+            acc += lens[b];
         }
-        order[j] = b;
+        cu[B] = acc;
+        cu[B + 1] = B;  // the row count of the last layer's first-token rows
+    }
+    int* order = cu + B + 2;
+    for (int b = threadIdx.x; b < B; b += blockDim.x) {
+        const int lb = lens[b];
+        int rank = 0;
+        for (int c = 0; c < B; ++c) rank += lens[c] > lb || (lens[c] == lb && c < b);
+        order[rank] = b;
     }
 }
 
@@ -609,7 +614,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     const float* prm = m->params;
     float* grd = m->grads;
 
-    hipLaunchKernelGGL(build_cu_kernel, dim3(1), dim3(64), 0, s, acts->lengths, B, L, P->cu);
+    hipLaunchKernelGGL(build_cu_kernel, dim3(1), dim3(256), sizeof(int) * B, s, acts->lengths, B, L, P->cu);
     {
         int64_t total = (int64_t)rows * (D / 8);
         int grid = (int)std::min<int64_t>(cdiv(total, 256), 8192);
