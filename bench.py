@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench with "
                          "--calib-copy into the HBM traffic summary (JSON on stdout)")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="CSV",
+                    help="turn rocprofv3 --pmc runs of this bench (MFMA and L2 counters, any number of "
+                         "passes) into a per-kernel table (Markdown on stdout)")
     return ap.parse_args()
 
 
@@ -146,6 +149,72 @@ def summarize_pmc(fetch_csv, write_csv):
                       "bytes_per_launch": round(rd + wr), "source_sha256": source_hash(files)}
     out["kernels"] = kern
     return out
+
+
+def summarize_counters(paths, top=12):
+    """Per-kernel averages of rocprofv3 --pmc counter passes over this bench.
+
+    Executed MFMA work is SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP (the unit the
+    counter counts in; it reproduces 2*M*N*K per pass of each product).  L2
+    requests are TCC_HIT + TCC_MISS (64-byte requests for these kernels).
+    Busy fractions divide by the dispatch's GRBM_GUI_ACTIVE / 8 (that counter
+    sums the eight XCDs) and by the unit count: 128 L2 channels, 256 CUs for
+    the texture address (TA) and data (TD) units."""
+    import csv
+    from collections import defaultdict
+    disp = defaultdict(dict)  # (path, dispatch) -> counters
+    info = {}
+    for path in paths:
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                key = (path, r["Dispatch_Id"])
+                c = disp[key]
+                c[r["Counter_Name"]] = c.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+                name = r["Kernel_Name"].replace("void ", "").replace("fo::(anonymous namespace)::", "")
+                name = name.split("(fo::")[0].split("(unsigned")[0].split("(float")[0].split("(int")[0]
+                info[key] = (name, (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    per = defaultdict(lambda: defaultdict(list))
+    calls = defaultdict(lambda: defaultdict(int))  # dispatches per pass
+    for key, c in disp.items():
+        name, dur = info[key]
+        if "at::native" in name or "__amd_rocclr" in name:  # the bench's own setup and copies
+            continue
+        calls[name][key[0]] += 1
+        per[name]["dur"].append(dur)
+        for k, v in c.items():
+            per[name][k].append(v)
+    mean = lambda xs: sum(xs) / len(xs) if xs else float("nan")
+    rows = []
+    for name, c in per.items():
+        d = mean(c["dur"])
+        cyc = {k: mean(v) / 8 for k, v in c.items() if k == "GRBM_GUI_ACTIVE"}.get("GRBM_GUI_ACTIVE")
+        g = lambda k: mean(c[k]) if c.get(k) else None
+        flop = g("SQ_INSTS_VALU_MFMA_MOPS_BF16")
+        hit, miss = g("TCC_HIT"), g("TCC_MISS")
+        frac = lambda k, units: (g(k) / units / cyc) if (g(k) is not None and cyc) else None
+        n = max(calls[name].values())
+        rows.append((d * n, name, {
+            "dispatches": n, "avg_us": d * 1e6,
+            "exec_tflops": flop * 512 / d / 1e12 if flop else None,
+            "pct_peak": 100 * flop * 512 / d / 1e12 / PEAK_BF16_TFLOPS if flop else None,
+            "l2_req": (hit + miss) if hit is not None else None,
+            "l2_hit": hit / (hit + miss) if hit is not None and hit + miss > 0 else None,
+            "l2_gbs": (hit + miss) * 64 / d / 1e9 if hit is not None else None,
+            "l2_busy": frac("TCC_BUSY", 128), "td_busy": frac("TD_TD_BUSY", 256),
+            "td_wait_l2": frac("TD_TC_STALL", 256), "ta_busy": frac("TA_TA_BUSY", 256)}))
+    rows.sort(key=lambda r: -r[0])
+    cols = [("dispatches", "dispatches per pass", "{:.0f}"), ("avg_us", "avg us", "{:.1f}"),
+            ("exec_tflops", "MFMA TFLOP/s executed", "{:.0f}"), ("pct_peak", "% of bf16 peak", "{:.1f}"),
+            ("l2_req", "L2 requests", "{:.3g}"), ("l2_hit", "L2 hit", "{:.2f}"),
+            ("l2_gbs", "L2 GB/s (64 B req.)", "{:.0f}"), ("l2_busy", "L2 busy", "{:.2f}"),
+            ("td_busy", "TD busy", "{:.2f}"), ("td_wait_l2", "TD waits on L2", "{:.2f}"),
+            ("ta_busy", "TA busy", "{:.2f}")]
+    out = ["| kernel | " + " | ".join(h for _, h, _ in cols) + " |",
+           "|---|" + "---:|" * len(cols)]
+    for _, name, v in rows[:top]:
+        cells = [("-" if v[k] is None else f.format(v[k])) for k, _, f in cols]
+        out.append(f"| `{name}` | " + " | ".join(cells) + " |")
+    return "\n".join(out)
 
 
 def traffic_for(name):
@@ -383,6 +452,9 @@ def main():
     args = parse()
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc), indent=1))
+        return
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters))
         return
     if args.gpus != 1:
         sys.stderr.write("bench.py measures one GPU only: this build has no multi-GPU path "
