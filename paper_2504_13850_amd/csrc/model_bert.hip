@@ -183,8 +183,9 @@ __device__ __forceinline__ void load_split_row(const SplitRows& src, int S, int 
         case 2: split_row<2>(src, row, lane, x); break;
         case 3: split_row<3>(src, row, lane, x); break;
         case 4: split_row<4>(src, row, lane, x); break;
+        case 8: split_row<8>(src, row, lane, x); break;  // the last layer's first-token products
         case 1: split_row<1>(src, row, lane, x); break;
-        default: {  // not used here (the products feeding a LayerNorm split at most 4 ways)
+        default: {  // other slice counts: loads issued four at a time
             const int64_t full = (int64_t)src.M * D;
             const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
