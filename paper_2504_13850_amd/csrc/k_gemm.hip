@@ -515,11 +515,11 @@ __device__ __forceinline__ float gelu_and_grad(float x, float* grad) {
 }
 
 // The epilogue in two halves: epi_load fetches the per-element operands
-// (residual, ReLU mask, GELU input, the weight a fused SGD updates), epi_store
-// applies activation, mask and GELU' and stores, so that a thread can issue
-// the loads of several rows before it needs any of them.
+// (residual, ReLU mask, GELU input), epi_store applies activation, mask and
+// GELU' and stores, so that a thread can issue the loads of several rows
+// before it needs any of them.
 struct EpiIn {
-    float resid = 0.f, mask = 1.f, dact = 1.f, theta = 0.f;
+    float resid = 0.f, mask = 1.f, dact = 1.f;
 };
 
 __device__ __forceinline__ EpiIn epi_load(const GemmDesc& d, int row, int col) {
@@ -527,7 +527,6 @@ __device__ __forceinline__ EpiIn epi_load(const GemmDesc& d, int row, int col) {
     if (d.resid) e.resid = d.resid[(int64_t)row * d.ldr + col];
     if (d.mask) e.mask = bf2f(d.mask[(int64_t)row * d.ldm + col]);
     if (d.dact) e.dact = bf2f(d.dact[(int64_t)row * d.ldm + col]);
-    if (d.sgd_theta) e.theta = d.sgd_theta[(int64_t)row * d.ldcf + col];
     return e;
 }
 
@@ -549,7 +548,7 @@ __device__ __forceinline__ float epi_store(const GemmDesc& d, int row, int col, 
     if (d.Cf) d.Cf[(int64_t)row * d.ldcf + col] = v;
     if (d.sgd_theta) {
         const int64_t o = (int64_t)row * d.ldcf + col;
-        const float th = __builtin_fmaf(-d.sgd_lr, v, e.theta);
+        const float th = __builtin_fmaf(-d.sgd_lr, v, d.sgd_theta[o]);
         d.sgd_theta[o] = th;
         const bf16_t h = f2bf(th);
         d.sgd_hi[o] = h;
@@ -597,7 +596,6 @@ __device__ __forceinline__ u32x2 f_to_bf4(f32x4 v, f32x4* lo) {
 
 struct EpiIn4 {
     f32x4 resid = {0.f, 0.f, 0.f, 0.f}, mask = {1.f, 1.f, 1.f, 1.f}, dact = {1.f, 1.f, 1.f, 1.f};
-    f32x4 theta = {0.f, 0.f, 0.f, 0.f};
 };
 
 __device__ __forceinline__ EpiIn4 epi_load4(const GemmDesc& d, int row, int col) {
@@ -605,7 +603,6 @@ __device__ __forceinline__ EpiIn4 epi_load4(const GemmDesc& d, int row, int col)
     if (d.resid) e.resid = *reinterpret_cast<const f32x4*>(d.resid + (int64_t)row * d.ldr + col);
     if (d.mask) e.mask = bf4_to_f(*reinterpret_cast<const u32x2*>(d.mask + (int64_t)row * d.ldm + col));
     if (d.dact) e.dact = bf4_to_f(*reinterpret_cast<const u32x2*>(d.dact + (int64_t)row * d.ldm + col));
-    if (d.sgd_theta) e.theta = *reinterpret_cast<const f32x4*>(d.sgd_theta + (int64_t)row * d.ldcf + col);
     return e;
 }
 
@@ -638,7 +635,7 @@ __device__ __forceinline__ f32x4 epi_store4(const GemmDesc& d, int row, int col,
     if (d.Cf) *reinterpret_cast<f32x4*>(d.Cf + (int64_t)row * d.ldcf + col) = v;
     if (d.sgd_theta) {
         const int64_t o = (int64_t)row * d.ldcf + col;
-        f32x4 th = e.theta, lo;
+        f32x4 th = *reinterpret_cast<const f32x4*>(d.sgd_theta + o), lo;
 #pragma unroll
         for (int q = 0; q < 4; ++q) th[q] = __builtin_fmaf(-d.sgd_lr, v[q], th[q]);
         *reinterpret_cast<f32x4*>(d.sgd_theta + o) = th;
@@ -1152,9 +1149,6 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
         const int64_t total4 = (int64_t)M * d.N / 4;
         for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total4; i += stride) {
             const float* p = d.ws + 4 * i;
-            const int row = (int)(4 * i / d.N), col = (int)(4 * i % d.N);
-            // (the epilogue operands are requested together with the partials)
-            const EpiIn4 e = d.vec_epi ? epi_load4(d, row, col) : EpiIn4();
             f32x4 v = *reinterpret_cast<const f32x4*>(p);
             int z = 1;
             for (; z + 3 < S; z += 4) {
@@ -1165,12 +1159,14 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
                 v += (a + b) + (e + f);
             }
             for (; z < S; ++z) v += *reinterpret_cast<const f32x4*>(p + z * full);
+            const int row = (int)(4 * i / d.N), col = (int)(4 * i % d.N);
             if (d.vec_epi) {
                 f32x4 bias = {0.f, 0.f, 0.f, 0.f};
                 if (d.bias) {
 #pragma unroll
                     for (int q = 0; q < 4; ++q) bias[q] = d.bias[col + q];
                 }
+                const EpiIn4 e = epi_load4(d, row, col);
                 epi_store4(d, row, col, v + bias + e.resid, e);
             } else {
 #pragma unroll
