@@ -217,6 +217,19 @@ def summarize_counters(paths, top=12):
     return "\n".join(out)
 
 
+def padded_bert_flops(B, L, d=768, ff=3072, layers=10, classes=2):
+    """Training FLOPs of the transformer step with every sequence padded to L
+    tokens and no first-token pruning: per layer the forward products
+    2 L (3 d d + d d + 2 d ff) and attention 4 d L^2 per sequence, times three
+    for forward, input and weight gradients, less the first layer's input
+    gradient (2 L 3 d d); plus the pooler and classifier (forward and both
+    gradients)."""
+    fwd_layer = 2 * L * (3 * d * d + d * d + 2 * d * ff) + 4 * d * L * L
+    per_seq = layers * 3 * fwd_layer - 2 * L * 3 * d * d
+    head = 3 * 2 * (d * d + d * classes)
+    return B * (per_seq + head)
+
+
 def traffic_for(name):
     """HBM bytes per launch from the committed counter summary, or None when it
     is missing or the kernel's source changed since the counters were taken."""
@@ -589,6 +602,10 @@ def main():
     config = {"workload": wl["workload"], "global_batch": B, "parallelism": "single-gpu"}
     if bert:
         config["seq_len"] = cfg.in_shape[0]
+    if bert:  # every sequence at its full 128 tokens: the work a padded run would do (context only)
+        out_extra = {"padded_dense_tflop_per_step": round(padded_bert_flops(B, cfg.in_shape[0]) / 1e12, 4)}
+    else:
+        out_extra = {}
     out = {
         "metric": "server train samples/s + % bf16 MFMA peak; async-aggregate HBM GB/s",
         "value": round(samples_s, 2),
@@ -607,6 +624,7 @@ def main():
         "mfu_peak_tflops": peak,
         "useful_tflop_per_step": round(flops_step / 1e12, 6),
         "mfma_tflop_per_step_executed": round(mfma_flops / args.steps / 1e12, 4),
+        **out_extra,
         "roofline": roofline,
         "aggregate": agg,
         "kernels": kernels[:12],

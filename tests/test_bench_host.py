@@ -89,3 +89,15 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_padded_dense_count():
+    # the padded-dense transformer step: 1.773 TFLOP at B = 32, L = 128 (every
+    # sequence full, no first-token pruning), and it scales linearly in B
+    f = bench.padded_bert_flops(32, 128)
+    assert f == pytest.approx(1.7734e12, rel=1e-4)
+    assert bench.padded_bert_flops(64, 128) == 2 * f
+    # one layer's forward matmuls alone: 24 d^2 L per sequence (ffn = 4 d)
+    d, L = 768, 128
+    one = bench.padded_bert_flops(1, L, layers=1) - 3 * 2 * (d * d + 2 * d) + 2 * L * 3 * d * d
+    assert one == 3 * (24 * d * d * L + 4 * d * L * L)
