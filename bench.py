@@ -46,7 +46,8 @@ def parse():
     ap.add_argument("--config", type=int, default=4, help="1-3: the parity workloads' step loops; 4: "
                     "transformer (default); 5: 128-device VGG with Poisson arrivals")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-steps", type=int, default=8)
+    ap.add_argument("--cpu-sample-steps", type=int, default=3,
+                    help="fp32 oracle steps at the workload's own batch timed for cpu_baseline")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a 1 GiB device-to-device copy (the HBM counter calibration kernel)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -67,18 +68,23 @@ def cpu_baseline(cid, sample_steps):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
     except Exception:  # pragma: no cover
         cores = os.cpu_count() or 1
-    Bs = 4
+    Bs = S.get_config(cid).batch  # the headline workload's own batch
     theta = S.init_params(cid)
     acts = S.make_acts(cid, sample_steps, batch=Bs, sub=99)
     labels = S.make_labels(cid, sample_steps, batch=Bs, sub=99)
     lengths = S.make_lengths(cid, sample_steps, batch=Bs, sub=99) if cid == 4 else [None] * sample_steps
     t0 = time.perf_counter()
+    cfg = S.get_config(cid)
+    mom = None
     for i in range(sample_steps):
-        r = oracle.server_step(cid, theta, acts[i], labels[i], lengths[i], dt=np.float32)
+        r = oracle.server_step(cid, theta, acts[i], labels[i], lengths[i], lr=cfg.lr, momentum=cfg.momentum,
+                               mom_buf=mom, dt=np.float32)
         theta = r["params"].astype(np.float32)
+        mom = r["momentum"]
     dt = time.perf_counter() - t0
     return {"value": round(Bs * sample_steps / dt, 3), "unit": "samples/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{sample_steps} fp32 oracle steps at batch {Bs} of the same workload ({dt:.1f} s)"}
+            "sample": f"{sample_steps} consecutive fp32 oracle steps at batch {Bs} (the workload's batch) "
+                      f"on fresh seeded batches of the same workload ({dt:.1f} s)"}
 
 
 # ---------------------------------------------------------------- HBM traffic
@@ -95,6 +101,11 @@ TRAFFIC_KERNELS = {
     "agg_lerp_kernel": ("agg_lerp_kernel(", ["paper_2504_13850_amd/csrc/k_update.hip"]),
 }
 CALIB_BYTES = 1 << 30
+# `traffic` is not measured by this run: it is read from the committed summary
+# of two rocprofv3 counter passes, and only while the kernel's sources still
+# hash to what they were when the counters were taken (else null).
+TRAFFIC_SOURCE = ("stored rocprofv3 FETCH_SIZE + WRITE_SIZE per launch from profiles/hbm_traffic_bert_step.txt "
+                  "(null when the kernel's sources changed since)")
 
 
 def source_hash(files):
@@ -579,7 +590,8 @@ def main():
         dom_tflops = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
         roofline = {"bound": "mfma", "kernel": dom["name"], "achieved": round(dom_tflops, 1), "peak": peak,
                     "unit": "TFLOP/s", "frac": round(dom_tflops / peak, 4), "launches": dom["launches"],
-                    "avg_launch_us": round(dom["ms"] / dom["launches"] * 1e3, 2), "traffic": traffic_for(dom["name"])}
+                    "avg_launch_us": round(dom["ms"] / dom["launches"] * 1e3, 2), "traffic": traffic_for(dom["name"]),
+                    "traffic_source": TRAFFIC_SOURCE}
     else:  # the fp32 direct-convolution CNN: the whole step against the fp32 vector peak
         roofline = {"bound": "alu", "kernel": "whole step (fp32 direct convolutions, not instrumented)",
                     "achieved": round(flops_step / (ms_step * 1e-3) / 1e12, 3), "peak": peak, "unit": "TFLOP/s",
@@ -591,6 +603,7 @@ def main():
     agg = bench_aggregate(A, torch, stream)
     t_agg = traffic_for("agg_lerp_kernel")
     agg["traffic"] = t_agg
+    agg["traffic_source"] = TRAFFIC_SOURCE
     agg["traffic_frac_of_algorithmic"] = round(t_agg / agg["bytes_per_call"], 4) if t_agg else None
     if args.calib_copy:
         calib_copy(torch)

@@ -111,8 +111,21 @@ FO_API void fo_model_destroy(fo_model* model);
  * of class ids in [0, classes).  `device_id` (>= 0) names the device the batch
  * came from and is counted per device (fo_model_steps).  Asynchronous on the
  * model's stream; loss and logits of this step stay readable until the next
- * step.  Errors: FO_EINVAL (NULL pointers, batch out of range, lengths
- * missing for config 4, device_id < 0), FO_EHIP. */
+ * step.
+ * Batches from a pool: when acts->x or labels lie in the slot memory of a live
+ * fo_queues pool, they must be that pool's batch in service (its activations,
+ * labels and lengths, from fo_queues_in_service) and device_id must be the
+ * device its last fo_pick_device returned.  If the model's stream is not the
+ * pool's, the step waits for the work queued on the pool's stream (the copies
+ * into the slot), and the slot's next reuse waits for the step, so the two
+ * streams need no other synchronisation.
+ * Labels outside [0, classes) and lengths outside [1, L] cannot be checked on
+ * the host without a synchronisation: the kernels clamp them (every access
+ * stays in bounds) and count them, and the next fo_model_read of LOSS or
+ * LOGITS returns FO_EINVAL.
+ * Errors: FO_EINVAL (NULL pointers, batch out of range, lengths missing for
+ * config 4, device_id < 0, a pool batch that is not the one in service or a
+ * device_id other than its pick's), FO_EHIP. */
 FO_API fo_status fo_server_step(fo_model* model, const fo_acts* acts, const int32_t* labels,
                          int32_t device_id);
 
@@ -143,7 +156,9 @@ FO_API int64_t fo_model_buffer_size(const fo_model* model, int32_t which);
 /* Synchronous copies between a model buffer and host memory (host_out/host_in
  * hold n fp32 values; n must equal fo_model_buffer_size, except LOGITS where
  * n = batch * classes of the last step).  Used for parity checks and for
- * checkpoint / resume.  Errors: FO_EINVAL, FO_ESTATE (no step yet), FO_EHIP. */
+ * checkpoint / resume.  Errors: FO_EINVAL (also, after copying, for LOSS and
+ * LOGITS of a step whose labels or lengths were out of range), FO_ESTATE (no
+ * step yet), FO_EHIP. */
 FO_API fo_status fo_model_read(fo_model* model, int32_t which, float* host_out, int64_t n);
 FO_API fo_status fo_model_write(fo_model* model, int32_t which, const float* host_in, int64_t n);
 
@@ -187,6 +202,8 @@ FO_API fo_status fo_set_max_delay(int64_t max_delay);
  * Errors: FO_EINVAL (K < 1, n_slots <= K, batch < 1), FO_ENOMEM, FO_EHIP. */
 FO_API fo_status fo_queues_create(int32_t K, int64_t slot_bytes, int32_t batch, int32_t with_lengths,
                            int64_t n_slots, void* hip_stream, fo_queues** out);
+/* Waits for the pool's stream (and for steps that read its slots from other
+ * streams), then frees the pool. */
 FO_API void fo_queues_destroy(fo_queues* q);
 
 /* put() for an activation batch from device k (Alg. 2).  x_src holds
@@ -216,16 +233,20 @@ FO_API int32_t fo_pick_device(fo_queues* q);
  * until fo_queues_release) plus its per-device sequence number and slot id. */
 FO_API fo_status fo_queues_in_service(fo_queues* q, fo_acts* acts_out, const int32_t** labels_out,
                                int64_t* seq_out, int64_t* slot_out);
-/* Returns the in-service slot to the free stack.  Later pushes reuse it with
- * copies ordered after the work already queued on the pool's stream, so call
- * this after fo_server_step has been enqueued on the same stream. */
+/* Returns the in-service slot to the free stack.  Call it after the
+ * fo_server_step calls on that batch have been enqueued: later pushes reuse the
+ * slot with copies ordered after them (by stream order when the model runs on
+ * the pool's stream, else by an event the step recorded on the model's
+ * stream). */
 FO_API fo_status fo_queues_release(fo_queues* q);
 
 /* Serves the oldest pending model message (Alg. 4, aggregation branch):
  * staleness s = t - t_k; if s > D it is dropped (FO_SKIPPED, t unchanged);
  * otherwise global is mixed with fo_async_aggregate's rule and t <- t + 1.
  * k_out / staleness_out (may be NULL) report the message.  FO_EMPTY if no
- * model is pending.  Runs on the pool's stream. */
+ * model is pending.  On an error (FO_EINVAL: length mismatch, misaligned
+ * vector, t_k > t; FO_EHIP) the message stays at the head of the FIFO and t is
+ * unchanged.  Runs on the pool's stream. */
 FO_API fo_status fo_aggregate_pending(fo_queues* q, fo_vec* global, float alpha, int32_t* k_out,
                                int64_t* staleness_out);
 
@@ -234,7 +255,10 @@ FO_API fo_status fo_aggregate_pending(fo_queues* q, fo_vec* global, float alpha,
  * (global read and written once per 64 messages), in FIFO order, so the
  * result equals the same sequence of fo_aggregate_pending calls bit for bit.
  * Stale messages are dropped as above and do not advance t.  applied_out /
- * skipped_out may be NULL.  Runs on the pool's stream. */
+ * skipped_out may be NULL.  The whole FIFO is validated before anything is
+ * launched; if a launch fails, the FIFO and t have advanced past exactly the
+ * messages whose launches were enqueued (reported in applied_out /
+ * skipped_out).  Runs on the pool's stream. */
 FO_API fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, float alpha, int32_t* applied_out,
                                    int32_t* skipped_out);
 

@@ -7,6 +7,7 @@
 #include <new>
 
 #include "model.h"
+#include "pool.h"
 #include "prof.h"
 
 namespace fo {
@@ -116,6 +117,7 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
     fo_status st = FO_OK;
     e = hipMemcpyAsync(m->params, host_init, sizeof(float) * np, hipMemcpyHostToDevice, m->stream);
     if (e == hipSuccess) e = hipMemsetAsync(m->grads, 0, sizeof(float) * np, m->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(m->loss, 0, sizeof(float) * 64, m->stream);
     if (e == hipSuccess && m->mom) e = hipMemsetAsync(m->mom, 0, sizeof(float) * np, m->stream);
     if (e != hipSuccess) {
         set_error("fo_model_create: upload: %s", hipGetErrorString(e));
@@ -231,9 +233,17 @@ extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int3
     FO_CHECK(device_id >= 0, "fo_server_step: device_id=%d must be >= 0", device_id);
     FO_CHECK(m->cid != 4 || acts->lengths != nullptr, "fo_server_step: config 4 needs sequence lengths");
     FO_CHECK(((uintptr_t)acts->x % 16) == 0, "fo_server_step: activations not 16-byte aligned");
-    // Kernel profiling records every launch with its own events: run eagerly then.
-    fo_status st = (g_graph_mode && !prof_active()) ? step_graph(m, acts, labels) : m->fam->step(m, acts, labels);
+    // A batch taken from a pool must be the one its last pick put in service.
+    fo_queues* owner = nullptr;
+    fo_status st = pool_step_begin(acts, labels, device_id, m->stream, &owner);
     if (st != FO_OK) return st;
+    // Kernel profiling records every launch with its own events: run eagerly then.
+    st = (g_graph_mode && !prof_active()) ? step_graph(m, acts, labels) : m->fam->step(m, acts, labels);
+    if (st != FO_OK) return st;
+    if (owner) {
+        st = pool_step_done(owner, m->stream);
+        if (st != FO_OK) return st;
+    }
     m->last_batch = acts->batch;
     m->steps_total++;
     if ((size_t)device_id >= m->steps_per_device.size()) m->steps_per_device.resize(device_id + 1, 0);
@@ -280,7 +290,16 @@ extern "C" fo_status fo_model_read(fo_model* m, int32_t which, float* host_out, 
     FO_CHECK(n == fo_model_buffer_size(m, which), "fo_model_read: n=%lld, buffer holds %lld", (long long)n,
              (long long)fo_model_buffer_size(m, which));
     FO_HIP(hipMemcpyAsync(host_out, p, sizeof(float) * n, hipMemcpyDeviceToHost, m->stream));
+    float flags[2] = {0.f, 0.f};  // labels / lengths out of range in the last step (clamped by the kernels)
+    if (which == FO_BUF_LOSS || which == FO_BUF_LOGITS)
+        FO_HIP(hipMemcpyAsync(flags, m->loss + 1, sizeof(flags), hipMemcpyDeviceToHost, m->stream));
     FO_HIP(hipStreamSynchronize(m->stream));
+    if (flags[0] != 0.f || flags[1] != 0.f) {
+        set_error("fo_model_read: the last step had %d label(s) outside [0,%d) and %d sequence length(s) outside "
+                  "[1,L]; they were clamped, so its loss and logits are not those of the batch as sent",
+                  (int)flags[0], m->classes, (int)flags[1]);
+        return FO_EINVAL;
+    }
     return FO_OK;
 }
 

@@ -11,6 +11,9 @@ namespace {
 __global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, const int32_t* __restrict__ labels,
                                                    float* __restrict__ dz, float* __restrict__ loss, int B, int C) {
     __shared__ float part[256];
+    __shared__ int bad;
+    if (threadIdx.x == 0) bad = 0;
+    __syncthreads();
     float mine = 0.f;
     for (int b = threadIdx.x; b < B; b += blockDim.x) {
         const float* zr = z + (int64_t)b * C;
@@ -20,7 +23,10 @@ __global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, 
         for (int c = 0; c < C; ++c) s += expf(zr[c] - m);
         float lse = m + logf(s);
         int y = labels[b];
-        y = y < 0 ? 0 : (y >= C ? C - 1 : y);
+        if (y < 0 || y >= C) {  // reported through loss[1]; clamped so that every access stays in bounds
+            atomicAdd(&bad, 1);
+            y = y < 0 ? 0 : C - 1;
+        }
         mine += lse - zr[y];
         for (int c = 0; c < C; ++c) dz[(int64_t)b * C + c] = (expf(zr[c] - lse) - (c == y ? 1.f : 0.f)) / (float)B;
     }
@@ -30,7 +36,10 @@ __global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, 
         if (threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
         __syncthreads();
     }
-    if (threadIdx.x == 0) loss[0] = part[0] / (float)B;
+    if (threadIdx.x == 0) {
+        loss[0] = part[0] / (float)B;
+        loss[1] = (float)bad;
+    }
 }
 
 // Column sums of a [rows][N] matrix in two passes.  colsum_partial: a block

@@ -51,7 +51,9 @@ fo_status launch_attn_cls_bwd(const bf16_t* qkv, const bf16_t* qkvlo, const int*
                               int d, hipStream_t s);
 
 // ------------------------------------------------------------------ k_common.hip
-// mean cross-entropy of logits z [B][C] and dz = (softmax - onehot)/B
+// mean cross-entropy of logits z [B][C] and dz = (softmax - onehot)/B into
+// loss[0]; loss[1] receives the number of labels outside [0, C) (each clamped
+// to the nearest class so that every access stays in bounds)
 fo_status launch_xent(const float* z, const int32_t* labels, float* dz, float* loss, int B, int C, hipStream_t s);
 // out[c] = sum over rows r < min(rows, *rows_dev) of X[r*ld + c]; ws holds colsum_ws_floats(rows, N)
 size_t colsum_ws_floats(int rows, int N);

@@ -72,14 +72,21 @@ struct Plan {
 // sequences by decreasing length (ties by index): the launch order of the
 // attention workgroups.  The clamped lengths go to LDS (dynamic, B ints); a
 // thread per sequence computes its rank, one thread the prefix sum.
+// Lengths outside [1, Lmax] are clamped (every access then stays in bounds)
+// and counted into *bad_out.
 __global__ void __launch_bounds__(256) build_cu_kernel(const int32_t* __restrict__ lengths, int B, int Lmax,
-                                                       int* __restrict__ cu) {
+                                                       int* __restrict__ cu, float* __restrict__ bad_out) {
     extern __shared__ int lens[];
+    __shared__ int bad;
+    if (threadIdx.x == 0) bad = 0;
+    __syncthreads();
     for (int b = threadIdx.x; b < B; b += blockDim.x) {
         const int len = lengths[b];
+        if (len < 1 || len > Lmax) atomicAdd(&bad, 1);
         lens[b] = len < 1 ? 1 : (len > Lmax ? Lmax : len);
     }
     __syncthreads();
+    if (threadIdx.x == 0) *bad_out = (float)bad;
     if (threadIdx.x == 0) {
         int acc = 0;
         for (int b = 0; b < B; ++b) {
@@ -615,7 +622,8 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     const float* prm = m->params;
     float* grd = m->grads;
 
-    hipLaunchKernelGGL(build_cu_kernel, dim3(1), dim3(256), sizeof(int) * B, s, acts->lengths, B, L, P->cu);
+    hipLaunchKernelGGL(build_cu_kernel, dim3(1), dim3(256), sizeof(int) * B, s, acts->lengths, B, L, P->cu,
+                       m->loss + 2);
     {
         int64_t total = (int64_t)rows * (D / 8);
         int grid = (int)std::min<int64_t>(cdiv(total, 256), 8192);

@@ -4,11 +4,20 @@
 // All state is host-side and O(K); the only device work is the copy of an
 // admitted batch into its preallocated slot and the aggregation kernels,
 // both ordered on the pool's stream.
+//
+// Live pools are kept in a registry so that a training step whose batch lies
+// in a pool slot can be checked against that pool's last pick, and so that a
+// step enqueued on a stream other than the pool's is ordered before the
+// slot's next reuse (an event recorded after the step, waited for by the
+// pool's stream before its next copy into that slot).
 #include <atomic>
 #include <deque>
+#include <mutex>
+#include <unordered_map>
 #include <vector>
 
 #include "kernels.h"
+#include "pool.h"
 
 namespace fo {
 std::atomic<int64_t> g_max_delay{-1};
@@ -40,12 +49,34 @@ struct fo_queues {
 
     int64_t t = 0, queued = 0, admitted = 0, refused = 0, picks = 0, peak = 0;
 
+    // Slot reuse across streams: svc_ev is recorded after a step that read the
+    // batch in service from another stream; on release it guards that slot,
+    // and the next push into the slot makes the pool's stream wait for it.
+    hipEvent_t svc_ev = nullptr;
+    hipEvent_t ready_ev = nullptr;  // the other direction: the step waits for the copies into its slot
+    std::unordered_map<int64_t, hipEvent_t> guard;
+    std::vector<hipEvent_t> ev_free;
+
+    bool in_slab(const void* p) const {
+        const char* c = (const char*)p;
+        return slab && c >= slab && c < slab + slot_bytes * n_slots;
+    }
+    bool in_labels(const void* p) const {
+        const int32_t* c = (const int32_t*)p;
+        return labels && c >= labels && c < labels + (int64_t)batch * n_slots;
+    }
+
     void turn_on_check(int32_t k) {
         if (queued < omega) sender_on[k] = 1;
     }
 };
 
 using fo::set_error;
+
+namespace {
+std::mutex g_pools_mu;
+std::vector<fo_queues*> g_pools;  // every pool between create and destroy
+}  // namespace
 
 extern "C" fo_status fo_queues_create(int32_t K, int64_t slot_bytes, int32_t batch, int32_t with_lengths,
                                       int64_t n_slots, void* hip_stream, fo_queues** out) {
@@ -89,17 +120,92 @@ extern "C" fo_status fo_queues_create(int32_t K, int64_t slot_bytes, int32_t bat
             return e == hipErrorOutOfMemory ? FO_ENOMEM : FO_EHIP;
         }
     }
+    try {
+        std::lock_guard<std::mutex> lk(g_pools_mu);
+        g_pools.push_back(q);
+    } catch (...) {
+        set_error("fo_queues_create: out of host memory");
+        fo_queues_destroy(q);
+        return FO_ENOMEM;
+    }
     *out = q;
     return FO_OK;
 }
 
 extern "C" void fo_queues_destroy(fo_queues* q) {
     if (!q) return;
+    {
+        std::lock_guard<std::mutex> lk(g_pools_mu);
+        for (size_t i = 0; i < g_pools.size(); ++i)
+            if (g_pools[i] == q) {
+                g_pools.erase(g_pools.begin() + i);
+                break;
+            }
+    }
+    if (q->slab || q->svc_ev || !q->guard.empty()) (void)hipStreamSynchronize(q->stream);
+    if (q->svc_ev) {
+        (void)hipEventSynchronize(q->svc_ev);
+        (void)hipEventDestroy(q->svc_ev);
+    }
+    for (auto& kv : q->guard) {
+        (void)hipEventSynchronize(kv.second);
+        (void)hipEventDestroy(kv.second);
+    }
+    for (hipEvent_t e : q->ev_free) (void)hipEventDestroy(e);
+    if (q->ready_ev) (void)hipEventDestroy(q->ready_ev);
     if (q->slab) (void)hipFree(q->slab);
     if (q->labels) (void)hipFree(q->labels);
     if (q->lengths) (void)hipFree(q->lengths);
     delete q;
 }
+
+namespace fo {
+
+fo_status pool_step_begin(const fo_acts* acts, const int32_t* labels, int32_t device_id, hipStream_t step_stream,
+                          fo_queues** owner) {
+    *owner = nullptr;
+    std::lock_guard<std::mutex> lk(g_pools_mu);
+    for (fo_queues* q : g_pools) {
+        const bool x_in = q->in_slab(acts->x), lab_in = q->in_labels(labels);
+        if (!x_in && !lab_in) continue;
+        FO_CHECK(q->busy, "fo_server_step: the batch lies in a pool slot that is not in service");
+        const char* x_svc = q->slab + q->svc.slot * q->slot_bytes;
+        const int32_t* lab_svc = q->labels + q->svc.slot * q->batch;
+        FO_CHECK(acts->x == x_svc, "fo_server_step: the activations lie in pool slot memory other than the "
+                 "batch in service (slot %lld)", (long long)q->svc.slot);
+        FO_CHECK(labels == lab_svc, "fo_server_step: the labels are not those of the batch in service (slot %lld)",
+                 (long long)q->svc.slot);
+        FO_CHECK(!q->lengths || acts->lengths == q->lengths + q->svc.slot * q->batch,
+                 "fo_server_step: the lengths are not those of the batch in service (slot %lld)",
+                 (long long)q->svc.slot);
+        FO_CHECK(device_id == q->svc_k, "fo_server_step: device_id=%d, but the batch in service came from "
+                 "device %d (the last pick)", device_id, q->svc_k);
+        if (step_stream != q->stream) {  // the step reads the slot after the copies into it
+            if (!q->ready_ev) FO_HIP(hipEventCreateWithFlags(&q->ready_ev, hipEventDisableTiming));
+            FO_HIP(hipEventRecord(q->ready_ev, q->stream));
+            FO_HIP(hipStreamWaitEvent(step_stream, q->ready_ev, 0));
+        }
+        *owner = q;
+        return FO_OK;
+    }
+    return FO_OK;
+}
+
+fo_status pool_step_done(fo_queues* q, hipStream_t step_stream) {
+    if (step_stream == q->stream) return FO_OK;  // stream order already keeps the reuse after the step
+    if (!q->svc_ev) {
+        if (!q->ev_free.empty()) {
+            q->svc_ev = q->ev_free.back();
+            q->ev_free.pop_back();
+        } else {
+            FO_HIP(hipEventCreateWithFlags(&q->svc_ev, hipEventDisableTiming));
+        }
+    }
+    FO_HIP(hipEventRecord(q->svc_ev, step_stream));
+    return FO_OK;
+}
+
+}  // namespace fo
 
 extern "C" fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, const int32_t* labels_src,
                                     const int32_t* lengths_src, int32_t src_on_host) {
@@ -119,6 +225,12 @@ extern "C" fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, 
         return FO_ESTATE;
     }
     int64_t slot = q->free_stack.back();
+    auto g = q->guard.find(slot);
+    if (g != q->guard.end()) {  // a step on another stream read this slot: copy after it
+        FO_HIP(hipStreamWaitEvent(q->stream, g->second, 0));
+        q->ev_free.push_back(g->second);
+        q->guard.erase(g);
+    }
     if (q->slab) {
         hipMemcpyKind kind = src_on_host ? hipMemcpyHostToDevice : hipMemcpyDeviceToDevice;
         FO_HIP(hipMemcpyAsync(q->slab + slot * q->slot_bytes, x_src, (size_t)q->slot_bytes, kind, q->stream));
@@ -207,6 +319,15 @@ extern "C" fo_status fo_queues_release(fo_queues* q) {
         fo::set_error("fo_queues_release: no batch in service");
         return FO_ESTATE;
     }
+    if (q->svc_ev) {
+        try {
+            q->guard.emplace(q->svc.slot, q->svc_ev);
+        } catch (...) {  // cannot keep the guard: order the pool's stream after the step now
+            FO_HIP(hipStreamWaitEvent(q->stream, q->svc_ev, 0));
+            q->ev_free.push_back(q->svc_ev);
+        }
+        q->svc_ev = nullptr;
+    }
     q->free_stack.push_back(q->svc.slot);
     q->busy = false;
     q->svc_k = -1;
@@ -231,20 +352,21 @@ extern "C" fo_status fo_aggregate_pending(fo_queues* q, fo_vec* global, float al
     FO_CHECK(m.n == global->n, "fo_aggregate_pending: model length %lld != global %lld", (long long)m.n,
              (long long)global->n);
     FO_CHECK(m.n == 0 || (uintptr_t)m.local % 16 == 0, "fo_aggregate_pending: local not 16-byte aligned");
-    q->qm.pop_front();
-    int64_t s = q->t - m.t_k;
+    const int64_t s = q->t - m.t_k;
+    // a failed check leaves the message at the head of the FIFO
+    FO_CHECK(s >= 0, "fo_aggregate_pending: model version %lld is newer than the global %lld", (long long)m.t_k,
+             (long long)q->t);
     if (k_out) *k_out = m.k;
     if (staleness_out) *staleness_out = s;
     int64_t D = fo::g_max_delay.load();
-    if (s < 0) {
-        fo::set_error("fo_aggregate_pending: model version %lld is newer than the global %lld", (long long)m.t_k,
-                      (long long)q->t);
-        return FO_EINVAL;
+    if (D >= 0 && s > D) {
+        q->qm.pop_front();
+        return FO_SKIPPED;
     }
-    if (D >= 0 && s > D) return FO_SKIPPED;
     float w = alpha / (float)(s + 1);
     st = fo::launch_agg_lerp(global->ptr, m.local, global->n, w, q->stream);
-    if (st != FO_OK) return st;
+    if (st != FO_OK) return st;  // not applied: the message stays queued and t is unchanged
+    q->qm.pop_front();
     q->t++;
     return FO_OK;
 }
@@ -269,34 +391,43 @@ extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, floa
             if (!(D >= 0 && s > D)) t_sim++;
         }
     }
+    // Each launch takes up to kAggMaxFused applied messages (and the stale ones
+    // between them).  The FIFO and t advance only past messages whose launch was
+    // enqueued, so a failing launch leaves them consistent with what the global
+    // model received.
     int32_t applied = 0, skipped = 0;
-    fo::AggTable tab;
-    tab.count = 0;
+    if (applied_out) *applied_out = 0;
+    if (skipped_out) *skipped_out = 0;
     while (!q->qm.empty()) {
-        fo_queues::ModelMsg m = q->qm.front();
-        q->qm.pop_front();
-        int64_t s = q->t - m.t_k;
-        if (D >= 0 && s > D) {
-            skipped++;
-            continue;
+        fo::AggTable tab;
+        tab.count = 0;
+        size_t used = 0;
+        int64_t t_next = q->t;
+        int32_t skipped_here = 0;
+        while (used < q->qm.size() && tab.count < fo::kAggMaxFused) {
+            const fo_queues::ModelMsg& m = q->qm[used];
+            const int64_t s = t_next - m.t_k;
+            ++used;
+            if (D >= 0 && s > D) {
+                skipped_here++;
+                continue;
+            }
+            tab.local[tab.count] = m.local;
+            tab.w[tab.count] = alpha / (float)(s + 1);
+            tab.count++;
+            t_next++;
         }
-        tab.local[tab.count] = m.local;
-        tab.w[tab.count] = alpha / (float)(s + 1);
-        tab.count++;
-        q->t++;
-        applied++;
-        if (tab.count == fo::kAggMaxFused) {
+        if (tab.count > 0) {
             st = fo::launch_agg_lerp_multi(global->ptr, tab, global->n, q->stream);
             if (st != FO_OK) return st;
-            tab.count = 0;
         }
+        q->qm.erase(q->qm.begin(), q->qm.begin() + used);
+        q->t = t_next;
+        applied += tab.count;
+        skipped += skipped_here;
+        if (applied_out) *applied_out = applied;
+        if (skipped_out) *skipped_out = skipped;
     }
-    if (tab.count > 0) {
-        st = fo::launch_agg_lerp_multi(global->ptr, tab, global->n, q->stream);
-        if (st != FO_OK) return st;
-    }
-    if (applied_out) *applied_out = applied;
-    if (skipped_out) *skipped_out = skipped;
     return FO_OK;
 }
 

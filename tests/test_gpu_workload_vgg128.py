@@ -1,15 +1,21 @@
-"""GPU test of the 128-device workload loop: lognormal device rates, Poisson
+"""GPU tests of the 128-device workload loop: lognormal device rates, Poisson
 arrivals per server step, each arrival an activation batch put into the HBM
 pool under flow control (Alg. 2, Sec. 3.4.1) and a model message; pending
 models are aggregated first in fused drains (Alg. 3, Alg. 4 aggregation
 branch), then one batch is picked and trained on.  Checked against the oracle
-scheduler and aggregation through the C ABI:
+scheduler, aggregation and server step through the C ABI:
   - every admission, pick, sequence number, slot id, counter, refusal count,
     peak occupancy and version bit for bit;
-  - the bytes in the slot of the batch in service are the bytes pushed for
-    that (device, sequence);
+  - the bytes and labels in the slot of the batch in service are the ones
+    pushed for that (device, sequence);
   - the global model equals the oracle's FIFO sequence of staleness-weighted
-    mixes (fp64, rounded to fp32 after each) within 1e-4 normwise."""
+    mixes (fp64, rounded to fp32 after each) within 1e-4 normwise;
+  - training: the small loop replays the oracle's server step over the same
+    picked batches and compares every step's loss and the final update; the
+    loop at the workload's own size (batch 64, 64 GiB pool = 32,768 slots of
+    2 MiB, past the step where the cap starts refusing arrivals) compares
+    sampled steps (loss, logits, update) with the oracle run from the
+    library's parameters just before that step."""
 import ctypes
 import os
 
@@ -17,12 +23,16 @@ import numpy as np
 import pytest
 
 import fo_synth as S
+import oracle
 from oracle import aggregate as OA
 from oracle.scheduler import TaskScheduler
 from tests.gpu_util import announce, normwise, torch_cuda
 
 pytestmark = pytest.mark.gpu
 A = pytest.importorskip("paper_2504_13850_amd.api")
+
+TOL = 2e-2
+GRAD_TOL = 6e-2
 
 
 def _d2h(torch, ptr, nbytes):
@@ -36,16 +46,23 @@ def _d2h(torch, ptr, nbytes):
     return out
 
 
-def test_vgg128_loop_matches_oracle():
+def _frob(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)
+
+
+def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=(), replay=False):
+    """Runs the loop; returns a summary.  sample_steps: steps whose training
+    is compared with the oracle from the library's parameters; replay: chain
+    the oracle over every trained batch (small batches only)."""
     torch = torch_cuda()
     cid = 5
     cfg = S.get_config(cid)
     K = cfg.n_devices
-    B, steps, n_slots, bank_n = 4, 12, 600, 8  # a small pool: the cap binds within a few steps
-    announce(f"128-device loop, {steps} steps, pool {n_slots} slots")
     stream = torch.cuda.current_stream()
     rates = S.make_arrival_rates(cid)
-    counts = S.make_arrival_counts(cid, rates, steps, sub=7)
+    counts = S.make_arrival_counts(cid, rates, steps, sub=counts_sub)
     acts = S.make_acts(cid, bank_n, batch=B, sub=7)
     labels = S.make_labels(cid, bank_n, batch=B, sub=7)
     acts_d = torch.from_numpy(acts.view(np.int16)).cuda()
@@ -55,15 +72,18 @@ def test_vgg128_loop_matches_oracle():
     locs = S.make_local_vectors(cid, K, sub=7)
     gd = torch.from_numpy(g0.copy()).cuda()
     ld = torch.from_numpy(locs).cuda()
-    model = A.fo_model_create(cid, B, S.init_params(cid), stream)
+    theta0 = S.init_params(cid)
+    model = A.fo_model_create(cid, B, theta0, stream)
     q = A.fo_queues_create(K, slot_bytes, B, False, n_slots, stream)
     A.fo_set_max_delay(-1)
     sch = TaskScheduler(K, n_slots)
-    ref_g = g0.copy()
     dev_version = [0] * K
     bank_of = {}
     nxt = 0
     trained = drains = 0
+    ref_theta = theta0.astype(np.float64)
+    sampled = []
+    ls_all, ss_all = [], []
     try:
         for t in range(steps):
             senders = []
@@ -73,7 +93,7 @@ def test_vgg128_loop_matches_oracle():
                     nxt += 1
                     ok, seq, _ = sch.put_act(k)
                     st = A.fo_queues_push(q, k, acts_d[i], labels_d[i])
-                    assert (st == A.FO_OK) == ok
+                    assert (st == A.FO_OK) == ok, (t, k)
                     if ok:
                         bank_of[(k, seq)] = i
                     sch.put_model(k, dev_version[k])
@@ -81,17 +101,16 @@ def test_vgg128_loop_matches_oracle():
                     senders.append(k)
             k = A.fo_pick_device(q)
             if k == -2:
-                ls, ss = [], []
+                n0 = len(ls_all)
                 while sch.q_model:
                     kind, kk, t_k = sch.get()
                     assert kind == "model"
                     ok, s = sch.aggregate_version(t_k)
                     assert ok
-                    ls.append(locs[kk])
-                    ss.append(s)
-                ref_g, _ = OA.mix_sequence(ref_g, ls, [1.0] * len(ls), ss)
+                    ls_all.append(kk)
+                    ss_all.append(s)
                 applied, skipped = A.fo_aggregate_pending_all(q, gd, 1.0)
-                assert (applied, skipped) == (len(ls), 0)
+                assert (applied, skipped) == (len(ls_all) - n0, 0)
                 v = A.fo_queues_stats(q).version
                 assert v == sch.t
                 for kk in senders:
@@ -102,22 +121,68 @@ def test_vgg128_loop_matches_oracle():
             if r is None:
                 assert k == -1
                 continue
-            assert r[0] == "act" and k == r[1]
+            assert r[0] == "act" and k == r[1], (t, k, r)
             fa, lab, seq, slot = A.fo_queues_in_service(q)
-            assert (seq, slot) == (r[2], r[3])
+            assert (seq, slot) == (r[2], r[3]), (t, k, seq, slot, r)
+            bi = bank_of[(k, seq)]
             got = _d2h(torch, fa.x, slot_bytes)
-            assert np.array_equal(got, acts[bank_of[(k, seq)]].view(np.uint8).reshape(-1)), (k, seq, slot)
+            assert np.array_equal(got, acts[bi].view(np.uint8).reshape(-1)), (k, seq, slot)
+            got_lab = _d2h(torch, lab, 4 * B).view(np.int32)
+            assert np.array_equal(got_lab, labels[bi]), (k, seq, slot)
+            before = A.fo_model_read(model, A.FO_BUF_PARAMS) if t in sample_steps else None
             A.fo_server_step(model, fa, lab, k)
             A.fo_queues_release(q)
             sch.release()
             trained += 1
+            if before is not None:
+                announce(f"128-device loop: oracle check of step {t} (device {k}, seq {seq}, slot {slot})")
+                rr = oracle.server_step(cid, before, acts[bi], labels[bi], lr=cfg.lr)
+                loss = A.fo_model_read(model, A.FO_BUF_LOSS)[0]
+                logits = A.fo_model_read(model, A.FO_BUF_LOGITS).reshape(B, cfg.n_classes)
+                after = A.fo_model_read(model, A.FO_BUF_PARAMS).astype(np.float64)
+                rec = dict(step=t, loss=abs(loss - rr["loss"]) / abs(rr["loss"]),
+                           logits=normwise(logits, rr["logits"]),
+                           update=_frob(after - before, rr["params"] - before))
+                sampled.append(rec)
+                assert rec["loss"] <= TOL and rec["logits"] <= TOL, rec
+                assert rec["update"] <= GRAD_TOL, rec
+            if replay:
+                rr = oracle.server_step(cid, ref_theta, acts[bi], labels[bi], lr=cfg.lr)
+                loss = A.fo_model_read(model, A.FO_BUF_LOSS)[0]
+                assert abs(loss - rr["loss"]) <= TOL * abs(rr["loss"]), (t, loss, rr["loss"])
+                ref_theta = rr["params"]
         st = A.fo_queues_stats(q)
         assert A.fo_queues_counters(q, K) == sch.c
         assert (st.refused, st.peak_queued, st.queued, st.version) == (sch.refused, sch.peak_queued, sch.queued(),
                                                                        sch.t)
-        assert st.refused > 0 and trained == steps and drains == steps
-        assert np.isfinite(A.fo_model_read(model, A.FO_BUF_LOSS)[0])
+        assert trained == steps and drains == steps
+        if replay:
+            final = A.fo_model_read(model, A.FO_BUF_PARAMS).astype(np.float64)
+            assert _frob(final - theta0, ref_theta - theta0) <= GRAD_TOL
+        ref_g, _ = OA.mix_sequence(g0, [locs[kk] for kk in ls_all], [1.0] * len(ls_all), ss_all)
         assert normwise(gd.cpu().numpy(), ref_g) <= 1e-4
     finally:
         A.fo_queues_destroy(q)
         A.fo_model_destroy(model)
+    return dict(refused=st.refused, peak=st.peak_queued, omega=st.omega, sampled=sampled)
+
+
+def test_vgg128_loop_matches_oracle():
+    """A small pool (600 slots) so that the cap binds within a few steps; batch 4;
+    the oracle's server step replayed over every trained batch."""
+    announce("128-device loop, 12 steps, pool 600 slots, batch 4")
+    out = _run_loop(B=4, steps=12, n_slots=600, bank_n=8, counts_sub=7, replay=True)
+    assert out["refused"] > 0
+
+
+def test_vgg128_loop_workload_scale():
+    """The workload's own sizes: batch 64, a 64 GiB pool of 2 MiB slots
+    (32,768 slots, omega = 32,640), the benchmark's arrival table, run past
+    step 161 where the cap starts refusing arrivals."""
+    steps = 175
+    announce(f"128-device loop at workload scale, {steps} steps, pool 32768 slots, batch 64")
+    out = _run_loop(B=64, steps=steps, n_slots=(64 << 30) // (2 << 20), bank_n=16, counts_sub=0,
+                    sample_steps=(0, steps - 1))
+    print(out)
+    assert out["refused"] > 0 and out["peak"] >= out["omega"]
+    assert len(out["sampled"]) == 2

@@ -213,3 +213,65 @@ def test_argument_errors_are_reported():
     with pytest.raises(A.FoError) as e:
         A.fo_model_create(1, 4, np.zeros(3, np.float32))
     assert "n_params" in str(e.value)
+
+
+def test_rejected_model_message_stays_queued():
+    """A model message whose version is newer than the global one is an
+    argument error: nothing is applied, the message stays at the head of the
+    FIFO and t is unchanged (both for the single and the draining call)."""
+    q = A.fo_queues_create(2, 0, 1, False, 10)
+    try:
+        A.fo_queues_push_model(q, 0, None, 0)
+        assert A.fo_aggregate_pending(q, _Empty(), 1.0)[0] == A.FO_OK  # t = 1
+        A.fo_queues_push_model(q, 1, None, 5)  # t_k = 5 > t = 1
+        for _ in range(2):
+            with pytest.raises(A.FoError) as e:
+                A.fo_aggregate_pending(q, _Empty(), 1.0)
+            assert e.value.status == A.FO_EINVAL and "newer" in str(e.value)
+            st = A.fo_queues_stats(q)
+            assert (st.models_pending, st.version) == (1, 1)
+        with pytest.raises(A.FoError):
+            A.fo_aggregate_pending_all(q, _Empty(), 1.0)
+        st = A.fo_queues_stats(q)
+        assert (st.models_pending, st.version) == (1, 1)
+    finally:
+        A.fo_queues_destroy(q)
+
+
+def test_drain_with_skips_matches_oracle_versions():
+    """The draining call over a FIFO mixing stale and fresh messages, more than
+    one launch's worth (64 applied per launch): applied / skipped counts and the
+    final version follow the oracle's Alg. 4 bookkeeping."""
+    A.fo_set_max_delay(2)
+    try:
+        q = A.fo_queues_create(4, 0, 1, False, 10)
+        sch = TaskScheduler(4, 10)
+        try:
+            rng = np.random.default_rng(3)
+            tks = []
+            for i in range(150):
+                tk = int(max(0, i - rng.integers(0, 5)))
+                tks.append(tk)
+            # versions as the devices would hold them: never newer than t at service time
+            t_sim, ok_tks = 0, []
+            for tk in tks:
+                tk = min(tk, t_sim)
+                ok_tks.append(tk)
+                if t_sim - tk <= 2:
+                    t_sim += 1
+            for i, tk in enumerate(ok_tks):
+                A.fo_queues_push_model(q, i % 4, None, tk)
+                sch.put_model(i % 4, tk)
+            applied, skipped = A.fo_aggregate_pending_all(q, _Empty(), 1.0)
+            n_ok = 0
+            while sch.q_model:
+                _, _, tk = sch.get()
+                n_ok += sch.aggregate_version(tk, max_delay=2)[0]
+            assert (applied, skipped) == (n_ok, 150 - n_ok)
+            assert applied > 64 and skipped > 0
+            st = A.fo_queues_stats(q)
+            assert (st.version, st.models_pending) == (sch.t, 0)
+        finally:
+            A.fo_queues_destroy(q)
+    finally:
+        A.fo_set_max_delay(-1)

@@ -112,3 +112,22 @@ def test_padded_tokens_never_matter():
     r2 = oracle.server_step(cid, theta, x2, labels, lengths)
     np.testing.assert_allclose(r2["logits"], r["logits"], rtol=1e-12, atol=1e-13)
     np.testing.assert_allclose(r2["grads"], r["grads"], rtol=1e-9, atol=1e-12 * np.abs(r["grads"]).max())
+
+
+def test_momentum_term_moves_the_second_update():
+    """The multi-step GPU check compares the update of each step by relative
+    Frobenius error (bound 6e-2).  A mistake planted in the oracle -- the
+    momentum buffer dropped at step 2 -- moves that update by far more than
+    the bound, so the check can see the mu v term of v <- mu v + g."""
+    cid = 3
+    theta = S.init_params(cid).astype(np.float64)
+    acts, labels, _ = _inputs(cid, 4)
+    a2 = S.make_acts(cid, 1, batch=4, sub=77)[0]
+    l2 = S.make_labels(cid, 1, batch=4, sub=77)[0]
+    r1 = oracle.server_step(cid, theta, acts, labels, lr=0.01, momentum=0.9)
+    good = oracle.server_step(cid, r1["params"], a2, l2, lr=0.01, momentum=0.9, mom_buf=r1["momentum"])
+    bad = oracle.server_step(cid, r1["params"], a2, l2, lr=0.01, momentum=0.9,
+                             mom_buf=np.zeros_like(r1["momentum"]))
+    d_good = good["params"] - r1["params"]
+    d_bad = bad["params"] - r1["params"]
+    assert np.linalg.norm(d_bad - d_good) / np.linalg.norm(d_good) > 0.6
