@@ -1,13 +1,12 @@
-"""Multi-step GPU parity: consecutive server steps on fresh seeded batches,
-each compared with the oracle chained on its own state.
+"""Multi-step GPU parity: consecutive server steps on fresh seeded batches.
 
 One training iteration of Alg. 4 updates the parameters (and, for the
 ResNet workload, the momentum buffer v <- mu v + g, theta <- theta - lr v).
 A single step from a zero buffer cannot show the mu v term (v_1 = g_1), so
-these tests run three steps in a row on three different batches and, after
-every step, compare the library's state with the oracle's state after the
-same number of steps, the oracle starting each step from its own parameters
-and momentum buffer:
+these tests run three steps in a row on three different batches.  Each step
+is checked as the function it is: the oracle takes the library's state just
+before the step (parameters and momentum buffer, read back) and the step's
+batch, and its result is compared with the library's state after the step:
 
   graded:   loss and logits of the step (2e-2, normwise for logits);
   checked:  every gradient tensor, the update of the step
@@ -15,8 +14,15 @@ and momentum buffer:
             Frobenius error <= 6e-2 (bf16 gradients; a dropped or mis-scaled
             term moves them by O(1)).
 
-A wrong momentum coefficient changes the step-2 update by about mu |v_1| /
-|v_2|, which is of order one here."""
+From step 2 on the oracle's v_i = mu v_{i-1} + g_i starts from the
+library's v_{i-1}: a wrong coefficient changes the update by about
+mu |v_{i-1}| / |v_i|, of order one here (a CPU test checks that size).
+
+The library's trajectory is not compared with the oracle's own three-step
+trajectory: these networks amplify a parameter difference of the size of one
+bf16 step's error (~1% of the update) into 5-25% gradient differences within
+two steps, in the fp64 oracle alone (also pinned by a CPU test), so that
+comparison would measure the dynamics, not the kernels."""
 import numpy as np
 import pytest
 
@@ -49,6 +55,15 @@ def _worst_tensor(cid, got, ref):
     return name, worst
 
 
+def _tensor_errors(cid, got, ref):
+    out, off = {}, 0
+    for nm, shape, _, _ in S.param_layout(cid):
+        n = int(np.prod(shape))
+        out[nm] = _frob(got[off:off + n], ref[off:off + n])
+        off += n
+    return out
+
+
 def _chain(cid, B, sub, with_lengths=False):
     torch = torch_cuda()
     cfg = S.get_config(cid)
@@ -57,9 +72,8 @@ def _chain(cid, B, sub, with_lengths=False):
     labels = S.make_labels(cid, N_STEPS, batch=B, sub=sub)
     lengths = S.make_lengths(cid, N_STEPS, batch=B, sub=sub) if with_lengths else [None] * N_STEPS
     model = A.fo_model_create(cid, B, theta, torch.cuda.current_stream())
-    ref_theta = theta.astype(np.float64)
-    ref_mom = None
     prev = theta.astype(np.float64)
+    prev_mom = None  # zero buffer before the first step
     report = []
     try:
         for i in range(N_STEPS):
@@ -71,28 +85,34 @@ def _chain(cid, B, sub, with_lengths=False):
             logits = A.fo_model_read(model, A.FO_BUF_LOGITS).reshape(B, cfg.n_classes)
             grads = A.fo_model_read(model, A.FO_BUF_GRADS)
             params = A.fo_model_read(model, A.FO_BUF_PARAMS).astype(np.float64)
-            r = oracle.server_step(cid, ref_theta, acts[i], labels[i], lengths[i], lr=cfg.lr,
-                                   momentum=cfg.momentum, mom_buf=ref_mom)
+            r = oracle.server_step(cid, prev, acts[i], labels[i], lengths[i], lr=cfg.lr,
+                                   momentum=cfg.momentum, mom_buf=prev_mom)
             e_loss = abs(loss - r["loss"]) / abs(r["loss"])
             e_logit = normwise(logits, r["logits"])
             gname, e_grad = _worst_tensor(cid, grads, r["grads"])
-            e_upd = _frob(params - prev, r["params"] - ref_theta)
+            e_upd = _frob(params - prev, r["params"] - prev)
             rec = dict(step=i + 1, loss=e_loss, logits=e_logit, grad=(gname, e_grad), update=e_upd)
             if cfg.momentum:
-                rec["momentum"] = _frob(A.fo_model_read(model, A.FO_BUF_MOMENTUM), r["momentum"])
+                mom = A.fo_model_read(model, A.FO_BUF_MOMENTUM).astype(np.float64)
+                rec["momentum"] = _frob(mom, r["momentum"])
+                prev_mom = mom
+            rec["grad_by_tensor"] = _tensor_errors(cid, grads, r["grads"])
             report.append(rec)
-            assert e_loss <= TOL, rec
-            assert e_logit <= TOL, rec
-            assert e_grad <= GRAD_TOL, rec
-            assert e_upd <= GRAD_TOL, rec
-            if cfg.momentum:
-                assert rec["momentum"] <= GRAD_TOL, rec
             prev = params
             ref_theta = r["params"]
             ref_mom = r["momentum"]
     finally:
         A.fo_model_destroy(model)
-    print(report)
+    for rec in report:
+        top = sorted(rec.pop("grad_by_tensor").items(), key=lambda kv: -kv[1])[:6]
+        print({k: v for k, v in rec.items()}, "worst tensors:", [(n, round(e, 4)) for n, e in top])
+    for rec in report:
+        assert rec["loss"] <= TOL, rec
+        assert rec["logits"] <= TOL, rec
+        assert rec["grad"][1] <= GRAD_TOL, rec
+        assert rec["update"] <= GRAD_TOL, rec
+        if cfg.momentum:
+            assert rec["momentum"] <= GRAD_TOL, rec
     return report
 
 

@@ -10,12 +10,13 @@ scheduler, aggregation and server step through the C ABI:
     pushed for that (device, sequence);
   - the global model equals the oracle's FIFO sequence of staleness-weighted
     mixes (fp64, rounded to fp32 after each) within 1e-4 normwise;
-  - training: the small loop replays the oracle's server step over the same
-    picked batches and compares every step's loss and the final update; the
-    loop at the workload's own size (batch 64, 64 GiB pool = 32,768 slots of
-    2 MiB, past the step where the cap starts refusing arrivals) compares
-    sampled steps (loss, logits, update) with the oracle run from the
-    library's parameters just before that step."""
+  - training: the step on each picked batch is compared with the oracle's
+    step on the batch and labels pushed for that (device, sequence), run from
+    the library's parameters just before the step (loss, logits, update): at
+    every step of the small loop, and at sampled steps of the loop at the
+    workload's own size (batch 64, 64 GiB pool = 32,768 slots of 2 MiB, past
+    the step where the cap starts refusing arrivals).  A wrong slot or label
+    moves the loss by far more than the bound."""
 import ctypes
 import os
 
@@ -52,10 +53,9 @@ def _frob(got, ref):
     return np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)
 
 
-def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=(), replay=False):
-    """Runs the loop; returns a summary.  sample_steps: steps whose training
-    is compared with the oracle from the library's parameters; replay: chain
-    the oracle over every trained batch (small batches only)."""
+def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=()):
+    """Runs the loop; returns a summary.  sample_steps: the steps whose
+    training is compared with the oracle from the library's parameters."""
     torch = torch_cuda()
     cid = 5
     cfg = S.get_config(cid)
@@ -72,8 +72,7 @@ def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=(), replay=Fal
     locs = S.make_local_vectors(cid, K, sub=7)
     gd = torch.from_numpy(g0.copy()).cuda()
     ld = torch.from_numpy(locs).cuda()
-    theta0 = S.init_params(cid)
-    model = A.fo_model_create(cid, B, theta0, stream)
+    model = A.fo_model_create(cid, B, S.init_params(cid), stream)
     q = A.fo_queues_create(K, slot_bytes, B, False, n_slots, stream)
     A.fo_set_max_delay(-1)
     sch = TaskScheduler(K, n_slots)
@@ -81,7 +80,6 @@ def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=(), replay=Fal
     bank_of = {}
     nxt = 0
     trained = drains = 0
-    ref_theta = theta0.astype(np.float64)
     sampled = []
     ls_all, ss_all = [], []
     try:
@@ -146,19 +144,11 @@ def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=(), replay=Fal
                 sampled.append(rec)
                 assert rec["loss"] <= TOL and rec["logits"] <= TOL, rec
                 assert rec["update"] <= GRAD_TOL, rec
-            if replay:
-                rr = oracle.server_step(cid, ref_theta, acts[bi], labels[bi], lr=cfg.lr)
-                loss = A.fo_model_read(model, A.FO_BUF_LOSS)[0]
-                assert abs(loss - rr["loss"]) <= TOL * abs(rr["loss"]), (t, loss, rr["loss"])
-                ref_theta = rr["params"]
         st = A.fo_queues_stats(q)
         assert A.fo_queues_counters(q, K) == sch.c
         assert (st.refused, st.peak_queued, st.queued, st.version) == (sch.refused, sch.peak_queued, sch.queued(),
                                                                        sch.t)
         assert trained == steps and drains == steps
-        if replay:
-            final = A.fo_model_read(model, A.FO_BUF_PARAMS).astype(np.float64)
-            assert _frob(final - theta0, ref_theta - theta0) <= GRAD_TOL
         ref_g, _ = OA.mix_sequence(g0, [locs[kk] for kk in ls_all], [1.0] * len(ls_all), ss_all)
         assert normwise(gd.cpu().numpy(), ref_g) <= 1e-4
     finally:
@@ -169,10 +159,10 @@ def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=(), replay=Fal
 
 def test_vgg128_loop_matches_oracle():
     """A small pool (600 slots) so that the cap binds within a few steps; batch 4;
-    the oracle's server step replayed over every trained batch."""
+    every step's training compared with the oracle."""
     announce("128-device loop, 12 steps, pool 600 slots, batch 4")
-    out = _run_loop(B=4, steps=12, n_slots=600, bank_n=8, counts_sub=7, replay=True)
-    assert out["refused"] > 0
+    out = _run_loop(B=4, steps=12, n_slots=600, bank_n=8, counts_sub=7, sample_steps=tuple(range(12)))
+    assert out["refused"] > 0 and len(out["sampled"]) == 12
 
 
 def test_vgg128_loop_workload_scale():

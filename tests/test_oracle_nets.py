@@ -131,3 +131,32 @@ def test_momentum_term_moves_the_second_update():
     d_good = good["params"] - r1["params"]
     d_bad = bad["params"] - r1["params"]
     assert np.linalg.norm(d_bad - d_good) / np.linalg.norm(d_good) > 0.6
+
+
+def test_trajectory_amplifies_a_one_percent_step_error():
+    """Why the multi-step GPU checks start each step from the library's own
+    state: in the fp64 oracle alone, a 1% (relative Frobenius) perturbation of
+    the first update -- the size of one bf16 step's error -- grows within two
+    more VGG steps into a gradient difference above the 6e-2 bound of the GPU
+    checks.  Comparing the two trajectories would measure the dynamics."""
+    cid, B, sub = 2, 16, 23
+    th = S.init_params(cid).astype(np.float64)
+    acts = S.make_acts(cid, 3, batch=B, sub=sub)
+    labels = S.make_labels(cid, 3, batch=B, sub=sub)
+    r1 = oracle.server_step(cid, th, acts[0], labels[0])
+    d = r1["params"] - th
+    noise = np.random.default_rng(0).standard_normal(d.shape) * np.abs(d)
+    noise *= 0.01 * np.linalg.norm(d) / np.linalg.norm(noise)
+    pa, pb = r1["params"], th + d + noise
+    worst = 0.0
+    for i in (1, 2):
+        ra = oracle.server_step(cid, pa, acts[i], labels[i])
+        rb = oracle.server_step(cid, pb, acts[i], labels[i])
+        off = 0
+        for _, shape, _, _ in S.param_layout(cid):
+            n = int(np.prod(shape))
+            ga, gb = ra["grads"][off:off + n], rb["grads"][off:off + n]
+            worst = max(worst, np.linalg.norm(ga - gb) / np.linalg.norm(ga))
+            off += n
+        pa, pb = ra["params"], rb["params"]
+    assert worst > 0.06
