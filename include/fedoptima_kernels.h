@@ -32,6 +32,25 @@ FO_API fo_status fo_gemm_bf16(int32_t M, int32_t N, int32_t K, int32_t a_layout,
                               const uint16_t* B_lo, int64_t ldb, float* C, int64_t ldc, int32_t splits,
                               float* workspace, void* hip_stream);
 
+/* fo_gemm_bf16 for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same product with the same kernels and results, and no workspace argument.
+ * Split-K partials go to a 16 MiB array that the library's code object holds
+ * on every GPU it is loaded on, from load until the process ends; so
+ * splits * M * N must not exceed 4,194,304 floats (FO_EINVAL otherwise,
+ * nothing launched).  splits == 1 uses no scratch.  The call allocates
+ * nothing: its first call on a device looks up that device's copy of the
+ * array (hip_stream must belong to the current device, else FO_EINVAL).
+ * Every slice writes all of its partials before they are summed, so nothing
+ * needs clearing between calls; but all calls on one GPU share the one array,
+ * so calls whose split-K work overlaps in time on one GPU (on different
+ * streams, or from different threads) race, and must be ordered by the
+ * caller.  Other arguments and errors as fo_gemm_bf16. */
+FO_API fo_status fo_gemm_bf16_noalloc(int32_t M, int32_t N, int32_t K, int32_t a_layout, const uint16_t* A,
+                                      const uint16_t* A_lo, int64_t lda, int32_t b_layout, const uint16_t* B,
+                                      const uint16_t* B_lo, int64_t ldb, float* C, int64_t ldc, int32_t splits,
+                                      void* hip_stream);
+
 /* One pass of a 2-D convolution (cross-correlation) in NHWC layout as an
  * implicit GEMM; weights are [Co][k][k][Ci].
  *   pass 0 (forward):          out[Bn][Ho][Wo][Co] = conv(x, w)           x = in [Bn][H][W][Ci]

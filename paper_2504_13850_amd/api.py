@@ -26,7 +26,7 @@ EXPORTS = [
     "fo_queues_push", "fo_queues_push_model", "fo_pick_device", "fo_queues_in_service",
     "fo_queues_release", "fo_aggregate_pending", "fo_aggregate_pending_all", "fo_queues_stats",
     "fo_queues_counters", "fo_queues_add_device", "fo_last_error", "fo_profile_enable", "fo_profile_read",
-    "fo_set_graph_mode", "fo_gemm_bf16", "fo_conv2d_bf16",
+    "fo_set_graph_mode", "fo_gemm_bf16", "fo_conv2d_bf16", "fo_gemm_bf16_noalloc",
 ]
 FO_LAYOUT_ROW_K, FO_LAYOUT_K_ROW = 0, 1
 
@@ -105,6 +105,8 @@ def lib():
             "fo_gemm_bf16": (C.c_int, [i32, i32, i32, i32, vp, vp, i64, i32, vp, vp, i64, vp, i64, i32, vp, vp]),
             "fo_conv2d_bf16": (C.c_int, [i32, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32,
                                          vp, vp]),
+            "fo_gemm_bf16_noalloc": (C.c_int, [i32, i32, i32, i32, vp, vp, i64, i32, vp, vp, i64, vp, i64, i32,
+                                               vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -311,6 +313,12 @@ def fo_gemm_bf16(M, N, K, a_layout, A, A_lo, lda, b_layout, B, B_lo, ldb, C, ldc
                  stream=None):
     _check(lib().fo_gemm_bf16(M, N, K, a_layout, _dptr(A), _dptr(A_lo), lda, b_layout, _dptr(B), _dptr(B_lo), ldb,
                               _dptr(C), ldc, splits, _dptr(workspace), _stream(stream)))
+
+
+def fo_gemm_bf16_noalloc(M, N, K, a_layout, A, A_lo, lda, b_layout, B, B_lo, ldb, C, ldc, splits=1,
+                         stream=None):
+    _check(lib().fo_gemm_bf16_noalloc(M, N, K, a_layout, _dptr(A), _dptr(A_lo), lda, b_layout, _dptr(B),
+                                      _dptr(B_lo), ldb, _dptr(C), ldc, splits, _stream(stream)))
 
 
 def fo_conv2d_bf16(pass_, Bn, H, W, Ci, Co, k, stride, pad, inp, inp_lo, in2, w, w_lo, out, splits=1,

@@ -1,9 +1,49 @@
 // Kernel-level C entry points (fedoptima_kernels.h): argument checks, then
 // one descriptor for the MFMA GEMM.
+#include <mutex>
+
 #include "../../include/fedoptima_kernels.h"
 #include "gemm.h"
 
 using namespace fo;
+
+// Split-K partials of fo_gemm_bf16_noalloc.  The array is part of the code
+// object: every GPU the library is loaded on holds its own copy from module
+// load until the process ends, and no call allocates.  In host code the name
+// `scratch` is only a host-side handle; kernels get the device address that
+// hipGetSymbolAddress returns for the current device.
+constexpr int64_t kNoAllocScratchFloats = int64_t(4) << 20;  // 16 MiB
+static __device__ __align__(256) float scratch[kNoAllocScratchFloats];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxScratchDevices] = {};  // per device, set on the first call there
+
+// The device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept; the stream must belong to it.
+fo_status scratch_ptr(hipStream_t stream, float** out) {
+    int dev = -1;
+    FO_HIP(hipGetDevice(&dev));
+    FO_CHECK(dev >= 0 && dev < kMaxScratchDevices, "fo_gemm_bf16_noalloc: device %d beyond %d", dev,
+             kMaxScratchDevices);
+    if (stream) {
+        int sdev = -1;
+        FO_HIP(hipStreamGetDevice(stream, &sdev));
+        FO_CHECK(sdev == dev, "fo_gemm_bf16_noalloc: the stream belongs to device %d, the current device is %d",
+                 sdev, dev);
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        FO_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        FO_CHECK(p != nullptr, "fo_gemm_bf16_noalloc: no device address for the scratch array");
+        g_scratch_ptr[dev] = (float*)p;
+    }
+    *out = g_scratch_ptr[dev];
+    return FO_OK;
+}
+}  // namespace
 
 extern "C" fo_status fo_gemm_bf16(int32_t M, int32_t N, int32_t K, int32_t a_layout, const uint16_t* A,
                                   const uint16_t* A_lo, int64_t lda, int32_t b_layout, const uint16_t* B,
@@ -28,6 +68,24 @@ extern "C" fo_status fo_gemm_bf16(int32_t M, int32_t N, int32_t K, int32_t a_lay
     d.Cf = C; d.ldcf = ldc;
     d.splits = splits; d.ws = workspace;
     return gemm(d, (hipStream_t)hip_stream);
+}
+
+extern "C" fo_status fo_gemm_bf16_noalloc(int32_t M, int32_t N, int32_t K, int32_t a_layout, const uint16_t* A,
+                                          const uint16_t* A_lo, int64_t lda, int32_t b_layout, const uint16_t* B,
+                                          const uint16_t* B_lo, int64_t ldb, float* C, int64_t ldc, int32_t splits,
+                                          void* hip_stream) {
+    FO_CHECK(splits >= 1, "fo_gemm_bf16_noalloc: splits=%d", splits);
+    FO_CHECK(M >= 1 && N >= 1 && K >= 1, "fo_gemm_bf16_noalloc: sizes %d x %d x %d", M, N, K);
+    float* ws = nullptr;
+    if (splits > 1) {
+        const int64_t need = (int64_t)splits * M * N;
+        FO_CHECK(need <= kNoAllocScratchFloats,
+                 "fo_gemm_bf16_noalloc: %d slices of a %d x %d product need %lld floats of scratch, the limit is "
+                 "%lld (16 MiB)", splits, M, N, (long long)need, (long long)kNoAllocScratchFloats);
+        fo_status st = scratch_ptr((hipStream_t)hip_stream, &ws);
+        if (st != FO_OK) return st;
+    }
+    return fo_gemm_bf16(M, N, K, a_layout, A, A_lo, lda, b_layout, B, B_lo, ldb, C, ldc, splits, ws, hip_stream);
 }
 
 extern "C" fo_status fo_conv2d_bf16(int32_t pass, int32_t Bn, int32_t H, int32_t W, int32_t Ci, int32_t Co,
