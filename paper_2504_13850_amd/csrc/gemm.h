@@ -119,6 +119,13 @@ struct SplitRows {
 // Enqueues the GEMM (and its split-K reduction) on stream s.
 fo_status gemm(const GemmDesc& d, hipStream_t s);
 
+// Enqueues n <= kGemmGroupMax independent products.  When all of them are
+// unsplit products of aligned k-major operands (weight gradients) they run as
+// one launch over the concatenation of their output tiles, each tile over its
+// whole K (no split-K partials, no reduction pass); otherwise one launch each.
+constexpr int kGemmGroupMax = 4;
+fo_status gemm_group(const GemmDesc* d, int n, hipStream_t s);
+
 // Bytes of split-K workspace a descriptor needs (0 if splits == 1).
 inline size_t gemm_ws_bytes(int M, int N, int splits) {
     return splits > 1 ? sizeof(float) * (size_t)M * N * splits : 0;

@@ -812,20 +812,15 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
     }
 }
 
+// Two K tiles (A and B each 128 x 72 bf16) = 72 KB of LDS; reused for the C tile.
+typedef bf16_t GemmSmem[2][2][BM * LDR];
+
+// One 128 x 128 output tile (one K slice of it) of the product d: the K loop
+// and the epilogue, shared by the single-product and the grouped kernels.
 template <int AM, int BMODE, bool AL>
-__global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
-    // two K tiles (A and B each 128 x 72 bf16) = 72 KB; reused for the C tile
-    __shared__ __attribute__((aligned(16))) bf16_t smem[2][2][BM * LDR];
+__device__ __forceinline__ void gemm_tile(const GemmDesc& d, const TileJob& job, int M, int Keff, GemmSmem& smem) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
-    const int Keff = d.Kdev ? min(d.K, *d.Kdev) : d.K;
-    if (d.prof_snap && (blockIdx.x | blockIdx.y | blockIdx.z) == 0 && tid == 0) {
-        d.prof_snap[0] = M;
-        d.prof_snap[1] = Keff;
-    }
-    TileJob job;
-    if (!map_tile(d, M, d.nseg * gemm_kseg(d, Keff), job)) return;  // uniform for the whole workgroup
     const int kseg = gemm_kseg(d, Keff);
     const int ktot = d.nseg * kseg;
     const int S = job.S, zt = job.zt, m0 = job.m0, n0 = job.n0;
@@ -932,6 +927,83 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
     }
 
     store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
+}
+
+template <int AM, int BMODE, bool AL>
+__global__ void __launch_bounds__(NT, 2) gemm_kernel(const GemmDesc d) {
+    __shared__ __attribute__((aligned(16))) GemmSmem smem;
+    const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
+    const int Keff = d.Kdev ? min(d.K, *d.Kdev) : d.K;
+    if (d.prof_snap && (blockIdx.x | blockIdx.y | blockIdx.z) == 0 && threadIdx.x == 0) {
+        d.prof_snap[0] = M;
+        d.prof_snap[1] = Keff;
+    }
+    TileJob job;
+    if (!map_tile(d, M, d.nseg * gemm_kseg(d, Keff), job)) return;  // uniform for the whole workgroup
+    gemm_tile<AM, BMODE, AL>(d, job, M, Keff, smem);
+}
+
+// Several independent products in one launch (each unsplit, over its whole K):
+// the grid is the concatenation of their 128 x 128 output tiles.  Workgroup
+// ids are renumbered as in map_tile so that each XCD owns a contiguous range
+// of the concatenated tiles, and within a product the tiles are walked in
+// groups of eight tile rows.  Used for the four weight gradients of an
+// encoder layer, which are ready at the same point of the backward.
+struct GemmGroupArg {
+    GemmDesc d[kGemmGroupMax];
+    int n;
+    int* prof_snap;  // (M, K) effective per member, when profiling
+};
+
+template <int AM, int BMODE, bool AL>
+__global__ void __launch_bounds__(NT, 2) gemm_group_kernel(const GemmGroupArg g) {
+    __shared__ __attribute__((aligned(16))) GemmSmem smem;
+    constexpr int GM = 8;
+    int Ms[kGemmGroupMax], Ks[kGemmGroupMax], start[kGemmGroupMax + 1];
+    start[0] = 0;
+#pragma unroll
+    for (int i = 0; i < kGemmGroupMax; ++i) {
+        const GemmDesc& d = g.d[i < g.n ? i : 0];
+        Ms[i] = d.Mdev ? min(d.M, *d.Mdev) : d.M;
+        Ks[i] = d.Kdev ? min(d.K, *d.Kdev) : d.K;
+        const int tiles = ((Ms[i] + BM - 1) / BM) * ((d.N + BN - 1) / BN);
+        start[i + 1] = start[i] + (i < g.n ? tiles : 0);
+    }
+    if (g.prof_snap && blockIdx.x == 0 && threadIdx.x == 0) {
+#pragma unroll
+        for (int i = 0; i < kGemmGroupMax; ++i)
+            if (i < g.n) {
+                g.prof_snap[2 * i] = Ms[i];
+                g.prof_snap[2 * i + 1] = Ks[i];
+            }
+    }
+    const int W = start[kGemmGroupMax];
+    const int w = blockIdx.x;
+    if (w >= W) return;  // tiles past a device-side row bound (uniform)
+    const int xq = W >> 3, xr = W & 7, xc = w & 7;
+    const int nid = xc * xq + min(xc, xr) + (w >> 3);
+    // the member owning tile nid (selects in registers: no dynamic indexing)
+    int m = 0, s0 = 0, Mm = Ms[0], Km = Ks[0];
+#pragma unroll
+    for (int i = 1; i < kGemmGroupMax; ++i)
+        if (nid >= start[i]) {
+            m = i;
+            s0 = start[i];
+            Mm = Ms[i];
+            Km = Ks[i];
+        }
+    const GemmDesc& d = g.d[m];
+    const int tt = nid - s0;
+    const int nN = (d.N + BN - 1) / BN, nMe = (Mm + BM - 1) / BM;
+    const int grp = tt / (GM * nN), tg = tt - grp * GM * nN;
+    const int gr = min(GM, nMe - grp * GM);
+    TileJob job;
+    job.mt = grp * GM + tg % gr;
+    job.m0 = job.mt * BM;
+    job.n0 = (tg / gr) * BN;
+    job.zt = 0;
+    job.S = 1;
+    gemm_tile<AM, BMODE, AL>(d, job, Mm, Km, smem);
 }
 
 // ------------------------------------------------------------------ single-pass compensated product
@@ -1224,6 +1296,62 @@ void launch(const GemmDesc& d, hipStream_t s) {
 }
 
 }  // namespace
+
+fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s) {
+    FO_CHECK(n >= 1 && n <= kGemmGroupMax, "gemm_group: %d products", n);
+    // a group runs in one launch when every member is an unsplit, aligned
+    // product of k-major operands (the weight-gradient form); otherwise each
+    // member is launched on its own
+    auto al16 = [](const void* p) { return p == nullptr || ((uintptr_t)p & 15) == 0; };
+    bool one = true;
+    for (int i = 0; i < n; ++i) {
+        const GemmDesc& d = ds[i];
+        one = one && d.amode == OP_KR && d.bmode == OP_KR && d.splits == 1 && d.nseg == 1 && !d.Mdev &&
+              !d.colpart && d.lda % 8 == 0 && d.ldb % 8 == 0 && d.M % 8 == 0 && d.N % 8 == 0 && al16(d.A) &&
+              al16(d.B);
+    }
+    if (!one) {
+        for (int i = 0; i < n; ++i) {
+            fo_status st = gemm(ds[i], s);
+            if (st != FO_OK) return st;
+        }
+        return FO_OK;
+    }
+    GemmGroupArg g;
+    g.n = n;
+    int tiles = 0;
+    ProfInfo pi;
+    pi.kind = PROF_GEMM;
+    pi.ngroup = n;
+    for (int i = 0; i < kGemmGroupMax; ++i) {
+        const GemmDesc& d = ds[i < n ? i : 0];
+        FO_CHECK(d.M > 0 && d.N > 0 && d.K > 0, "gemm_group: empty product %dx%dx%d", d.M, d.N, d.K);
+        FO_CHECK(d.Cf || d.Cb, "gemm_group: no output");
+        FO_CHECK(!d.sgd_theta || (d.Cf && d.sgd_hi && d.sgd_lo), "gemm_group: the fused SGD needs Cf and both parts");
+        g.d[i] = d;
+        auto al = [](const void* p, uintptr_t m) { return p == nullptr || ((uintptr_t)p & (m - 1)) == 0; };
+        bool v = d.N % 4 == 0 && al(d.Cf, 16) && al(d.resid, 16) && al(d.Cb, 8) && al(d.Cb2, 8) &&
+                 al(d.dact_out, 8) && al(d.mask, 8) && al(d.dact, 8) && al(d.sgd_theta, 16) && al(d.sgd_hi, 8) &&
+                 al(d.sgd_lo, 8);
+        if (d.Cf) v = v && d.ldcf % 4 == 0;
+        if (d.resid) v = v && d.ldr % 4 == 0;
+        if (d.Cb) v = v && d.ldcb % 4 == 0;
+        if (d.dact_out || d.mask || d.dact) v = v && d.ldm % 4 == 0;
+        g.d[i].vec_epi = v ? 1 : 0;
+        g.d[i].prof_snap = nullptr;
+        if (i < n) {
+            tiles += (int)(cdiv(d.M, BM) * cdiv(d.N, BN));
+            pi.gN[i] = d.N;
+        }
+    }
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext("gemm_group_kernel<6, 6>", pi, &ea, &eb);
+    g.prof_snap = prof_snap(h);
+    hipExtLaunchKernelGGL((gemm_group_kernel<OP_KRT, OP_KRT, true>), dim3(tiles), dim3(NT), 0, s, ea, eb, 0, g);
+    prof_end_ext(h);
+    FO_LAUNCHED();
+    return FO_OK;
+}
 
 fo_status gemm(const GemmDesc& d, hipStream_t s) {
     FO_CHECK(d.M > 0 && d.N > 0 && d.K > 0, "gemm: empty problem %dx%dx%d", d.M, d.N, d.K);

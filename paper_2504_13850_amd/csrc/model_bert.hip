@@ -49,12 +49,11 @@ struct Plan {
     // of layer l run on the side stream while the main stream goes on to l - 1
     bf16_t *du2b[2], *dA1[2], *du1b[2], *dqkv[2];
     bf16_t* dO;
-    float *splitws, *splitws2, *slws;
+    float *splitws, *slws;
     // column-sum partials per layer parity, finished on the side stream: the FFN1
     // bias gradient (colwsF), the two norms' dgamma / dbeta / bias gradient
     // (lnpart[parity][0] LN2, [1] LN1); colws2: the side stream's own (bqkv)
     float *colwsF[2], *lnpart[2][2], *colws2;
-    int split_qkv, split_o, split_f1, split_f2;
     float *pooled, *dz, *dpool, *dxc;
     float* xres;  // the last layer's residual input at the first tokens, [B][D]
     // parameter ranges whose SGD update is not fused into a weight-gradient
@@ -350,17 +349,6 @@ __global__ void __launch_bounds__(256) scatter_cls_kernel(const float* __restric
 }
 
 // ------------------------------------------------------------------ plan
-// K slices of a weight-gradient product (static M x N, K = the packed rows):
-// about 300 workgroups in all (these products share the GPU with the
-// input-gradient chain; fewer slices also leave less for the reduction to
-// read), at most four, each at least 256 long.
-int split_for(int M, int N, int K) {
-    int tiles = (int)(cdiv(M, 128) * cdiv(N, 128));
-    int s = std::max(1, std::min(4, 300 / std::max(tiles, 1)));
-    while (s > 1 && (int64_t)K / s < 256) --s;
-    return s;
-}
-
 // Maximum K slices of a forward / input-gradient product over the packed rows;
 // the kernel takes as many of them as the device-side row count needs to fill
 // the CUs (fused epilogue in the reduction pass).  K is the product's full
@@ -424,15 +412,9 @@ size_t ws_bytes(const fo_model* m) {
         add(2 * R * D); add(2 * R * FF); add(2 * R * D); add(2 * R * 3 * D);  // du2b, dA1, du1b, dqkv
     }
     add(2 * R * D);                                 // dO
-    const int K = (int)R;
-    size_t sw = 0;
-    sw = std::max(sw, gemm_ws_bytes(3 * D, D, split_for(3 * D, D, K)));
-    sw = std::max(sw, gemm_ws_bytes(D, D, split_for(D, D, K)));
-    sw = std::max(sw, gemm_ws_bytes(FF, D, split_for(FF, D, K)));
-    sw = std::max(sw, gemm_ws_bytes(D, FF, split_for(D, FF, K)));
-    sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
-    add(sw);
-    add(sw);  // the side stream's split-K partials
+    // split-K partials of the forward and input-gradient products (weight
+    // gradients run unsplit, grouped per layer)
+    add(std::max(gemm_ws_bytes((int)R, D, 4), gemm_ws_bytes((int)B, FF, 4)));
     for (int q = 0; q < 2; ++q) add(4 * colsum_ws_floats((int)R, FF));
     add(4 * colsum_ws_floats((int)R, 3 * D));
     for (int q = 0; q < 4; ++q) add(4 * (size_t)cdiv(R, LNB_ROWS) * 3 * D);
@@ -512,19 +494,8 @@ fo_status init(fo_model* m) {
         P->dqkv[p] = a.take<bf16_t>(R * 3 * D);
     }
     P->dO = a.take<bf16_t>(R * D);
-    const int K = (int)R;
-    P->split_qkv = split_for(3 * D, D, K);
-    P->split_o = split_for(D, D, K);
-    P->split_f1 = split_for(FF, D, K);
-    P->split_f2 = split_for(D, FF, K);
-    size_t sw = 0;
-    sw = std::max(sw, gemm_ws_bytes(3 * D, D, P->split_qkv));
-    sw = std::max(sw, gemm_ws_bytes(D, D, P->split_o));
-    sw = std::max(sw, gemm_ws_bytes(FF, D, P->split_f1));
-    sw = std::max(sw, gemm_ws_bytes(D, FF, P->split_f2));
-    sw = std::max(sw, gemm_ws_bytes((int)R, D, 4));
+    const size_t sw = std::max(gemm_ws_bytes((int)R, D, 4), gemm_ws_bytes((int)B, FF, 4));
     P->splitws = a.take<float>(sw / 4 + 1);
-    P->splitws2 = a.take<float>(sw / 4 + 1);
     for (int q = 0; q < 2; ++q) P->colwsF[q] = a.take<float>(colsum_ws_floats((int)R, FF));
     P->colws2 = a.take<float>(colsum_ws_floats((int)R, 3 * D));
     for (int q = 0; q < 4; ++q) P->lnpart[q / 2][q % 2] = a.take<float>((size_t)cdiv(R, LNB_ROWS) * 3 * D);
@@ -717,8 +688,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     float* prmw = m->params;
     bf16_t* w16 = m->w16;
     bf16_t* w16lo = m->w16lo;
-    auto wgrad = [&](int M_, int N_, const bf16_t* A_, const bf16_t* B_, int64_t off, int K_, const int* Kdev_,
-                     int splits) {
+    auto wgrad = [&](int M_, int N_, const bf16_t* A_, const bf16_t* B_, int64_t off, int K_, const int* Kdev_) {
         GemmDesc w;  // dW = A^T B over K_ rows -> grads; theta -= lr dW; bf16 parts
         w.M = M_; w.N = N_; w.K = K_; w.Kdev = Kdev_;
         w.amode = OP_KR; w.A = A_; w.lda = M_;
@@ -728,8 +698,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         w.sgd_hi = w16 + off;
         w.sgd_lo = w16lo + off;
         w.sgd_lr = lr;
-        w.splits = splits; w.ws = P->splitws2;
-        return gemm(w, s2);
+        return w;
     };
     int cur = 0;
     SplitRows dy_rows;  // the LN2 backward's input: the deferred dX of the layer above
@@ -833,16 +802,16 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             jq.out.p[0] = grd + f.bqkv; jq.out.seg = 3 * D;
             TRY(launch_colsum_finish_multi(cj, s2));
         }
-        if (cls) {  // over the B first-token rows (static count)
-            TRY(wgrad(D, FF, du2b, t.G, f.w2, B, nullptr, 1));
-            TRY(wgrad(FF, D, dA1, t.Hb, f.w1, B, nullptr, 1));
-            TRY(wgrad(D, D, du1b, t.O, f.wo, B, nullptr, 1));
-        } else {
-            TRY(wgrad(D, FF, du2b, t.G, f.w2, rows, Tdev, P->split_f2));  // dW2 = du2^T G
-            TRY(wgrad(FF, D, dA1, t.Hb, f.w1, rows, Tdev, P->split_f1));  // dW1 = dA1^T H
-            TRY(wgrad(D, D, du1b, t.O, f.wo, rows, Tdev, P->split_o));    // dWo = du1^T O
-        }
-        TRY(wgrad(3 * D, D, dqkv, P->Xb[l], f.wqkv, rows, Tdev, P->split_qkv));  // dWqkv = dqkv^T X
+        // the layer's four weight gradients in one launch, each tile over the
+        // whole K (the packed rows, or the B first-token rows of the last layer)
+        GemmDesc wg[4];
+        const int Kw = cls ? B : rows;
+        const int* Kwdev = cls ? nullptr : Tdev;
+        wg[0] = wgrad(D, FF, du2b, t.G, f.w2, Kw, Kwdev);          // dW2 = du2^T G
+        wg[1] = wgrad(FF, D, dA1, t.Hb, f.w1, Kw, Kwdev);          // dW1 = dA1^T H
+        wg[2] = wgrad(D, D, du1b, t.O, f.wo, Kw, Kwdev);           // dWo = du1^T O
+        wg[3] = wgrad(3 * D, D, dqkv, P->Xb[l], f.wqkv, rows, Tdev);  // dWqkv = dqkv^T X
+        TRY(gemm_group(wg, 4, s2));
         FO_HIP(hipEventRecord(P->ev_done[pb], s2));
         cur ^= 1;
     }

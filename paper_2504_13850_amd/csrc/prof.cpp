@@ -158,7 +158,10 @@ extern "C" int32_t fo_profile_read(fo_kernel_stat* out, int32_t max) {
         const int* sn = snap.data() + (size_t)h * kSnapInts;
         double flops = 0, mfma = 0;
         const ProfInfo& f = r.info;
-        if (f.kind == PROF_GEMM) {
+        if (f.kind == PROF_GEMM && f.ngroup > 0) {  // grouped launch: (M, K) per member
+            for (int i = 0; i < f.ngroup && i < 4; ++i) flops += 2.0 * sn[2 * i] * f.gN[i] * sn[2 * i + 1];
+            mfma = flops;
+        } else if (f.kind == PROF_GEMM) {
             double M = sn[0], K = sn[1];  // effective sizes written by the kernel
             flops = 2.0 * M * f.N * K;
             mfma = flops * f.nseg;

@@ -11,6 +11,9 @@ struct ProfInfo {
     int kind = PROF_OTHER;
     // GEMM: algorithmic flops 2*M*N*K with M, K taken from *Mdev / *Kdev when set
     int M = 0, N = 0, K = 0, nseg = 1;
+    // grouped GEMM launch: ngroup products, their N; the kernel snapshots (M, K) of each
+    int ngroup = 0;
+    int gN[4] = {0, 0, 0, 0};
     const int* Mdev = nullptr;
     const int* Kdev = nullptr;
     // attention: cu[B+1] packed offsets, width d
