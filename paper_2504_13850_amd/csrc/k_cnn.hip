@@ -1,6 +1,7 @@
 // Elementwise and reduction kernels of the bf16 CNN server networks (NHWC):
 // layout change at the boundary, 2x2 max pooling, global average pooling,
-// training-mode batch normalisation, ReLU masks, and fp32 -> bf16 splits.
+// training-mode batch normalisation (with the ReLU around it), and fp32 ->
+// bf16 splits.
 // Activations that feed a GEMM are kept as bf16 (high, low) pairs so the
 // forward products can be compensated; gradients are single bf16 (plus fp32
 // where a reduction reads them).
@@ -113,115 +114,238 @@ __global__ void __launch_bounds__(256) gap_relu_bwd(const float* __restrict__ dh
 }
 
 // ---- batch norm (training mode): per-channel statistics over the N*H*W rows
-constexpr int BN_ROWS = 64;
+// A block covers 64 channels (one per lane: each row segment is one 256-byte
+// access per wave) and BN_RPB rows (its four waves take every fourth row).
+// Statistics come in two launches: per row block, partial sums written to
+// part[row block][2][C]; the kernel that applies them first adds up the
+// partials of its own channels (in row-block order, so the result does not
+// depend on scheduling).  Requires C % 64 == 0.
+constexpr int BN_RPB = 32;
+constexpr int BN_PER = BN_RPB / 4;  // rows per wave
 
-// partial column sums of (z - shift) and (z - shift)^2; shift = z of row 0
-// (a per-channel shift keeps the one-pass variance well conditioned)
-__global__ void __launch_bounds__(256) bn_stats_partial(const float* __restrict__ z, int rows, int C,
-                                                        float* __restrict__ part) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    if (c >= C) return;
-    const float sh = z[c];
-    const int r0 = blockIdx.y * BN_ROWS, r1 = min(rows, r0 + BN_ROWS);
-    float s = 0.f, q = 0.f;
-    for (int r = r0; r < r1; ++r) {
-        const float d = z[(int64_t)r * C + c] - sh;
-        s += d;
-        q = fmaf(d, d, q);
+// Sums the S split-K slices ws[z][row][c] of the convolution that produced
+// z (S = 1: z was written by the convolution itself), stores the sum to z,
+// and writes partial sums of (z - shift) and (z - shift)^2 per channel, with
+// shift = the channel's value at row 0 (keeps the one-pass variance well
+// conditioned; every block computes it the same way).  S is a template
+// parameter (up to 8) so that all S x BN_PER loads of a lane are in flight
+// together; the slices are added in index order.
+template <int S>
+__global__ void __launch_bounds__(256) bn_fwd_stats(const float* __restrict__ ws, float* __restrict__ z, int rows,
+                                                    int C, float* __restrict__ part) {
+    __shared__ float red[4][2][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int c = blockIdx.x * 64 + lane;
+    const int r0 = blockIdx.y * BN_RPB;
+    const int64_t full = (int64_t)rows * C;
+    const float* src = S > 1 ? ws : z;
+    float x[S][BN_PER + 1];  // [slice][row], the last row is row 0 (the shift)
+#pragma unroll
+    for (int k = 0; k < S; ++k) {
+#pragma unroll
+        for (int i = 0; i < BN_PER; ++i) {
+            const int r = min(r0 + w + 4 * i, rows - 1);  // rows past the end load the last row and are skipped
+            x[k][i] = src[k * full + (int64_t)r * C + c];
+        }
+        x[k][BN_PER] = src[k * full + c];
     }
-    part[((int64_t)blockIdx.y * 2 + 0) * C + c] = s;
-    part[((int64_t)blockIdx.y * 2 + 1) * C + c] = q;
+    float v[BN_PER + 1];
+#pragma unroll
+    for (int i = 0; i <= BN_PER; ++i) {
+        v[i] = x[0][i];
+#pragma unroll
+        for (int k = 1; k < S; ++k) v[i] += x[k][i];
+    }
+    const float sh = v[BN_PER];
+    float sm = 0.f, sq = 0.f;
+#pragma unroll
+    for (int i = 0; i < BN_PER; ++i) {
+        const int r = r0 + w + 4 * i;
+        if (r < rows) {
+            if (S > 1) z[(int64_t)r * C + c] = v[i];
+            const float d = v[i] - sh;
+            sm += d;
+            sq = fmaf(d, d, sq);
+        }
+    }
+    red[w][0][lane] = sm;
+    red[w][1][lane] = sq;
+    __syncthreads();
+    if (w < 2) {
+        const float t = (red[0][w][lane] + red[1][w][lane]) + (red[2][w][lane] + red[3][w][lane]);
+        part[((int64_t)blockIdx.y * 2 + w) * C + c] = t;
+    }
 }
 
-__global__ void __launch_bounds__(256) bn_stats_finish(const float* __restrict__ z, const float* __restrict__ part,
-                                                       int chunks, int rows, int C, float eps,
-                                                       float* __restrict__ mean, float* __restrict__ rstd) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    if (c >= C) return;
-    double s = 0.0, q = 0.0;
-    for (int k = 0; k < chunks; ++k) {
-        s += part[((int64_t)k * 2 + 0) * C + c];
-        q += part[((int64_t)k * 2 + 1) * C + c];
+// y = relu(gamma (z - mean) rstd + beta [+ residual]) -> fp32 and/or (hi, lo)
+// bf16.  Each block first completes the statistics of its 64 channels from
+// the nrb partial rows (fp64, its waves over interleaved partial rows, then
+// in wave order); row block 0 also stores mean and rstd for the backward.
+__global__ void __launch_bounds__(256) bn_fwd_apply(const float* __restrict__ z, const float* __restrict__ part,
+                                                    int nrb, int rows, int C, float eps, const float* __restrict__ g,
+                                                    const float* __restrict__ beta, const float* __restrict__ resf,
+                                                    const bf16_t* __restrict__ resh, const bf16_t* __restrict__ resl,
+                                                    int relu, float* __restrict__ mean_out,
+                                                    float* __restrict__ rstd_out, float* __restrict__ yf,
+                                                    bf16_t* __restrict__ yh, bf16_t* __restrict__ yl) {
+    __shared__ double red[4][2][64];
+    __shared__ float stat[2][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int c = blockIdx.x * 64 + lane;
+    double s1 = 0.0, s2 = 0.0;
+    int k = w;
+    for (; k + 12 < nrb; k += 16) {  // four partial rows in flight
+        float a[4], b[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            a[u] = part[((int64_t)(k + 4 * u) * 2 + 0) * C + c];
+            b[u] = part[((int64_t)(k + 4 * u) * 2 + 1) * C + c];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            s1 += a[u];
+            s2 += b[u];
+        }
     }
-    const double n = rows, m = s / n;
-    double var = q / n - m * m;
-    var = var < 0.0 ? 0.0 : var;
-    mean[c] = (float)(z[c] + m);
-    rstd[c] = (float)(1.0 / sqrt(var + eps));
-}
-
-// y = relu(gamma (z - mean) rstd + beta [+ residual]) -> (hi, lo) bf16
-__global__ void __launch_bounds__(256) bn_apply(const float* __restrict__ z, const float* __restrict__ mean,
-                                                const float* __restrict__ rstd, const float* __restrict__ g,
-                                                const float* __restrict__ beta, const float* __restrict__ resf,
-                                                const bf16_t* __restrict__ resh, const bf16_t* __restrict__ resl,
-                                                int relu, int64_t total, int C, float* __restrict__ yf,
-                                                bf16_t* __restrict__ yh, bf16_t* __restrict__ yl) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int c = (int)(i % C);
-        float v = fmaf((z[i] - mean[c]) * rstd[c], g[c], beta[c]);
-        if (resf) v += resf[i];
-        if (resh) v += bf2f(resh[i]) + (resl ? bf2f(resl[i]) : 0.f);
+    for (; k < nrb; k += 4) {
+        s1 += part[((int64_t)k * 2 + 0) * C + c];
+        s2 += part[((int64_t)k * 2 + 1) * C + c];
+    }
+    red[w][0][lane] = s1;
+    red[w][1][lane] = s2;
+    __syncthreads();
+    if (w == 0) {
+        const double sm = (red[0][0][lane] + red[1][0][lane]) + (red[2][0][lane] + red[3][0][lane]);
+        const double sq = (red[0][1][lane] + red[1][1][lane]) + (red[2][1][lane] + red[3][1][lane]);
+        const double n = rows, m = sm / n;
+        double var = sq / n - m * m;
+        var = var < 0.0 ? 0.0 : var;
+        const float mean = (float)(z[c] + m), rstd = (float)(1.0 / sqrt(var + eps));
+        stat[0][lane] = mean;
+        stat[1][lane] = rstd;
+        if (blockIdx.y == 0) {
+            mean_out[c] = mean;
+            rstd_out[c] = rstd;
+        }
+    }
+    __syncthreads();
+    const float mean = stat[0][lane], rstd = stat[1][lane];
+    const float gs = g[c] * rstd, bs = fmaf(-mean, gs, beta[c]);  // y = z gs + bs
+    const int r0 = blockIdx.y * BN_RPB;
+#pragma unroll
+    for (int i = 0; i < BN_PER; ++i) {
+        const int r = r0 + w + 4 * i;
+        if (r >= rows) break;
+        const int64_t o = (int64_t)r * C + c;
+        float v = fmaf(z[o], gs, bs);
+        if (resf) v += resf[o];
+        if (resh) v += bf2f(resh[o]) + (resl ? bf2f(resl[o]) : 0.f);
         if (relu) v = v > 0.f ? v : 0.f;
-        if (yf) yf[i] = v;
-        if (yh) split_store(yh, yl, i, v);
+        if (yf) yf[o] = v;
+        if (yh) split_store(yh, yl, o, v);
     }
 }
 
-// dbeta = sum dy, dgamma = sum dy * xhat (partials)
-__global__ void __launch_bounds__(256) bn_bwd_partial(const float* __restrict__ dy, const float* __restrict__ z,
-                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
-                                                      int rows, int C, float* __restrict__ part) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    if (c >= C) return;
-    const int r0 = blockIdx.y * BN_ROWS, r1 = min(rows, r0 + BN_ROWS);
+// Backward partial sums per row block: dbeta = sum dy, dgamma = sum dy xhat,
+// with dy = gout [* (mask > 0)] (the ReLU of the norm's output, when mask is
+// set), which is also stored to dy_out when that is set.
+__global__ void __launch_bounds__(256) bn_bwd_stats(const float* __restrict__ gout, const bf16_t* __restrict__ mask,
+                                                    float* __restrict__ dy_out, const float* __restrict__ z,
+                                                    const float* __restrict__ mean, const float* __restrict__ rstd,
+                                                    int rows, int C, float* __restrict__ part) {
+    __shared__ float red[4][2][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int c = blockIdx.x * 64 + lane;
+    const int r0 = blockIdx.y * BN_RPB;
     const float m = mean[c], rs = rstd[c];
-    float sb = 0.f, sg = 0.f;
-    for (int r = r0; r < r1; ++r) {
-        const float d = dy[(int64_t)r * C + c];
-        sb += d;
-        sg = fmaf(d, (z[(int64_t)r * C + c] - m) * rs, sg);
+    float d[BN_PER], x[BN_PER];
+#pragma unroll
+    for (int i = 0; i < BN_PER; ++i) {
+        const int r = r0 + w + 4 * i;
+        const int64_t o = (int64_t)r * C + c;
+        d[i] = r < rows ? gout[o] : 0.f;
+        x[i] = r < rows ? z[o] : 0.f;
+        if (mask && r < rows && !(bf2f(mask[o]) > 0.f)) d[i] = 0.f;
     }
-    part[((int64_t)blockIdx.y * 2 + 0) * C + c] = sg;
-    part[((int64_t)blockIdx.y * 2 + 1) * C + c] = sb;
+    float sg = 0.f, sb = 0.f;
+#pragma unroll
+    for (int i = 0; i < BN_PER; ++i) {
+        const int r = r0 + w + 4 * i;
+        if (r < rows) {
+            if (dy_out) dy_out[(int64_t)r * C + c] = d[i];
+            sb += d[i];
+            sg = fmaf(d[i], (x[i] - m) * rs, sg);
+        }
+    }
+    red[w][0][lane] = sg;
+    red[w][1][lane] = sb;
+    __syncthreads();
+    if (w < 2) {
+        const float t = (red[0][w][lane] + red[1][w][lane]) + (red[2][w][lane] + red[3][w][lane]);
+        part[((int64_t)blockIdx.y * 2 + w) * C + c] = t;
+    }
 }
 
-__global__ void __launch_bounds__(256) bn_bwd_finish(const float* __restrict__ part, int chunks, int C,
-                                                     float* __restrict__ dg, float* __restrict__ db) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    if (c >= C) return;
+// dz = gamma rstd (dy - dbeta / N - xhat dgamma / N) -> fp32 and/or bf16, dy as
+// in bn_bwd_stats.  Each block completes dgamma and dbeta of its channels from
+// the partial rows (in row-block order); row block 0 stores them.
+__global__ void __launch_bounds__(256) bn_bwd_apply(const float* __restrict__ gout, const bf16_t* __restrict__ mask,
+                                                    const float* __restrict__ z, const float* __restrict__ mean,
+                                                    const float* __restrict__ rstd, const float* __restrict__ g,
+                                                    const float* __restrict__ part, int nrb, int rows, int C,
+                                                    float* __restrict__ dg_out, float* __restrict__ db_out,
+                                                    float* __restrict__ dzf, bf16_t* __restrict__ dzb) {
+    __shared__ float red[4][2][64];
+    __shared__ float stat[2][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int c = blockIdx.x * 64 + lane;
     float sg = 0.f, sb = 0.f;
-    for (int k = 0; k < chunks; ++k) {
+    int k = w;
+    for (; k + 12 < nrb; k += 16) {  // four partial rows in flight
+        float a[4], b[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            a[u] = part[((int64_t)(k + 4 * u) * 2 + 0) * C + c];
+            b[u] = part[((int64_t)(k + 4 * u) * 2 + 1) * C + c];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            sg += a[u];
+            sb += b[u];
+        }
+    }
+    for (; k < nrb; k += 4) {
         sg += part[((int64_t)k * 2 + 0) * C + c];
         sb += part[((int64_t)k * 2 + 1) * C + c];
     }
-    dg[c] = sg;
-    db[c] = sb;
-}
-
-// dz = gamma rstd (dy - dbeta/N - xhat dgamma/N) -> fp32 and bf16
-__global__ void __launch_bounds__(256) bn_bwd_apply(const float* __restrict__ dy, const float* __restrict__ z,
-                                                    const float* __restrict__ mean, const float* __restrict__ rstd,
-                                                    const float* __restrict__ g, const float* __restrict__ dg,
-                                                    const float* __restrict__ db, int rows, int C,
-                                                    float* __restrict__ dzf, bf16_t* __restrict__ dzb) {
-    const int64_t total = (int64_t)rows * C;
-    const float inv = 1.f / (float)rows;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int c = (int)(i % C);
-        const float xh = (z[i] - mean[c]) * rstd[c];
-        const float v = g[c] * rstd[c] * (dy[i] - db[c] * inv - xh * dg[c] * inv);
-        if (dzf) dzf[i] = v;
-        if (dzb) dzb[i] = f2bf(v);
+    red[w][0][lane] = sg;
+    red[w][1][lane] = sb;
+    __syncthreads();
+    if (w == 0) {
+        const float tg = (red[0][0][lane] + red[1][0][lane]) + (red[2][0][lane] + red[3][0][lane]);
+        const float tb = (red[0][1][lane] + red[1][1][lane]) + (red[2][1][lane] + red[3][1][lane]);
+        stat[0][lane] = tg;
+        stat[1][lane] = tb;
+        if (blockIdx.y == 0) {
+            dg_out[c] = tg;
+            db_out[c] = tb;
+        }
     }
-}
-
-// d = dy * [y > 0] (fp32), optionally adding a second gradient
-__global__ void __launch_bounds__(256) relu_mask(const float* __restrict__ dy, const float* __restrict__ add,
-                                                 const bf16_t* __restrict__ y, int64_t total, float* __restrict__ d) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        float v = dy[i] + (add ? add[i] : 0.f);
-        d[i] = bf2f(y[i]) > 0.f ? v : 0.f;
+    __syncthreads();
+    const float inv = 1.f / (float)rows, m = mean[c], rs = rstd[c];
+    const float dgn = stat[0][lane] * inv, dbn = stat[1][lane] * inv, gr = g[c] * rs;
+    const int r0 = blockIdx.y * BN_RPB;
+#pragma unroll
+    for (int i = 0; i < BN_PER; ++i) {
+        const int r = r0 + w + 4 * i;
+        if (r >= rows) break;
+        const int64_t o = (int64_t)r * C + c;
+        float d = gout[o];
+        if (mask && !(bf2f(mask[o]) > 0.f)) d = 0.f;
+        const float xh = (z[o] - m) * rs;
+        const float v = gr * (d - dbn - xh * dgn);
+        if (dzf) dzf[o] = v;
+        if (dzb) dzb[o] = f2bf(v);
     }
 }
 
@@ -268,40 +392,47 @@ fo_status launch_gap_relu_bwd(const float* dh, const bf16_t* y, float* dxf, int 
     return FO_OK;
 }
 
-size_t bn_ws_floats(int rows, int C) { return (size_t)cdiv(rows, BN_ROWS) * 2 * C; }
+size_t bn_ws_floats(int rows, int C) { return (size_t)cdiv(rows, BN_RPB) * 2 * C; }
 
-fo_status launch_bn_stats(const float* z, int rows, int C, float eps, float* mean, float* rstd, float* ws,
-                          hipStream_t s) {
-    const int chunks = (int)cdiv(rows, BN_ROWS);
-    hipLaunchKernelGGL(bn_stats_partial, dim3(cdiv(C, 256), chunks), dim3(256), 0, s, z, rows, C, ws);
-    hipLaunchKernelGGL(bn_stats_finish, dim3(cdiv(C, 256)), dim3(256), 0, s, z, ws, chunks, rows, C, eps, mean, rstd);
+fo_status launch_bn_fwd_stats(const float* ws, int S, float* z, int rows, int C, float* part, hipStream_t s) {
+    FO_CHECK(C % 64 == 0 && rows >= 1, "batch norm: %d channels (multiples of 64), %d rows", C, rows);
+    FO_CHECK(S == 1 || ws != nullptr, "batch norm: %d slices without a workspace", S);
+    const dim3 grid(C / 64, cdiv(rows, BN_RPB));
+    switch (S) {
+        case 1: hipLaunchKernelGGL(bn_fwd_stats<1>, grid, dim3(256), 0, s, ws, z, rows, C, part); break;
+        case 2: hipLaunchKernelGGL(bn_fwd_stats<2>, grid, dim3(256), 0, s, ws, z, rows, C, part); break;
+        case 3: hipLaunchKernelGGL(bn_fwd_stats<3>, grid, dim3(256), 0, s, ws, z, rows, C, part); break;
+        case 4: hipLaunchKernelGGL(bn_fwd_stats<4>, grid, dim3(256), 0, s, ws, z, rows, C, part); break;
+        case 5: hipLaunchKernelGGL(bn_fwd_stats<5>, grid, dim3(256), 0, s, ws, z, rows, C, part); break;
+        case 6: hipLaunchKernelGGL(bn_fwd_stats<6>, grid, dim3(256), 0, s, ws, z, rows, C, part); break;
+        case 7: hipLaunchKernelGGL(bn_fwd_stats<7>, grid, dim3(256), 0, s, ws, z, rows, C, part); break;
+        case 8: hipLaunchKernelGGL(bn_fwd_stats<8>, grid, dim3(256), 0, s, ws, z, rows, C, part); break;
+        default: FO_CHECK(false, "batch norm: %d split-K slices (at most 8)", S);
+    }
     FO_LAUNCHED();
     return FO_OK;
 }
 
-fo_status launch_bn_apply(const float* z, const float* mean, const float* rstd, const float* g, const float* beta,
-                          const float* resf, const bf16_t* resh, const bf16_t* resl, bool relu, int rows, int C,
-                          float* yf, bf16_t* yh, bf16_t* yl, hipStream_t s) {
-    const int64_t total = (int64_t)rows * C;
-    hipLaunchKernelGGL(bn_apply, dim3(grid_for(total)), dim3(256), 0, s, z, mean, rstd, g, beta, resf, resh, resl,
-                       relu ? 1 : 0, total, C, yf, yh, yl);
+fo_status launch_bn_fwd_apply(const float* z, const float* part, int rows, int C, float eps, const float* g,
+                              const float* beta, const float* resf, const bf16_t* resh, const bf16_t* resl, bool relu,
+                              float* mean, float* rstd, float* yf, bf16_t* yh, bf16_t* yl, hipStream_t s) {
+    FO_CHECK(C % 64 == 0 && rows >= 1, "batch norm: %d channels (multiples of 64), %d rows", C, rows);
+    const int nrb = (int)cdiv(rows, BN_RPB);
+    hipLaunchKernelGGL(bn_fwd_apply, dim3(C / 64, nrb), dim3(256), 0, s, z, part, nrb, rows, C, eps, g, beta, resf,
+                       resh, resl, relu ? 1 : 0, mean, rstd, yf, yh, yl);
     FO_LAUNCHED();
     return FO_OK;
 }
 
-fo_status launch_bn_bwd(const float* dy, const float* z, const float* mean, const float* rstd, const float* g,
-                        int rows, int C, float* dg, float* db, float* dzf, bf16_t* dzb, float* ws, hipStream_t s) {
-    const int chunks = (int)cdiv(rows, BN_ROWS);
-    hipLaunchKernelGGL(bn_bwd_partial, dim3(cdiv(C, 256), chunks), dim3(256), 0, s, dy, z, mean, rstd, rows, C, ws);
-    hipLaunchKernelGGL(bn_bwd_finish, dim3(cdiv(C, 256)), dim3(256), 0, s, ws, chunks, C, dg, db);
-    hipLaunchKernelGGL(bn_bwd_apply, dim3(grid_for((int64_t)rows * C)), dim3(256), 0, s, dy, z, mean, rstd, g, dg, db,
-                       rows, C, dzf, dzb);
-    FO_LAUNCHED();
-    return FO_OK;
-}
-
-fo_status launch_relu_mask(const float* dy, const float* add, const bf16_t* y, int64_t n, float* d, hipStream_t s) {
-    hipLaunchKernelGGL(relu_mask, dim3(grid_for(n)), dim3(256), 0, s, dy, add, y, n, d);
+fo_status launch_bn_bwd(const float* gout, const bf16_t* mask, float* dy_out, const float* z, const float* mean,
+                        const float* rstd, const float* g, int rows, int C, float* dg, float* db, float* dzf,
+                        bf16_t* dzb, float* part, hipStream_t s) {
+    FO_CHECK(C % 64 == 0 && rows >= 1, "batch norm: %d channels (multiples of 64), %d rows", C, rows);
+    const int nrb = (int)cdiv(rows, BN_RPB);
+    hipLaunchKernelGGL(bn_bwd_stats, dim3(C / 64, nrb), dim3(256), 0, s, gout, mask, dy_out, z, mean, rstd, rows, C,
+                       part);
+    hipLaunchKernelGGL(bn_bwd_apply, dim3(C / 64, nrb), dim3(256), 0, s, gout, mask, z, mean, rstd, g, part, nrb, rows,
+                       C, dg, db, dzf, dzb);
     FO_LAUNCHED();
     return FO_OK;
 }

@@ -8,37 +8,60 @@ namespace {
 
 // Mean softmax cross-entropy over the batch and dz = (softmax - onehot) / B.
 // Labels outside [0, C) are clamped into range.
-__global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, const int32_t* __restrict__ labels,
-                                                   float* __restrict__ dz, float* __restrict__ loss, int B, int C) {
-    __shared__ float part[256];
-    __shared__ int bad;
-    if (threadIdx.x == 0) bad = 0;
-    __syncthreads();
+// Mean softmax cross-entropy of z [B][C] and dz = (softmax - onehot) / B.
+// One wave per sample (lanes over the classes, 64 at a time; the block's 16
+// waves take samples w, w + 16, ...), max and sum by wave reductions; the
+// loss adds each wave's samples in order, then the waves in order.
+constexpr int XENT_WAVES = 16;
+__device__ __forceinline__ float xent_wave_max(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+    return v;
+}
+__device__ __forceinline__ float xent_wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+__global__ void __launch_bounds__(64 * XENT_WAVES) xent_kernel(const float* __restrict__ z,
+                                                               const int32_t* __restrict__ labels,
+                                                               float* __restrict__ dz, float* __restrict__ loss, int B,
+                                                               int C) {
+    __shared__ float part[XENT_WAVES];
+    __shared__ int bad_w[XENT_WAVES];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     float mine = 0.f;
-    for (int b = threadIdx.x; b < B; b += blockDim.x) {
+    int bad = 0;
+    for (int b = w; b < B; b += XENT_WAVES) {
         const float* zr = z + (int64_t)b * C;
-        float m = zr[0];
-        for (int c = 1; c < C; ++c) m = fmaxf(m, zr[c]);
+        float m = -INFINITY;
+        for (int c = lane; c < C; c += 64) m = fmaxf(m, zr[c]);
+        m = xent_wave_max(m);
         float s = 0.f;
-        for (int c = 0; c < C; ++c) s += expf(zr[c] - m);
-        float lse = m + logf(s);
+        for (int c = lane; c < C; c += 64) s += expf(zr[c] - m);
+        const float lse = m + logf(xent_wave_sum(s));
         int y = labels[b];
-        if (y < 0 || y >= C) {  // reported through loss[1]; clamped so that every access stays in bounds
-            atomicAdd(&bad, 1);
+        if (y < 0 || y >= C) {  // counted into loss[1]; clamped so that every access stays in bounds
+            bad++;
             y = y < 0 ? 0 : C - 1;
         }
         mine += lse - zr[y];
-        for (int c = 0; c < C; ++c) dz[(int64_t)b * C + c] = (expf(zr[c] - lse) - (c == y ? 1.f : 0.f)) / (float)B;
+        for (int c = lane; c < C; c += 64) dz[(int64_t)b * C + c] = (expf(zr[c] - lse) - (c == y ? 1.f : 0.f)) / (float)B;
     }
-    part[threadIdx.x] = mine;
+    if (lane == 0) {
+        part[w] = mine;
+        bad_w[w] = bad;
+    }
     __syncthreads();
-    for (int s = blockDim.x / 2; s > 0; s >>= 1) {
-        if (threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
-        __syncthreads();
-    }
     if (threadIdx.x == 0) {
-        loss[0] = part[0] / (float)B;
-        loss[1] = (float)bad;
+        float t = 0.f;
+        int nb = 0;
+        for (int k = 0; k < XENT_WAVES; ++k) {
+            t += part[k];
+            nb += bad_w[k];
+        }
+        loss[0] = t / (float)B;
+        loss[1] = (float)nb;
     }
 }
 
@@ -308,7 +331,7 @@ __global__ void __launch_bounds__(256) small_linear_dgrad_finish(const float* __
 }  // namespace
 
 fo_status launch_xent(const float* z, const int32_t* labels, float* dz, float* loss, int B, int C, hipStream_t s) {
-    hipLaunchKernelGGL(xent_kernel, dim3(1), dim3(256), 0, s, z, labels, dz, loss, B, C);
+    hipLaunchKernelGGL(xent_kernel, dim3(1), dim3(64 * XENT_WAVES), 0, s, z, labels, dz, loss, B, C);
     FO_LAUNCHED();
     return FO_OK;
 }

@@ -25,14 +25,14 @@ fo_status launch_maxpool_relu_bwd(const float* dy, const uint8_t* arg, const bf1
 fo_status launch_gap_fwd(const bf16_t* xh, const bf16_t* xl, float* h, int B, int HW, int C, hipStream_t s);
 fo_status launch_gap_relu_bwd(const float* dh, const bf16_t* y, float* dxf, int B, int HW, int C, hipStream_t s);
 size_t bn_ws_floats(int rows, int C);
-fo_status launch_bn_stats(const float* z, int rows, int C, float eps, float* mean, float* rstd, float* ws,
-                          hipStream_t s);
-fo_status launch_bn_apply(const float* z, const float* mean, const float* rstd, const float* g, const float* beta,
-                          const float* resf, const bf16_t* resh, const bf16_t* resl, bool relu, int rows, int C,
-                          float* yf, bf16_t* yh, bf16_t* yl, hipStream_t s);
-fo_status launch_bn_bwd(const float* dy, const float* z, const float* mean, const float* rstd, const float* g,
-                        int rows, int C, float* dg, float* db, float* dzf, bf16_t* dzb, float* ws, hipStream_t s);
-fo_status launch_relu_mask(const float* dy, const float* add, const bf16_t* y, int64_t n, float* d, hipStream_t s);
+// batch norm (training mode) over rows x C (C % 64 == 0); see k_cnn.hip
+fo_status launch_bn_fwd_stats(const float* ws, int S, float* z, int rows, int C, float* part, hipStream_t s);
+fo_status launch_bn_fwd_apply(const float* z, const float* part, int rows, int C, float eps, const float* g,
+                              const float* beta, const float* resf, const bf16_t* resh, const bf16_t* resl, bool relu,
+                              float* mean, float* rstd, float* yf, bf16_t* yh, bf16_t* yl, hipStream_t s);
+fo_status launch_bn_bwd(const float* gout, const bf16_t* mask, float* dy_out, const float* z, const float* mean,
+                        const float* rstd, const float* g, int rows, int C, float* dg, float* db, float* dzf,
+                        bf16_t* dzb, float* part, hipStream_t s);
 fo_status launch_to_bf16(const float* x, bf16_t* y, int64_t n, hipStream_t s);
 
 namespace {
@@ -54,6 +54,7 @@ struct Conv {
     // activations
     bf16_t *yh, *yl;            // VGG: post-ReLU output (hi, lo)
     float *z, *mean, *rstd;     // ResNet: pre-norm output and its batch statistics
+    float* part;                // ResNet: the norm's per-row-block partial sums
 };
 
 struct Pool {
@@ -199,7 +200,7 @@ size_t ws_bytes(const fo_model* m) {
     for (const Conv& c : P.convs) {
         const size_t n = (size_t)B * c.Ho * c.Wo * c.cout;
         amax = std::max(amax, n);
-        if (P.resnet) { add(4 * n); add(4 * c.cout); add(4 * c.cout); }
+        if (P.resnet) { add(4 * n); add(4 * c.cout); add(4 * c.cout); add(4 * bn_ws_floats(B * c.Ho * c.Wo, c.cout)); }
         else { add(2 * n); add(2 * n); }
         sw = std::max(sw, gemm_ws_bytes(c.cout, c.k * c.k * c.cin, c.splits));
         sw = std::max(sw, gemm_ws_bytes(B * c.Ho * c.Wo, c.cout, c.fsplits));
@@ -248,6 +249,7 @@ fo_status init(fo_model* m) {
             c.z = a.take<float>(n);
             c.mean = a.take<float>(c.cout);
             c.rstd = a.take<float>(c.cout);
+            c.part = a.take<float>(bn_ws_floats(B * c.Ho * c.Wo, c.cout));
         } else {
             c.yh = a.take<bf16_t>(n);
             c.yl = a.take<bf16_t>(n);
@@ -462,29 +464,30 @@ fo_status step_resnet(fo_model* m, Plan* P, int B, const int32_t* labels) {
     for (Block& b : P->blocks) {
         Conv &c1 = P->convs[b.c1], &c2 = P->convs[b.c2];
         const int rows = B * c2.Ho * c2.Wo;
-        GemmDesc d1 = conv_fwd_desc(m, c1, B, xh, xl);
-        d1.Cf = c1.z; d1.ldcf = c1.cout;
-        TRY(gemm(d1, s));
-        TRY(launch_bn_stats(c1.z, rows, c1.cout, eps, c1.mean, c1.rstd, P->redws, s));
-        TRY(launch_bn_apply(c1.z, c1.mean, c1.rstd, m->params + c1.g, m->params + c1.be, nullptr, nullptr, nullptr,
-                            true, rows, c1.cout, nullptr, b.a1h, b.a1l, s));
-        GemmDesc d2 = conv_fwd_desc(m, c2, B, b.a1h, b.a1l);
-        d2.Cf = c2.z; d2.ldcf = c2.cout;
-        TRY(gemm(d2, s));
-        TRY(launch_bn_stats(c2.z, rows, c2.cout, eps, c2.mean, c2.rstd, P->redws, s));
+        // Each convolution leaves its split-K partials to the statistics kernel of
+        // its norm, which sums them into z.
+        auto conv_bn_stats = [&](Conv& c, const bf16_t* inh, const bf16_t* inl) -> fo_status {
+            GemmDesc d = conv_fwd_desc(m, c, B, inh, inl);
+            d.Cf = c.z; d.ldcf = c.cout;
+            d.defer_reduce = true;
+            TRY(gemm(d, s));
+            return launch_bn_fwd_stats(P->splitws, d.splits, c.z, rows, c.cout, c.part, s);
+        };
+        auto bn_apply = [&](Conv& c, const float* resf, const bf16_t* resh, const bf16_t* resl, bool relu, float* yf,
+                            bf16_t* yh, bf16_t* yl) {
+            return launch_bn_fwd_apply(c.z, c.part, rows, c.cout, eps, m->params + c.g, m->params + c.be, resf, resh,
+                                       resl, relu, c.mean, c.rstd, yf, yh, yl, s);
+        };
+        TRY(conv_bn_stats(c1, xh, xl));
+        TRY(bn_apply(c1, nullptr, nullptr, nullptr, true, nullptr, b.a1h, b.a1l));
+        TRY(conv_bn_stats(c2, b.a1h, b.a1l));
         if (b.cd >= 0) {
             Conv& cd = P->convs[b.cd];
-            GemmDesc dd = conv_fwd_desc(m, cd, B, xh, xl);
-            dd.Cf = cd.z; dd.ldcf = cd.cout;
-            TRY(gemm(dd, s));
-            TRY(launch_bn_stats(cd.z, rows, cd.cout, eps, cd.mean, cd.rstd, P->redws, s));
-            TRY(launch_bn_apply(cd.z, cd.mean, cd.rstd, m->params + cd.g, m->params + cd.be, nullptr, nullptr,
-                                nullptr, false, rows, cd.cout, b.scf, nullptr, nullptr, s));
-            TRY(launch_bn_apply(c2.z, c2.mean, c2.rstd, m->params + c2.g, m->params + c2.be, b.scf, nullptr, nullptr,
-                                true, rows, c2.cout, nullptr, b.outh, b.outl, s));
+            TRY(conv_bn_stats(cd, xh, xl));
+            TRY(bn_apply(cd, nullptr, nullptr, nullptr, false, b.scf, nullptr, nullptr));
+            TRY(bn_apply(c2, b.scf, nullptr, nullptr, true, nullptr, b.outh, b.outl));
         } else {
-            TRY(launch_bn_apply(c2.z, c2.mean, c2.rstd, m->params + c2.g, m->params + c2.be, nullptr, xh, xl, true,
-                                rows, c2.cout, nullptr, b.outh, b.outl, s));
+            TRY(bn_apply(c2, nullptr, xh, xl, true, nullptr, b.outh, b.outl));
         }
         xh = b.outh; xl = b.outl;
     }
@@ -505,16 +508,14 @@ fo_status step_resnet(fo_model* m, Plan* P, int B, const int32_t* labels) {
         Block& b = P->blocks[bi];
         Conv &c1 = P->convs[b.c1], &c2 = P->convs[b.c2];
         const int rows = B * c2.Ho * c2.Wo;
-        const int64_t n = (int64_t)rows * c2.cout;
-        float* g = P->df[1];  // gradient of the pre-ReLU sum
-        TRY(launch_relu_mask(gout, nullptr, b.outh, n, g, s));
-        // main branch: second conv + norm
-        TRY(launch_bn_bwd(g, c2.z, c2.mean, c2.rstd, m->params + c2.g, rows, c2.cout, m->grads + c2.g,
-                          m->grads + c2.be, nullptr, P->db[0], P->redws, s));
+        float* g = P->df[1];  // gradient of the pre-ReLU sum (stored by the first norm backward)
+        // main branch: second conv + norm (its input gradient is gout through the block's ReLU)
+        TRY(launch_bn_bwd(gout, b.outh, g, c2.z, c2.mean, c2.rstd, m->params + c2.g, rows, c2.cout, m->grads + c2.g,
+                          m->grads + c2.be, nullptr, P->db[0], c2.part, s));
         TRY(conv_wgrad(m, P, c2, B, P->db[0], b.a1h));
         TRY(conv_dgrad(m, c2, B, P->db[0], b.a1h, nullptr, P->dtmp, nullptr));
-        TRY(launch_bn_bwd(P->dtmp, c1.z, c1.mean, c1.rstd, m->params + c1.g, rows, c1.cout, m->grads + c1.g,
-                          m->grads + c1.be, nullptr, P->db[1], P->redws, s));
+        TRY(launch_bn_bwd(P->dtmp, nullptr, nullptr, c1.z, c1.mean, c1.rstd, m->params + c1.g, rows, c1.cout,
+                          m->grads + c1.g, m->grads + c1.be, nullptr, P->db[1], c1.part, s));
         const bf16_t* xin_h = bi == 0 ? P->xin : P->blocks[bi - 1].outh;
         TRY(conv_wgrad(m, P, c1, B, P->db[1], xin_h));
         const bool need_dx = bi > 0;
@@ -523,8 +524,8 @@ fo_status step_resnet(fo_model* m, Plan* P, int B, const int32_t* labels) {
         const float* sc_grad = g;
         if (b.cd >= 0) {
             Conv& cd = P->convs[b.cd];
-            TRY(launch_bn_bwd(g, cd.z, cd.mean, cd.rstd, m->params + cd.g, rows, cd.cout, m->grads + cd.g,
-                              m->grads + cd.be, nullptr, P->db[0], P->redws, s));
+            TRY(launch_bn_bwd(g, nullptr, nullptr, cd.z, cd.mean, cd.rstd, m->params + cd.g, rows, cd.cout,
+                              m->grads + cd.g, m->grads + cd.be, nullptr, P->db[0], cd.part, s));
             TRY(conv_wgrad(m, P, cd, B, P->db[0], xin_h));
             if (need_dx) TRY(conv_dgrad(m, cd, B, P->db[0], nullptr, nullptr, P->dsc, nullptr));
             sc_grad = P->dsc;
