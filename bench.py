@@ -382,30 +382,33 @@ def bench_vgg128(args, A, torch, S):
     n = cfg.agg_n
     glob = torch.from_numpy(S.make_global_vector(cid)).cuda()
     locs = torch.from_numpy(S.make_local_vectors(cid, K)).cuda()
-    dev_version = [0] * K
+    dev_version = np.zeros(K, np.int64)
     seq = [0]
     tallies = {"arrivals": 0, "applied": 0, "skipped": 0, "drains": 0, "idle_steps": 0}
+    # raw device addresses of the bank's batches and labels and of the device-side models
+    acts_base, lab_base, loc_base = (np.uint64(t.data_ptr()) for t in (acts_d, labels_d, locs))
+    act_stride, lab_stride, loc_stride = np.uint64(slot_bytes), np.uint64(4 * B), np.uint64(4 * n)
 
     def one_step(t):
-        senders = []
-        row = counts[t]
-        for k in np.nonzero(row)[0].tolist():
-            for _ in range(int(row[k])):
-                i = seq[0] % bank_n
-                seq[0] += 1
-                A.fo_queues_push(q, k, acts_d[i], labels_d[i])
-                A.fo_queues_push_model(q, k, locs[k], dev_version[k])
-                senders.append(k)
-        tallies["arrivals"] += len(senders)
+        # this step's arrivals, in device order: one activation send attempt and one
+        # model message each (Alg. 2 put()), handed over in two calls
+        senders = np.repeat(np.arange(K, dtype=np.int32), counts[t])
+        m = int(senders.size)
+        if m:
+            idx = (np.uint64(seq[0]) + np.arange(m, dtype=np.uint64)) % np.uint64(bank_n)
+            seq[0] += m
+            A.fo_queues_push_batch(q, senders, acts_base + idx * act_stride, lab_base + idx * lab_stride)
+            A.fo_queues_push_model_batch(q, senders, loc_base + senders.astype(np.uint64) * loc_stride, n,
+                                         dev_version[senders])
+        tallies["arrivals"] += m
         k = A.fo_pick_device(q)
         if k == -2:  # Alg. 3: models first
             applied, skipped = A.fo_aggregate_pending_all(q, glob, 1.0)
             tallies["applied"] += applied
             tallies["skipped"] += skipped
             tallies["drains"] += 1
-            v = A.fo_queues_stats(q).version
-            for kk in senders:  # each sender receives the aggregated global (Alg. 4)
-                dev_version[kk] = v
+            # each sender receives the aggregated global (Alg. 4)
+            dev_version[senders] = A.fo_queues_stats(q).version
             k = A.fo_pick_device(q)
         if k < 0:
             tallies["idle_steps"] += 1

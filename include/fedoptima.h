@@ -131,10 +131,12 @@ FO_API fo_status fo_server_step(fo_model* model, const fo_acts* acts, const int3
 
 /* Process-wide switch for how fo_server_step issues its kernels (default 1).
  * Every step of a model at one batch size is the same sequence of launches
- * over the same buffers, so with enable != 0 the step copies the batch (and
- * labels, lengths) into staging buffers owned by the model, captures the
- * launch sequence once per batch size into a HIP graph on a private stream,
- * and replays that graph on the model's stream afterwards.  Results are
+ * over the same buffers: the step's first launch stores the batch pointers
+ * (activations, labels, lengths) in a model-owned device record that the
+ * other kernels read.  With enable != 0 the launch sequence is captured once
+ * per batch size into a HIP graph on a private stream and replayed on the
+ * model's stream afterwards, with only that first launch's arguments changed
+ * to the new batch's pointers (the batch is never copied).  Results are
  * bit-identical to enable == 0, which launches every kernel directly.  While
  * the calling thread profiles (fo_profile_enable) steps always launch
  * directly.  Steps already captured stay cached until fo_model_destroy.
@@ -209,16 +211,37 @@ FO_API void fo_queues_destroy(fo_queues* q);
 /* put() for an activation batch from device k (Alg. 2).  x_src holds
  * slot_bytes, labels_src batch int32, lengths_src batch int32 (if the pool has
  * lengths); src_on_host says whether the sources are host or device memory.
- * The copies into the slot are ordered on the pool's stream.  Returns FO_OK
+ * The copies into the slot are ordered on the pool's stream: from device
+ * memory (activations 16-byte aligned) one kernel launch moves the
+ * activations, labels and lengths; from host memory, or from unaligned device
+ * activations, one copy each.  Returns FO_OK
  * (admitted), FO_FULL (refused by flow control; nothing copied) or an error
  * (FO_EINVAL: k out of range, NULL source for a pool with device memory). */
 FO_API fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, const int32_t* labels_src,
                          const int32_t* lengths_src, int32_t src_on_host);
 
+/* put() for n activation batches in arrival order: the same admissions,
+ * refusals, slots and sequence numbers as n fo_queues_push calls.  k[i] is the
+ * sending device; x_src[i], labels_src[i] and (if the pool has lengths)
+ * lengths_src[i] are device pointers, the activations 16-byte aligned.
+ * status_out[i] (host, may be NULL) receives FO_OK (admitted) or FO_FULL
+ * (refused by flow control).  The copies of the admitted batches run on the
+ * pool's stream, up to 32 batches per launch.  Every entry is checked before
+ * anything changes (FO_EINVAL: device out of range, NULL or unaligned source);
+ * after a failed launch (FO_EHIP) the batches admitted so far are queued but
+ * may not have been copied. */
+FO_API fo_status fo_queues_push_batch(fo_queues* q, int32_t n, const int32_t* k, const void* const* x_src,
+                                      const int32_t* const* labels_src, const int32_t* const* lengths_src,
+                                      int32_t* status_out);
+
 /* put() for a model message from device k with local version t_k (Alg. 2):
  * appended to the model FIFO.  `local` (device fp32[n]) is not copied and must
  * stay valid until the message is aggregated. */
 FO_API fo_status fo_queues_push_model(fo_queues* q, int32_t k, const float* local, int64_t n, int64_t t_k);
+/* The same for n messages in arrival order (device k[i], vector local[i] of
+ * len floats, version t_k[i]); every entry is checked before any is queued. */
+FO_API fo_status fo_queues_push_model_batch(fo_queues* q, int32_t n, const int32_t* k, const float* const* local,
+                                            int64_t len, const int64_t* t_k);
 
 /* get() (Alg. 3).  Returns:
  *   -2  a model message is pending; serve it first (fo_aggregate_pending);

@@ -26,7 +26,8 @@ EXPORTS = [
     "fo_queues_push", "fo_queues_push_model", "fo_pick_device", "fo_queues_in_service",
     "fo_queues_release", "fo_aggregate_pending", "fo_aggregate_pending_all", "fo_queues_stats",
     "fo_queues_counters", "fo_queues_add_device", "fo_last_error", "fo_profile_enable", "fo_profile_read",
-    "fo_set_graph_mode", "fo_gemm_bf16", "fo_conv2d_bf16", "fo_gemm_bf16_noalloc",
+    "fo_set_graph_mode", "fo_gemm_bf16", "fo_conv2d_bf16", "fo_gemm_bf16_noalloc", "fo_queues_push_batch",
+    "fo_queues_push_model_batch",
 ]
 FO_LAYOUT_ROW_K, FO_LAYOUT_K_ROW = 0, 1
 
@@ -89,6 +90,8 @@ def lib():
             "fo_queues_destroy": (None, [vp]),
             "fo_queues_push": (C.c_int, [vp, i32, vp, vp, vp, i32]),
             "fo_queues_push_model": (C.c_int, [vp, i32, vp, i64, i64]),
+            "fo_queues_push_batch": (C.c_int, [vp, i32, vp, vp, vp, vp, vp]),
+            "fo_queues_push_model_batch": (C.c_int, [vp, i32, vp, vp, i64, vp]),
             "fo_pick_device": (i32, [vp]),
             "fo_queues_in_service": (C.c_int, [vp, C.POINTER(fo_acts), C.POINTER(vp), C.POINTER(i64),
                                                C.POINTER(i64)]),
@@ -230,6 +233,26 @@ def fo_queues_destroy(q):
 def fo_queues_push(q, k: int, x=None, labels=None, lengths=None, on_host: bool = False) -> int:
     return _check(lib().fo_queues_push(q, k, _dptr(x), _dptr(labels), _dptr(lengths), int(on_host)),
                   (FO_OK, FO_FULL))
+
+
+def fo_queues_push_batch(q, k, x_ptrs=None, label_ptrs=None, length_ptrs=None) -> np.ndarray:
+    """n arrivals: k, x_ptrs, label_ptrs, length_ptrs are sequences of device ids and
+    raw device addresses (ints).  Returns the per-entry status (FO_OK / FO_FULL)."""
+    kk = np.ascontiguousarray(k, dtype=np.int32)
+    n = int(kk.size)
+    arr = lambda v: None if v is None else np.ascontiguousarray(v, dtype=np.uint64)
+    xs, ls, ns = arr(x_ptrs), arr(label_ptrs), arr(length_ptrs)
+    st = np.zeros(n, np.int32)
+    _check(lib().fo_queues_push_batch(q, n, kk.ctypes.data, _dptr(xs), _dptr(ls), _dptr(ns), st.ctypes.data))
+    return st
+
+
+def fo_queues_push_model_batch(q, k, local_ptrs, length: int, t_k):
+    kk = np.ascontiguousarray(k, dtype=np.int32)
+    ps = np.ascontiguousarray(local_ptrs, dtype=np.uint64)
+    tt = np.ascontiguousarray(t_k, dtype=np.int64)
+    _check(lib().fo_queues_push_model_batch(q, int(kk.size), kk.ctypes.data, ps.ctypes.data, int(length),
+                                            tt.ctypes.data))
 
 
 def fo_queues_push_model(q, k: int, local, t_k: int):

@@ -92,9 +92,7 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
     if (bf16) add(sizeof(bf16_t) * np);               // shadow (low part)
     add(sizeof(float) * (size_t)max_batch * m->classes);
     add(sizeof(float) * 64);
-    add((size_t)fam->sample_bytes * max_batch);       // staged batch (graph replay)
-    add(sizeof(int32_t) * max_batch);                 // staged labels
-    add(sizeof(int32_t) * max_batch);                 // staged lengths
+    add(sizeof(StepIn));                              // the step's batch pointers
     bytes += fam->workspace_bytes(m) + 4096;
     hipError_t e = hipMalloc((void**)&m->mem, bytes);
     if (e != hipSuccess) {
@@ -111,9 +109,7 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
     if (bf16) m->w16lo = m->arena.take<bf16_t>(np);
     m->logits = m->arena.take<float>((size_t)max_batch * m->classes);
     m->loss = m->arena.take<float>(64);
-    m->stage_x = m->arena.take<char>((size_t)fam->sample_bytes * max_batch);
-    m->stage_labels = m->arena.take<int32_t>(max_batch);
-    m->stage_lengths = m->arena.take<int32_t>(max_batch);
+    m->dev_in = m->arena.take<StepIn>(1);
     fo_status st = FO_OK;
     e = hipMemcpyAsync(m->params, host_init, sizeof(float) * np, hipMemcpyHostToDevice, m->stream);
     if (e == hipSuccess) e = hipMemsetAsync(m->grads, 0, sizeof(float) * np, m->stream);
@@ -143,7 +139,10 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
 extern "C" void fo_model_destroy(fo_model* m) {
     if (!m) return;
     if (m->mem) (void)hipStreamSynchronize(m->stream);
-    for (auto& kv : m->graphs) (void)hipGraphExecDestroy(kv.second);
+    for (auto& kv : m->graphs) {
+        if (kv.second.exec) (void)hipGraphExecDestroy(kv.second.exec);
+        if (kv.second.graph) (void)hipGraphDestroy(kv.second.graph);
+    }
     m->graphs.clear();
     if (m->capture_stream) (void)hipStreamDestroy(m->capture_stream);
     if (m->fam && m->plan) m->fam->destroy(m);
@@ -155,65 +154,113 @@ extern "C" void fo_model_destroy(fo_model* m) {
 // A step is a fixed sequence of launches for a given batch size (sizes that
 // depend on the batch's contents, such as the packed token count, stay on the
 // device), so it is captured once per batch size into a HIP graph and replayed:
-// one launch instead of one per kernel.  The batch, labels and lengths are first
-// copied into model-owned buffers, so the graph never names the caller's
-// pointers.  Capture runs on a private stream (the null stream cannot be
-// captured) with the model's stream swapped for it; replays go to the model's
-// stream.
+// one launch instead of one per kernel.  The kernels read the batch through
+// the model's StepIn record, which the step's first launch (latch_inputs)
+// fills; that launch is the graph's only root, and before each replay its
+// arguments are set to the new batch's pointers, so the batch is never copied.
+// Capture runs on a private stream (the null stream cannot be captured) with
+// the model's stream swapped for it; replays go to the model's stream.
 static int g_graph_mode = 1;
+
+__global__ void latch_inputs(StepIn* __restrict__ in, const void* x, const int32_t* labels, const int32_t* lengths) {
+    in->x = x;
+    in->labels = labels;
+    in->lengths = lengths;
+}
+
+static fo_status launch_latch(fo_model* m, const fo_acts* acts, const int32_t* labels, hipStream_t s) {
+    hipLaunchKernelGGL(latch_inputs, dim3(1), dim3(1), 0, s, m->dev_in, acts->x, labels, acts->lengths);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+// The step as launched directly: the latch, then the family's kernels.
+static fo_status step_direct(fo_model* m, const fo_acts* acts, const int32_t* labels) {
+    fo_status st = launch_latch(m, acts, labels, m->stream);
+    return st != FO_OK ? st : m->fam->step(m, acts, labels);
+}
+
+static fo_status capture_step(fo_model* m, const fo_acts* acts, const int32_t* labels, fo_model::Captured* out) {
+    if (!m->capture_stream && hipStreamCreateWithFlags(&m->capture_stream, hipStreamNonBlocking) != hipSuccess) {
+        m->capture_stream = nullptr;
+        set_error("fo_server_step: hipStreamCreateWithFlags failed");
+        return FO_EHIP;
+    }
+    hipStream_t user = m->stream;
+    hipError_t e = hipStreamBeginCapture(m->capture_stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) {
+        set_error("fo_server_step: hipStreamBeginCapture: %s", hipGetErrorString(e));
+        return FO_EHIP;
+    }
+    m->stream = m->capture_stream;
+    const fo_status st = step_direct(m, acts, labels);
+    m->stream = user;
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(m->capture_stream, &g);
+    if (st != FO_OK || e != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        if (st != FO_OK) return st;
+        set_error("fo_server_step: hipStreamEndCapture: %s", hipGetErrorString(e));
+        return FO_EHIP;
+    }
+    // the latch is the graph's only root: every other launch follows it in stream order
+    size_t nroot = 0;
+    e = hipGraphGetRootNodes(g, nullptr, &nroot);
+    hipGraphNode_t root = nullptr;
+    hipGraphNodeType type = hipGraphNodeTypeEmpty;
+    if (e == hipSuccess && nroot == 1) e = hipGraphGetRootNodes(g, &root, &nroot);
+    if (e == hipSuccess && nroot == 1) e = hipGraphNodeGetType(root, &type);
+    if (e != hipSuccess || nroot != 1 || type != hipGraphNodeTypeKernel) {
+        (void)hipGraphDestroy(g);
+        set_error("fo_server_step: the captured step does not start with its input latch (%zu roots)", nroot);
+        return FO_EHIP;
+    }
+    hipGraphExec_t ex = nullptr;
+    e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+        (void)hipGraphDestroy(g);
+        set_error("fo_server_step: hipGraphInstantiate: %s", hipGetErrorString(e));
+        return FO_EHIP;
+    }
+    out->graph = g;
+    out->exec = ex;
+    out->latch = root;
+    return FO_OK;
+}
 
 static fo_status step_graph(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     const int B = acts->batch;
-    hipError_t e = hipMemcpyAsync(m->stage_x, acts->x, (size_t)m->fam->sample_bytes * B, hipMemcpyDeviceToDevice,
-                                  m->stream);
-    if (e == hipSuccess)
-        e = hipMemcpyAsync(m->stage_labels, labels, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, m->stream);
-    if (e == hipSuccess && acts->lengths)
-        e = hipMemcpyAsync(m->stage_lengths, acts->lengths, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, m->stream);
-    if (e != hipSuccess) {
-        set_error("fo_server_step: staging copy: %s", hipGetErrorString(e));
-        return FO_EHIP;
-    }
     auto it = m->graphs.find(B);
     if (it == m->graphs.end()) {
-        if (!m->capture_stream && hipStreamCreateWithFlags(&m->capture_stream, hipStreamNonBlocking) != hipSuccess) {
-            m->capture_stream = nullptr;
-            set_error("fo_server_step: hipStreamCreateWithFlags failed");
-            return FO_EHIP;
+        fo_model::Captured c;
+        fo_status st = capture_step(m, acts, labels, &c);
+        if (st != FO_OK) return st;
+        try {
+            it = m->graphs.emplace(B, c).first;
+        } catch (...) {
+            (void)hipGraphExecDestroy(c.exec);
+            (void)hipGraphDestroy(c.graph);
+            set_error("fo_server_step: out of host memory");
+            return FO_ENOMEM;
         }
-        fo_acts staged;
-        staged.x = m->stage_x;
-        staged.lengths = acts->lengths ? m->stage_lengths : nullptr;
-        staged.batch = B;
-        hipStream_t user = m->stream;
-        e = hipStreamBeginCapture(m->capture_stream, hipStreamCaptureModeThreadLocal);
-        if (e != hipSuccess) {
-            set_error("fo_server_step: hipStreamBeginCapture: %s", hipGetErrorString(e));
-            return FO_EHIP;
-        }
-        m->stream = m->capture_stream;
-        const fo_status st = m->fam->step(m, &staged, m->stage_labels);
-        m->stream = user;
-        hipGraph_t g = nullptr;
-        e = hipStreamEndCapture(m->capture_stream, &g);
-        if (st != FO_OK || e != hipSuccess) {
-            if (g) (void)hipGraphDestroy(g);
-            if (st != FO_OK) return st;
-            set_error("fo_server_step: hipStreamEndCapture: %s", hipGetErrorString(e));
-            return FO_EHIP;
-        }
-        hipGraphExec_t ex = nullptr;
-        e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
-        (void)hipGraphDestroy(g);
-        if (e != hipSuccess) {
-            set_error("fo_server_step: hipGraphInstantiate: %s", hipGetErrorString(e));
-            return FO_EHIP;
-        }
-        it = m->graphs.emplace(B, ex).first;
     }
-    e = hipGraphLaunch(it->second, m->stream);
+    // this batch's pointers into the latch launch
+    StepIn* in = m->dev_in;
+    const void* x = acts->x;
+    const int32_t* lab = labels;
+    const int32_t* len = acts->lengths;
+    void* args[] = {&in, &x, &lab, &len};
+    hipKernelNodeParams p = {};
+    p.func = reinterpret_cast<void*>(&latch_inputs);
+    p.gridDim = dim3(1);
+    p.blockDim = dim3(1);
+    p.sharedMemBytes = 0;
+    p.kernelParams = args;
+    p.extra = nullptr;
+    hipError_t e = hipGraphExecKernelNodeSetParams(it->second.exec, it->second.latch, &p);
+    if (e == hipSuccess) e = hipGraphLaunch(it->second.exec, m->stream);
     if (e != hipSuccess) {
-        set_error("fo_server_step: hipGraphLaunch: %s", hipGetErrorString(e));
+        set_error("fo_server_step: graph replay: %s", hipGetErrorString(e));
         return FO_EHIP;
     }
     return FO_OK;
@@ -238,7 +285,7 @@ extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int3
     fo_status st = pool_step_begin(acts, labels, device_id, m->stream, &owner);
     if (st != FO_OK) return st;
     // Kernel profiling records every launch with its own events: run eagerly then.
-    st = (g_graph_mode && !prof_active()) ? step_graph(m, acts, labels) : m->fam->step(m, acts, labels);
+    st = (g_graph_mode && !prof_active()) ? step_graph(m, acts, labels) : step_direct(m, acts, labels);
     if (st != FO_OK) return st;
     if (owner) {
         st = pool_step_done(owner, m->stream);

@@ -79,6 +79,16 @@ __device__ inline uint32_t f2bf2(float a, float b) {
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// The batch of a training step as its kernels read it: a model-owned device
+// record that the step's first launch fills with the caller's pointers, so
+// that a captured step can be replayed on another batch by changing the
+// arguments of that one launch (no copy of the batch).
+struct StepIn {
+    const void* x;
+    const int32_t* labels;
+    const int32_t* lengths;
+};
+
 // Device memory arena: one hipMalloc, bump allocation, 256-byte alignment.
 struct Arena {
     char* base = nullptr;

@@ -16,10 +16,11 @@ __device__ __forceinline__ void split_store(bf16_t* hi, bf16_t* lo, int64_t i, f
     if (lo) lo[i] = f2bf(v - bf2f(h));
 }
 
-// x [B][C][H][W] -> y [B][H][W][C] (bf16 bits)
-__global__ void __launch_bounds__(256) nchw_to_nhwc(const bf16_t* __restrict__ x, bf16_t* __restrict__ y, int B,
+// x [B][C][H][W] -> y [B][H][W][C] (bf16 bits); x is the step's batch (in->x)
+__global__ void __launch_bounds__(256) nchw_to_nhwc(const StepIn* __restrict__ in, bf16_t* __restrict__ y, int B,
                                                     int C, int HW) {
     __shared__ bf16_t tile[32][33];
+    const bf16_t* __restrict__ x = static_cast<const bf16_t*>(in->x);
     const int b = blockIdx.z;
     const int c0 = blockIdx.y * 32, p0 = blockIdx.x * 32;
     const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
@@ -358,8 +359,8 @@ inline int grid_for(int64_t n) { return (int)std::min<int64_t>(cdiv(n, 256), 819
 
 }  // namespace
 
-fo_status launch_nchw_to_nhwc(const bf16_t* x, bf16_t* y, int B, int C, int HW, hipStream_t s) {
-    hipLaunchKernelGGL(nchw_to_nhwc, dim3(cdiv(HW, 32), cdiv(C, 32), B), dim3(256), 0, s, x, y, B, C, HW);
+fo_status launch_nchw_to_nhwc(const StepIn* in, bf16_t* y, int B, int C, int HW, hipStream_t s) {
+    hipLaunchKernelGGL(nchw_to_nhwc, dim3(cdiv(HW, 32), cdiv(C, 32), B), dim3(256), 0, s, in, y, B, C, HW);
     FO_LAUNCHED();
     return FO_OK;
 }

@@ -24,10 +24,11 @@ __device__ __forceinline__ float xent_wave_sum(float v) {
     return v;
 }
 __global__ void __launch_bounds__(64 * XENT_WAVES) xent_kernel(const float* __restrict__ z,
-                                                               const int32_t* __restrict__ labels,
+                                                               const StepIn* __restrict__ in,
                                                                float* __restrict__ dz, float* __restrict__ loss, int B,
                                                                int C) {
     __shared__ float part[XENT_WAVES];
+    const int32_t* __restrict__ labels = in->labels;
     __shared__ int bad_w[XENT_WAVES];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     float mine = 0.f;
@@ -330,8 +331,8 @@ __global__ void __launch_bounds__(256) small_linear_dgrad_finish(const float* __
 
 }  // namespace
 
-fo_status launch_xent(const float* z, const int32_t* labels, float* dz, float* loss, int B, int C, hipStream_t s) {
-    hipLaunchKernelGGL(xent_kernel, dim3(1), dim3(64 * XENT_WAVES), 0, s, z, labels, dz, loss, B, C);
+fo_status launch_xent(const float* z, const StepIn* in, float* dz, float* loss, int B, int C, hipStream_t s) {
+    hipLaunchKernelGGL(xent_kernel, dim3(1), dim3(64 * XENT_WAVES), 0, s, z, in, dz, loss, B, C);
     FO_LAUNCHED();
     return FO_OK;
 }

@@ -108,6 +108,88 @@ static int stream_grid(int64_t n4, int64_t chunk) {
 }
 static int stream_grid(int64_t n4) { return stream_grid(n4, SCHUNK); }
 
+// ------------------------------------------------------------------ pool arrival
+// One admitted activation batch into its pool slot: the activations (n16
+// 16-byte chunks) and the int32 labels and lengths (batch each, lengths
+// optional) in one launch.  The first block also copies labels and lengths.
+__global__ void __launch_bounds__(256) pool_put_kernel(const uint4* __restrict__ xs, uint4* __restrict__ xd,
+                                                       int64_t n16, const int32_t* __restrict__ ls,
+                                                       int32_t* __restrict__ ld, const int32_t* __restrict__ ns,
+                                                       int32_t* __restrict__ nd, int batch) {
+    const int64_t stride = (int64_t)gridDim.x * 256 * SU;
+    for (int64_t base = (int64_t)blockIdx.x * 256 * SU + threadIdx.x; base < n16; base += stride) {
+        uint4 v[SU];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int64_t i = base + 256 * u;
+            if (i < n16) v[u] = xs[i];
+        }
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int64_t i = base + 256 * u;
+            if (i < n16) xd[i] = v[u];
+        }
+    }
+    if (blockIdx.x == 0)
+        for (int b = threadIdx.x; b < batch; b += 256) {
+            ld[b] = ls[b];
+            if (nd) nd[b] = ns[b];
+        }
+}
+
+fo_status launch_pool_put(const void* x_src, void* x_dst, int64_t bytes, const int32_t* lab_src, int32_t* lab_dst,
+                          const int32_t* len_src, int32_t* len_dst, int batch, hipStream_t s) {
+    FO_CHECK(bytes % 16 == 0 && ((uintptr_t)x_src & 15) == 0 && ((uintptr_t)x_dst & 15) == 0,
+             "pool put: the activations must be whole, 16-byte aligned chunks");
+    const int64_t n16 = bytes / 16;
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cdiv(n16, 256 * SU), 1024));
+    hipLaunchKernelGGL(pool_put_kernel, dim3(grid), dim3(256), 0, s, (const uint4*)x_src, (uint4*)x_dst, n16, lab_src,
+                       lab_dst, len_src, len_dst, batch);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+// Up to kPutMaxBatches admitted batches in one launch: blockIdx.y = the batch,
+// blocks along x stride over its activations; block (0, y) copies its labels
+// and lengths.
+__global__ void __launch_bounds__(256) pool_put_gather_kernel(const PutTable t, int64_t n16, int batch) {
+    const int e = blockIdx.y;
+    const uint4* __restrict__ xs = t.xs[e];
+    uint4* __restrict__ xd = t.xd[e];
+    const int64_t stride = (int64_t)gridDim.x * 256 * SU;
+    for (int64_t base = (int64_t)blockIdx.x * 256 * SU + threadIdx.x; base < n16; base += stride) {
+        uint4 v[SU];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int64_t i = base + 256 * u;
+            if (i < n16) v[u] = xs[i];
+        }
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int64_t i = base + 256 * u;
+            if (i < n16) xd[i] = v[u];
+        }
+    }
+    if (blockIdx.x == 0)
+        for (int b = threadIdx.x; b < batch; b += 256) {
+            t.ld[e][b] = t.ls[e][b];
+            if (t.nd[e]) t.nd[e][b] = t.ns[e][b];
+        }
+}
+
+fo_status launch_pool_put_gather(const PutTable& t, int64_t bytes, int batch, hipStream_t s) {
+    FO_CHECK(t.count >= 1 && t.count <= kPutMaxBatches, "pool put: %d batches in one launch", t.count);
+    FO_CHECK(bytes % 16 == 0, "pool put: slot bytes not a multiple of 16");
+    for (int i = 0; i < t.count; ++i)
+        FO_CHECK(((uintptr_t)t.xs[i] & 15) == 0 && ((uintptr_t)t.xd[i] & 15) == 0,
+                 "pool put: activations of batch %d not 16-byte aligned", i);
+    const int64_t n16 = bytes / 16;
+    const int gx = (int)std::max<int64_t>(1, std::min<int64_t>(cdiv(n16, 256 * SU), 128));
+    hipLaunchKernelGGL(pool_put_gather_kernel, dim3(gx, t.count), dim3(256), 0, s, t, n16, batch);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
 fo_status launch_agg_lerp(float* g, const float* l, int64_t n, float w, hipStream_t s) {
     if (n == 0) return FO_OK;
     int64_t n4 = n / 4;

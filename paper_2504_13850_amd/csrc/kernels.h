@@ -15,6 +15,22 @@ struct AggTable {
     float w[kAggMaxFused];
 };
 fo_status launch_agg_lerp(float* g, const float* l, int64_t n, float w, hipStream_t s);
+// One activation batch (bytes, a multiple of 16; 16-byte aligned device
+// pointers), its labels and (if len_src) lengths into a pool slot: one launch.
+fo_status launch_pool_put(const void* x_src, void* x_dst, int64_t bytes, const int32_t* lab_src, int32_t* lab_dst,
+                          const int32_t* len_src, int32_t* len_dst, int batch, hipStream_t s);
+// Several admitted batches (same slot size) in one launch.
+constexpr int kPutMaxBatches = 32;
+struct PutTable {
+    const uint4* xs[kPutMaxBatches];
+    uint4* xd[kPutMaxBatches];
+    const int32_t* ls[kPutMaxBatches];
+    int32_t* ld[kPutMaxBatches];
+    const int32_t* ns[kPutMaxBatches];
+    int32_t* nd[kPutMaxBatches];
+    int count;
+};
+fo_status launch_pool_put_gather(const PutTable& t, int64_t bytes, int batch, hipStream_t s);
 fo_status launch_agg_lerp_multi(float* g, const AggTable& tab, int64_t n, hipStream_t s);
 // theta -= lr * g (momentum v <- mu v + g first when v is set); refreshes the
 // bf16 high/low shadows of theta when w16/w16lo are set.
@@ -54,7 +70,8 @@ fo_status launch_attn_cls_bwd(const bf16_t* qkv, const bf16_t* qkvlo, const int*
 // mean cross-entropy of logits z [B][C] and dz = (softmax - onehot)/B into
 // loss[0]; loss[1] receives the number of labels outside [0, C) (each clamped
 // to the nearest class so that every access stays in bounds)
-fo_status launch_xent(const float* z, const int32_t* labels, float* dz, float* loss, int B, int C, hipStream_t s);
+// (labels: in->labels, device int32[B])
+fo_status launch_xent(const float* z, const StepIn* in, float* dz, float* loss, int B, int C, hipStream_t s);
 // out[c] = sum over rows r < min(rows, *rows_dev) of X[r*ld + c]; ws holds colsum_ws_floats(rows, N)
 size_t colsum_ws_floats(int rows, int N);
 fo_status launch_colsum(const float* X, int64_t ld, int rows, const int* rows_dev, int N, float* out, float* ws,

@@ -31,13 +31,18 @@ struct fo_model {
     int64_t steps_total = 0;
     std::vector<int64_t> steps_per_device;
 
-    // Graph replay of the step: the batch is first copied into these model-owned
-    // buffers, so the captured launches never name the caller's pointers.
-    void* stage_x = nullptr;             // max_batch * sample bytes
-    int32_t* stage_labels = nullptr;     // [max_batch]
-    int32_t* stage_lengths = nullptr;    // [max_batch]
+    // The batch pointers of the current step (device record read by the step's
+    // kernels; filled by the step's first launch).
+    fo::StepIn* dev_in = nullptr;
+    // Graph replay of the step: one captured graph per batch size; its only root
+    // is the launch that fills dev_in, whose arguments change per replay.
+    struct Captured {
+        hipGraph_t graph = nullptr;
+        hipGraphExec_t exec = nullptr;
+        hipGraphNode_t latch = nullptr;
+    };
     hipStream_t capture_stream = nullptr;  // private (capture cannot run on the null stream)
-    std::map<int32_t, hipGraphExec_t> graphs;  // one per batch size
+    std::map<int32_t, Captured> graphs;    // one per batch size
 
     char* mem = nullptr;       // one allocation for everything above and the workspace
     fo::Arena arena;

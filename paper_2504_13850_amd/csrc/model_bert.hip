@@ -73,9 +73,10 @@ struct Plan {
 // thread per sequence computes its rank, one thread the prefix sum.
 // Lengths outside [1, Lmax] are clamped (every access then stays in bounds)
 // and counted into *bad_out.
-__global__ void __launch_bounds__(256) build_cu_kernel(const int32_t* __restrict__ lengths, int B, int Lmax,
+__global__ void __launch_bounds__(256) build_cu_kernel(const StepIn* __restrict__ in, int B, int Lmax,
                                                        int* __restrict__ cu, float* __restrict__ bad_out) {
     extern __shared__ int lens[];
+    const int32_t* __restrict__ lengths = in->lengths;
     __shared__ int bad;
     if (threadIdx.x == 0) bad = 0;
     __syncthreads();
@@ -105,8 +106,9 @@ __global__ void __launch_bounds__(256) build_cu_kernel(const int32_t* __restrict
 }
 
 // padded [B][L][D] bf16 -> packed rows (bf16 and fp32 copies)
-__global__ void __launch_bounds__(256) pack_kernel(const bf16_t* __restrict__ x, const int* __restrict__ cu, int B,
+__global__ void __launch_bounds__(256) pack_kernel(const StepIn* __restrict__ in, const int* __restrict__ cu, int B,
                                                    bf16_t* __restrict__ xb, float* __restrict__ xf) {
+    const bf16_t* __restrict__ x = static_cast<const bf16_t*>(in->x);
     const int64_t total = (int64_t)B * L * (D / 8);
     for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
          idx += (int64_t)gridDim.x * blockDim.x) {
@@ -593,12 +595,12 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     const float* prm = m->params;
     float* grd = m->grads;
 
-    hipLaunchKernelGGL(build_cu_kernel, dim3(1), dim3(256), sizeof(int) * B, s, acts->lengths, B, L, P->cu,
+    hipLaunchKernelGGL(build_cu_kernel, dim3(1), dim3(256), sizeof(int) * B, s, m->dev_in, B, L, P->cu,
                        m->loss + 2);
     {
         int64_t total = (int64_t)rows * (D / 8);
         int grid = (int)std::min<int64_t>(cdiv(total, 256), 8192);
-        hipLaunchKernelGGL(pack_kernel, dim3(grid), dim3(256), 0, s, (const bf16_t*)acts->x, P->cu, B, P->Xb[0],
+        hipLaunchKernelGGL(pack_kernel, dim3(grid), dim3(256), 0, s, m->dev_in, P->cu, B, P->Xb[0],
                            P->Xf[0]);
     }
     FO_LAUNCHED();
@@ -666,7 +668,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     const float* xcls = P->Xf[NL];
     TRY(launch_small_linear_fwd(xcls, prm + P->pool_w, prm + P->pool_b, P->pooled, B, D, D, true, s));
     TRY(launch_small_linear_fwd(P->pooled, prm + P->cls_w, prm + P->cls_b, m->logits, B, D, NC, false, s));
-    TRY(launch_xent(m->logits, labels, P->dz, m->loss, B, NC, s));
+    TRY(launch_xent(m->logits, m->dev_in, P->dz, m->loss, B, NC, s));
 
     // ---------------- backward (Alg. 4: backward pass of M_s)
     TRY(launch_small_linear_bwd(P->dz, P->pooled, prm + P->cls_w, P->pooled, grd + P->cls_w, grd + P->cls_b,

@@ -17,7 +17,7 @@
 
 namespace fo {
 
-fo_status launch_nchw_to_nhwc(const bf16_t* x, bf16_t* y, int B, int C, int HW, hipStream_t s);
+fo_status launch_nchw_to_nhwc(const StepIn* in, bf16_t* y, int B, int C, int HW, hipStream_t s);
 fo_status launch_maxpool_fwd(const bf16_t* xh, const bf16_t* xl, bf16_t* yh, bf16_t* yl, uint8_t* arg, int B, int H,
                              int W, int C, hipStream_t s);
 fo_status launch_maxpool_relu_bwd(const float* dy, const uint8_t* arg, const bf16_t* y, float* dxf, bf16_t* dxb, int B,
@@ -410,7 +410,7 @@ fo_status step_vgg(fo_model* m, Plan* P, int B, const int32_t* labels) {
     TRY(fc_fwd(m, f0, B, xh, xl, true, nullptr, f0.yh, f0.yl));
     TRY(fc_fwd(m, f1, B, f0.yh, f0.yl, true, nullptr, f1.yh, f1.yl));
     TRY(fc_fwd(m, f2, B, f1.yh, f1.yl, false, m->logits, nullptr, nullptr));
-    TRY(launch_xent(m->logits, labels, P->dz, m->loss, B, f2.out, s));
+    TRY(launch_xent(m->logits, m->dev_in, P->dz, m->loss, B, f2.out, s));
     // backward through the classifier
     TRY(launch_to_bf16(P->dz, P->dzb, (int64_t)B * f2.out, s));
     TRY(fc_bwd(m, P, f2, B, P->dz, P->dzb, f1.yh, f1.yh, P->df[0], P->db[0]));
@@ -498,7 +498,7 @@ fo_status step_resnet(fo_model* m, Plan* P, int B, const int32_t* labels) {
     TRY(launch_cast_bf16(P->gap, P->gaph, P->gapl, (int64_t)B * 512, s));
     Fc& fc = P->fcs[0];
     TRY(fc_fwd(m, fc, B, P->gaph, P->gapl, false, m->logits, nullptr, nullptr));
-    TRY(launch_xent(m->logits, labels, P->dz, m->loss, B, fc.out, s));
+    TRY(launch_xent(m->logits, m->dev_in, P->dz, m->loss, B, fc.out, s));
     TRY(launch_to_bf16(P->dz, P->dzb, (int64_t)B * fc.out, s));
     TRY(fc_bwd(m, P, fc, B, P->dz, P->dzb, P->gaph, nullptr, P->df[1], nullptr));
     // gradient of the last block's output (through the average pool and its ReLU)
@@ -543,7 +543,7 @@ fo_status step_resnet(fo_model* m, Plan* P, int B, const int32_t* labels) {
 fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     Plan* P = (Plan*)m->plan;
     const int B = acts->batch;
-    TRY(launch_nchw_to_nhwc((const bf16_t*)acts->x, P->xin, B, kIn, kHW * kHW, m->stream));
+    TRY(launch_nchw_to_nhwc(m->dev_in, P->xin, B, kIn, kHW * kHW, m->stream));
     return P->resnet ? step_resnet(m, P, B, labels) : step_vgg(m, P, B, labels);
 }
 

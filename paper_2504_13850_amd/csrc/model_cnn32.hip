@@ -33,10 +33,12 @@ struct Plan {
     float *d1;       // dpre conv1    [B,64,16,16]
 };
 
-// y[b,co,y,x] = relu(bias[co] + sum_{ci,ky,kx} x[b,ci,y+ky-1,x+kx-1] w[co,ky,kx,ci])
-__global__ void conv3x3_fwd_relu(const float* __restrict__ x, const float* __restrict__ w,
-                                 const float* __restrict__ bias, float* __restrict__ y, int B, int Ci, int Co,
-                                 int H, int W) {
+// y[b,co,y,x] = relu(bias[co] + sum_{ci,ky,kx} x[b,ci,y+ky-1,x+kx-1] w[co,ky,kx,ci]);
+// x is the step's batch (in->x) when in is set
+__global__ void conv3x3_fwd_relu(const float* __restrict__ x_, const StepIn* __restrict__ in,
+                                 const float* __restrict__ w, const float* __restrict__ bias, float* __restrict__ y,
+                                 int B, int Ci, int Co, int H, int W) {
+    const float* __restrict__ x = in ? static_cast<const float*>(in->x) : x_;
     int idx = blockIdx.x * blockDim.x + threadIdx.x;
     int total = B * Co * H * W;
     if (idx >= total) return;
@@ -128,9 +130,11 @@ __global__ void gap_relu_bwd(const float* __restrict__ dh, const float* __restri
 
 // Weight and bias gradient of a 3x3 pad-1 conv: one block per (co, ci),
 // threads stride over (b, y, x), nine partial sums, block reduction.
-__global__ void __launch_bounds__(256) conv3x3_wgrad(const float* __restrict__ d, const float* __restrict__ x,
-                                                     float* __restrict__ gw, float* __restrict__ gb, int B, int Ci,
-                                                     int Co, int H, int W) {
+// (x is the step's batch, in->x, when in is set)
+__global__ void __launch_bounds__(256) conv3x3_wgrad(const float* __restrict__ d, const float* __restrict__ x_,
+                                                     const StepIn* __restrict__ in, float* __restrict__ gw,
+                                                     float* __restrict__ gb, int B, int Ci, int Co, int H, int W) {
+    const float* __restrict__ x = in ? static_cast<const float*>(in->x) : x_;
     int ci = blockIdx.x % Ci, co = blockIdx.x / Ci;
     float acc[9];
 #pragma unroll
@@ -254,19 +258,20 @@ fo_status init(fo_model* m) {
 fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     Plan* P = (Plan*)m->plan;
     hipStream_t s = m->stream;
-    const int B = acts->batch;
-    const float* x = (const float*)acts->x;
+    const int B = acts->batch;  // (the batch's data is read through m->dev_in)
     // forward (Alg. 4: forward pass of M_s, loss f_s)
-    hipLaunchKernelGGL(conv3x3_fwd_relu, dim3(nb((int64_t)B * C1 * H0 * W0)), dim3(256), 0, s, x, P->w1, P->b1,
+    hipLaunchKernelGGL(conv3x3_fwd_relu, dim3(nb((int64_t)B * C1 * H0 * W0)), dim3(256), 0, s, nullptr, m->dev_in,
+                       P->w1, P->b1,
                        P->y1, B, C0, C1, H0, W0);
     hipLaunchKernelGGL(maxpool2_fwd, dim3(nb((int64_t)B * C1 * H1 * W1)), dim3(256), 0, s, P->y1, P->p1, P->arg1,
                        B * C1, H0, W0);
-    hipLaunchKernelGGL(conv3x3_fwd_relu, dim3(nb((int64_t)B * C2 * H1 * W1)), dim3(256), 0, s, P->p1, P->w2, P->b2,
+    hipLaunchKernelGGL(conv3x3_fwd_relu, dim3(nb((int64_t)B * C2 * H1 * W1)), dim3(256), 0, s, P->p1, nullptr,
+                       P->w2, P->b2,
                        P->y2, B, C1, C2, H1, W1);
     hipLaunchKernelGGL(gap_fwd, dim3(nb(B * C2)), dim3(256), 0, s, P->y2, P->h, B * C2, H1 * W1);
     hipLaunchKernelGGL(linear_fwd, dim3(nb(B * NCLS)), dim3(256), 0, s, P->h, P->wf, P->bf, m->logits, B, C2, NCLS);
     FO_LAUNCHED();
-    fo_status st = launch_xent(m->logits, labels, P->dz, m->loss, B, NCLS, s);
+    fo_status st = launch_xent(m->logits, m->dev_in, P->dz, m->loss, B, NCLS, s);
     if (st != FO_OK) return st;
     // backward (Alg. 4: backward pass of M_s)
     int64_t lin_threads = (int64_t)(NCLS * C2 > B * C2 ? NCLS * C2 : B * C2);
@@ -274,13 +279,15 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
                        B, C2, NCLS);
     hipLaunchKernelGGL(gap_relu_bwd, dim3(nb((int64_t)B * C2 * H1 * W1)), dim3(256), 0, s, P->dh, P->y2, P->d2,
                        B * C2, H1 * W1);
-    hipLaunchKernelGGL(conv3x3_wgrad, dim3(C2 * C1), dim3(256), 0, s, P->d2, P->p1, P->gw2, P->gb2, B, C1, C2, H1,
+    hipLaunchKernelGGL(conv3x3_wgrad, dim3(C2 * C1), dim3(256), 0, s, P->d2, P->p1, nullptr, P->gw2, P->gb2, B, C1,
+                       C2, H1,
                        W1);
     hipLaunchKernelGGL(conv3x3_dgrad, dim3(nb((int64_t)B * C1 * H1 * W1)), dim3(256), 0, s, P->d2, P->w2, P->dp1, B,
                        C1, C2, H1, W1);
     hipLaunchKernelGGL(maxpool2_relu_bwd, dim3(nb((int64_t)B * C1 * H0 * W0)), dim3(256), 0, s, P->dp1, P->arg1,
                        P->y1, P->d1, B * C1, H0, W0);
-    hipLaunchKernelGGL(conv3x3_wgrad, dim3(C1 * C0), dim3(256), 0, s, P->d1, x, P->gw1, P->gb1, B, C0, C1, H0, W0);
+    hipLaunchKernelGGL(conv3x3_wgrad, dim3(C1 * C0), dim3(256), 0, s, P->d1, nullptr, m->dev_in, P->gw1, P->gb1, B,
+                       C0, C1, H0, W0);
     FO_LAUNCHED();
     // SGD (Alg. 4: theta_s <- theta_s - gamma_s grad)
     return launch_sgd(m->params, m->grads, nullptr, nullptr, nullptr, m->n_params, m->lr, 0.f, s);

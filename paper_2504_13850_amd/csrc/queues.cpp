@@ -207,15 +207,13 @@ fo_status pool_step_done(fo_queues* q, hipStream_t step_stream) {
 
 }  // namespace fo
 
-extern "C" fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, const int32_t* labels_src,
-                                    const int32_t* lengths_src, int32_t src_on_host) {
-    FO_CHECK(q != nullptr, "fo_queues_push: NULL handle");
-    FO_CHECK(k >= 0 && k < q->K, "fo_queues_push: device %d out of range [0,%d)", k, q->K);
-    if (q->slab) {
-        FO_CHECK(x_src != nullptr && labels_src != nullptr, "fo_queues_push: NULL source");
-        FO_CHECK(!q->with_lengths || lengths_src != nullptr, "fo_queues_push: this pool needs lengths");
-    }
-    // Alg. 2 / Sec. 3.4.1: a batch sent while the Sender Status is off never arrives.
+namespace {
+
+// put() bookkeeping of one activation batch from device k (Alg. 2, Sec. 3.4.1):
+// FO_FULL when the Sender Status is off (the batch never arrives), else the
+// slot it goes to (*slot_out), with the pool's stream ordered after any step
+// on another stream that last read that slot.
+fo_status admit(fo_queues* q, int32_t k, int64_t* slot_out) {
     if (!q->sender_on[k]) {
         q->refused++;
         return FO_FULL;
@@ -224,21 +222,12 @@ extern "C" fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, 
         fo::set_error("fo_queues_push: pool exhausted (internal invariant broken)");
         return FO_ESTATE;
     }
-    int64_t slot = q->free_stack.back();
+    const int64_t slot = q->free_stack.back();
     auto g = q->guard.find(slot);
     if (g != q->guard.end()) {  // a step on another stream read this slot: copy after it
         FO_HIP(hipStreamWaitEvent(q->stream, g->second, 0));
         q->ev_free.push_back(g->second);
         q->guard.erase(g);
-    }
-    if (q->slab) {
-        hipMemcpyKind kind = src_on_host ? hipMemcpyHostToDevice : hipMemcpyDeviceToDevice;
-        FO_HIP(hipMemcpyAsync(q->slab + slot * q->slot_bytes, x_src, (size_t)q->slot_bytes, kind, q->stream));
-        FO_HIP(hipMemcpyAsync(q->labels + slot * q->batch, labels_src, sizeof(int32_t) * q->batch, kind,
-                              q->stream));
-        if (q->with_lengths)
-            FO_HIP(hipMemcpyAsync(q->lengths + slot * q->batch, lengths_src, sizeof(int32_t) * q->batch, kind,
-                                  q->stream));
     }
     try {
         q->q[k].push_back({q->next_seq[k], slot});
@@ -253,7 +242,81 @@ extern "C" fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, 
     if (q->queued > q->peak) q->peak = q->queued;
     q->sender_on[k] = 0;   // deactivated until the server turns it on
     q->turn_on_check(k);   // enqueue: below the cap -> 'turn-on'
+    *slot_out = slot;
     return FO_OK;
+}
+
+}  // namespace
+
+extern "C" fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, const int32_t* labels_src,
+                                    const int32_t* lengths_src, int32_t src_on_host) {
+    FO_CHECK(q != nullptr, "fo_queues_push: NULL handle");
+    FO_CHECK(k >= 0 && k < q->K, "fo_queues_push: device %d out of range [0,%d)", k, q->K);
+    if (q->slab) {
+        FO_CHECK(x_src != nullptr && labels_src != nullptr, "fo_queues_push: NULL source");
+        FO_CHECK(!q->with_lengths || lengths_src != nullptr, "fo_queues_push: this pool needs lengths");
+    }
+    int64_t slot = -1;
+    fo_status st = admit(q, k, &slot);
+    if (st != FO_OK || !q->slab) return st;
+    char* xd = q->slab + slot * q->slot_bytes;
+    int32_t* ld = q->labels + slot * q->batch;
+    int32_t* nd = q->with_lengths ? q->lengths + slot * q->batch : nullptr;
+    if (!src_on_host && ((uintptr_t)x_src & 15) == 0)  // device sources: one launch for the three parts
+        return fo::launch_pool_put(x_src, xd, q->slot_bytes, labels_src, ld, nd ? lengths_src : nullptr, nd, q->batch,
+                                   q->stream);
+    hipMemcpyKind kind = src_on_host ? hipMemcpyHostToDevice : hipMemcpyDeviceToDevice;
+    FO_HIP(hipMemcpyAsync(xd, x_src, (size_t)q->slot_bytes, kind, q->stream));
+    FO_HIP(hipMemcpyAsync(ld, labels_src, sizeof(int32_t) * q->batch, kind, q->stream));
+    if (nd) FO_HIP(hipMemcpyAsync(nd, lengths_src, sizeof(int32_t) * q->batch, kind, q->stream));
+    return FO_OK;
+}
+
+extern "C" fo_status fo_queues_push_batch(fo_queues* q, int32_t n, const int32_t* k, const void* const* x_src,
+                                          const int32_t* const* labels_src, const int32_t* const* lengths_src,
+                                          int32_t* status_out) {
+    FO_CHECK(q != nullptr, "fo_queues_push_batch: NULL handle");
+    FO_CHECK(n >= 0 && (n == 0 || k != nullptr), "fo_queues_push_batch: n=%d", n);
+    for (int32_t i = 0; i < n; ++i) {  // every argument checked before any state changes
+        FO_CHECK(k[i] >= 0 && k[i] < q->K, "fo_queues_push_batch: entry %d: device %d out of range [0,%d)", i, k[i],
+                 q->K);
+        if (q->slab) {
+            FO_CHECK(x_src && labels_src && x_src[i] && labels_src[i], "fo_queues_push_batch: entry %d: NULL source",
+                     i);
+            FO_CHECK(((uintptr_t)x_src[i] & 15) == 0, "fo_queues_push_batch: entry %d: activations not 16-byte aligned",
+                     i);
+            FO_CHECK(!q->with_lengths || (lengths_src && lengths_src[i]),
+                     "fo_queues_push_batch: entry %d: this pool needs lengths", i);
+        }
+    }
+    fo::PutTable t;
+    t.count = 0;
+    auto flush = [&]() -> fo_status {
+        if (t.count == 0) return FO_OK;
+        fo_status st = fo::launch_pool_put_gather(t, q->slot_bytes, q->batch, q->stream);
+        t.count = 0;
+        return st;
+    };
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t slot = -1;
+        fo_status st = admit(q, k[i], &slot);
+        if (status_out) status_out[i] = st == FO_FULL ? FO_FULL : FO_OK;
+        if (st == FO_FULL) continue;
+        if (st != FO_OK) return st;
+        if (!q->slab) continue;
+        const int e = t.count++;
+        t.xs[e] = (const uint4*)x_src[i];
+        t.xd[e] = (uint4*)(q->slab + slot * q->slot_bytes);
+        t.ls[e] = labels_src[i];
+        t.ld[e] = q->labels + slot * q->batch;
+        t.ns[e] = q->with_lengths ? lengths_src[i] : nullptr;
+        t.nd[e] = q->with_lengths ? q->lengths + slot * q->batch : nullptr;
+        if (t.count == fo::kPutMaxBatches) {
+            st = flush();
+            if (st != FO_OK) return st;
+        }
+    }
+    return flush();
 }
 
 extern "C" fo_status fo_queues_push_model(fo_queues* q, int32_t k, const float* local, int64_t n, int64_t t_k) {
@@ -265,6 +328,25 @@ extern "C" fo_status fo_queues_push_model(fo_queues* q, int32_t k, const float* 
         q->qm.push_back({k, local, n, t_k});
     } catch (...) {
         set_error("fo_queues_push_model: out of host memory");
+        return FO_ENOMEM;
+    }
+    return FO_OK;
+}
+
+extern "C" fo_status fo_queues_push_model_batch(fo_queues* q, int32_t n, const int32_t* k, const float* const* local,
+                                                int64_t len, const int64_t* t_k) {
+    FO_CHECK(q != nullptr, "fo_queues_push_model_batch: NULL handle");
+    FO_CHECK(n >= 0 && (n == 0 || (k != nullptr && t_k != nullptr)), "fo_queues_push_model_batch: n=%d", n);
+    FO_CHECK(len >= 0 && (len == 0 || n == 0 || local != nullptr), "fo_queues_push_model_batch: bad vectors");
+    for (int32_t i = 0; i < n; ++i) {
+        FO_CHECK(k[i] >= 0 && k[i] < q->K, "fo_queues_push_model_batch: entry %d: device %d out of range", i, k[i]);
+        FO_CHECK(t_k[i] >= 0, "fo_queues_push_model_batch: entry %d: negative version", i);
+        FO_CHECK(len == 0 || local[i] != nullptr, "fo_queues_push_model_batch: entry %d: NULL vector", i);
+    }
+    try {
+        for (int32_t i = 0; i < n; ++i) q->qm.push_back({k[i], len ? local[i] : nullptr, len, t_k[i]});
+    } catch (...) {
+        set_error("fo_queues_push_model_batch: out of host memory");
         return FO_ENOMEM;
     }
     return FO_OK;

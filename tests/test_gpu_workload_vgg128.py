@@ -16,7 +16,10 @@ scheduler, aggregation and server step through the C ABI:
     every step of the small loop, and at sampled steps of the loop at the
     workload's own size (batch 64, 64 GiB pool = 32,768 slots of 2 MiB, past
     the step where the cap starts refusing arrivals).  A wrong slot or label
-    moves the loss by far more than the bound."""
+    moves the loss by far more than the bound.
+The small loop hands each arrival over with its own put() calls, the loop at
+workload scale with the batched calls (one per step for the activation
+batches, one for the model messages)."""
 import ctypes
 import os
 
@@ -53,9 +56,10 @@ def _frob(got, ref):
     return np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)
 
 
-def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=()):
+def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=(), batched=False):
     """Runs the loop; returns a summary.  sample_steps: the steps whose
-    training is compared with the oracle from the library's parameters."""
+    training is compared with the oracle from the library's parameters;
+    batched: each step's arrivals go through the batched put() calls."""
     torch = torch_cuda()
     cid = 5
     cfg = S.get_config(cid)
@@ -82,6 +86,7 @@ def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=()):
     trained = drains = 0
     sampled = []
     ls_all, ss_all = [], []
+    want, bank_i = [], []
     try:
         for t in range(steps):
             senders = []
@@ -90,13 +95,27 @@ def _run_loop(B, steps, n_slots, bank_n, counts_sub, sample_steps=()):
                     i = nxt % bank_n
                     nxt += 1
                     ok, seq, _ = sch.put_act(k)
-                    st = A.fo_queues_push(q, k, acts_d[i], labels_d[i])
-                    assert (st == A.FO_OK) == ok, (t, k)
+                    if batched:
+                        want.append(ok)
+                        bank_i.append(i)
+                    else:
+                        st = A.fo_queues_push(q, k, acts_d[i], labels_d[i])
+                        assert (st == A.FO_OK) == ok, (t, k)
                     if ok:
                         bank_of[(k, seq)] = i
                     sch.put_model(k, dev_version[k])
-                    A.fo_queues_push_model(q, k, ld[k], dev_version[k])
+                    if not batched:
+                        A.fo_queues_push_model(q, k, ld[k], dev_version[k])
                     senders.append(k)
+            if batched and senders:
+                bi_ = np.array(bank_i, np.uint64)
+                st = A.fo_queues_push_batch(q, senders, acts_d.data_ptr() + bi_ * slot_bytes,
+                                            labels_d.data_ptr() + bi_ * (4 * B))
+                assert st.tolist() == [A.FO_OK if ok else A.FO_FULL for ok in want], t
+                ks_ = np.array(senders, np.int64)
+                A.fo_queues_push_model_batch(q, senders, ld.data_ptr() + ks_ * (4 * ld.shape[1]), ld.shape[1],
+                                             [dev_version[k] for k in senders])
+            want, bank_i = [], []
             k = A.fo_pick_device(q)
             if k == -2:
                 n0 = len(ls_all)
@@ -172,7 +191,7 @@ def test_vgg128_loop_workload_scale():
     steps = 175
     announce(f"128-device loop at workload scale, {steps} steps, pool 32768 slots, batch 64")
     out = _run_loop(B=64, steps=steps, n_slots=(64 << 30) // (2 << 20), bank_n=16, counts_sub=0,
-                    sample_steps=(0, steps - 1))
+                    sample_steps=(0, steps - 1), batched=True)
     print(out)
     assert out["refused"] > 0 and out["peak"] >= out["omega"]
     assert len(out["sampled"]) == 2

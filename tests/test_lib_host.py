@@ -275,3 +275,62 @@ def test_drain_with_skips_matches_oracle_versions():
             A.fo_queues_destroy(q)
     finally:
         A.fo_set_max_delay(-1)
+
+
+def test_batched_pushes_equal_single_pushes():
+    """fo_queues_push_batch / fo_queues_push_model_batch take a step's arrivals
+    in one call: admissions, refusals, slots, sequence numbers, counters and
+    versions equal those of one call per arrival and the oracle's, bit for bit
+    (128 devices, the 128-device workload's arrival rates, a pool small enough
+    for the cap to bind)."""
+    cid = 5
+    K = 128
+    rates = S.make_arrival_rates(cid)
+    counts = S.make_arrival_counts(cid, rates, 40, sub=3)
+    n_slots = K + 200
+    q1 = A.fo_queues_create(K, 0, 1, False, n_slots)
+    q2 = A.fo_queues_create(K, 0, 1, False, n_slots)
+    sch = TaskScheduler(K, n_slots)
+    try:
+        for t in range(counts.shape[0]):
+            ks = [k for k in range(K) for _ in range(int(counts[t][k]))]
+            single = [A.fo_queues_push(q1, k) for k in ks]
+            for k in ks:
+                A.fo_queues_push_model(q1, k, None, 0)
+            batch = A.fo_queues_push_batch(q2, ks).tolist() if ks else []
+            if ks:
+                A.fo_queues_push_model_batch(q2, ks, np.zeros(len(ks), np.uint64), 0, np.zeros(len(ks), np.int64))
+            ref = []
+            for k in ks:
+                ref.append(A.FO_OK if sch.put_act(k)[0] else A.FO_FULL)
+                sch.put_model(k, 0)
+            assert single == batch == ref, t
+            for q in (q1, q2):
+                while A.fo_pick_device(q) == -2:
+                    A.fo_aggregate_pending_all(q, _Empty(), 1.0)
+            while sch.q_model:
+                _, _, tk = sch.get()
+                sch.aggregate_version(tk)
+            r = sch.get()
+            got = []
+            for q in (q1, q2):
+                st = A.fo_queues_stats(q)
+                if st.in_service:
+                    _, _, seq, slot = A.fo_queues_in_service(q)
+                    got.append((seq, slot))
+                    A.fo_queues_release(q)
+                else:
+                    got.append(None)
+            exp = None if r is None else (r[2], r[3])
+            if r is not None:
+                sch.release()
+            assert got == [exp, exp], t
+        s1, s2 = A.fo_queues_stats(q1), A.fo_queues_stats(q2)
+        for f in ("queued", "admitted", "refused", "picks", "peak_queued", "version"):
+            assert getattr(s1, f) == getattr(s2, f), f
+        assert (s1.refused, s1.peak_queued, s1.version) == (sch.refused, sch.peak_queued, sch.t)
+        assert s1.refused > 0
+        assert A.fo_queues_counters(q1, K) == A.fo_queues_counters(q2, K) == sch.c
+    finally:
+        A.fo_queues_destroy(q1)
+        A.fo_queues_destroy(q2)
