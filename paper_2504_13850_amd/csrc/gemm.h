@@ -123,8 +123,11 @@ fo_status gemm(const GemmDesc& d, hipStream_t s);
 // unsplit products of aligned k-major operands (weight gradients) they run as
 // one launch over the concatenation of their output tiles, each tile over its
 // whole K (no split-K partials, no reduction pass); otherwise one launch each.
+// max_wg > 0 caps the workgroups of the grouped launch (rounded down to a
+// multiple of 8); they then walk the tiles in rounds, leaving workgroup slots
+// to work on other streams.
 constexpr int kGemmGroupMax = 4;
-fo_status gemm_group(const GemmDesc* d, int n, hipStream_t s);
+fo_status gemm_group(const GemmDesc* d, int n, hipStream_t s, int max_wg = 0);
 
 // Bytes of split-K workspace a descriptor needs (0 if splits == 1).
 inline size_t gemm_ws_bytes(int M, int N, int splits) {

@@ -978,32 +978,35 @@ __global__ void __launch_bounds__(NT, 2) gemm_group_kernel(const GemmGroupArg g)
             }
     }
     const int W = start[kGemmGroupMax];
-    const int w = blockIdx.x;
-    if (w >= W) return;  // tiles past a device-side row bound (uniform)
-    const int xq = W >> 3, xr = W & 7, xc = w & 7;
-    const int nid = xc * xq + min(xc, xr) + (w >> 3);
-    // the member owning tile nid (selects in registers: no dynamic indexing)
-    int m = 0, s0 = 0, Mm = Ms[0], Km = Ks[0];
+    // A grid smaller than the tile count (a multiple of 8, so that a workgroup
+    // stays on its XCD's share) walks the tiles in rounds.
+    for (int w = blockIdx.x; w < W; w += gridDim.x) {
+        const int xq = W >> 3, xr = W & 7, xc = w & 7;
+        const int nid = xc * xq + min(xc, xr) + (w >> 3);
+        // the member owning tile nid (selects in registers: no dynamic indexing)
+        int m = 0, s0 = 0, Mm = Ms[0], Km = Ks[0];
 #pragma unroll
-    for (int i = 1; i < kGemmGroupMax; ++i)
-        if (nid >= start[i]) {
-            m = i;
-            s0 = start[i];
-            Mm = Ms[i];
-            Km = Ks[i];
-        }
-    const GemmDesc& d = g.d[m];
-    const int tt = nid - s0;
-    const int nN = (d.N + BN - 1) / BN, nMe = (Mm + BM - 1) / BM;
-    const int grp = tt / (GM * nN), tg = tt - grp * GM * nN;
-    const int gr = min(GM, nMe - grp * GM);
-    TileJob job;
-    job.mt = grp * GM + tg % gr;
-    job.m0 = job.mt * BM;
-    job.n0 = (tg / gr) * BN;
-    job.zt = 0;
-    job.S = 1;
-    gemm_tile<AM, BMODE, AL>(d, job, Mm, Km, smem);
+        for (int i = 1; i < kGemmGroupMax; ++i)
+            if (nid >= start[i]) {
+                m = i;
+                s0 = start[i];
+                Mm = Ms[i];
+                Km = Ks[i];
+            }
+        const GemmDesc& d = g.d[m];
+        const int tt = nid - s0;
+        const int nN = (d.N + BN - 1) / BN, nMe = (Mm + BM - 1) / BM;
+        const int grp = tt / (GM * nN), tg = tt - grp * GM * nN;
+        const int gr = min(GM, nMe - grp * GM);
+        TileJob job;
+        job.mt = grp * GM + tg % gr;
+        job.m0 = job.mt * BM;
+        job.n0 = (tg / gr) * BN;
+        job.zt = 0;
+        job.S = 1;
+        gemm_tile<AM, BMODE, AL>(d, job, Mm, Km, smem);
+        __syncthreads();  // the next tile's stores reuse the LDS of this one's C tile
+    }
 }
 
 // ------------------------------------------------------------------ single-pass compensated product
@@ -1297,7 +1300,7 @@ void launch(const GemmDesc& d, hipStream_t s) {
 
 }  // namespace
 
-fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s) {
+fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s, int max_wg) {
     FO_CHECK(n >= 1 && n <= kGemmGroupMax, "gemm_group: %d products", n);
     // a group runs in one launch when every member is an unsplit, aligned
     // product of k-major operands (the weight-gradient form); otherwise each
@@ -1347,7 +1350,9 @@ fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s) {
     hipEvent_t ea, eb;
     const int h = prof_begin_ext("gemm_group_kernel<6, 6>", pi, &ea, &eb);
     g.prof_snap = prof_snap(h);
-    hipExtLaunchKernelGGL((gemm_group_kernel<OP_KRT, OP_KRT, true>), dim3(tiles), dim3(NT), 0, s, ea, eb, 0, g);
+    int grid = tiles;
+    if (max_wg > 0 && grid > max_wg) grid = std::max(8, max_wg / 8 * 8);
+    hipExtLaunchKernelGGL((gemm_group_kernel<OP_KRT, OP_KRT, true>), dim3(grid), dim3(NT), 0, s, ea, eb, 0, g);
     prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;

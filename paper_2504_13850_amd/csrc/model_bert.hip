@@ -21,6 +21,10 @@ namespace fo {
 namespace {
 
 constexpr int D = 768, NH = 12, FF = 3072, NL = 10, L = 128, NC = 2;
+// Workgroups of a layer's grouped weight-gradient launch (side stream): fewer
+// than its tiles, so that the input-gradient chain on the main stream keeps
+// workgroup slots on every CU.
+constexpr int kWgradMaxWG = 256;
 constexpr int64_t kLayer = (int64_t)3 * D * D + 3 * D + (int64_t)D * D + D + 2 * D + (int64_t)FF * D + FF +
                            (int64_t)D * FF + D + 2 * D;
 constexpr int64_t kParams = NL * kLayer + (int64_t)D * D + D + (int64_t)NC * D + NC;
@@ -813,7 +817,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         wg[1] = wgrad(FF, D, dA1, t.Hb, f.w1, Kw, Kwdev);          // dW1 = dA1^T H
         wg[2] = wgrad(D, D, du1b, t.O, f.wo, Kw, Kwdev);           // dWo = du1^T O
         wg[3] = wgrad(3 * D, D, dqkv, P->Xb[l], f.wqkv, rows, Tdev);  // dWqkv = dqkv^T X
-        TRY(gemm_group(wg, 4, s2));
+        TRY(gemm_group(wg, 4, s2, kWgradMaxWG));
         FO_HIP(hipEventRecord(P->ev_done[pb], s2));
         cur ^= 1;
     }
