@@ -24,7 +24,7 @@ from typing import List, Tuple
 class ConfigSpec:
     cid: int
     name: str
-    family: str              # "cnn" (C1), "vgg" (C2, C5), "resnet" (C3), "bert" (C4)
+    family: str              # "cnn" (C1), "vgg" (C2, C5), "resnet" (C3), "bert" (C4), "vgg_device" (6)
     batch: int
     in_shape: Tuple[int, ...]  # per-sample activation shape at the boundary (NCHW or [L, d])
     n_classes: int
@@ -51,6 +51,12 @@ CONFIGS = {
     5: ConfigSpec(5, "vgg16-split-128dev-bf16", "vgg", 64, (64, 16, 16), 10, 128, "bf16",
                   0.01, 0.0, 38_720, 1.0, 1000,
                   {"pool_bytes": 64 << 30, "bank": 256}),
+    # The device side of the VGG-16 split of configurations 2 and 5 (Alg. 1):
+    # device network conv1-2 of VGG-16 plus its auxiliary network, trained on
+    # CIFAR-10-shaped 32x32 RGB inputs (fp32 at the boundary) against the local
+    # loss; its output activations are the [64,16,16] batches the server trains on.
+    6: ConfigSpec(6, "vgg16-device-side", "vgg_device", 64, (3, 32, 32), 10, 16, "f32",
+                  0.01, 0.0, 0, 1.0, 100, {"server_config": 2}),
 }
 
 
@@ -112,6 +118,11 @@ def param_layout(cid: int) -> List[Entry]:
                     lay += _norm(p + ".dsbn", c)
             cin = c
         lay += _linear("fc", cfg.n_classes, 512)
+    elif cfg.family == "vgg_device":
+        lay += _conv("conv1", 64, 3, 3, True)
+        lay += _conv("conv2", 64, 64, 3, True)
+        lay += _conv("aux.conv", 64, 64, 3, True)
+        lay += _linear("aux.fc", cfg.n_classes, 64)
     elif cfg.family == "bert":
         d, f = cfg.in_shape[1], cfg.extra["ffn"]
         for li in range(cfg.extra["layers"]):

@@ -5,6 +5,8 @@ unoptimised NumPy implementation of what the server computes:
 
 * the server-side training iteration of Algorithm 4 (forward of M_s, the
   loss f_s of Eq. 5, the backward pass and the SGD update),
+* the device-side training iteration of Algorithm 1 (device network, its
+  output activations, auxiliary network, local loss f_d, backward, SGD),
 * the staleness-weighted asynchronous aggregation of Algorithm 4,
 * the Task Scheduler of Algorithms 2 and 3 together with the activation
   flow control of Sec. 3.4.1.
@@ -20,6 +22,6 @@ Parity status: every function here is pinned by the ``-m "not gpu"`` tests
 independent autograd library on tiny inputs).  No function is unpinned.
 """
 from . import layers, nets, aggregate, scheduler  # noqa: F401
-from .nets import server_step, server_forward, param_layout, sgd_update  # noqa: F401
+from .nets import server_step, server_forward, device_step, param_layout, sgd_update  # noqa: F401
 from .aggregate import mix, mix_sequence  # noqa: F401
 from .scheduler import TaskScheduler  # noqa: F401

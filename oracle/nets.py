@@ -22,9 +22,9 @@ from . import layers as Lyr
 VGG_PLAN = [128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M", 512, 512, 512, "M"]
 RESNET_STAGES = [(2, 128, 2), (3, 256, 2), (4, 512, 2)]  # (stage, channels, blocks)
 BERT = dict(d=768, heads=12, ffn=3072, layers=10, classes=2)
-FAMILY = {1: "cnn", 2: "vgg", 3: "resnet", 4: "bert", 5: "vgg"}
-IN_CH = {1: 32, 2: 64, 3: 64, 5: 64}
-CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10}
+FAMILY = {1: "cnn", 2: "vgg", 3: "resnet", 4: "bert", 5: "vgg", 6: "vgg_device"}
+IN_CH = {1: 32, 2: 64, 3: 64, 5: 64, 6: 3}
+CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10, 6: 10}
 
 
 def param_layout(cid: int):
@@ -49,6 +49,13 @@ def param_layout(cid: int):
         conv("conv1", 64, 32, 3)
         conv("conv2", 64, 64, 3)
         lin("fc", 10, 64)
+    elif fam == "vgg_device":
+        # device network M_d: VGG-16's first block; auxiliary network: one layer
+        # of the type of M_d's last layer, then a dense classifier (Sec. 3.2.2)
+        conv("conv1", 64, IN_CH[cid], 3)
+        conv("conv2", 64, 64, 3)
+        conv("aux.conv", 64, 64, 3)
+        lin("aux.fc", CLASSES[cid], 64)
     elif fam == "vgg":
         ci, n = IN_CH[cid], 0
         for v in VGG_PLAN:
@@ -138,6 +145,34 @@ class CNN(_Net):
         self.c1.bwd(self.r1.bwd(dh), need_dx=False)
         self.G = {"conv1.w": self.c1.dw, "conv1.b": self.c1.db, "conv2.w": self.c2.dw,
                   "conv2.b": self.c2.db, "fc.w": self.fc.dw, "fc.b": self.fc.db}
+
+
+class DeviceVGG(_Net):
+    """The device-side network M_d of the VGG-16 split (conv3x3 3->64 + ReLU,
+    conv3x3 64->64 + ReLU, 2x2 max pool; its output xi is the activation batch
+    the device sends to the server) followed by the auxiliary network on xi
+    (conv3x3 64->64 + ReLU, global average pool, dense 64 -> classes), which
+    gives the device its local loss f_d (Alg. 1, Sec. 3.2.2)."""
+
+    def __init__(self, P):
+        self.c1, self.r1 = Lyr.Conv2d(P["conv1.w"], P["conv1.b"]), Lyr.ReLU()
+        self.c2, self.r2 = Lyr.Conv2d(P["conv2.w"], P["conv2.b"]), Lyr.ReLU()
+        self.mp = Lyr.MaxPool2()
+        self.ca, self.ra = Lyr.Conv2d(P["aux.conv.w"], P["aux.conv.b"]), Lyr.ReLU()
+        self.gap = Lyr.GlobalAvgPool()
+        self.fc = Lyr.Linear(P["aux.fc.w"], P["aux.fc.b"])
+
+    def fwd(self, x, lengths=None):
+        self.xi = self.mp.fwd(self.r2.fwd(self.c2.fwd(self.r1.fwd(self.c1.fwd(x)))))
+        return self.fc.fwd(self.gap.fwd(self.ra.fwd(self.ca.fwd(self.xi))))
+
+    def bwd(self, dz):
+        dxi = self.ca.bwd(self.ra.bwd(self.gap.bwd(self.fc.bwd(dz))))
+        dh = self.c2.bwd(self.r2.bwd(self.mp.bwd(dxi)))
+        self.c1.bwd(self.r1.bwd(dh), need_dx=False)  # the input is data: no gradient
+        self.G = {"conv1.w": self.c1.dw, "conv1.b": self.c1.db, "conv2.w": self.c2.dw, "conv2.b": self.c2.db,
+                  "aux.conv.w": self.ca.dw, "aux.conv.b": self.ca.db, "aux.fc.w": self.fc.dw,
+                  "aux.fc.b": self.fc.db}
 
 
 class VGG(_Net):
@@ -317,6 +352,8 @@ def build(cid, P):
     fam = FAMILY[cid]
     if fam == "cnn":
         return CNN(P)
+    if fam == "vgg_device":
+        return DeviceVGG(P)
     if fam == "vgg":
         return VGG(P, cid)
     if fam == "resnet":
@@ -365,3 +402,20 @@ def server_step(cid, params_flat, acts, labels, lengths=None, lr=0.01, momentum=
     theta = np.asarray(params_flat, dtype=dt)
     new, v = sgd_update(theta, g, lr, momentum, None if mom_buf is None else np.asarray(mom_buf, dt))
     return {"loss": loss, "logits": z, "grads": g, "params": new, "momentum": v}
+
+
+def device_step(cid, params_flat, x, labels, lr=0.01, dt=np.float64):
+    """One local training iteration of a device (Alg. 1): forward of the
+    device network M_dk on the mini-batch, its output activations xi (what
+    the device sends), forward of the auxiliary network on xi, the local loss
+    f_d, backward through both networks and the SGD step with rate gamma_d on
+    theta_dk and the auxiliary parameters.  Returns server_step's dict plus
+    "acts" (xi, [B, 64, 16, 16])."""
+    P = unpack(cid, params_flat, dt)
+    net = build(cid, P)
+    z = net.fwd(np.asarray(x, dtype=dt))
+    loss, dz = Lyr.cross_entropy(z, np.asarray(labels))
+    net.bwd(dz)
+    g = pack(cid, net.grads()).astype(dt)
+    new, _ = sgd_update(np.asarray(params_flat, dtype=dt), g, lr)
+    return {"loss": loss, "logits": z, "grads": g, "params": new, "acts": net.xi}

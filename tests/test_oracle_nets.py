@@ -14,7 +14,7 @@ import oracle
 from oracle import nets
 from tests import torch_ref
 
-SMALL_B = {1: 3, 2: 2, 3: 4, 4: 2, 5: 2}
+SMALL_B = {1: 3, 2: 2, 3: 4, 4: 2, 5: 2, 6: 2}
 
 
 def _inputs(cid, B, sub=7):
@@ -24,7 +24,7 @@ def _inputs(cid, B, sub=7):
     return acts, labels, lengths
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5, 6])
 def test_layout_matches_workload(cid):
     a = [(n, tuple(s)) for n, s in nets.param_layout(cid)]
     b = [(n, tuple(s)) for n, s, _, _ in S.param_layout(cid)]
@@ -32,7 +32,7 @@ def test_layout_matches_workload(cid):
     assert sum(int(np.prod(s)) for _, s in a) == S.param_count(cid)
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 6])
 def test_step_matches_independent_autograd(cid):
     B = SMALL_B[cid]
     theta = S.init_params(cid)
@@ -53,7 +53,7 @@ def test_step_matches_independent_autograd(cid):
     np.testing.assert_allclose(r["params"], theta - 0.01 * r["grads"], rtol=1e-15, atol=1e-18)
 
 
-@pytest.mark.parametrize("cid,n_probe", [(1, 12), (3, 10)])
+@pytest.mark.parametrize("cid,n_probe", [(1, 12), (3, 10), (6, 12)])
 def test_step_gradient_finite_differences(cid, n_probe):
     B = 2
     theta = S.init_params(cid).astype(np.float64)
@@ -75,7 +75,7 @@ def test_step_gradient_finite_differences(cid, n_probe):
         assert abs(num - r["grads"][i]) <= 1e-6 * gmax, (i, num, r["grads"][i])
 
 
-@pytest.mark.parametrize("cid,C", [(1, 10), (2, 10), (3, 100), (4, 2)])
+@pytest.mark.parametrize("cid,C", [(1, 10), (2, 10), (3, 100), (4, 2), (6, 10)])
 def test_zero_classifier_gives_ln_c(cid, C):
     theta = S.init_params(cid).astype(np.float64)
     lay = S.param_layout(cid)
@@ -160,3 +160,24 @@ def test_trajectory_amplifies_a_one_percent_step_error():
             off += n
         pa, pb = ra["params"], rb["params"]
     assert worst > 0.06
+
+
+def test_device_step_matches_independent_autograd_and_sends_its_activations():
+    """The device-side iteration (Alg. 1): loss, logits and every gradient
+    against torch fp64 autograd of the same two networks, the activations it
+    sends against torch's forward of the device network alone, and the SGD
+    step on device and auxiliary parameters."""
+    cid, B = 6, 3
+    theta = S.init_params(cid)
+    x = S.make_acts(cid, 1, batch=B, sub=4)[0]
+    labels = S.make_labels(cid, 1, batch=B, sub=4)[0]
+    r = oracle.device_step(cid, theta, x, labels, lr=0.01)
+    tl, tz, tg = torch_ref.step(cid, theta, x, labels)
+    acts = torch_ref.forward.last_acts.detach().numpy()
+    assert r["acts"].shape == (B, 64, 16, 16)
+    np.testing.assert_allclose(r["acts"], acts, rtol=0, atol=1e-12 * np.abs(acts).max())
+    assert abs(r["loss"] - tl) <= 1e-12 * abs(tl)
+    np.testing.assert_allclose(r["grads"], tg, rtol=0, atol=1e-10 * np.abs(tg).max())
+    np.testing.assert_allclose(r["params"], theta - 0.01 * r["grads"], rtol=1e-15, atol=1e-18)
+    # the device step's loss is the server step's definition applied to these networks
+    assert r["loss"] == pytest.approx(oracle.server_step(cid, theta, x, labels)["loss"], abs=1e-15)

@@ -52,6 +52,12 @@ def forward(cid, P, x, lengths=None):
                 sc = bn(F.conv2d(h, _w4(P[p + ".ds.w"]), stride=2), p + ".dsbn") if bi == 0 else h
                 h = F.relu(o + sc)
         return F.linear(h.mean((2, 3)), P["fc.w"], P["fc.b"])
+    if cid == 6:  # device network, then the auxiliary network on its output
+        xi = F.max_pool2d(F.relu(F.conv2d(F.relu(F.conv2d(x, _w4(P["conv1.w"]), P["conv1.b"], padding=1)),
+                                          _w4(P["conv2.w"]), P["conv2.b"], padding=1)), 2)
+        forward.last_acts = xi
+        h = F.relu(F.conv2d(xi, _w4(P["aux.conv.w"]), P["aux.conv.b"], padding=1)).mean((2, 3))
+        return F.linear(h, P["aux.fc.w"], P["aux.fc.b"])
     if cid == 4:
         B, L, d = x.shape
         H, dh = 12, 64
