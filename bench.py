@@ -44,7 +44,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=None, help="timed steps (transformer 30, 128-device VGG 1000)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (transformer 5, 128-device VGG 10)")
     ap.add_argument("--config", type=int, default=4, help="1-3: the parity workloads' step loops; 4: "
-                    "transformer (default); 5: 128-device VGG with Poisson arrivals")
+                    "transformer (default); 5: 128-device VGG with Poisson arrivals; 6: the device-side "
+                    "iteration of the VGG split")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=3,
                     help="fp32 oracle steps at the workload's own batch timed for cpu_baseline")
@@ -475,6 +476,71 @@ def bench_vgg128(args, A, torch, S):
     print(json.dumps(out), flush=True)
 
 
+def device_flops_per_sample():
+    """Useful FLOPs of one device-side training iteration per sample (config 6):
+    forward of conv1 (3->64 at 32x32), conv2 (64->64 at 32x32), the auxiliary
+    conv (64->64 at 16x16) and linear (64->10); input and weight gradients of
+    all but conv1, whose input is data (weight gradient only)."""
+    conv1 = 2 * 32 * 32 * 64 * 27
+    conv2 = 2 * 32 * 32 * 64 * 576
+    aux = 2 * 16 * 16 * 64 * 576
+    fc = 2 * 64 * 10
+    return (conv1 + conv2 + aux + fc) + (conv1 + 2 * conv2 + 2 * aux + 2 * fc)
+
+
+def bench_device(args, A, torch, S):
+    """The device-side iteration of Alg. 1 (config 6) on one GPU: device
+    network, the activations it sends, auxiliary network, local loss,
+    backward and SGD, over a bank of CIFAR-10-shaped input batches."""
+    cid = 6
+    cfg = S.get_config(cid)
+    B = cfg.batch
+    stream = torch.cuda.current_stream()
+    bank_n = 8
+    xs = torch.from_numpy(S.make_acts(cid, bank_n)).cuda()
+    labs = torch.from_numpy(S.make_labels(cid, bank_n)).cuda()
+    out = torch.empty((bank_n, B * 64 * 16 * 16), dtype=torch.int16, device="cuda")
+    model = A.fo_model_create(cid, B, S.init_params(cid), stream)
+    try:
+        def run(t0, n):
+            for t in range(t0, t0 + n):
+                i = t % bank_n
+                A.fo_device_step(model, xs[i], labs[i], B, out[i])
+        run(0, args.warmup)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        run(args.warmup, args.steps)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / args.steps
+        A.fo_profile_enable(100 * args.steps)
+        run(0, args.steps)
+        torch.cuda.synchronize()
+        stats = A.fo_profile_read(64)
+        A.fo_profile_enable(0)
+    finally:
+        A.fo_model_destroy(model)
+    flops = device_flops_per_sample() * B
+    kernels = [{"name": s["name"], "launches": s["launches"], "ms_per_step": round(s["ms"] / args.steps, 4),
+                "TFLOP/s": round(s["flops"] / max(s["ms"], 1e-9) / 1e9, 1) if s["flops"] else None}
+               for s in sorted(stats, key=lambda s: -s["ms"])]
+    out_line = {
+        "metric": "device-side train samples/s (Alg. 1: device network, activations sent, auxiliary network, "
+                  "local loss, backward, SGD)",
+        "value": round(B / (ms * 1e-3), 2), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "vgg16 split device side: conv3x3 3->64, conv3x3 64->64, maxpool (sends "
+                               "[64,16,16]), auxiliary conv3x3 64->64 + avgpool + linear 64->10, batch 64 of "
+                               "32x32 RGB", "global_batch": B, "parallelism": "single-gpu"},
+        "mfu": round(flops / (ms * 1e-3) / (PEAK_BF16_TFLOPS * 1e12), 5),
+        "useful_gflop_per_step": round(flops / 1e9, 3),
+        "kernels": kernels[:10],
+    }
+    print(json.dumps(out_line), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -493,6 +559,11 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cid = args.config
+    if cid == 6:
+        args.steps = 30 if args.steps is None else args.steps
+        args.warmup = 5 if args.warmup is None else args.warmup
+        bench_device(args, A, torch, S)
+        return
     if cid == 5:
         args.steps = 1000 if args.steps is None else args.steps
         args.warmup = 10 if args.warmup is None else args.warmup

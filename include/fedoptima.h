@@ -82,6 +82,11 @@ typedef struct { const void* x; const int32_t* lengths; int32_t batch; } fo_acts
  *   4  BERT-base-shaped: 10 post-LN encoder layers (d=768, 12 heads, FFN 3072,
  *      exact GELU), tanh pooler on token 0, linear 768->2; bf16; plain SGD.
  *   5  same network as 2 (the 128-device pool-stress workload).
+ *   6  the device side of configs 2 and 5 (Alg. 1): the device network
+ *      (VGG-16's first block: conv3x3 3->64 + ReLU, conv3x3 64->64 + ReLU,
+ *      2x2 max pool) and its auxiliary network (conv3x3 64->64 + ReLU, global
+ *      average pool, linear 64->10, Sec. 3.2.2); trained with fo_device_step on
+ *      fp32 [B][3][32][32] inputs; bf16 GEMMs, fp32 master weights; plain SGD.
  * Loss: mean softmax cross-entropy over the batch (the server loss f_s, Eq. 5).
  * Learning rate 0.01.  Parameter layout of the flat fp32 vector ("library
  * layout"): layers in network order; per layer weight then bias (or scale then
@@ -128,6 +133,23 @@ FO_API void fo_model_destroy(fo_model* model);
  * device_id other than its pick's), FO_EHIP. */
 FO_API fo_status fo_server_step(fo_model* model, const fo_acts* acts, const int32_t* labels,
                          int32_t device_id);
+
+/* One local training iteration of a device (Alg. 1) on a config 6 model:
+ * forward of the device network on the mini-batch x (device, fp32 NCHW
+ * [batch][3][32][32], 16-byte aligned), its output activations written to
+ * acts_out (device, bf16 bit patterns NCHW [batch][64][16][16], 16-byte
+ * aligned: the batch the device sends to the server, in the layout
+ * fo_queues_push and fo_server_step take for configs 2 and 5), forward of the
+ * auxiliary network on them, the local loss f_d (mean cross-entropy against
+ * labels, device int32[batch] in [0, 10)), backward through both networks and
+ * SGD on the device and auxiliary parameters (one flat vector in the library
+ * layout: conv1, conv2, auxiliary conv, auxiliary linear).  Asynchronous on
+ * the model's stream; loss and logits (of the auxiliary classifier) readable
+ * with fo_model_read.  Graph replay as for fo_server_step.  Errors: FO_EINVAL
+ * (not a config 6 model, NULL or unaligned pointers, batch out of range),
+ * FO_EHIP. */
+FO_API fo_status fo_device_step(fo_model* model, const float* x, const int32_t* labels, int32_t batch,
+                                uint16_t* acts_out);
 
 /* Process-wide switch for how fo_server_step issues its kernels (default 1).
  * Every step of a model at one batch size is the same sequence of launches

@@ -27,7 +27,7 @@ EXPORTS = [
     "fo_queues_release", "fo_aggregate_pending", "fo_aggregate_pending_all", "fo_queues_stats",
     "fo_queues_counters", "fo_queues_add_device", "fo_last_error", "fo_profile_enable", "fo_profile_read",
     "fo_set_graph_mode", "fo_gemm_bf16", "fo_conv2d_bf16", "fo_gemm_bf16_noalloc", "fo_queues_push_batch",
-    "fo_queues_push_model_batch",
+    "fo_queues_push_model_batch", "fo_device_step",
 ]
 FO_LAYOUT_ROW_K, FO_LAYOUT_K_ROW = 0, 1
 
@@ -79,6 +79,7 @@ def lib():
             "fo_model_create": (C.c_int, [i32, i32, vp, i64, vp, C.POINTER(vp)]),
             "fo_model_destroy": (None, [vp]),
             "fo_server_step": (C.c_int, [vp, C.POINTER(fo_acts), vp, i32]),
+            "fo_device_step": (C.c_int, [vp, vp, vp, i32, vp]),
             "fo_model_steps": (i64, [vp, i32]),
             "fo_model_buffer_size": (i64, [vp, i32]),
             "fo_model_read": (C.c_int, [vp, i32, vp, i64]),
@@ -178,6 +179,10 @@ def fo_server_step(model, acts, labels, device_id: int):
     if not isinstance(acts, fo_acts):
         acts = make_acts(*acts) if isinstance(acts, tuple) else make_acts(acts)
     return _check(lib().fo_server_step(model, C.byref(acts), _dptr(labels), device_id))
+
+
+def fo_device_step(model, x, labels, batch: int, acts_out):
+    return _check(lib().fo_device_step(model, _dptr(x), _dptr(labels), int(batch), _dptr(acts_out)))
 
 
 def fo_set_graph_mode(enable: bool):

@@ -28,6 +28,7 @@ void set_error(const char* fmt, ...) {
 int64_t cnn32_param_count();
 int64_t cnn16_param_count(int32_t cid);
 int64_t bert_param_count();
+int64_t device_param_count();
 
 }  // namespace fo
 
@@ -40,13 +41,14 @@ extern "C" int64_t fo_config_param_count(int32_t cid) {
         case 1: return cnn32_param_count();
         case 2: case 3: case 5: return cnn16_param_count(cid);
         case 4: return bert_param_count();
+        case 6: return device_param_count();
         default: return -1;
     }
 }
 
 extern "C" int32_t fo_config_num_classes(int32_t cid) {
     switch (cid) {
-        case 1: case 2: case 5: return 10;
+        case 1: case 2: case 5: case 6: return 10;
         case 3: return 100;
         case 4: return 2;
         default: return -1;
@@ -58,6 +60,7 @@ static const Family* family_of(int32_t cid) {
         case 1: return family_cnn32();
         case 2: case 3: case 5: return family_cnn16();
         case 4: return family_bert();
+        case 6: return family_device();
         default: return nullptr;
     }
 }
@@ -162,25 +165,28 @@ extern "C" void fo_model_destroy(fo_model* m) {
 // the model's stream swapped for it; replays go to the model's stream.
 static int g_graph_mode = 1;
 
-__global__ void latch_inputs(StepIn* __restrict__ in, const void* x, const int32_t* labels, const int32_t* lengths) {
+__global__ void latch_inputs(StepIn* __restrict__ in, const void* x, const int32_t* labels, const int32_t* lengths,
+                             void* out) {
     in->x = x;
     in->labels = labels;
     in->lengths = lengths;
+    in->out = out;
 }
 
-static fo_status launch_latch(fo_model* m, const fo_acts* acts, const int32_t* labels, hipStream_t s) {
-    hipLaunchKernelGGL(latch_inputs, dim3(1), dim3(1), 0, s, m->dev_in, acts->x, labels, acts->lengths);
+static fo_status launch_latch(fo_model* m, const fo_acts* acts, const int32_t* labels, void* out, hipStream_t s) {
+    hipLaunchKernelGGL(latch_inputs, dim3(1), dim3(1), 0, s, m->dev_in, acts->x, labels, acts->lengths, out);
     FO_LAUNCHED();
     return FO_OK;
 }
 
 // The step as launched directly: the latch, then the family's kernels.
-static fo_status step_direct(fo_model* m, const fo_acts* acts, const int32_t* labels) {
-    fo_status st = launch_latch(m, acts, labels, m->stream);
+static fo_status step_direct(fo_model* m, const fo_acts* acts, const int32_t* labels, void* out) {
+    fo_status st = launch_latch(m, acts, labels, out, m->stream);
     return st != FO_OK ? st : m->fam->step(m, acts, labels);
 }
 
-static fo_status capture_step(fo_model* m, const fo_acts* acts, const int32_t* labels, fo_model::Captured* out) {
+static fo_status capture_step(fo_model* m, const fo_acts* acts, const int32_t* labels, void* outp,
+                              fo_model::Captured* out) {
     if (!m->capture_stream && hipStreamCreateWithFlags(&m->capture_stream, hipStreamNonBlocking) != hipSuccess) {
         m->capture_stream = nullptr;
         set_error("fo_server_step: hipStreamCreateWithFlags failed");
@@ -193,7 +199,7 @@ static fo_status capture_step(fo_model* m, const fo_acts* acts, const int32_t* l
         return FO_EHIP;
     }
     m->stream = m->capture_stream;
-    const fo_status st = step_direct(m, acts, labels);
+    const fo_status st = step_direct(m, acts, labels, outp);
     m->stream = user;
     hipGraph_t g = nullptr;
     e = hipStreamEndCapture(m->capture_stream, &g);
@@ -228,12 +234,12 @@ static fo_status capture_step(fo_model* m, const fo_acts* acts, const int32_t* l
     return FO_OK;
 }
 
-static fo_status step_graph(fo_model* m, const fo_acts* acts, const int32_t* labels) {
+static fo_status step_graph(fo_model* m, const fo_acts* acts, const int32_t* labels, void* outp) {
     const int B = acts->batch;
     auto it = m->graphs.find(B);
     if (it == m->graphs.end()) {
         fo_model::Captured c;
-        fo_status st = capture_step(m, acts, labels, &c);
+        fo_status st = capture_step(m, acts, labels, outp, &c);
         if (st != FO_OK) return st;
         try {
             it = m->graphs.emplace(B, c).first;
@@ -249,7 +255,7 @@ static fo_status step_graph(fo_model* m, const fo_acts* acts, const int32_t* lab
     const void* x = acts->x;
     const int32_t* lab = labels;
     const int32_t* len = acts->lengths;
-    void* args[] = {&in, &x, &lab, &len};
+    void* args[] = {&in, &x, &lab, &len, &outp};
     hipKernelNodeParams p = {};
     p.func = reinterpret_cast<void*>(&latch_inputs);
     p.gridDim = dim3(1);
@@ -273,6 +279,7 @@ extern "C" fo_status fo_set_graph_mode(int32_t enable) {
 
 extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int32_t* labels, int32_t device_id) {
     FO_CHECK(m != nullptr, "fo_server_step: NULL model");
+    FO_CHECK(m->cid != 6, "fo_server_step: config 6 is a device-side model (fo_device_step)");
     FO_CHECK(acts != nullptr && acts->x != nullptr, "fo_server_step: NULL activations");
     FO_CHECK(labels != nullptr, "fo_server_step: NULL labels");
     FO_CHECK(acts->batch >= 1 && acts->batch <= m->max_batch, "fo_server_step: batch=%d outside [1,%d]",
@@ -285,7 +292,7 @@ extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int3
     fo_status st = pool_step_begin(acts, labels, device_id, m->stream, &owner);
     if (st != FO_OK) return st;
     // Kernel profiling records every launch with its own events: run eagerly then.
-    st = (g_graph_mode && !prof_active()) ? step_graph(m, acts, labels) : step_direct(m, acts, labels);
+    st = (g_graph_mode && !prof_active()) ? step_graph(m, acts, labels, nullptr) : step_direct(m, acts, labels, nullptr);
     if (st != FO_OK) return st;
     if (owner) {
         st = pool_step_done(owner, m->stream);
@@ -295,6 +302,26 @@ extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int3
     m->steps_total++;
     if ((size_t)device_id >= m->steps_per_device.size()) m->steps_per_device.resize(device_id + 1, 0);
     m->steps_per_device[device_id]++;
+    return FO_OK;
+}
+
+extern "C" fo_status fo_device_step(fo_model* m, const float* x, const int32_t* labels, int32_t batch,
+                                    uint16_t* acts_out) {
+    FO_CHECK(m != nullptr, "fo_device_step: NULL model");
+    FO_CHECK(m->cid == 6, "fo_device_step: config %d is a server-side model (fo_server_step)", m->cid);
+    FO_CHECK(x != nullptr && labels != nullptr && acts_out != nullptr, "fo_device_step: NULL pointer");
+    FO_CHECK(batch >= 1 && batch <= m->max_batch, "fo_device_step: batch=%d outside [1,%d]", batch, m->max_batch);
+    FO_CHECK(((uintptr_t)x % 16) == 0 && ((uintptr_t)acts_out % 16) == 0,
+             "fo_device_step: input and output must be 16-byte aligned");
+    fo_acts acts;
+    acts.x = x;
+    acts.lengths = nullptr;
+    acts.batch = batch;
+    fo_status st = (g_graph_mode && !prof_active()) ? step_graph(m, &acts, labels, acts_out)
+                                                    : step_direct(m, &acts, labels, acts_out);
+    if (st != FO_OK) return st;
+    m->last_batch = batch;
+    m->steps_total++;
     return FO_OK;
 }
 

@@ -87,6 +87,7 @@ struct StepIn {
     const void* x;
     const int32_t* labels;
     const int32_t* lengths;
+    void* out;  // the device-side step's output activations (NULL for server steps)
 };
 
 // Device memory arena: one hipMalloc, bump allocation, 256-byte alignment.

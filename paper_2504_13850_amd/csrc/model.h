@@ -68,5 +68,6 @@ struct Family {
 const Family* family_cnn32();   // config 1
 const Family* family_cnn16();   // configs 2, 3, 5
 const Family* family_bert();    // config 4
+const Family* family_device();  // config 6 (device side of configs 2 and 5)
 
 }  // namespace fo

@@ -1,7 +1,9 @@
-"""Graph replay of the server step (fo_set_graph_mode) against direct launches.
+"""Graph replay of the server and device steps (fo_set_graph_mode) against
+direct launches.
 
-With graph mode on, fo_server_step copies the batch into model-owned staging
-buffers and replays a HIP graph captured once per batch size.  Every kernel of
+With graph mode on, fo_server_step (fo_device_step) replays a HIP graph
+captured once per batch size, after setting the arguments of its first
+launch, which stores the batch's pointers for the other kernels.  Every kernel of
 the step is deterministic (no atomics), so a replayed step must give results
 bit-identical to the same step launched kernel by kernel.  Each case runs one
 model per mode through the same sequence of batches: several replays at one
@@ -49,7 +51,7 @@ def _eager_noise(torch, step):
     return float(a.sum().item())
 
 
-@pytest.mark.parametrize("cid,Bmax", [(1, 8), (2, 8), (3, 8), (4, 6), (5, 8)])
+@pytest.mark.parametrize("cid,Bmax", [(1, 8), (2, 8), (3, 8), (4, 6), (5, 8), (6, 8)])
 def test_graph_replay_matches_direct_launches(cid, Bmax):
     torch = torch_cuda()
     cfg = S.get_config(cid)
@@ -68,8 +70,15 @@ def test_graph_replay_matches_direct_launches(cid, Bmax):
                 A.fo_set_graph_mode(mode)
                 x, lab = to_dev(acts), to_dev(labels)
                 ln = to_dev(lengths) if lengths is not None else None
-                A.fo_server_step(model, (x, ln, B), lab, step % 3)
-                outs.append(_read_all(model, cfg, B))
+                if cid == 6:  # the device step: its activations are compared too
+                    out = torch.empty(B * 64 * 16 * 16, dtype=torch.int16, device="cuda")
+                    A.fo_device_step(model, x, lab, B, out)
+                    outs.append(_read_all(model, cfg, B))
+                    outs[-1]["acts"] = out.cpu().numpy()
+                    del out
+                else:
+                    A.fo_server_step(model, (x, ln, B), lab, step % 3)
+                    outs.append(_read_all(model, cfg, B))
                 del x, lab, ln
                 _eager_noise(torch, step)
                 torch.cuda.synchronize()
