@@ -89,18 +89,38 @@ __global__ void __launch_bounds__(256) maxpool_relu_bwd(const float* __restrict_
     }
 }
 
-// h[b][c] = mean over the H*W pixels of x (hi + lo)
+// h[b][c] = mean over the H*W pixels of x (hi + lo).  Block = (sample b,
+// 64 channels c0 ..): lane = channel (one 128-byte row segment per wave and
+// pixel), the four waves take every fourth pixel, eight loads in flight per
+// lane, the waves' sums added in wave order.
 __global__ void __launch_bounds__(256) gap_fwd(const bf16_t* __restrict__ xh, const bf16_t* __restrict__ xl,
                                                float* __restrict__ h, int B, int HW, int C) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)B * C) return;
-    const int b = (int)(i / C), c = (int)(i % C);
+    __shared__ float red[4][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int b = blockIdx.y, c = blockIdx.x * 64 + lane;
     float s = 0.f;
-    for (int p = 0; p < HW; ++p) {
-        const int64_t k = ((int64_t)b * HW + p) * C + c;
-        s += bf2f(xh[k]) + (xl ? bf2f(xl[k]) : 0.f);
+    if (c < C) {
+        const int64_t base = (int64_t)b * HW * C + c;
+        int p = w;
+        for (; p + 28 < HW; p += 32) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int64_t k = base + (int64_t)(p + 4 * u) * C;
+                v[u] = bf2f(xh[k]) + (xl ? bf2f(xl[k]) : 0.f);
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; p < HW; p += 4) {
+            const int64_t k = base + (int64_t)p * C;
+            s += bf2f(xh[k]) + (xl ? bf2f(xl[k]) : 0.f);
+        }
     }
-    h[i] = s / (float)HW;
+    red[w][lane] = s;
+    __syncthreads();
+    if (w == 0 && c < C)
+        h[(int64_t)b * C + c] = ((red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane])) / (float)HW;
 }
 
 // dx[b][p][c] = dh[b][c] / HW * [y > 0]
@@ -382,7 +402,7 @@ fo_status launch_maxpool_relu_bwd(const float* dy, const uint8_t* arg, const bf1
 }
 
 fo_status launch_gap_fwd(const bf16_t* xh, const bf16_t* xl, float* h, int B, int HW, int C, hipStream_t s) {
-    hipLaunchKernelGGL(gap_fwd, dim3(cdiv((int64_t)B * C, 256)), dim3(256), 0, s, xh, xl, h, B, HW, C);
+    hipLaunchKernelGGL(gap_fwd, dim3(cdiv(C, 64), B), dim3(256), 0, s, xh, xl, h, B, HW, C);
     FO_LAUNCHED();
     return FO_OK;
 }

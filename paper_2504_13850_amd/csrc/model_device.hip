@@ -43,8 +43,8 @@ constexpr int KK = 9 * C;  // reduction length of a 64-channel 3x3 conv
 constexpr int64_t W1 = 0, B1 = W1 + (int64_t)C * 9 * CI, W2 = B1 + C, B2 = W2 + (int64_t)C * KK, WA = B2 + C,
                   BA = WA + (int64_t)C * KK, WF = BA + C, BF = WF + (int64_t)NCLS * C, kParams = BF + NCLS;
 
-// conv1 weight gradient: positions per block of the partial-sum pass
-constexpr int W1_POS = 1024;
+// conv1 weight gradient: image rows per block of the partial-sum pass
+constexpr int W1_ROWS = 4;
 
 struct Plan {
     int B;
@@ -120,41 +120,41 @@ __global__ void __launch_bounds__(256) acts_out_nchw(const StepIn* __restrict__ 
     for (int r = ty; r < 32; r += 8) out[((int64_t)b * C + c0 + r) * HW + p0 + tx] = tile[tx][r];
 }
 
-// conv1 weight and bias gradients, pass 1: block = W1_POS output positions
-// (its four waves take every fourth position), lane = output channel co;
-// per lane the 27 weight sums dh1[p][co] x[b][ci][y + ky - 1][x + kx - 1] and
-// the bias sum dh1[p][co], written as part[block][28][64].
+// conv1 weight and bias gradients, pass 1: block = W1_ROWS image rows of one
+// sample (their input rows, with the padding, staged once in LDS), lane =
+// output channel co, the four waves take every fourth pixel; per lane the 27
+// weight sums dh1[p][co] x[b][ci][y + ky - 1][x + kx - 1] and the bias sum
+// dh1[p][co] (coalesced 256-byte rows of dh1; the input values are LDS
+// broadcasts), written as part[block][28][64].
 __global__ void __launch_bounds__(256) conv1_wgrad_partial(const StepIn* __restrict__ in,
-                                                           const float* __restrict__ dh1, int B,
-                                                           float* __restrict__ part) {
+                                                           const float* __restrict__ dh1, float* __restrict__ part) {
     const float* __restrict__ x = static_cast<const float*>(in->x);
+    __shared__ float xs[CI][W1_ROWS + 2][H0 + 2];
     __shared__ float red[4][28][64];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    constexpr int strips = H0 / W1_ROWS;
+    const int b = blockIdx.x / strips, y0 = (blockIdx.x % strips) * W1_ROWS;
+    for (int i = threadIdx.x; i < CI * (W1_ROWS + 2) * (H0 + 2); i += 256) {
+        const int ci = i / ((W1_ROWS + 2) * (H0 + 2)), r = (i / (H0 + 2)) % (W1_ROWS + 2), cx = i % (H0 + 2);
+        const int iy = y0 + r - 1, ix = cx - 1;
+        xs[ci][r][cx] = (iy >= 0 && iy < H0 && ix >= 0 && ix < H0) ? x[(((int64_t)b * CI + ci) * H0 + iy) * H0 + ix]
+                                                                    : 0.f;
+    }
+    __syncthreads();
     float acc[28];
 #pragma unroll
     for (int t = 0; t < 28; ++t) acc[t] = 0.f;
-    const int64_t total = (int64_t)B * H0 * H0;
-    const int64_t p0 = (int64_t)blockIdx.x * W1_POS;
-    for (int j = w; j < W1_POS; j += 4) {
-        const int64_t p = p0 + j;
-        if (p >= total) break;
-        const float d = dh1[p * C + lane];
-        const int xx = (int)(p % H0), yy = (int)((p / H0) % H0), b = (int)(p / (H0 * H0));
+    for (int j = w; j < W1_ROWS * H0; j += 4) {
+        const int r = j / H0, xx = j % H0;
+        const float d = dh1[(((int64_t)b * H0 + y0 + r) * H0 + xx) * C + lane];
         acc[27] += d;
 #pragma unroll
-        for (int ky = 0; ky < 3; ++ky) {
-            const int iy = yy + ky - 1;
+        for (int ky = 0; ky < 3; ++ky)
 #pragma unroll
-            for (int kx = 0; kx < 3; ++kx) {
-                const int ix = xx + kx - 1;
-                const bool ok = iy >= 0 && iy < H0 && ix >= 0 && ix < H0;
+            for (int kx = 0; kx < 3; ++kx)
 #pragma unroll
-                for (int ci = 0; ci < CI; ++ci) {
-                    const float xv = ok ? x[(((int64_t)b * CI + ci) * H0 + iy) * H0 + ix] : 0.f;
-                    acc[(ky * 3 + kx) * CI + ci] = fmaf(d, xv, acc[(ky * 3 + kx) * CI + ci]);
-                }
-            }
-        }
+                for (int ci = 0; ci < CI; ++ci)
+                    acc[(ky * 3 + kx) * CI + ci] = fmaf(d, xs[ci][r + ky][xx + kx], acc[(ky * 3 + kx) * CI + ci]);
     }
 #pragma unroll
     for (int t = 0; t < 28; ++t) red[w][t][lane] = acc[t];
@@ -165,16 +165,23 @@ __global__ void __launch_bounds__(256) conv1_wgrad_partial(const StepIn* __restr
     }
 }
 
-// pass 2: the partials in block order -> dW1 [co][ky][kx][ci] and db1.
+// pass 2: one wave per output (28 x 64 of them: 27 weights and the bias per
+// channel), its lanes over the partial rows, then a wave sum in a fixed order
+// -> dW1 [co][ky][kx][ci] and db1.
 __global__ void __launch_bounds__(256) conv1_wgrad_finish(const float* __restrict__ part, int nblk,
                                                           float* __restrict__ gw, float* __restrict__ gb) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= 28 * 64) return;
-    const int t = i / 64, c = i % 64;
+    const int lane = threadIdx.x & 63;
+    const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (o >= 28 * 64) return;  // (uniform per wave)
+    const int t = o / 64, c = o % 64;
     float s = 0.f;
-    for (int k = 0; k < nblk; ++k) s += part[((int64_t)k * 28 + t) * 64 + c];
-    if (t < 27) gw[(int64_t)c * 27 + t] = s;  // t = (ky * 3 + kx) * 3 + ci: the [co][ky][kx][ci] order
-    else gb[c] = s;
+    for (int k = lane; k < nblk; k += 64) s += part[((int64_t)k * 28 + t) * 64 + c];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    if (lane == 0) {
+        if (t < 27) gw[(int64_t)c * 27 + t] = s;  // t = (ky * 3 + kx) * 3 + ci: the [co][ky][kx][ci] order
+        else gb[c] = s;
+    }
 }
 
 // ------------------------------------------------------------------ GEMM wrappers
@@ -250,7 +257,7 @@ size_t ws_bytes(const fo_model* m) {
     add(sw + 256);
     add(4 * colsum_ws_floats(Bi * H0 * H0, C));
     add(4 * small_linear_ws_floats(Bi, C, NCLS));
-    add(4 * (size_t)cdiv((int64_t)B * H0 * H0, W1_POS) * 28 * 64);
+    add(4 * B * (H0 / W1_ROWS) * 28 * 64);
     return s;
 }
 
@@ -283,7 +290,7 @@ fo_status init(fo_model* m) {
     P->splitws = a.take<float>(sw / 4 + 64);
     P->colws = a.take<float>(colsum_ws_floats(B * H0 * H0, C));
     P->slws = a.take<float>(small_linear_ws_floats(B, C, NCLS));
-    P->w1part = a.take<float>((size_t)cdiv((int64_t)B * H0 * H0, W1_POS) * 28 * 64);
+    P->w1part = a.take<float>((size_t)B * (H0 / W1_ROWS) * 28 * 64);
     if (!P->w1part) {
         set_error("device model: workspace arena too small");
         return FO_ENOMEM;
@@ -329,10 +336,9 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     TRY(launch_colsum(P->dh2f, C, rows0, nullptr, C, grd + B2, P->colws, s));
     TRY(conv_dgrad(m, P, B, H0, P->dh2b, W2, P->h1h, 1, P->dh1));  // times conv1's ReLU mask
     {
-        const int nblk = (int)cdiv(rows0, W1_POS);
-        hipLaunchKernelGGL(conv1_wgrad_partial, dim3(nblk), dim3(256), 0, s, m->dev_in, P->dh1, B, P->w1part);
-        hipLaunchKernelGGL(conv1_wgrad_finish, dim3(cdiv(28 * 64, 256)), dim3(256), 0, s, P->w1part, nblk, grd + W1,
-                           grd + B1);
+        const int nblk = B * (H0 / W1_ROWS);
+        hipLaunchKernelGGL(conv1_wgrad_partial, dim3(nblk), dim3(256), 0, s, m->dev_in, P->dh1, P->w1part);
+        hipLaunchKernelGGL(conv1_wgrad_finish, dim3(28 * 64 / 4), dim3(256), 0, s, P->w1part, nblk, grd + W1, grd + B1);
         FO_LAUNCHED();
     }
     // ---- SGD on the device and auxiliary parameters (rate gamma_d)
