@@ -242,148 +242,179 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const bf16_t* __restrict
 // gradients only).  With P = softmax(S), S = scale Q K^T and D_i = sum_c dO_ic O_ic:
 //   dS_ij = P_ij (dO_i . V_j - D_i)
 //   dQ_i = scale sum_j dS_ij K_j;  dK_j = scale sum_i dS_ij Q_i;  dV_j = sum_i P_ij dO_i
-// Phase 1, wave w on queries 32w..: S^T = K Q^T and dP^T = V dO^T (K, V rows
-// from LDS, Q and dO rows from the registers); P = exp(S - lse) from the
-// forward's log-sum-exp and dS; both go to LDS as [query][key] rows, and
-// dQ^T = K^T dS^T takes dS^T straight from the registers.  Phase 2, wave w on
-// keys 32w..: dK^T = Q^T dS and dV^T = dO^T P, every operand a transpose read,
-// so each lane ends with four consecutive columns of one key row.
-__global__ void __launch_bounds__(256) attn_bwd_mfma(const bf16_t* __restrict__ qkv, const int* __restrict__ cu,
-                                                     const bf16_t* __restrict__ out, const bf16_t* __restrict__ dout,
-                                                     const float* __restrict__ lse, bf16_t* __restrict__ dqkv, int H,
-                                                     int d, float scale, int* __restrict__ snap, int nb,
-                                                     const int* __restrict__ order) {
-    __shared__ __attribute__((aligned(16))) bf16_t Kr[LMAX * DH], Vr[LMAX * DH], Qr[LMAX * DH], Gr[LMAX * DH];
-    __shared__ __attribute__((aligned(16))) bf16_t Pq[LMAX * LMAX], Dq[LMAX * LMAX];  // [query][key]
+// Two workgroups per (sequence, head), each recomputing P (from the forward's
+// log-sum-exp) and dS for the rows it owns:
+//  - the query workgroup, wave w on queries 32w..: K and V in LDS, the lane's
+//    Q and dO row in registers; S^T = K Q^T and dP^T = V dO^T, then
+//    dQ^T = K^T dS^T with dS^T straight from the registers;
+//  - the key workgroup, wave w on keys 32w..: Q and dO in LDS with each
+//    query's lse and D, the lane's K and V row in registers; per tile of 32
+//    queries S = Q K^T and dP = dO V^T, then dK^T += Q^T dS and dV^T += dO^T P,
+//    dS and P again straight from the registers (the query index of a tile
+//    taken in the attention key order on both operands).
+// Neither stores P or dS: a workgroup holds 33 KB of LDS, so all 2 B H of them
+// are resident at once.
+// D_i of the lane's row: dO and O over head columns 16 kk + 8 half + 0..7, the
+// two halves summed by the caller (one exchange), in the same order on both
+// workgroups so that they agree bit for bit.
+__device__ __forceinline__ float dsum_half(const bf16_t* dout, const bf16_t* out, int64_t o, bool ok) {
+    float acc = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        const u32x4_t g = __builtin_bit_cast(u32x4_t, ld8(dout + o + 16 * kk, ok));
+        const u32x4_t v = __builtin_bit_cast(u32x4_t, ld8(out + o + 16 * kk, ok));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc = fmaf(bf2f((bf16_t)(g[e] & 0xFFFFu)), bf2f((bf16_t)(v[e] & 0xFFFFu)), acc);
+            acc = fmaf(bf2f((bf16_t)(g[e] >> 16)), bf2f((bf16_t)(v[e] >> 16)), acc);
+        }
+    }
+    return acc;
+}
+__device__ __forceinline__ bf16x8_t pack8(const float* v) {
+    u32x4_t u;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) u[e] = f2bf2(v[2 * e], v[2 * e + 1]);
+    return __builtin_bit_cast(bf16x8_t, u);
+}
+// A [64][32] transposed accumulator pair (rows = head columns 32 t + 8 q + 4 lh
+// + r mod 4, column = the lane's row) times s, as bf16, into a token row.
+__device__ __forceinline__ void store_rowT(bf16_t* row, const f32x16* acc, float s, int lh) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<uint2*>(row + 32 * t + 8 * q + 4 * lh) =
+                pack4f(acc[t][4 * q] * s, acc[t][4 * q + 1] * s, acc[t][4 * q + 2] * s, acc[t][4 * q + 3] * s);
+}
+
+__global__ void __launch_bounds__(256, 2) attn_bwd_mfma(const bf16_t* __restrict__ qkv, const int* __restrict__ cu,
+                                                        const bf16_t* __restrict__ out, const bf16_t* __restrict__ dout,
+                                                        const float* __restrict__ lse, bf16_t* __restrict__ dqkv, int H,
+                                                        int d, float scale, int* __restrict__ snap, int nb,
+                                                        const int* __restrict__ order) {
+    __shared__ __attribute__((aligned(16))) bf16_t T0[LMAX * DH], T1[LMAX * DH];
+    __shared__ __attribute__((aligned(16))) float rowL[LMAX], rowD[LMAX];
     if (snap && blockIdx.x == 0)
         for (int i = threadIdx.x; i <= nb; i += blockDim.x) snap[i] = cu[i];
-    const int b = order ? order[blockIdx.x / H] : blockIdx.x / H, h = blockIdx.x % H;
+    const int pair = blockIdx.x >> 1;
+    const bool keys = blockIdx.x & 1;
+    const int b = order ? order[pair / H] : pair / H, h = pair % H;
     const int base = cu[b], len = cu[b + 1] - cu[b];
     const int64_t ld = 3 * d;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int lr = lane & 31, lh = lane >> 5;
-    const int i0 = 32 * w, qi = i0 + lr;
-    const bool active = i0 < len;
-    const int nj = (len + 31) >> 5;
+    const int r0 = 32 * w, ri = r0 + lr;  // the lane's query (query workgroup) or key (key workgroup)
+    const int n32 = (len + 31) >> 5;
     const int64_t rb = ((int64_t)b * H + h) * LMAX;
-    // this lane's query: Q, dO and O at head columns 16 kk + 8 lh + 0..7
-    bf16x8_t qa[4], ga[4];
-    u32x4_t ov[4];
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-        const int c = h * DH + 16 * kk + 8 * lh;
-        qa[kk] = ld8(qkv + (int64_t)(base + qi) * ld + c, qi < len);
-        ga[kk] = ld8(dout + (int64_t)(base + qi) * d + c, qi < len);
-        ov[kk] = __builtin_bit_cast(u32x4_t, ld8(out + (int64_t)(base + qi) * d + c, qi < len));
-    }
-    const float lq = qi < len ? lse[rb + qi] * kLog2e : 0.f;
-    stage64(Kr, qkv + d + h * DH, ld, base, len, tid);
-    stage64(Vr, qkv + 2 * d + h * DH, ld, base, len, tid);
-    stage64(Qr, qkv + h * DH, ld, base, len, tid);
-    stage64(Gr, dout + h * DH, d, base, len, tid);
-    __syncthreads();
     const float c2 = scale * kLog2e;
-    f32x16 dq[2];
+    const int hc = h * DH + 8 * lh;  // first head column of the lane's operand rows
+    f32x16 acc0[2], acc1[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dq[t][r] = 0.f;
-    if (active) {
-        float dsum = 0.f;
+        for (int r = 0; r < 16; ++r) acc0[t][r] = acc1[t][r] = 0.f;
+    if (!keys) {
+        bf16x8_t qa[4], ga[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-            const u32x4_t g2 = __builtin_bit_cast(u32x4_t, ga[kk]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                dsum = fmaf(bf2f((bf16_t)(g2[e] & 0xFFFFu)), bf2f((bf16_t)(ov[kk][e] & 0xFFFFu)), dsum);
-                dsum = fmaf(bf2f((bf16_t)(g2[e] >> 16)), bf2f((bf16_t)(ov[kk][e] >> 16)), dsum);
-            }
+            qa[kk] = ld8(qkv + (int64_t)(base + ri) * ld + hc + 16 * kk, ri < len);
+            ga[kk] = ld8(dout + (int64_t)(base + ri) * d + hc + 16 * kk, ri < len);
         }
-        const float Dv = dsum + __shfl_xor(dsum, 32);
-#pragma unroll
-        for (int jt = 0; jt < 4; ++jt) {
-            if (jt >= nj) break;
+        const float lq = ri < len ? lse[rb + ri] * kLog2e : 0.f;
+        float Dv = dsum_half(dout, out, (int64_t)(base + ri) * d + hc, ri < len);
+        stage64(T0, qkv + d + h * DH, ld, base, len, tid);
+        stage64(T1, qkv + 2 * d + h * DH, ld, base, len, tid);
+        __syncthreads();
+        if (r0 >= len) return;  // no barrier follows
+        Dv += __shfl_xor(Dv, 32);
+        for (int jt = 0; jt < n32; ++jt) {
             f32x16 S, G;
 #pragma unroll
             for (int r = 0; r < 16; ++r) S[r] = G[r] = 0.f;
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
-                S = mfma(frag_row(Kr, 32 * jt, 16 * kk, lane), qa[kk], S);
-                G = mfma(frag_row(Vr, 32 * jt, 16 * kk, lane), ga[kk], G);
+                S = mfma(frag_row(T0, 32 * jt, 16 * kk, lane), qa[kk], S);
+                G = mfma(frag_row(T1, 32 * jt, 16 * kk, lane), ga[kk], G);
             }
-            float pv[16], dsv[16];
+            float dsv[16];
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int j = 32 * jt + 8 * (r >> 2) + 4 * lh + (r & 3);
-                const bool ok = qi < len && j < len;
-                const float p = ok ? __builtin_amdgcn_exp2f(fmaf(S[r], c2, -lq)) : 0.f;
-                pv[r] = p;
+                const float p = ri < len && j < len ? __builtin_amdgcn_exp2f(fmaf(S[r], c2, -lq)) : 0.f;
                 dsv[r] = p * (G[r] - Dv);
-            }
-            // P and dS rows of this query: keys 32 jt + 8 q + 4 lh .. + 3
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int i = idx128(qi, 32 * jt + 8 * q + 4 * lh);
-                *reinterpret_cast<uint2*>(&Pq[i]) = pack4f(pv[4 * q], pv[4 * q + 1], pv[4 * q + 2], pv[4 * q + 3]);
-                *reinterpret_cast<uint2*>(&Dq[i]) = pack4f(dsv[4 * q], dsv[4 * q + 1], dsv[4 * q + 2], dsv[4 * q + 3]);
             }
             // dQ^T += K^T dS^T over this tile's keys (dS^T in the attention key order)
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
-                u32x4_t sv;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) sv[e] = f2bf2(dsv[8 * kb + 2 * e], dsv[8 * kb + 2 * e + 1]);
-                const bf16x8_t bs = __builtin_bit_cast(bf16x8_t, sv);
+                const bf16x8_t bs = pack8(dsv + 8 * kb);
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
-                    dq[t] = mfma(frag_tr<false>(Kr, 32 * jt + 16 * kb, 32 * t, true, lane), bs, dq[t]);
+                    acc0[t] = mfma(frag_tr<false>(T0, 32 * jt + 16 * kb, 32 * t, true, lane), bs, acc0[t]);
             }
         }
+        if (ri < len) store_rowT(dqkv + (int64_t)(base + ri) * ld + h * DH, acc0, scale, lh);
+        return;
     }
+    // key workgroup: per-query base-2 lse and D, then Q and dO tiles
+    {
+        const int i = tid >> 1, half = tid & 1;
+        float Dv = dsum_half(dout, out, (int64_t)(base + i) * d + h * DH + 8 * half, i < len);
+        Dv += __shfl_xor(Dv, 1);
+        if (!half) {
+            rowL[i] = i < len ? lse[rb + i] * kLog2e : 0.f;
+            rowD[i] = Dv;
+        }
+    }
+    bf16x8_t ka[4], va[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        ka[kk] = ld8(qkv + (int64_t)(base + ri) * ld + d + hc + 16 * kk, ri < len);
+        va[kk] = ld8(qkv + (int64_t)(base + ri) * ld + 2 * d + hc + 16 * kk, ri < len);
+    }
+    stage64(T0, qkv + h * DH, ld, base, len, tid);
+    stage64(T1, dout + h * DH, d, base, len, tid);
     __syncthreads();
-    if (!active) return;  // no barrier follows
-    if (qi < len) {
-        // dQ^T accumulator: head column c = 32 t + 8 q + 4 lh + (r mod 4), query qi
-        bf16_t* row = dqkv + (int64_t)(base + qi) * ld + h * DH;
+    if (r0 >= len) return;  // no barrier follows
+    for (int it = 0; it < n32; ++it) {
+        f32x16 S, G;
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int r = 0; r < 16; ++r) S[r] = G[r] = 0.f;
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                *reinterpret_cast<uint2*>(row + 32 * t + 8 * q + 4 * lh) =
-                    pack4f(dq[t][4 * q] * scale, dq[t][4 * q + 1] * scale, dq[t][4 * q + 2] * scale,
-                           dq[t][4 * q + 3] * scale);
-    }
-    // phase 2: keys j0 .. j0 + 31 (j0 < len: this wave was active)
-    f32x16 dk[2], dv[2];
+        for (int kk = 0; kk < 4; ++kk) {
+            S = mfma(frag_row(T0, 32 * it, 16 * kk, lane), ka[kk], S);
+            G = mfma(frag_row(T1, 32 * it, 16 * kk, lane), va[kk], G);
+        }
+        // S, G: the lane's key ri, queries i = 32 it + 8 q + 4 lh + (r mod 4)
+        float pv[16], dsv[16];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+        for (int q = 0; q < 4; ++q) {
+            const int i0 = 32 * it + 8 * q + 4 * lh;
+            const f32x4 L4 = *reinterpret_cast<const f32x4*>(&rowL[i0]);
+            const f32x4 D4 = *reinterpret_cast<const f32x4*>(&rowD[i0]);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dk[t][r] = dv[t][r] = 0.f;
-    const int j0 = 32 * w;
-    for (int k16 = 0; k16 < 2 * nj; ++k16) {
-        const bf16x8_t b_ds = frag_tr<true>(Dq, 16 * k16, j0, false, lane);
-        const bf16x8_t b_p = frag_tr<true>(Pq, 16 * k16, j0, false, lane);
+            for (int e = 0; e < 4; ++e) {
+                const int r = 4 * q + e;
+                const float p = ri < len && i0 + e < len ? __builtin_amdgcn_exp2f(fmaf(S[r], c2, -L4[e])) : 0.f;
+                pv[r] = p;
+                dsv[r] = p * (G[r] - D4[e]);
+            }
+        }
+        // dV^T += dO^T P and dK^T += Q^T dS over this tile's queries
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            dk[t] = mfma(frag_tr<false>(Qr, 16 * k16, 32 * t, false, lane), b_ds, dk[t]);
-            dv[t] = mfma(frag_tr<false>(Gr, 16 * k16, 32 * t, false, lane), b_p, dv[t]);
+        for (int kb = 0; kb < 2; ++kb) {
+            const bf16x8_t bp = pack8(pv + 8 * kb), bs = pack8(dsv + 8 * kb);
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                acc1[t] = mfma(frag_tr<false>(T1, 32 * it + 16 * kb, 32 * t, true, lane), bp, acc1[t]);
+                acc0[t] = mfma(frag_tr<false>(T0, 32 * it + 16 * kb, 32 * t, true, lane), bs, acc0[t]);
+            }
         }
     }
-    // dK^T, dV^T accumulators: key j0 + lr, head columns 32 t + 8 q + 4 lh + (r mod 4)
-    const int j = j0 + lr;
-    if (j < len) {
-        bf16_t* row = dqkv + (int64_t)(base + j) * ld + h * DH;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int c = 32 * t + 8 * q + 4 * lh;
-                *reinterpret_cast<uint2*>(row + d + c) =
-                    pack4f(dk[t][4 * q] * scale, dk[t][4 * q + 1] * scale, dk[t][4 * q + 2] * scale,
-                           dk[t][4 * q + 3] * scale);
-                *reinterpret_cast<uint2*>(row + 2 * d + c) =
-                    pack4f(dv[t][4 * q], dv[t][4 * q + 1], dv[t][4 * q + 2], dv[t][4 * q + 3]);
-            }
+    if (ri < len) {
+        bf16_t* row = dqkv + (int64_t)(base + ri) * ld + h * DH;
+        store_rowT(row + d, acc0, scale, lh);
+        store_rowT(row + 2 * d, acc1, 1.f, lh);
     }
 }
 
@@ -559,7 +590,7 @@ fo_status launch_attn_bwd(const bf16_t* qkv, const int* cu, const bf16_t* out, c
     hipEvent_t ea, eb;
     const int h = prof_begin_ext("attn_bwd_mfma", pi, &ea, &eb);
     int* snap = B + 1 <= kProfSnapInts ? prof_snap(h) : nullptr;
-    hipExtLaunchKernelGGL(attn_bwd_mfma, dim3(B * H), dim3(256), 0, s, ea, eb, 0, qkv, cu, out, dout, lse, dqkv, H, d,
+    hipExtLaunchKernelGGL(attn_bwd_mfma, dim3(2 * B * H), dim3(256), 0, s, ea, eb, 0, qkv, cu, out, dout, lse, dqkv, H, d,
                           scale, snap, B, order);
     prof_end_ext(h);
     FO_LAUNCHED();

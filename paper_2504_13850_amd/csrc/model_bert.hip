@@ -267,7 +267,7 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const SplitRows src, float*
 // parameter gradients and of dx: part[block][0][c] = sum dy * xhat (dgamma),
 // part[block][1][c] = sum dy (dbeta), part[block][2][c] = sum dx (the bias
 // gradient of the sublayer whose sum with the residual this norm normalises).
-constexpr int LNB_ROWS = 16;
+constexpr int LNB_ROWS = 4;
 __global__ void __launch_bounds__(256) ln_bwd_kernel(const SplitRows dy, const float* __restrict__ u,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
                                                      const float* __restrict__ g, const int* __restrict__ Tdev,
