@@ -22,6 +22,16 @@ paper is silent:
   slot goes on top.
 * Aggregation versions (Alg. 4): staleness s = t - t_k; a model with
   s > D is skipped and t is unchanged; otherwise t increases by one.
+* FIFO policy (the scheduler ablation of Sec. 6.5): get() serves the
+  activation batch admitted earliest over all devices instead of the
+  least-served device; c_k is still counted.
+* 'Turn-on' signals (Sec. 3.4.1): a signal is counted each time the check
+  after an enqueue or dequeue switches an off Sender back on.
+* Leaving and rejoining (Sec. 3.4.2, dropout of Sec. 6.4): a device that
+  leaves has its Sender switched off and kept off (it sends nothing); the
+  batches it already sent stay queued and are served as usual.  A device
+  that rejoins starts with its Sender on, like a device joining for the
+  first time, and keeps its counter c_k.
 """
 from __future__ import annotations
 
@@ -29,7 +39,10 @@ from collections import deque
 
 
 class TaskScheduler:
-    def __init__(self, K: int, n_slots: int | None = None):
+    def __init__(self, K: int, n_slots: int | None = None, policy: str = "counter"):
+        if policy not in ("counter", "fifo"):
+            raise ValueError(policy)
+        self.policy = policy
         self.K = K
         self.n_slots = n_slots
         self.omega = None if n_slots is None else n_slots - K
@@ -45,14 +58,20 @@ class TaskScheduler:
         self.t = 0
         self.refused = 0
         self.peak_queued = 0
+        self.active = [True] * K
+        self.admissions = 0  # admission order over all devices (FIFO policy)
+        self.turn_on_signals = 0
 
     # ------------------------------------------------------------ helpers
     def queued(self) -> int:
         return sum(len(q) for q in self.q_act)
 
     def _turn_on_check(self, k):
+        if not self.active[k] or self.sender_on[k]:
+            return
         if self.omega is None or self.queued() < self.omega:
             self.sender_on[k] = True
+            self.turn_on_signals += 1
 
     # ------------------------------------------------------------ Alg. 2
     def put_act(self, k: int):
@@ -65,7 +84,8 @@ class TaskScheduler:
             slot = self.free.pop()
         s = self.seq[k]
         self.seq[k] += 1
-        self.q_act[k].append((s, slot))
+        self.q_act[k].append((s, slot, self.admissions))
+        self.admissions += 1
         self.sender_on[k] = False
         self._turn_on_check(k)
         self.peak_queued = max(self.peak_queued, self.queued())
@@ -82,11 +102,17 @@ class TaskScheduler:
             return ("model", k, t_k)
         best = None
         for k in range(self.K):
-            if self.q_act[k] and (best is None or self.c[k] < self.c[best]):
+            if not self.q_act[k]:
+                continue
+            if best is None:
+                best = k
+            elif self.policy == "counter" and self.c[k] < self.c[best]:
+                best = k
+            elif self.policy == "fifo" and self.q_act[k][0][2] < self.q_act[best][0][2]:
                 best = k
         if best is None:
             return None
-        s, slot = self.q_act[best].popleft()
+        s, slot, _ = self.q_act[best].popleft()
         self.c[best] += 1
         self._turn_on_check(best)
         self.in_service = slot
@@ -120,4 +146,11 @@ class TaskScheduler:
         self.c.append(0)
         self.sender_on.append(True)
         self.seq.append(0)
+        self.active.append(True)
         return self.K - 1
+
+    def set_active(self, k: int, active: bool):
+        """Device k leaves (active False: its Sender goes off and stays off) or
+        rejoins (active True: its Sender starts on)."""
+        self.active[k] = bool(active)
+        self.sender_on[k] = bool(active)

@@ -66,8 +66,8 @@ def test_sequence_matches_closed_form():
 
 
 # ----------------------------------------------------------------------------- scheduler
-def _run_trace(name, K, n_slots, with_slot):
-    sch = TaskScheduler(K, n_slots)
+def _run_trace(name, K, n_slots, with_slot, policy="counter"):
+    sch = TaskScheduler(K, n_slots, policy=policy)
     for op, args, exp in read_trace(name):
         if op == "put_act":
             ok, seq, slot = sch.put_act(args[0])
@@ -83,6 +83,9 @@ def _run_trace(name, K, n_slots, with_slot):
         elif op == "release":
             sch.release()
             got = "-"
+        elif op in ("leave", "join"):
+            sch.set_active(args[0], op == "join")
+            got = "-"
         assert got == exp, (op, args, got, exp)
     return sch
 
@@ -94,6 +97,62 @@ def test_golden_scheduler_trace():
 def test_golden_flow_control_trace():
     sch = _run_trace("flow_trace_k2.txt", 2, 4, True)
     assert sch.refused == 3
+
+
+def test_golden_fifo_leave_trace():
+    sch = _run_trace("fifo_leave_trace_k3.txt", 3, 5, True, policy="fifo")
+    assert sch.refused == 2 and sch.turn_on_signals == 5
+
+
+def test_fifo_matches_one_global_queue_random_trace():
+    """FIFO against an independent statement: one list of every admitted
+    batch in admission order, served from its head; devices leave and rejoin
+    at random and the memory bound of the flow control still holds."""
+    K, n_slots = 5, 12
+    rng = np.random.default_rng(11)
+    sch = TaskScheduler(K, n_slots, policy="fifo")
+    order = []
+    active = [True] * K
+    for step in range(2000):
+        k = int(rng.integers(K))
+        if rng.random() < 0.05:
+            active[k] = not active[k]
+            sch.set_active(k, active[k])
+        for k in range(K):
+            for _ in range(rng.poisson(0.8)):
+                ok, seq, _ = sch.put_act(k)
+                assert not (ok and not active[k])  # a device that left sends nothing
+                if ok:
+                    order.append((k, seq))
+        assert sch.queued() <= sch.omega + K - 1
+        r = sch.get()
+        if order:
+            assert r[:3] == ("act",) + order.pop(0)
+            sch.release()
+        else:
+            assert r is None
+    assert sch.refused > 0 and sch.turn_on_signals > 0
+
+
+def test_counter_and_fifo_differ_on_skewed_arrivals():
+    """Device 0 sends three batches per server step, device 1 one every third
+    step, and the server trains on one batch per step, so a backlog builds.
+    The counter policy serves device 1's batches as they come (c_1 = all 67
+    of them); FIFO serves the backlog in arrival order, and device 1 gets
+    only its share of the first 200 arrivals (the effect Sec. 6.5 measures)."""
+    res = {}
+    for policy in ("counter", "fifo"):
+        sch = TaskScheduler(2, policy=policy)
+        for step in range(200):
+            for _ in range(3):
+                sch.put_act(0)
+            if step % 3 == 0:
+                sch.put_act(1)
+            sch.get()
+            sch.release()
+        res[policy] = list(sch.c)
+    assert res["counter"] == [133, 67]
+    assert res["fifo"][1] <= 20 and sum(res["fifo"]) == 200
 
 
 def _brute_force_pick(queues, c):
