@@ -223,6 +223,10 @@ FO_API fo_status fo_set_max_delay(int64_t max_delay);
  * below omega = n_slots - K.  Queued plus in-service batches therefore never
  * exceed n_slots, whatever K is (Eq. 3: memory = model + omega activation
  * batches, independent of the number of devices).
+ * Threads: every pool entry point takes the pool's lock, so pushes (the
+ * Receiver's side) and picks, releases and aggregations (the Compute
+ * Engine's side) may come from different host threads; the order in which
+ * the pool performed them is the order of its event record.
  * Errors: FO_EINVAL (K < 1, n_slots <= K, batch < 1), FO_ENOMEM, FO_EHIP. */
 FO_API fo_status fo_queues_create(int32_t K, int64_t slot_bytes, int32_t batch, int32_t with_lengths,
                            int64_t n_slots, void* hip_stream, fo_queues** out);
@@ -313,6 +317,9 @@ typedef struct {
     int64_t queued, in_service, models_pending;
     int64_t admitted, refused, picks, peak_queued;
     int64_t version;            /* global version t */
+    int64_t turn_on_signals;    /* off Senders switched on by the cap check (Sec. 3.4.1) */
+    int32_t active_devices;     /* devices that have not left */
+    int32_t policy;             /* FO_SCHED_COUNTER or FO_SCHED_FIFO */
 } fo_queue_stats;
 FO_API fo_status fo_queues_stats(const fo_queues* q, fo_queue_stats* out);
 /* Copies the counters c_k of the first K devices into c_out. */
@@ -320,6 +327,114 @@ FO_API fo_status fo_queues_counters(const fo_queues* q, int64_t* c_out, int32_t 
 /* A device joining mid-run: a new empty queue with c_k = 0 and its Sender on.
  * Returns the new device index, or -1 on error. */
 FO_API int32_t fo_queues_add_device(fo_queues* q);
+
+/* Which activation batch get() serves (Alg. 3 and the scheduler ablation of
+ * Sec. 6.5).  FO_SCHED_COUNTER (default): the oldest batch of the device with
+ * the smallest consumption counter c_k among devices with a queued batch,
+ * lowest index on ties.  FO_SCHED_FIFO: the batch admitted earliest over all
+ * devices.  c_k is counted under both.  Models are always served first.
+ * Errors: FO_EINVAL (unknown policy). */
+enum { FO_SCHED_COUNTER = 0, FO_SCHED_FIFO = 1 };
+FO_API fo_status fo_queues_set_policy(fo_queues* q, int32_t policy);
+
+/* Device k leaves (active = 0) or rejoins (active = 1) training (Sec. 3.4.2;
+ * the dropout of Sec. 6.4).  A device that has left has its Sender Status off
+ * and kept off: every batch it would send is refused (FO_FULL) and no
+ * 'turn-on' signal reaches it; the batches it sent before leaving stay queued
+ * and are served as usual.  On rejoining its Sender starts on, as for a device
+ * joining for the first time, and it keeps its counter c_k.  Setting the state
+ * a device already has does nothing.  Errors: FO_EINVAL (k out of range). */
+FO_API fo_status fo_queues_set_device_active(fo_queues* q, int32_t k, int32_t active);
+
+/* The Sender Status of device k as the device sees it (Sec. 3.4.1): 1 if its
+ * next batch would be admitted, 0 if it would be refused, -1 on error. */
+FO_API int32_t fo_queues_sender_status(fo_queues* q, int32_t k);
+
+/* Event record of the pool: every state transition in the order the pool
+ * performed them, four int64 per event (type, device k, a, b):
+ *   FO_EV_PUSH     a = 1 admitted (b = its sequence number) | 0 refused (b = -1)
+ *   FO_EV_MODEL    a = t_k of the model message put (Alg. 2)
+ *   FO_EV_PICK     a = sequence number, b = slot of the batch served (Alg. 3)
+ *   FO_EV_RELEASE  a = sequence number, b = slot
+ *   FO_EV_AGG      a = 1 applied | 0 skipped (staleness > D), b = staleness (Alg. 4)
+ *   FO_EV_LEAVE    device k left
+ *   FO_EV_JOIN     a = 1: new device (fo_queues_add_device) | 0: device k rejoined
+ * fo_queues_log_enable reserves room for max_events (host memory, allocated
+ * here, never during recording), clears the record and starts recording; events
+ * beyond max_events are dropped.  fo_queues_log_read copies the first
+ * min(max_events, recorded) events into out ([max_events][4]) and reports the
+ * number recorded in *n_out.  Errors: FO_EINVAL, FO_ENOMEM. */
+enum { FO_EV_PUSH = 1, FO_EV_MODEL = 2, FO_EV_PICK = 3, FO_EV_RELEASE = 4, FO_EV_AGG = 5, FO_EV_LEAVE = 6,
+       FO_EV_JOIN = 7 };
+FO_API fo_status fo_queues_log_enable(fo_queues* q, int64_t max_events);
+FO_API fo_status fo_queues_log_read(fo_queues* q, int64_t* out, int64_t max_events, int64_t* n_out);
+
+/* ------------------------------------------------------------------ concurrent pipeline
+ * The server's concurrent structure (Sec. 5.1: Receiver, Task Scheduler and
+ * Compute Engine threads) run for a fixed wall-clock time against K emulated
+ * devices, with the flow control of Sec. 3.4.1, devices leaving and rejoining
+ * (Sec. 3.4.2) and the dropout and bandwidth variation of Sec. 6.4.
+ *
+ * Receiver thread (the devices, Alg. 1): device k runs local iterations of
+ * iter_seconds[k] x s seconds each, s the slow-down factor of the current
+ * interval.  After each iteration it puts its next activation batch if its
+ * Sender Status is on, else goes on without sending; after every H
+ * iterations it also puts its model (tagged with the global version t_k it
+ * holds) and waits for the server's reply before its next iteration.  At the
+ * start of every interval of interval_seconds each device is away for that
+ * interval with probability p_drop (fo_queues_set_device_active), and a
+ * present device draws s from U[1, slow_max]; the draws come from splitmix64
+ * of (seed, interval, device), so they do not depend on thread timing.
+ * Compute Engine thread (the server, Alg. 3 and Alg. 4): a pending model is
+ * aggregated with weight alpha / (staleness + 1) (or skipped past the maximum
+ * delay) on the pool's stream, and its device then holds the current global
+ * version; otherwise the pick is trained on with fo_server_step on the model's
+ * stream, at most max_inflight steps ahead of the GPU.  With nothing queued
+ * the engine first waits for its steps to finish and then sleeps until a
+ * device puts something: that sleep is the server's idle time.
+ *
+ * Activations the devices send: bank_n batches in device memory laid out like
+ * the pool's slots; device k's n-th sent batch is entry (k + n) mod bank_n.
+ * Device models: n_local vectors of global->n floats (n % 4 == 0, 16-byte
+ * aligned) in device memory; device k's r-th model is entry (k + r) mod
+ * n_local.  The run ends after `seconds` (whatever is still queued stays in
+ * the pool) once the GPU work it enqueued has finished.  With the pool's
+ * event record enabled, the record is the exact interleaving of the two
+ * threads' pool operations.
+ * Errors: FO_EINVAL (bad configuration, a device-side model, a batch in
+ * service), FO_ENOMEM, FO_EHIP, or the first error either thread hit (its
+ * message in fo_last_error). */
+typedef struct {
+    double seconds;              /* wall-clock length of the run, > 0 */
+    const double* iter_seconds;  /* host [K]: seconds per local iteration of device k, > 0 */
+    int32_t H;                   /* local iterations per round (a model put every H), >= 1 */
+    double p_drop;               /* probability a device is away for an interval, in [0, 1) */
+    double interval_seconds;     /* length of a dropout / bandwidth interval, > 0 */
+    double slow_max;             /* slow-down factors drawn from U[1, slow_max], >= 1 */
+    uint64_t seed;
+    const void* bank_x;          /* device [bank_n][slot_bytes], 16-byte aligned */
+    const int32_t* bank_labels;  /* device [bank_n][batch] */
+    const int32_t* bank_lengths; /* device [bank_n][batch] if the pool has lengths, else NULL */
+    int32_t bank_n;
+    const float* local_bank;     /* device [n_local][global->n] */
+    int32_t n_local;
+    float alpha;                 /* aggregation weight of Alg. 4, in [0, 1] */
+    int32_t max_inflight;        /* in [1, 64] */
+} fo_pipeline_config;
+
+typedef struct {
+    double wall_seconds;         /* start to the end of the last GPU work */
+    double idle_seconds;         /* Compute Engine idle: nothing queued, no step in flight */
+    int64_t steps, samples;      /* training iterations (Alg. 4) and their samples */
+    int64_t aggregations, skipped; /* models applied / skipped (staleness > D) */
+    int64_t sent, not_sent;      /* activation batches sent / withheld (Sender off) */
+    int64_t models_sent;
+    int64_t leaves, rejoins;     /* dropout transitions after the first interval's draw */
+    int64_t device_iterations;   /* local iterations completed by all devices */
+} fo_pipeline_stats;
+
+FO_API fo_status fo_pipeline_run(fo_queues* q, fo_model* m, fo_vec* global, const fo_pipeline_config* cfg,
+                                 fo_pipeline_stats* out);
 
 /* ------------------------------------------------------------------ instrumentation
  * Kernel timing for benchmarks and tuning.  While enabled on a thread, every

@@ -27,8 +27,11 @@ EXPORTS = [
     "fo_queues_release", "fo_aggregate_pending", "fo_aggregate_pending_all", "fo_queues_stats",
     "fo_queues_counters", "fo_queues_add_device", "fo_last_error", "fo_profile_enable", "fo_profile_read",
     "fo_set_graph_mode", "fo_gemm_bf16", "fo_conv2d_bf16", "fo_gemm_bf16_noalloc", "fo_queues_push_batch",
-    "fo_queues_push_model_batch", "fo_device_step",
+    "fo_queues_push_model_batch", "fo_device_step", "fo_queues_set_policy", "fo_queues_set_device_active",
+    "fo_queues_sender_status", "fo_queues_log_enable", "fo_queues_log_read", "fo_pipeline_run",
 ]
+FO_SCHED_COUNTER, FO_SCHED_FIFO = 0, 1
+FO_EV_PUSH, FO_EV_MODEL, FO_EV_PICK, FO_EV_RELEASE, FO_EV_AGG, FO_EV_LEAVE, FO_EV_JOIN = range(1, 8)
 FO_LAYOUT_ROW_K, FO_LAYOUT_K_ROW = 0, 1
 
 
@@ -55,7 +58,23 @@ class fo_queue_stats(C.Structure):
     _fields_ = [("K", C.c_int32), ("n_slots", C.c_int64), ("omega", C.c_int64), ("queued", C.c_int64),
                 ("in_service", C.c_int64), ("models_pending", C.c_int64), ("admitted", C.c_int64),
                 ("refused", C.c_int64), ("picks", C.c_int64), ("peak_queued", C.c_int64),
-                ("version", C.c_int64)]
+                ("version", C.c_int64), ("turn_on_signals", C.c_int64), ("active_devices", C.c_int32),
+                ("policy", C.c_int32)]
+
+
+class fo_pipeline_config(C.Structure):
+    _fields_ = [("seconds", C.c_double), ("iter_seconds", C.c_void_p), ("H", C.c_int32), ("p_drop", C.c_double),
+                ("interval_seconds", C.c_double), ("slow_max", C.c_double), ("seed", C.c_uint64),
+                ("bank_x", C.c_void_p), ("bank_labels", C.c_void_p), ("bank_lengths", C.c_void_p),
+                ("bank_n", C.c_int32), ("local_bank", C.c_void_p), ("n_local", C.c_int32), ("alpha", C.c_float),
+                ("max_inflight", C.c_int32)]
+
+
+class fo_pipeline_stats(C.Structure):
+    _fields_ = [("wall_seconds", C.c_double), ("idle_seconds", C.c_double), ("steps", C.c_int64),
+                ("samples", C.c_int64), ("aggregations", C.c_int64), ("skipped", C.c_int64), ("sent", C.c_int64),
+                ("not_sent", C.c_int64), ("models_sent", C.c_int64), ("leaves", C.c_int64), ("rejoins", C.c_int64),
+                ("device_iterations", C.c_int64)]
 
 
 _lib = None
@@ -102,6 +121,13 @@ def lib():
             "fo_queues_stats": (C.c_int, [vp, C.POINTER(fo_queue_stats)]),
             "fo_queues_counters": (C.c_int, [vp, vp, i32]),
             "fo_queues_add_device": (i32, [vp]),
+            "fo_queues_set_policy": (C.c_int, [vp, i32]),
+            "fo_queues_set_device_active": (C.c_int, [vp, i32, i32]),
+            "fo_queues_sender_status": (i32, [vp, i32]),
+            "fo_queues_log_enable": (C.c_int, [vp, i64]),
+            "fo_queues_log_read": (C.c_int, [vp, vp, i64, C.POINTER(i64)]),
+            "fo_pipeline_run": (C.c_int, [vp, vp, C.POINTER(fo_vec), C.POINTER(fo_pipeline_config),
+                                          C.POINTER(fo_pipeline_stats)]),
             "fo_last_error": (C.c_char_p, []),
             "fo_profile_enable": (C.c_int, [i32]),
             "fo_set_graph_mode": (C.c_int, [i32]),
@@ -319,6 +345,59 @@ def fo_queues_add_device(q) -> int:
     if r < 0:
         raise FoError(FO_EINVAL, last_error())
     return r
+
+
+def fo_queues_set_policy(q, policy: int):
+    _check(lib().fo_queues_set_policy(q, policy))
+
+
+def fo_queues_set_device_active(q, k: int, active: bool):
+    _check(lib().fo_queues_set_device_active(q, k, 1 if active else 0))
+
+
+def fo_queues_sender_status(q, k: int) -> int:
+    r = lib().fo_queues_sender_status(q, k)
+    if r < 0:
+        raise FoError(FO_EINVAL, last_error())
+    return r
+
+
+def fo_queues_log_enable(q, max_events: int):
+    _check(lib().fo_queues_log_enable(q, max_events))
+
+
+def fo_queues_log_read(q, max_events: int) -> np.ndarray:
+    """The pool's event record as an int64 array [n][4] (type, device, a, b)."""
+    out = np.zeros((max(max_events, 0), 4), np.int64)
+    n = C.c_int64(0)
+    _check(lib().fo_queues_log_read(q, out.ctypes.data, max_events, C.byref(n)))
+    return out[:min(n.value, max_events)]
+
+
+def fo_pipeline_run(q, model, global_vec, cfg: dict) -> fo_pipeline_stats:
+    """Runs the concurrent pipeline; cfg holds the fo_pipeline_config fields
+    (iter_seconds as a sequence of floats, device buffers as tensors)."""
+    iters = np.ascontiguousarray(cfg["iter_seconds"], np.float64)
+    c = fo_pipeline_config()
+    c.seconds = cfg["seconds"]
+    c.iter_seconds = iters.ctypes.data
+    c.H = cfg["H"]
+    c.p_drop = cfg.get("p_drop", 0.0)
+    c.interval_seconds = cfg.get("interval_seconds", 1.0)
+    c.slow_max = cfg.get("slow_max", 1.0)
+    c.seed = cfg.get("seed", 0)
+    c.bank_x = _dptr(cfg["bank_x"])
+    c.bank_labels = _dptr(cfg["bank_labels"])
+    c.bank_lengths = _dptr(cfg.get("bank_lengths"))
+    c.bank_n = cfg["bank_n"]
+    c.local_bank = _dptr(cfg["local_bank"])
+    c.n_local = cfg["n_local"]
+    c.alpha = cfg.get("alpha", 0.5)
+    c.max_inflight = cfg.get("max_inflight", 2)
+    g = fo_vec(_dptr(global_vec), int(global_vec.numel()))
+    st = fo_pipeline_stats()
+    _check(lib().fo_pipeline_run(q, model, C.byref(g), C.byref(c), C.byref(st)))
+    return st
 
 
 # ------------------------------------------------------------------ instrumentation

@@ -18,4 +18,8 @@ fo_status pool_step_begin(const fo_acts* acts, const int32_t* labels, int32_t de
 // makes the next copy into the slot wait for the step.
 fo_status pool_step_done(fo_queues* q, hipStream_t step_stream);
 
+// Slot size, batch and whether slots hold lengths; the pool's stream.
+void pool_geometry(const fo_queues* q, int64_t* slot_bytes, int32_t* batch, int32_t* with_lengths);
+hipStream_t pool_stream(const fo_queues* q);
+
 }  // namespace fo

@@ -5,11 +5,16 @@
 // admitted batch into its preallocated slot and the aggregation kernels,
 // both ordered on the pool's stream.
 //
+// Every entry point takes the pool's own lock, so that the Receiver side
+// (pushes of activations and models) and the Compute Engine side (picks,
+// releases, aggregations) may run on different host threads.
+//
 // Live pools are kept in a registry so that a training step whose batch lies
 // in a pool slot can be checked against that pool's last pick, and so that a
 // step enqueued on a stream other than the pool's is ordered before the
 // slot's next reuse (an event recorded after the step, waited for by the
 // pool's stream before its next copy into that slot).
+#include <algorithm>
 #include <atomic>
 #include <deque>
 #include <mutex>
@@ -34,20 +39,37 @@ struct fo_queues {
     int32_t* labels = nullptr;
     int32_t* lengths = nullptr;
 
-    struct Item { int64_t seq, slot; };
+    mutable std::mutex mu;
+    int32_t policy = FO_SCHED_COUNTER;
+
+    struct Item { int64_t seq, slot, order; };  // order: admission index over all devices
     std::vector<std::deque<Item>> q;
     std::vector<int64_t> c, next_seq;
     std::vector<uint8_t> sender_on;
+    std::vector<uint8_t> active;  // 0 while a device has left
     std::vector<int64_t> free_stack;
 
     bool busy = false;  // a batch is in service
     int32_t svc_k = -1;
-    Item svc{-1, -1};
+    Item svc{-1, -1, -1};
 
     struct ModelMsg { int32_t k; const float* local; int64_t n; int64_t t_k; };
     std::deque<ModelMsg> qm;
 
-    int64_t t = 0, queued = 0, admitted = 0, refused = 0, picks = 0, peak = 0;
+    int64_t t = 0, queued = 0, admitted = 0, refused = 0, picks = 0, peak = 0, turn_ons = 0;
+
+    // Optional record of every state transition, four int64 per event
+    // (type, device, a, b), reserved up front so recording never allocates.
+    int64_t log_cap = 0;
+    std::vector<int64_t> log;
+    void log_ev(int64_t type, int64_t k, int64_t a, int64_t b) {
+        if ((int64_t)log.size() < 4 * log_cap) {
+            log.push_back(type);
+            log.push_back(k);
+            log.push_back(a);
+            log.push_back(b);
+        }
+    }
 
     // Slot reuse across streams: svc_ev is recorded after a step that read the
     // batch in service from another stream; on release it guards that slot,
@@ -66,8 +88,13 @@ struct fo_queues {
         return labels && c >= labels && c < labels + (int64_t)batch * n_slots;
     }
 
+    // after an enqueue to or dequeue from Q_k: below the cap, an off Sender of a
+    // present device gets a 'turn-on' signal
     void turn_on_check(int32_t k) {
-        if (queued < omega) sender_on[k] = 1;
+        if (active[k] && !sender_on[k] && queued < omega) {
+            sender_on[k] = 1;
+            turn_ons++;
+        }
     }
 };
 
@@ -101,6 +128,7 @@ extern "C" fo_status fo_queues_create(int32_t K, int64_t slot_bytes, int32_t bat
         q->c.assign(K, 0);
         q->next_seq.assign(K, 0);
         q->sender_on.assign(K, 1);
+        q->active.assign(K, 1);
         q->free_stack.reserve(n_slots);
         for (int64_t s = n_slots - 1; s >= 0; --s) q->free_stack.push_back(s);
     } catch (...) {
@@ -168,6 +196,7 @@ fo_status pool_step_begin(const fo_acts* acts, const int32_t* labels, int32_t de
     for (fo_queues* q : g_pools) {
         const bool x_in = q->in_slab(acts->x), lab_in = q->in_labels(labels);
         if (!x_in && !lab_in) continue;
+        std::lock_guard<std::mutex> ql(q->mu);
         FO_CHECK(q->busy, "fo_server_step: the batch lies in a pool slot that is not in service");
         const char* x_svc = q->slab + q->svc.slot * q->slot_bytes;
         const int32_t* lab_svc = q->labels + q->svc.slot * q->batch;
@@ -191,8 +220,16 @@ fo_status pool_step_begin(const fo_acts* acts, const int32_t* labels, int32_t de
     return FO_OK;
 }
 
+void pool_geometry(const fo_queues* q, int64_t* slot_bytes, int32_t* batch, int32_t* with_lengths) {
+    *slot_bytes = q->slot_bytes;
+    *batch = q->batch;
+    *with_lengths = q->with_lengths;
+}
+hipStream_t pool_stream(const fo_queues* q) { return q->stream; }
+
 fo_status pool_step_done(fo_queues* q, hipStream_t step_stream) {
     if (step_stream == q->stream) return FO_OK;  // stream order already keeps the reuse after the step
+    std::lock_guard<std::mutex> lk(q->mu);
     if (!q->svc_ev) {
         if (!q->ev_free.empty()) {
             q->svc_ev = q->ev_free.back();
@@ -216,6 +253,7 @@ namespace {
 fo_status admit(fo_queues* q, int32_t k, int64_t* slot_out) {
     if (!q->sender_on[k]) {
         q->refused++;
+        q->log_ev(FO_EV_PUSH, k, 0, -1);
         return FO_FULL;
     }
     if (q->free_stack.empty()) {  // cannot happen while omega = n_slots - K holds
@@ -230,7 +268,7 @@ fo_status admit(fo_queues* q, int32_t k, int64_t* slot_out) {
         q->guard.erase(g);
     }
     try {
-        q->q[k].push_back({q->next_seq[k], slot});
+        q->q[k].push_back({q->next_seq[k], slot, q->admitted});
     } catch (...) {
         set_error("fo_queues_push: out of host memory");
         return FO_ENOMEM;
@@ -241,6 +279,7 @@ fo_status admit(fo_queues* q, int32_t k, int64_t* slot_out) {
     q->admitted++;
     if (q->queued > q->peak) q->peak = q->queued;
     q->sender_on[k] = 0;   // deactivated until the server turns it on
+    q->log_ev(FO_EV_PUSH, k, 1, q->next_seq[k] - 1);
     q->turn_on_check(k);   // enqueue: below the cap -> 'turn-on'
     *slot_out = slot;
     return FO_OK;
@@ -251,6 +290,7 @@ fo_status admit(fo_queues* q, int32_t k, int64_t* slot_out) {
 extern "C" fo_status fo_queues_push(fo_queues* q, int32_t k, const void* x_src, const int32_t* labels_src,
                                     const int32_t* lengths_src, int32_t src_on_host) {
     FO_CHECK(q != nullptr, "fo_queues_push: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
     FO_CHECK(k >= 0 && k < q->K, "fo_queues_push: device %d out of range [0,%d)", k, q->K);
     if (q->slab) {
         FO_CHECK(x_src != nullptr && labels_src != nullptr, "fo_queues_push: NULL source");
@@ -276,6 +316,7 @@ extern "C" fo_status fo_queues_push_batch(fo_queues* q, int32_t n, const int32_t
                                           const int32_t* const* labels_src, const int32_t* const* lengths_src,
                                           int32_t* status_out) {
     FO_CHECK(q != nullptr, "fo_queues_push_batch: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
     FO_CHECK(n >= 0 && (n == 0 || k != nullptr), "fo_queues_push_batch: n=%d", n);
     for (int32_t i = 0; i < n; ++i) {  // every argument checked before any state changes
         FO_CHECK(k[i] >= 0 && k[i] < q->K, "fo_queues_push_batch: entry %d: device %d out of range [0,%d)", i, k[i],
@@ -321,11 +362,13 @@ extern "C" fo_status fo_queues_push_batch(fo_queues* q, int32_t n, const int32_t
 
 extern "C" fo_status fo_queues_push_model(fo_queues* q, int32_t k, const float* local, int64_t n, int64_t t_k) {
     FO_CHECK(q != nullptr, "fo_queues_push_model: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
     FO_CHECK(k >= 0 && k < q->K, "fo_queues_push_model: device %d out of range [0,%d)", k, q->K);
     FO_CHECK(n >= 0 && (n == 0 || local != nullptr), "fo_queues_push_model: bad vector");
     FO_CHECK(t_k >= 0, "fo_queues_push_model: negative version");
     try {
         q->qm.push_back({k, local, n, t_k});
+        q->log_ev(FO_EV_MODEL, k, t_k, 0);
     } catch (...) {
         set_error("fo_queues_push_model: out of host memory");
         return FO_ENOMEM;
@@ -336,6 +379,7 @@ extern "C" fo_status fo_queues_push_model(fo_queues* q, int32_t k, const float* 
 extern "C" fo_status fo_queues_push_model_batch(fo_queues* q, int32_t n, const int32_t* k, const float* const* local,
                                                 int64_t len, const int64_t* t_k) {
     FO_CHECK(q != nullptr, "fo_queues_push_model_batch: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
     FO_CHECK(n >= 0 && (n == 0 || (k != nullptr && t_k != nullptr)), "fo_queues_push_model_batch: n=%d", n);
     FO_CHECK(len >= 0 && (len == 0 || n == 0 || local != nullptr), "fo_queues_push_model_batch: bad vectors");
     for (int32_t i = 0; i < n; ++i) {
@@ -344,7 +388,10 @@ extern "C" fo_status fo_queues_push_model_batch(fo_queues* q, int32_t n, const i
         FO_CHECK(len == 0 || local[i] != nullptr, "fo_queues_push_model_batch: entry %d: NULL vector", i);
     }
     try {
-        for (int32_t i = 0; i < n; ++i) q->qm.push_back({k[i], len ? local[i] : nullptr, len, t_k[i]});
+        for (int32_t i = 0; i < n; ++i) {
+            q->qm.push_back({k[i], len ? local[i] : nullptr, len, t_k[i]});
+            q->log_ev(FO_EV_MODEL, k[i], t_k[i], 0);
+        }
     } catch (...) {
         set_error("fo_queues_push_model_batch: out of host memory");
         return FO_ENOMEM;
@@ -357,14 +404,20 @@ extern "C" int32_t fo_pick_device(fo_queues* q) {
         fo::set_error("fo_pick_device: NULL handle");
         return -3;
     }
+    std::lock_guard<std::mutex> lk(q->mu);
     if (!q->qm.empty()) return -2;  // Alg. 3: models are served first
     if (q->busy) {
         fo::set_error("fo_pick_device: release the batch in service first");
         return -3;
     }
     int32_t best = -1;
-    for (int32_t k = 0; k < q->K; ++k)
-        if (!q->q[k].empty() && (best < 0 || q->c[k] < q->c[best])) best = k;
+    for (int32_t k = 0; k < q->K; ++k) {
+        if (q->q[k].empty()) continue;
+        if (best < 0 ||
+            (q->policy == FO_SCHED_COUNTER ? q->c[k] < q->c[best]
+                                           : q->q[k].front().order < q->q[best].front().order))
+            best = k;
+    }
     if (best < 0) return -1;
     q->svc = q->q[best].front();
     q->q[best].pop_front();
@@ -373,6 +426,7 @@ extern "C" int32_t fo_pick_device(fo_queues* q) {
     q->queued--;
     q->c[best]++;
     q->picks++;
+    q->log_ev(FO_EV_PICK, best, q->svc.seq, q->svc.slot);
     q->turn_on_check(best);  // dequeue: below the cap -> 'turn-on'
     return best;
 }
@@ -380,6 +434,7 @@ extern "C" int32_t fo_pick_device(fo_queues* q) {
 extern "C" fo_status fo_queues_in_service(fo_queues* q, fo_acts* acts_out, const int32_t** labels_out,
                                           int64_t* seq_out, int64_t* slot_out) {
     FO_CHECK(q != nullptr, "fo_queues_in_service: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
     if (!q->busy) {
         fo::set_error("fo_queues_in_service: no batch in service");
         return FO_ESTATE;
@@ -397,6 +452,7 @@ extern "C" fo_status fo_queues_in_service(fo_queues* q, fo_acts* acts_out, const
 
 extern "C" fo_status fo_queues_release(fo_queues* q) {
     FO_CHECK(q != nullptr, "fo_queues_release: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
     if (!q->busy) {
         fo::set_error("fo_queues_release: no batch in service");
         return FO_ESTATE;
@@ -411,6 +467,7 @@ extern "C" fo_status fo_queues_release(fo_queues* q) {
         q->svc_ev = nullptr;
     }
     q->free_stack.push_back(q->svc.slot);
+    q->log_ev(FO_EV_RELEASE, q->svc_k, q->svc.seq, q->svc.slot);
     q->busy = false;
     q->svc_k = -1;
     return FO_OK;
@@ -426,6 +483,7 @@ static fo_status check_global(const fo_vec* global, const char* who) {
 extern "C" fo_status fo_aggregate_pending(fo_queues* q, fo_vec* global, float alpha, int32_t* k_out,
                                           int64_t* staleness_out) {
     FO_CHECK(q != nullptr, "fo_aggregate_pending: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
     fo_status st = check_global(global, "fo_aggregate_pending");
     if (st != FO_OK) return st;
     FO_CHECK(alpha >= 0.f && alpha <= 1.f, "fo_aggregate_pending: alpha=%g outside [0,1]", (double)alpha);
@@ -443,6 +501,7 @@ extern "C" fo_status fo_aggregate_pending(fo_queues* q, fo_vec* global, float al
     int64_t D = fo::g_max_delay.load();
     if (D >= 0 && s > D) {
         q->qm.pop_front();
+        q->log_ev(FO_EV_AGG, m.k, 0, s);
         return FO_SKIPPED;
     }
     float w = alpha / (float)(s + 1);
@@ -450,12 +509,14 @@ extern "C" fo_status fo_aggregate_pending(fo_queues* q, fo_vec* global, float al
     if (st != FO_OK) return st;  // not applied: the message stays queued and t is unchanged
     q->qm.pop_front();
     q->t++;
+    q->log_ev(FO_EV_AGG, m.k, 1, s);
     return FO_OK;
 }
 
 extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, float alpha, int32_t* applied_out,
                                               int32_t* skipped_out) {
     FO_CHECK(q != nullptr, "fo_aggregate_pending_all: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
     fo_status st = check_global(global, "fo_aggregate_pending_all");
     if (st != FO_OK) return st;
     FO_CHECK(alpha >= 0.f && alpha <= 1.f, "fo_aggregate_pending_all: alpha=%g outside [0,1]", (double)alpha);
@@ -503,6 +564,15 @@ extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, floa
             st = fo::launch_agg_lerp_multi(global->ptr, tab, global->n, q->stream);
             if (st != FO_OK) return st;
         }
+        {
+            int64_t tl = q->t;
+            for (size_t i = 0; i < used; ++i) {
+                const int64_t s = tl - q->qm[i].t_k;
+                const bool skip = D >= 0 && s > D;
+                q->log_ev(FO_EV_AGG, q->qm[i].k, skip ? 0 : 1, s);
+                if (!skip) tl++;
+            }
+        }
         q->qm.erase(q->qm.begin(), q->qm.begin() + used);
         q->t = t_next;
         applied += tab.count;
@@ -515,6 +585,7 @@ extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, floa
 
 extern "C" fo_status fo_queues_stats(const fo_queues* q, fo_queue_stats* out) {
     FO_CHECK(q != nullptr && out != nullptr, "fo_queues_stats: NULL argument");
+    std::lock_guard<std::mutex> lk(q->mu);
     out->K = q->K;
     out->n_slots = q->n_slots;
     out->omega = q->omega;
@@ -526,11 +597,17 @@ extern "C" fo_status fo_queues_stats(const fo_queues* q, fo_queue_stats* out) {
     out->picks = q->picks;
     out->peak_queued = q->peak;
     out->version = q->t;
+    out->turn_on_signals = q->turn_ons;
+    int32_t present = 0;
+    for (int32_t k = 0; k < q->K; ++k) present += q->active[k] ? 1 : 0;
+    out->active_devices = present;
+    out->policy = q->policy;
     return FO_OK;
 }
 
 extern "C" fo_status fo_queues_counters(const fo_queues* q, int64_t* c_out, int32_t K) {
     FO_CHECK(q != nullptr && c_out != nullptr, "fo_queues_counters: NULL argument");
+    std::lock_guard<std::mutex> lk(q->mu);
     FO_CHECK(K >= 0 && K <= q->K, "fo_queues_counters: K=%d out of range", K);
     for (int32_t k = 0; k < K; ++k) c_out[k] = q->c[k];
     return FO_OK;
@@ -541,6 +618,7 @@ extern "C" int32_t fo_queues_add_device(fo_queues* q) {
         fo::set_error("fo_queues_add_device: NULL handle");
         return -1;
     }
+    std::lock_guard<std::mutex> lk(q->mu);
     if (q->n_slots - (q->K + 1) < 1) {
         fo::set_error("fo_queues_add_device: pool of %lld slots cannot take another device", (long long)q->n_slots);
         return -1;
@@ -550,13 +628,75 @@ extern "C" int32_t fo_queues_add_device(fo_queues* q) {
         q->c.push_back(0);
         q->next_seq.push_back(0);
         q->sender_on.push_back(1);
+        q->active.push_back(1);
     } catch (...) {
         fo::set_error("fo_queues_add_device: out of host memory");
         return -1;
     }
     q->K++;
     q->omega = q->n_slots - q->K;
+    q->log_ev(FO_EV_JOIN, q->K - 1, 1, 0);
     return q->K - 1;
+}
+
+extern "C" fo_status fo_queues_set_policy(fo_queues* q, int32_t policy) {
+    FO_CHECK(q != nullptr, "fo_queues_set_policy: NULL handle");
+    FO_CHECK(policy == FO_SCHED_COUNTER || policy == FO_SCHED_FIFO, "fo_queues_set_policy: unknown policy %d",
+             policy);
+    std::lock_guard<std::mutex> lk(q->mu);
+    q->policy = policy;
+    return FO_OK;
+}
+
+extern "C" fo_status fo_queues_set_device_active(fo_queues* q, int32_t k, int32_t active) {
+    FO_CHECK(q != nullptr, "fo_queues_set_device_active: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
+    FO_CHECK(k >= 0 && k < q->K, "fo_queues_set_device_active: device %d out of range [0,%d)", k, q->K);
+    const uint8_t a = active ? 1 : 0;
+    if (q->active[k] == a) return FO_OK;
+    q->active[k] = a;
+    q->sender_on[k] = a;  // leaving: off and kept off; rejoining: on, as for a new device
+    q->log_ev(a ? FO_EV_JOIN : FO_EV_LEAVE, k, 0, 0);
+    return FO_OK;
+}
+
+extern "C" int32_t fo_queues_sender_status(fo_queues* q, int32_t k) {
+    if (!q) {
+        fo::set_error("fo_queues_sender_status: NULL handle");
+        return -1;
+    }
+    std::lock_guard<std::mutex> lk(q->mu);
+    if (k < 0 || k >= q->K) {
+        fo::set_error("fo_queues_sender_status: device %d out of range [0,%d)", k, q->K);
+        return -1;
+    }
+    return q->sender_on[k];
+}
+
+extern "C" fo_status fo_queues_log_enable(fo_queues* q, int64_t max_events) {
+    FO_CHECK(q != nullptr, "fo_queues_log_enable: NULL handle");
+    FO_CHECK(max_events >= 0, "fo_queues_log_enable: max_events=%lld", (long long)max_events);
+    std::lock_guard<std::mutex> lk(q->mu);
+    std::vector<int64_t> fresh;
+    try {
+        fresh.reserve((size_t)(4 * max_events));
+    } catch (...) {
+        set_error("fo_queues_log_enable: %lld events do not fit in host memory", (long long)max_events);
+        return FO_ENOMEM;
+    }
+    q->log.swap(fresh);
+    q->log_cap = max_events;
+    return FO_OK;
+}
+
+extern "C" fo_status fo_queues_log_read(fo_queues* q, int64_t* out, int64_t max_events, int64_t* n_out) {
+    FO_CHECK(q != nullptr && n_out != nullptr, "fo_queues_log_read: NULL argument");
+    FO_CHECK(max_events >= 0 && (max_events == 0 || out != nullptr), "fo_queues_log_read: bad buffer");
+    std::lock_guard<std::mutex> lk(q->mu);
+    const int64_t n = std::min<int64_t>((int64_t)q->log.size() / 4, max_events);
+    for (int64_t i = 0; i < 4 * n; ++i) out[i] = q->log[i];
+    *n_out = (int64_t)q->log.size() / 4;
+    return FO_OK;
 }
 
 extern "C" fo_status fo_set_max_delay(int64_t max_delay) {

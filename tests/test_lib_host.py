@@ -12,6 +12,7 @@ import pytest
 import fo_synth as S
 from oracle.scheduler import TaskScheduler
 from tests.golden_io import fmt_get, read_trace
+from tests.pool_log import replay
 
 A = pytest.importorskip("paper_2504_13850_amd.api")
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -42,8 +43,10 @@ def test_param_counts_and_classes():
     assert A.fo_config_param_count(9) == -1
 
 
-def _lib_trace(name, K, n_slots, with_slot):
+def _lib_trace(name, K, n_slots, with_slot, policy=None):
     q = A.fo_queues_create(K, 0, 1, False, n_slots if n_slots else 1 << 16)
+    if policy is not None:
+        A.fo_queues_set_policy(q, policy)
     try:
         for op, args, exp in read_trace(name):
             if op == "put_act":
@@ -72,6 +75,9 @@ def _lib_trace(name, K, n_slots, with_slot):
             elif op == "release":
                 A.fo_queues_release(q)
                 got = "-"
+            elif op in ("leave", "join"):
+                A.fo_queues_set_device_active(q, args[0], op == "join")
+                got = "-"
             if op == "put_act" and got == "admit":
                 assert exp.startswith("admit"), (op, args, exp)
             else:
@@ -98,6 +104,12 @@ def test_golden_scheduler_trace_through_c_abi():
 def test_golden_flow_trace_through_c_abi():
     st = _lib_trace("flow_trace_k2.txt", 2, 4, True)
     assert st.refused == 3 and st.picks == 5
+
+
+def test_golden_fifo_leave_trace_through_c_abi():
+    st = _lib_trace("fifo_leave_trace_k3.txt", 3, 5, True, policy=A.FO_SCHED_FIFO)
+    assert st.refused == 2 and st.turn_on_signals == 5 and st.policy == A.FO_SCHED_FIFO
+    assert st.active_devices == 3
 
 
 def _random_trace(K, n_slots, steps, seed, rates=None, models=False, D=None):
@@ -334,3 +346,80 @@ def test_batched_pushes_equal_single_pushes():
     finally:
         A.fo_queues_destroy(q1)
         A.fo_queues_destroy(q2)
+
+
+@pytest.mark.parametrize("policy", ["counter", "fifo"])
+def test_random_leave_rejoin_trace_and_event_record(policy):
+    """Library and oracle driven with the same events (arrivals, models,
+    devices leaving and rejoining at random) agree on every observable, the
+    Sender Status included; the library's event record then replays through
+    a fresh oracle event by event."""
+    K, n_slots, D = 6, 16, 2
+    rng = np.random.default_rng(21 if policy == "counter" else 22)
+    sch = TaskScheduler(K, n_slots, policy=policy)
+    q = A.fo_queues_create(K, 0, 1, False, n_slots)
+    A.fo_queues_set_policy(q, A.FO_SCHED_COUNTER if policy == "counter" else A.FO_SCHED_FIFO)
+    A.fo_queues_log_enable(q, 100000)
+    A.fo_set_max_delay(D)
+    version = [0] * K
+    try:
+        for step in range(400):
+            for k in range(K):
+                if rng.random() < 0.04:
+                    on = not sch.active[k]
+                    sch.set_active(k, on)
+                    A.fo_queues_set_device_active(q, k, on)
+            for k in range(K):
+                assert A.fo_queues_sender_status(q, k) == int(sch.sender_on[k])
+                for _ in range(rng.poisson(0.9)):
+                    ok, _, _ = sch.put_act(k)
+                    assert (A.fo_queues_push(q, k) == A.FO_OK) == ok
+                if rng.random() < 0.05:
+                    sch.put_model(k, version[k])
+                    A.fo_queues_push_model(q, k, None, version[k])
+            while True:
+                k = A.fo_pick_device(q)
+                if k != -2:
+                    break
+                r = sch.get()
+                ok, s = sch.aggregate_version(r[2], D)
+                st, kk, ss = A.fo_aggregate_pending(q, _Empty(), 1.0)
+                assert (kk, ss, st) == (r[1], s, A.FO_OK if ok else A.FO_SKIPPED)
+                version[kk] = sch.t
+            r = sch.get()
+            if r is None:
+                assert k == -1
+                continue
+            assert k == r[1]
+            sch.release()
+            A.fo_queues_release(q)
+        st = A.fo_queues_stats(q)
+        assert A.fo_queues_counters(q, K) == sch.c
+        assert (st.refused, st.turn_on_signals, st.version) == (sch.refused, sch.turn_on_signals, sch.t)
+        assert st.active_devices == sum(sch.active)
+        log = A.fo_queues_log_read(q, 100000)
+        assert len(log) > 1000
+        sch2, picks, aggs = replay(log, K, n_slots, policy, D)
+        assert sch2.c == sch.c and sch2.t == sch.t and sch2.refused == sch.refused
+        assert len(picks) == st.picks and any(not a[3] for a in aggs)
+    finally:
+        A.fo_queues_destroy(q)
+        A.fo_set_max_delay(-1)
+
+
+def test_event_record_is_bounded_and_policy_checked():
+    q = A.fo_queues_create(2, 0, 1, False, 10)
+    try:
+        A.fo_queues_log_enable(q, 3)
+        for _ in range(3):
+            A.fo_queues_push(q, 0)
+            A.fo_queues_push(q, 1)
+        assert len(A.fo_queues_log_read(q, 100)) == 3
+        with pytest.raises(A.FoError):
+            A.fo_queues_set_policy(q, 7)
+        with pytest.raises(A.FoError):
+            A.fo_queues_set_device_active(q, 2, False)
+        with pytest.raises(A.FoError):
+            A.fo_queues_sender_status(q, -1)
+    finally:
+        A.fo_queues_destroy(q)
