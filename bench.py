@@ -47,6 +47,11 @@ def parse():
                     "transformer (default); 5: 128-device VGG with Poisson arrivals; 6: the device-side "
                     "iteration of the VGG split")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="the concurrent pipeline (Receiver and Compute Engine threads) on the 128-device VGG "
+                         "workload: throughput T(p), retention R(p) = T(p)/T(0) and server idle time under "
+                         "device dropout p")
+    ap.add_argument("--pipeline-seconds", type=float, default=3.0, help="wall-clock seconds per pipeline run")
     ap.add_argument("--cpu-sample-steps", type=int, default=3,
                     help="fp32 oracle steps at the workload's own batch timed for cpu_baseline")
     ap.add_argument("--calib-copy", action="store_true",
@@ -476,6 +481,77 @@ def bench_vgg128(args, A, torch, S):
     print(json.dumps(out), flush=True)
 
 
+def bench_pipeline(args, A, torch, S):
+    """The concurrent pipeline (fo_pipeline_run) on the 128-device VGG-16 split
+    workload: config 5's server model, 64 GiB pool, bank of activation batches
+    and 38,720-parameter device models.  Device k's local iteration takes
+    step_ms / lambda_k (lambda_k ~ LogNormal(0,1) arrivals per server step, as in
+    the step loop: server-bound), or, in the balanced regime, periods scaled so
+    that all devices together send one batch per server step time.  Each run
+    lasts --pipeline-seconds; dropout draws every 0.25 s, slow-down factors
+    U[1, 2]; a model message every local iteration (H = 1), alpha 1."""
+    cid = 5
+    cfg = S.get_config(cid)
+    K, B = cfg.n_devices, cfg.batch
+    stream = torch.cuda.current_stream()
+    pool_stream = torch.cuda.Stream()
+    bank_n = cfg.extra["bank"]
+    acts_d = torch.from_numpy(S.make_acts(cid, bank_n).view(np.int16)).cuda()
+    labels_d = torch.from_numpy(S.make_labels(cid, bank_n)).cuda()
+    locs = torch.from_numpy(S.make_local_vectors(cid, K)).cuda()
+    slot_bytes = int(acts_d[0].numel()) * 2
+    n_slots = cfg.extra["pool_bytes"] // slot_bytes
+    rates = S.make_arrival_rates(cid)
+    A.fo_set_max_delay(-1)
+    # the server step alone, for the device periods
+    model = A.fo_model_create(cid, B, S.init_params(cid), stream)
+    for _ in range(3):
+        A.fo_server_step(model, (acts_d[0], None, B), labels_d[0], 0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(20):
+        A.fo_server_step(model, (acts_d[0], None, B), labels_d[0], 0)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    step_s = e0.elapsed_time(e1) / 20 * 1e-3
+    A.fo_model_destroy(model)
+    regimes = {"workload rates (server-bound)": step_s / rates,
+               "balanced": step_s / rates * float(rates.sum())}
+    runs = []
+    for regime, periods in regimes.items():
+        T0 = None
+        for p in (0.0, 0.25, 0.5):
+            model = A.fo_model_create(cid, B, S.init_params(cid), stream)
+            q = A.fo_queues_create(K, slot_bytes, B, False, n_slots, pool_stream)
+            glob = torch.from_numpy(S.make_global_vector(cid)).cuda()
+            try:
+                st = A.fo_pipeline_run(q, model, glob, dict(
+                    seconds=args.pipeline_seconds, iter_seconds=periods, H=1, p_drop=p, interval_seconds=0.25,
+                    slow_max=2.0, seed=17, bank_x=acts_d, bank_labels=labels_d, bank_n=bank_n, local_bank=locs,
+                    n_local=K, alpha=1.0, max_inflight=2))
+            finally:
+                A.fo_queues_destroy(q)
+                A.fo_model_destroy(model)
+            T = st.samples / st.wall_seconds
+            T0 = T if p == 0.0 else T0
+            runs.append({"regime": regime, "p": p, "T_samples_per_s": round(T, 1), "R": round(T / T0, 3),
+                         "server_idle_fraction": round(st.idle_seconds / st.wall_seconds, 4),
+                         "steps": st.steps, "sent": st.sent, "not_sent": st.not_sent,
+                         "aggregations": st.aggregations, "leaves": st.leaves, "rejoins": st.rejoins,
+                         "wall_s": round(st.wall_seconds, 3)})
+            print(json.dumps(runs[-1]), flush=True)
+    print(json.dumps({"metric": "concurrent pipeline: server train samples/s T(p) and retention R(p) under "
+                                "device dropout p (Sec. 6.4)",
+                      "unit": "samples/s", "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                      "step_only_ms": round(step_s * 1e3, 4),
+                      "config": {"workload": "vgg16 split server step, batch 64 of [64,16,16] bf16 activations, "
+                                             "128 emulated devices, 64 GiB activation pool, counter-based "
+                                             "scheduler, dropout draws every 0.25 s, slow-down U[1,2]",
+                                 "parallelism": "single-gpu"},
+                      "runs": runs}), flush=True)
+
+
 def device_flops_per_sample():
     """Useful FLOPs of one device-side training iteration per sample (config 6):
     forward of conv1 (3->64 at 32x32), conv2 (64->64 at 32x32), the auxiliary
@@ -559,6 +635,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cid = args.config
+    if args.pipeline:
+        bench_pipeline(args, A, torch, S)
+        return
     if cid == 6:
         args.steps = 30 if args.steps is None else args.steps
         args.warmup = 5 if args.warmup is None else args.warmup

@@ -385,10 +385,11 @@ FO_API fo_status fo_queues_log_read(fo_queues* q, int64_t* out, int64_t max_even
  * interval with probability p_drop (fo_queues_set_device_active), and a
  * present device draws s from U[1, slow_max]; the draws come from splitmix64
  * of (seed, interval, device), so they do not depend on thread timing.
- * Compute Engine thread (the server, Alg. 3 and Alg. 4): a pending model is
- * aggregated with weight alpha / (staleness + 1) (or skipped past the maximum
- * delay) on the pool's stream, and its device then holds the current global
- * version; otherwise the pick is trained on with fo_server_step on the model's
+ * Compute Engine thread (the server, Alg. 3 and Alg. 4): pending models are
+ * aggregated with weights alpha / (staleness + 1) (or skipped past the maximum
+ * delay), all that are pending in fused launches on the pool's stream as
+ * fo_aggregate_pending_all does, and each of their devices then holds the
+ * current global version; otherwise the pick is trained on with fo_server_step on the model's
  * stream, at most max_inflight steps ahead of the GPU.  With nothing queued
  * the engine first waits for its steps to finish and then sleeps until a
  * device puts something: that sleep is the server's idle time.

@@ -14,9 +14,10 @@
 // every interval each device is away for that interval with probability
 // p_drop and, if present, draws its slow-down factor from U[1, slow_max].
 //
-// Compute Engine thread: get() from the Task Scheduler; a model is
-// aggregated (or skipped past the maximum delay) on the pool's stream and
-// the device is told the global version it now holds; an activation batch is
+// Compute Engine thread: get() from the Task Scheduler; pending models are
+// aggregated (or skipped past the maximum delay), all of them in fused
+// launches on the pool's stream, and each device is told the global version it
+// now holds; an activation batch is
 // trained on with fo_server_step on the model's stream, at most max_inflight
 // steps ahead of the GPU; with nothing queued the engine first waits for its
 // GPU work, then sleeps until a device puts something, and that sleep is the
@@ -190,6 +191,13 @@ void engine(fo_queues* q, fo_model* m, fo_vec* global, const fo_pipeline_config&
             Shared& sh, fo_pipeline_stats& st, std::vector<hipEvent_t>& ring) {
     size_t head = 0, inflight = 0;  // ring[head] is the oldest step still in flight
     hipEvent_t last = nullptr;
+    std::vector<int32_t> drained;
+    try {
+        drained.reserve(4096);
+    } catch (...) {
+        set_error("out of host memory");
+        return sh.fail(FO_ENOMEM, "fo_pipeline_run");
+    }
     for (;;) {
         int64_t seen;
         {
@@ -199,25 +207,21 @@ void engine(fo_queues* q, fo_model* m, fo_vec* global, const fo_pipeline_config&
         }
         if (Clock::now() >= end) break;
         const int32_t k = fo_pick_device(q);
-        if (k == -2) {  // a model first (Alg. 3)
-            int32_t kk = -1;
-            int64_t s = 0;
-            fo_status r = fo_aggregate_pending(q, global, c.alpha, &kk, &s);
-            if (r == FO_OK) {
-                st.aggregations++;
-            } else if (r == FO_SKIPPED) {
-                st.skipped++;
-            } else {
-                return sh.fail(r, "fo_pipeline_run (aggregation)");
-            }
-            fo_queue_stats qs;
-            r = fo_queues_stats(q, &qs);
-            if (r != FO_OK) return sh.fail(r, "fo_pipeline_run (stats)");
+        if (k == -2) {  // models first (Alg. 3), every pending one in fused launches
+            int32_t applied = 0, skipped = 0;
+            int64_t version = 0;
+            drained.clear();
+            fo_status r = fo::pool_drain_models(q, global, c.alpha, &applied, &skipped, &drained, &version);
+            if (r != FO_OK) return sh.fail(r, "fo_pipeline_run (aggregation)");
+            st.aggregations += applied;
+            st.skipped += skipped;
             {
                 std::lock_guard<std::mutex> lk(sh.mu);
-                sh.version[kk] = qs.version;  // the device now holds the current global model
-                sh.awaiting[kk] = 0;
-                sh.replied[kk] = 1;
+                for (int32_t kk : drained) {  // each device now holds the current global model
+                    sh.version[kk] = version;
+                    sh.awaiting[kk] = 0;
+                    sh.replied[kk] = 1;
+                }
             }
             sh.cv.notify_all();
             continue;

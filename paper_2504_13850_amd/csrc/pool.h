@@ -1,6 +1,8 @@
 // What the training step needs to know about the activation pools.
 #pragma once
 
+#include <vector>
+
 #include "common.h"
 
 namespace fo {
@@ -21,5 +23,10 @@ fo_status pool_step_done(fo_queues* q, hipStream_t step_stream);
 // Slot size, batch and whether slots hold lengths; the pool's stream.
 void pool_geometry(const fo_queues* q, int64_t* slot_bytes, int32_t* batch, int32_t* with_lengths);
 hipStream_t pool_stream(const fo_queues* q);
+
+// fo_aggregate_pending_all that also reports, atomically with the drain, the
+// device of every message drained (in FIFO order) and the global version after it.
+fo_status pool_drain_models(fo_queues* q, fo_vec* global, float alpha, int32_t* applied, int32_t* skipped,
+                            std::vector<int32_t>* devices, int64_t* version);
 
 }  // namespace fo

@@ -513,10 +513,12 @@ extern "C" fo_status fo_aggregate_pending(fo_queues* q, fo_vec* global, float al
     return FO_OK;
 }
 
-extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, float alpha, int32_t* applied_out,
-                                              int32_t* skipped_out) {
-    FO_CHECK(q != nullptr, "fo_aggregate_pending_all: NULL handle");
-    std::lock_guard<std::mutex> lk(q->mu);
+namespace {
+
+// The fused drain of every pending model message, under the pool's lock;
+// devices (if given) receives the device of every message drained, in order.
+fo_status drain_models(fo_queues* q, fo_vec* global, float alpha, int32_t* applied_out, int32_t* skipped_out,
+                       std::vector<int32_t>* devices) {
     fo_status st = check_global(global, "fo_aggregate_pending_all");
     if (st != FO_OK) return st;
     FO_CHECK(alpha >= 0.f && alpha <= 1.f, "fo_aggregate_pending_all: alpha=%g outside [0,1]", (double)alpha);
@@ -560,6 +562,14 @@ extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, floa
             tab.count++;
             t_next++;
         }
+        if (devices) {  // room for this group's devices before anything is launched
+            try {
+                devices->reserve(devices->size() + used);
+            } catch (...) {
+                set_error("fo_aggregate_pending_all: out of host memory");
+                return FO_ENOMEM;
+            }
+        }
         if (tab.count > 0) {
             st = fo::launch_agg_lerp_multi(global->ptr, tab, global->n, q->stream);
             if (st != FO_OK) return st;
@@ -573,6 +583,8 @@ extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, floa
                 if (!skip) tl++;
             }
         }
+        if (devices)
+            for (size_t i = 0; i < used; ++i) devices->push_back(q->qm[i].k);
         q->qm.erase(q->qm.begin(), q->qm.begin() + used);
         q->t = t_next;
         applied += tab.count;
@@ -582,6 +594,25 @@ extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, floa
     }
     return FO_OK;
 }
+
+}  // namespace
+
+extern "C" fo_status fo_aggregate_pending_all(fo_queues* q, fo_vec* global, float alpha, int32_t* applied_out,
+                                              int32_t* skipped_out) {
+    FO_CHECK(q != nullptr, "fo_aggregate_pending_all: NULL handle");
+    std::lock_guard<std::mutex> lk(q->mu);
+    return drain_models(q, global, alpha, applied_out, skipped_out, nullptr);
+}
+
+namespace fo {
+fo_status pool_drain_models(fo_queues* q, fo_vec* global, float alpha, int32_t* applied, int32_t* skipped,
+                            std::vector<int32_t>* devices, int64_t* version) {
+    std::lock_guard<std::mutex> lk(q->mu);
+    fo_status st = drain_models(q, global, alpha, applied, skipped, devices);
+    *version = q->t;
+    return st;
+}
+}  // namespace fo
 
 extern "C" fo_status fo_queues_stats(const fo_queues* q, fo_queue_stats* out) {
     FO_CHECK(q != nullptr && out != nullptr, "fo_queues_stats: NULL argument");
