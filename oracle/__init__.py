@@ -9,7 +9,9 @@ unoptimised NumPy implementation of what the server computes:
   output activations, auxiliary network, local loss f_d, backward, SGD),
 * the staleness-weighted asynchronous aggregation of Algorithm 4,
 * the Task Scheduler of Algorithms 2 and 3 together with the activation
-  flow control of Sec. 3.4.1.
+  flow control of Sec. 3.4.1,
+* the pre-processor of the initialization stage: layer profiles, the
+  split-point rule of Eq. 6-8 and the default auxiliary network (Sec. 3.2).
 
 It is used by the tests, by the smoke check and by the benchmark's CPU
 baseline leg only; the product library never imports, links or calls it,
@@ -21,7 +23,7 @@ Parity status: every function here is pinned by the ``-m "not gpu"`` tests
 (finite differences, closed forms, invariants, brute force and an
 independent autograd library on tiny inputs).  No function is unpinned.
 """
-from . import layers, nets, aggregate, scheduler  # noqa: F401
+from . import layers, nets, aggregate, scheduler, preproc  # noqa: F401
 from .nets import server_step, server_forward, device_step, param_layout, sgd_update  # noqa: F401
 from .aggregate import mix, mix_sequence  # noqa: F401
 from .scheduler import TaskScheduler  # noqa: F401
