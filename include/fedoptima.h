@@ -437,6 +437,70 @@ typedef struct {
 FO_API fo_status fo_pipeline_run(fo_queues* q, fo_model* m, fo_vec* global, const fo_pipeline_config* cfg,
                                  fo_pipeline_stats* out);
 
+/* ------------------------------------------------------------------ pre-processor
+ * The initialization stage's Pre-processor (Sec. 3.2.1; auxiliary network of
+ * Sec. 3.2.2).  Host code, no GPU work.
+ *
+ * A network is a table of units the split may follow: a convolution (with its
+ * normalisation and activation), a pooling layer, a fully connected layer, a
+ * MobileNetV3 bottleneck block (expansion, depthwise, optional
+ * squeeze-excitation, projection), an embedding, a transformer encoder layer.
+ * Blocks are never cut: the paper splits only at sequential connections.
+ * Per unit and sample, fwd_flops counts 2 per multiply-add of its
+ * convolutions and matrix products (normalisation, activations, pooling and
+ * softmax not counted) and out_elems its output values. */
+enum { FO_UNIT_CONV = 1, FO_UNIT_POOL = 2, FO_UNIT_FC = 3, FO_UNIT_BNECK = 4, FO_UNIT_EMB = 6, FO_UNIT_ENC = 7 };
+typedef struct {
+    int32_t kind;               /* FO_UNIT_* */
+    int32_t k, stride;          /* kernel side and stride (0, 1 for a global pool) */
+    int32_t c_in, c_out;        /* channels, features, or model width */
+    int32_t h_out, w_out;       /* output rows and columns; sequence units: length, 1 */
+    int32_t expand;             /* bottleneck expansion width */
+    int32_t heads, hidden;      /* encoder heads and FFN width */
+    int32_t norm, se;           /* has normalisation; has squeeze-excitation */
+    int64_t params;             /* trainable parameters */
+    double fwd_flops;           /* forward FLOPs of one sample */
+    double out_elems;           /* output values of one sample */
+} fo_unit;
+
+/* The unit tables of the paper's networks (Table 4) and of VGG-16:
+ *   FO_NET_VGG5              conv3-32, pool, conv3-64, pool, conv3-64, pool, fc-128, fc-classes
+ *                            (bias and batch norm per convolution); in_hw = image side, % 8 == 0
+ *   FO_NET_MOBILENETV3_LARGE conv3-16 stride 2, the 15 bottlenecks, conv1-960, global pool,
+ *                            fc-1280, fc-classes; in_hw = image side
+ *   FO_NET_TRANSFORMER6/12   EMB-100, 6 encoders (d 100, 5 heads, FFN 100) or 12 (50 heads),
+ *                            fc-classes; in_hw = sequence length (the embedding table, whose
+ *                            size the paper does not give, counts no parameters)
+ *   FO_NET_VGG16             thirteen conv3 (bias) with five pools, fc 512-512-classes;
+ *                            in_hw = image side, % 32 == 0
+ * Writes min(count, max_units) units to out and returns the count, or -1
+ * (unknown network, bad sizes; message in fo_last_error). */
+enum { FO_NET_VGG5 = 1, FO_NET_MOBILENETV3_LARGE = 2, FO_NET_TRANSFORMER6 = 3, FO_NET_TRANSFORMER12 = 4,
+       FO_NET_VGG16 = 5 };
+FO_API int32_t fo_net_units(int32_t net, int32_t classes, int32_t in_hw, fo_unit* out, int32_t max_units);
+
+/* Split-point selection (Eq. 6-8): for every split l = 1..L (M_d = units
+ * 1..l), cost(l) = max over devices k of max(sum_{i<=l} O_i / o_k, S_l / b_k),
+ * with O_i = 3 x fwd_flops x batch (forward, input- and weight-gradient
+ * products of one iteration) and S_l = out_elems x batch x bytes_per_value;
+ * *split_out = the l of least cost (the smallest on ties).  flops_per_s[k]
+ * (o_k) and bytes_per_s[k] (b_k) are device k's compute rate and bandwidth,
+ * host arrays of K > 0 values.  cost_out (host [L], may be NULL) receives
+ * every cost.  Errors: FO_EINVAL. */
+FO_API fo_status fo_select_split(const fo_unit* units, int32_t L, int32_t batch, int32_t bytes_per_value,
+                                 int32_t K, const double* flops_per_s, const double* bytes_per_s,
+                                 double* cost_out, int32_t* split_out);
+
+/* The default auxiliary network (Sec. 3.2.2) for the split after unit
+ * `split` (1-based): one unit of the same kind as the last unit of M_d that
+ * has parameters (pools skipped), as wide as M_d's output, stride 1, then the
+ * classifier: global average pool and fc-classes after a convolution or a
+ * bottleneck, fc-classes on the first token after an encoder, fc-classes
+ * after a fully connected unit; after an embedding, the classifier alone.
+ * Writes min(count, max_units) units and returns the count, or -1. */
+FO_API int32_t fo_aux_network(const fo_unit* units, int32_t L, int32_t split, int32_t classes, fo_unit* out,
+                              int32_t max_units);
+
 /* ------------------------------------------------------------------ instrumentation
  * Kernel timing for benchmarks and tuning.  While enabled on a thread, every
  * MFMA GEMM and attention launch that thread enqueues is bracketed by two HIP

@@ -29,7 +29,9 @@ EXPORTS = [
     "fo_set_graph_mode", "fo_gemm_bf16", "fo_conv2d_bf16", "fo_gemm_bf16_noalloc", "fo_queues_push_batch",
     "fo_queues_push_model_batch", "fo_device_step", "fo_queues_set_policy", "fo_queues_set_device_active",
     "fo_queues_sender_status", "fo_queues_log_enable", "fo_queues_log_read", "fo_pipeline_run",
+    "fo_net_units", "fo_select_split", "fo_aux_network",
 ]
+FO_NET_VGG5, FO_NET_MOBILENETV3_LARGE, FO_NET_TRANSFORMER6, FO_NET_TRANSFORMER12, FO_NET_VGG16 = range(1, 6)
 FO_SCHED_COUNTER, FO_SCHED_FIFO = 0, 1
 FO_EV_PUSH, FO_EV_MODEL, FO_EV_PICK, FO_EV_RELEASE, FO_EV_AGG, FO_EV_LEAVE, FO_EV_JOIN = range(1, 8)
 FO_LAYOUT_ROW_K, FO_LAYOUT_K_ROW = 0, 1
@@ -60,6 +62,16 @@ class fo_queue_stats(C.Structure):
                 ("refused", C.c_int64), ("picks", C.c_int64), ("peak_queued", C.c_int64),
                 ("version", C.c_int64), ("turn_on_signals", C.c_int64), ("active_devices", C.c_int32),
                 ("policy", C.c_int32)]
+
+
+class fo_unit(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("k", C.c_int32), ("stride", C.c_int32), ("c_in", C.c_int32),
+                ("c_out", C.c_int32), ("h_out", C.c_int32), ("w_out", C.c_int32), ("expand", C.c_int32),
+                ("heads", C.c_int32), ("hidden", C.c_int32), ("norm", C.c_int32), ("se", C.c_int32),
+                ("params", C.c_int64), ("fwd_flops", C.c_double), ("out_elems", C.c_double)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
 
 
 class fo_pipeline_config(C.Structure):
@@ -126,6 +138,9 @@ def lib():
             "fo_queues_sender_status": (i32, [vp, i32]),
             "fo_queues_log_enable": (C.c_int, [vp, i64]),
             "fo_queues_log_read": (C.c_int, [vp, vp, i64, C.POINTER(i64)]),
+            "fo_net_units": (i32, [i32, i32, i32, C.POINTER(fo_unit), i32]),
+            "fo_select_split": (C.c_int, [C.POINTER(fo_unit), i32, i32, i32, i32, vp, vp, vp, C.POINTER(i32)]),
+            "fo_aux_network": (i32, [C.POINTER(fo_unit), i32, i32, i32, C.POINTER(fo_unit), i32]),
             "fo_pipeline_run": (C.c_int, [vp, vp, C.POINTER(fo_vec), C.POINTER(fo_pipeline_config),
                                           C.POINTER(fo_pipeline_stats)]),
             "fo_last_error": (C.c_char_p, []),
@@ -398,6 +413,37 @@ def fo_pipeline_run(q, model, global_vec, cfg: dict) -> fo_pipeline_stats:
     st = fo_pipeline_stats()
     _check(lib().fo_pipeline_run(q, model, C.byref(g), C.byref(c), C.byref(st)))
     return st
+
+
+# ------------------------------------------------------------------ pre-processor
+def fo_net_units(net: int, classes: int, in_hw: int):
+    """The unit table of a network, as a ctypes array of fo_unit."""
+    n = lib().fo_net_units(net, classes, in_hw, None, 0)
+    if n < 0:
+        raise FoError(FO_EINVAL, last_error())
+    arr = (fo_unit * n)()
+    lib().fo_net_units(net, classes, in_hw, arr, n)
+    return arr
+
+
+def fo_select_split(units, batch: int, bytes_per_value: int, flops_per_s, bytes_per_s):
+    """Returns (split l, per-split costs)."""
+    o = np.ascontiguousarray(flops_per_s, np.float64)
+    b = np.ascontiguousarray(bytes_per_s, np.float64)
+    costs = np.zeros(len(units), np.float64)
+    l = C.c_int32()
+    _check(lib().fo_select_split(units, len(units), batch, bytes_per_value, len(o), o.ctypes.data, b.ctypes.data,
+                                 costs.ctypes.data, C.byref(l)))
+    return l.value, costs
+
+
+def fo_aux_network(units, split: int, classes: int):
+    n = lib().fo_aux_network(units, len(units), split, classes, None, 0)
+    if n < 0:
+        raise FoError(FO_EINVAL, last_error())
+    arr = (fo_unit * n)()
+    lib().fo_aux_network(units, len(units), split, classes, arr, n)
+    return arr
 
 
 # ------------------------------------------------------------------ instrumentation
