@@ -59,6 +59,8 @@ def parse():
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench with "
                          "--calib-copy into the HBM traffic summary (JSON on stdout)")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_STATS_CSV",
+                    help="print the per-kernel table of a rocprofv3 --kernel-trace --stats summary and exit")
     ap.add_argument("--summarize-counters", nargs="+", metavar="CSV",
                     help="turn rocprofv3 --pmc runs of this bench (MFMA and L2 counters, any number of "
                          "passes) into a per-kernel table (Markdown on stdout)")
@@ -103,7 +105,7 @@ TRAFFIC_KERNELS = {
     # compensated forward products, input gradients, weight gradients of the transformer step
     "gemm_comp_dma_kernel<3>": ("gemm_comp_dma_kernel<3, 2, fo::(anonymous namespace)::DmaRKc>", GEMM_SOURCES),
     "gemm_kernel<0, 6>": ("gemm_kernel<0, 6, true>", GEMM_SOURCES),
-    "gemm_kernel<6, 6>": ("gemm_kernel<6, 6, true>", GEMM_SOURCES),
+    "gemm_group_kernel<6, 6>": ("gemm_group_kernel<6, 6, true>", GEMM_SOURCES),
     "agg_lerp_kernel": ("agg_lerp_kernel(", ["paper_2504_13850_amd/csrc/k_update.hip"]),
 }
 CALIB_BYTES = 1 << 30
@@ -166,6 +168,25 @@ def summarize_pmc(fetch_csv, write_csv):
                       "bytes_per_launch": round(rd + wr), "source_sha256": source_hash(files)}
     out["kernels"] = kern
     return out
+
+
+def summarize_trace(path, top=25):
+    """Markdown table of a rocprofv3 kernel_stats.csv: calls, average and total
+    time and share per kernel (names shortened)."""
+    import csv
+    rows = []
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            name = r["Name"].replace("void ", "").replace("fo::(anonymous namespace)::", "fo::")
+            name = name.split("(fo::")[0].split("(unsigned")[0].split("(float")[0].split("(int")[0]
+            name = name.split("(__hip")[0].split("(const")[0].split("(long")[0]
+            rows.append((float(r["TotalDurationNs"]), name, int(r["Calls"]), float(r["AverageNs"]),
+                         float(r["Percentage"])))
+    rows.sort(key=lambda t: -t[0])
+    out = ["| kernel | calls | avg us | total ms | share % |", "|---|---:|---:|---:|---:|"]
+    for tot, name, calls, avg, pct in rows[:top]:
+        out.append(f"| `{name[:90]}` | {calls} | {avg / 1e3:.1f} | {tot / 1e6:.2f} | {pct:.2f} |")
+    return "\n".join(out)
 
 
 def summarize_counters(paths, top=12):
@@ -621,6 +642,9 @@ def main():
     args = parse()
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc), indent=1))
+        return
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
         return
     if args.summarize_counters:
         print(summarize_counters(args.summarize_counters))
