@@ -1,4 +1,4 @@
-"""Workload descriptions for the five server-side configurations.
+"""Workload descriptions for the server-side configurations (and the device side of one).
 
 Each configuration is a split of a network between devices and the server:
 the devices send the activations of their last layer, and the server trains
@@ -24,7 +24,8 @@ from typing import List, Tuple
 class ConfigSpec:
     cid: int
     name: str
-    family: str              # "cnn" (C1), "vgg" (C2, C5), "resnet" (C3), "bert" (C4), "vgg_device" (6)
+    family: str              # "cnn" (C1), "vgg" (C2, C5), "resnet" (C3), "bert" (C4), "vgg_device" (6),
+                             # "tfsmall" (7, 8)
     batch: int
     in_shape: Tuple[int, ...]  # per-sample activation shape at the boundary (NCHW or [L, d])
     n_classes: int
@@ -57,6 +58,16 @@ CONFIGS = {
     # loss; its output activations are the [64,16,16] batches the server trains on.
     6: ConfigSpec(6, "vgg16-device-side", "vgg_device", 64, (3, 32, 32), 10, 16, "f32",
                   0.01, 0.0, 0, 1.0, 100, {"server_config": 2}),
+    # The paper's own transformers (Table 4), split after the embedding (the
+    # split the pre-processor chooses for them): the server trains every
+    # encoder layer (d = 100, FFN 100, ReLU, post-norm) and the classifier on the
+    # first token, in fp32.  Transformer-6 (5 heads of width 20) on SST-2-shaped
+    # batches of 64 tokens; Transformer-12 (50 heads of width 2) on IMDB-shaped
+    # batches of 256 tokens.
+    7: ConfigSpec(7, "transformer6-split-fp32", "tfsmall", 16, (64, 100), 2, 8, "f32",
+                  0.01, 0.0, 0, 1.0, 100, {"layers": 6, "heads": 5, "ffn": 100, "min_len": 4}),
+    8: ConfigSpec(8, "transformer12-split-fp32", "tfsmall", 16, (256, 100), 2, 16, "f32",
+                  0.01, 0.0, 0, 1.0, 100, {"layers": 12, "heads": 50, "ffn": 100, "min_len": 16}),
 }
 
 
@@ -123,7 +134,7 @@ def param_layout(cid: int) -> List[Entry]:
         lay += _conv("conv2", 64, 64, 3, True)
         lay += _conv("aux.conv", 64, 64, 3, True)
         lay += _linear("aux.fc", cfg.n_classes, 64)
-    elif cfg.family == "bert":
+    elif cfg.family in ("bert", "tfsmall"):
         d, f = cfg.in_shape[1], cfg.extra["ffn"]
         for li in range(cfg.extra["layers"]):
             p = f"enc{li}"
@@ -133,7 +144,8 @@ def param_layout(cid: int) -> List[Entry]:
             lay += _linear(p + ".ffn1", f, d)
             lay += _linear(p + ".ffn2", d, f)
             lay += _norm(p + ".ln2", d)
-        lay += _linear("pool", d, d)
+        if cfg.family == "bert":
+            lay += _linear("pool", d, d)
         lay += _linear("cls", cfg.n_classes, d)
     else:  # pragma: no cover
         raise ValueError(cfg.family)

@@ -57,8 +57,8 @@ def init_params(cid: int, sub: int = 0) -> np.ndarray:
 def make_acts(cid: int, n_batches: int, batch: int | None = None, sub: int = 0) -> np.ndarray:
     """Activation batches as sent by the devices.
 
-    CNN configs: ReLU(N(0,1)) in NCHW, [n, B, C, H, W].  Transformer config:
-    hidden states N(0,1), [n, B, L, d].  Device side (config 6): normalised
+    CNN configs: ReLU(N(0,1)) in NCHW, [n, B, C, H, W].  Transformer configs
+    (4, 7, 8): hidden states N(0,1), [n, B, L, d].  Device side (config 6): normalised
     32x32 RGB images N(0,1), [n, B, 3, 32, 32], standing in for CIFAR-10.
     fp32 configs return float32; bf16 configs return the uint16 bit patterns
     of the bf16-rounded values."""
@@ -66,7 +66,7 @@ def make_acts(cid: int, n_batches: int, batch: int | None = None, sub: int = 0) 
     B = cfg.batch if batch is None else batch
     rng = rng_for(cid, "acts", sub)
     x = rng.standard_normal(size=(n_batches, B) + tuple(cfg.in_shape), dtype=np.float32)
-    if cfg.family not in ("bert", "vgg_device"):
+    if cfg.family not in ("bert", "vgg_device", "tfsmall"):
         np.maximum(x, 0.0, out=x)
     if cfg.dtype == "f32":
         return x
@@ -77,7 +77,7 @@ def make_labels(cid: int, n_batches: int, batch: int | None = None, sub: int = 0
     cfg = get_config(cid)
     B = cfg.batch if batch is None else batch
     rng = rng_for(cid, "labels", sub)
-    if cfg.family == "bert":
+    if cfg.family in ("bert", "tfsmall"):
         return (rng.random(size=(n_batches, B)) < 0.5).astype(np.int32)
     return rng.integers(0, cfg.n_classes, size=(n_batches, B), dtype=np.int64).astype(np.int32)
 

@@ -1,4 +1,4 @@
-"""Server-side networks M_s of the five configurations and one training
+"""Server-side networks M_s of the server configurations and one training
 iteration of the activation branch of Algorithm 4 (forward of M_s, the loss
 f_s, the backward pass, then theta_s <- theta_s - gamma_s * grad).
 
@@ -22,9 +22,11 @@ from . import layers as Lyr
 VGG_PLAN = [128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M", 512, 512, 512, "M"]
 RESNET_STAGES = [(2, 128, 2), (3, 256, 2), (4, 512, 2)]  # (stage, channels, blocks)
 BERT = dict(d=768, heads=12, ffn=3072, layers=10, classes=2)
-FAMILY = {1: "cnn", 2: "vgg", 3: "resnet", 4: "bert", 5: "vgg", 6: "vgg_device"}
+# the paper's Transformer-6 and Transformer-12 (Table 4) after their embedding
+TFSMALL = {7: dict(d=100, heads=5, ffn=100, layers=6), 8: dict(d=100, heads=50, ffn=100, layers=12)}
+FAMILY = {1: "cnn", 2: "vgg", 3: "resnet", 4: "bert", 5: "vgg", 6: "vgg_device", 7: "tfsmall", 8: "tfsmall"}
 IN_CH = {1: 32, 2: 64, 3: 64, 5: 64, 6: 3}
-CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10, 6: 10}
+CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10, 6: 10, 7: 2, 8: 2}
 
 
 def param_layout(cid: int):
@@ -80,8 +82,9 @@ def param_layout(cid: int):
             ci = c
         lin("fc", CLASSES[cid], 512)
     else:
-        d, f = BERT["d"], BERT["ffn"]
-        for li in range(BERT["layers"]):
+        arch = BERT if fam == "bert" else TFSMALL[cid]
+        d, f = arch["d"], arch["ffn"]
+        for li in range(arch["layers"]):
             p = f"enc{li}"
             lin(p + ".qkv", 3 * d, d)
             lin(p + ".o", d, d)
@@ -89,8 +92,9 @@ def param_layout(cid: int):
             lin(p + ".ffn1", f, d)
             lin(p + ".ffn2", d, f)
             norm(p + ".ln2", d)
-        lin("pool", d, d)
-        lin("cls", BERT["classes"], d)
+        if fam == "bert":
+            lin("pool", d, d)
+        lin("cls", CLASSES[cid], d)
     return out
 
 
@@ -288,13 +292,14 @@ class ResNet(_Net):
 
 class EncoderLayer:
     """Post-LN transformer encoder layer: h = LN1(x + MHA(x));
-    y = LN2(h + W2 GELU(W1 h + b1) + b2)."""
+    y = LN2(h + W2 act(W1 h + b1) + b2), act = GELU (BERT) or ReLU (the
+    paper's own transformers, as in the original encoder)."""
 
-    def __init__(self, P, p, heads):
+    def __init__(self, P, p, heads, act="gelu"):
         self.att = Lyr.MultiHeadAttention(P[p + ".qkv.w"], P[p + ".qkv.b"], P[p + ".o.w"], P[p + ".o.b"], heads)
         self.ln1 = Lyr.LayerNorm(P[p + ".ln1.g"], P[p + ".ln1.b"])
         self.f1 = Lyr.Linear(P[p + ".ffn1.w"], P[p + ".ffn1.b"])
-        self.act = Lyr.GELU()
+        self.act = Lyr.GELU() if act == "gelu" else Lyr.ReLU()
         self.f2 = Lyr.Linear(P[p + ".ffn2.w"], P[p + ".ffn2.b"])
         self.ln2 = Lyr.LayerNorm(P[p + ".ln2.g"], P[p + ".ln2.b"])
         self.p = p
@@ -348,8 +353,37 @@ class Bert(_Net):
         self.G = G
 
 
+class SmallTransformer(_Net):
+    """The server part of Transformer-6/12 (Table 4) split after EMB-100: the
+    encoder layers (ReLU FFN) and FC-X on the first token."""
+
+    def __init__(self, P, cid):
+        a = TFSMALL[cid]
+        self.layers = [EncoderLayer(P, f"enc{i}", a["heads"], act="relu") for i in range(a["layers"])]
+        self.cls = Lyr.Linear(P["cls.w"], P["cls.b"])
+
+    def fwd(self, x, lengths):
+        h = x
+        for l in self.layers:
+            h = l.fwd(h, lengths)
+        self.hshape = h.shape
+        return self.cls.fwd(h[:, 0, :])
+
+    def bwd(self, dz):
+        G = {}
+        d0 = self.cls.bwd(dz)
+        G["cls.w"], G["cls.b"] = self.cls.dw, self.cls.db
+        dh = np.zeros(self.hshape, d0.dtype)
+        dh[:, 0, :] = d0
+        for i in range(len(self.layers) - 1, -1, -1):
+            dh = self.layers[i].bwd(dh, i > 0, G)
+        self.G = G
+
+
 def build(cid, P):
     fam = FAMILY[cid]
+    if fam == "tfsmall":
+        return SmallTransformer(P, cid)
     if fam == "cnn":
         return CNN(P)
     if fam == "vgg_device":

@@ -14,17 +14,17 @@ import oracle
 from oracle import nets
 from tests import torch_ref
 
-SMALL_B = {1: 3, 2: 2, 3: 4, 4: 2, 5: 2, 6: 2}
+SMALL_B = {1: 3, 2: 2, 3: 4, 4: 2, 5: 2, 6: 2, 7: 3, 8: 2}
 
 
 def _inputs(cid, B, sub=7):
     acts = S.make_acts(cid, 1, batch=B, sub=sub)[0]
     labels = S.make_labels(cid, 1, batch=B, sub=sub)[0]
-    lengths = S.make_lengths(cid, 1, batch=B, sub=sub)[0] if cid == 4 else None
+    lengths = S.make_lengths(cid, 1, batch=B, sub=sub)[0] if cid in (4, 7, 8) else None
     return acts, labels, lengths
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5, 6, 7, 8])
 def test_layout_matches_workload(cid):
     a = [(n, tuple(s)) for n, s in nets.param_layout(cid)]
     b = [(n, tuple(s)) for n, s, _, _ in S.param_layout(cid)]
@@ -32,7 +32,7 @@ def test_layout_matches_workload(cid):
     assert sum(int(np.prod(s)) for _, s in a) == S.param_count(cid)
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4, 6])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 6, 7, 8])
 def test_step_matches_independent_autograd(cid):
     B = SMALL_B[cid]
     theta = S.init_params(cid)
@@ -53,7 +53,7 @@ def test_step_matches_independent_autograd(cid):
     np.testing.assert_allclose(r["params"], theta - 0.01 * r["grads"], rtol=1e-15, atol=1e-18)
 
 
-@pytest.mark.parametrize("cid,n_probe", [(1, 12), (3, 10), (6, 12)])
+@pytest.mark.parametrize("cid,n_probe", [(1, 12), (3, 10), (6, 12), (7, 12)])
 def test_step_gradient_finite_differences(cid, n_probe):
     B = 2
     theta = S.init_params(cid).astype(np.float64)
@@ -75,7 +75,7 @@ def test_step_gradient_finite_differences(cid, n_probe):
         assert abs(num - r["grads"][i]) <= 1e-6 * gmax, (i, num, r["grads"][i])
 
 
-@pytest.mark.parametrize("cid,C", [(1, 10), (2, 10), (3, 100), (4, 2), (6, 10)])
+@pytest.mark.parametrize("cid,C", [(1, 10), (2, 10), (3, 100), (4, 2), (6, 10), (7, 2), (8, 2)])
 def test_zero_classifier_gives_ln_c(cid, C):
     theta = S.init_params(cid).astype(np.float64)
     lay = S.param_layout(cid)
@@ -100,15 +100,15 @@ def test_lr_zero_and_momentum_recursion():
     np.testing.assert_allclose(r2["params"], r1["params"] - 0.01 * r2["momentum"], rtol=1e-15)
 
 
-def test_padded_tokens_never_matter():
-    cid = 4
+@pytest.mark.parametrize("cid,lens", [(4, (40, 77)), (7, (5, 33)), (8, (17, 200))])
+def test_padded_tokens_never_matter(cid, lens):
     theta = S.init_params(cid)
     acts, labels, lengths = _inputs(cid, 2)
-    lengths = np.array([40, 77], np.int32)
+    lengths = np.array(lens, np.int32)
     r = oracle.server_step(cid, theta, acts, labels, lengths)
     x2 = nets.decode_acts(acts, np.float64).copy()
-    x2[0, 40:] = 123.0
-    x2[1, 77:] = -55.0
+    x2[0, lens[0]:] = 123.0
+    x2[1, lens[1]:] = -55.0
     r2 = oracle.server_step(cid, theta, x2, labels, lengths)
     np.testing.assert_allclose(r2["logits"], r["logits"], rtol=1e-12, atol=1e-13)
     np.testing.assert_allclose(r2["grads"], r["grads"], rtol=1e-9, atol=1e-12 * np.abs(r["grads"]).max())

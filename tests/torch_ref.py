@@ -58,6 +58,23 @@ def forward(cid, P, x, lengths=None):
         forward.last_acts = xi
         h = F.relu(F.conv2d(xi, _w4(P["aux.conv.w"]), P["aux.conv.b"], padding=1)).mean((2, 3))
         return F.linear(h, P["aux.fc.w"], P["aux.fc.b"])
+    if cid in (7, 8):
+        B, L, d = x.shape
+        H = 5 if cid == 7 else 50
+        dh = d // H
+        mask = torch.arange(L)[None, :] >= torch.as_tensor(lengths)[:, None]
+        h = x
+        for li in range(6 if cid == 7 else 12):
+            p = f"enc{li}"
+            qkv = F.linear(h, P[p + ".qkv.w"], P[p + ".qkv.b"])
+            q, k, v = (qkv[..., i * d:(i + 1) * d].reshape(B, L, H, dh).transpose(1, 2) for i in range(3))
+            s = torch.matmul(q, k.transpose(-1, -2)) / dh ** 0.5
+            s = s.masked_fill(mask[:, None, None, :], float("-inf"))
+            o = torch.matmul(torch.softmax(s, -1), v).transpose(1, 2).reshape(B, L, d)
+            h = F.layer_norm(h + F.linear(o, P[p + ".o.w"], P[p + ".o.b"]), (d,), P[p + ".ln1.g"], P[p + ".ln1.b"], 1e-5)
+            f = F.linear(F.relu(F.linear(h, P[p + ".ffn1.w"], P[p + ".ffn1.b"])), P[p + ".ffn2.w"], P[p + ".ffn2.b"])
+            h = F.layer_norm(h + f, (d,), P[p + ".ln2.g"], P[p + ".ln2.b"], 1e-5)
+        return F.linear(h[:, 0], P["cls.w"], P["cls.b"])
     if cid == 4:
         B, L, d = x.shape
         H, dh = 12, 64
