@@ -1,6 +1,6 @@
 """Benchmark of the FedOptima server hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..5, default 4]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..8, default 4] [--pipeline]
 
 One step = one pass of the server's hot path over one activation batch:
 an arriving batch is copied into the HBM activation pool (Alg. 2 put() with
@@ -45,7 +45,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (transformer 5, 128-device VGG 10)")
     ap.add_argument("--config", type=int, default=4, help="1-3: the parity workloads' step loops; 4: "
                     "transformer (default); 5: 128-device VGG with Poisson arrivals; 6: the device-side "
-                    "iteration of the VGG split")
+                    "iteration of the VGG split; 7, 8: the paper's Transformer-6 / Transformer-12 server parts")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pipeline", action="store_true",
                     help="the concurrent pipeline (Receiver and Compute Engine threads) on the 128-device VGG "
@@ -80,7 +80,8 @@ def cpu_baseline(cid, sample_steps):
     theta = S.init_params(cid)
     acts = S.make_acts(cid, sample_steps, batch=Bs, sub=99)
     labels = S.make_labels(cid, sample_steps, batch=Bs, sub=99)
-    lengths = S.make_lengths(cid, sample_steps, batch=Bs, sub=99) if cid == 4 else [None] * sample_steps
+    lengths = (S.make_lengths(cid, sample_steps, batch=Bs, sub=99) if cid in (4, 7, 8)
+               else [None] * sample_steps)
     t0 = time.perf_counter()
     cfg = S.get_config(cid)
     mom = None
@@ -347,7 +348,25 @@ WORKLOADS = {
     4: {"workload": "bert-base split server step: 10 post-LN encoder layers d=768 h=12 ffn=3072, "
                     "batch 32 x 128 tokens, lengths U[32,128], 16 devices, plain SGD",
         "peak": PEAK_BF16_TFLOPS, "gflop": 1099.0},
+    7: {"workload": "Transformer-6 split server step (fp32): 6 post-LN encoder layers d=100 h=5 ffn=100 ReLU, "
+                    "classifier on the first token, batch 16 x 64 tokens, lengths U[4,64], 8 devices",
+        "peak": PEAK_F32_TFLOPS, "gflop": None},
+    8: {"workload": "Transformer-12 split server step (fp32): 12 post-LN encoder layers d=100 h=50 ffn=100 ReLU, "
+                    "classifier on the first token, batch 16 x 256 tokens, lengths U[16,256], 16 devices",
+        "peak": PEAK_F32_TFLOPS, "gflop": None},
 }
+
+
+def tfsmall_gflop(cid):
+    """FLOPs the fp32 transformer step executes (padded [B][L] layout): per
+    encoder layer and sequence 2 L d (3d + d + 2 ffn) + 4 d L^2, three times
+    (forward, input and weight gradients) less the first layer's input
+    gradient, plus the classifier."""
+    L, layers = (64, 6) if cid == 7 else (256, 12)
+    d, ff, B = 100, 100, 16
+    fwd = 2 * L * d * (3 * d + d + 2 * ff) + 4 * d * L * L
+    per_seq = layers * 3 * fwd - 2 * L * 3 * d * d + 3 * 2 * d * 2
+    return B * per_seq / 1e9
 
 
 def fused_aggregation(A, torch, n, m):
@@ -673,12 +692,12 @@ def main():
         bench_vgg128(args, A, torch, S)
         return
     if cid not in WORKLOADS:
-        raise SystemExit("bench.py: --config 1..5 (4, the transformer, is the default)")
+        raise SystemExit("bench.py: --config 1..8 (4, the transformer, is the default)")
     args.steps = 30 if args.steps is None else args.steps
     args.warmup = 5 if args.warmup is None else args.warmup
     cfg = S.get_config(cid)
     B, K = cfg.batch, cfg.n_devices
-    bert = cfg.family == "bert"
+    bert = cfg.family in ("bert", "tfsmall")  # batches carry sequence lengths
     stream = torch.cuda.current_stream()
 
     # ---------------- synthetic inputs, resident in HBM before timing
@@ -759,7 +778,8 @@ def main():
     # the workload's fixed count where its kernels carry no records (fp32 CNN)
     alg_flops = sum(s["flops"] for s in stats)
     mfma_flops = sum(s["mfma_flops"] for s in stats)
-    flops_step = alg_flops / args.steps if alg_flops else wl["gflop"] * 1e9
+    gflop = wl["gflop"] if wl["gflop"] is not None else tfsmall_gflop(cid)
+    flops_step = alg_flops / args.steps if alg_flops else gflop * 1e9
     mfu = flops_step / (ms_step * 1e-3) / (peak * 1e12)
     gemms = [s for s in stats if s["name"].startswith("gemm")]
     if gemms:
@@ -770,7 +790,7 @@ def main():
                     "avg_launch_us": round(dom["ms"] / dom["launches"] * 1e3, 2), "traffic": traffic_for(dom["name"]),
                     "traffic_source": TRAFFIC_SOURCE}
     else:  # the fp32 direct-convolution CNN: the whole step against the fp32 vector peak
-        roofline = {"bound": "alu", "kernel": "whole step (fp32 direct convolutions, not instrumented)",
+        roofline = {"bound": "alu", "kernel": "whole step (fp32 FMA kernels, not instrumented)",
                     "achieved": round(flops_step / (ms_step * 1e-3) / 1e12, 3), "peak": peak, "unit": "TFLOP/s",
                     "frac": round(mfu, 5), "traffic": None}
     kernels = [{"name": s["name"], "launches": s["launches"], "ms_per_step": round(s["ms"] / args.steps, 4),

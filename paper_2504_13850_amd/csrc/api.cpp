@@ -29,6 +29,7 @@ int64_t cnn32_param_count();
 int64_t cnn16_param_count(int32_t cid);
 int64_t bert_param_count();
 int64_t device_param_count();
+int64_t tfsmall_param_count(int32_t cid);
 
 }  // namespace fo
 
@@ -42,6 +43,7 @@ extern "C" int64_t fo_config_param_count(int32_t cid) {
         case 2: case 3: case 5: return cnn16_param_count(cid);
         case 4: return bert_param_count();
         case 6: return device_param_count();
+        case 7: case 8: return tfsmall_param_count(cid);
         default: return -1;
     }
 }
@@ -50,7 +52,7 @@ extern "C" int32_t fo_config_num_classes(int32_t cid) {
     switch (cid) {
         case 1: case 2: case 5: case 6: return 10;
         case 3: return 100;
-        case 4: return 2;
+        case 4: case 7: case 8: return 2;
         default: return -1;
     }
 }
@@ -61,6 +63,8 @@ static const Family* family_of(int32_t cid) {
         case 2: case 3: case 5: return family_cnn16();
         case 4: return family_bert();
         case 6: return family_device();
+        case 7: return family_tfsmall7();
+        case 8: return family_tfsmall8();
         default: return nullptr;
     }
 }
@@ -85,7 +89,7 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
     m->n_params = np;
     m->momentum = cid == 3 ? 0.9f : 0.f;
     m->fam = fam;
-    const bool bf16 = cid != 1;
+    const bool bf16 = cid != 1 && cid != 7 && cid != 8;  // fp32 configs keep no bf16 shadows
     size_t bytes = 0;
     auto add = [&](size_t b) { bytes += (b + 255) & ~size_t(255); };
     add(sizeof(float) * np);                          // params
@@ -285,7 +289,8 @@ extern "C" fo_status fo_server_step(fo_model* m, const fo_acts* acts, const int3
     FO_CHECK(acts->batch >= 1 && acts->batch <= m->max_batch, "fo_server_step: batch=%d outside [1,%d]",
              acts->batch, m->max_batch);
     FO_CHECK(device_id >= 0, "fo_server_step: device_id=%d must be >= 0", device_id);
-    FO_CHECK(m->cid != 4 || acts->lengths != nullptr, "fo_server_step: config 4 needs sequence lengths");
+    FO_CHECK((m->cid != 4 && m->cid != 7 && m->cid != 8) || acts->lengths != nullptr,
+             "fo_server_step: config %d needs sequence lengths", m->cid);
     FO_CHECK(((uintptr_t)acts->x % 16) == 0, "fo_server_step: activations not 16-byte aligned");
     // A batch taken from a pool must be the one its last pick put in service.
     fo_queues* owner = nullptr;

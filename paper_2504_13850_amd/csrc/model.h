@@ -69,5 +69,7 @@ const Family* family_cnn32();   // config 1
 const Family* family_cnn16();   // configs 2, 3, 5
 const Family* family_bert();    // config 4
 const Family* family_device();  // config 6 (device side of configs 2 and 5)
+const Family* family_tfsmall7();  // config 7 (Transformer-6 after its embedding)
+const Family* family_tfsmall8();  // config 8 (Transformer-12 after its embedding)
 
 }  // namespace fo

@@ -27,7 +27,7 @@ def _batch(cid, B, sub):
     if cfg.dtype != "f32":
         acts = acts.view(np.int16)
     labels = S.make_labels(cid, 1, batch=B, sub=sub)[0]
-    lengths = S.make_lengths(cid, 1, batch=B, sub=sub)[0] if cfg.family == "bert" else None
+    lengths = S.make_lengths(cid, 1, batch=B, sub=sub)[0] if cfg.family in ("bert", "tfsmall") else None
     return acts, labels, lengths
 
 
@@ -51,7 +51,7 @@ def _eager_noise(torch, step):
     return float(a.sum().item())
 
 
-@pytest.mark.parametrize("cid,Bmax", [(1, 8), (2, 8), (3, 8), (4, 6), (5, 8), (6, 8)])
+@pytest.mark.parametrize("cid,Bmax", [(1, 8), (2, 8), (3, 8), (4, 6), (5, 8), (6, 8), (7, 8), (8, 4)])
 def test_graph_replay_matches_direct_launches(cid, Bmax):
     torch = torch_cuda()
     cfg = S.get_config(cid)

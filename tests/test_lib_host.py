@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_param_counts_and_classes():
-    for cid in range(1, 7):
+    for cid in range(1, 9):
         assert A.fo_config_param_count(cid) == S.param_count(cid)
         assert A.fo_config_num_classes(cid) == S.get_config(cid).n_classes
     assert A.fo_config_param_count(9) == -1
