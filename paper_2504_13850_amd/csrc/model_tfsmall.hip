@@ -57,7 +57,8 @@ struct Gf {
     const StepIn* inAdd;  // add = the batch when set
 };
 
-constexpr int GT = 64, GK = 16;
+constexpr int GT = 64, GK = 32;
+constexpr int GV = GT * GK / 256;  // operand values per thread per K chunk (8)
 
 __device__ __forceinline__ float epi(const Gf& g, const float* add, int m, int n, float v) {
     if (g.bias) v += g.bias[n];
@@ -67,42 +68,76 @@ __device__ __forceinline__ float epi(const Gf& g, const float* add, int m, int n
     return v;
 }
 
+// One operand's share of a 64 x 32 chunk: value v of thread t is element
+// e = t + 256 v; with K contiguous (KF) the 32 k of a row are consecutive
+// threads, else the 64 rows are.
+template <bool KF>
+__device__ __forceinline__ void chunk_rc(int e, int& r, int& k) {
+    r = KF ? e >> 5 : e & 63;
+    k = KF ? e & 31 : e >> 6;
+}
+template <bool KF>
+__device__ __forceinline__ void load_chunk(const float* P, int64_t sr, int64_t sk, int r0, int R, int k0, int ke,
+                                           float (&v)[GV]) {
+#pragma unroll
+    for (int i = 0; i < GV; ++i) {
+        int r, k;
+        chunk_rc<KF>(threadIdx.x + 256 * i, r, k);
+        const int gr = r0 + r, gk = k0 + k;
+        v[i] = gr < R && gk < ke ? P[(int64_t)gr * sr + (KF ? (int64_t)gk : (int64_t)gk * sk)] : 0.f;
+    }
+}
+template <bool KF>
+__device__ __forceinline__ void store_chunk(float (*T)[GT + 4], const float (&v)[GV]) {
+#pragma unroll
+    for (int i = 0; i < GV; ++i) {
+        int r, k;
+        chunk_rc<KF>(threadIdx.x + 256 * i, r, k);
+        T[k][r] = v[i];
+    }
+}
+
+// 64 x 64 output tile per workgroup, 4 x 4 per thread; K in chunks of 32,
+// the next chunk's loads in flight (registers) while this one is computed
+// from LDS, two LDS buffers (one barrier per chunk).
+template <bool AKF, bool BKF>
 __global__ void __launch_bounds__(256) gemm_f32(const Gf g) {
-    __shared__ float As[GK][GT + 4], Bs[GK][GT + 4];
+    __shared__ float As[2][GK][GT + 4], Bs[2][GK][GT + 4];
     const float* A = g.inA ? (const float*)g.inA->x : g.A;
     const float* Bp = g.inB ? (const float*)g.inB->x : g.B;
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
     const int n0 = blockIdx.x * GT, m0 = blockIdx.y * GT, z = blockIdx.z;
     const int kc = ((g.K + g.S - 1) / g.S + GK - 1) / GK * GK;
     const int kb = z * kc, ke = min(g.K, kb + kc);
+    const int nch = ke > kb ? (ke - kb + GK - 1) / GK : 0;
     float acc[4][4] = {};
-    const bool a_kfast = g.ak == 1, b_kfast = g.bk == 1;
-    for (int k0 = kb; k0 < ke; k0 += GK) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {  // 64 x 16 elements of each operand, 4 per thread
-            const int e = tid + 256 * i;
-            int r = a_kfast ? e >> 4 : e & 63, k = a_kfast ? e & 15 : e >> 6;
-            int gm = m0 + r, gk = k0 + k;
-            As[k][r] = gm < g.M && gk < ke ? A[(int64_t)gm * g.am + (int64_t)gk * g.ak] : 0.f;
-            r = b_kfast ? e >> 4 : e & 63;
-            k = b_kfast ? e & 15 : e >> 6;
-            const int gn = n0 + r;
-            gk = k0 + k;
-            Bs[k][r] = gn < g.N && gk < ke ? Bp[(int64_t)gn * g.bn + (int64_t)gk * g.bk] : 0.f;
+    float ra[GV], rb[GV];
+    if (nch > 0) {
+        load_chunk<AKF>(A, g.am, g.ak, m0, g.M, kb, ke, ra);
+        load_chunk<BKF>(Bp, g.bn, g.bk, n0, g.N, kb, ke, rb);
+        store_chunk<AKF>(As[0], ra);
+        store_chunk<BKF>(Bs[0], rb);
+    }
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+        const int u = c & 1;
+        if (c + 1 < nch) {  // next chunk in flight during this chunk's FMAs
+            load_chunk<AKF>(A, g.am, g.ak, m0, g.M, kb + (c + 1) * GK, ke, ra);
+            load_chunk<BKF>(Bp, g.bn, g.bk, n0, g.N, kb + (c + 1) * GK, ke, rb);
         }
-        __syncthreads();
 #pragma unroll
         for (int k = 0; k < GK; ++k) {
-            float a[4], b[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                a[i] = As[k][ty * 4 + i];
-                b[i] = Bs[k][tx * 4 + i];
-            }
+            const float4 a4 = *reinterpret_cast<const float4*>(&As[u][k][ty * 4]);
+            const float4 b4 = *reinterpret_cast<const float4*>(&Bs[u][k][tx * 4]);
+            const float a[4] = {a4.x, a4.y, a4.z, a4.w}, b[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        }
+        if (c + 1 < nch) {
+            store_chunk<AKF>(As[u ^ 1], ra);
+            store_chunk<BKF>(Bs[u ^ 1], rb);
         }
         __syncthreads();
     }
@@ -455,7 +490,16 @@ fo_status gemm(const Ctx& c, Gf g) {
     }
     if (g.S < 1) g.S = 1;
     g.part = c.P->part;
-    hipLaunchKernelGGL(gemm_f32, dim3((int)cdiv(g.N, GT), (int)cdiv(g.M, GT), g.S), dim3(256), 0, c.s, g);
+    const dim3 grid((int)cdiv(g.N, GT), (int)cdiv(g.M, GT), g.S);
+    const bool akf = g.ak == 1, bkf = g.bk == 1;
+    if (akf && bkf)
+        hipLaunchKernelGGL((gemm_f32<true, true>), grid, dim3(256), 0, c.s, g);
+    else if (akf)
+        hipLaunchKernelGGL((gemm_f32<true, false>), grid, dim3(256), 0, c.s, g);
+    else if (bkf)
+        hipLaunchKernelGGL((gemm_f32<false, true>), grid, dim3(256), 0, c.s, g);
+    else
+        hipLaunchKernelGGL((gemm_f32<false, false>), grid, dim3(256), 0, c.s, g);
     FO_LAUNCHED();
     if (g.S > 1) {
         hipLaunchKernelGGL(gemm_f32_reduce, dim3(nblk((int64_t)g.M * g.N)), dim3(256), 0, c.s, g);
