@@ -68,6 +68,12 @@ CONFIGS = {
                   0.01, 0.0, 0, 1.0, 100, {"layers": 6, "heads": 5, "ffn": 100, "min_len": 4}),
     8: ConfigSpec(8, "transformer12-split-fp32", "tfsmall", 16, (256, 100), 2, 16, "f32",
                   0.01, 0.0, 0, 1.0, 100, {"layers": 12, "heads": 50, "ffn": 100, "min_len": 16}),
+    # The paper's VGG-5 (Table 4) on CIFAR-10, split after its second pool (the
+    # split the pre-processor chooses for Raspberry-Pi-class devices): the server
+    # trains conv3x3 64->64 with training-mode batch norm and ReLU, a 2x2 max
+    # pool, fc 1024->128 with ReLU and fc 128->10, in fp32, on [64, 8, 8] inputs.
+    9: ConfigSpec(9, "vgg5-split-fp32", "vgg5", 32, (64, 8, 8), 10, 8, "f32",
+                  0.01, 0.0, 0, 1.0, 100),
 }
 
 
@@ -129,6 +135,11 @@ def param_layout(cid: int) -> List[Entry]:
                     lay += _norm(p + ".dsbn", c)
             cin = c
         lay += _linear("fc", cfg.n_classes, 512)
+    elif cfg.family == "vgg5":
+        lay += _conv("conv", 64, cfg.in_shape[0], 3, False)
+        lay += _norm("bn", 64)
+        lay += _linear("fc1", 128, 64 * 4 * 4)
+        lay += _linear("fc2", cfg.n_classes, 128)
     elif cfg.family == "vgg_device":
         lay += _conv("conv1", 64, 3, 3, True)
         lay += _conv("conv2", 64, 64, 3, True)

@@ -465,7 +465,7 @@ typedef struct {
 
 /* The unit tables of the paper's networks (Table 4) and of VGG-16:
  *   FO_NET_VGG5              conv3-32, pool, conv3-64, pool, conv3-64, pool, fc-128, fc-classes
- *                            (bias and batch norm per convolution); in_hw = image side, % 8 == 0
+ *                            (batch norm, no bias, per convolution); in_hw = image side, % 8 == 0
  *   FO_NET_MOBILENETV3_LARGE conv3-16 stride 2, the 15 bottlenecks, conv1-960, global pool,
  *                            fc-1280, fc-classes; in_hw = image side
  *   FO_NET_TRANSFORMER6/12   EMB-100, 6 encoders (d 100, 5 heads, FFN 100) or 12 (50 heads),

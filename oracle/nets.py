@@ -24,9 +24,10 @@ RESNET_STAGES = [(2, 128, 2), (3, 256, 2), (4, 512, 2)]  # (stage, channels, blo
 BERT = dict(d=768, heads=12, ffn=3072, layers=10, classes=2)
 # the paper's Transformer-6 and Transformer-12 (Table 4) after their embedding
 TFSMALL = {7: dict(d=100, heads=5, ffn=100, layers=6), 8: dict(d=100, heads=50, ffn=100, layers=12)}
-FAMILY = {1: "cnn", 2: "vgg", 3: "resnet", 4: "bert", 5: "vgg", 6: "vgg_device", 7: "tfsmall", 8: "tfsmall"}
-IN_CH = {1: 32, 2: 64, 3: 64, 5: 64, 6: 3}
-CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10, 6: 10, 7: 2, 8: 2}
+FAMILY = {1: "cnn", 2: "vgg", 3: "resnet", 4: "bert", 5: "vgg", 6: "vgg_device", 7: "tfsmall", 8: "tfsmall",
+          9: "vgg5"}
+IN_CH = {1: 32, 2: 64, 3: 64, 5: 64, 6: 3, 9: 64}
+CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10, 6: 10, 7: 2, 8: 2, 9: 10}
 
 
 def param_layout(cid: int):
@@ -51,6 +52,13 @@ def param_layout(cid: int):
         conv("conv1", 64, 32, 3)
         conv("conv2", 64, 64, 3)
         lin("fc", 10, 64)
+    elif fam == "vgg5":
+        # the server part of VGG-5 (Table 4) after its second pool: CONV-3-64 with
+        # batch norm (no bias), pool, FC-128, FC-X on [64, 8, 8] inputs
+        conv("conv", 64, IN_CH[cid], 3, bias=False)
+        norm("bn", 64)
+        lin("fc1", 128, 64 * 4 * 4)
+        lin("fc2", CLASSES[cid], 128)
     elif fam == "vgg_device":
         # device network M_d: VGG-16's first block; auxiliary network: one layer
         # of the type of M_d's last layer, then a dense classifier (Sec. 3.2.2)
@@ -353,6 +361,28 @@ class Bert(_Net):
         self.G = G
 
 
+class VGG5Server(_Net):
+    """conv3x3 (no bias) -> BN (train) -> ReLU -> maxpool 2x2 -> flatten (C, H, W)
+    -> fc1 -> ReLU -> fc2."""
+
+    def __init__(self, P):
+        self.conv = Lyr.Conv2d(P["conv.w"], None)
+        self.bn = Lyr.BatchNorm2d(P["bn.g"], P["bn.b"])
+        self.r1, self.pool = Lyr.ReLU(), Lyr.MaxPool2()
+        self.fc1, self.r2, self.fc2 = Lyr.Linear(P["fc1.w"], P["fc1.b"]), Lyr.ReLU(), Lyr.Linear(P["fc2.w"], P["fc2.b"])
+
+    def fwd(self, x, lengths=None):
+        p = self.pool.fwd(self.r1.fwd(self.bn.fwd(self.conv.fwd(x))))
+        self.pshape = p.shape
+        return self.fc2.fwd(self.r2.fwd(self.fc1.fwd(p.reshape(p.shape[0], -1))))
+
+    def bwd(self, dz):
+        dp = self.fc1.bwd(self.r2.bwd(self.fc2.bwd(dz))).reshape(self.pshape)
+        self.conv.bwd(self.bn.bwd(self.r1.bwd(self.pool.bwd(dp))), need_dx=False)
+        self.G = {"conv.w": self.conv.dw, "bn.g": self.bn.dg, "bn.b": self.bn.db,
+                  "fc1.w": self.fc1.dw, "fc1.b": self.fc1.db, "fc2.w": self.fc2.dw, "fc2.b": self.fc2.db}
+
+
 class SmallTransformer(_Net):
     """The server part of Transformer-6/12 (Table 4) split after EMB-100: the
     encoder layers (ReLU FFN) and FC-X on the first token."""
@@ -384,6 +414,8 @@ def build(cid, P):
     fam = FAMILY[cid]
     if fam == "tfsmall":
         return SmallTransformer(P, cid)
+    if fam == "vgg5":
+        return VGG5Server(P)
     if fam == "cnn":
         return CNN(P)
     if fam == "vgg_device":

@@ -17,8 +17,8 @@ paper is silent:
   bytes per value (what a device sends if the split follows layer l).  The
   split l ranges over 1..L as in Eq. 8; ties go to the smallest l.
 * Architectures.  VGG-5 (Table 4): conv3-32, pool, conv3-64, pool, conv3-64,
-  pool, fc-128, fc-X on 32x32x3 inputs; convolutions carry a bias and a batch
-  norm.  MobileNetV3-Large (Table 4, with the bottleneck expansions, strides,
+  pool, fc-128, fc-X on 32x32x3 inputs; each convolution is followed by a
+  batch norm and carries no bias (the norm's shift makes one redundant).  MobileNetV3-Large (Table 4, with the bottleneck expansions, strides,
   squeeze-excitation placement and activations of its own definition,
   Howard et al., 2019): squeeze width = the expansion / 4 rounded to a
   multiple of 8 as in that definition; the last two layers after the global
@@ -116,7 +116,7 @@ def net_layers(net: str, classes: int, in_hw: int):
     if net == "vgg5":
         h = in_hw
         for c_in, c_out in ((3, 32), (32, 64), (64, 64)):
-            L.append(conv(3, 1, c_in, c_out, h, h))
+            L.append(conv(3, 1, c_in, c_out, h, h, bias=False))
             L.append(pool(c_out, h, h))
             h //= 2
         L.append(fc(64 * h * h, 128))

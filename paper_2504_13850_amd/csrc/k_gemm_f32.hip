@@ -1,0 +1,150 @@
+// fp32 products for the small fp32 models (the paper's Transformer-6/12 and
+// VGG-5 server parts): C[m][n] = epilogue(sum_k A(m, k) B(n, k)) over strided
+// operands, as LDS-tiled FMA with the next K chunk's loads in flight, and an
+// optional deterministic split over K (slices summed in order afterwards).
+#include "kernels.h"
+
+namespace fo {
+namespace {
+
+constexpr int GT = 64, GK = 32;
+constexpr int GV = GT * GK / 256;  // operand values per thread per K chunk (8)
+
+__device__ __forceinline__ float epi(const GemmF32& g, const float* add, int m, int n, float v) {
+    if (g.bias) v += g.bias[n];
+    if (add) v += add[(int64_t)m * g.ldadd + n];
+    if (g.relu) v = fmaxf(v, 0.f);
+    if (g.mask && !(g.mask[(int64_t)m * g.ldmask + n] > 0.f)) v = 0.f;
+    return v;
+}
+
+// One operand's share of a 64 x 32 chunk: value v of thread t is element
+// e = t + 256 v; with K contiguous (KF) the 32 k of a row are consecutive
+// threads, else the 64 rows are.
+template <bool KF>
+__device__ __forceinline__ void chunk_rc(int e, int& r, int& k) {
+    r = KF ? e >> 5 : e & 63;
+    k = KF ? e & 31 : e >> 6;
+}
+template <bool KF>
+__device__ __forceinline__ void load_chunk(const float* P, int64_t sr, int64_t sk, int r0, int R, int k0, int ke,
+                                           float (&v)[GV]) {
+#pragma unroll
+    for (int i = 0; i < GV; ++i) {
+        int r, k;
+        chunk_rc<KF>(threadIdx.x + 256 * i, r, k);
+        const int gr = r0 + r, gk = k0 + k;
+        v[i] = gr < R && gk < ke ? P[(int64_t)gr * sr + (KF ? (int64_t)gk : (int64_t)gk * sk)] : 0.f;
+    }
+}
+template <bool KF>
+__device__ __forceinline__ void store_chunk(float (*T)[GT + 4], const float (&v)[GV]) {
+#pragma unroll
+    for (int i = 0; i < GV; ++i) {
+        int r, k;
+        chunk_rc<KF>(threadIdx.x + 256 * i, r, k);
+        T[k][r] = v[i];
+    }
+}
+
+// 64 x 64 output tile per workgroup, 4 x 4 per thread; K in chunks of 32,
+// the next chunk's loads in flight (registers) while this one is computed
+// from LDS, two LDS buffers (one barrier per chunk).
+template <bool AKF, bool BKF>
+__global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
+    __shared__ float As[2][GK][GT + 4], Bs[2][GK][GT + 4];
+    const float* A = g.inA ? (const float*)g.inA->x : g.A;
+    const float* Bp = g.inB ? (const float*)g.inB->x : g.B;
+    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+    const int n0 = blockIdx.x * GT, m0 = blockIdx.y * GT, z = blockIdx.z;
+    const int kc = ((g.K + g.S - 1) / g.S + GK - 1) / GK * GK;
+    const int kb = z * kc, ke = min(g.K, kb + kc);
+    const int nch = ke > kb ? (ke - kb + GK - 1) / GK : 0;
+    float acc[4][4] = {};
+    float ra[GV], rb[GV];
+    if (nch > 0) {
+        load_chunk<AKF>(A, g.am, g.ak, m0, g.M, kb, ke, ra);
+        load_chunk<BKF>(Bp, g.bn, g.bk, n0, g.N, kb, ke, rb);
+        store_chunk<AKF>(As[0], ra);
+        store_chunk<BKF>(Bs[0], rb);
+    }
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+        const int u = c & 1;
+        if (c + 1 < nch) {  // next chunk in flight during this chunk's FMAs
+            load_chunk<AKF>(A, g.am, g.ak, m0, g.M, kb + (c + 1) * GK, ke, ra);
+            load_chunk<BKF>(Bp, g.bn, g.bk, n0, g.N, kb + (c + 1) * GK, ke, rb);
+        }
+#pragma unroll
+        for (int k = 0; k < GK; ++k) {
+            const float4 a4 = *reinterpret_cast<const float4*>(&As[u][k][ty * 4]);
+            const float4 b4 = *reinterpret_cast<const float4*>(&Bs[u][k][tx * 4]);
+            const float a[4] = {a4.x, a4.y, a4.z, a4.w}, b[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        }
+        if (c + 1 < nch) {
+            store_chunk<AKF>(As[u ^ 1], ra);
+            store_chunk<BKF>(Bs[u ^ 1], rb);
+        }
+        __syncthreads();
+    }
+    const float* add = g.inAdd ? (const float*)g.inAdd->x : g.add;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = m0 + ty * 4 + i;
+        if (m >= g.M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int n = n0 + tx * 4 + j;
+            if (n >= g.N) continue;
+            if (g.S > 1)
+                g.part[((int64_t)z * g.M + m) * g.N + n] = acc[i][j];
+            else
+                g.C[(int64_t)m * g.ldc + n] = epi(g, add, m, n, acc[i][j]);
+        }
+    }
+}
+
+__global__ void __launch_bounds__(256) gemm_f32_reduce(const GemmF32 g) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)g.M * g.N) return;
+    const int m = (int)(i / g.N), n = (int)(i % g.N);
+    float v = 0.f;
+    for (int z = 0; z < g.S; ++z) v += g.part[(int64_t)z * g.M * g.N + i];
+    const float* add = g.inAdd ? (const float*)g.inAdd->x : g.add;
+    g.C[(int64_t)m * g.ldc + n] = epi(g, add, m, n, v);
+}
+
+
+}  // namespace
+
+fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_t s) {
+    FO_CHECK(g.M >= 1 && g.N >= 1 && g.K >= 1, "fp32 product: M=%d N=%d K=%d", g.M, g.N, g.K);
+    if (g.S > 1) {
+        const size_t per = (size_t)g.M * g.N;
+        if (!part || (size_t)g.S * per > part_floats) g.S = part ? (int)(part_floats / per) : 1;
+    }
+    if (g.S < 1) g.S = 1;
+    g.part = part;
+    const dim3 grid((int)cdiv(g.N, GT), (int)cdiv(g.M, GT), g.S);
+    const bool akf = g.ak == 1, bkf = g.bk == 1;
+    if (akf && bkf)
+        hipLaunchKernelGGL((gemm_f32<true, true>), grid, dim3(256), 0, s, g);
+    else if (akf)
+        hipLaunchKernelGGL((gemm_f32<true, false>), grid, dim3(256), 0, s, g);
+    else if (bkf)
+        hipLaunchKernelGGL((gemm_f32<false, true>), grid, dim3(256), 0, s, g);
+    else
+        hipLaunchKernelGGL((gemm_f32<false, false>), grid, dim3(256), 0, s, g);
+    FO_LAUNCHED();
+    if (g.S > 1) {
+        hipLaunchKernelGGL(gemm_f32_reduce, dim3((int)cdiv((int64_t)g.M * g.N, 256)), dim3(256), 0, s, g);
+        FO_LAUNCHED();
+    }
+    return FO_OK;
+}
+
+}  // namespace fo

@@ -115,4 +115,33 @@ size_t small_linear_ws_floats(int B, int I, int O);
 fo_status launch_small_linear_bwd(const float* dy, const float* x, const float* w, const float* xin_tanh, float* gw,
                                   float* gb, float* dx, int B, int I, int O, float* ws, hipStream_t s);
 
+// ------------------------------------------------------------------ k_gemm_f32.hip
+// C[m][n] = epi(sum_k A(m, k) B(n, k)) in fp32, A(m, k) at A[m am + k ak], B(n, k)
+// at B[n bn + k bk], C row m at C + m ldc; epi adds bias[n] and add[m ldadd + n],
+// applies ReLU, and zeroes entries whose mask[m ldmask + n] is not positive
+// (each optional).  S > 1 splits K into S slices whose sums go to part
+// ([S][M][N], part_floats available; fewer slices if it is smaller) and are
+// added in order by a second launch.  inA / inB / inAdd take that operand from
+// the step's batch record instead.
+struct GemmF32 {
+    const float* A;
+    int64_t am, ak;
+    const float* B;
+    int64_t bn, bk;
+    float* C;
+    int64_t ldc;
+    int M, N, K, S;
+    const float* bias;
+    const float* add;
+    int64_t ldadd;
+    const float* mask;
+    int64_t ldmask;
+    int relu;
+    float* part;
+    const StepIn* inA;
+    const StepIn* inB;
+    const StepIn* inAdd;
+};
+fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_t s);
+
 }  // namespace fo

@@ -179,7 +179,7 @@ extern "C" int32_t fo_net_units(int32_t net, int32_t classes, int32_t in_hw, fo_
             int32_t h = in_hw;
             const int32_t ch[4] = {3, 32, 64, 64};
             for (int i = 0; i < 3; ++i) {
-                t.push(conv_unit(3, 1, ch[i], ch[i + 1], h, h, true, true));
+                t.push(conv_unit(3, 1, ch[i], ch[i + 1], h, h, false, true));
                 t.push(pool_unit(ch[i + 1], h, h, 2));
                 h /= 2;
             }

@@ -85,7 +85,7 @@ def _torch_units(net, classes, hw):
                 h //= 2
             else:
                 bn = [nn.BatchNorm2d(v)] if net == "vgg5" else []
-                units.append((nn.Sequential(nn.Conv2d(c, v, 3, 1, 1), *bn, nn.ReLU()), (c, h, h)))
+                units.append((nn.Sequential(nn.Conv2d(c, v, 3, 1, 1, bias=net != "vgg5"), *bn, nn.ReLU()), (c, h, h)))
                 c = v
         widths = (128,) if net == "vgg5" else (512, 512)
         n_in = c * h * h

@@ -52,6 +52,11 @@ def forward(cid, P, x, lengths=None):
                 sc = bn(F.conv2d(h, _w4(P[p + ".ds.w"]), stride=2), p + ".dsbn") if bi == 0 else h
                 h = F.relu(o + sc)
         return F.linear(h.mean((2, 3)), P["fc.w"], P["fc.b"])
+    if cid == 9:
+        h = F.batch_norm(F.conv2d(x, _w4(P["conv.w"]), padding=1), None, None, P["bn.g"], P["bn.b"],
+                         training=True, eps=1e-5)
+        h = F.max_pool2d(F.relu(h), 2).flatten(1)
+        return F.linear(F.relu(F.linear(h, P["fc1.w"], P["fc1.b"])), P["fc2.w"], P["fc2.b"])
     if cid == 6:  # device network, then the auxiliary network on its output
         xi = F.max_pool2d(F.relu(F.conv2d(F.relu(F.conv2d(x, _w4(P["conv1.w"]), P["conv1.b"], padding=1)),
                                           _w4(P["conv2.w"]), P["conv2.b"], padding=1)), 2)
