@@ -1,6 +1,6 @@
 """Benchmark of the FedOptima server hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..8, default 4] [--pipeline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..9, default 4] [--pipeline]
 
 One step = one pass of the server's hot path over one activation batch:
 an arriving batch is copied into the HBM activation pool (Alg. 2 put() with
@@ -45,7 +45,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (transformer 5, 128-device VGG 10)")
     ap.add_argument("--config", type=int, default=4, help="1-3: the parity workloads' step loops; 4: "
                     "transformer (default); 5: 128-device VGG with Poisson arrivals; 6: the device-side "
-                    "iteration of the VGG split; 7, 8: the paper's Transformer-6 / Transformer-12 server parts")
+                    "iteration of the VGG split; 7, 8, 9: the paper's Transformer-6 / Transformer-12 / VGG-5 "
+                    "server parts")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pipeline", action="store_true",
                     help="the concurrent pipeline (Receiver and Compute Engine threads) on the 128-device VGG "
@@ -354,6 +355,10 @@ WORKLOADS = {
     8: {"workload": "Transformer-12 split server step (fp32): 12 post-LN encoder layers d=100 h=50 ffn=100 ReLU, "
                     "classifier on the first token, batch 16 x 256 tokens, lengths U[16,256], 16 devices",
         "peak": PEAK_F32_TFLOPS, "gflop": None},
+    9: {"workload": "VGG-5 split server step (fp32): conv3x3 64->64 + batch norm + ReLU, maxpool, fc 1024-128-10, "
+                    "batch 32 of [64,8,8], 8 devices",
+        # the convolution's forward and weight gradient (no input gradient), both fc layers three times
+        "peak": PEAK_F32_TFLOPS, "gflop": 32 * (2 * 2 * 64 * 576 * 64 + 3 * (2 * 1024 * 128 + 2 * 128 * 10)) / 1e9},
 }
 
 
@@ -692,7 +697,7 @@ def main():
         bench_vgg128(args, A, torch, S)
         return
     if cid not in WORKLOADS:
-        raise SystemExit("bench.py: --config 1..8 (4, the transformer, is the default)")
+        raise SystemExit("bench.py: --config 1..9 (4, the transformer, is the default)")
     args.steps = 30 if args.steps is None else args.steps
     args.warmup = 5 if args.warmup is None else args.warmup
     cfg = S.get_config(cid)
