@@ -74,7 +74,28 @@ CONFIGS = {
     # pool, fc 1024->128 with ReLU and fc 128->10, in fp32, on [64, 8, 8] inputs.
     9: ConfigSpec(9, "vgg5-split-fp32", "vgg5", 32, (64, 8, 8), 10, 8, "f32",
                   0.01, 0.0, 0, 1.0, 100),
+    # The paper's MobileNetV3-Large (Table 4) on Tiny ImageNet (64x64, 200
+    # classes), split after its seventh bottleneck (the split the pre-processor
+    # chooses for Jetson-class devices): the server trains the last eight
+    # bottlenecks (hard-swish, four with squeeze-excitation, one stride 2), the
+    # 1x1 convolution to 960 channels, the global pool and fc 960-1280-200, in
+    # fp32, on [80, 4, 4] inputs.
+    10: ConfigSpec(10, "mobilenetv3l-split-fp32", "mbv3", 32, (80, 4, 4), 200, 16, "f32",
+                   0.01, 0.0, 0, 1.0, 100),
 }
+
+# The server part of MobileNetV3-Large after its seventh bottleneck:
+# (kernel, expansion, output channels, squeeze-excitation, stride)
+MBV3_SERVER = [(3, 200, 80, False, 1), (3, 184, 80, False, 1), (3, 184, 80, False, 1), (3, 480, 112, True, 1),
+               (3, 672, 112, True, 1), (5, 672, 160, True, 2), (5, 960, 160, True, 1), (5, 960, 160, True, 1)]
+
+
+def squeeze_width(e: int) -> int:
+    """The squeeze-excitation width of an expansion e: e / 4 rounded to a
+    multiple of 8 (at least 8, never below 90% of e / 4)."""
+    v = e // 4
+    n = max(8, int(v + 4) // 8 * 8)
+    return n + 8 if n < 0.9 * v else n
 
 
 def get_config(cid: int) -> ConfigSpec:
@@ -135,6 +156,25 @@ def param_layout(cid: int) -> List[Entry]:
                     lay += _norm(p + ".dsbn", c)
             cin = c
         lay += _linear("fc", cfg.n_classes, 512)
+    elif cfg.family == "mbv3":
+        cin = cfg.in_shape[0]
+        for j, (k, e, co, se, _) in enumerate(MBV3_SERVER):
+            p = f"b{j}"
+            lay += _conv(p + ".expand", e, cin, 1, False)
+            lay += _norm(p + ".bn1", e)
+            lay += [(p + ".dw.w", (e, k, k, 1), "kaiming", k * k)]
+            lay += _norm(p + ".bn2", e)
+            if se:
+                s = squeeze_width(e)
+                lay += _linear(p + ".se.fc1", s, e)
+                lay += _linear(p + ".se.fc2", e, s)
+            lay += _conv(p + ".proj", co, e, 1, False)
+            lay += _norm(p + ".bn3", co)
+            cin = co
+        lay += _conv("last", 960, cin, 1, False)
+        lay += _norm("last_bn", 960)
+        lay += _linear("fc1", 1280, 960)
+        lay += _linear("fc2", cfg.n_classes, 1280)
     elif cfg.family == "vgg5":
         lay += _conv("conv", 64, cfg.in_shape[0], 3, False)
         lay += _norm("bn", 64)

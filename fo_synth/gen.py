@@ -66,7 +66,7 @@ def make_acts(cid: int, n_batches: int, batch: int | None = None, sub: int = 0) 
     B = cfg.batch if batch is None else batch
     rng = rng_for(cid, "acts", sub)
     x = rng.standard_normal(size=(n_batches, B) + tuple(cfg.in_shape), dtype=np.float32)
-    if cfg.family not in ("bert", "vgg_device", "tfsmall"):
+    if cfg.family not in ("bert", "vgg_device", "tfsmall", "mbv3"):  # mbv3: a linear bottleneck's output
         np.maximum(x, 0.0, out=x)
     if cfg.dtype == "f32":
         return x

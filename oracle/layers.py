@@ -65,6 +65,42 @@ class Conv2d:
         return dxp[:, :, p:p + H, p:p + W]
 
 
+class DepthwiseConv2d:
+    """One k x k filter per channel (groups = channels), NCHW input, weight
+    [C, 1, k, k], zero padding k // 2, no bias.  y[b,c,o] = sum over the
+    window of x[b,c,i] w[c,tap]; backward by the same sums read the other way."""
+
+    def __init__(self, w, stride=1):
+        self.w, self.s = w, stride
+
+    def fwd(self, x):
+        B, C, H, W = x.shape
+        k = self.w.shape[-1]
+        p, s = k // 2, self.s
+        Ho, Wo = (H + 2 * p - k) // s + 1, (W + 2 * p - k) // s + 1
+        xp = np.zeros((B, C, H + 2 * p, W + 2 * p), x.dtype)
+        xp[:, :, p:p + H, p:p + W] = x
+        y = np.zeros((B, C, Ho, Wo), x.dtype)
+        for i in range(k):
+            for j in range(k):
+                y += xp[:, :, i:i + s * Ho:s, j:j + s * Wo:s] * self.w[None, :, 0, i, j, None, None]
+        self.cache = (xp, x.shape, Ho, Wo)
+        return y
+
+    def bwd(self, dy, need_dx=True):
+        xp, (B, C, H, W), Ho, Wo = self.cache
+        k = self.w.shape[-1]
+        p, s = k // 2, self.s
+        self.dw = np.zeros_like(self.w)
+        dxp = np.zeros_like(xp)
+        for i in range(k):
+            for j in range(k):
+                win = xp[:, :, i:i + s * Ho:s, j:j + s * Wo:s]
+                self.dw[:, 0, i, j] = (dy * win).sum(axis=(0, 2, 3))
+                dxp[:, :, i:i + s * Ho:s, j:j + s * Wo:s] += dy * self.w[None, :, 0, i, j, None, None]
+        return dxp[:, :, p:p + H, p:p + W] if need_dx else None
+
+
 # ----------------------------------------------------------------------------- elementwise
 class ReLU:
     def fwd(self, x):
@@ -87,6 +123,30 @@ class GELU:
         cdf = 0.5 * (1.0 + erf(x / np.sqrt(2.0)))
         pdf = np.exp(-0.5 * x * x) / np.sqrt(2.0 * np.pi)
         return dy * (cdf + x * pdf)
+
+
+class HardSwish:
+    """x ReLU6(x + 3) / 6; derivative 0 below -3, 1 above 3, (2x + 3) / 6 between."""
+
+    def fwd(self, x):
+        self.x = x
+        return x * np.clip(x + 3.0, 0.0, 6.0) / 6.0
+
+    def bwd(self, dy):
+        x = self.x
+        return dy * np.where(x < -3.0, 0.0, np.where(x > 3.0, 1.0, (2.0 * x + 3.0) / 6.0))
+
+
+class HardSigmoid:
+    """ReLU6(x + 3) / 6; derivative 1/6 strictly between -3 and 3, else 0."""
+
+    def fwd(self, x):
+        self.x = x
+        return np.clip(x + 3.0, 0.0, 6.0) / 6.0
+
+    def bwd(self, dy):
+        x = self.x
+        return dy * np.where((x > -3.0) & (x < 3.0), 1.0 / 6.0, 0.0)
 
 
 class Tanh:

@@ -25,9 +25,20 @@ BERT = dict(d=768, heads=12, ffn=3072, layers=10, classes=2)
 # the paper's Transformer-6 and Transformer-12 (Table 4) after their embedding
 TFSMALL = {7: dict(d=100, heads=5, ffn=100, layers=6), 8: dict(d=100, heads=50, ffn=100, layers=12)}
 FAMILY = {1: "cnn", 2: "vgg", 3: "resnet", 4: "bert", 5: "vgg", 6: "vgg_device", 7: "tfsmall", 8: "tfsmall",
-          9: "vgg5"}
-IN_CH = {1: 32, 2: 64, 3: 64, 5: 64, 6: 3, 9: 64}
-CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10, 6: 10, 7: 2, 8: 2, 9: 10}
+          9: "vgg5", 10: "mbv3"}
+IN_CH = {1: 32, 2: 64, 3: 64, 5: 64, 6: 3, 9: 64, 10: 80}
+CLASSES = {1: 10, 2: 10, 3: 100, 4: 2, 5: 10, 6: 10, 7: 2, 8: 2, 9: 10, 10: 200}
+# MobileNetV3-Large's last eight bottlenecks (its own definition): kernel,
+# expansion, output channels, squeeze-excitation, stride; all hard-swish
+MBV3_TAIL = [(3, 200, 80, False, 1), (3, 184, 80, False, 1), (3, 184, 80, False, 1), (3, 480, 112, True, 1),
+             (3, 672, 112, True, 1), (5, 672, 160, True, 2), (5, 960, 160, True, 1), (5, 960, 160, True, 1)]
+
+
+def se_width(e):
+    """Squeeze width: e / 4 to a multiple of 8, at least 8, not below 90% of e / 4."""
+    v = e // 4
+    n = max(8, int(v + 4) // 8 * 8)
+    return n + 8 if n < 0.9 * v else n
 
 
 def param_layout(cid: int):
@@ -52,6 +63,24 @@ def param_layout(cid: int):
         conv("conv1", 64, 32, 3)
         conv("conv2", 64, 64, 3)
         lin("fc", 10, 64)
+    elif fam == "mbv3":
+        ci = IN_CH[cid]
+        for j, (k, e, co, se, _) in enumerate(MBV3_TAIL):
+            p = f"b{j}"
+            conv(p + ".expand", e, ci, 1, bias=False)
+            norm(p + ".bn1", e)
+            out.append((p + ".dw.w", (e, k, k, 1)))
+            norm(p + ".bn2", e)
+            if se:
+                lin(p + ".se.fc1", se_width(e), e)
+                lin(p + ".se.fc2", e, se_width(e))
+            conv(p + ".proj", co, e, 1, bias=False)
+            norm(p + ".bn3", co)
+            ci = co
+        conv("last", 960, ci, 1, bias=False)
+        norm("last_bn", 960)
+        lin("fc1", 1280, 960)
+        lin("fc2", CLASSES[cid], 1280)
     elif fam == "vgg5":
         # the server part of VGG-5 (Table 4) after its second pool: CONV-3-64 with
         # batch norm (no bias), pool, FC-128, FC-X on [64, 8, 8] inputs
@@ -361,6 +390,85 @@ class Bert(_Net):
         self.G = G
 
 
+class Bottleneck:
+    """MobileNetV3 bottleneck: expansion 1x1 conv, BN, hard-swish; depthwise
+    k x k conv (stride s), BN, hard-swish; squeeze-excitation (global mean,
+    fc, ReLU, fc, hard-sigmoid, channel scale) when present; projection 1x1
+    conv, BN; plus the input when the stride is 1 and the widths agree."""
+
+    def __init__(self, P, p, k, e, ci, co, se, stride):
+        self.p, self.se, self.res = p, se, stride == 1 and ci == co
+        self.ex = Lyr.Conv2d(P[p + ".expand.w"], None, pad=0)
+        self.bn1, self.a1 = Lyr.BatchNorm2d(P[p + ".bn1.g"], P[p + ".bn1.b"]), Lyr.HardSwish()
+        self.dw = Lyr.DepthwiseConv2d(P[p + ".dw.w"], stride)
+        self.bn2, self.a2 = Lyr.BatchNorm2d(P[p + ".bn2.g"], P[p + ".bn2.b"]), Lyr.HardSwish()
+        if se:
+            self.f1, self.r = Lyr.Linear(P[p + ".se.fc1.w"], P[p + ".se.fc1.b"]), Lyr.ReLU()
+            self.f2, self.hs = Lyr.Linear(P[p + ".se.fc2.w"], P[p + ".se.fc2.b"]), Lyr.HardSigmoid()
+        self.pr = Lyr.Conv2d(P[p + ".proj.w"], None, pad=0)
+        self.bn3 = Lyr.BatchNorm2d(P[p + ".bn3.g"], P[p + ".bn3.b"])
+
+    def fwd(self, x):
+        h = self.a2.fwd(self.bn2.fwd(self.dw.fwd(self.a1.fwd(self.bn1.fwd(self.ex.fwd(x))))))
+        if self.se:
+            self.h = h
+            self.s = self.hs.fwd(self.f2.fwd(self.r.fwd(self.f1.fwd(h.mean(axis=(2, 3))))))
+            h = h * self.s[:, :, None, None]
+        y = self.bn3.fwd(self.pr.fwd(h))
+        return y + x if self.res else y
+
+    def bwd(self, dy, need_dx, G):
+        p = self.p
+        dh = self.pr.bwd(self.bn3.bwd(dy))
+        G[p + ".proj.w"], G[p + ".bn3.g"], G[p + ".bn3.b"] = self.pr.dw, self.bn3.dg, self.bn3.db
+        if self.se:
+            h, s = self.h, self.s
+            ds = (dh * h).sum(axis=(2, 3))
+            dm = self.f1.bwd(self.r.bwd(self.f2.bwd(self.hs.bwd(ds))))
+            G[p + ".se.fc1.w"], G[p + ".se.fc1.b"] = self.f1.dw, self.f1.db
+            G[p + ".se.fc2.w"], G[p + ".se.fc2.b"] = self.f2.dw, self.f2.db
+            dh = dh * s[:, :, None, None] + dm[:, :, None, None] / (h.shape[2] * h.shape[3])
+        dh = self.dw.bwd(self.bn2.bwd(self.a2.bwd(dh)))
+        G[p + ".dw.w"], G[p + ".bn2.g"], G[p + ".bn2.b"] = self.dw.dw, self.bn2.dg, self.bn2.db
+        dx = self.ex.bwd(self.bn1.bwd(self.a1.bwd(dh)), need_dx)
+        G[p + ".expand.w"], G[p + ".bn1.g"], G[p + ".bn1.b"] = self.ex.dw, self.bn1.dg, self.bn1.db
+        if not need_dx:
+            return None
+        return dx + dy if self.res else dx
+
+
+class MBV3Server(_Net):
+    """MobileNetV3-Large after its seventh bottleneck: eight bottlenecks, conv
+    1x1 to 960 + BN + hard-swish, global mean, fc 1280 + hard-swish, fc X."""
+
+    def __init__(self, P, cid):
+        self.blocks, ci = [], IN_CH[cid]
+        for j, (k, e, co, se, st) in enumerate(MBV3_TAIL):
+            self.blocks.append(Bottleneck(P, f"b{j}", k, e, ci, co, se, st))
+            ci = co
+        self.last = Lyr.Conv2d(P["last.w"], None, pad=0)
+        self.lbn, self.la = Lyr.BatchNorm2d(P["last_bn.g"], P["last_bn.b"]), Lyr.HardSwish()
+        self.gap = Lyr.GlobalAvgPool()
+        self.fc1, self.fa, self.fc2 = Lyr.Linear(P["fc1.w"], P["fc1.b"]), Lyr.HardSwish(), Lyr.Linear(P["fc2.w"], P["fc2.b"])
+
+    def fwd(self, x, lengths=None):
+        h = x
+        for b in self.blocks:
+            h = b.fwd(h)
+        g = self.gap.fwd(self.la.fwd(self.lbn.fwd(self.last.fwd(h))))
+        return self.fc2.fwd(self.fa.fwd(self.fc1.fwd(g)))
+
+    def bwd(self, dz):
+        G = {}
+        dg = self.fc1.bwd(self.fa.bwd(self.fc2.bwd(dz)))
+        G["fc2.w"], G["fc2.b"], G["fc1.w"], G["fc1.b"] = self.fc2.dw, self.fc2.db, self.fc1.dw, self.fc1.db
+        dh = self.last.bwd(self.lbn.bwd(self.la.bwd(self.gap.bwd(dg))))
+        G["last.w"], G["last_bn.g"], G["last_bn.b"] = self.last.dw, self.lbn.dg, self.lbn.db
+        for i in range(len(self.blocks) - 1, -1, -1):
+            dh = self.blocks[i].bwd(dh, i > 0, G)
+        self.G = G
+
+
 class VGG5Server(_Net):
     """conv3x3 (no bias) -> BN (train) -> ReLU -> maxpool 2x2 -> flatten (C, H, W)
     -> fc1 -> ReLU -> fc2."""
@@ -416,6 +524,8 @@ def build(cid, P):
         return SmallTransformer(P, cid)
     if fam == "vgg5":
         return VGG5Server(P)
+    if fam == "mbv3":
+        return MBV3Server(P, cid)
     if fam == "cnn":
         return CNN(P)
     if fam == "vgg_device":

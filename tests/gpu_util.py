@@ -25,12 +25,18 @@ def normwise(got, ref):
     return 0.0 if scale == 0.0 and err == 0.0 else err / max(scale, 1e-300)
 
 
-def per_tensor_errors(cid, got_flat, ref_flat):
+def per_tensor_errors(cid, got_flat, ref_flat, floor=0.0):
+    """normwise error per parameter tensor; with floor > 0 a tensor's scale is
+    at least floor times the largest gradient entry of the whole model (for
+    gradients that are zero by construction and hold round-off only)."""
     import fo_synth as S
     out, off = {}, 0
+    gscale = float(np.abs(np.asarray(ref_flat, np.float64)).max()) if floor > 0 else 0.0
     for name, shape, _, _ in S.param_layout(cid):
         n = int(np.prod(shape))
-        out[name] = normwise(got_flat[off:off + n], ref_flat[off:off + n])
+        got, ref = np.asarray(got_flat[off:off + n], np.float64), np.asarray(ref_flat[off:off + n], np.float64)
+        scale = max(np.abs(ref).max(), floor * gscale)
+        out[name] = np.abs(got - ref).max() / max(scale, 1e-300)
         off += n
     return out
 

@@ -14,7 +14,7 @@ import oracle
 from oracle import nets
 from tests import torch_ref
 
-SMALL_B = {1: 3, 2: 2, 3: 4, 4: 2, 5: 2, 6: 2, 7: 3, 8: 2, 9: 3}
+SMALL_B = {1: 3, 2: 2, 3: 4, 4: 2, 5: 2, 6: 2, 7: 3, 8: 2, 9: 3, 10: 3}
 
 
 def _inputs(cid, B, sub=7):
@@ -24,7 +24,7 @@ def _inputs(cid, B, sub=7):
     return acts, labels, lengths
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5, 6, 7, 8, 9])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5, 6, 7, 8, 9, 10])
 def test_layout_matches_workload(cid):
     a = [(n, tuple(s)) for n, s in nets.param_layout(cid)]
     b = [(n, tuple(s)) for n, s, _, _ in S.param_layout(cid)]
@@ -32,7 +32,7 @@ def test_layout_matches_workload(cid):
     assert sum(int(np.prod(s)) for _, s in a) == S.param_count(cid)
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4, 6, 7, 8, 9])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 6, 7, 8, 9, 10])
 def test_step_matches_independent_autograd(cid):
     B = SMALL_B[cid]
     theta = S.init_params(cid)
@@ -42,18 +42,22 @@ def test_step_matches_independent_autograd(cid):
     tl, tz, tg = torch_ref.step(cid, theta, x, labels, lengths)
     assert abs(r["loss"] - tl) <= 1e-12 * abs(tl)
     np.testing.assert_allclose(r["logits"], tz, rtol=0, atol=1e-11 * np.abs(tz).max())
-    # every gradient entry, normwise per tensor
+    # every gradient entry, normwise per tensor; a tensor whose gradient is zero
+    # by construction (the bias of a batch norm whose output reaches the loss
+    # only through later batch norms: config 10's first three bottlenecks) holds
+    # round-off on both sides, so scales have a floor of 1e-6 of the largest
     off = 0
+    gscale = np.abs(tg).max()
     for name, shape, _, _ in S.param_layout(cid):
         n = int(np.prod(shape))
         g, t = r["grads"][off:off + n], tg[off:off + n]
-        scale = np.abs(t).max()
+        scale = max(np.abs(t).max(), 1e-6 * gscale)
         assert np.abs(g - t).max() <= 1e-9 * scale + 1e-300, name
         off += n
     np.testing.assert_allclose(r["params"], theta - 0.01 * r["grads"], rtol=1e-15, atol=1e-18)
 
 
-@pytest.mark.parametrize("cid,n_probe", [(1, 12), (3, 10), (6, 12), (7, 12), (9, 12)])
+@pytest.mark.parametrize("cid,n_probe", [(1, 12), (3, 10), (6, 12), (7, 12), (9, 12), (10, 12)])
 def test_step_gradient_finite_differences(cid, n_probe):
     B = 2
     theta = S.init_params(cid).astype(np.float64)
@@ -75,7 +79,7 @@ def test_step_gradient_finite_differences(cid, n_probe):
         assert abs(num - r["grads"][i]) <= 1e-6 * gmax, (i, num, r["grads"][i])
 
 
-@pytest.mark.parametrize("cid,C", [(1, 10), (2, 10), (3, 100), (4, 2), (6, 10), (7, 2), (8, 2), (9, 10)])
+@pytest.mark.parametrize("cid,C", [(1, 10), (2, 10), (3, 100), (4, 2), (6, 10), (7, 2), (8, 2), (9, 10), (10, 200)])
 def test_zero_classifier_gives_ln_c(cid, C):
     theta = S.init_params(cid).astype(np.float64)
     lay = S.param_layout(cid)

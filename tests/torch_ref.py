@@ -52,6 +52,30 @@ def forward(cid, P, x, lengths=None):
                 sc = bn(F.conv2d(h, _w4(P[p + ".ds.w"]), stride=2), p + ".dsbn") if bi == 0 else h
                 h = F.relu(o + sc)
         return F.linear(h.mean((2, 3)), P["fc.w"], P["fc.b"])
+    if cid == 10:
+        from oracle.nets import MBV3_TAIL
+
+        def hswish(t):  # x ReLU6(x + 3) / 6, differentiated exactly by autograd
+            return t * torch.clamp(t + 3.0, 0.0, 6.0) / 6.0
+
+        def hsigmoid(t):
+            return torch.clamp(t + 3.0, 0.0, 6.0) / 6.0
+
+        def bn(h, n):
+            return F.batch_norm(h, None, None, P[n + ".g"], P[n + ".b"], training=True, eps=1e-5)
+        h, ci = x, 80
+        for j, (k, e, co, se, st) in enumerate(MBV3_TAIL):
+            p = f"b{j}"
+            t = hswish(bn(F.conv2d(h, _w4(P[p + ".expand.w"])), p + ".bn1"))
+            t = hswish(bn(F.conv2d(t, _w4(P[p + ".dw.w"]), stride=st, padding=k // 2, groups=e), p + ".bn2"))
+            if se:
+                sq = F.relu(F.linear(t.mean((2, 3)), P[p + ".se.fc1.w"], P[p + ".se.fc1.b"]))
+                t = t * hsigmoid(F.linear(sq, P[p + ".se.fc2.w"], P[p + ".se.fc2.b"]))[:, :, None, None]
+            t = bn(F.conv2d(t, _w4(P[p + ".proj.w"])), p + ".bn3")
+            h = t + h if st == 1 and ci == co else t
+            ci = co
+        h = hswish(bn(F.conv2d(h, _w4(P["last.w"])), "last_bn")).mean((2, 3))
+        return F.linear(hswish(F.linear(h, P["fc1.w"], P["fc1.b"])), P["fc2.w"], P["fc2.b"])
     if cid == 9:
         h = F.batch_norm(F.conv2d(x, _w4(P["conv.w"]), padding=1), None, None, P["bn.g"], P["bn.b"],
                          training=True, eps=1e-5)
