@@ -1,6 +1,6 @@
 """Benchmark of the FedOptima server hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..9, default 4] [--pipeline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..10, default 4] [--pipeline]
 
 One step = one pass of the server's hot path over one activation batch:
 an arriving batch is copied into the HBM activation pool (Alg. 2 put() with
@@ -45,8 +45,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (transformer 5, 128-device VGG 10)")
     ap.add_argument("--config", type=int, default=4, help="1-3: the parity workloads' step loops; 4: "
                     "transformer (default); 5: 128-device VGG with Poisson arrivals; 6: the device-side "
-                    "iteration of the VGG split; 7, 8, 9: the paper's Transformer-6 / Transformer-12 / VGG-5 "
-                    "server parts")
+                    "iteration of the VGG split; 7, 8, 9, 10: the paper's Transformer-6 / Transformer-12 / VGG-5 / "
+                    "MobileNetV3-Large server parts")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pipeline", action="store_true",
                     help="the concurrent pipeline (Receiver and Compute Engine threads) on the 128-device VGG "
@@ -359,7 +359,23 @@ WORKLOADS = {
                     "batch 32 of [64,8,8], 8 devices",
         # the convolution's forward and weight gradient (no input gradient), both fc layers three times
         "peak": PEAK_F32_TFLOPS, "gflop": 32 * (2 * 2 * 64 * 576 * 64 + 3 * (2 * 1024 * 128 + 2 * 128 * 10)) / 1e9},
+    10: {"workload": "MobileNetV3-Large split server step (fp32): 8 bottlenecks (depthwise conv, squeeze-excitation, "
+                     "hard-swish), conv1x1 960, pool, fc 960-1280-200, batch 32 of [80,4,4], 16 devices",
+         "peak": PEAK_F32_TFLOPS, "gflop": None},
 }
+
+
+def mbv3_gflop():
+    """FLOPs of the MobileNetV3 step (config 10, batch 32) from the
+    pre-processor's unit table of MobileNetV3-Large at 64x64: the forward of the
+    units after the split, three times, less the first unit's input gradient
+    (its expansion product)."""
+    import ctypes  # noqa: F401
+    from paper_2504_13850_amd import api as A
+    units = A.fo_net_units(A.FO_NET_MOBILENETV3_LARGE, 200, 64)
+    fwd = sum(u.fwd_flops for u in list(units)[8:])
+    first_dx = 2 * 80 * 200 * 16  # expansion of the first server block: 80 -> 200 channels on 4x4
+    return 32 * (3 * fwd - first_dx) / 1e9
 
 
 def tfsmall_gflop(cid):
@@ -697,7 +713,7 @@ def main():
         bench_vgg128(args, A, torch, S)
         return
     if cid not in WORKLOADS:
-        raise SystemExit("bench.py: --config 1..9 (4, the transformer, is the default)")
+        raise SystemExit("bench.py: --config 1..10 (4, the transformer, is the default)")
     args.steps = 30 if args.steps is None else args.steps
     args.warmup = 5 if args.warmup is None else args.warmup
     cfg = S.get_config(cid)
@@ -783,7 +799,7 @@ def main():
     # the workload's fixed count where its kernels carry no records (fp32 CNN)
     alg_flops = sum(s["flops"] for s in stats)
     mfma_flops = sum(s["mfma_flops"] for s in stats)
-    gflop = wl["gflop"] if wl["gflop"] is not None else tfsmall_gflop(cid)
+    gflop = wl["gflop"] if wl["gflop"] is not None else (tfsmall_gflop(cid) if cid in (7, 8) else mbv3_gflop())
     flops_step = alg_flops / args.steps if alg_flops else gflop * 1e9
     mfu = flops_step / (ms_step * 1e-3) / (peak * 1e12)
     gemms = [s for s in stats if s["name"].startswith("gemm")]

@@ -31,6 +31,7 @@ int64_t bert_param_count();
 int64_t device_param_count();
 int64_t tfsmall_param_count(int32_t cid);
 int64_t vgg5_param_count();
+int64_t mbv3_param_count();
 
 }  // namespace fo
 
@@ -46,6 +47,7 @@ extern "C" int64_t fo_config_param_count(int32_t cid) {
         case 6: return device_param_count();
         case 7: case 8: return tfsmall_param_count(cid);
         case 9: return vgg5_param_count();
+        case 10: return mbv3_param_count();
         default: return -1;
     }
 }
@@ -55,6 +57,7 @@ extern "C" int32_t fo_config_num_classes(int32_t cid) {
         case 1: case 2: case 5: case 6: case 9: return 10;
         case 3: return 100;
         case 4: case 7: case 8: return 2;
+        case 10: return 200;
         default: return -1;
     }
 }
@@ -68,6 +71,7 @@ static const Family* family_of(int32_t cid) {
         case 7: return family_tfsmall7();
         case 8: return family_tfsmall8();
         case 9: return family_vgg5();
+        case 10: return family_mbv3();
         default: return nullptr;
     }
 }
@@ -92,7 +96,7 @@ extern "C" fo_status fo_model_create(int32_t cid, int32_t max_batch, const float
     m->n_params = np;
     m->momentum = cid == 3 ? 0.9f : 0.f;
     m->fam = fam;
-    const bool bf16 = cid != 1 && cid != 7 && cid != 8 && cid != 9;  // fp32 configs keep no bf16 shadows
+    const bool bf16 = cid != 1 && cid < 7;  // the fp32 configs (1, 7-10) keep no bf16 shadows
     size_t bytes = 0;
     auto add = [&](size_t b) { bytes += (b + 255) & ~size_t(255); };
     add(sizeof(float) * np);                          // params

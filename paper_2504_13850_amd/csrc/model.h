@@ -72,5 +72,6 @@ const Family* family_device();  // config 6 (device side of configs 2 and 5)
 const Family* family_tfsmall7();  // config 7 (Transformer-6 after its embedding)
 const Family* family_tfsmall8();  // config 8 (Transformer-12 after its embedding)
 const Family* family_vgg5();      // config 9 (VGG-5 after its second pool)
+const Family* family_mbv3();      // config 10 (MobileNetV3-Large after its seventh bottleneck)
 
 }  // namespace fo

@@ -51,7 +51,7 @@ def _eager_noise(torch, step):
     return float(a.sum().item())
 
 
-@pytest.mark.parametrize("cid,Bmax", [(1, 8), (2, 8), (3, 8), (4, 6), (5, 8), (6, 8), (7, 8), (8, 4), (9, 8)])
+@pytest.mark.parametrize("cid,Bmax", [(1, 8), (2, 8), (3, 8), (4, 6), (5, 8), (6, 8), (7, 8), (8, 4), (9, 8), (10, 8)])
 def test_graph_replay_matches_direct_launches(cid, Bmax):
     torch = torch_cuda()
     cfg = S.get_config(cid)

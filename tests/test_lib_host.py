@@ -37,10 +37,10 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_param_counts_and_classes():
-    for cid in range(1, 10):
+    for cid in range(1, 11):
         assert A.fo_config_param_count(cid) == S.param_count(cid)
         assert A.fo_config_num_classes(cid) == S.get_config(cid).n_classes
-    assert A.fo_config_param_count(10) == -1
+    assert A.fo_config_param_count(11) == -1
 
 
 def _lib_trace(name, K, n_slots, with_slot, policy=None):
