@@ -106,8 +106,8 @@ GEMM_SOURCES = ["paper_2504_13850_amd/csrc/k_gemm.hip", "paper_2504_13850_amd/cs
 TRAFFIC_KERNELS = {
     # compensated forward products, input gradients, weight gradients of the transformer step
     "gemm_comp_dma_kernel<3>": ("gemm_comp_dma_kernel<3, 2, fo::(anonymous namespace)::DmaRKc>", GEMM_SOURCES),
-    "gemm_kernel<0, 6>": ("gemm_kernel<0, 6, true>", GEMM_SOURCES),
-    "gemm_group_kernel<6, 6>": ("gemm_group_kernel<6, 6, true>", GEMM_SOURCES),
+    "gemm_rk_krt_dma_kernel": ("gemm_rk_krt_dma_kernel<4>", GEMM_SOURCES),
+    "gemm_wgrad_dma_kernel": ("gemm_wgrad_dma_kernel<32, 4>", GEMM_SOURCES),
     "agg_lerp_kernel": ("agg_lerp_kernel(", ["paper_2504_13850_amd/csrc/k_update.hip"]),
 }
 CALIB_BYTES = 1 << 30
@@ -254,6 +254,31 @@ def summarize_counters(paths, top=12):
     for _, name, v in rows[:top]:
         cells = [("-" if v[k] is None else f.format(v[k])) for k, _, f in cols]
         out.append(f"| `{name}` | " + " | ".join(cells) + " |")
+    # latency passes, when given: average cycles of an L1 -> L2 read
+    # (TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ), of an L2 -> fabric read
+    # (TCC_EA0_RDREQ_LEVEL / TCC_EA0_RDREQ), the fraction of wave cycles spent
+    # waiting (SQ_WAIT_ANY, SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES) and the vector
+    # memory instructions in flight per wave (SQ_INST_LEVEL_VMEM / SQ_INSTS_VMEM_RD)
+    lat = []
+    for _, name, _v in rows[:top]:
+        c = per[name]
+        g = lambda k: mean(c[k]) if c.get(k) else None
+        ratio = lambda a, b: (g(a) / g(b)) if g(a) is not None and g(b) else None
+        v = {"l1l2": ratio("TCP_TCC_READ_REQ_LATENCY_sum", "TCP_TCC_READ_REQ_sum"),
+             "ea": ratio("TCC_EA0_RDREQ_LEVEL_sum", "TCC_EA0_RDREQ_sum"),
+             "wait": ratio("SQ_WAIT_ANY", "SQ_WAVE_CYCLES"), "wait_inst": ratio("SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES"),
+             "vmem_level": ratio("SQ_INST_LEVEL_VMEM", "SQ_INSTS_VMEM_RD"),
+             "lds_fifo": g("SQ_LDS_DATA_FIFO_FULL")}
+        if any(x is not None for x in v.values()):
+            lat.append((name, v))
+    if lat:
+        lc = [("l1l2", "L1->L2 read latency (cyc)", "{:.0f}"), ("ea", "L2->fabric read latency (cyc)", "{:.0f}"),
+              ("wait", "wave cycles waiting", "{:.2f}"), ("wait_inst", "waiting to issue", "{:.2f}"),
+              ("vmem_level", "vector memory ops in flight per issue", "{:.0f}"),
+              ("lds_fifo", "LDS data FIFO full (cyc)", "{:.3g}")]
+        out += ["", "| kernel | " + " | ".join(h for _, h, _ in lc) + " |", "|---|" + "---:|" * len(lc)]
+        for name, v in lat:
+            out.append(f"| `{name}` | " + " | ".join("-" if v[k] is None else f.format(v[k]) for k, _, f in lc) + " |")
     return "\n".join(out)
 
 

@@ -26,6 +26,11 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
+// Rings of the kernels with copies into LDS: weight gradients in 32-deep K
+// tiles, four stages; input gradients four stages (64 KB of LDS each, two
+// workgroups per CU: deeper rings at one workgroup per CU starve the
+// concurrent input-gradient chain of LDS).
+constexpr int kWgradKT = 32, kWgradNST = 4, kDgradNST = 4;
 constexpr int NV = BM * BK / 8 / NT;  // 16-byte vectors per thread per operand per K tile (4)
 
 // LDS tiles are 128 rows x 64 k with rows padded to 72 elements (144 B = 36
@@ -955,9 +960,9 @@ struct GemmGroupArg {
     int* prof_snap;  // (M, K) effective per member, when profiling
 };
 
-template <int AM, int BMODE, bool AL>
-__global__ void __launch_bounds__(NT, 2) gemm_group_kernel(const GemmGroupArg g) {
-    __shared__ __attribute__((aligned(16))) GemmSmem smem;
+// Calls f(d, job, M, K) for each tile of a group that this workgroup owns.
+template <class F>
+__device__ __forceinline__ void for_group_tiles(const GemmGroupArg& g, F&& f) {
     constexpr int GM = 8;
     int Ms[kGemmGroupMax], Ks[kGemmGroupMax], start[kGemmGroupMax + 1];
     start[0] = 0;
@@ -1004,9 +1009,17 @@ __global__ void __launch_bounds__(NT, 2) gemm_group_kernel(const GemmGroupArg g)
         job.n0 = (tg / gr) * BN;
         job.zt = 0;
         job.S = 1;
-        gemm_tile<AM, BMODE, AL>(d, job, Mm, Km, smem);
+        f(d, job, Mm, Km);
         __syncthreads();  // the next tile's stores reuse the LDS of this one's C tile
     }
+}
+
+template <int AM, int BMODE, bool AL>
+__global__ void __launch_bounds__(NT, 2) gemm_group_kernel(const GemmGroupArg g) {
+    __shared__ __attribute__((aligned(16))) GemmSmem smem;
+    for_group_tiles(g, [&](const GemmDesc& d, const TileJob& job, int M, int K) {
+        gemm_tile<AM, BMODE, AL>(d, job, M, K, smem);
+    });
 }
 
 // ------------------------------------------------------------------ single-pass compensated product
@@ -1211,6 +1224,281 @@ __global__ void __launch_bounds__(NT, NST == 2 ? 2 : 1) gemm_comp_dma_kernel(con
     store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
 }
 
+// ------------------------------------------------------------------ weight gradients, copies into LDS
+// The transpose reads of this kernel are written as inline assembly: with the
+// intrinsic, the compiler waits for every copy into LDS still in flight
+// (vmcnt(0)) before each read, which would leave one stage of the ring in use.
+// The compiler does not track these reads, so their results are used only
+// after lgkm_wait_tr, whose operands tie the registers to the wait.
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16_t*)p;
+}
+__device__ __forceinline__ i32x2_t tr_read(uint32_t addr) {
+    i32x2_t v;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+}
+// waits until at most 8 n (n = 0, 1) LDS operations are in flight (the reads
+// of the next k block; LDS operations complete in order) and hands r on
+__device__ __forceinline__ void lgkm_wait_tr(i32x2_t (&r)[8], int n) {
+    if (n)
+        asm volatile("s_waitcnt lgkmcnt(8)"
+                     : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7]));
+    else
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7]));
+}
+__device__ __forceinline__ bf16x8_t frag_cat(i32x2_t a, i32x2_t b) {
+    const i32x4_t v = {a.x, a.y, b.x, b.y};
+    return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// Both operands k-major (A = [K][M], B = [K][N], the rows of a tile contiguous
+// in memory), as in the products of weight gradients.  The tiles keep the
+// [k][row] layout of the transposed loaders (kr_idx) that the transpose reads
+// take their fragments from, but are filled by global_load_lds: instruction i
+// of the workgroup writes k rows 4i .. 4i + 3, lane L its 16-byte slot L of
+// them, which under the swizzle is k row 4i + L / 16 and the eight rows
+// 8 ((L mod 16) xor 4 (L / 16)) .. + 7.  No staging registers and no LDS store
+// instructions; the waits name exactly the tile the next step reads.
+template <int KT>
+struct DmaKRt {
+    static_assert(KT % 32 == 0 && KT <= 64, "tile depth");
+    static constexpr int NI = KT / 16;  // instructions per wave and operand tile (KT / 4 per workgroup)
+    int64_t off[NI];                    // element offset of the lane's chunk at k = 0, -1 outside the rows
+    int64_t ld;
+    int kk[NI];
+    __device__ void init(int64_t ld_, int r0, int R, int lane, int wave) {
+        ld = ld_;
+        const int sub = lane >> 4, r = r0 + 8 * ((lane & 15) ^ (4 * sub));
+#pragma unroll
+        for (int v = 0; v < NI; ++v) {
+            kk[v] = 4 * (wave + 4 * v) + sub;
+            off[v] = r < R ? (int64_t)kk[v] * ld + r : -1;
+        }
+    }
+    __device__ void copy(const bf16_t* P, int kb, int kend, bf16_t* tile, int wave) const {
+        const int64_t kofs = (int64_t)kb * ld;
+#pragma unroll
+        for (int v = 0; v < NI; ++v)
+            __builtin_amdgcn_global_load_lds(off[v] >= 0 && kb + kk[v] < kend ? P + off[v] + kofs : kZero8,
+                                             FO_LDS(tile + (wave + 4 * v) * 512), 16, 0, 0);
+    }
+};
+
+// One 128 x 128 tile of a weight-gradient product over its whole K, NST stages
+// of KT-deep tiles in a ring (the copy of tile t + NST - 1 issued before the
+// MFMAs of tile t; every copy issued, past the last tile too, so that the
+// number in flight is static).  The stages (NST x 2 x KT x 128 bf16) hold the
+// fp32 C tile afterwards.
+template <int KT, int NST>
+__device__ __forceinline__ void wgrad_tile(const GemmDesc& d, const TileJob& job, int M, int K,
+                                           bf16_t (*smem)[2][KT * BM]) {
+    static_assert(NST * 2 * KT * BM * 2 >= BM * BN * 4, "the C tile lives in the stages");
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int nk = (K + KT - 1) / KT;
+    DmaKRt<KT> la, lb;
+    la.init(d.lda, job.m0, M, lane, wave);
+    lb.init(d.ldb, job.n0, d.N, lane, wave);
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    constexpr int CPT = 2 * DmaKRt<KT>::NI;  // copy instructions per tile and thread
+    auto copy_tile = [&](int st, int t) {
+        const int kb = t * KT, ke = t < nk ? K : 0;
+        la.copy(d.A, kb, ke, smem[st][0], wave);
+        lb.copy(d.B, kb, ke, smem[st][1], wave);
+    };
+    // byte addresses in LDS of this lane's transpose reads for k block 0 of
+    // stage 0: A fragments i = 0, 1 (first and second four k), then B fragments
+    const uint32_t sbase = lds_addr(&smem[0][0][0]);
+    uint32_t ra[8];
+    {
+        const int2 o[4] = {frag_tr_off(lane, wm * 64), frag_tr_off(lane, wm * 64 + 32), frag_tr_off(lane, wn * 64),
+                           frag_tr_off(lane, wn * 64 + 32)};
+#pragma unroll
+        for (int f = 0; f < 4; ++f) {
+            const uint32_t op = f < 2 ? 0u : (uint32_t)(KT * BM * 2);
+            ra[2 * f] = sbase + op + 2 * o[f].x;
+            ra[2 * f + 1] = sbase + op + 2 * o[f].y;
+        }
+    }
+    // k blocks in pairs: the sixteen reads of a pair are issued together, the
+    // first block's MFMAs wait for its eight (lgkmcnt counts up to 15)
+    auto compute = [&](int st) {
+        const uint32_t so = (uint32_t)st * (2 * KT * BM * 2);
+#pragma unroll
+        for (int kp = 0; kp < KT / 32; ++kp) {
+            i32x2_t r[2][8];
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int q = 0; q < 8; ++q) r[h][q] = tr_read(ra[q] + so + (2 * kp + h) * 16 * BM * 2);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                lgkm_wait_tr(r[h], 1 - h);
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            frag_cat(r[h][2 * i], r[h][2 * i + 1]), frag_cat(r[h][4 + 2 * j], r[h][5 + 2 * j]),
+                            acc[i][j], 0, 0, 0);
+            }
+        }
+    };
+    auto step = [&](int t, int u) {
+        copy_tile((u + NST - 1) % NST, t + NST - 1);
+        compute(u);
+        __builtin_amdgcn_s_waitcnt(vmcnt_lds0_imm(CPT * (NST - 2)));  // tile t + 1 has landed
+        ring_barrier();
+    };
+#pragma unroll
+    for (int u = 0; u < NST - 1; ++u) copy_tile(u, u);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));  // tile 0 has landed
+    ring_barrier();
+    int t = 0;
+    for (; t + NST <= nk; t += NST) {  // whole rounds: static stage indices
+#pragma unroll
+        for (int u = 0; u < NST; ++u) step(t + u, u);
+    }
+    for (int u = 0; t < nk; ++t, ++u) step(t, u);
+    __builtin_amdgcn_s_waitcnt(0);  // copies past the last tile
+    __syncthreads();
+    store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
+}
+
+template <int KT, int NST>
+__global__ void __launch_bounds__(NT, 2) gemm_wgrad_dma_kernel(const GemmGroupArg g) {
+    __shared__ __attribute__((aligned(1024))) bf16_t smem[NST][2][KT * BM];
+    for_group_tiles(g, [&](const GemmDesc& d, const TileJob& job, int M, int K) {
+        wgrad_tile<KT, NST>(d, job, M, K, smem);
+    });
+}
+
+// ------------------------------------------------------------------ input gradients, copies into LDS
+// C = A B with A row-major (k contiguous) and B k-major ([K][N], the rows of
+// the tile contiguous), as in the input gradients dX = dY W: A in the 128 x 32
+// tile layout of DmaRKc (its fragments by plain LDS reads), B in the [32 k][128
+// row] layout of DmaKRt (its fragments by transpose reads), NST stages in a
+// ring as in gemm_comp_dma_kernel; split-K slices and the epilogue as in
+// gemm_kernel.
+__device__ __forceinline__ void lgkm_wait_tr4(i32x2_t (&r)[4], int n) {
+    if (n)
+        asm volatile("s_waitcnt lgkmcnt(4)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]));
+    else
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]));
+}
+
+template <int NST>
+__global__ void __launch_bounds__(NT, 2) gemm_rk_krt_dma_kernel(const GemmDesc d) {
+    constexpr int KT = CBK;
+    // NST stages of an A tile (128 x 32) and a B tile (32 x 128), 16 KB each;
+    // reused for the C tile (64 KB)
+    __shared__ __attribute__((aligned(1024))) bf16_t smem[NST][2][BM * KT];
+    static_assert(NST * 2 * KT * BM * 2 >= BM * BN * 4, "the C tile lives in the stages");
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int M = d.Mdev ? min(d.M, *d.Mdev) : d.M;
+    const int K = d.K;
+    if (d.prof_snap && (blockIdx.x | blockIdx.y | blockIdx.z) == 0 && tid == 0) {
+        d.prof_snap[0] = M;
+        d.prof_snap[1] = K;
+    }
+    TileJob job;
+    if (!map_tile(d, M, K, job)) return;  // uniform for the whole workgroup
+    const int S = job.S;
+    const int kpad = (K + KT - 1) / KT * KT;
+    const int kc = ((kpad + S - 1) / S + KT - 1) / KT * KT;
+    const int kbeg = job.zt * kc;
+    const int kstop = min(kpad, kbeg + kc);
+    const int nk = kstop > kbeg ? (kstop - kbeg) / KT : 0;
+
+    DmaRKc la;
+    DmaKRt<KT> lb;
+    la.init(d.lda, job.m0, M, lane, wave);
+    lb.init(d.ldb, job.n0, d.N, lane, wave);
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    constexpr int CPT = 2 + DmaKRt<KT>::NI;  // copy instructions per tile and thread
+    auto copy_tile = [&](int st, int t) {
+        const int kb = kbeg + t * KT, ke = t < nk ? K : 0;
+        la.copy(d.A, kb, ke, smem[st][0], wave);
+        lb.copy(d.B, kb, ke, smem[st][1], wave);
+    };
+    const int lrow = lane & 31, lc = lane >> 5;
+    // byte addresses in LDS of this lane's B transpose reads for k block 0 of stage 0
+    uint32_t rb[4];
+    {
+        const uint32_t b0 = lds_addr(&smem[0][1][0]);
+        const int2 o0 = frag_tr_off(lane, wn * 64), o1 = frag_tr_off(lane, wn * 64 + 32);
+        rb[0] = b0 + 2 * o0.x;
+        rb[1] = b0 + 2 * o0.y;
+        rb[2] = b0 + 2 * o1.x;
+        rb[3] = b0 + 2 * o1.y;
+    }
+    auto compute = [&](int st) {
+        const bf16_t* At = smem[st][0];
+        const uint32_t so = (uint32_t)st * (2 * KT * BM * 2);
+        i32x2_t r[2][4];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) r[h][q] = tr_read(rb[q] + so + h * 16 * BM * 2);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            bf16x8_t a[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int row = wm * 64 + i * 32 + lrow, C = 2 * ks + lc;
+                a[i] = *reinterpret_cast<const bf16x8_t*>(&At[row * KT + 8 * (C ^ ((row >> 2) & 3))]);
+            }
+            lgkm_wait_tr4(r[ks], 1 - ks);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], frag_cat(r[ks][2 * j], r[ks][2 * j + 1]),
+                                                                       acc[i][j], 0, 0, 0);
+        }
+    };
+    auto step = [&](int t, int u) {
+        copy_tile((u + NST - 1) % NST, t + NST - 1);
+        compute(u);
+        __builtin_amdgcn_s_waitcnt(vmcnt_lds0_imm(CPT * (NST - 2)));  // tile t + 1 has landed
+        ring_barrier();
+    };
+#pragma unroll
+    for (int u = 0; u < NST - 1; ++u) copy_tile(u, u);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));  // tile 0 has landed
+    ring_barrier();
+    int t = 0;
+    for (; t + NST <= nk; t += NST) {
+#pragma unroll
+        for (int u = 0; u < NST; ++u) step(t + u, u);
+    }
+    for (int u = 0; t < nk; ++t, ++u) step(t, u);
+    __builtin_amdgcn_s_waitcnt(0);  // copies past the last tile
+    __syncthreads();
+    store_tile(d, acc, reinterpret_cast<float*>(&smem[0][0][0]), job, M, tid);
+}
+
 // Sums the split-K partials and runs the epilogue; four columns per thread
 // when N % 4 == 0, with the slices loaded four at a time.
 __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
@@ -1276,6 +1564,20 @@ void launch_comp(const GemmDesc& d, hipStream_t s) {
     prof_end_ext(h);
 }
 
+void launch_rk_krt(const GemmDesc& d, hipStream_t s) {
+    ProfInfo pi;
+    pi.kind = PROF_GEMM;
+    pi.M = d.M; pi.N = d.N; pi.K = d.K; pi.nseg = d.nseg;
+    pi.Mdev = d.Mdev; pi.Kdev = d.Kdev;
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext("gemm_rk_krt_dma_kernel", pi, &ea, &eb);
+    GemmDesc dd = d;
+    dd.prof_snap = prof_snap(h);
+    dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
+    hipExtLaunchKernelGGL((gemm_rk_krt_dma_kernel<kDgradNST>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
+    prof_end_ext(h);
+}
+
 template <int AM, int BMODE, bool AL = false>
 void launch(const GemmDesc& d, hipStream_t s) {
     // kernel names as the profilers print them
@@ -1299,6 +1601,7 @@ void launch(const GemmDesc& d, hipStream_t s) {
 }
 
 }  // namespace
+
 
 fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s, int max_wg) {
     FO_CHECK(n >= 1 && n <= kGemmGroupMax, "gemm_group: %d products", n);
@@ -1348,11 +1651,11 @@ fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s, int max_wg) {
         }
     }
     hipEvent_t ea, eb;
-    const int h = prof_begin_ext("gemm_group_kernel<6, 6>", pi, &ea, &eb);
+    const int h = prof_begin_ext("gemm_wgrad_dma_kernel", pi, &ea, &eb);
     g.prof_snap = prof_snap(h);
     int grid = tiles;
     if (max_wg > 0 && grid > max_wg) grid = std::max(8, max_wg / 8 * 8);
-    hipExtLaunchKernelGGL((gemm_group_kernel<OP_KRT, OP_KRT, true>), dim3(grid), dim3(NT), 0, s, ea, eb, 0, g);
+    hipExtLaunchKernelGGL((gemm_wgrad_dma_kernel<kWgradKT, kWgradNST>), dim3(grid), dim3(NT), 0, s, ea, eb, 0, g);
     prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;
@@ -1407,11 +1710,15 @@ fo_status gemm(const GemmDesc& d, hipStream_t s) {
     // 16-byte aligned input and weights, Ci % 64 == 0, static sizes
     const bool conv_comp = a == OP_CONV_FWD && b == OP_RK && d.nseg > 1 && !d.Kdev && d.g.Ci % 64 == 0 &&
                            al16(d.A) && al16(d.A2) && op_aligned(OP_RK, d.B, d.B2, d.ldb, d.N);
+    // an unsplit aligned product of two k-major operands (a weight gradient)
+    // runs as a group of one on the kernel with copies into LDS
+    if (a == OP_KR && b == OP_KR && al && d.splits == 1 && d.nseg == 1 && !d.colpart) return gemm_group(&d, 1, s, 0);
     // (two stages and two workgroups per CU beat deeper rings at one per CU, and
     // 256 x 128 tiles with a three-stage ring at one per CU on these products)
     if (a == OP_RK && b == OP_RK && al && d.nseg > 1 && !d.Kdev)
         d.nseg == 3 ? launch_comp<3>(dv, s) : launch_comp<2>(dv, s);
     else if (a == OP_RK && b == OP_RK) al ? launch<OP_RK, OP_RK, true>(dv, s) : launch<OP_RK, OP_RK>(dv, s);
+    else if (a == OP_RK && b == OP_KR && al && d.nseg == 1 && !d.Kdev) launch_rk_krt(dv, s);
     else if (a == OP_RK && b == OP_KR) al ? launch<OP_RK, OP_KRT, true>(dv, s) : launch<OP_RK, OP_KR>(dv, s);
     else if (a == OP_KR && b == OP_KR) al ? launch<OP_KRT, OP_KRT, true>(dv, s) : launch<OP_KR, OP_KR>(dv, s);
     else if (a == OP_KR && b == OP_RK) al ? launch<OP_KRT, OP_RK, true>(dv, s) : launch<OP_KR, OP_RK>(dv, s);

@@ -33,7 +33,13 @@ def _dev16(h):
 
 @pytest.mark.parametrize("M,N,K,la,lb", [
     (256, 256, 256, 0, 0), (200, 130, 96, 0, 0), (129, 257, 70, 0, 1), (64, 10, 512, 0, 1),
-    (512, 768, 3072, 0, 0), (300, 200, 1000, 1, 1), (10, 512, 64, 1, 1), (3, 5, 7, 0, 0), (1, 1, 1, 1, 0)])
+    (512, 768, 3072, 0, 0), (300, 200, 1000, 1, 1), (10, 512, 64, 1, 1), (3, 5, 7, 0, 0), (1, 1, 1, 1, 0),
+    # k-major, rows in whole chunks of 8 (the weight-gradient kernel with copies
+    # into LDS): ragged row tiles and K tails of every depth
+    (264, 136, 1000, 1, 1), (776, 392, 70, 1, 1), (8, 8, 5, 1, 1), (128, 1152, 4097, 1, 1),
+    # row-major A times k-major B with every dimension in chunks of 8 (the
+    # input-gradient kernel with copies into LDS)
+    (264, 136, 1000, 0, 1), (776, 392, 72, 0, 1), (8, 8, 8, 0, 1), (2496, 768, 2304, 0, 1)])
 def test_gemm_plain(M, N, K, la, lb):
     torch = torch_cuda()
     announce(f"gemm {M}x{N}x{K} layouts {la}{lb}")
@@ -48,16 +54,18 @@ def test_gemm_plain(M, N, K, la, lb):
     assert normwise(C.cpu().numpy(), ref) <= 1e-5
 
 
-@pytest.mark.parametrize("M,N,K,splits", [(256, 384, 1024, 4), (100, 70, 333, 3), (768, 768, 4096, 8)])
-def test_gemm_split_k(M, N, K, splits):
+@pytest.mark.parametrize("M,N,K,splits,la", [(256, 384, 1024, 4, 1), (100, 70, 333, 3, 1), (768, 768, 4096, 8, 1),
+                                             (2496, 768, 3072, 2, 0), (264, 136, 1000, 3, 0)])
+def test_gemm_split_k(M, N, K, splits, la):
     torch = torch_cuda()
-    announce(f"gemm split-K {M}x{N}x{K} s={splits}")
+    announce(f"gemm split-K {M}x{N}x{K} s={splits} A layout {la}")
     rng = np.random.default_rng(K)
-    a, av = _bf16(rng, (K, M))      # k-major operands, as in weight gradients
+    a, av = _bf16(rng, (K, M))      # k-major B (and A when la = 1), as in weight and input gradients
     b, bv = _bf16(rng, (K, N))
+    Ad = _dev16(a) if la == 1 else _dev16(np.ascontiguousarray(a.T))
     C = torch.zeros((M, N), dtype=torch.float32, device="cuda")
     ws = torch.empty(splits * M * N, dtype=torch.float32, device="cuda")
-    A.fo_gemm_bf16(M, N, K, 1, _dev16(a), None, M, 1, _dev16(b), None, N, C, N, splits, ws)
+    A.fo_gemm_bf16(M, N, K, la, Ad, None, M if la == 1 else K, 1, _dev16(b), None, N, C, N, splits, ws)
     assert normwise(C.cpu().numpy(), av.T @ bv) <= 1e-5
 
 
