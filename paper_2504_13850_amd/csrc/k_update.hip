@@ -100,13 +100,17 @@ __global__ void __launch_bounds__(256) agg_lerp_multi_kernel(float* __restrict__
     }
 }
 
-static int stream_grid(int64_t n4, int64_t chunk) {
+static int stream_grid(int64_t n4, int64_t chunk, int64_t cap = 2048) {
     // 256 CUs x 8 blocks of 256 threads keep HBM busy; small vectors use fewer.
     int64_t blocks = cdiv(n4 > 0 ? n4 : 1, chunk);
-    if (blocks > 2048) blocks = 2048;
+    if (blocks > cap) blocks = cap;
     return (int)blocks;
 }
 static int stream_grid(int64_t n4) { return stream_grid(n4, SCHUNK); }
+// The aggregation's 2:1 read-write stream: 16384 blocks (each pass of a block
+// 16 KiB of either vector) measured 6.1 TB/s on 1 GiB vectors against 5.8 TB/s
+// with 2048 blocks (read-only streams reach 7.1 TB/s, write-only 4.9).
+constexpr int64_t kAggGridCap = 16384;
 
 // ------------------------------------------------------------------ pool arrival
 // One admitted activation batch into its pool slot: the activations (n16
@@ -193,7 +197,7 @@ fo_status launch_pool_put_gather(const PutTable& t, int64_t bytes, int batch, hi
 fo_status launch_agg_lerp(float* g, const float* l, int64_t n, float w, hipStream_t s) {
     if (n == 0) return FO_OK;
     int64_t n4 = n / 4;
-    int grid = stream_grid(n4);
+    int grid = stream_grid(n4, SCHUNK, kAggGridCap);
     int tail = (int)(n - n4 * 4);
     if (grid * 256 < tail) grid = 1;
     hipLaunchKernelGGL(agg_lerp_kernel, dim3(grid), dim3(256), 0, s, g, l, n4, n, w);
@@ -204,7 +208,7 @@ fo_status launch_agg_lerp(float* g, const float* l, int64_t n, float w, hipStrea
 fo_status launch_agg_lerp_multi(float* g, const AggTable& tab, int64_t n, hipStream_t s) {
     if (n == 0 || tab.count == 0) return FO_OK;
     int64_t n4 = n / 4;
-    int grid = stream_grid(n4, 256 * MU);
+    int grid = stream_grid(n4, 256 * MU, kAggGridCap);
     hipLaunchKernelGGL(agg_lerp_multi_kernel, dim3(grid), dim3(256), 0, s, g, tab, n4, n);
     FO_LAUNCHED();
     return FO_OK;
