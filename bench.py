@@ -106,7 +106,7 @@ GEMM_SOURCES = ["paper_2504_13850_amd/csrc/k_gemm.hip", "paper_2504_13850_amd/cs
 TRAFFIC_KERNELS = {
     # compensated forward products, input gradients, weight gradients of the transformer step
     "gemm_comp_dma_kernel<3>": ("gemm_comp_dma_kernel<3, 2, fo::(anonymous namespace)::DmaRKc>", GEMM_SOURCES),
-    "gemm_rk_krt_dma_kernel": ("gemm_rk_krt_dma_kernel<4>", GEMM_SOURCES),
+    "gemm_rk_krt_dma_kernel": ("gemm_rk_krt_dma_kernel<32, 4>", GEMM_SOURCES),
     "gemm_wgrad_dma_kernel": ("gemm_wgrad_dma_kernel<32, 4>", GEMM_SOURCES),
     "agg_lerp_kernel": ("agg_lerp_kernel(", ["paper_2504_13850_amd/csrc/k_update.hip"]),
 }

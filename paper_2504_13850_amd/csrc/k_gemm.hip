@@ -30,7 +30,7 @@ constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
 // tiles, four stages; input gradients four stages (64 KB of LDS each, two
 // workgroups per CU: deeper rings at one workgroup per CU starve the
 // concurrent input-gradient chain of LDS).
-constexpr int kWgradKT = 32, kWgradNST = 4, kDgradNST = 4;
+constexpr int kWgradKT = 32, kWgradNST = 4, kDgradKT = 32, kDgradNST = 4;
 constexpr int NV = BM * BK / 8 / NT;  // 16-byte vectors per thread per operand per K tile (4)
 
 // LDS tiles are 128 rows x 64 k with rows padded to 72 elements (144 B = 36
@@ -1399,11 +1399,12 @@ __device__ __forceinline__ void lgkm_wait_tr4(i32x2_t (&r)[4], int n) {
         asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]));
 }
 
-template <int NST>
+template <int KT, int NST>
 __global__ void __launch_bounds__(NT, 2) gemm_rk_krt_dma_kernel(const GemmDesc d) {
-    constexpr int KT = CBK;
-    // NST stages of an A tile (128 x 32) and a B tile (32 x 128), 16 KB each;
+    // NST stages of an A tile (KT / 32 blocks of 128 x 32) and a B tile (KT x 128);
     // reused for the C tile (64 KB)
+    static_assert(KT == 32 || KT == 64, "tile depth");
+    constexpr int KA = KT / CBK;  // A blocks per stage
     __shared__ __attribute__((aligned(1024))) bf16_t smem[NST][2][BM * KT];
     static_assert(NST * 2 * KT * BM * 2 >= BM * BN * 4, "the C tile lives in the stages");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1436,10 +1437,11 @@ __global__ void __launch_bounds__(NT, 2) gemm_rk_krt_dma_kernel(const GemmDesc d
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    constexpr int CPT = 2 + DmaKRt<KT>::NI;  // copy instructions per tile and thread
+    constexpr int CPT = 2 * KA + DmaKRt<KT>::NI;  // copy instructions per tile and thread
     auto copy_tile = [&](int st, int t) {
         const int kb = kbeg + t * KT, ke = t < nk ? K : 0;
-        la.copy(d.A, kb, ke, smem[st][0], wave);
+#pragma unroll
+        for (int a = 0; a < KA; ++a) la.copy(d.A, kb + CBK * a, ke, smem[st][0] + a * BM * CBK, wave);
         lb.copy(d.B, kb, ke, smem[st][1], wave);
     };
     const int lrow = lane & 31, lc = lane >> 5;
@@ -1453,29 +1455,34 @@ __global__ void __launch_bounds__(NT, 2) gemm_rk_krt_dma_kernel(const GemmDesc d
         rb[2] = b0 + 2 * o1.x;
         rb[3] = b0 + 2 * o1.y;
     }
+    // k blocks of 16 in pairs (one A block of 32): the pair's eight transpose
+    // reads are issued together, the first block's MFMAs wait for its four
     auto compute = [&](int st) {
-        const bf16_t* At = smem[st][0];
         const uint32_t so = (uint32_t)st * (2 * KT * BM * 2);
-        i32x2_t r[2][4];
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int kp = 0; kp < KA; ++kp) {
+            const bf16_t* At = smem[st][0] + kp * BM * CBK;
+            i32x2_t r[2][4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) r[h][q] = tr_read(rb[q] + so + h * 16 * BM * 2);
+            for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            bf16x8_t a[2];
+                for (int q = 0; q < 4; ++q) r[h][q] = tr_read(rb[q] + so + (2 * kp + h) * 16 * BM * 2);
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int row = wm * 64 + i * 32 + lrow, C = 2 * ks + lc;
-                a[i] = *reinterpret_cast<const bf16x8_t*>(&At[row * KT + 8 * (C ^ ((row >> 2) & 3))]);
+            for (int ks = 0; ks < 2; ++ks) {
+                bf16x8_t a[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const int row = wm * 64 + i * 32 + lrow, C = 2 * ks + lc;
+                    a[i] = *reinterpret_cast<const bf16x8_t*>(&At[row * CBK + 8 * (C ^ ((row >> 2) & 3))]);
+                }
+                lgkm_wait_tr4(r[ks], 1 - ks);
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            a[i], frag_cat(r[ks][2 * j], r[ks][2 * j + 1]), acc[i][j], 0, 0, 0);
             }
-            lgkm_wait_tr4(r[ks], 1 - ks);
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], frag_cat(r[ks][2 * j], r[ks][2 * j + 1]),
-                                                                       acc[i][j], 0, 0, 0);
         }
     };
     auto step = [&](int t, int u) {
@@ -1574,7 +1581,7 @@ void launch_rk_krt(const GemmDesc& d, hipStream_t s) {
     GemmDesc dd = d;
     dd.prof_snap = prof_snap(h);
     dim3 grid((d.N + BN - 1) / BN, (d.M + BM - 1) / BM, d.splits);
-    hipExtLaunchKernelGGL((gemm_rk_krt_dma_kernel<kDgradNST>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
+    hipExtLaunchKernelGGL((gemm_rk_krt_dma_kernel<kDgradKT, kDgradNST>), grid, dim3(NT), 0, s, ea, eb, 0, dd);
     prof_end_ext(h);
 }
 

@@ -56,8 +56,9 @@ struct Plan {
     float *splitws, *slws;
     // column-sum partials per layer parity, finished on the side stream: the FFN1
     // bias gradient (colwsF), the two norms' dgamma / dbeta / bias gradient
-    // (lnpart[parity][0] LN2, [1] LN1); colws2: the side stream's own (bqkv)
-    float *colwsF[2], *lnpart[2][2], *colws2;
+    // (lnpart[parity][0] LN2, [1] LN1); colws2: the side stream's own (bqkv);
+    // colws2m: the main stream's, for the first layer's (the backward's last)
+    float *colwsF[2], *lnpart[2][2], *colws2, *colws2m;
     float *pooled, *dz, *dpool, *dxc;
     float* xres;  // the last layer's residual input at the first tokens, [B][D]
     // parameter ranges whose SGD update is not fused into a weight-gradient
@@ -68,6 +69,7 @@ struct Plan {
     hipEvent_t ev_fork = nullptr;    // main -> side: an operand is ready
     hipEvent_t ev_done[2] = {};      // side -> main: a parity's operands are free again
     hipEvent_t ev_join = nullptr;    // side -> main: every weight gradient is written
+    hipEvent_t ev_cols = nullptr;    // side -> main: the column sums of every layer but the first are written
 };
 
 // ------------------------------------------------------------------ kernels
@@ -423,6 +425,7 @@ size_t ws_bytes(const fo_model* m) {
     add(std::max(gemm_ws_bytes((int)R, D, 4), gemm_ws_bytes((int)B, FF, 4)));
     for (int q = 0; q < 2; ++q) add(4 * colsum_ws_floats((int)R, FF));
     add(4 * colsum_ws_floats((int)R, 3 * D));
+    add(4 * colsum_ws_floats((int)R, 3 * D));
     for (int q = 0; q < 4; ++q) add(4 * (size_t)cdiv(R, LNB_ROWS) * 3 * D);
     add(4 * small_linear_ws_floats((int)B, D, D));
     add(4 * B * D); add(4 * B * NC); add(4 * B * D); add(4 * B * D); add(4 * B * D);
@@ -504,6 +507,7 @@ fo_status init(fo_model* m) {
     P->splitws = a.take<float>(sw / 4 + 1);
     for (int q = 0; q < 2; ++q) P->colwsF[q] = a.take<float>(colsum_ws_floats((int)R, FF));
     P->colws2 = a.take<float>(colsum_ws_floats((int)R, 3 * D));
+    P->colws2m = a.take<float>(colsum_ws_floats((int)R, 3 * D));
     for (int q = 0; q < 4; ++q) P->lnpart[q / 2][q % 2] = a.take<float>((size_t)cdiv(R, LNB_ROWS) * 3 * D);
     P->slws = a.take<float>(small_linear_ws_floats((int)B, D, D));
     P->pooled = a.take<float>(B * D);
@@ -528,7 +532,7 @@ fo_status init(fo_model* m) {
     }
     // default priority, no implicit ordering with the null stream
     FO_HIP(hipStreamCreateWithFlags(&P->side, hipStreamNonBlocking));
-    for (hipEvent_t* e : {&P->ev_fork, &P->ev_done[0], &P->ev_done[1], &P->ev_join})
+    for (hipEvent_t* e : {&P->ev_fork, &P->ev_done[0], &P->ev_done[1], &P->ev_join, &P->ev_cols})
         FO_HIP(hipEventCreateWithFlags(e, hipEventDisableTiming));
     return FO_OK;
 }
@@ -785,9 +789,14 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         }
         // the layer's parameter gradients off the input-gradient chain: bias and
         // norm gradients from their partials, then the weight gradients with
-        // their SGD updates
+        // their SGD updates.  After the first layer's chain the main stream has
+        // nothing left but the final SGD pass, so it takes that layer's column
+        // sums itself while the side stream runs the weight gradients.
+        const bool last = l == 0;
+        hipStream_t cs = last ? s : s2;
+        float* colws = last ? P->colws2m : P->colws2;
         TRY(order_after(s2, s, P->ev_fork));
-        TRY(launch_colsum_partial(dqkv, 3 * D, rows, Tdev, 3 * D, P->colws2, s2));
+        TRY(launch_colsum_partial(dqkv, 3 * D, rows, Tdev, 3 * D, colws, cs));
         {
             // one launch finishes LN2's dgamma / dbeta / dbias of FFN2, the FFN1 bias,
             // LN1's dgamma / dbeta / dbias of the output projection and the QKV bias
@@ -803,10 +812,11 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             jf.part = P->colwsF[pb]; jf.rows = M; jf.rows_dev = Mdev; jf.rows_per_part = 128; jf.N = FF;
             jf.out.p[0] = grd + f.bf1; jf.out.seg = FF;
             ColJob& jq = cj.j[3];
-            jq.part = P->colws2; jq.rows = rows; jq.rows_dev = Tdev; jq.rows_per_part = colsum_rows_per_part();
+            jq.part = colws; jq.rows = rows; jq.rows_dev = Tdev; jq.rows_per_part = colsum_rows_per_part();
             jq.N = 3 * D;
             jq.out.p[0] = grd + f.bqkv; jq.out.seg = 3 * D;
-            TRY(launch_colsum_finish_multi(cj, s2));
+            TRY(launch_colsum_finish_multi(cj, cs));
+            if (l == 1) FO_HIP(hipEventRecord(P->ev_cols, s2));
         }
         // the layer's four weight gradients in one launch, each tile over the
         // whole K (the packed rows, or the B first-token rows of the last layer)
@@ -817,21 +827,27 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         wg[1] = wgrad(FF, D, dA1, t.Hb, f.w1, Kw, Kwdev);          // dW1 = dA1^T H
         wg[2] = wgrad(D, D, du1b, t.O, f.wo, Kw, Kwdev);           // dWo = du1^T O
         wg[3] = wgrad(3 * D, D, dqkv, P->Xb[l], f.wqkv, rows, Tdev);  // dWqkv = dqkv^T X
-        TRY(gemm_group(wg, 4, s2, kWgradMaxWG));
+        // (the last group has the GPU to itself: no cap on its workgroups)
+        TRY(gemm_group(wg, 4, s2, last ? 0 : kWgradMaxWG));
         FO_HIP(hipEventRecord(P->ev_done[pb], s2));
         cur ^= 1;
     }
     FO_LAUNCHED();
-    TRY(order_after(s, s2, P->ev_join));
     // ---------------- SGD (Alg. 4: theta_s <- theta_s - gamma_s grad) of the
-    // parameters not updated by their weight-gradient product; refreshes the bf16 shadow
-    return launch_sgd_chunks(m->params, m->grads, m->w16, m->w16lo, P->sgd_chunks, P->n_sgd_chunks, m->lr, s);
+    // parameters not updated by their weight-gradient product (biases, norms,
+    // pooler, classifier; disjoint from the weight matrices the side stream is
+    // still updating); refreshes the bf16 shadow.  It needs every layer's column
+    // sums: the first layer's are on this stream, the others before ev_cols.
+    static_assert(NL >= 2, "the column sums of the layers above the first finish on the side stream");
+    FO_HIP(hipStreamWaitEvent(s, P->ev_cols, 0));
+    TRY(launch_sgd_chunks(m->params, m->grads, m->w16, m->w16lo, P->sgd_chunks, P->n_sgd_chunks, m->lr, s));
+    return order_after(s, s2, P->ev_join);
 }
 
 void destroy(fo_model* m) {
     Plan* P = (Plan*)m->plan;
     if (P) {
-        for (hipEvent_t e : {P->ev_fork, P->ev_done[0], P->ev_done[1], P->ev_join})
+        for (hipEvent_t e : {P->ev_fork, P->ev_done[0], P->ev_done[1], P->ev_join, P->ev_cols})
             if (e) (void)hipEventDestroy(e);
         if (P->side) (void)hipStreamDestroy(P->side);
     }
