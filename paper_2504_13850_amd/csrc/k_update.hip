@@ -113,6 +113,30 @@ static int stream_grid(int64_t n4) { return stream_grid(n4, SCHUNK); }
 constexpr int64_t kAggGridCap = 16384;
 
 // ------------------------------------------------------------------ pool arrival
+// Copies n16 16-byte chunks in the streaming shape above: full passes with
+// every load of the pass issued before the first store and no per-lane test
+// (with a test on each unrolled load the compiler waits after every load:
+// 19.5 us against 7 us for a 6 MiB batch), then one guarded partial pass.
+__device__ __forceinline__ void stream_copy16(const uint4* __restrict__ xs, uint4* __restrict__ xd, int64_t n16) {
+    const int tid = threadIdx.x;
+    const int64_t step = (int64_t)gridDim.x * SCHUNK;
+    int64_t base = (int64_t)blockIdx.x * SCHUNK;
+    for (; base + SCHUNK <= n16; base += step) {
+        uint4 v[SU];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) v[u] = xs[base + 256 * u + tid];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) xd[base + 256 * u + tid] = v[u];
+    }
+    if (base < n16) {
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int64_t i = base + 256 * u + tid;
+            if (i < n16) xd[i] = xs[i];
+        }
+    }
+}
+
 // One admitted activation batch into its pool slot: the activations (n16
 // 16-byte chunks) and the int32 labels and lengths (batch each, lengths
 // optional) in one launch.  The first block also copies labels and lengths.
@@ -120,20 +144,7 @@ __global__ void __launch_bounds__(256) pool_put_kernel(const uint4* __restrict__
                                                        int64_t n16, const int32_t* __restrict__ ls,
                                                        int32_t* __restrict__ ld, const int32_t* __restrict__ ns,
                                                        int32_t* __restrict__ nd, int batch) {
-    const int64_t stride = (int64_t)gridDim.x * 256 * SU;
-    for (int64_t base = (int64_t)blockIdx.x * 256 * SU + threadIdx.x; base < n16; base += stride) {
-        uint4 v[SU];
-#pragma unroll
-        for (int u = 0; u < SU; ++u) {
-            const int64_t i = base + 256 * u;
-            if (i < n16) v[u] = xs[i];
-        }
-#pragma unroll
-        for (int u = 0; u < SU; ++u) {
-            const int64_t i = base + 256 * u;
-            if (i < n16) xd[i] = v[u];
-        }
-    }
+    stream_copy16(xs, xd, n16);
     if (blockIdx.x == 0)
         for (int b = threadIdx.x; b < batch; b += 256) {
             ld[b] = ls[b];
@@ -160,20 +171,7 @@ __global__ void __launch_bounds__(256) pool_put_gather_kernel(const PutTable t, 
     const int e = blockIdx.y;
     const uint4* __restrict__ xs = t.xs[e];
     uint4* __restrict__ xd = t.xd[e];
-    const int64_t stride = (int64_t)gridDim.x * 256 * SU;
-    for (int64_t base = (int64_t)blockIdx.x * 256 * SU + threadIdx.x; base < n16; base += stride) {
-        uint4 v[SU];
-#pragma unroll
-        for (int u = 0; u < SU; ++u) {
-            const int64_t i = base + 256 * u;
-            if (i < n16) v[u] = xs[i];
-        }
-#pragma unroll
-        for (int u = 0; u < SU; ++u) {
-            const int64_t i = base + 256 * u;
-            if (i < n16) xd[i] = v[u];
-        }
-    }
+    stream_copy16(xs, xd, n16);
     if (blockIdx.x == 0)
         for (int b = threadIdx.x; b < batch; b += 256) {
             t.ld[e][b] = t.ls[e][b];
