@@ -523,15 +523,20 @@ __device__ __forceinline__ float gelu_and_grad(float x, float* grad) {
 // (residual, ReLU mask, GELU input), epi_store applies activation, mask and
 // GELU' and stores, so that a thread can issue the loads of several rows
 // before it needs any of them.
+// The epilogue's per-element operands, loaded in batches before the first
+// use; bf16 operands stay raw bits until used, so that converting them does
+// not make each load of a batch wait for the previous one.
 struct EpiIn {
-    float resid = 0.f, mask = 1.f, dact = 1.f;
+    float resid = 0.f, theta = 0.f;
+    bf16_t mask = 0x3F80, dact = 0x3F80;  // 1.0
 };
 
 __device__ __forceinline__ EpiIn epi_load(const GemmDesc& d, int row, int col) {
     EpiIn e;
     if (d.resid) e.resid = d.resid[(int64_t)row * d.ldr + col];
-    if (d.mask) e.mask = bf2f(d.mask[(int64_t)row * d.ldm + col]);
-    if (d.dact) e.dact = bf2f(d.dact[(int64_t)row * d.ldm + col]);
+    if (d.mask) e.mask = d.mask[(int64_t)row * d.ldm + col];
+    if (d.dact) e.dact = d.dact[(int64_t)row * d.ldm + col];
+    if (d.sgd_theta) e.theta = d.sgd_theta[(int64_t)row * d.ldcf + col];
     return e;
 }
 
@@ -548,12 +553,12 @@ __device__ __forceinline__ float epi_store(const GemmDesc& d, int row, int col, 
     } else if (d.act == ACT_RELU) {
         v = v > 0.f ? v : 0.f;
     }
-    if (d.mask && !(e.mask > 0.f)) v = 0.f;
-    if (d.dact) v *= e.dact;
+    if (d.mask && !(bf2f(e.mask) > 0.f)) v = 0.f;
+    if (d.dact) v *= bf2f(e.dact);
     if (d.Cf) d.Cf[(int64_t)row * d.ldcf + col] = v;
     if (d.sgd_theta) {
         const int64_t o = (int64_t)row * d.ldcf + col;
-        const float th = __builtin_fmaf(-d.sgd_lr, v, d.sgd_theta[o]);
+        const float th = __builtin_fmaf(-d.sgd_lr, v, e.theta);
         d.sgd_theta[o] = th;
         const bf16_t h = f2bf(th);
         d.sgd_hi[o] = h;
@@ -599,16 +604,61 @@ __device__ __forceinline__ u32x2 f_to_bf4(f32x4 v, f32x4* lo) {
     return w;
 }
 
-struct EpiIn4 {
-    f32x4 resid = {0.f, 0.f, 0.f, 0.f}, mask = {1.f, 1.f, 1.f, 1.f}, dact = {1.f, 1.f, 1.f, 1.f};
+struct EpiIn4 {  // as EpiIn, four columns (bf16 operands as raw bits)
+    f32x4 resid = {0.f, 0.f, 0.f, 0.f}, theta = {0.f, 0.f, 0.f, 0.f};
+    u32x2 mask = {0x3F803F80u, 0x3F803F80u}, dact = {0x3F803F80u, 0x3F803F80u};  // 1.0 x 4
 };
 
 __device__ __forceinline__ EpiIn4 epi_load4(const GemmDesc& d, int row, int col) {
     EpiIn4 e;
     if (d.resid) e.resid = *reinterpret_cast<const f32x4*>(d.resid + (int64_t)row * d.ldr + col);
-    if (d.mask) e.mask = bf4_to_f(*reinterpret_cast<const u32x2*>(d.mask + (int64_t)row * d.ldm + col));
-    if (d.dact) e.dact = bf4_to_f(*reinterpret_cast<const u32x2*>(d.dact + (int64_t)row * d.ldm + col));
+    if (d.mask) e.mask = *reinterpret_cast<const u32x2*>(d.mask + (int64_t)row * d.ldm + col);
+    if (d.dact) e.dact = *reinterpret_cast<const u32x2*>(d.dact + (int64_t)row * d.ldm + col);
+    if (d.sgd_theta) e.theta = *reinterpret_cast<const f32x4*>(d.sgd_theta + (int64_t)row * d.ldcf + col);
     return e;
+}
+
+// The operands of NB rows (clamped into the product by the caller, so every
+// load is in bounds): each operand's loads sit in one uniform branch, all of
+// them issued before the first use.
+template <int NB>
+__device__ __forceinline__ void epi_load4_batch(const GemmDesc& d, const int (&row)[NB], int col, EpiIn4 (&e)[NB]) {
+    if (d.resid) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) e[u].resid = *reinterpret_cast<const f32x4*>(d.resid + (int64_t)row[u] * d.ldr + col);
+    }
+    if (d.mask) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) e[u].mask = *reinterpret_cast<const u32x2*>(d.mask + (int64_t)row[u] * d.ldm + col);
+    }
+    if (d.dact) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) e[u].dact = *reinterpret_cast<const u32x2*>(d.dact + (int64_t)row[u] * d.ldm + col);
+    }
+    if (d.sgd_theta) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u)
+            e[u].theta = *reinterpret_cast<const f32x4*>(d.sgd_theta + (int64_t)row[u] * d.ldcf + col);
+    }
+}
+template <int NB>
+__device__ __forceinline__ void epi_load_batch(const GemmDesc& d, const int (&row)[NB], int col, EpiIn (&e)[NB]) {
+    if (d.resid) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) e[u].resid = d.resid[(int64_t)row[u] * d.ldr + col];
+    }
+    if (d.mask) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) e[u].mask = d.mask[(int64_t)row[u] * d.ldm + col];
+    }
+    if (d.dact) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) e[u].dact = d.dact[(int64_t)row[u] * d.ldm + col];
+    }
+    if (d.sgd_theta) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) e[u].theta = d.sgd_theta[(int64_t)row[u] * d.ldcf + col];
+    }
 }
 
 // v already holds bias and residual
@@ -632,15 +682,16 @@ __device__ __forceinline__ f32x4 epi_store4(const GemmDesc& d, int row, int col,
         for (int q = 0; q < 4; ++q) v[q] = v[q] > 0.f ? v[q] : 0.f;
     }
     if (d.mask) {
+        const f32x4 mk = bf4_to_f(e.mask);
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            if (!(e.mask[q] > 0.f)) v[q] = 0.f;
+            if (!(mk[q] > 0.f)) v[q] = 0.f;
     }
-    if (d.dact) v *= e.dact;
+    if (d.dact) v *= bf4_to_f(e.dact);
     if (d.Cf) *reinterpret_cast<f32x4*>(d.Cf + (int64_t)row * d.ldcf + col) = v;
     if (d.sgd_theta) {
         const int64_t o = (int64_t)row * d.ldcf + col;
-        f32x4 th = *reinterpret_cast<const f32x4*>(d.sgd_theta + o), lo;
+        f32x4 th = e.theta, lo;
 #pragma unroll
         for (int q = 0; q < 4; ++q) th[q] = __builtin_fmaf(-d.sgd_lr, v[q], th[q]);
         *reinterpret_cast<f32x4*>(d.sgd_theta + o) = th;
@@ -748,11 +799,10 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
                 }
                 for (int lr0 = rr; lr0 < BMt && m0 + lr0 < M; lr0 += 8 * RP) {
                     EpiIn4 e[8];
+                    int rows[8];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) {
-                        const int row = m0 + lr0 + RP * u;
-                        if (row < M) e[u] = epi_load4(d, row, col);
-                    }
+                    for (int u = 0; u < 8; ++u) rows[u] = min(m0 + lr0 + RP * u, M - 1);
+                    epi_load4_batch(d, rows, col, e);
 #pragma unroll
                     for (int u = 0; u < 8; ++u) {
                         const int lr = lr0 + RP * u, row = m0 + lr;
@@ -791,11 +841,10 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
             // eight rows per batch: their operand loads are in flight together
             for (int lr0 = tid / BNt; lr0 < BMt && m0 + lr0 < M; lr0 += 8 * HP) {
                 EpiIn e[8];
+                int rows[8];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int row = m0 + lr0 + HP * u;
-                    if (row < M) e[u] = epi_load(d, row, col);
-                }
+                for (int u = 0; u < 8; ++u) rows[u] = min(m0 + lr0 + HP * u, M - 1);
+                epi_load_batch(d, rows, col, e);
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
                     const int lr = lr0 + HP * u, row = m0 + lr;
