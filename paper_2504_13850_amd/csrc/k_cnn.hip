@@ -49,20 +49,29 @@ __global__ void __launch_bounds__(256) maxpool_fwd(const bf16_t* __restrict__ xh
         r /= Wo;
         const int oy = (int)(r % Ho);
         const int b = (int)(r / Ho);
-        int64_t src[4];
-        float v[4];
+        // the four taps' high (and low) parts, each in one uniform branch, before the first use
+        bf16_t hv[4], lv[4] = {};
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const int iy = 2 * oy + (t >> 1), ix = 2 * ox + (t & 1);
-            src[t] = (((int64_t)b * H + iy) * W + ix) * C + c;
-            v[t] = bf2f(xh[src[t]]) + (xl ? bf2f(xl[src[t]]) : 0.f);
+            hv[t] = xh[(((int64_t)b * H + iy) * W + ix) * C + c];
         }
+        if (xl) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int iy = 2 * oy + (t >> 1), ix = 2 * ox + (t & 1);
+                lv[t] = xl[(((int64_t)b * H + iy) * W + ix) * C + c];
+            }
+        }
+        float v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[t] = bf2f(hv[t]) + (xl ? bf2f(lv[t]) : 0.f);
         int a = 0;
 #pragma unroll
         for (int t = 1; t < 4; ++t)
             if (v[t] > v[a]) a = t;
-        yh[i] = xh[src[a]];
-        if (yl) yl[i] = xl ? xl[src[a]] : (bf16_t)0;
+        yh[i] = hv[a];
+        if (yl) yl[i] = lv[a];
         arg[i] = (uint8_t)a;
     }
 }
@@ -103,14 +112,15 @@ __global__ void __launch_bounds__(256) gap_fwd(const bf16_t* __restrict__ xh, co
         const int64_t base = (int64_t)b * HW * C + c;
         int p = w;
         for (; p + 28 < HW; p += 32) {
-            float v[8];
+            bf16_t hv[8], lv[8] = {};
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int64_t k = base + (int64_t)(p + 4 * u) * C;
-                v[u] = bf2f(xh[k]) + (xl ? bf2f(xl[k]) : 0.f);
+            for (int u = 0; u < 8; ++u) hv[u] = xh[base + (int64_t)(p + 4 * u) * C];
+            if (xl) {  // (one uniform branch: no select right after each load)
+#pragma unroll
+                for (int u = 0; u < 8; ++u) lv[u] = xl[base + (int64_t)(p + 4 * u) * C];
             }
 #pragma unroll
-            for (int u = 0; u < 8; ++u) s += v[u];
+            for (int u = 0; u < 8; ++u) s += bf2f(hv[u]) + (xl ? bf2f(lv[u]) : 0.f);
         }
         for (; p < HW; p += 4) {
             const int64_t k = base + (int64_t)p * C;
@@ -253,14 +263,38 @@ __global__ void __launch_bounds__(256) bn_fwd_apply(const float* __restrict__ z,
     const float mean = stat[0][lane], rstd = stat[1][lane];
     const float gs = g[c] * rstd, bs = fmaf(-mean, gs, beta[c]);  // y = z gs + bs
     const int r0 = blockIdx.y * BN_RPB;
+    // every row's operands first (rows clamped into the tensor), then the
+    // guarded stores: a bound test before each row's loads serialises them
+    // (each operand's loads in one uniform branch, so that no value needs a
+    // select right after its load)
+    int64_t ov[BN_PER];
+    float zv[BN_PER], rv[BN_PER] = {};
+    bf16_t hv[BN_PER] = {}, lv[BN_PER] = {};
+#pragma unroll
+    for (int i = 0; i < BN_PER; ++i) {
+        ov[i] = (int64_t)min(r0 + w + 4 * i, rows - 1) * C + c;
+        zv[i] = z[ov[i]];
+    }
+    if (resf) {
+#pragma unroll
+        for (int i = 0; i < BN_PER; ++i) rv[i] = resf[ov[i]];
+    }
+    if (resh) {
+#pragma unroll
+        for (int i = 0; i < BN_PER; ++i) hv[i] = resh[ov[i]];
+    }
+    if (resl) {
+#pragma unroll
+        for (int i = 0; i < BN_PER; ++i) lv[i] = resl[ov[i]];
+    }
 #pragma unroll
     for (int i = 0; i < BN_PER; ++i) {
         const int r = r0 + w + 4 * i;
         if (r >= rows) break;
         const int64_t o = (int64_t)r * C + c;
-        float v = fmaf(z[o], gs, bs);
-        if (resf) v += resf[o];
-        if (resh) v += bf2f(resh[o]) + (resl ? bf2f(resl[o]) : 0.f);
+        float v = fmaf(zv[i], gs, bs);
+        if (resf) v += rv[i];
+        if (resh) v += bf2f(hv[i]) + (resl ? bf2f(lv[i]) : 0.f);
         if (relu) v = v > 0.f ? v : 0.f;
         if (yf) yf[o] = v;
         if (yh) split_store(yh, yl, o, v);
@@ -356,14 +390,29 @@ __global__ void __launch_bounds__(256) bn_bwd_apply(const float* __restrict__ go
     const float inv = 1.f / (float)rows, m = mean[c], rs = rstd[c];
     const float dgn = stat[0][lane] * inv, dbn = stat[1][lane] * inv, gr = g[c] * rs;
     const int r0 = blockIdx.y * BN_RPB;
+    // every row's operands first (rows clamped into the tensor), then the guarded stores
+    int64_t ov[BN_PER];
+    float dv[BN_PER], zv[BN_PER];
+    bf16_t mv[BN_PER];
+#pragma unroll
+    for (int i = 0; i < BN_PER; ++i) {
+        ov[i] = (int64_t)min(r0 + w + 4 * i, rows - 1) * C + c;
+        dv[i] = gout[ov[i]];
+        zv[i] = z[ov[i]];
+        mv[i] = 0x3F80;  // 1.0
+    }
+    if (mask) {  // (one uniform branch: no select right after each load)
+#pragma unroll
+        for (int i = 0; i < BN_PER; ++i) mv[i] = mask[ov[i]];
+    }
 #pragma unroll
     for (int i = 0; i < BN_PER; ++i) {
         const int r = r0 + w + 4 * i;
         if (r >= rows) break;
         const int64_t o = (int64_t)r * C + c;
-        float d = gout[o];
-        if (mask && !(bf2f(mask[o]) > 0.f)) d = 0.f;
-        const float xh = (z[o] - m) * rs;
+        float d = dv[i];
+        if (mask && !(bf2f(mv[i]) > 0.f)) d = 0.f;
+        const float xh = (zv[i] - m) * rs;
         const float v = gr * (d - dbn - xh * dgn);
         if (dzf) dzf[o] = v;
         if (dzb) dzb[o] = f2bf(v);

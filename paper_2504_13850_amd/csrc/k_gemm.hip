@@ -1568,24 +1568,28 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
         const int64_t total4 = (int64_t)M * d.N / 4;
         for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total4; i += stride) {
             const float* p = d.ws + 4 * i;
+            const int row = (int)(4 * i / d.N), col = (int)(4 * i % d.N);
+            // the epilogue's operands are loaded with the slices, before the first sum
+            f32x4 bias = {0.f, 0.f, 0.f, 0.f};
+            EpiIn4 e;
+            if (d.vec_epi) {
+                if (d.bias) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) bias[q] = d.bias[col + q];
+                }
+                e = epi_load4(d, row, col);
+            }
             f32x4 v = *reinterpret_cast<const f32x4*>(p);
             int z = 1;
             for (; z + 3 < S; z += 4) {
                 const f32x4 a = *reinterpret_cast<const f32x4*>(p + z * full);
                 const f32x4 b = *reinterpret_cast<const f32x4*>(p + (z + 1) * full);
-                const f32x4 e = *reinterpret_cast<const f32x4*>(p + (z + 2) * full);
+                const f32x4 c = *reinterpret_cast<const f32x4*>(p + (z + 2) * full);
                 const f32x4 f = *reinterpret_cast<const f32x4*>(p + (z + 3) * full);
-                v += (a + b) + (e + f);
+                v += (a + b) + (c + f);
             }
             for (; z < S; ++z) v += *reinterpret_cast<const f32x4*>(p + z * full);
-            const int row = (int)(4 * i / d.N), col = (int)(4 * i % d.N);
             if (d.vec_epi) {
-                f32x4 bias = {0.f, 0.f, 0.f, 0.f};
-                if (d.bias) {
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) bias[q] = d.bias[col + q];
-                }
-                const EpiIn4 e = epi_load4(d, row, col);
                 epi_store4(d, row, col, v + bias + e.resid, e);
             } else {
 #pragma unroll

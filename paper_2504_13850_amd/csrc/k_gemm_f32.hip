@@ -26,6 +26,10 @@ __device__ __forceinline__ void chunk_rc(int e, int& r, int& k) {
     r = KF ? e >> 5 : e & 63;
     k = KF ? e & 31 : e >> 6;
 }
+// Every load reads a valid element (row and k clamped into the operand, R and
+// ke >= 1) and the values outside the chunk are zeroed when stored: with
+// "in range ? load : 0" the compiler selects right after each load, so each
+// load waits for the previous one and the chunk in flight is not in flight.
 template <bool KF>
 __device__ __forceinline__ void load_chunk(const float* P, int64_t sr, int64_t sk, int r0, int R, int k0, int ke,
                                            float (&v)[GV]) {
@@ -33,17 +37,18 @@ __device__ __forceinline__ void load_chunk(const float* P, int64_t sr, int64_t s
     for (int i = 0; i < GV; ++i) {
         int r, k;
         chunk_rc<KF>(threadIdx.x + 256 * i, r, k);
-        const int gr = r0 + r, gk = k0 + k;
-        v[i] = gr < R && gk < ke ? P[(int64_t)gr * sr + (KF ? (int64_t)gk : (int64_t)gk * sk)] : 0.f;
+        const int gr = min(r0 + r, R - 1), gk = min(k0 + k, ke - 1);
+        v[i] = P[(int64_t)gr * sr + (KF ? (int64_t)gk : (int64_t)gk * sk)];
     }
 }
 template <bool KF>
-__device__ __forceinline__ void store_chunk(float (*T)[GT + 4], const float (&v)[GV]) {
+__device__ __forceinline__ void store_chunk(float (*T)[GT + 4], const float (&v)[GV], int r0, int R, int k0,
+                                            int ke) {
 #pragma unroll
     for (int i = 0; i < GV; ++i) {
         int r, k;
         chunk_rc<KF>(threadIdx.x + 256 * i, r, k);
-        T[k][r] = v[i];
+        T[k][r] = r0 + r < R && k0 + k < ke ? v[i] : 0.f;
     }
 }
 
@@ -65,8 +70,8 @@ __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
     if (nch > 0) {
         load_chunk<AKF>(A, g.am, g.ak, m0, g.M, kb, ke, ra);
         load_chunk<BKF>(Bp, g.bn, g.bk, n0, g.N, kb, ke, rb);
-        store_chunk<AKF>(As[0], ra);
-        store_chunk<BKF>(Bs[0], rb);
+        store_chunk<AKF>(As[0], ra, m0, g.M, kb, ke);
+        store_chunk<BKF>(Bs[0], rb, n0, g.N, kb, ke);
     }
     __syncthreads();
     for (int c = 0; c < nch; ++c) {
@@ -86,12 +91,50 @@ __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
                 for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
         }
         if (c + 1 < nch) {
-            store_chunk<AKF>(As[u ^ 1], ra);
-            store_chunk<BKF>(Bs[u ^ 1], rb);
+            store_chunk<AKF>(As[u ^ 1], ra, m0, g.M, kb + (c + 1) * GK, ke);
+            store_chunk<BKF>(Bs[u ^ 1], rb, n0, g.N, kb + (c + 1) * GK, ke);
         }
         __syncthreads();
     }
+    if (g.S > 1) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int m = m0 + ty * 4 + i;
+            if (m >= g.M) continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = n0 + tx * 4 + j;
+                if (n < g.N) g.part[((int64_t)z * g.M + m) * g.N + n] = acc[i][j];
+            }
+        }
+        return;
+    }
+    // the epilogue's operands of all 16 elements first (indices clamped into
+    // the product, so every load is valid), then the guarded stores
     const float* add = g.inAdd ? (const float*)g.inAdd->x : g.add;
+    int mi[4], nj[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        mi[i] = min(m0 + ty * 4 + i, g.M - 1);
+        nj[i] = min(n0 + tx * 4 + i, g.N - 1);
+    }
+    float bv[4] = {0.f, 0.f, 0.f, 0.f}, av[4][4] = {}, mv[4][4];
+    if (g.bias) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bv[j] = g.bias[nj[j]];
+    }
+    if (add) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) av[i][j] = add[(int64_t)mi[i] * g.ldadd + nj[j]];
+    }
+    if (g.mask) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) mv[i][j] = g.mask[(int64_t)mi[i] * g.ldmask + nj[j]];
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int m = m0 + ty * 4 + i;
@@ -100,10 +143,10 @@ __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
         for (int j = 0; j < 4; ++j) {
             const int n = n0 + tx * 4 + j;
             if (n >= g.N) continue;
-            if (g.S > 1)
-                g.part[((int64_t)z * g.M + m) * g.N + n] = acc[i][j];
-            else
-                g.C[(int64_t)m * g.ldc + n] = epi(g, add, m, n, acc[i][j]);
+            float v = acc[i][j] + bv[j] + av[i][j];
+            if (g.relu) v = fmaxf(v, 0.f);
+            if (g.mask && !(mv[i][j] > 0.f)) v = 0.f;
+            g.C[(int64_t)m * g.ldc + n] = v;
         }
     }
 }

@@ -126,13 +126,24 @@ __global__ void __launch_bounds__(256) dw_fwd(const float* __restrict__ x, const
     const int c = (int)(i % C);
     const int64_t r = i / C;
     const int b = (int)(r / (Ho * Ho)), oy = (int)(r / Ho % Ho), ox = (int)(r % Ho);
+    // the taps (k <= 5) in order: inputs and weights loaded first from clamped
+    // coordinates, the taps outside the filter or the image add zero
+    float xv[25], wv[25];
+#pragma unroll
+    for (int q = 0; q < 25; ++q) {
+        const int ky = min(q / 5, k - 1), kx = min(q % 5, k - 1);
+        const int yy = min(max(oy * s + ky - k / 2, 0), H - 1), xx = min(max(ox * s + kx - k / 2, 0), H - 1);
+        xv[q] = x[(((int64_t)b * H + yy) * H + xx) * C + c];
+        wv[q] = w[(c * k + ky) * k + kx];
+    }
     float acc = 0.f;
-    for (int ky = 0; ky < k; ++ky)
-        for (int kx = 0; kx < k; ++kx) {
-            const int yy = oy * s + ky - k / 2, xx = ox * s + kx - k / 2;
-            if (yy < 0 || yy >= H || xx < 0 || xx >= H) continue;
-            acc = fmaf(x[(((int64_t)b * H + yy) * H + xx) * C + c], w[(c * k + ky) * k + kx], acc);
-        }
+#pragma unroll
+    for (int q = 0; q < 25; ++q) {
+        const int ky = q / 5, kx = q % 5;
+        const int yy = oy * s + ky - k / 2, xx = ox * s + kx - k / 2;
+        const bool in = ky < k && kx < k && yy >= 0 && yy < H && xx >= 0 && xx < H;
+        if (in) acc = fmaf(xv[q], wv[q], acc);
+    }
     y[i] = acc;
 }
 // dx[b, yy, xx, c] = sum over the outputs whose window holds (yy, xx) of dy w
@@ -144,15 +155,25 @@ __global__ void __launch_bounds__(256) dw_bwd_x(const float* __restrict__ dy, co
     const int c = (int)(i % C);
     const int64_t r = i / C;
     const int b = (int)(r / (H * H)), yy = (int)(r / H % H), xx = (int)(r % H);
+    // the taps (k <= 5) in order, operands loaded first from clamped
+    // coordinates; taps that reach no output pixel add nothing
+    float gv[25], wv[25];
+#pragma unroll
+    for (int q = 0; q < 25; ++q) {
+        const int ky = min(q / 5, k - 1), kx = min(q % 5, k - 1);
+        const int oy = min(max(yy + k / 2 - ky, 0) / s, Ho - 1), ox = min(max(xx + k / 2 - kx, 0) / s, Ho - 1);
+        gv[q] = dy[(((int64_t)b * Ho + oy) * Ho + ox) * C + c];
+        wv[q] = w[(c * k + ky) * k + kx];
+    }
     float acc = 0.f;
-    for (int ky = 0; ky < k; ++ky)
-        for (int kx = 0; kx < k; ++kx) {
-            const int ty = yy + k / 2 - ky, tx = xx + k / 2 - kx;  // = oy * s, ox * s
-            if (ty < 0 || tx < 0 || ty % s || tx % s) continue;
-            const int oy = ty / s, ox = tx / s;
-            if (oy >= Ho || ox >= Ho) continue;
-            acc = fmaf(dy[(((int64_t)b * Ho + oy) * Ho + ox) * C + c], w[(c * k + ky) * k + kx], acc);
-        }
+#pragma unroll
+    for (int q = 0; q < 25; ++q) {
+        const int ky = q / 5, kx = q % 5;
+        const int ty = yy + k / 2 - ky, tx = xx + k / 2 - kx;  // = oy * s, ox * s
+        const bool in = ky < k && kx < k && ty >= 0 && tx >= 0 && ty % s == 0 && tx % s == 0 && ty / s < Ho &&
+                        tx / s < Ho;
+        if (in) acc = fmaf(gv[q], wv[q], acc);
+    }
     dx[i] = acc;
 }
 // Block c: dw[c][tap] = sum over outputs of dy x at the tap (k <= 5)
@@ -166,13 +187,22 @@ __global__ void __launch_bounds__(256) dw_bwd_w(const float* __restrict__ dy, co
     for (int p = t; p < B * Ho * Ho; p += 256) {
         const int b = p / (Ho * Ho), oy = p / Ho % Ho, ox = p % Ho;
         const float g = dy[(int64_t)p * C + c];
+        // every tap's input first (coordinates clamped into the image, so each
+        // load is valid), then the products of the taps inside the image: a
+        // bound test before each load makes each wait for the previous one
+        float xv[25];
 #pragma unroll
         for (int q = 0; q < 25; ++q) {
             const int ky = q / 5, kx = q % 5;
-            if (ky >= k || kx >= k) continue;
+            const int yy = min(max(oy * s + ky - k / 2, 0), H - 1), xx = min(max(ox * s + kx - k / 2, 0), H - 1);
+            xv[q] = ky < k && kx < k ? x[(((int64_t)b * H + yy) * H + xx) * C + c] : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < 25; ++q) {
+            const int ky = q / 5, kx = q % 5;
             const int yy = oy * s + ky - k / 2, xx = ox * s + kx - k / 2;
-            if (yy < 0 || yy >= H || xx < 0 || xx >= H) continue;
-            acc[q] = fmaf(g, x[(((int64_t)b * H + yy) * H + xx) * C + c], acc[q]);
+            const bool in = ky < k && kx < k && yy >= 0 && yy < H && xx >= 0 && xx < H;
+            if (in) acc[q] = fmaf(g, xv[q], acc[q]);
         }
     }
 #pragma unroll
