@@ -230,6 +230,13 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const SplitRows src, float*
     const int T = *Tdev;
     if (row >= T) return;
     const int S = src.active(T);
+    // the norm's parameters are loaded with the row, not after its reductions
+    f32x4 gg[PER4], bb[PER4];
+#pragma unroll
+    for (int k = 0; k < PER4; ++k) {
+        gg[k] = ld4(g + 4 * lane + 256 * k);
+        bb[k] = ld4(beta + 4 * lane + 256 * k);
+    }
     f32x4 x[PER4];
     load_split_row(src, S, row, lane, x);
     float s = 0.f;
@@ -250,10 +257,9 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const SplitRows src, float*
 #pragma unroll
     for (int k = 0; k < PER4; ++k) {
         const int c = 4 * lane + 256 * k;
-        const f32x4 gg = ld4(g + c), bb = ld4(beta + c);
         f32x4 y;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) y[q] = fmaf(x[k][q] * rs, gg[q], bb[q]);
+        for (int q = 0; q < 4; ++q) y[q] = fmaf(x[k][q] * rs, gg[k][q], bb[k][q]);
         st4(yf + (int64_t)row * D + c, y);
         st4bf(yb + (int64_t)row * D + c, y);
         st4bf(ylo + (int64_t)row * D + c, bf4lo(y));
