@@ -293,6 +293,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_mfma(const bf16_t* __restrict
                                                         const float* __restrict__ lse, bf16_t* __restrict__ dqkv, int H,
                                                         int d, float scale, int* __restrict__ snap, int nb,
                                                         const int* __restrict__ order) {
+    __builtin_amdgcn_s_setprio(2);  // on the input-gradient chain: its waves win issue arbitration
     __shared__ __attribute__((aligned(16))) bf16_t T0[LMAX * DH], T1[LMAX * DH];
     __shared__ __attribute__((aligned(16))) float rowL[LMAX], rowD[LMAX];
     if (snap && blockIdx.x == 0)

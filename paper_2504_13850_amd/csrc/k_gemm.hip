@@ -1450,6 +1450,10 @@ __device__ __forceinline__ void lgkm_wait_tr4(i32x2_t (&r)[4], int n) {
 
 template <int KT, int NST>
 __global__ void __launch_bounds__(NT, 2) gemm_rk_krt_dma_kernel(const GemmDesc d) {
+    // the input-gradient chain is the critical path of the backward: its waves
+    // win the issue arbitration against the weight-gradient waves they share
+    // SIMDs with (wave priority, not a stream priority)
+    __builtin_amdgcn_s_setprio(2);
     // NST stages of an A tile (KT / 32 blocks of 128 x 32) and a B tile (KT x 128);
     // reused for the C tile (64 KB)
     static_assert(KT == 32 || KT == 64, "tile depth");

@@ -281,6 +281,7 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const SplitRows dy, const f
                                                      const float* __restrict__ g, const int* __restrict__ Tdev,
                                                      float* __restrict__ dxf, bf16_t* __restrict__ dxb,
                                                      float* __restrict__ part) {
+    __builtin_amdgcn_s_setprio(2);  // on the input-gradient chain (see gemm_rk_krt_dma_kernel)
     constexpr int RW = LNB_ROWS / 4;  // rows per wave
     __shared__ float red[4][D];
     const int T = *Tdev;
