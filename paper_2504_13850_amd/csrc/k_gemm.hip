@@ -2,14 +2,23 @@
 //
 // Tiling: a 256-thread workgroup (4 waves of 64) computes a 128x128 tile of C;
 // each wave owns a 64x64 sub-tile = 2x2 v_mfma_f32_32x32x16_bf16 accumulators
-// (64 fp32 per lane).  K advances in tiles of 64 through two LDS buffers; the
-// global loads of tile t+2 are issued before the MFMAs of tile t, into one of
-// two register sets, so each load has two compute phases to arrive.  LDS
-// tiles hold 128 rows x 64 k (128 B per row) with an XOR swizzle of the
-// 16-byte chunks so that the 128-bit MFMA operand reads and the stores of
-// k-contiguous operands are bank-conflict free.  Operands whose rows are
-// contiguous in memory (weight gradients, input gradients through W) are
-// transposed on their way into LDS (k pairs packed into 32-bit stores).
+// (64 fp32 per lane).  Four kernels share the tile, its XCD-aware order and its
+// fused epilogue:
+//  - gemm_kernel: the general form (any operand layout, unaligned sizes,
+//    implicit-GEMM convolution operands).  K advances in tiles of 64 through
+//    two LDS buffers, staged through registers; LDS tiles hold 128 rows x 64 k
+//    with an XOR swizzle of the 16-byte chunks.  Operands whose rows are
+//    contiguous in memory are either transposed on their way into LDS (k
+//    pairs packed into 32-bit stores) or stored [k][row] and read back with
+//    the LDS transpose read.
+//  - gemm_comp_dma_kernel: compensated products of row-major operands
+//    (A.B + A.B_lo + A_lo.B in one pass over K), tiles copied straight into
+//    LDS by global_load_lds in a two-stage ring.
+//  - gemm_wgrad_dma_kernel: groups of products of two k-major operands
+//    (weight gradients), tiles copied into LDS in the [k][row] layout and read
+//    by transpose reads, four-stage ring.
+//  - gemm_rk_krt_dma_kernel: row-major A times k-major B (input gradients),
+//    the same copies and ring.
 #include <algorithm>
 #include <type_traits>
 
@@ -1061,14 +1070,6 @@ __device__ __forceinline__ void for_group_tiles(const GemmGroupArg& g, F&& f) {
         f(d, job, Mm, Km);
         __syncthreads();  // the next tile's stores reuse the LDS of this one's C tile
     }
-}
-
-template <int AM, int BMODE, bool AL>
-__global__ void __launch_bounds__(NT, 2) gemm_group_kernel(const GemmGroupArg g) {
-    __shared__ __attribute__((aligned(16))) GemmSmem smem;
-    for_group_tiles(g, [&](const GemmDesc& d, const TileJob& job, int M, int K) {
-        gemm_tile<AM, BMODE, AL>(d, job, M, K, smem);
-    });
 }
 
 // ------------------------------------------------------------------ single-pass compensated product
