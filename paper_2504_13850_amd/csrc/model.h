@@ -64,6 +64,14 @@ struct Family {
     void (*destroy)(fo_model* m);
 };
 
+// Orders `to` after everything enqueued so far on `from` (a fork or a join of
+// two streams of one model; inside a capture it becomes a graph edge).
+inline fo_status order_after(hipStream_t to, hipStream_t from, hipEvent_t e) {
+    FO_HIP(hipEventRecord(e, from));
+    FO_HIP(hipStreamWaitEvent(to, e, 0));
+    return FO_OK;
+}
+
 // Accessors (function-local statics keep the tables out of device code).
 const Family* family_cnn32();   // config 1
 const Family* family_cnn16();   // configs 2, 3, 5

@@ -544,12 +544,6 @@ fo_status init(fo_model* m) {
     return FO_OK;
 }
 
-// Orders `to` after everything enqueued so far on `from`.
-fo_status order_after(hipStream_t to, hipStream_t from, hipEvent_t e) {
-    FO_HIP(hipEventRecord(e, from));
-    FO_HIP(hipStreamWaitEvent(to, e, 0));
-    return FO_OK;
-}
 
 #define TRY(x)                           \
     do {                                 \
