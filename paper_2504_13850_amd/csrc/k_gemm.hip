@@ -40,6 +40,9 @@ constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
 // workgroups per CU: deeper rings at one workgroup per CU starve the
 // concurrent input-gradient chain of LDS).
 constexpr int kWgradKT = 32, kWgradNST = 4, kDgradKT = 32, kDgradNST = 4;
+#ifndef WGRAD_TALL
+#define WGRAD_TALL 1
+#endif
 constexpr int NV = BM * BK / 8 / NT;  // 16-byte vectors per thread per operand per K tile (4)
 
 // LDS tiles are 128 rows x 64 k with rows padded to 72 elements (144 B = 36
@@ -202,7 +205,8 @@ struct LdKR {
 // k row (256 B).  Row segments of 32 elements (64 B) are XOR-swizzled by
 // k mod 4: the four k rows that half a wave's transpose read touches then fall
 // in distinct 64-byte bank groups.
-__device__ __forceinline__ int kr_idx(int k, int r) { return k * BM + (r ^ ((k & 3) << 5)); }
+template <int R = BM>
+__device__ __forceinline__ int kr_idx(int k, int r) { return k * R + (r ^ ((k & 3) << 5)); }
 
 struct LdKRt {
     int64_t base;  // element offset of (k row kr, row r0 + 8 c)
@@ -251,10 +255,11 @@ __device__ __forceinline__ bf16x8_t frag_tr(const bf16_t* T, int2 off, int kadd)
     const s16x8_t v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
     return __builtin_bit_cast(bf16x8_t, v);
 }
+template <int R = BM>
 __device__ __forceinline__ int2 frag_tr_off(int lane, int row0) {
     const int g = lane >> 4, s = lane & 15;
     const int k = 8 * (g >> 1) + (s >> 2), r = row0 + 16 * (g & 1) + 4 * (s & 3);
-    return make_int2(kr_idx(k, r), kr_idx(k + 4, r));
+    return make_int2(kr_idx<R>(k, r), kr_idx<R>(k + 4, r));
 }
 
 // Conv forward A: rows = output pixels (b, oy, ox); k = (ky, kx, ci), Ci % 64 == 0
@@ -773,24 +778,15 @@ __device__ __forceinline__ bool map_tile(const GemmDesc& d, int M, int ktot_spli
 // whole product runs the epilogue (and the optional column sums).
 // BMt rows by NTt threads (4 waves of 64 x 64 per 128 rows); RP = NTt / 32 rows per
 // pass of the four-column path, HP = NTt / 128 row groups of the one-column path.
-template <int BMt = BM, int NTt = NT, int BNt = BN, int WNF = 2>
-__device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc)[2][WNF], float* Cs,
-                                           const TileJob& job, int M, int tid) {
+// drain_tile is the second half: from the tile staged in LDS (Cs[row][BNt]) to
+// memory, for rows job.m0 .. job.m0 + BMt - 1, the epilogue's operands of NB
+// rows loaded together.
+template <int BMt = BM, int NTt = NT, int BNt = BN, int NB = 8>
+__device__ __forceinline__ void drain_tile(const GemmDesc& d, float* Cs, const TileJob& job, int M, int tid) {
     // TPR threads per row in the four-column path, RP rows per pass; HP row
     // groups in the one-column path
     constexpr int TPR = BNt / 4, RP = NTt / TPR, HP = NTt / BNt;
-    static_assert(BNt == 32 * 2 * WNF && HP >= 1, "tile shape");
-    const int lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < WNF; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int lr = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                Cs[lr * BNt + wn * 32 * WNF + j * 32 + (lane & 31)] = acc[i][j][r];
-            }
-    __syncthreads();
+    static_assert(HP >= 1, "tile shape");
     if (d.vec_epi) {
         // four columns per thread: rows tid / TPR + RP u, columns n0 + 4 (tid % TPR) .. + 3
         const int m0 = job.m0, c4 = (tid % TPR) * 4, col = job.n0 + c4, rr = tid / TPR;
@@ -806,14 +802,14 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
 #pragma unroll
                     for (int q = 0; q < 4; ++q) bias[q] = d.bias[col + q];
                 }
-                for (int lr0 = rr; lr0 < BMt && m0 + lr0 < M; lr0 += 8 * RP) {
-                    EpiIn4 e[8];
-                    int rows[8];
+                for (int lr0 = rr; lr0 < BMt && m0 + lr0 < M; lr0 += NB * RP) {
+                    EpiIn4 e[NB];
+                    int rows[NB];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) rows[u] = min(m0 + lr0 + RP * u, M - 1);
+                    for (int u = 0; u < NB; ++u) rows[u] = min(m0 + lr0 + RP * u, M - 1);
                     epi_load4_batch(d, rows, col, e);
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) {
+                    for (int u = 0; u < NB; ++u) {
                         const int lr = lr0 + RP * u, row = m0 + lr;
                         if (row < M)
                             csum += epi_store4(d, row, col,
@@ -847,15 +843,15 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
             }
         } else {
             const float bcol = d.bias ? d.bias[col] : 0.f;
-            // eight rows per batch: their operand loads are in flight together
-            for (int lr0 = tid / BNt; lr0 < BMt && m0 + lr0 < M; lr0 += 8 * HP) {
-                EpiIn e[8];
-                int rows[8];
+            // NB rows per batch: their operand loads are in flight together
+            for (int lr0 = tid / BNt; lr0 < BMt && m0 + lr0 < M; lr0 += NB * HP) {
+                EpiIn e[NB];
+                int rows[NB];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) rows[u] = min(m0 + lr0 + HP * u, M - 1);
+                for (int u = 0; u < NB; ++u) rows[u] = min(m0 + lr0 + HP * u, M - 1);
                 epi_load_batch(d, rows, col, e);
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
+                for (int u = 0; u < NB; ++u) {
                     const int lr = lr0 + HP * u, row = m0 + lr;
                     if (row < M) csum += epi_store(d, row, col, Cs[lr * BNt + c] + bcol + e[u].resid, e[u]);
                 }
@@ -873,6 +869,24 @@ __device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc
             d.colpart[(int64_t)job.mt * d.N + col] = t;
         }
     }
+}
+
+template <int BMt = BM, int NTt = NT, int BNt = BN, int WNF = 2>
+__device__ __forceinline__ void store_tile(const GemmDesc& d, const f32x16 (&acc)[2][WNF], float* Cs,
+                                           const TileJob& job, int M, int tid) {
+    static_assert(BNt == 32 * 2 * WNF, "tile shape");
+    const int lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < WNF; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int lr = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                Cs[lr * BNt + wn * 32 * WNF + j * 32 + (lane & 31)] = acc[i][j][r];
+            }
+    __syncthreads();
+    drain_tile<BMt, NTt, BNt>(d, Cs, job, M, tid);
 }
 
 // Two K tiles (A and B each 128 x 72 bf16) = 72 KB of LDS; reused for the C tile.
@@ -1018,8 +1032,9 @@ struct GemmGroupArg {
     int* prof_snap;  // (M, K) effective per member, when profiling
 };
 
-// Calls f(d, job, M, K) for each tile of a group that this workgroup owns.
-template <class F>
+// Calls f(d, job, M, K) for each BMt x 128 tile of a group that this
+// workgroup owns.
+template <int BMt = BM, class F>
 __device__ __forceinline__ void for_group_tiles(const GemmGroupArg& g, F&& f) {
     constexpr int GM = 8;
     int Ms[kGemmGroupMax], Ks[kGemmGroupMax], start[kGemmGroupMax + 1];
@@ -1029,7 +1044,7 @@ __device__ __forceinline__ void for_group_tiles(const GemmGroupArg& g, F&& f) {
         const GemmDesc& d = g.d[i < g.n ? i : 0];
         Ms[i] = d.Mdev ? min(d.M, *d.Mdev) : d.M;
         Ks[i] = d.Kdev ? min(d.K, *d.Kdev) : d.K;
-        const int tiles = ((Ms[i] + BM - 1) / BM) * ((d.N + BN - 1) / BN);
+        const int tiles = ((Ms[i] + BMt - 1) / BMt) * ((d.N + BN - 1) / BN);
         start[i + 1] = start[i] + (i < g.n ? tiles : 0);
     }
     if (g.prof_snap && blockIdx.x == 0 && threadIdx.x == 0) {
@@ -1058,12 +1073,12 @@ __device__ __forceinline__ void for_group_tiles(const GemmGroupArg& g, F&& f) {
             }
         const GemmDesc& d = g.d[m];
         const int tt = nid - s0;
-        const int nN = (d.N + BN - 1) / BN, nMe = (Mm + BM - 1) / BM;
+        const int nN = (d.N + BN - 1) / BN, nMe = (Mm + BMt - 1) / BMt;
         const int grp = tt / (GM * nN), tg = tt - grp * GM * nN;
         const int gr = min(GM, nMe - grp * GM);
         TileJob job;
         job.mt = grp * GM + tg % gr;
-        job.m0 = job.mt * BM;
+        job.m0 = job.mt * BMt;
         job.n0 = (tg / gr) * BN;
         job.zt = 0;
         job.S = 1;
@@ -1306,34 +1321,39 @@ __device__ __forceinline__ bf16x8_t frag_cat(i32x2_t a, i32x2_t b) {
 }
 
 // Both operands k-major (A = [K][M], B = [K][N], the rows of a tile contiguous
-// in memory), as in the products of weight gradients.  The tiles keep the
-// [k][row] layout of the transposed loaders (kr_idx) that the transpose reads
-// take their fragments from, but are filled by global_load_lds: instruction i
-// of the workgroup writes k rows 4i .. 4i + 3, lane L its 16-byte slot L of
-// them, which under the swizzle is k row 4i + L / 16 and the eight rows
-// 8 ((L mod 16) xor 4 (L / 16)) .. + 7.  No staging registers and no LDS store
-// instructions; the waits name exactly the tile the next step reads.
-template <int KT>
+// in memory), as in the products of weight gradients.  The tiles (KT k rows of
+// RT operand rows) keep the [k][row] layout of the transposed loaders (kr_idx)
+// that the transpose reads take their fragments from, but are filled by
+// global_load_lds: a k row is RT / 8 16-byte chunks, so instruction i of the
+// workgroup writes KPI = 64 / (RT / 8) k rows from KPI i on, lane L its 16-byte
+// slot L of them, which under the swizzle is k row k = KPI i + L / (RT / 8) and
+// the eight rows 8 ((L mod RT / 8) xor 4 (k mod 4)) .. + 7.  No staging
+// registers and no LDS store instructions; the waits name exactly the tile
+// the next step reads.
+template <int KT, int RT = BM>
 struct DmaKRt {
-    static_assert(KT % 32 == 0 && KT <= 64, "tile depth");
-    static constexpr int NI = KT / 16;  // instructions per wave and operand tile (KT / 4 per workgroup)
-    int64_t off[NI];                    // element offset of the lane's chunk at k = 0, -1 outside the rows
+    static constexpr int CPR = RT / 8;     // 16-byte chunks per k row
+    static constexpr int KPI = 64 / CPR;   // k rows per copy instruction
+    static constexpr int NI = KT / KPI / 4;  // instructions per wave and operand tile
+    static_assert((RT == 128 || RT == 256) && KT % (4 * KPI) == 0 && KT <= 64, "tile shape");
+    // Instruction v of a wave covers k row kk0 + 4 KPI v; k mod 4, hence the
+    // lane's rows, is the same for every v (4 KPI is a multiple of 4).
+    int64_t off0;  // element offset of the lane's chunk at k = kk0 (-1 outside the rows)
     int64_t ld;
-    int kk[NI];
+    int kk0;
     __device__ void init(int64_t ld_, int r0, int R, int lane, int wave) {
         ld = ld_;
-        const int sub = lane >> 4, r = r0 + 8 * ((lane & 15) ^ (4 * sub));
-#pragma unroll
-        for (int v = 0; v < NI; ++v) {
-            kk[v] = 4 * (wave + 4 * v) + sub;
-            off[v] = r < R ? (int64_t)kk[v] * ld + r : -1;
-        }
+        const int sub = lane / CPR, slot = lane % CPR;
+        kk0 = KPI * wave + sub;
+        const int r = r0 + 8 * (slot ^ (4 * (kk0 & 3)));
+        off0 = r < R ? (int64_t)kk0 * ld + r : -1;
     }
     __device__ void copy(const bf16_t* P, int kb, int kend, bf16_t* tile, int wave) const {
-        const int64_t kofs = (int64_t)kb * ld;
+        const bf16_t* p = P + off0 + (int64_t)kb * ld;
 #pragma unroll
         for (int v = 0; v < NI; ++v)
-            __builtin_amdgcn_global_load_lds(off[v] >= 0 && kb + kk[v] < kend ? P + off[v] + kofs : kZero8,
+            __builtin_amdgcn_global_load_lds(off0 >= 0 && kb + kk0 + 4 * KPI * v < kend ? p + (int64_t)4 * KPI * v * ld
+                                                                                          : kZero8,
                                              FO_LDS(tile + (wave + 4 * v) * 512), 16, 0, 0);
     }
 };
@@ -1432,6 +1452,132 @@ __global__ void __launch_bounds__(NT, 2) gemm_wgrad_dma_kernel(const GemmGroupAr
     __shared__ __attribute__((aligned(1024))) bf16_t smem[NST][2][KT * BM];
     for_group_tiles(g, [&](const GemmDesc& d, const TileJob& job, int M, int K) {
         wgrad_tile<KT, NST>(d, job, M, K, smem);
+    });
+}
+
+// Tall tiles: 256 x 128 per workgroup, 128 x 64 per wave (4 x 2 accumulators),
+// for groups that run beside other work with a capped grid.  Per MFMA they
+// read a quarter fewer operand bytes than 128 x 128 tiles (A 256 rows, B 128
+// rows per k).  Three 24 KB stages of KT = 32 (two workgroups per CU); the C
+// tile leaves in two 128-row halves through the stages.
+__device__ __forceinline__ void lgkm_wait_tr12(i32x2_t (&r)[12]) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7]),
+                   "+v"(r[8]), "+v"(r[9]), "+v"(r[10]), "+v"(r[11]));
+}
+
+constexpr int kTallRows = 2 * BM;
+
+template <int KT, int NST>
+__device__ __forceinline__ void wgrad_tall_tile(const GemmDesc& d, const TileJob& job, int M, int K,
+                                                bf16_t (*smem)[KT * (kTallRows + BN)]) {
+    constexpr int RA = kTallRows, RB = BN, SA = KT * RA, SB = KT * RB;
+    static_assert(NST * (SA + SB) * 2 >= BM * BN * 4, "a 128-row half of the C tile lives in the stages");
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int nk = (K + KT - 1) / KT;
+    DmaKRt<KT, RA> la;
+    DmaKRt<KT, RB> lb;
+    la.init(d.lda, job.m0, M, lane, wave);
+    lb.init(d.ldb, job.n0, d.N, lane, wave);
+
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    constexpr int CPT = DmaKRt<KT, RA>::NI + DmaKRt<KT, RB>::NI;  // copy instructions per tile and thread
+    auto copy_tile = [&](int st, int t) {
+        const int kb = t * KT, ke = t < nk ? K : 0;
+        la.copy(d.A, kb, ke, smem[st], wave);
+        lb.copy(d.B, kb, ke, smem[st] + SA, wave);
+    };
+    // byte addresses in LDS of this lane's transpose reads for k block 0 of
+    // stage 0: A fragments i = 0..3 (rows 128 wm + 32 i), then B fragments
+    // j = 0, 1 (rows 64 wn + 32 j); two reads each (first and second four k)
+    const uint32_t sbase = lds_addr(&smem[0][0]);
+    uint32_t ra[12];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int2 o = frag_tr_off<RA>(lane, wm * 128 + 32 * i);
+        ra[2 * i] = sbase + 2 * o.x;
+        ra[2 * i + 1] = sbase + 2 * o.y;
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int2 o = frag_tr_off<RB>(lane, wn * 64 + 32 * j);
+        ra[8 + 2 * j] = sbase + 2 * SA + 2 * o.x;
+        ra[9 + 2 * j] = sbase + 2 * SA + 2 * o.y;
+    }
+    // k blocks of 16: twelve reads, then the block's eight MFMAs (which run
+    // while the next block's reads are issued)
+    auto compute = [&](int st) {
+        const uint32_t so = (uint32_t)st * ((SA + SB) * 2);
+#pragma unroll
+        for (int kb16 = 0; kb16 < KT / 16; ++kb16) {
+            i32x2_t r[12];
+            const uint32_t ka = kb16 * 16 * RA * 2, kb = kb16 * 16 * RB * 2;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) r[q] = tr_read(ra[q] + so + ka);
+#pragma unroll
+            for (int q = 8; q < 12; ++q) r[q] = tr_read(ra[q] + so + kb);
+            lgkm_wait_tr12(r);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        frag_cat(r[2 * i], r[2 * i + 1]), frag_cat(r[8 + 2 * j], r[9 + 2 * j]), acc[i][j], 0, 0, 0);
+        }
+    };
+    auto step = [&](int t, int u) {
+        copy_tile((u + NST - 1) % NST, t + NST - 1);
+        compute(u);
+        __builtin_amdgcn_s_waitcnt(vmcnt_lds0_imm(CPT * (NST - 2)));  // tile t + 1 has landed
+        ring_barrier();
+    };
+#pragma unroll
+    for (int u = 0; u < NST - 1; ++u) copy_tile(u, u);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPT * (NST - 2)));  // tile 0 has landed
+    ring_barrier();
+    int t = 0;
+    for (; t + NST <= nk; t += NST) {  // whole rounds: static stage indices
+#pragma unroll
+        for (int u = 0; u < NST; ++u) step(t + u, u);
+    }
+    for (int u = 0; t < nk; ++t, ++u) step(t, u);
+    __builtin_amdgcn_s_waitcnt(0);  // copies past the last tile
+    // the two 128-row halves: waves 2h and 2h + 1 stage half h, all drain it
+    float* Cs = reinterpret_cast<float*>(&smem[0][0]);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        __syncthreads();  // the stages (h = 0) or the first half (h = 1) are free
+        if (wm == h) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int lr = i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                        Cs[lr * BN + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+                    }
+        }
+        __syncthreads();
+        TileJob half = job;
+        half.m0 = job.m0 + h * BM;
+        drain_tile<BM, NT, BN, 4>(d, Cs, half, M, tid);  // four-row batches: the other half's accumulators stay live
+    }
+}
+
+template <int KT, int NST>
+__global__ void __launch_bounds__(NT, 2) gemm_wgrad_tall_kernel(const GemmGroupArg g) {
+    __shared__ __attribute__((aligned(1024))) bf16_t smem[NST][KT * (kTallRows + BN)];
+    for_group_tiles<kTallRows>(g, [&](const GemmDesc& d, const TileJob& job, int M, int K) {
+        wgrad_tall_tile<KT, NST>(d, job, M, K, smem);
     });
 }
 
@@ -1690,7 +1836,7 @@ fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s, int max_wg) {
     }
     GemmGroupArg g;
     g.n = n;
-    int tiles = 0;
+    int tiles = 0, tall_tiles = 0;
     ProfInfo pi;
     pi.kind = PROF_GEMM;
     pi.ngroup = n;
@@ -1712,15 +1858,21 @@ fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s, int max_wg) {
         g.d[i].prof_snap = nullptr;
         if (i < n) {
             tiles += (int)(cdiv(d.M, BM) * cdiv(d.N, BN));
+            tall_tiles += (int)(cdiv(d.M, kTallRows) * cdiv(d.N, BN));
             pi.gN[i] = d.N;
         }
     }
+    const bool tall = WGRAD_TALL == 2 || (WGRAD_TALL == 1 && max_wg > 0);
     hipEvent_t ea, eb;
-    const int h = prof_begin_ext("gemm_wgrad_dma_kernel", pi, &ea, &eb);
+    const int h = prof_begin_ext(tall ? "gemm_wgrad_tall_kernel" : "gemm_wgrad_dma_kernel", pi, &ea, &eb);
     g.prof_snap = prof_snap(h);
-    int grid = tiles;
+    int grid = tall ? tall_tiles : tiles;
     if (max_wg > 0 && grid > max_wg) grid = std::max(8, max_wg / 8 * 8);
-    hipExtLaunchKernelGGL((gemm_wgrad_dma_kernel<kWgradKT, kWgradNST>), dim3(grid), dim3(NT), 0, s, ea, eb, 0, g);
+    if (tall)
+        hipExtLaunchKernelGGL((gemm_wgrad_tall_kernel<32, 3>), dim3(grid), dim3(NT), 0, s, ea, eb, 0, g);
+    else
+        hipExtLaunchKernelGGL((gemm_wgrad_dma_kernel<kWgradKT, kWgradNST>), dim3(grid), dim3(NT), 0, s, ea, eb, 0,
+                              g);
     prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;
