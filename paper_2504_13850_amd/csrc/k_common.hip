@@ -107,6 +107,42 @@ __global__ void __launch_bounds__(256) colsum_partial(const T* __restrict__ X, i
         part[(int64_t)blockIdx.y * N + col] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
 }
 
+// colsum_partial over several matrices: blocks are dealt to the jobs in order,
+// job i taking ceil(N_i / 64) x ceil(rows_i / CS_ROWS) of them (column blocks
+// fastest); the arithmetic per column is colsum_partial's.
+__global__ void __launch_bounds__(256) colsum_partial_multi(const ColPartJobs jobs) {
+    __shared__ float red[4][64];
+    int bid = blockIdx.x, ji = 0;
+    for (; ji < jobs.n - 1; ++ji) {
+        const int nb = ((jobs.j[ji].N + 63) / 64) * ((jobs.j[ji].rows + CS_ROWS - 1) / CS_ROWS);
+        if (bid < nb) break;
+        bid -= nb;
+    }
+    const ColPartJob& J = jobs.j[ji];
+    const int ncb = (J.N + 63) / 64;
+    const int by = bid / ncb, bx = bid - by * ncb;
+    const int r0 = by * CS_ROWS;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = bx * 64 + lane;
+    const int r1 = min(J.rows, r0 + CS_ROWS);
+    float s = 0.f;
+    if (col < J.N) {
+        int r = r0 + wave;
+        for (; r + 28 < r1; r += 32) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = J.X[(int64_t)(r + 4 * u) * J.ld + col];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; r < r1; r += 4) s += J.X[(int64_t)r * J.ld + col];
+    }
+    red[wave][lane] = s;
+    __syncthreads();
+    if (wave == 0 && col < J.N)
+        J.part[(int64_t)by * J.N + col] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+}
+
 // part[p][N] for p < ceil(min(rows, *rows_dev) / rows_per_part); column col
 // goes to out.p[col / out.seg][col % out.seg].
 __global__ void __launch_bounds__(256) colsum_finish(const float* __restrict__ part, int rows,
@@ -348,8 +384,40 @@ fo_status launch_colsum_finish(const float* part, int rows, const int* rows_dev,
     return FO_OK;
 }
 
+fo_status launch_colsum_partial_multi(const ColPartJobs& jobs, hipStream_t s) {
+    FO_CHECK(jobs.n >= 1 && jobs.n <= kColJobsMax, "colsum: %d jobs", jobs.n);
+    int64_t blocks = 0;
+    for (int i = 0; i < jobs.n; ++i) {
+        const ColPartJob& J = jobs.j[i];
+        FO_CHECK(J.X && J.part && J.N > 0 && J.rows > 0 && J.ld >= J.N, "colsum: bad partial job %d", i);
+        blocks += cdiv(J.N, 64) * cdiv(J.rows, CS_ROWS);
+    }
+    hipLaunchKernelGGL(colsum_partial_multi, dim3((unsigned)blocks), dim3(256), 0, s, jobs);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+void ColSums::add(const float* X, int64_t ld, int rows, int N, float* part, float* out) {
+    if (parts.n >= kColJobsMax) {  // launch_colsums refuses the set
+        parts.n = kColJobsMax + 1;
+        return;
+    }
+    ColPartJob& p = parts.j[parts.n++];
+    p.X = X; p.ld = ld; p.rows = rows; p.N = N; p.part = part;
+    ColJob& f = fin.j[fin.n++];
+    f.part = part; f.rows = rows; f.rows_per_part = CS_ROWS; f.N = N;
+    f.out.p[0] = out; f.out.seg = N;
+}
+
+fo_status launch_colsums(const ColSums& c, hipStream_t s) {
+    FO_CHECK(c.parts.n <= kColJobsMax, "colsum: more than %d matrices in one pass", kColJobsMax);
+    if (c.parts.n == 0) return FO_OK;
+    fo_status st = launch_colsum_partial_multi(c.parts, s);
+    return st != FO_OK ? st : launch_colsum_finish_multi(c.fin, s);
+}
+
 fo_status launch_colsum_finish_multi(const ColJobs& jobs, hipStream_t s) {
-    FO_CHECK(jobs.n >= 1 && jobs.n <= 4, "colsum: %d jobs", jobs.n);
+    FO_CHECK(jobs.n >= 1 && jobs.n <= kColJobsMax, "colsum: %d jobs", jobs.n);
     int blocks = 0;
     for (int i = 0; i < jobs.n; ++i) {
         const ColJob& J = jobs.j[i];

@@ -87,7 +87,8 @@ struct ColOut {
 fo_status launch_colsum_finish(const float* part, int rows, const int* rows_dev, int rows_per_part, int N,
                                const ColOut& out, hipStream_t s);
 // Several finishing passes in one launch: job i adds the partial rows of part_i
-// (as launch_colsum_finish) into out_i; at most four jobs.
+// (as launch_colsum_finish) into out_i; at most kColJobsMax jobs.
+constexpr int kColJobsMax = 16;
 struct ColJob {
     const float* part = nullptr;
     int rows = 0, rows_per_part = 1, N = 0;
@@ -95,10 +96,33 @@ struct ColJob {
     ColOut out;
 };
 struct ColJobs {
-    ColJob j[4];
+    ColJob j[kColJobsMax];
     int n = 0;
 };
 fo_status launch_colsum_finish_multi(const ColJobs& jobs, hipStream_t s);
+// Several first passes of launch_colsum (fp32 matrices) in one launch: job i
+// writes the partial rows of X_i [rows_i][N_i] (leading dimension ld_i) to
+// part_i, with colsum_partial's arithmetic; at most kColJobsMax jobs.
+struct ColPartJob {
+    const float* X = nullptr;
+    int64_t ld = 0;
+    int rows = 0, N = 0;
+    float* part = nullptr;
+};
+struct ColPartJobs {
+    ColPartJob j[kColJobsMax];
+    int n = 0;
+};
+fo_status launch_colsum_partial_multi(const ColPartJobs& jobs, hipStream_t s);
+// A pass over several fp32 matrices: adds each X_i's column sums to out_i,
+// as launch_colsum would, in two launches whatever the count (part_i holds
+// colsum_ws_floats(rows_i, N_i) floats each, distinct).
+struct ColSums {
+    ColPartJobs parts;
+    ColJobs fin;
+    void add(const float* X, int64_t ld, int rows, int N, float* part, float* out);
+};
+fo_status launch_colsums(const ColSums& c, hipStream_t s);
 // The first pass of launch_colsum alone: ws receives the partial rows (CS_ROWS
 // rows each) that launch_colsum_finish (rows_per_part = colsum_rows_per_part())
 // completes.

@@ -249,13 +249,17 @@ struct Plan {
     LayerP* ly;        // [layers] (host array)
     const float *wc, *bc;
     float *gwc, *gbc;
-    float *dz, *dy, *du2, *df, *dh1, *du1, *dO, *dqkv, *dx, *gx;
+    float *dz, *dy, *du2, *df, *dh1, *du1, *dO, *dqkv, *dx, *gx, *gx1;
     float* part;       // split-K slices
     float* colws;      // column-sum workspace
+    float* sumws;      // partial rows of a layer's kLayerSums column sums
     size_t part_floats;
 };
 
 constexpr int kMaxSlices = 16;
+// column sums per layer in the backward: the biases of the four products and
+// the two norms' gain and shift
+constexpr int kLayerSums = 8;
 
 size_t ws_bytes(const fo_model* m) {
     const Arch a = arch_of(m->cid);
@@ -278,8 +282,10 @@ size_t ws_bytes(const fo_model* m) {
     add(4 * Bm * NCLS);                                               // dz
     for (int i = 0; i < 8; ++i) add(4 * R * 3 * D);                   // dy, du2, df, dh1, du1, dO, dqkv, dx (+gx)
     add(4 * R * D);                                                   // gx
+    add(4 * R * D);                                                   // gx1
     add(4 * (size_t)kMaxSlices * 3 * D * D);                          // part
     add(4 * colsum_ws_floats((int)R, 3 * D));                         // colws
+    add(4 * kLayerSums * colsum_ws_floats((int)R, 3 * D));            // sumws
     return s;
 }
 
@@ -332,10 +338,12 @@ fo_status init(fo_model* m) {
     float** bufs[8] = {&P->dy, &P->du2, &P->df, &P->dh1, &P->du1, &P->dO, &P->dqkv, &P->dx};
     for (float** b : bufs) *b = ar.take<float>(R * 3 * D);
     P->gx = ar.take<float>(R * D);
+    P->gx1 = ar.take<float>(R * D);
     P->part_floats = (size_t)kMaxSlices * 3 * D * D;
     P->part = ar.take<float>(P->part_floats);
     P->colws = ar.take<float>(colsum_ws_floats((int)R, 3 * D));
-    if (!P->colws) {
+    P->sumws = ar.take<float>(kLayerSums * colsum_ws_floats((int)R, 3 * D));
+    if (!P->sumws) {
         set_error("tfsmall: workspace arena too small");
         return FO_ENOMEM;
     }
@@ -461,30 +469,37 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         hipLaunchKernelGGL(ln_small_bwd, dim3((int)cdiv(R, 4)), dim3(256), 0, s, dy, Y.xh2, Y.rs2, Y.g2, P->du2,
                            P->gx, R);
         FO_LAUNCHED();
-        TRY(colsum(c, P->gx, R, D, Y.gg2));
-        TRY(colsum(c, dy, R, D, Y.gb2n));
+        // The layer's eight column sums (biases, norm gains and shifts) run as
+        // one pass at the end of the layer, over buffers that stay intact until then.
+        ColSums sums;
+        const size_t sw = colsum_ws_floats(R, 3 * D);
+        auto sum = [&](const float* X, int N, float* out) {
+            sums.add(X, N, R, N, P->sumws + sums.parts.n * sw, out);
+        };
+        sum(P->gx, D, Y.gg2);
+        sum(dy, D, Y.gb2n);
         // FFN2 and FFN1 (ReLU mask from the stored activation)
         TRY(linear_dw(c, P->du2, Y.f, nullptr, Y.gw2, R, D, FF));
-        TRY(colsum(c, P->du2, R, D, Y.gb2));
+        sum(P->du2, D, Y.gb2);
         Gf gdf = linear_dx(P->du2, Y.w2, P->df, R, D, FF);
         gdf.mask = Y.f;
         gdf.ldmask = FF;
         TRY(gemm(c, gdf));
         TRY(linear_dw(c, P->df, Y.h1, nullptr, Y.gw1, R, FF, D));
-        TRY(colsum(c, P->df, R, FF, Y.gb1));
+        sum(P->df, FF, Y.gb1);
         Gf gdh = linear_dx(P->df, Y.w1, P->dh1, R, FF, D);  // dh1 = du2 + df W1
         gdh.add = P->du2;
         gdh.ldadd = D;
         TRY(gemm(c, gdh));
         // LN1
         hipLaunchKernelGGL(ln_small_bwd, dim3((int)cdiv(R, 4)), dim3(256), 0, s, P->dh1, Y.xh1, Y.rs1, Y.g1, P->du1,
-                           P->gx, R);
+                           P->gx1, R);
         FO_LAUNCHED();
-        TRY(colsum(c, P->gx, R, D, Y.gg1));
-        TRY(colsum(c, P->dh1, R, D, Y.gb1n));
+        sum(P->gx1, D, Y.gg1);
+        sum(P->dh1, D, Y.gb1n);
         // output projection
         TRY(linear_dw(c, P->du1, Y.O, nullptr, Y.gwo, R, D, D));
-        TRY(colsum(c, P->du1, R, D, Y.gbo));
+        sum(P->du1, D, Y.gbo);
         TRY(gemm(c, linear_dx(P->du1, Y.wo, P->dO, R, D, D)));
         // attention
         if (dh == 20)
@@ -496,7 +511,8 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         FO_LAUNCHED();
         // QKV projection (no input gradient for the first server layer: nothing is sent back)
         TRY(linear_dw(c, P->dqkv, x, inx, Y.gwqkv, R, 3 * D, D));
-        TRY(colsum(c, P->dqkv, R, 3 * D, Y.gbqkv));
+        sum(P->dqkv, 3 * D, Y.gbqkv);
+        TRY(launch_colsums(sums, s));
         if (l > 0) {
             Gf gx = linear_dx(P->dqkv, Y.wqkv, dx, R, 3 * D, D);  // dx = du1 + dqkv Wqkv
             gx.add = P->du1;
