@@ -57,6 +57,8 @@ struct Conv {
     bf16_t *yh, *yl;            // VGG: post-ReLU output (hi, lo)
     float *z, *mean, *rstd;     // ResNet: pre-norm output and its batch statistics
     float* part;                // ResNet: the norm's per-row-block partial sums
+    float *dzf, *dzpart;        // VGG: fp32 gradient of the pre-activation, and the
+                                // partial rows of its column sums (the bias gradient)
 };
 
 struct Pool {
@@ -211,7 +213,7 @@ size_t ws_bytes(const fo_model* m) {
         const size_t n = (size_t)B * c.Ho * c.Wo * c.cout;
         amax = std::max(amax, n);
         if (P.resnet) { add(4 * n); add(4 * c.cout); add(4 * c.cout); add(4 * bn_ws_floats(B * c.Ho * c.Wo, c.cout)); }
-        else { add(2 * n); add(2 * n); }
+        else { add(2 * n); add(2 * n); add(4 * n); add(4 * colsum_ws_floats(B * c.Ho * c.Wo, c.cout)); }
         sw = std::max(sw, gemm_ws_bytes(c.cout, c.k * c.k * c.cin, c.splits));
         sw = std::max(sw, gemm_ws_bytes(B * c.Ho * c.Wo, c.cout, c.fsplits));
         sw = std::max(sw, gemm_ws_bytes(B * c.H * c.W, c.cin, c.dsplits));
@@ -231,6 +233,7 @@ size_t ws_bytes(const fo_model* m) {
     for (const Fc& f : P.fcs) {
         add(2 * (size_t)B * f.out); add(2 * (size_t)B * f.out);
         red = std::max(red, colsum_ws_floats(B, f.out));
+        red = std::max(red, 3 * colsum_ws_floats(B, 512));  // VGG: the classifier's three bias sums together
     }
     add(4 * (size_t)B * 512); add(2 * (size_t)B * 512); add(2 * (size_t)B * 512);
     add(4 * (size_t)B * 128); add(2 * (size_t)B * 128);
@@ -260,9 +263,12 @@ fo_status init(fo_model* m) {
             c.mean = a.take<float>(c.cout);
             c.rstd = a.take<float>(c.cout);
             c.part = a.take<float>(bn_ws_floats(B * c.Ho * c.Wo, c.cout));
+            c.dzf = c.dzpart = nullptr;
         } else {
             c.yh = a.take<bf16_t>(n);
             c.yl = a.take<bf16_t>(n);
+            c.dzf = a.take<float>(n);
+            c.dzpart = a.take<float>(colsum_ws_floats(B * c.Ho * c.Wo, c.cout));
         }
         sw = std::max(sw, gemm_ws_bytes(c.cout, c.k * c.k * c.cin, c.splits));
         sw = std::max(sw, gemm_ws_bytes(B * c.Ho * c.Wo, c.cout, c.fsplits));
@@ -289,6 +295,7 @@ fo_status init(fo_model* m) {
         f.yh = a.take<bf16_t>((size_t)B * f.out);
         f.yl = a.take<bf16_t>((size_t)B * f.out);
         red = std::max(red, colsum_ws_floats(B, f.out));
+        red = std::max(red, 3 * colsum_ws_floats(B, 512));  // VGG: the classifier's three bias sums together
     }
     P->gap = a.take<float>((size_t)B * 512);
     P->gaph = a.take<bf16_t>((size_t)B * 512);
@@ -374,15 +381,19 @@ fo_status fc_fwd(fo_model* m, const Fc& f, int B, const bf16_t* xh, const bf16_t
 }
 
 // fully connected backward: weight and bias gradients, then the input gradient
+// (the bias gradient's column sums join `sums` when given, else run here)
 fo_status fc_bwd(fo_model* m, Plan* P, const Fc& f, int B, const float* dyf, const bf16_t* dyb, const bf16_t* xh,
-                 const bf16_t* mask, float* dxf, bf16_t* dxb) {
+                 const bf16_t* mask, float* dxf, bf16_t* dxb, ColSums* sums = nullptr, float* sum_part = nullptr) {
     GemmDesc w;
     w.M = f.out; w.N = f.in; w.K = B;
     w.amode = OP_KR; w.A = dyb; w.lda = f.out;
     w.bmode = OP_KR; w.B = xh; w.ldb = f.in;
     w.Cf = m->grads + f.w; w.ldcf = f.in;
     TRY(gemm(w, m->stream));
-    TRY(launch_colsum(dyf, f.out, B, nullptr, f.out, m->grads + f.b, P->redws, m->stream));
+    if (sums)
+        sums->add(dyf, f.out, B, f.out, sum_part, m->grads + f.b);
+    else
+        TRY(launch_colsum(dyf, f.out, B, nullptr, f.out, m->grads + f.b, P->redws, m->stream));
     if (dxf || dxb) {
         GemmDesc d;
         d.M = B; d.N = f.in; d.K = f.out;
@@ -421,16 +432,21 @@ fo_status step_vgg(fo_model* m, Plan* P, int B, const int32_t* labels) {
     TRY(fc_fwd(m, f1, B, f0.yh, f0.yl, true, nullptr, f1.yh, f1.yl));
     TRY(fc_fwd(m, f2, B, f1.yh, f1.yl, false, m->logits, nullptr, nullptr));
     TRY(launch_xent(m->logits, m->dev_in, P->dz, m->loss, B, f2.out, s));
-    // backward through the classifier
+    // backward through the classifier (its bias sums join the convs' pass at
+    // the end; dz, df[0] and df[1] stay intact until then)
+    ColSums bias_sums;
+    const size_t fcpart = colsum_ws_floats(B, 512);
     TRY(launch_to_bf16(P->dz, P->dzb, (int64_t)B * f2.out, s));
-    TRY(fc_bwd(m, P, f2, B, P->dz, P->dzb, f1.yh, f1.yh, P->df[0], P->db[0]));
-    TRY(fc_bwd(m, P, f1, B, P->df[0], P->db[0], f0.yh, f0.yh, P->df[1], P->db[1]));
+    TRY(fc_bwd(m, P, f2, B, P->dz, P->dzb, f1.yh, f1.yh, P->df[0], P->db[0], &bias_sums, P->redws));
+    TRY(fc_bwd(m, P, f1, B, P->df[0], P->db[0], f0.yh, f0.yh, P->df[1], P->db[1], &bias_sums, P->redws + fcpart));
     const Pool& last = P->pools.back();
-    TRY(fc_bwd(m, P, f0, B, P->df[1], P->db[1], last.yh, nullptr, P->df[2], nullptr));
-    // Backward through the convolutions.  df[0]/db[0] and df[1]/db[1] alternate
-    // as the gradient of a conv's pre-activation (fp32 for the bias sums, bf16
-    // for the GEMMs); df[2] holds the gradient of a pool's output.
-    const float* gf = P->df[2];
+    TRY(fc_bwd(m, P, f0, B, P->df[1], P->db[1], last.yh, nullptr, P->df[2], nullptr, &bias_sums,
+               P->redws + 2 * fcpart));
+    // Backward through the convolutions.  db[0] and db[1] alternate as the bf16
+    // gradient of a conv's pre-activation (the GEMMs' operand); its fp32 copy
+    // goes to the conv's own dzf, whose column sums (the bias gradients) run
+    // for all convs in one pass at the end.  df[2] holds the gradient of a
+    // pool's output.
     const bf16_t* gb = nullptr;
     int pf = 0;
     for (int idx = (int)P->order.size() - 1; idx >= 0; --idx) {
@@ -439,30 +455,29 @@ fo_status step_vgg(fo_model* m, Plan* P, int B, const int32_t* labels) {
             // pool: route to the window winner, mask with the producing conv's ReLU
             const Pool& p = P->pools[-op - 1];
             const Conv& prod = P->convs[P->order[idx - 1]];
-            TRY(launch_maxpool_relu_bwd(gf, p.arg, prod.yh, P->df[pf], P->db[pf], B, p.H, p.W, p.C, s));
-            gf = P->df[pf];
+            TRY(launch_maxpool_relu_bwd(P->df[2], p.arg, prod.yh, prod.dzf, P->db[pf], B, p.H, p.W, p.C, s));
             gb = P->db[pf];
             pf ^= 1;
             continue;
         }
         const Conv& c = P->convs[op];
-        TRY(launch_colsum(gf, c.cout, B * c.Ho * c.Wo, nullptr, c.cout, m->grads + c.b, P->redws, s));
+        bias_sums.add(c.dzf, c.cout, B * c.Ho * c.Wo, c.cout, c.dzpart, m->grads + c.b);
         const int prev = idx > 0 ? P->order[idx - 1] : 0;
         const bf16_t* in = idx == 0 ? P->xin : (prev >= 0 ? P->convs[prev].yh : P->pools[-prev - 1].yh);
         TRY(conv_wgrad(m, P, c, B, gb, in));
         if (idx == 0) break;  // the first server layer: no input gradient
         if (prev >= 0) {
             // the input is a conv's ReLU output: mask in the epilogue
-            TRY(conv_dgrad(m, c, B, gb, P->convs[prev].yh, nullptr, P->df[pf], P->db[pf]));
-            gf = P->df[pf];
+            const Conv& pc = P->convs[prev];
+            TRY(conv_dgrad(m, c, B, gb, pc.yh, nullptr, pc.dzf, P->db[pf]));
             gb = P->db[pf];
             pf ^= 1;
         } else {
             TRY(conv_dgrad(m, c, B, gb, nullptr, nullptr, P->df[2], nullptr));
-            gf = P->df[2];
             gb = nullptr;
         }
     }
+    TRY(launch_colsums(bias_sums, s));
     return launch_sgd(m->params, m->grads, nullptr, m->w16, m->w16lo, m->n_params, m->lr, 0.f, s);
 }
 
