@@ -445,9 +445,12 @@ template <typename T>
 static fo_status colsum_impl(const T* X, int64_t ld, int rows, const int* rows_dev, int N, float* out, float* ws,
                              hipStream_t s) {
     if (rows <= 0 || N <= 0) return FO_OK;
+    // one chunk of rows: its partial row is the sum, written straight to out
+    const bool one = !rows_dev && rows <= CS_ROWS;
     hipLaunchKernelGGL((colsum_partial<T>), dim3(cdiv(N, 64), cdiv(rows, CS_ROWS)), dim3(256), 0, s, X, ld, rows,
-                       rows_dev, N, ws);
+                       rows_dev, N, one ? out : ws);
     FO_LAUNCHED();
+    if (one) return FO_OK;
     ColOut o;
     o.p[0] = out;
     o.seg = N;
