@@ -129,6 +129,24 @@ fo_status gemm(const GemmDesc& d, hipStream_t s);
 constexpr int kGemmGroupMax = 4;
 fo_status gemm_group(const GemmDesc* d, int n, hipStream_t s, int max_wg = 0);
 
+// Deferred split-K sums of several products with a plain epilogue (no bias,
+// activation or mask: a weight gradient): job i adds slices 0 .. S_i - 1 of
+// ws_i ([S_i][M_i][N_i], as a launch with defer_reduce left them) into
+// C_i[m][n] = C_i[m ldc_i + n], in splitk_reduce's order.  One launch for up to
+// kSplitJobsMax products.
+constexpr int kSplitJobsMax = 16;
+struct SplitJob {
+    const float* ws = nullptr;
+    float* C = nullptr;
+    int64_t ldc = 0;
+    int S = 1, M = 0, N = 0;
+};
+struct SplitJobs {
+    SplitJob j[kSplitJobsMax];
+    int n = 0;
+};
+fo_status launch_splitk_sum_multi(const SplitJobs& jobs, hipStream_t s);
+
 // Bytes of split-K workspace a descriptor needs (0 if splits == 1).
 inline size_t gemm_ws_bytes(int M, int N, int splits) {
     return splits > 1 ? sizeof(float) * (size_t)M * N * splits : 0;

@@ -1757,6 +1757,45 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmDesc d) {
     }
 }
 
+// launch_splitk_sum_multi: blocks are dealt to the jobs in order, job i
+// taking ceil(M_i N_i / 1024) of them; each thread sums four consecutive
+// elements (one when N_i % 4 != 0 or C_i is not 16-byte aligned).
+__global__ void __launch_bounds__(256) splitk_sum_multi(const SplitJobs jobs) {
+    int bid = blockIdx.x, ji = 0;
+    for (; ji < jobs.n - 1; ++ji) {
+        const int nb = (int)(((int64_t)jobs.j[ji].M * jobs.j[ji].N + 1023) / 1024);
+        if (bid < nb) break;
+        bid -= nb;
+    }
+    const SplitJob& J = jobs.j[ji];
+    const int64_t full = (int64_t)J.M * J.N;
+    const int64_t e0 = (int64_t)bid * 1024 + 4 * threadIdx.x;
+    if (e0 >= full) return;
+    const bool vec = (J.N & 3) == 0 && (J.ldc & 3) == 0 && ((uintptr_t)J.C & 15) == 0;
+    if (vec) {
+        const float* p = J.ws + e0;
+        f32x4 v = *reinterpret_cast<const f32x4*>(p);
+        int z = 1;
+        for (; z + 3 < J.S; z += 4) {
+            const f32x4 a = *reinterpret_cast<const f32x4*>(p + z * full);
+            const f32x4 b = *reinterpret_cast<const f32x4*>(p + (z + 1) * full);
+            const f32x4 c = *reinterpret_cast<const f32x4*>(p + (z + 2) * full);
+            const f32x4 f = *reinterpret_cast<const f32x4*>(p + (z + 3) * full);
+            v += (a + b) + (c + f);
+        }
+        for (; z < J.S; ++z) v += *reinterpret_cast<const f32x4*>(p + z * full);
+        const int64_t row = e0 / J.N, col = e0 - row * J.N;
+        *reinterpret_cast<f32x4*>(J.C + row * J.ldc + col) = v;
+    } else {
+        for (int64_t e = e0; e < min(e0 + 4, full); ++e) {
+            float v = 0.f;
+            for (int z = 0; z < J.S; ++z) v += J.ws[(int64_t)z * full + e];
+            const int64_t row = e / J.N, col = e - row * J.N;
+            J.C[row * J.ldc + col] = v;
+        }
+    }
+}
+
 template <int NSEG, class LA = DmaRKc, int NST = 2>
 void launch_comp(const GemmDesc& d, hipStream_t s) {
     ProfInfo pi;
@@ -1873,6 +1912,22 @@ fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s, int max_wg) {
     else
         hipExtLaunchKernelGGL((gemm_wgrad_dma_kernel<kWgradKT, kWgradNST>), dim3(grid), dim3(NT), 0, s, ea, eb, 0,
                               g);
+    prof_end_ext(h);
+    FO_LAUNCHED();
+    return FO_OK;
+}
+
+fo_status launch_splitk_sum_multi(const SplitJobs& jobs, hipStream_t s) {
+    FO_CHECK(jobs.n >= 1 && jobs.n <= kSplitJobsMax, "split-K sums: %d jobs", jobs.n);
+    int64_t blocks = 0;
+    for (int i = 0; i < jobs.n; ++i) {
+        const SplitJob& J = jobs.j[i];
+        FO_CHECK(J.ws && J.C && J.S >= 1 && J.M >= 1 && J.N >= 1 && J.ldc >= J.N, "split-K sums: bad job %d", i);
+        blocks += cdiv((int64_t)J.M * J.N, 1024);
+    }
+    hipEvent_t ea, eb;
+    const int h = prof_begin_ext("splitk_sum_multi", ProfInfo(), &ea, &eb);
+    hipExtLaunchKernelGGL(splitk_sum_multi, dim3((unsigned)blocks), dim3(256), 0, s, ea, eb, 0, jobs);
     prof_end_ext(h);
     FO_LAUNCHED();
     return FO_OK;
