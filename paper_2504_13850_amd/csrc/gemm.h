@@ -134,7 +134,7 @@ fo_status gemm_group(const GemmDesc* d, int n, hipStream_t s, int max_wg = 0);
 // ws_i ([S_i][M_i][N_i], as a launch with defer_reduce left them) into
 // C_i[m][n] = C_i[m ldc_i + n], in splitk_reduce's order.  One launch for up to
 // kSplitJobsMax products.
-constexpr int kSplitJobsMax = 16;
+constexpr int kSplitJobsMax = 48;
 struct SplitJob {
     const float* ws = nullptr;
     float* C = nullptr;

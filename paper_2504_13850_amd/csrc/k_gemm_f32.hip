@@ -166,6 +166,9 @@ __global__ void __launch_bounds__(256) gemm_f32_reduce(const GemmF32 g) {
 
 fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_t s) {
     FO_CHECK(g.M >= 1 && g.N >= 1 && g.K >= 1, "fp32 product: M=%d N=%d K=%d", g.M, g.N, g.K);
+    FO_CHECK(!g.defer || (!g.bias && !g.add && !g.inAdd && !g.mask && !g.relu &&
+                          (g.S <= 1 || (part && (size_t)g.S * g.M * g.N <= part_floats))),
+             "fp32 product: deferred slices need a plain epilogue and room for all of them");
     if (g.S > 1) {
         const size_t per = (size_t)g.M * g.N;
         if (!part || (size_t)g.S * per > part_floats) g.S = part ? (int)(part_floats / per) : 1;
@@ -183,7 +186,7 @@ fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_
     else
         hipLaunchKernelGGL((gemm_f32<false, false>), grid, dim3(256), 0, s, g);
     FO_LAUNCHED();
-    if (g.S > 1) {
+    if (g.S > 1 && !g.defer) {
         hipLaunchKernelGGL(gemm_f32_reduce, dim3((int)cdiv((int64_t)g.M * g.N, 256)), dim3(256), 0, s, g);
         FO_LAUNCHED();
     }

@@ -165,6 +165,9 @@ struct GemmF32 {
     const StepIn* inA;
     const StepIn* inB;
     const StepIn* inAdd;
+    // S > 1: leave the slices in part for the caller to sum (no epilogue
+    // operands then), instead of the second launch
+    int defer;
 };
 fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_t s);
 

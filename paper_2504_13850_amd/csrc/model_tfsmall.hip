@@ -15,6 +15,7 @@
 // staged in LDS, LayerNorm as one wave per row.  Batches stay padded
 // [B][L][d]; queries past a sequence's length are computed like the others
 // (nothing reads them, so their gradients are zero) and keys past it are masked.
+#include "gemm.h"
 #include "model.h"
 
 namespace fo {
@@ -253,6 +254,7 @@ struct Plan {
     float* part;       // split-K slices
     float* colws;      // column-sum workspace
     float* sumws;      // partial rows of a layer's kLayerSums column sums
+    float* wgpart;     // the weight gradients' K slices of every layer (layer_wgrad_part each)
     size_t part_floats;
 };
 
@@ -260,6 +262,17 @@ constexpr int kMaxSlices = 16;
 // column sums per layer in the backward: the biases of the four products and
 // the two norms' gain and shift
 constexpr int kLayerSums = 8;
+
+// K slices of a weight gradient (K = the R packed rows)
+int wgrad_slices(int64_t R) { return (int)std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, R / 256)); }
+// Floats of a layer's weight-gradient slices (its four products, each rounded
+// up to 64 floats), kept until the step sums them all before the update.
+size_t layer_wgrad_part(int64_t R) {
+    const int S = wgrad_slices(R);
+    if (S <= 1) return 0;
+    auto r64 = [](size_t n) { return (n + 63) / 64 * 64; };
+    return r64((size_t)S * D * FF) + r64((size_t)S * FF * D) + r64((size_t)S * D * D) + r64((size_t)S * 3 * D * D);
+}
 
 size_t ws_bytes(const fo_model* m) {
     const Arch a = arch_of(m->cid);
@@ -286,6 +299,7 @@ size_t ws_bytes(const fo_model* m) {
     add(4 * (size_t)kMaxSlices * 3 * D * D);                          // part
     add(4 * colsum_ws_floats((int)R, 3 * D));                         // colws
     add(4 * kLayerSums * colsum_ws_floats((int)R, 3 * D));            // sumws
+    add(4 * a.layers * layer_wgrad_part((int64_t)R));                 // wgpart
     return s;
 }
 
@@ -343,7 +357,8 @@ fo_status init(fo_model* m) {
     P->part = ar.take<float>(P->part_floats);
     P->colws = ar.take<float>(colsum_ws_floats((int)R, 3 * D));
     P->sumws = ar.take<float>(kLayerSums * colsum_ws_floats((int)R, 3 * D));
-    if (!P->sumws) {
+    P->wgpart = ar.take<float>(std::max<size_t>(1, P->a.layers * layer_wgrad_part((int64_t)R)));
+    if (!P->wgpart) {
         set_error("tfsmall: workspace arena too small");
         return FO_ENOMEM;
     }
@@ -387,12 +402,24 @@ Gf linear(const float* x, const StepIn* inx, const float* W, const float* b, flo
 Gf linear_dx(const float* dy, const float* W, float* dx, int R, int N, int K) {
     return prod(dy, N, 1, W, 1, K, dx, K, R, K, N);
 }
-// dW[n][k] = sum_r dy[r][n] x[r][k] (x = the batch when inx is set)
-fo_status linear_dw(const Ctx& c, const float* dy, const float* x, const StepIn* inx, float* dW, int R, int N, int K) {
+// dW[n][k] = sum_r dy[r][n] x[r][k] (x = the batch when inx is set).  Nothing
+// reads dW before the update, so its K slices stay at *part (which advances)
+// and join `sums`, added up for every layer in one launch at the end of the
+// backward instead of one reduction launch per product.
+fo_status linear_dw(const Ctx& c, const float* dy, const float* x, const StepIn* inx, float* dW, int R, int N, int K,
+                    SplitJobs& sums, float*& part) {
     Gf g = prod(dy, 1, N, x, 1, K, dW, K, N, K, R);
     g.inB = inx;
-    g.S = (int)std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, R / 256));
-    return gemm(c, g);
+    g.S = wgrad_slices(R);
+    if (g.S <= 1) return gemm(c, g);
+    FO_CHECK(sums.n < kSplitJobsMax, "tfsmall: more than %d deferred weight-gradient sums", kSplitJobsMax);
+    g.defer = 1;
+    const size_t n = (size_t)g.S * N * K;
+    SplitJob& j = sums.j[sums.n++];
+    j.ws = part; j.C = dW; j.ldc = K; j.S = g.S; j.M = N; j.N = K;
+    const fo_status st = launch_gemm_f32(g, part, n, c.s);
+    part += (n + 63) / 64 * 64;
+    return st;
 }
 fo_status colsum(const Ctx& c, const float* X, int R, int N, float* out) {
     return launch_colsum(X, N, R, nullptr, N, out, c.P->colws, c.s);
@@ -461,6 +488,8 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
     TRY(colsum(c, P->dz, B, NCLS, P->gbc));
     TRY(launch_fill(dy, (int64_t)R * D, 0.f, s));
     TRY(gemm(c, prod(P->dz, NCLS, 1, P->wc, 1, D, dy, (int64_t)L * D, B, D, NCLS)));
+    SplitJobs wsums;
+    float* wpart = P->wgpart;
     for (int l = a.layers - 1; l >= 0; --l) {
         LayerP& Y = P->ly[l];
         const float* x = l ? P->ly[l - 1].y : nullptr;
@@ -479,13 +508,13 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         sum(P->gx, D, Y.gg2);
         sum(dy, D, Y.gb2n);
         // FFN2 and FFN1 (ReLU mask from the stored activation)
-        TRY(linear_dw(c, P->du2, Y.f, nullptr, Y.gw2, R, D, FF));
+        TRY(linear_dw(c, P->du2, Y.f, nullptr, Y.gw2, R, D, FF, wsums, wpart));
         sum(P->du2, D, Y.gb2);
         Gf gdf = linear_dx(P->du2, Y.w2, P->df, R, D, FF);
         gdf.mask = Y.f;
         gdf.ldmask = FF;
         TRY(gemm(c, gdf));
-        TRY(linear_dw(c, P->df, Y.h1, nullptr, Y.gw1, R, FF, D));
+        TRY(linear_dw(c, P->df, Y.h1, nullptr, Y.gw1, R, FF, D, wsums, wpart));
         sum(P->df, FF, Y.gb1);
         Gf gdh = linear_dx(P->df, Y.w1, P->dh1, R, FF, D);  // dh1 = du2 + df W1
         gdh.add = P->du2;
@@ -498,7 +527,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         sum(P->gx1, D, Y.gg1);
         sum(P->dh1, D, Y.gb1n);
         // output projection
-        TRY(linear_dw(c, P->du1, Y.O, nullptr, Y.gwo, R, D, D));
+        TRY(linear_dw(c, P->du1, Y.O, nullptr, Y.gwo, R, D, D, wsums, wpart));
         sum(P->du1, D, Y.gbo);
         TRY(gemm(c, linear_dx(P->du1, Y.wo, P->dO, R, D, D)));
         // attention
@@ -510,7 +539,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
                                Y.lse, P->dqkv, H, L, scale);
         FO_LAUNCHED();
         // QKV projection (no input gradient for the first server layer: nothing is sent back)
-        TRY(linear_dw(c, P->dqkv, x, inx, Y.gwqkv, R, 3 * D, D));
+        TRY(linear_dw(c, P->dqkv, x, inx, Y.gwqkv, R, 3 * D, D, wsums, wpart));
         sum(P->dqkv, 3 * D, Y.gbqkv);
         TRY(launch_colsums(sums, s));
         if (l > 0) {
@@ -521,6 +550,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             std::swap(dy, dx);
         }
     }
+    if (wsums.n) TRY(launch_splitk_sum_multi(wsums, s));
 #undef TRY
     // SGD (Alg. 4)
     return launch_sgd(m->params, m->grads, nullptr, nullptr, nullptr, m->n_params, m->lr, 0.f, s);
