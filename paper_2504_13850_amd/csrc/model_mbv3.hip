@@ -12,6 +12,7 @@
 // (batch statistics, with the activation and the residual fused), the
 // depthwise convolution one thread per output (forward) or input (input
 // gradient) and one workgroup per channel for its weight gradient.
+#include "gemm.h"
 #include "model.h"
 
 namespace fo {
@@ -278,7 +279,29 @@ struct Plan {
     float *gwl, *ggl, *gbl, *gwf1, *gbf1, *gwf2, *gbf2;
     float *x0, *zl, *xhl, *al, *rsl, *gp, *fpre, *f, *dz, *df, *dg, *z, *d0, *d1, *d2, *dm, *dt, *dq, *part, *colws;
     size_t part_floats;
+    float* wgpart;  // the weight gradients' K slices until the update (wgrad_part_floats)
+    size_t wgpart_floats;
 };
+
+// K slices of a weight gradient over R rows
+int wgrad_slices(int64_t R) { return (int)std::min<int64_t>(kMaxSlices, std::max<int64_t>(1, R / 64)); }
+// Floats for the weight gradients' K slices of one step, an upper bound (every
+// product at the largest row count, each rounded up to 64 floats): the slices
+// stay until the step sums them all before the update.
+size_t wgrad_part_floats(int B) {
+    const int64_t Rmax = (int64_t)B * HIN * HIN;
+    const size_t S = wgrad_slices(Rmax), Sb = wgrad_slices(B);
+    auto r64 = [](size_t n) { return (n + 63) / 64 * 64; };
+    size_t n = r64(Sb * NCLS * F1) + r64(Sb * F1 * CLAST);
+    int ci = CIN;
+    for (int j = 0; j < NBLK; ++j) {
+        const Blk& b = kBlk[j];
+        n += r64(S * b.co * b.e) + r64(S * b.e * ci);
+        if (b.se) n += 2 * r64(Sb * b.e * se_width(b.e));
+        ci = b.co;
+    }
+    return n + r64(S * CLAST * ci);
+}
 
 size_t ws_floats(int B) {
     const size_t R = (size_t)B * HIN * HIN;
@@ -300,6 +323,7 @@ size_t ws_floats(int B) {
     add((size_t)B * 960 * 3);           // dm, dt, dq
     add((size_t)kMaxSlices * CLAST * 200 + (size_t)kMaxSlices * F1 * CLAST / 4);  // part
     add(colsum_ws_floats(B, F1));       // colws
+    add(wgrad_part_floats(B));          // wgpart
     return s;
 }
 
@@ -388,7 +412,9 @@ fo_status init(fo_model* m) {
     P->part_floats = (size_t)kMaxSlices * CLAST * 200 + (size_t)kMaxSlices * F1 * CLAST / 4;
     P->part = ar.take<float>(P->part_floats);
     P->colws = ar.take<float>(colsum_ws_floats(B, F1));
-    if (!P->colws) {
+    P->wgpart_floats = wgrad_part_floats(B);
+    P->wgpart = ar.take<float>(P->wgpart_floats);
+    if (!P->wgpart) {
         set_error("mbv3: workspace arena too small");
         return FO_ENOMEM;
     }
@@ -427,11 +453,24 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
         g.relu = relu;
         return gemm(g);
     };
-    // dW[n][k] = sum_r dy[r][n] x[r][k]
-    auto linear_dw = [&](const float* dy, const float* x, float* dW, int R, int N, int K) {
+    // dW[n][k] = sum_r dy[r][n] x[r][k].  Nothing reads dW before the update,
+    // so its K slices stay in wgpart and join `wsums`, added up for every
+    // product in one launch at the end of the backward.
+    SplitJobs wsums;
+    size_t wused = 0;
+    auto linear_dw = [&](const float* dy, const float* x, float* dW, int R, int N, int K) -> fo_status {
         GemmF32 g = prod(dy, 1, N, x, 1, K, dW, K, N, K, R);
-        g.S = std::min(kMaxSlices, std::max(1, R / 64));
-        return gemm(g);
+        g.S = wgrad_slices(R);
+        if (g.S <= 1) return gemm(g);
+        const size_t n = (size_t)g.S * N * K;
+        FO_CHECK(wsums.n < kSplitJobsMax && wused + n <= P->wgpart_floats,
+                 "mbv3: deferred weight-gradient slices exceed their workspace");
+        g.defer = 1;
+        SplitJob& j = wsums.j[wsums.n++];
+        j.ws = P->wgpart + wused; j.C = dW; j.ldc = K; j.S = g.S; j.M = N; j.N = K;
+        const fo_status r = launch_gemm_f32(g, P->wgpart + wused, n, s);
+        wused += (n + 63) / 64 * 64;
+        return r;
     };
     // dx[r][k] = dy[r][:] . W[:][k] (+ add, times mask > 0)
     auto linear_dx = [&](const float* dy, const float* W, float* dx, int R, int N, int K, const float* add,
@@ -565,6 +604,7 @@ fo_status step(fo_model* m, const fo_acts* acts, const int32_t* labels) {
             dy = dx;
         }
     }
+    if (wsums.n) TRY(launch_splitk_sum_multi(wsums, s));
 #undef TRY
     // SGD (Alg. 4)
     return launch_sgd(m->params, m->grads, nullptr, nullptr, nullptr, m->n_params, m->lr, 0.f, s);
