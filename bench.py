@@ -108,6 +108,7 @@ TRAFFIC_KERNELS = {
     "gemm_comp_dma_kernel<3>": ("gemm_comp_dma_kernel<3, 2, fo::(anonymous namespace)::DmaRKc>", GEMM_SOURCES),
     "gemm_rk_krt_dma_kernel": ("gemm_rk_krt_dma_kernel<32, 4>", GEMM_SOURCES),
     "gemm_wgrad_dma_kernel": ("gemm_wgrad_dma_kernel<32, 4>", GEMM_SOURCES),
+    "gemm_wgrad_tall_kernel": ("gemm_wgrad_tall_kernel<32, 3>", GEMM_SOURCES),
     "agg_lerp_kernel": ("agg_lerp_kernel(", ["paper_2504_13850_amd/csrc/k_update.hip"]),
 }
 CALIB_BYTES = 1 << 30
