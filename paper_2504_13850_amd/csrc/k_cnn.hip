@@ -81,20 +81,31 @@ __global__ void __launch_bounds__(256) maxpool_fwd(const bf16_t* __restrict__ xh
 __global__ void __launch_bounds__(256) maxpool_relu_bwd(const float* __restrict__ dy, const uint8_t* __restrict__ arg,
                                                         const bf16_t* __restrict__ y, float* __restrict__ dxf,
                                                         bf16_t* __restrict__ dxb, int B, int H, int W, int C) {
-    const int64_t total = (int64_t)B * H * W * C;
+    // one thread per pooled output (b, yo, xo, c): its four window inputs, the
+    // index arithmetic done once for them
     const int Ho = H / 2, Wo = W / 2;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int c = (int)(i % C);
-        int64_t r = i / C;
-        const int x = (int)(r % W);
-        r /= W;
-        const int yy = (int)(r % H);
-        const int b = (int)(r / H);
-        const int64_t o = (((int64_t)b * Ho + yy / 2) * Wo + x / 2) * C + c;
-        const int pos = (yy & 1) * 2 + (x & 1);
-        float g = (arg[o] == pos && bf2f(y[i]) > 0.f) ? dy[o] : 0.f;
-        dxf[i] = g;
-        dxb[i] = f2bf(g);
+    const int64_t total = (int64_t)B * Ho * Wo * C;
+    const int64_t rowC = (int64_t)W * C;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total; o += (int64_t)gridDim.x * blockDim.x) {
+        const int c = (int)(o % C);
+        int64_t r = o / C;
+        const int xo = (int)(r % Wo);
+        r /= Wo;
+        const int yo = (int)(r % Ho);
+        const int b = (int)(r / Ho);
+        const int64_t i0 = (((int64_t)b * H + 2 * yo) * W + 2 * xo) * C + c;
+        const int64_t off[4] = {0, C, rowC, rowC + C};  // window position (yy & 1) * 2 + (x & 1)
+        const int a = arg[o];
+        const float g = dy[o];
+        bf16_t yv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) yv[q] = y[i0 + off[q]];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float v = (a == q && bf2f(yv[q]) > 0.f) ? g : 0.f;
+            dxf[i0 + off[q]] = v;
+            dxb[i0 + off[q]] = f2bf(v);
+        }
     }
 }
 
@@ -444,8 +455,9 @@ fo_status launch_maxpool_fwd(const bf16_t* xh, const bf16_t* xl, bf16_t* yh, bf1
 
 fo_status launch_maxpool_relu_bwd(const float* dy, const uint8_t* arg, const bf16_t* y, float* dxf, bf16_t* dxb, int B,
                                   int H, int W, int C, hipStream_t s) {
-    hipLaunchKernelGGL(maxpool_relu_bwd, dim3(grid_for((int64_t)B * H * W * C)), dim3(256), 0, s, dy, arg, y, dxf, dxb,
-                       B, H, W, C);
+    FO_CHECK(H % 2 == 0 && W % 2 == 0, "max pool backward: %d x %d input (even sizes only)", H, W);
+    hipLaunchKernelGGL(maxpool_relu_bwd, dim3(grid_for((int64_t)B * (H / 2) * (W / 2) * C)), dim3(256), 0, s, dy,
+                       arg, y, dxf, dxb, B, H, W, C);
     FO_LAUNCHED();
     return FO_OK;
 }

@@ -79,7 +79,13 @@ int split_for(int M, int N, int K, int max_s = 8) {
 __global__ void __launch_bounds__(256) conv1_fwd(const StepIn* __restrict__ in, const float* __restrict__ w,
                                                  const float* __restrict__ bias, bf16_t* __restrict__ yh,
                                                  bf16_t* __restrict__ yl, int B) {
+    static_assert(C == 64, "a wave is the 64 channels of one pixel");
     const float* __restrict__ x = static_cast<const float*>(in->x);
+    // the weights as [tap][channel] in LDS: a wave's 64 lanes read one row
+    // (w itself is [channel][tap], 27 floats apart from lane to lane)
+    __shared__ float wl[9 * CI][C];
+    for (int t = threadIdx.x; t < 9 * CI * C; t += blockDim.x) wl[t % (9 * CI)][t / (9 * CI)] = w[t];
+    __syncthreads();
     const int64_t total = (int64_t)B * H0 * H0 * C;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
         const int co = (int)(i % C);
@@ -96,8 +102,7 @@ __global__ void __launch_bounds__(256) conv1_fwd(const StepIn* __restrict__ in, 
                 if (ix < 0 || ix >= H0) continue;
 #pragma unroll
                 for (int ci = 0; ci < CI; ++ci)
-                    acc = fmaf(x[(((int64_t)b * CI + ci) * H0 + iy) * H0 + ix], w[((co * 3 + ky) * 3 + kx) * CI + ci],
-                               acc);
+                    acc = fmaf(x[(((int64_t)b * CI + ci) * H0 + iy) * H0 + ix], wl[(ky * 3 + kx) * CI + ci][co], acc);
             }
         }
         const float v = acc > 0.f ? acc : 0.f;
