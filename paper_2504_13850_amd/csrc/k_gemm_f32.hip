@@ -8,6 +8,9 @@ namespace fo {
 namespace {
 
 constexpr int GT = 64, GK = 32;
+// automatic K split (GemmF32::auto_split): products with fewer than kAutoTiles
+// output tiles take min(16, kAutoSlots / tiles, K / kAutoMinK) slices
+constexpr int64_t kAutoTiles = 128, kAutoSlots = 512, kAutoMinK = 64;
 constexpr int GV = GT * GK / 256;  // operand values per thread per K chunk (8)
 
 __device__ __forceinline__ float epi(const GemmF32& g, const float* add, int m, int n, float v) {
@@ -169,6 +172,14 @@ fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_
     FO_CHECK(!g.defer || (!g.bias && !g.add && !g.inAdd && !g.mask && !g.relu &&
                           (g.S <= 1 || (part && (size_t)g.S * g.M * g.N <= part_floats))),
              "fp32 product: deferred slices need a plain epilogue and room for all of them");
+    if (g.auto_split && g.S == 1 && !g.defer) {
+        // few 64 x 64 tiles over a long K leave most CUs idle while each
+        // workgroup walks K chunk by chunk: split K so that about kAutoSlots
+        // workgroups run, each slice at least kAutoMinK long
+        const int64_t tiles = cdiv(g.N, GT) * cdiv(g.M, GT);
+        if (tiles < kAutoTiles)
+            g.S = (int)std::max<int64_t>(1, std::min<int64_t>({16, kAutoSlots / tiles, g.K / kAutoMinK}));
+    }
     if (g.S > 1) {
         const size_t per = (size_t)g.M * g.N;
         if (!part || (size_t)g.S * per > part_floats) g.S = part ? (int)(part_floats / per) : 1;

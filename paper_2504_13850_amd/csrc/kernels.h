@@ -168,6 +168,11 @@ struct GemmF32 {
     // S > 1: leave the slices in part for the caller to sum (no epilogue
     // operands then), instead of the second launch
     int defer;
+    // with S == 1: let the launcher split K when the product has few output
+    // tiles and a long K (its slices then summed by the second launch).  Used
+    // by the VGG-5 and MobileNetV3 server parts (their classifier and SE
+    // products run on 2 to 20 tiles over K up to 1280)
+    int auto_split;
 };
 fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_t s);
 

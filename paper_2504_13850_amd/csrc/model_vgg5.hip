@@ -217,6 +217,7 @@ GemmF32 prod(const float* A, int64_t am, int64_t ak, const float* B, int64_t bn,
     g.N = N;
     g.K = K;
     g.S = 1;
+    g.auto_split = 1;
     return g;
 }
 
