@@ -16,7 +16,8 @@
 //    LDS by global_load_lds in a two-stage ring.
 //  - gemm_wgrad_dma_kernel: groups of products of two k-major operands
 //    (weight gradients), tiles copied into LDS in the [k][row] layout and read
-//    by transpose reads, four-stage ring.
+//    by transpose reads, four-stage ring; gemm_wgrad_tall_kernel, the same on
+//    256 x 128 tiles (128 x 64 per wave) for groups that share the GPU.
 //  - gemm_rk_krt_dma_kernel: row-major A times k-major B (input gradients),
 //    the same copies and ring.
 #include <algorithm>
@@ -40,9 +41,6 @@ constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
 // workgroups per CU: deeper rings at one workgroup per CU starve the
 // concurrent input-gradient chain of LDS).
 constexpr int kWgradKT = 32, kWgradNST = 4, kDgradKT = 32, kDgradNST = 4;
-#ifndef WGRAD_TALL
-#define WGRAD_TALL 1
-#endif
 constexpr int NV = BM * BK / 8 / NT;  // 16-byte vectors per thread per operand per K tile (4)
 
 // LDS tiles are 128 rows x 64 k with rows padded to 72 elements (144 B = 36
@@ -1901,7 +1899,10 @@ fo_status gemm_group(const GemmDesc* ds, int n, hipStream_t s, int max_wg) {
             pi.gN[i] = d.N;
         }
     }
-    const bool tall = WGRAD_TALL == 2 || (WGRAD_TALL == 1 && max_wg > 0);
+    // a capped group runs beside other work: 256 x 128 tiles read a quarter
+    // fewer operand bytes per MFMA and leave more of the GPU to that work; an
+    // uncapped group has the GPU to itself and fills it better with 128 x 128
+    const bool tall = max_wg > 0;
     hipEvent_t ea, eb;
     const int h = prof_begin_ext(tall ? "gemm_wgrad_tall_kernel" : "gemm_wgrad_dma_kernel", pi, &ea, &eb);
     g.prof_snap = prof_snap(h);
