@@ -78,7 +78,9 @@ __global__ void __launch_bounds__(256) attn_small_fwd(const float* __restrict__ 
 #pragma unroll
         for (int c = 0; c < DH; ++c) s = fmaf(q[c], Ks[j * DH + c], s);
         const float mn = fmaxf(mx, s);
-        const float f = expf(mx - mn), p = expf(s - mn);  // exp(-inf) = 0 on the first key
+        // the hardware exponential (v_exp_f32 on x log2 e): its error on these
+        // arguments (<= 0 after the running-max shift) is far below the fp32 path's
+        const float f = __expf(mx - mn), p = __expf(s - mn);  // exp(-inf) = 0 on the first key
         sum = sum * f + p;
 #pragma unroll
         for (int c = 0; c < DH; ++c) acc[c] = fmaf(acc[c], f, p * Vs[j * DH + c]);
@@ -136,7 +138,7 @@ __global__ void __launch_bounds__(256) attn_small_bwd(const float* __restrict__ 
                 s = fmaf(q[c], T0[j * DH + c], s);
                 dp = fmaf(g[c], T1[j * DH + c], dp);
             }
-            const float p = expf(s * scale - li), ds = p * (dp - dsum);
+            const float p = __expf(s * scale - li), ds = p * (dp - dsum);
 #pragma unroll
             for (int c = 0; c < DH; ++c) dq[c] = fmaf(ds, T0[j * DH + c], dq[c]);
         }
@@ -171,7 +173,7 @@ __global__ void __launch_bounds__(256) attn_small_bwd(const float* __restrict__ 
                 s = fmaf(T0[i * DH + c], kj[c], s);
                 dp = fmaf(T1[i * DH + c], vj[c], dp);
             }
-            const float p = expf(s * scale - Ls[i]), ds = p * (dp - Ds[i]);
+            const float p = __expf(s * scale - Ls[i]), ds = p * (dp - Ds[i]);
 #pragma unroll
             for (int c = 0; c < DH; ++c) {
                 dk[c] = fmaf(ds, T0[i * DH + c], dk[c]);
