@@ -11,7 +11,10 @@ constexpr int GT = 64, GK = 32;
 // automatic K split (GemmF32::auto_split): products with fewer than kAutoTiles
 // output tiles take min(16, kAutoSlots / tiles, K / kAutoMinK) slices
 constexpr int64_t kAutoTiles = 128, kAutoSlots = 512, kAutoMinK = 64;
-constexpr int GV = GT * GK / 256;  // operand values per thread per K chunk (8)
+// workgroups of 64-row tiles below which a product runs on 32-row tiles (the
+// fp32 server parts' products all fall below: 256, 512, 1024 or always gave
+// the same step times, all 12-21% below 64-row tiles)
+constexpr int64_t kRows32Below = 512;
 
 __device__ __forceinline__ float epi(const GemmF32& g, const float* add, int m, int n, float v) {
     if (g.bias) v += g.bias[n];
@@ -21,88 +24,99 @@ __device__ __forceinline__ float epi(const GemmF32& g, const float* add, int m, 
     return v;
 }
 
-// One operand's share of a 64 x 32 chunk: value v of thread t is element
-// e = t + 256 v; with K contiguous (KF) the 32 k of a row are consecutive
-// threads, else the 64 rows are.
-template <bool KF>
+// One operand's share of an RT x 32 chunk (RT = 64 or 32 rows): value v of
+// thread t is element e = t + 256 v; with K contiguous (KF) the 32 k of a row
+// are consecutive threads, else the RT rows are.
+template <bool KF, int RT>
 __device__ __forceinline__ void chunk_rc(int e, int& r, int& k) {
-    r = KF ? e >> 5 : e & 63;
-    k = KF ? e & 31 : e >> 6;
+    r = KF ? e >> 5 : e % RT;
+    k = KF ? e & 31 : e / RT;
 }
 // Every load reads a valid element (row and k clamped into the operand, R and
 // ke >= 1) and the values outside the chunk are zeroed when stored: with
 // "in range ? load : 0" the compiler selects right after each load, so each
 // load waits for the previous one and the chunk in flight is not in flight.
-template <bool KF>
+template <bool KF, int RT, int NV>
 __device__ __forceinline__ void load_chunk(const float* P, int64_t sr, int64_t sk, int r0, int R, int k0, int ke,
-                                           float (&v)[GV]) {
+                                           float (&v)[NV]) {
+    static_assert(NV * 256 == RT * GK, "chunk share");
 #pragma unroll
-    for (int i = 0; i < GV; ++i) {
+    for (int i = 0; i < NV; ++i) {
         int r, k;
-        chunk_rc<KF>(threadIdx.x + 256 * i, r, k);
+        chunk_rc<KF, RT>(threadIdx.x + 256 * i, r, k);
         const int gr = min(r0 + r, R - 1), gk = min(k0 + k, ke - 1);
         v[i] = P[(int64_t)gr * sr + (KF ? (int64_t)gk : (int64_t)gk * sk)];
     }
 }
-template <bool KF>
-__device__ __forceinline__ void store_chunk(float (*T)[GT + 4], const float (&v)[GV], int r0, int R, int k0,
+template <bool KF, int RT, int NV>
+__device__ __forceinline__ void store_chunk(float (*T)[RT + 4], const float (&v)[NV], int r0, int R, int k0,
                                             int ke) {
 #pragma unroll
-    for (int i = 0; i < GV; ++i) {
+    for (int i = 0; i < NV; ++i) {
         int r, k;
-        chunk_rc<KF>(threadIdx.x + 256 * i, r, k);
+        chunk_rc<KF, RT>(threadIdx.x + 256 * i, r, k);
         T[k][r] = r0 + r < R && k0 + k < ke ? v[i] : 0.f;
     }
 }
 
-// 64 x 64 output tile per workgroup, 4 x 4 per thread; K in chunks of 32,
-// the next chunk's loads in flight (registers) while this one is computed
-// from LDS, two LDS buffers (one barrier per chunk).
-template <bool AKF, bool BKF>
+// TM x 16 = 64 or 32 rows by 64 columns of output per workgroup, TM x 4 per
+// thread; K in chunks of 32, the next chunk's loads in flight (registers)
+// while this one is computed from LDS, two LDS buffers (one barrier per
+// chunk).  The 32-row form doubles the workgroups of a product with few
+// tiles, whose time is otherwise the latency of each workgroup's K walk.
+template <bool AKF, bool BKF, int TM>
 __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
-    __shared__ float As[2][GK][GT + 4], Bs[2][GK][GT + 4];
+    constexpr int BMt = 16 * TM, NA = BMt * GK / 256, NB = GT * GK / 256;
+    __shared__ float As[2][GK][BMt + 4], Bs[2][GK][GT + 4];
     const float* A = g.inA ? (const float*)g.inA->x : g.A;
     const float* Bp = g.inB ? (const float*)g.inB->x : g.B;
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-    const int n0 = blockIdx.x * GT, m0 = blockIdx.y * GT, z = blockIdx.z;
+    const int n0 = blockIdx.x * GT, m0 = blockIdx.y * BMt, z = blockIdx.z;
     const int kc = ((g.K + g.S - 1) / g.S + GK - 1) / GK * GK;
     const int kb = z * kc, ke = min(g.K, kb + kc);
     const int nch = ke > kb ? (ke - kb + GK - 1) / GK : 0;
-    float acc[4][4] = {};
-    float ra[GV], rb[GV];
+    float acc[TM][4] = {};
+    float ra[NA], rb[NB];
     if (nch > 0) {
-        load_chunk<AKF>(A, g.am, g.ak, m0, g.M, kb, ke, ra);
-        load_chunk<BKF>(Bp, g.bn, g.bk, n0, g.N, kb, ke, rb);
-        store_chunk<AKF>(As[0], ra, m0, g.M, kb, ke);
-        store_chunk<BKF>(Bs[0], rb, n0, g.N, kb, ke);
+        load_chunk<AKF, BMt>(A, g.am, g.ak, m0, g.M, kb, ke, ra);
+        load_chunk<BKF, GT>(Bp, g.bn, g.bk, n0, g.N, kb, ke, rb);
+        store_chunk<AKF, BMt>(As[0], ra, m0, g.M, kb, ke);
+        store_chunk<BKF, GT>(Bs[0], rb, n0, g.N, kb, ke);
     }
     __syncthreads();
     for (int c = 0; c < nch; ++c) {
         const int u = c & 1;
         if (c + 1 < nch) {  // next chunk in flight during this chunk's FMAs
-            load_chunk<AKF>(A, g.am, g.ak, m0, g.M, kb + (c + 1) * GK, ke, ra);
-            load_chunk<BKF>(Bp, g.bn, g.bk, n0, g.N, kb + (c + 1) * GK, ke, rb);
+            load_chunk<AKF, BMt>(A, g.am, g.ak, m0, g.M, kb + (c + 1) * GK, ke, ra);
+            load_chunk<BKF, GT>(Bp, g.bn, g.bk, n0, g.N, kb + (c + 1) * GK, ke, rb);
         }
 #pragma unroll
         for (int k = 0; k < GK; ++k) {
-            const float4 a4 = *reinterpret_cast<const float4*>(&As[u][k][ty * 4]);
+            float a[TM];
+            if constexpr (TM == 4) {
+                const float4 a4 = *reinterpret_cast<const float4*>(&As[u][k][ty * 4]);
+                a[0] = a4.x; a[1] = a4.y; a[2] = a4.z; a[3] = a4.w;
+            } else {
+                const float2 a2 = *reinterpret_cast<const float2*>(&As[u][k][ty * TM]);
+                a[0] = a2.x; a[1] = a2.y;
+            }
             const float4 b4 = *reinterpret_cast<const float4*>(&Bs[u][k][tx * 4]);
-            const float a[4] = {a4.x, a4.y, a4.z, a4.w}, b[4] = {b4.x, b4.y, b4.z, b4.w};
+            const float b[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
         }
         if (c + 1 < nch) {
-            store_chunk<AKF>(As[u ^ 1], ra, m0, g.M, kb + (c + 1) * GK, ke);
-            store_chunk<BKF>(Bs[u ^ 1], rb, n0, g.N, kb + (c + 1) * GK, ke);
+            store_chunk<AKF, BMt>(As[u ^ 1], ra, m0, g.M, kb + (c + 1) * GK, ke);
+            store_chunk<BKF, GT>(Bs[u ^ 1], rb, n0, g.N, kb + (c + 1) * GK, ke);
         }
         __syncthreads();
     }
     if (g.S > 1) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int m = m0 + ty * 4 + i;
+        for (int i = 0; i < TM; ++i) {
+            const int m = m0 + ty * TM + i;
             if (m >= g.M) continue;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -115,32 +129,31 @@ __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
     // the epilogue's operands of all 16 elements first (indices clamped into
     // the product, so every load is valid), then the guarded stores
     const float* add = g.inAdd ? (const float*)g.inAdd->x : g.add;
-    int mi[4], nj[4];
+    int mi[TM], nj[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        mi[i] = min(m0 + ty * 4 + i, g.M - 1);
-        nj[i] = min(n0 + tx * 4 + i, g.N - 1);
-    }
-    float bv[4] = {0.f, 0.f, 0.f, 0.f}, av[4][4] = {}, mv[4][4];
+    for (int i = 0; i < TM; ++i) mi[i] = min(m0 + ty * TM + i, g.M - 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) nj[j] = min(n0 + tx * 4 + j, g.N - 1);
+    float bv[4] = {0.f, 0.f, 0.f, 0.f}, av[TM][4] = {}, mv[TM][4];
     if (g.bias) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) bv[j] = g.bias[nj[j]];
     }
     if (add) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) av[i][j] = add[(int64_t)mi[i] * g.ldadd + nj[j]];
     }
     if (g.mask) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) mv[i][j] = g.mask[(int64_t)mi[i] * g.ldmask + nj[j]];
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = m0 + ty * 4 + i;
+    for (int i = 0; i < TM; ++i) {
+        const int m = m0 + ty * TM + i;
         if (m >= g.M) continue;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -186,16 +199,26 @@ fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_
     }
     if (g.S < 1) g.S = 1;
     g.part = part;
-    const dim3 grid((int)cdiv(g.N, GT), (int)cdiv(g.M, GT), g.S);
+    // 32-row tiles when 64-row ones would not give every CU two workgroups
+    const bool rows32 = cdiv(g.N, GT) * cdiv(g.M, GT) * g.S < kRows32Below;
+    const dim3 grid((int)cdiv(g.N, GT), (int)cdiv(g.M, rows32 ? 32 : GT), g.S);
     const bool akf = g.ak == 1, bkf = g.bk == 1;
+#define FO_GEMM_F32(AK, BK)                                                       \
+    do {                                                                         \
+        if (rows32)                                                              \
+            hipLaunchKernelGGL((gemm_f32<AK, BK, 2>), grid, dim3(256), 0, s, g); \
+        else                                                                     \
+            hipLaunchKernelGGL((gemm_f32<AK, BK, 4>), grid, dim3(256), 0, s, g); \
+    } while (0)
     if (akf && bkf)
-        hipLaunchKernelGGL((gemm_f32<true, true>), grid, dim3(256), 0, s, g);
+        FO_GEMM_F32(true, true);
     else if (akf)
-        hipLaunchKernelGGL((gemm_f32<true, false>), grid, dim3(256), 0, s, g);
+        FO_GEMM_F32(true, false);
     else if (bkf)
-        hipLaunchKernelGGL((gemm_f32<false, true>), grid, dim3(256), 0, s, g);
+        FO_GEMM_F32(false, true);
     else
-        hipLaunchKernelGGL((gemm_f32<false, false>), grid, dim3(256), 0, s, g);
+        FO_GEMM_F32(false, false);
+#undef FO_GEMM_F32
     FO_LAUNCHED();
     if (g.S > 1 && !g.defer) {
         hipLaunchKernelGGL(gemm_f32_reduce, dim3((int)cdiv((int64_t)g.M * g.N, 256)), dim3(256), 0, s, g);
