@@ -11,9 +11,9 @@ constexpr int GT = 64, GK = 32;
 // automatic K split (GemmF32::auto_split): products with fewer than kAutoTiles
 // output tiles take min(16, kAutoSlots / tiles, K / kAutoMinK) slices
 constexpr int64_t kAutoTiles = 128, kAutoSlots = 512, kAutoMinK = 64;
-// workgroups of 64-row tiles below which a product runs on 32-row tiles (the
-// fp32 server parts' products all fall below: 256, 512, 1024 or always gave
-// the same step times, all 12-21% below 64-row tiles)
+// workgroups of 64-row tiles below which a product runs on 32-row tiles, and
+// of 32-row tiles below which it runs on 16-row tiles (for the 32-row step,
+// thresholds of 256, 512, 1024 or always gave the same step times)
 constexpr int64_t kRows32Below = 512;
 
 __device__ __forceinline__ float epi(const GemmF32& g, const float* add, int m, int n, float v) {
@@ -24,7 +24,7 @@ __device__ __forceinline__ float epi(const GemmF32& g, const float* add, int m, 
     return v;
 }
 
-// One operand's share of an RT x 32 chunk (RT = 64 or 32 rows): value v of
+// One operand's share of an RT x 32 chunk (RT = 64, 32 or 16 rows): value v of
 // thread t is element e = t + 256 v; with K contiguous (KF) the 32 k of a row
 // are consecutive threads, else the RT rows are.
 template <bool KF, int RT>
@@ -59,8 +59,8 @@ __device__ __forceinline__ void store_chunk(float (*T)[RT + 4], const float (&v)
     }
 }
 
-// TM x 16 = 64 or 32 rows by 64 columns of output per workgroup, TM x 4 per
-// thread; K in chunks of 32, the next chunk's loads in flight (registers)
+// TM x 16 = 64, 32 or 16 rows by 64 columns of output per workgroup, TM x 4
+// per thread; K in chunks of 32, the next chunk's loads in flight (registers)
 // while this one is computed from LDS, two LDS buffers (one barrier per
 // chunk).  The 32-row form doubles the workgroups of a product with few
 // tiles, whose time is otherwise the latency of each workgroup's K walk.
@@ -96,9 +96,11 @@ __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
             if constexpr (TM == 4) {
                 const float4 a4 = *reinterpret_cast<const float4*>(&As[u][k][ty * 4]);
                 a[0] = a4.x; a[1] = a4.y; a[2] = a4.z; a[3] = a4.w;
-            } else {
+            } else if constexpr (TM == 2) {
                 const float2 a2 = *reinterpret_cast<const float2*>(&As[u][k][ty * TM]);
                 a[0] = a2.x; a[1] = a2.y;
+            } else {
+                a[0] = As[u][k][ty];
             }
             const float4 b4 = *reinterpret_cast<const float4*>(&Bs[u][k][tx * 4]);
             const float b[4] = {b4.x, b4.y, b4.z, b4.w};
@@ -199,13 +201,17 @@ fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_
     }
     if (g.S < 1) g.S = 1;
     g.part = part;
-    // 32-row tiles when 64-row ones would not give every CU two workgroups
+    // 32-row tiles when 64-row ones would not give every CU two workgroups,
+    // 16-row tiles when 32-row ones would not either
     const bool rows32 = cdiv(g.N, GT) * cdiv(g.M, GT) * g.S < kRows32Below;
-    const dim3 grid((int)cdiv(g.N, GT), (int)cdiv(g.M, rows32 ? 32 : GT), g.S);
+    const bool rows16 = rows32 && cdiv(g.N, GT) * cdiv(g.M, 32) * g.S < kRows32Below;
+    const dim3 grid((int)cdiv(g.N, GT), (int)cdiv(g.M, rows16 ? 16 : rows32 ? 32 : GT), g.S);
     const bool akf = g.ak == 1, bkf = g.bk == 1;
 #define FO_GEMM_F32(AK, BK)                                                       \
     do {                                                                         \
-        if (rows32)                                                              \
+        if (rows16)                                                              \
+            hipLaunchKernelGGL((gemm_f32<AK, BK, 1>), grid, dim3(256), 0, s, g); \
+        else if (rows32)                                                         \
             hipLaunchKernelGGL((gemm_f32<AK, BK, 2>), grid, dim3(256), 0, s, g); \
         else                                                                     \
             hipLaunchKernelGGL((gemm_f32<AK, BK, 4>), grid, dim3(256), 0, s, g); \
