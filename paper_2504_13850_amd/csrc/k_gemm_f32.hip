@@ -11,9 +11,10 @@ constexpr int GT = 64, GK = 32;
 // automatic K split (GemmF32::auto_split): products with fewer than kAutoTiles
 // output tiles take min(16, kAutoSlots / tiles, K / kAutoMinK) slices
 constexpr int64_t kAutoTiles = 128, kAutoSlots = 512, kAutoMinK = 64;
-// workgroups of 64-row tiles below which a product runs on 32-row tiles, and
-// of 32-row tiles below which it runs on 16-row tiles (for the 32-row step,
-// thresholds of 256, 512, 1024 or always gave the same step times)
+// workgroups of 64-row tiles below which a product runs on 32-row tiles, of
+// 32-row tiles below which it runs on 16-row tiles, and of 16 x 64 tiles below
+// which it runs on 16 x 32 (for the 32-row step, thresholds of 256, 512, 1024
+// or always gave the same step times)
 constexpr int64_t kRows32Below = 512;
 
 __device__ __forceinline__ float epi(const GemmF32& g, const float* add, int m, int n, float v) {
@@ -64,31 +65,31 @@ __device__ __forceinline__ void store_chunk(float (*T)[RT + 4], const float (&v)
 // while this one is computed from LDS, two LDS buffers (one barrier per
 // chunk).  The 32-row form doubles the workgroups of a product with few
 // tiles, whose time is otherwise the latency of each workgroup's K walk.
-template <bool AKF, bool BKF, int TM>
+template <bool AKF, bool BKF, int TM, int TN>
 __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
-    constexpr int BMt = 16 * TM, NA = BMt * GK / 256, NB = GT * GK / 256;
-    __shared__ float As[2][GK][BMt + 4], Bs[2][GK][GT + 4];
+    constexpr int BMt = 16 * TM, BNt = 16 * TN, NA = BMt * GK / 256, NB = BNt * GK / 256;
+    __shared__ float As[2][GK][BMt + 4], Bs[2][GK][BNt + 4];
     const float* A = g.inA ? (const float*)g.inA->x : g.A;
     const float* Bp = g.inB ? (const float*)g.inB->x : g.B;
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-    const int n0 = blockIdx.x * GT, m0 = blockIdx.y * BMt, z = blockIdx.z;
+    const int n0 = blockIdx.x * BNt, m0 = blockIdx.y * BMt, z = blockIdx.z;
     const int kc = ((g.K + g.S - 1) / g.S + GK - 1) / GK * GK;
     const int kb = z * kc, ke = min(g.K, kb + kc);
     const int nch = ke > kb ? (ke - kb + GK - 1) / GK : 0;
-    float acc[TM][4] = {};
+    float acc[TM][TN] = {};
     float ra[NA], rb[NB];
     if (nch > 0) {
         load_chunk<AKF, BMt>(A, g.am, g.ak, m0, g.M, kb, ke, ra);
-        load_chunk<BKF, GT>(Bp, g.bn, g.bk, n0, g.N, kb, ke, rb);
+        load_chunk<BKF, BNt>(Bp, g.bn, g.bk, n0, g.N, kb, ke, rb);
         store_chunk<AKF, BMt>(As[0], ra, m0, g.M, kb, ke);
-        store_chunk<BKF, GT>(Bs[0], rb, n0, g.N, kb, ke);
+        store_chunk<BKF, BNt>(Bs[0], rb, n0, g.N, kb, ke);
     }
     __syncthreads();
     for (int c = 0; c < nch; ++c) {
         const int u = c & 1;
         if (c + 1 < nch) {  // next chunk in flight during this chunk's FMAs
             load_chunk<AKF, BMt>(A, g.am, g.ak, m0, g.M, kb + (c + 1) * GK, ke, ra);
-            load_chunk<BKF, GT>(Bp, g.bn, g.bk, n0, g.N, kb + (c + 1) * GK, ke, rb);
+            load_chunk<BKF, BNt>(Bp, g.bn, g.bk, n0, g.N, kb + (c + 1) * GK, ke, rb);
         }
 #pragma unroll
         for (int k = 0; k < GK; ++k) {
@@ -102,16 +103,22 @@ __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
             } else {
                 a[0] = As[u][k][ty];
             }
-            const float4 b4 = *reinterpret_cast<const float4*>(&Bs[u][k][tx * 4]);
-            const float b[4] = {b4.x, b4.y, b4.z, b4.w};
+            float b[TN];
+            if constexpr (TN == 4) {
+                const float4 b4 = *reinterpret_cast<const float4*>(&Bs[u][k][tx * 4]);
+                b[0] = b4.x; b[1] = b4.y; b[2] = b4.z; b[3] = b4.w;
+            } else {
+                const float2 b2 = *reinterpret_cast<const float2*>(&Bs[u][k][tx * 2]);
+                b[0] = b2.x; b[1] = b2.y;
+            }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+                for (int j = 0; j < TN; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
         }
         if (c + 1 < nch) {
             store_chunk<AKF, BMt>(As[u ^ 1], ra, m0, g.M, kb + (c + 1) * GK, ke);
-            store_chunk<BKF, GT>(Bs[u ^ 1], rb, n0, g.N, kb + (c + 1) * GK, ke);
+            store_chunk<BKF, BNt>(Bs[u ^ 1], rb, n0, g.N, kb + (c + 1) * GK, ke);
         }
         __syncthreads();
     }
@@ -121,8 +128,8 @@ __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
             const int m = m0 + ty * TM + i;
             if (m >= g.M) continue;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int n = n0 + tx * 4 + j;
+            for (int j = 0; j < TN; ++j) {
+                const int n = n0 + tx * TN + j;
                 if (n < g.N) g.part[((int64_t)z * g.M + m) * g.N + n] = acc[i][j];
             }
         }
@@ -131,35 +138,35 @@ __global__ void __launch_bounds__(256) gemm_f32(const GemmF32 g) {
     // the epilogue's operands of all 16 elements first (indices clamped into
     // the product, so every load is valid), then the guarded stores
     const float* add = g.inAdd ? (const float*)g.inAdd->x : g.add;
-    int mi[TM], nj[4];
+    int mi[TM], nj[TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i) mi[i] = min(m0 + ty * TM + i, g.M - 1);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) nj[j] = min(n0 + tx * 4 + j, g.N - 1);
-    float bv[4] = {0.f, 0.f, 0.f, 0.f}, av[TM][4] = {}, mv[TM][4];
+    for (int j = 0; j < TN; ++j) nj[j] = min(n0 + tx * TN + j, g.N - 1);
+    float bv[TN] = {}, av[TM][TN] = {}, mv[TM][TN];
     if (g.bias) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) bv[j] = g.bias[nj[j]];
+        for (int j = 0; j < TN; ++j) bv[j] = g.bias[nj[j]];
     }
     if (add) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) av[i][j] = add[(int64_t)mi[i] * g.ldadd + nj[j]];
+            for (int j = 0; j < TN; ++j) av[i][j] = add[(int64_t)mi[i] * g.ldadd + nj[j]];
     }
     if (g.mask) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) mv[i][j] = g.mask[(int64_t)mi[i] * g.ldmask + nj[j]];
+            for (int j = 0; j < TN; ++j) mv[i][j] = g.mask[(int64_t)mi[i] * g.ldmask + nj[j]];
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
         const int m = m0 + ty * TM + i;
         if (m >= g.M) continue;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int n = n0 + tx * 4 + j;
+        for (int j = 0; j < TN; ++j) {
+            const int n = n0 + tx * TN + j;
             if (n >= g.N) continue;
             float v = acc[i][j] + bv[j] + av[i][j];
             if (g.relu) v = fmaxf(v, 0.f);
@@ -202,19 +209,22 @@ fo_status launch_gemm_f32(GemmF32 g, float* part, size_t part_floats, hipStream_
     if (g.S < 1) g.S = 1;
     g.part = part;
     // 32-row tiles when 64-row ones would not give every CU two workgroups,
-    // 16-row tiles when 32-row ones would not either
+    // 16-row tiles when 32-row ones would not either, then 32-column tiles
     const bool rows32 = cdiv(g.N, GT) * cdiv(g.M, GT) * g.S < kRows32Below;
     const bool rows16 = rows32 && cdiv(g.N, GT) * cdiv(g.M, 32) * g.S < kRows32Below;
-    const dim3 grid((int)cdiv(g.N, GT), (int)cdiv(g.M, rows16 ? 16 : rows32 ? 32 : GT), g.S);
+    const bool cols32 = rows16 && cdiv(g.N, GT) * cdiv(g.M, 16) * g.S < kRows32Below;
+    const dim3 grid((int)cdiv(g.N, cols32 ? 32 : GT), (int)cdiv(g.M, rows16 ? 16 : rows32 ? 32 : GT), g.S);
     const bool akf = g.ak == 1, bkf = g.bk == 1;
 #define FO_GEMM_F32(AK, BK)                                                       \
     do {                                                                         \
-        if (rows16)                                                              \
-            hipLaunchKernelGGL((gemm_f32<AK, BK, 1>), grid, dim3(256), 0, s, g); \
-        else if (rows32)                                                         \
-            hipLaunchKernelGGL((gemm_f32<AK, BK, 2>), grid, dim3(256), 0, s, g); \
-        else                                                                     \
-            hipLaunchKernelGGL((gemm_f32<AK, BK, 4>), grid, dim3(256), 0, s, g); \
+        if (cols32)                                                                 \
+            hipLaunchKernelGGL((gemm_f32<AK, BK, 1, 2>), grid, dim3(256), 0, s, g); \
+        else if (rows16)                                                            \
+            hipLaunchKernelGGL((gemm_f32<AK, BK, 1, 4>), grid, dim3(256), 0, s, g); \
+        else if (rows32)                                                            \
+            hipLaunchKernelGGL((gemm_f32<AK, BK, 2, 4>), grid, dim3(256), 0, s, g); \
+        else                                                                        \
+            hipLaunchKernelGGL((gemm_f32<AK, BK, 4, 4>), grid, dim3(256), 0, s, g); \
     } while (0)
     if (akf && bkf)
         FO_GEMM_F32(true, true);
