@@ -35,6 +35,25 @@ struct Plan {
 
 // y[b,co,y,x] = relu(bias[co] + sum_{ci,ky,kx} x[b,ci,y+ky-1,x+kx-1] w[co,ky,kx,ci]);
 // x is the step's batch (in->x) when in is set
+// part[u] += sum over channels c = u, u + 8, ... < n of a[c sa] b[c sb]: eight
+// independent chains whose loads are in flight together (a single chain over
+// the channels waits for each pair of loads in turn).
+__device__ __forceinline__ void chan_dot(const float* __restrict__ a, int64_t sa, const float* __restrict__ b,
+                                         int64_t sb, int n, float (&part)[8]) {
+    int c = 0;
+    for (; c + 8 <= n; c += 8) {
+        float av[8], bv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            av[u] = a[(c + u) * sa];
+            bv[u] = b[(c + u) * sb];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) part[u] = fmaf(av[u], bv[u], part[u]);
+    }
+    for (; c < n; ++c) part[c & 7] = fmaf(a[c * sa], b[c * sb], part[c & 7]);
+}
+
 __global__ void conv3x3_fwd_relu(const float* __restrict__ x_, const StepIn* __restrict__ in,
                                  const float* __restrict__ w, const float* __restrict__ bias, float* __restrict__ y,
                                  int B, int Ci, int Co, int H, int W) {
@@ -44,6 +63,7 @@ __global__ void conv3x3_fwd_relu(const float* __restrict__ x_, const StepIn* __r
     if (idx >= total) return;
     int xx = idx % W, yy = (idx / W) % H, co = (idx / (W * H)) % Co, b = idx / (W * H * Co);
     float acc = bias[co];
+    float part[8] = {};
     for (int ky = 0; ky < 3; ++ky) {
         int iy = yy + ky - 1;
         if (iy < 0 || iy >= H) continue;
@@ -52,9 +72,10 @@ __global__ void conv3x3_fwd_relu(const float* __restrict__ x_, const StepIn* __r
             if (ix < 0 || ix >= W) continue;
             const float* wp = w + ((int64_t)co * 9 + ky * 3 + kx) * Ci;
             const float* xp = x + ((int64_t)b * Ci * H + iy) * W + ix;
-            for (int ci = 0; ci < Ci; ++ci) acc = fmaf(xp[(int64_t)ci * H * W], wp[ci], acc);
+            chan_dot(xp, (int64_t)H * W, wp, 1, Ci, part);
         }
     }
+    acc += ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
     y[idx] = acc > 0.f ? acc : 0.f;
 }
 
@@ -146,14 +167,22 @@ __global__ void __launch_bounds__(256) conv3x3_wgrad(const float* __restrict__ d
         float g = d[((int64_t)b * Co + co) * HW + yy * W + xx];
         bacc += g;
         const float* xp = x + ((int64_t)b * Ci + ci) * HW;
+        // the nine taps loaded together (indices clamped into the image), the
+        // ones outside it zeroed afterwards
+        float v[9];
+#pragma unroll
+        for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+            for (int kx = 0; kx < 3; ++kx)
+                v[ky * 3 + kx] = xp[min(max(yy + ky - 1, 0), H - 1) * W + min(max(xx + kx - 1, 0), W - 1)];
 #pragma unroll
         for (int ky = 0; ky < 3; ++ky) {
-            int iy = yy + ky - 1;
+            const int iy = yy + ky - 1;
 #pragma unroll
             for (int kx = 0; kx < 3; ++kx) {
-                int ix = xx + kx - 1;
-                float v = (iy >= 0 && iy < H && ix >= 0 && ix < W) ? xp[iy * W + ix] : 0.f;
-                acc[ky * 3 + kx] = fmaf(g, v, acc[ky * 3 + kx]);
+                const int ix = xx + kx - 1;
+                const float vv = (iy >= 0 && iy < H && ix >= 0 && ix < W) ? v[ky * 3 + kx] : 0.f;
+                acc[ky * 3 + kx] = fmaf(g, vv, acc[ky * 3 + kx]);
             }
         }
     }
@@ -177,7 +206,7 @@ __global__ void conv3x3_dgrad(const float* __restrict__ d, const float* __restri
     int idx = blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= B * Ci * H * W) return;
     int xx = idx % W, yy = (idx / W) % H, ci = (idx / (W * H)) % Ci, b = idx / (W * H * Ci);
-    float acc = 0.f;
+    float part[8] = {};
     for (int ky = 0; ky < 3; ++ky) {
         int oy = yy - ky + 1;
         if (oy < 0 || oy >= H) continue;
@@ -186,10 +215,10 @@ __global__ void conv3x3_dgrad(const float* __restrict__ d, const float* __restri
             if (ox < 0 || ox >= W) continue;
             const float* dp = d + ((int64_t)b * Co * H + oy) * W + ox;
             const float* wp = w + (int64_t)(ky * 3 + kx) * Ci + ci;
-            for (int co = 0; co < Co; ++co) acc = fmaf(dp[(int64_t)co * H * W], wp[(int64_t)co * 9 * Ci], acc);
+            chan_dot(dp, (int64_t)H * W, wp, (int64_t)9 * Ci, Co, part);
         }
     }
-    dx[idx] = acc;
+    dx[idx] = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
 }
 
 // d1[b,c,Y,X] = dp[b,c,Y/2,X/2] if (Y,X) was the window's argmax, times [y1 > 0]
