@@ -52,6 +52,10 @@ __global__ void __launch_bounds__(256) nchw_rows(const StepIn* __restrict__ in, 
     y[i] = ((const float*)in->x)[((int64_t)b * C + c) * HW + p];
 }
 
+// rows a BatchNorm thread keeps in registers (up to 256 x BN_REG_ROWS rows per
+// channel read once; more rows take the three-pass loops)
+constexpr int BN_REG_ROWS = 8;
+
 __device__ __forceinline__ float block_sum(float v, float* red) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
     __syncthreads();
@@ -68,6 +72,42 @@ __global__ void __launch_bounds__(256) bn_rows_fwd(const float* __restrict__ z, 
                                                    const float* __restrict__ add, int R, int C, int act) {
     __shared__ float red[4];
     const int c = blockIdx.x;
+    if (R <= 256 * BN_REG_ROWS) {
+        // the thread's rows (r = t + 256 i, i < n) read once, kept in registers
+        // for the mean, the variance and the output
+        const int n = (R + 255) / 256;
+        float zv[BN_REG_ROWS];
+#pragma unroll
+        for (int i = 0; i < BN_REG_ROWS; ++i)
+            if (i < n) zv[i] = z[(int64_t)min((int)threadIdx.x + 256 * i, R - 1) * C + c];
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < BN_REG_ROWS; ++i)
+            if (i < n && threadIdx.x + 256 * i < R) s += zv[i];
+        const float mu = block_sum(s, red) / R;
+        float v = 0.f;
+#pragma unroll
+        for (int i = 0; i < BN_REG_ROWS; ++i)
+            if (i < n && threadIdx.x + 256 * i < R) {
+                const float d = zv[i] - mu;
+                v = fmaf(d, d, v);
+            }
+        const float rs = 1.f / sqrtf(block_sum(v, red) / R + BN_EPS);
+        const float gc = gam[c], bc = bet[c];
+#pragma unroll
+        for (int i = 0; i < BN_REG_ROWS; ++i) {
+            const int r = threadIdx.x + 256 * i;
+            if (i < n && r < R) {
+                const int64_t o = (int64_t)r * C + c;
+                const float xh = (zv[i] - mu) * rs;
+                const float u = fmaf(gc, xh, bc);
+                xhat[o] = xh;
+                y[o] = (act ? hswish(u) : u) + (add ? add[o] : 0.f);
+            }
+        }
+        if (threadIdx.x == 0) rstd_out[c] = rs;
+        return;
+    }
     float s = 0.f;
     for (int r = threadIdx.x; r < R; r += 256) s += z[(int64_t)r * C + c];
     const float mu = block_sum(s, red) / R;
@@ -97,6 +137,39 @@ __global__ void __launch_bounds__(256) bn_rows_bwd(const float* __restrict__ dy,
     __shared__ float red[4];
     const int c = blockIdx.x;
     const float g = gam[c], bb = bet[c];
+    if (R <= 256 * BN_REG_ROWS) {
+        // the thread's rows read once (dy, xhat), du kept in registers
+        const int n = (R + 255) / 256;
+        float duv[BN_REG_ROWS], xv[BN_REG_ROWS];
+#pragma unroll
+        for (int i = 0; i < BN_REG_ROWS; ++i)
+            if (i < n) {
+                const int64_t o = (int64_t)min((int)threadIdx.x + 256 * i, R - 1) * C + c;
+                xv[i] = xhat[o];
+                duv[i] = dy[o];
+            }
+        float sg = 0.f, sb = 0.f;
+#pragma unroll
+        for (int i = 0; i < BN_REG_ROWS; ++i)
+            if (i < n && threadIdx.x + 256 * i < R) {
+                const float du = act ? duv[i] * hswish_d(fmaf(g, xv[i], bb)) : duv[i];
+                duv[i] = du;
+                sg = fmaf(du, xv[i], sg);
+                sb += du;
+            }
+        const float dg = block_sum(sg, red), db = block_sum(sb, red);
+        const float k = g * rstd[c];
+#pragma unroll
+        for (int i = 0; i < BN_REG_ROWS; ++i) {
+            const int r = threadIdx.x + 256 * i;
+            if (i < n && r < R) dz[(int64_t)r * C + c] = k * (duv[i] - db / R - xv[i] * dg / R);
+        }
+        if (threadIdx.x == 0) {
+            dgam[c] = dg;
+            dbet[c] = db;
+        }
+        return;
+    }
     float sg = 0.f, sb = 0.f;
     for (int r = threadIdx.x; r < R; r += 256) {
         const int64_t o = (int64_t)r * C + c;
