@@ -162,27 +162,41 @@ __global__ void __launch_bounds__(256) conv3x3_wgrad(const float* __restrict__ d
     for (int t = 0; t < 9; ++t) acc[t] = 0.f;
     float bacc = 0.f;
     int HW = H * W;
-    for (int p = threadIdx.x; p < B * HW; p += blockDim.x) {
-        int b = p / HW, yy = (p / W) % H, xx = p % W;
-        float g = d[((int64_t)b * Co + co) * HW + yy * W + xx];
-        bacc += g;
-        const float* xp = x + ((int64_t)b * Ci + ci) * HW;
-        // the nine taps loaded together (indices clamped into the image), the
-        // ones outside it zeroed afterwards
-        float v[9];
+    // pixels p = t + 256 (2 q + h), h = 0, 1: each pair's twenty loads (the
+    // gradient and nine taps of both, taps at indices clamped into the image)
+    // issued together, the taps outside the image zeroed afterwards
+    const int P = B * HW;
+    for (int p0 = threadIdx.x; p0 < P; p0 += 2 * blockDim.x) {
+        float g[2], v[2][9];
+        int yy[2], xx[2];
 #pragma unroll
-        for (int ky = 0; ky < 3; ++ky)
+        for (int h = 0; h < 2; ++h) {
+            const int p = min(p0 + h * (int)blockDim.x, P - 1);
+            const int b = p / HW;
+            yy[h] = (p / W) % H;
+            xx[h] = p % W;
+            g[h] = d[((int64_t)b * Co + co) * HW + yy[h] * W + xx[h]];
+            const float* xp = x + ((int64_t)b * Ci + ci) * HW;
 #pragma unroll
-            for (int kx = 0; kx < 3; ++kx)
-                v[ky * 3 + kx] = xp[min(max(yy + ky - 1, 0), H - 1) * W + min(max(xx + kx - 1, 0), W - 1)];
+            for (int ky = 0; ky < 3; ++ky)
 #pragma unroll
-        for (int ky = 0; ky < 3; ++ky) {
-            const int iy = yy + ky - 1;
+                for (int kx = 0; kx < 3; ++kx)
+                    v[h][ky * 3 + kx] =
+                        xp[min(max(yy[h] + ky - 1, 0), H - 1) * W + min(max(xx[h] + kx - 1, 0), W - 1)];
+        }
 #pragma unroll
-            for (int kx = 0; kx < 3; ++kx) {
-                const int ix = xx + kx - 1;
-                const float vv = (iy >= 0 && iy < H && ix >= 0 && ix < W) ? v[ky * 3 + kx] : 0.f;
-                acc[ky * 3 + kx] = fmaf(g, vv, acc[ky * 3 + kx]);
+        for (int h = 0; h < 2; ++h) {
+            if (p0 + h * (int)blockDim.x >= P) break;
+            bacc += g[h];
+#pragma unroll
+            for (int ky = 0; ky < 3; ++ky) {
+                const int iy = yy[h] + ky - 1;
+#pragma unroll
+                for (int kx = 0; kx < 3; ++kx) {
+                    const int ix = xx[h] + kx - 1;
+                    const float vv = (iy >= 0 && iy < H && ix >= 0 && ix < W) ? v[h][ky * 3 + kx] : 0.f;
+                    acc[ky * 3 + kx] = fmaf(g[h], vv, acc[ky * 3 + kx]);
+                }
             }
         }
     }
