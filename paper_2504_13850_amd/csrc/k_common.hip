@@ -174,9 +174,13 @@ __global__ void __launch_bounds__(256) colsum_finish(const float* __restrict__ p
 }
 
 // colsum_finish over several jobs: blocks are dealt to the jobs in order, each
-// job taking ceil(N / 64) of them; the arithmetic per column is colsum_finish's.
-__global__ void __launch_bounds__(256) colsum_finish_multi(const ColJobs jobs) {
-    __shared__ float red[4][64];
+// job taking ceil(N / 64) of them.  W waves take interleaved partial rows (eight
+// loads in flight per lane) and are added in wave order: with hundreds of
+// partial rows per column (the LayerNorm partials, one per four rows) the
+// 16-wave form keeps a wave's chain of dependent loads short.
+template <int W>
+__global__ void __launch_bounds__(64 * W) colsum_finish_multi(const ColJobs jobs) {
+    __shared__ float red[W][64];
     int bid = blockIdx.x, ji = 0;
     while (ji < jobs.n - 1 && bid >= (jobs.j[ji].N + 63) / 64) {
         bid -= (jobs.j[ji].N + 63) / 64;
@@ -190,20 +194,23 @@ __global__ void __launch_bounds__(256) colsum_finish_multi(const ColJobs jobs) {
     float s = 0.f;
     if (col < J.N) {
         int p = wave;
-        for (; p + 28 < nparts; p += 32) {
+        for (; p + 7 * W < nparts; p += 8 * W) {
             float v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = J.part[(int64_t)(p + 4 * u) * J.N + col];
+            for (int u = 0; u < 8; ++u) v[u] = J.part[(int64_t)(p + W * u) * J.N + col];
 #pragma unroll
             for (int u = 0; u < 8; ++u) s += v[u];
         }
-        for (; p < nparts; p += 4) s += J.part[(int64_t)p * J.N + col];
+        for (; p < nparts; p += W) s += J.part[(int64_t)p * J.N + col];
     }
     red[wave][lane] = s;
     __syncthreads();
     if (wave == 0 && col < J.N) {
+        float t = 0.f;
+#pragma unroll
+        for (int w = 0; w < W; w += 4) t += (red[w][lane] + red[w + 1][lane]) + (red[w + 2][lane] + red[w + 3][lane]);
         const int j = col / J.out.seg;
-        J.out.p[j][col - j * J.out.seg] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+        J.out.p[j][col - j * J.out.seg] = t;
     }
 }
 
@@ -416,16 +423,23 @@ fo_status launch_colsums(const ColSums& c, hipStream_t s) {
     return st != FO_OK ? st : launch_colsum_finish_multi(c.fin, s);
 }
 
+// partial rows per column above which the finish runs 16 waves per block
+constexpr int kFinishWide = 64;
+
 fo_status launch_colsum_finish_multi(const ColJobs& jobs, hipStream_t s) {
     FO_CHECK(jobs.n >= 1 && jobs.n <= kColJobsMax, "colsum: %d jobs", jobs.n);
-    int blocks = 0;
+    int blocks = 0, most = 0;
     for (int i = 0; i < jobs.n; ++i) {
         const ColJob& J = jobs.j[i];
         FO_CHECK(J.part && J.N > 0 && J.rows_per_part > 0 && J.out.seg > 0 && cdiv(J.N, J.out.seg) <= 3,
                  "colsum: bad job %d", i);
         blocks += (int)cdiv(J.N, 64);
+        most = std::max(most, (int)cdiv(J.rows, J.rows_per_part));
     }
-    hipLaunchKernelGGL(colsum_finish_multi, dim3(blocks), dim3(256), 0, s, jobs);
+    if (most > kFinishWide)
+        hipLaunchKernelGGL(colsum_finish_multi<16>, dim3(blocks), dim3(1024), 0, s, jobs);
+    else
+        hipLaunchKernelGGL(colsum_finish_multi<4>, dim3(blocks), dim3(256), 0, s, jobs);
     FO_LAUNCHED();
     return FO_OK;
 }
