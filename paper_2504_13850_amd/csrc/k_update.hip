@@ -55,37 +55,50 @@ __global__ void __launch_bounds__(256) agg_lerp_kernel(float* __restrict__ g, co
 }
 
 // Several arrivals applied in order to each element while it sits in a
-// register; the next arrival's vectors load while the current one is applied.
-constexpr int MU = 2;
+// register.  The vectors of the next AP arrivals are in flight while the
+// current one is applied: each element's arrivals form a chain of dependent
+// updates, so with a small model (a few hundred blocks at most) the chain's
+// load latency, not HBM bandwidth, sets the time.
+constexpr int MU = 1;
+constexpr int AP = 8;
 
 __global__ void __launch_bounds__(256) agg_lerp_multi_kernel(float* __restrict__ g, AggTable tab, int64_t n4,
                                                              int64_t n) {
     f32x4* g4 = reinterpret_cast<f32x4*>(g);
     const int tid = threadIdx.x;
     const int64_t chunk = 256 * MU;
+    const int cnt = tab.count;
     for (int64_t base = (int64_t)blockIdx.x * chunk; base < n4; base += (int64_t)gridDim.x * chunk) {
         int64_t idx[MU];
         bool ok[MU];
-        f32x4 a[MU], b[MU];
+        f32x4 a[MU], ring[AP][MU];
 #pragma unroll
         for (int u = 0; u < MU; ++u) {
             idx[u] = base + 256 * u + tid;
             ok[u] = idx[u] < n4;
             if (!ok[u]) idx[u] = 0;  // in range; the result is not stored
             a[u] = g4[idx[u]];
-            b[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(tab.local[0]) + idx[u]);
         }
-        for (int m = 0; m < tab.count; ++m) {
-            f32x4 c[MU];
-            const int mn = m + 1 < tab.count ? m + 1 : m;
 #pragma unroll
-            for (int u = 0; u < MU; ++u)
-                c[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(tab.local[mn]) + idx[u]);
-            const float w = tab.w[m];
+        for (int p = 0; p < AP; ++p)
+            if (p < cnt)
 #pragma unroll
-            for (int u = 0; u < MU; ++u) {
-                a[u] = lerp4(a[u], b[u], w);
-                b[u] = c[u];
+                for (int u = 0; u < MU; ++u)
+                    ring[p][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(tab.local[p]) + idx[u]);
+        for (int m0 = 0; m0 < cnt; m0 += AP) {
+#pragma unroll
+            for (int p = 0; p < AP; ++p) {
+                const int m = m0 + p;
+                if (m < cnt) {
+                    const float w = tab.w[m];
+#pragma unroll
+                    for (int u = 0; u < MU; ++u) a[u] = lerp4(a[u], ring[p][u], w);
+                    if (m + AP < cnt)
+#pragma unroll
+                        for (int u = 0; u < MU; ++u)
+                            ring[p][u] = __builtin_nontemporal_load(
+                                reinterpret_cast<const f32x4*>(tab.local[m + AP]) + idx[u]);
+                }
             }
         }
 #pragma unroll
