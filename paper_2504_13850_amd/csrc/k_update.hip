@@ -60,7 +60,7 @@ __global__ void __launch_bounds__(256) agg_lerp_kernel(float* __restrict__ g, co
 // updates, so with a small model (a few hundred blocks at most) the chain's
 // load latency, not HBM bandwidth, sets the time.
 constexpr int MU = 1;
-constexpr int AP = 8;
+constexpr int AP = 32;
 
 __global__ void __launch_bounds__(256) agg_lerp_multi_kernel(float* __restrict__ g, AggTable tab, int64_t n4,
                                                              int64_t n) {
